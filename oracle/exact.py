@@ -1,0 +1,118 @@
+"""Exact law of one replay-and-verify round, by enumeration (oracle side).
+
+TEST INFRASTRUCTURE ONLY: used by the tests to check the losslessness claim
+(Section 3.3, Proposition 1) with no random numbers at all.
+
+For a fixed topology, a context-free draft table q[d] and a prefix-keyed
+target p(. | s), every random choice of the round is enumerated:
+  * replay draws at each parent u: ordered samples without replacement from
+    q[depth(u)] with Plackett-Luce weight prod_j q(y_j) / (1 - sum_{i<j} q(y_i))
+    (Appendix A, sampling without replacement);
+  * each acceptance test: accept child j with probability min{1, ratio_j},
+    ratios and residual updates taken from oracle.verify (the same code the
+    sampling oracle runs);
+  * the bonus token: the normalised final residual (or p at a leaf).
+Subtrees that the walk never enters are marginalised out, which is exact
+because the draws of different parents are independent.
+"""
+import itertools
+
+import numpy as np
+
+from . import verify as verify_mod
+
+
+def _wor_orders(q, m):
+    """All ordered m-samples without replacement from q with their probabilities."""
+    V = q.shape[0]
+    for seq in itertools.permutations(range(V), m):
+        w = 1.0
+        used = 0.0
+        for y in seq:
+            rem = 1.0 - used
+            if rem <= 0.0 or q[y] <= 0.0:
+                w = 0.0
+                break
+            w *= q[y] / rem
+            used += q[y]
+        if w > 0.0:
+            yield seq, w
+
+
+def emitted_law(tree, q, p_of_prefix):
+    """Exact distribution of the emitted sequence (accepted tokens + bonus).
+
+    tree: BFS topology dict (n_children, first_child, depth).
+    q: array [D, V] of draft distributions per depth.
+    p_of_prefix(tuple) -> target distribution after that token prefix.
+    Returns dict {tuple(sequence): probability}.
+    """
+    law = {}
+
+    def add(seq, w):
+        law[seq] = law.get(seq, 0.0) + w
+
+    def at_node(u, prefix, weight):
+        m = int(tree["n_children"][u])
+        p_u = np.asarray(p_of_prefix(prefix), dtype=np.float64)
+        if m == 0:
+            for v in range(p_u.shape[0]):
+                if p_u[v] > 0:
+                    add(prefix + (v,), weight * p_u[v])
+            return
+        qd = np.asarray(q[int(tree["depth"][u])], dtype=np.float64)
+        fc = int(tree["first_child"][u])
+        for seq, w_draw in _wor_orders(qd, m):
+            P, Q = p_u.copy(), qd.copy()
+            reach = weight * w_draw
+            degenerate = False
+            for j, y in enumerate(seq):
+                ratio = verify_mod.accept_ratio(P, Q, y)
+                pa = min(1.0, ratio)
+                if pa > 0.0:
+                    at_node(fc + j, prefix + (y,), reach * pa)
+                reach *= (1.0 - pa)
+                if reach == 0.0:
+                    break
+                P, Q, Z, S = verify_mod.reject(P, Q, y)
+                if Z <= 0.0 or (j + 1 < m and S <= 0.0):
+                    degenerate = True
+                    break
+            if reach == 0.0:
+                continue
+            final = p_u if degenerate else P
+            tot = final.sum()
+            for v in range(final.shape[0]):
+                if final[v] > 0:
+                    add(prefix + (v,), reach * final[v] / tot)
+
+    at_node(0, (), 1.0)
+    return law
+
+
+def extend_law(law, p_of_prefix, length):
+    """Continue every emitted sequence by sampling the target up to `length` tokens."""
+    out = {}
+    stack = list(law.items())
+    while stack:
+        seq, w = stack.pop()
+        if len(seq) >= length:
+            key = seq[:length]
+            out[key] = out.get(key, 0.0) + w
+            continue
+        p = np.asarray(p_of_prefix(seq), dtype=np.float64)
+        for v in range(p.shape[0]):
+            if p[v] > 0:
+                stack.append((seq + (v,), w * p[v]))
+    return out
+
+
+def target_law(p_of_prefix, V, length):
+    """Law of `length` tokens sampled autoregressively from the target."""
+    out = {}
+    for seq in itertools.product(range(V), repeat=length):
+        w = 1.0
+        for i in range(length):
+            w *= p_of_prefix(seq[:i])[seq[i]]
+        out[seq] = w
+    return out
