@@ -1,0 +1,205 @@
+#!/usr/bin/env python
+"""Throughput of the tree-replay round on one MI355X.
+
+A step is one full round (plan -> replay -> verify, every kernel of the
+path) over one batch of R requests, through tsb_step. Default workload: the
+batched serving shape, R=16 requests, V=151936, draft block D=16, budget
+B=128 (non-root nodes), K=10 planning candidates, bf16 logits, T=1. Inputs
+are synthetic (workloads package), resident in HBM before timing starts; a
+pool of P distinct input sets is rotated so that no step reuses cached rows.
+
+Prints one JSON line: steps/s as `value`, verified tree nodes/s, the
+roofline of the dominant (target-streaming) kernel measured live with HIP
+events on the launch stream, a per-kernel breakdown, and the CPU oracle
+timed on a bounded sample of the same workload on the host cores.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import workloads as W  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+# ---------------------------------------------------------------- CPU oracle
+_CPU = {}
+
+
+def _cpu_task(args):
+    r, step = args
+    from oracle import step as ostep
+    c = _CPU["cfg"]
+    d = _CPU["draft"][r].float().numpy()
+    t = _CPU["target"][r].float().numpy()
+    out = ostep.step_request(d, t, c["T"], c["K"], c["B"], _CPU["seed"], step, r)
+    return out["n_acc"]
+
+
+def cpu_baseline(cfg, seed, requests):
+    """Time the oracle over `requests` request-steps of one input set (runs before any GPU use)."""
+    import multiprocessing as mp
+
+    import torch
+    from oracle import step as ostep
+    base, sigma = W.base_rows(cfg, 0, device="cpu")
+    draft = W.draft_from_base(cfg, base)
+    dep = torch.zeros(cfg["R"], cfg["B"] + 1, dtype=torch.int64)
+    for r in range(min(requests, cfg["R"])):
+        pl = ostep.plan_request(draft[r].float().numpy(), cfg["T"], cfg["K"], cfg["B"])
+        dep[r, :pl["tree"]["n_nodes"]] = torch.from_numpy(pl["tree"]["depth"])
+    target = W.target_from_base(cfg, base, sigma, dep)
+    del base
+    _CPU.update(cfg=cfg, draft=draft, target=target, seed=seed)
+    tasks = [(r % cfg["R"], r // cfg["R"]) for r in range(requests)]
+    cores = min(16, len(os.sched_getaffinity(0)), len(tasks))
+    ctx = mp.get_context("fork")
+    t0 = time.perf_counter()
+    with ctx.Pool(cores) as pool:
+        pool.map(_cpu_task, tasks, chunksize=1)
+    dt = time.perf_counter() - t0
+    _CPU.clear()
+    return dict(value=(len(tasks) / cfg["R"]) / dt, unit="steps/s", cores=cores, kind="oracle",
+                sample="%d request-steps (%g steps) of the %s workload, CPU-generated set 0; wall %.2f s"
+                       % (len(tasks), len(tasks) / cfg["R"], cfg["name"], dt))
+
+
+# ---------------------------------------------------------------- GPU
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", type=int, default=4)
+    ap.add_argument("--pool", type=int, default=4)
+    ap.add_argument("--cpu-requests", type=int, default=None, help="oracle request-steps in the CPU baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--breakdown-steps", type=int, default=20)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (requests shard with no "
+              "exchange; see the design notes). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    cfg = W.config(args.config)
+    seed = W.replay_seed(args.config)
+    R, D, V, B, K = cfg["R"], cfg["D"], cfg["V"], cfg["B"], cfg["K"]
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        nreq = args.cpu_requests if args.cpu_requests is not None else R
+        log("cpu baseline: %d oracle request-steps" % nreq)
+        cpu = cpu_baseline(cfg, seed, nreq)
+        log("cpu baseline:", cpu)
+
+    import torch
+    import paper_2609_33652_amd as tsb
+    tsb.load()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    c = tsb.make_config(R, D, V, B, K, cfg["T"], cfg["dtype"], seed)
+    rnd = tsb.Round(c, dev)
+
+    # input pool, resident in HBM
+    drafts, targets = [], []
+    for p in range(args.pool):
+        base, sigma = W.base_rows(cfg, p, device=dev)
+        draft = W.draft_from_base(cfg, base)
+        rnd.plan(draft)
+        dep = rnd.tree["depth"].long().clamp(min=0)
+        targets.append(W.target_from_base(cfg, base, sigma, dep, set_idx=p))
+        drafts.append(draft)
+        del base
+    torch.cuda.synchronize()
+    log("pool ready: %d sets, %.1f GB" % (args.pool, sum(d.numel() * d.element_size() + t.numel() *
+                                                           t.element_size() for d, t in zip(drafts, targets)) / 1e9))
+
+    P = args.pool
+    for s in range(args.warmup):
+        rnd.step(drafts[s % P], targets[s % P], s)
+    torch.cuda.synchronize()
+
+    K4 = tsb.KERNELS.index("target_partials")
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_host0 = time.perf_counter()
+    start.record()
+    for i in range(args.steps):
+        s = args.warmup + i
+        tsb.profile_kernel(K4, ev[i][0], ev[i][1])
+        rnd.step(drafts[s % P], targets[s % P], s)
+    stop.record()
+    torch.cuda.synchronize()
+    t_host1 = time.perf_counter()
+    tsb.profile_kernel(K4, None)
+    ms = start.elapsed_time(stop) / args.steps
+    k4_ms = sum(a.elapsed_time(b) for a, b in ev) / args.steps
+
+    # untimed passes: per-kernel breakdown and acceptance statistics
+    kern_us = {}
+    for kid, name in enumerate(tsb.KERNELS):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.breakdown_steps)]
+        for i in range(args.breakdown_steps):
+            tsb.profile_kernel(kid, evs[i][0], evs[i][1])
+            rnd.step(drafts[i % P], targets[i % P], i)
+        torch.cuda.synchronize()
+        tsb.profile_kernel(kid, None)
+        kern_us[name] = round(1000.0 * sum(a.elapsed_time(b) for a, b in evs) / args.breakdown_steps, 2)
+    acc, nodes, flagged = 0, 0, 0
+    for i in range(P):
+        rnd.step(drafts[i], targets[i], i)
+        h = rnd.host()
+        acc += int(h["n_acc"].clamp(min=0).sum()) + int((h["n_acc"] >= 0).sum())
+        nodes += int((h["n_nodes"] - 1).sum())
+        flagged += int((h["req_status"] & (tsb.REQ_NONFINITE | tsb.REQ_WALK_TIMEOUT)).ne(0).sum())
+    tau = acc / (P * R)
+    nodes_per_step = nodes / P
+
+    b = 2 if cfg["dtype"] == "bf16" else 4
+    k4_bytes = R * (B + 1) * V * b  # every target row of a full tree, read once
+    achieved = k4_bytes / (k4_ms * 1e-3) / 1e9
+    steps_per_s = 1000.0 / ms
+    out = {
+        "metric": "tree-replay steps/sec + verified nodes/sec at V=151936,B=128,bs=16; % HBM peak",
+        "value": round(steps_per_s, 2),
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg["dtype"],
+        "data": "synthetic",
+        "config": {"workload": "%s: %s" % (cfg["name"], W.describe(cfg)), "requests": R, "vocab": V,
+                   "draft_depth": D, "budget": B, "topk": K, "temperature": cfg["T"], "pool": P,
+                   "seed": seed},
+        "nodes_verified_per_s": round(nodes_per_step * steps_per_s, 1),
+        "accepted_tokens_per_s": round(tau * R * steps_per_s, 1),
+        "tau": round(tau, 4),
+        "roofline": {"kernel": "target_partials", "bound": "hbm", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": None, "bytes_per_launch": k4_bytes, "avg_launch_us": round(k4_ms * 1000, 2)},
+        "kernels_us": kern_us,
+        "host_wall_s": round(t_host1 - t_host0, 3),
+        "flagged_requests": flagged,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,194 @@
+/*
+ * tsubame.h - C ABI of the MI355X (gfx950) tree-replay library.
+ *
+ * One decoding round of Tsubame (Tree Replay for Diffusion-Based Speculative
+ * Decoding) for R independent requests, over vocabulary-wide logits:
+ *
+ *   tsb_plan    first pass: row normalisers, planning candidates and a frozen
+ *               topology by best-first expansion of draft path scores under a
+ *               node budget B (Section 3.1; Appendix B.3; Figure 1).
+ *   tsb_replay  second pass: refill every node of the frozen topology with
+ *               fresh samples drawn without replacement from the draft
+ *               distribution of its depth (Section 3.2, eq. (2); Appendix A).
+ *   tsb_verify  recursive rejection sampling without replacement over the
+ *               replayed tree against the target, accepted path plus one bonus
+ *               token (Section 2.3, eq. (1); Appendix A; Section 3.3,
+ *               Proposition 1: the probabilities used are those of the
+ *               replayed candidates).
+ *   tsb_step    plan -> replay -> verify with target logits supplied up front.
+ *
+ * Conventions shared by every entry point
+ *   - Every array pointer is a DEVICE pointer owned by the caller, row-major,
+ *     vocabulary index fastest. The library never allocates, frees or
+ *     synchronises; all work is enqueued on `stream` and returns immediately.
+ *   - Arguments are validated on the host before anything is enqueued; a
+ *     non-zero status means nothing was enqueued (except TSB_E_HIP, where a
+ *     launch failed part-way; tsb_last_error() has the detail).
+ *   - Scratch memory comes from the caller's `workspace` of at least
+ *     tsb_workspace_bytes(cfg) bytes, 256-byte aligned. One workspace may be
+ *     reused by successive calls on one stream; calls that overlap in time
+ *     need separate workspaces.
+ *   - Results are a deterministic function of (inputs, cfg.seed, step): the
+ *     randomness is Philox4x32-10 (Salmon et al., SC'11) keyed by
+ *     (seed, step, request, node, draw), independent of launch shapes.
+ *   - Problems found on the device are reported per request in `req_status`
+ *     (TSB_REQ_* bits); the outputs of such a request are defined (n_acc =
+ *     -1, bonus = -1 on NONFINITE) but carry no meaning.
+ *
+ * Numeric contract (the paper states no precision):
+ *   invT = fl32(1/T); a = fl32(x * invT) for every logit x (fp32 or bf16).
+ *   draft_lse[r,d] = binary64 log-sum-exp of row a_{r,d}; its binary32
+ *   rounding lse32 is canonical: topk_lp = fl32(a(tok) - lse32).
+ *   Path scores are binary64 sums of topk_lp from the root.
+ */
+#ifndef TSUBAME_H
+#define TSUBAME_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define TSB_MAX_D 64   /* draft block depth */
+#define TSB_MAX_K 32   /* planning candidates per position */
+#define TSB_MAX_B 1023 /* non-root nodes per tree */
+#define TSB_TRACE_MAX 256 /* acceptance tests recorded per request in the optional trace */
+
+typedef enum tsb_status {
+    TSB_OK = 0,
+    TSB_E_NULL = 1,        /* a required pointer is NULL */
+    TSB_E_SHAPE = 2,       /* R, D, V, B or K out of range */
+    TSB_E_DTYPE = 3,       /* unknown logit dtype */
+    TSB_E_TEMPERATURE = 4, /* temperature not finite or not > 0 */
+    TSB_E_WORKSPACE = 5,   /* workspace too small or not 256-byte aligned */
+    TSB_E_HIP = 6,         /* a HIP runtime call failed (see tsb_last_error) */
+    TSB_E_DEVICE = 7       /* no usable device */
+} tsb_status;
+
+typedef enum tsb_dtype { TSB_F32 = 0, TSB_BF16 = 1 } tsb_dtype;
+
+/* Bits of req_status[r]. */
+enum {
+    TSB_REQ_NONFINITE = 1,           /* NaN/+inf logit, or a row with no finite logit */
+    TSB_REQ_DEGENERATE_RESIDUAL = 2, /* empty residual after a rejection: bonus drawn from p at that node */
+    TSB_REQ_BUDGET_SHORT = 4,        /* fewer than B nodes exist: n_nodes < B + 1 */
+    TSB_REQ_WALK_TIMEOUT = 8         /* a cross-workgroup wait in verification hit its spin limit */
+};
+
+/* cfg.flags */
+enum {
+    TSB_FLAG_NO_PRUNE = 1 /* replay scores every token (no early rejection by the Gumbel bound) */
+};
+
+typedef struct tsb_config {
+    int32_t R;           /* requests in the batch, >= 1 */
+    int32_t D;           /* draft positions (maximum tree depth), 1..TSB_MAX_D */
+    int32_t V;           /* vocabulary size, K..2^30 */
+    int32_t B;           /* node budget excluding the root, 0..TSB_MAX_B */
+    int32_t K;           /* planning candidates per position, 1..min(TSB_MAX_K, V) */
+    float temperature;   /* T > 0 */
+    uint32_t dtype;      /* tsb_dtype of draft and target logits */
+    uint32_t flags;      /* TSB_FLAG_* */
+    uint64_t seed;       /* Philox key */
+} tsb_config;
+
+/* Frozen topology, BFS order (depth, then parent, then rank); node 0 is the
+ * root; parent[i] < i; the children of a node are contiguous, in rank order.
+ * Arrays are [R, B+1] except n_nodes and plan_margin ([R]). Entries at
+ * i >= n_nodes[r] are filled with -1 (score: 0). */
+typedef struct tsb_tree {
+    int32_t* parent;      /* -1 at the root */
+    int32_t* depth;       /* 0 at the root */
+    int32_t* rank;        /* child slot among siblings, -1 at the root */
+    int32_t* n_children;
+    int32_t* first_child; /* -1 if none */
+    double* score;        /* binary64 draft path log-probability, 0 at the root */
+    int32_t* n_nodes;     /* 1 + committed nodes */
+    double* plan_margin;  /* score(last committed) - score(best uncommitted); +inf if none left */
+} tsb_tree;
+
+/* Outputs of verification. n_acc, bonus and req_status are [R]; acc_node and
+ * acc_tok are [R, D] (entries >= n_acc[r] set to -1). req_status is OR-ed
+ * into (tsb_plan clears it). target_lse ([R, B+1], binary64 log-sum-exp of
+ * the scaled target rows, NaN beyond n_nodes) and trace are optional (NULL
+ * to skip). trace is [R, TSB_TRACE_MAX, 4] doubles per acceptance test, in
+ * walk order: (child node, uniform U, ratio, residual mass after rejection or
+ * -1), unused entries -1. */
+typedef struct tsb_verdict {
+    int32_t* n_acc;
+    int32_t* acc_node;
+    int32_t* acc_tok;
+    int32_t* bonus;
+    int32_t* req_status;
+    double* target_lse;
+    double* trace;
+} tsb_verdict;
+
+/* Bytes of workspace every entry point needs for this configuration (0 if
+ * the configuration is invalid). */
+size_t tsb_workspace_bytes(const tsb_config* cfg);
+
+/* First pass (Section 3.1). draft: [R, D, V] logits of dtype cfg.dtype.
+ * Writes draft_lse [R, D] (binary64), topk_tok [R, D, K] (token ids by logit
+ * desc, id asc), topk_lp [R, D, K] (binary32), the tree, and clears and sets
+ * req_status [R] (NONFINITE, BUDGET_SHORT). A request with a non-finite
+ * draft row gets a root-only tree. */
+tsb_status tsb_plan(const tsb_config* cfg, const void* draft, double* draft_lse, int32_t* topk_tok,
+                    float* topk_lp, const tsb_tree* tree, int32_t* req_status, void* workspace,
+                    size_t workspace_bytes, hipStream_t stream);
+
+/* Second pass (Section 3.2, eq. (2)). For every node u with m children at
+ * depth d the children receive, in rank order, the m largest keys of
+ * a_{d,v} + G(seed, step, request, u, v) over all v (Gumbel-top-k sampling
+ * without replacement; equal keys to the smaller id). topk_tok is the output
+ * of tsb_plan. Writes node_tok [R, B+1] (-1 at the root and beyond n_nodes). */
+tsb_status tsb_replay(const tsb_config* cfg, const void* draft, const int32_t* topk_tok,
+                      const tsb_tree* tree, uint32_t step, int32_t* node_tok, void* workspace,
+                      size_t workspace_bytes, hipStream_t stream);
+
+/* Verification (eq. (1); Appendix A). target: [R, B+1, V] logits, row i is
+ * the target's next-token logits at tree node i (rows >= n_nodes unread).
+ * draft_lse as written by tsb_plan. */
+tsb_status tsb_verify(const tsb_config* cfg, const void* draft, const double* draft_lse,
+                      const void* target, const tsb_tree* tree, const int32_t* node_tok,
+                      uint32_t step, const tsb_verdict* out, void* workspace,
+                      size_t workspace_bytes, hipStream_t stream);
+
+/* plan -> replay -> verify back to back on one stream (target supplied up front). */
+tsb_status tsb_step(const tsb_config* cfg, const void* draft, const void* target, uint32_t step,
+                    double* draft_lse, int32_t* topk_tok, float* topk_lp, const tsb_tree* tree,
+                    int32_t* node_tok, const tsb_verdict* out, void* workspace,
+                    size_t workspace_bytes, hipStream_t stream);
+
+/* Instrumentation (for benchmarks). On the calling thread, every later
+ * launch of kernel `kernel_id` (a TSB_KERNEL_* value) is bracketed by
+ * hipEventRecord(start) / hipEventRecord(stop) on the launch stream, so
+ * hipEventElapsedTime(start, stop) is that kernel's duration. kernel_id < 0
+ * clears the hook. The events stay owned by the caller. */
+enum {
+    TSB_KERNEL_DRAFT_PARTIALS = 0, /* draft row statistics + candidates (streams the draft) */
+    TSB_KERNEL_DRAFT_MERGE = 1,
+    TSB_KERNEL_PLAN_TREE = 2,
+    TSB_KERNEL_REPLAY_SCAN = 3,
+    TSB_KERNEL_REPLAY_MERGE = 4,
+    TSB_KERNEL_TARGET_PARTIALS = 5, /* target row statistics (streams the target) */
+    TSB_KERNEL_VERIFY_WALK = 6,
+    TSB_KERNEL_COUNT = 7
+};
+tsb_status tsb_profile_kernel(int32_t kernel_id, hipEvent_t start, hipEvent_t stop);
+
+const char* tsb_status_string(tsb_status status);
+/* Detail of the last failure on the calling thread ("" if none). */
+const char* tsb_last_error(void);
+/* Library ABI version (major * 10000 + minor * 100 + patch). */
+int32_t tsb_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TSUBAME_H */

@@ -1,0 +1,175 @@
+// Device-side building blocks shared by the gfx950 kernels of the
+// tree-replay library: counter-based RNG, uniform and Gumbel maps, logit
+// loads, order-preserving keys and wave64 reductions.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "tsb_internal.hpp"
+
+namespace tsb {
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------- Philox
+// Philox4x32 with 10 rounds (Salmon, Moraes, Dror, Shaw, SC'11): each round
+// multiplies counter words 0 and 2 by fixed 32-bit constants and mixes the
+// high halves with the other words and the key; the key advances by two Weyl
+// increments between rounds.
+constexpr uint32_t kPhiloxM0 = 0xD2511F53u;
+constexpr uint32_t kPhiloxM1 = 0xCD9E8D57u;
+constexpr uint32_t kPhiloxW0 = 0x9E3779B9u;
+constexpr uint32_t kPhiloxW1 = 0xBB67AE85u;
+
+__device__ __forceinline__ uint4 philox10(uint4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        const uint64_t p0 = (uint64_t)kPhiloxM0 * c.x;
+        const uint64_t p1 = (uint64_t)kPhiloxM1 * c.z;
+        const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+        const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+        c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+        k0 += kPhiloxW0;
+        k1 += kPhiloxW1;
+    }
+    return c;
+}
+
+// Counter layout: (draw >> 2, node | stream << 16, request, step); key =
+// (seed lo, seed hi); the draw uses output word draw & 3.
+struct RngKey {
+    uint32_t k0, k1;
+    uint32_t request, step;
+};
+
+__device__ __forceinline__ uint4 rng_block(const RngKey& key, uint32_t node, uint32_t stream,
+                                           uint32_t block) {
+    return philox10(make_uint4(block, (node & 0xFFFFu) | (stream << 16), key.request, key.step),
+                    key.k0, key.k1);
+}
+
+__device__ __forceinline__ uint32_t rng_word(const RngKey& key, uint32_t node, uint32_t stream,
+                                             uint32_t draw) {
+    const uint4 w = rng_block(key, node, stream, draw >> 2);
+    const uint32_t s = draw & 3u;
+    return s == 0 ? w.x : (s == 1 ? w.y : (s == 2 ? w.z : w.w));
+}
+
+// Uniform (2 * (w >> 9) + 1) * 2^-24 in (0, 1): exact in binary32.
+__device__ __forceinline__ float u24f(uint32_t w) {
+    return (float)(((w >> 9) << 1) | 1u) * 0x1p-24f;
+}
+__device__ __forceinline__ double u24d(uint32_t w) {
+    return (double)(((w >> 9) << 1) | 1u) * 0x1p-24;
+}
+
+// Standard Gumbel -ln(-ln u) in binary32 via base-2 logarithms:
+// -ln u = ln2 * (-log2 u);  G = -ln2 * log2(-log2 u) - ln(ln 2).
+__device__ __forceinline__ float gumbel_f32(uint32_t w) {
+    const float u = u24f(w);
+    const float e2 = -__log2f(u);  // > 0
+    return fmaf(-0.69314718055994531f, __log2f(e2), 0.36651292058166432f);
+}
+
+// Upper bound of gumbel_f32 over all 2^23 uniforms, with slack for rounding.
+constexpr float kGumbelMaxBound = 16.75f;
+
+// ---------------------------------------------------------------- logits
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+template <int DT>
+__device__ __forceinline__ float load_logit(const void* base, size_t i) {
+    if (DT == TSB_BF16)
+        return bf16_to_f32(((const uint16_t*)base)[i]);
+    else
+        return ((const float*)base)[i];
+}
+
+// Order-preserving map of a binary32 value to uint32 (larger float -> larger
+// key); -0 is folded onto +0 so equal values give equal keys.
+__device__ __forceinline__ uint32_t ordered_bits(float x) {
+    uint32_t u = __float_as_uint(x);
+    if (u == 0x80000000u) u = 0u;
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float from_ordered_bits(uint32_t k) {
+    const uint32_t u = (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
+    return __uint_as_float(u);
+}
+
+// Candidate key: logit desc, then token id asc.
+__device__ __forceinline__ uint64_t cand_key(float x, uint32_t id) {
+    return ((uint64_t)ordered_bits(x) << 32) | (uint32_t)(~id);
+}
+__device__ __forceinline__ uint32_t cand_id(uint64_t k) { return ~(uint32_t)k; }
+__device__ __forceinline__ float cand_value(uint64_t k) { return from_ordered_bits((uint32_t)(k >> 32)); }
+
+// ---------------------------------------------------------------- wave ops
+__device__ __forceinline__ int lane_id() { return (int)__lane_id(); }
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+    return v;
+}
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+    return v;
+}
+__device__ __forceinline__ int wave_or(int v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v |= __shfl_xor(v, o, kWave);
+    return v;
+}
+__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
+    const uint32_t lo = __shfl((uint32_t)v, src, kWave);
+    const uint32_t hi = __shfl((uint32_t)(v >> 32), src, kWave);
+    return ((uint64_t)hi << 32) | lo;
+}
+__device__ __forceinline__ uint64_t shfl_up_u64(uint64_t v, int d) {
+    const uint32_t lo = __shfl_up((uint32_t)v, d, kWave);
+    const uint32_t hi = __shfl_up((uint32_t)(v >> 32), d, kWave);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// A descending list of the `k` (<= 64) largest uint64 keys seen so far,
+// one entry per lane (lane i holds the i-th largest; lanes >= k hold 0).
+// Key 0 is reserved as "empty".
+struct WaveTopList {
+    uint64_t v;    // this lane's entry
+    uint64_t thr;  // smallest kept key (entry of lane k-1), uniform
+    int k;
+
+    __device__ void init(int kk) {
+        k = kk;
+        v = 0;
+        thr = 0;
+    }
+    // Insert the key held by every lane whose `want` is set (lanes may hold
+    // different keys). Keys <= thr are ignored.
+    __device__ void offer(uint64_t key, bool want) {
+        want = want && key > thr;
+        uint64_t ballot = __ballot(want);
+        while (ballot) {
+            const int src = __ffsll((unsigned long long)ballot) - 1;
+            ballot &= ballot - 1;
+            const uint64_t c = shfl_u64(key, src);
+            if (c <= thr) continue;
+            const int lane = lane_id();
+            const uint64_t gt = __ballot(lane < k && v > c);
+            const int pos = __popcll(gt);
+            const uint64_t up = shfl_up_u64(v, 1);
+            if (lane < k) {
+                if (lane == pos)
+                    v = c;
+                else if (lane > pos)
+                    v = up;
+            }
+            thr = shfl_u64(v, k - 1);
+        }
+    }
+};
+
+}  // namespace tsb

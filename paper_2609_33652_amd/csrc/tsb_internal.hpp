@@ -1,0 +1,105 @@
+// Internal definitions shared by the host layer and the kernels of the
+// tree-replay library: launch geometry and workspace layout.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/tsubame.h"
+
+namespace tsb {
+
+// RNG stream tags (word 1 of the Philox counter, above the node index).
+enum : uint32_t { kStreamReplay = 0, kStreamAccept = 1, kStreamBonus = 2 };
+
+constexpr int kBlock = 256;          // threads per workgroup of the streaming kernels
+constexpr int kReplayTile = 4096;    // vocabulary tile of the replay scan
+constexpr int kWalkGroupsMax = 64;   // workgroups per request in verification
+constexpr int kTargetWorkgroups = 2048;
+
+struct Geometry {
+    int S1;          // workgroups per draft row (row statistics)
+    int seg1;        // elements per draft segment (multiple of 8)
+    int S4;          // workgroups per target row
+    int seg4;        // elements per target segment (multiple of 8)
+    int T;           // replay tiles per row
+    int G;           // workgroups per request in verification (upper bound)
+};
+
+inline int ceil_div(long long a, long long b) { return (int)((a + b - 1) / b); }
+
+inline Geometry geometry(const tsb_config& c) {
+    Geometry g;
+    const long long drows = (long long)c.R * c.D;
+    int s1 = ceil_div(kTargetWorkgroups, drows);
+    int s1max = ceil_div(c.V, 2048);
+    g.S1 = s1 < 1 ? 1 : (s1 > s1max ? s1max : s1);
+    g.seg1 = ceil_div(ceil_div(c.V, g.S1), 8) * 8;
+    g.S1 = ceil_div(c.V, g.seg1);
+    const long long trows = (long long)c.R * (c.B + 1);
+    int s4 = ceil_div(kTargetWorkgroups / 2, trows);
+    int s4max = ceil_div(c.V, 4096);
+    g.S4 = s4 < 1 ? 1 : (s4 > s4max ? s4max : s4);
+    g.seg4 = ceil_div(ceil_div(c.V, g.S4), 8) * 8;
+    g.S4 = ceil_div(c.V, g.seg4);
+    g.T = ceil_div(c.V, kReplayTile);
+    int gw = 512 / (c.R > 0 ? c.R : 1);
+    g.G = gw < 1 ? 1 : (gw > kWalkGroupsMax ? kWalkGroupsMax : gw);
+    return g;
+}
+
+// Workspace carving: every region starts on a 256-byte boundary.
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct PlanWs {  // row statistics partials
+    size_t pm, ps, pk, pf, total;
+};
+struct ReplayWs {  // per (parent, tile) candidates
+    size_t key, idx, cnt, total;
+};
+struct VerifyWs {  // target partials + walk exchange
+    size_t tm, ts, tf, counter, zpart, bkey, bidx, total;
+};
+
+inline PlanWs plan_ws(const tsb_config& c) {
+    const Geometry g = geometry(c);
+    const size_t n = (size_t)c.R * c.D * g.S1;
+    PlanWs w;
+    size_t o = 0;
+    w.pm = o; o = align256(o + n * sizeof(float));
+    w.ps = o; o = align256(o + n * sizeof(double));
+    w.pk = o; o = align256(o + n * (size_t)c.K * sizeof(uint64_t));
+    w.pf = o; o = align256(o + n * sizeof(int32_t));
+    w.total = o;
+    return w;
+}
+
+inline ReplayWs replay_ws(const tsb_config& c) {
+    const Geometry g = geometry(c);
+    const size_t slots = (size_t)c.R * (c.B + 1) * g.T;
+    ReplayWs w;
+    size_t o = 0;
+    w.key = o; o = align256(o + slots * c.K * sizeof(float));
+    w.idx = o; o = align256(o + slots * c.K * sizeof(int32_t));
+    w.cnt = o; o = align256(o + slots * sizeof(int32_t));
+    w.total = o;
+    return w;
+}
+
+inline VerifyWs verify_ws(const tsb_config& c) {
+    const Geometry g = geometry(c);
+    const size_t n = (size_t)c.R * (c.B + 1) * g.S4;
+    VerifyWs w;
+    size_t o = 0;
+    w.tm = o; o = align256(o + n * sizeof(float));
+    w.ts = o; o = align256(o + n * sizeof(double));
+    w.tf = o; o = align256(o + n * sizeof(int32_t));
+    w.counter = o; o = align256(o + (size_t)c.R * sizeof(uint32_t));
+    w.zpart = o; o = align256(o + (size_t)c.R * 2 * kWalkGroupsMax * sizeof(double));
+    w.bkey = o; o = align256(o + (size_t)c.R * 2 * kWalkGroupsMax * sizeof(float));
+    w.bidx = o; o = align256(o + (size_t)c.R * 2 * kWalkGroupsMax * sizeof(int32_t));
+    w.total = o;
+    return w;
+}
+
+}  // namespace tsb

@@ -1,0 +1,37 @@
+// Launchers of the gfx950 kernels (one per stage of a round). Each returns
+// the first HIP error met while enqueueing on `st`.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "tsb_internal.hpp"
+
+namespace tsb {
+
+// Optional event pair around one kernel kind (tsb_profile_kernel).
+struct ProfileHook {
+    int kernel = -1;
+    hipEvent_t start = nullptr, stop = nullptr;
+};
+ProfileHook& profile_hook();
+
+inline hipError_t hook_before(int kernel, hipStream_t st) {
+    const ProfileHook& h = profile_hook();
+    return h.kernel == kernel ? hipEventRecord(h.start, st) : hipSuccess;
+}
+inline hipError_t hook_after(int kernel, hipStream_t st) {
+    const ProfileHook& h = profile_hook();
+    return h.kernel == kernel ? hipEventRecord(h.stop, st) : hipSuccess;
+}
+
+hipError_t launch_plan(const tsb_config& c, float invT, const void* draft, double* draft_lse, int32_t* topk_tok,
+                       float* topk_lp, const tsb_tree& tree, int32_t* req_status, char* ws, hipStream_t st);
+
+hipError_t launch_replay(const tsb_config& c, float invT, const void* draft, const int32_t* topk_tok,
+                         const tsb_tree& tree, uint32_t step, int32_t* node_tok, char* ws, hipStream_t st);
+
+hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, const double* draft_lse,
+                         const void* target, const tsb_tree& tree, const int32_t* node_tok, uint32_t step,
+                         const tsb_verdict& out, char* ws, hipStream_t st);
+
+}  // namespace tsb

@@ -1,0 +1,200 @@
+// Host layer of the C ABI declared in include/tsubame.h: argument
+// validation (before anything is enqueued), workspace sizing and carving,
+// status strings, and the stage sequence of tsb_step.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <hip/hip_runtime.h>
+
+#include "tsb_internal.hpp"
+#include "tsb_kernels.hpp"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+tsb_status fail(tsb_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+tsb_status fail(tsb_status s, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+tsb_status hip_fail(hipError_t e, const char* where) {
+    return fail(TSB_E_HIP, "%s: %s (%d)", where, hipGetErrorString(e), (int)e);
+}
+
+tsb_status check_config(const tsb_config* c) {
+    if (!c) return fail(TSB_E_NULL, "cfg is NULL");
+    if (c->R < 1) return fail(TSB_E_SHAPE, "R=%d must be >= 1", c->R);
+    if (c->D < 1 || c->D > TSB_MAX_D) return fail(TSB_E_SHAPE, "D=%d must be in [1, %d]", c->D, TSB_MAX_D);
+    if (c->K < 1 || c->K > TSB_MAX_K) return fail(TSB_E_SHAPE, "K=%d must be in [1, %d]", c->K, TSB_MAX_K);
+    if (c->V < c->K || c->V > (1 << 30)) return fail(TSB_E_SHAPE, "V=%d must be in [K=%d, 2^30]", c->V, c->K);
+    if (c->B < 0 || c->B > TSB_MAX_B) return fail(TSB_E_SHAPE, "B=%d must be in [0, %d]", c->B, TSB_MAX_B);
+    if ((long long)c->R * (c->B + 1) > (1ll << 31) / 64)
+        return fail(TSB_E_SHAPE, "R*(B+1)=%lld too large", (long long)c->R * (c->B + 1));
+    if (c->dtype != TSB_F32 && c->dtype != TSB_BF16) return fail(TSB_E_DTYPE, "dtype=%u unknown", c->dtype);
+    if (!(isfinite(c->temperature) && c->temperature > 0.f))
+        return fail(TSB_E_TEMPERATURE, "temperature=%g must be finite and > 0", (double)c->temperature);
+    return TSB_OK;
+}
+
+tsb_status check_ws(const tsb_config* c, void* ws, size_t bytes) {
+    const size_t need = tsb_workspace_bytes(c);
+    if (!ws) return fail(TSB_E_NULL, "workspace is NULL");
+    if (((uintptr_t)ws & 255) != 0) return fail(TSB_E_WORKSPACE, "workspace not 256-byte aligned");
+    if (bytes < need) return fail(TSB_E_WORKSPACE, "workspace has %zu bytes, needs %zu", bytes, need);
+    return TSB_OK;
+}
+
+tsb_status check_tree(const tsb_tree* t) {
+    if (!t) return fail(TSB_E_NULL, "tree is NULL");
+    if (!t->parent || !t->depth || !t->rank || !t->n_children || !t->first_child || !t->score || !t->n_nodes ||
+        !t->plan_margin)
+        return fail(TSB_E_NULL, "a tree array is NULL");
+    return TSB_OK;
+}
+
+tsb_status check_verdict(const tsb_verdict* o) {
+    if (!o) return fail(TSB_E_NULL, "verdict is NULL");
+    if (!o->n_acc || !o->acc_node || !o->acc_tok || !o->bonus || !o->req_status)
+        return fail(TSB_E_NULL, "a required verdict array is NULL");
+    return TSB_OK;
+}
+
+float inv_temperature(float T) {
+    volatile float one = 1.0f;  // binary32 division, correctly rounded
+    return one / T;
+}
+
+#define TRY(x)                              \
+    do {                                    \
+        const tsb_status s__ = (x);         \
+        if (s__ != TSB_OK) return s__;      \
+    } while (0)
+
+}  // namespace
+
+namespace tsb {
+ProfileHook& profile_hook() {
+    static thread_local ProfileHook h;
+    return h;
+}
+}  // namespace tsb
+
+extern "C" {
+
+size_t tsb_workspace_bytes(const tsb_config* cfg) {
+    if (!cfg) return 0;
+    char saved[sizeof g_last_error];
+    memcpy(saved, g_last_error, sizeof saved);
+    const tsb_status s = check_config(cfg);
+    memcpy(g_last_error, saved, sizeof saved);
+    if (s != TSB_OK) return 0;
+    const size_t a = tsb::plan_ws(*cfg).total;
+    const size_t b = tsb::replay_ws(*cfg).total;
+    const size_t c = tsb::verify_ws(*cfg).total;
+    size_t m = a > b ? a : b;
+    m = m > c ? m : c;
+    return m < 256 ? 256 : m;
+}
+
+tsb_status tsb_plan(const tsb_config* cfg, const void* draft, double* draft_lse, int32_t* topk_tok, float* topk_lp,
+                    const tsb_tree* tree, int32_t* req_status, void* workspace, size_t workspace_bytes,
+                    hipStream_t stream) {
+    g_last_error[0] = 0;
+    TRY(check_config(cfg));
+    if (!draft || !draft_lse || !topk_tok || !topk_lp || !req_status)
+        return fail(TSB_E_NULL, "tsb_plan: a required array is NULL");
+    TRY(check_tree(tree));
+    TRY(check_ws(cfg, workspace, workspace_bytes));
+    const hipError_t e = tsb::launch_plan(*cfg, inv_temperature(cfg->temperature), draft, draft_lse, topk_tok,
+                                          topk_lp, *tree, req_status, (char*)workspace, stream);
+    return e == hipSuccess ? TSB_OK : hip_fail(e, "tsb_plan");
+}
+
+tsb_status tsb_replay(const tsb_config* cfg, const void* draft, const int32_t* topk_tok, const tsb_tree* tree,
+                      uint32_t step, int32_t* node_tok, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    g_last_error[0] = 0;
+    TRY(check_config(cfg));
+    if (!draft || !topk_tok || !node_tok) return fail(TSB_E_NULL, "tsb_replay: a required array is NULL");
+    TRY(check_tree(tree));
+    TRY(check_ws(cfg, workspace, workspace_bytes));
+    const hipError_t e = tsb::launch_replay(*cfg, inv_temperature(cfg->temperature), draft, topk_tok, *tree, step,
+                                            node_tok, (char*)workspace, stream);
+    return e == hipSuccess ? TSB_OK : hip_fail(e, "tsb_replay");
+}
+
+tsb_status tsb_verify(const tsb_config* cfg, const void* draft, const double* draft_lse, const void* target,
+                      const tsb_tree* tree, const int32_t* node_tok, uint32_t step, const tsb_verdict* out,
+                      void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    g_last_error[0] = 0;
+    TRY(check_config(cfg));
+    if (!draft || !draft_lse || !target || !node_tok) return fail(TSB_E_NULL, "tsb_verify: a required array is NULL");
+    TRY(check_tree(tree));
+    TRY(check_verdict(out));
+    TRY(check_ws(cfg, workspace, workspace_bytes));
+    const hipError_t e = tsb::launch_verify(*cfg, inv_temperature(cfg->temperature), draft, draft_lse, target, *tree,
+                                            node_tok, step, *out, (char*)workspace, stream);
+    return e == hipSuccess ? TSB_OK : hip_fail(e, "tsb_verify");
+}
+
+tsb_status tsb_step(const tsb_config* cfg, const void* draft, const void* target, uint32_t step, double* draft_lse,
+                    int32_t* topk_tok, float* topk_lp, const tsb_tree* tree, int32_t* node_tok,
+                    const tsb_verdict* out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    g_last_error[0] = 0;
+    TRY(check_config(cfg));
+    if (!draft || !target || !draft_lse || !topk_tok || !topk_lp || !node_tok)
+        return fail(TSB_E_NULL, "tsb_step: a required array is NULL");
+    TRY(check_tree(tree));
+    TRY(check_verdict(out));
+    TRY(check_ws(cfg, workspace, workspace_bytes));
+    const float invT = inv_temperature(cfg->temperature);
+    char* ws = (char*)workspace;
+    hipError_t e = tsb::launch_plan(*cfg, invT, draft, draft_lse, topk_tok, topk_lp, *tree, out->req_status, ws, stream);
+    if (e != hipSuccess) return hip_fail(e, "tsb_step/plan");
+    e = tsb::launch_replay(*cfg, invT, draft, topk_tok, *tree, step, node_tok, ws, stream);
+    if (e != hipSuccess) return hip_fail(e, "tsb_step/replay");
+    e = tsb::launch_verify(*cfg, invT, draft, draft_lse, target, *tree, node_tok, step, *out, ws, stream);
+    if (e != hipSuccess) return hip_fail(e, "tsb_step/verify");
+    return TSB_OK;
+}
+
+tsb_status tsb_profile_kernel(int32_t kernel_id, hipEvent_t start, hipEvent_t stop) {
+    g_last_error[0] = 0;
+    tsb::ProfileHook& h = tsb::profile_hook();
+    if (kernel_id < 0) {
+        h = tsb::ProfileHook();
+        return TSB_OK;
+    }
+    if (kernel_id >= TSB_KERNEL_COUNT) return fail(TSB_E_SHAPE, "kernel_id=%d unknown", kernel_id);
+    if (!start || !stop) return fail(TSB_E_NULL, "events are NULL");
+    h.kernel = kernel_id;
+    h.start = start;
+    h.stop = stop;
+    return TSB_OK;
+}
+
+const char* tsb_status_string(tsb_status s) {
+    switch (s) {
+        case TSB_OK: return "ok";
+        case TSB_E_NULL: return "a required pointer is NULL";
+        case TSB_E_SHAPE: return "a size is out of range";
+        case TSB_E_DTYPE: return "unknown logit dtype";
+        case TSB_E_TEMPERATURE: return "temperature must be finite and > 0";
+        case TSB_E_WORKSPACE: return "workspace too small or misaligned";
+        case TSB_E_HIP: return "HIP runtime error";
+        case TSB_E_DEVICE: return "no usable device";
+    }
+    return "unknown status";
+}
+
+const char* tsb_last_error(void) { return g_last_error; }
+
+int32_t tsb_version(void) { return 100; }
+
+}  // extern "C"
