@@ -31,6 +31,17 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def events(n):
+    """n pairs of timing events, created up front (torch creates them lazily on first record)."""
+    import torch
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    for a, b in ev:
+        a.record()
+        b.record()
+    torch.cuda.synchronize()
+    return ev
+
+
 # ---------------------------------------------------------------- CPU oracle
 _CPU = {}
 
@@ -39,9 +50,7 @@ def _cpu_task(args):
     r, step = args
     from oracle import step as ostep
     c = _CPU["cfg"]
-    d = _CPU["draft"][r].float().numpy()
-    t = _CPU["target"][r].float().numpy()
-    out = ostep.step_request(d, t, c["T"], c["K"], c["B"], _CPU["seed"], step, r)
+    out = ostep.step_request(_CPU["draft"][r], _CPU["target"][r], c["T"], c["K"], c["B"], _CPU["seed"], step, r)
     return out["n_acc"]
 
 
@@ -59,8 +68,12 @@ def cpu_baseline(cfg, seed, requests):
         dep[r, :pl["tree"]["n_nodes"]] = torch.from_numpy(pl["tree"]["depth"])
     target = W.target_from_base(cfg, base, sigma, dep)
     del base
-    _CPU.update(cfg=cfg, draft=draft, target=target, seed=seed)
-    tasks = [(r % cfg["R"], r // cfg["R"]) for r in range(requests)]
+    # plain numpy in the workers: no torch (OpenMP) use after fork
+    nr = min(requests, cfg["R"])
+    _CPU.update(cfg=cfg, draft=draft[:nr].float().numpy(), target=target[:nr].float().numpy(), seed=seed)
+    del draft, target
+    log("cpu baseline: inputs ready")
+    tasks = [(r % nr, r // nr) for r in range(requests)]
     cores = min(16, len(os.sched_getaffinity(0)), len(tasks))
     ctx = mp.get_context("fork")
     t0 = time.perf_counter()
@@ -129,7 +142,7 @@ def main():
     torch.cuda.synchronize()
 
     K4 = tsb.KERNELS.index("target_partials")
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    ev = events(args.steps)
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -149,8 +162,7 @@ def main():
     # untimed passes: per-kernel breakdown and acceptance statistics
     kern_us = {}
     for kid, name in enumerate(tsb.KERNELS):
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-               for _ in range(args.breakdown_steps)]
+        evs = events(args.breakdown_steps)
         for i in range(args.breakdown_steps):
             tsb.profile_kernel(kid, evs[i][0], evs[i][1])
             rnd.step(drafts[i % P], targets[i % P], i)
