@@ -32,6 +32,9 @@ __global__ __launch_bounds__(kBlock) void draft_partials(const void* __restrict_
     const int lo = s * seg;
     const int hi = min(V, lo + seg);
 
+    __shared__ double s_exp[kExpTable];
+    exp64_table_init(s_exp);
+
     float m = -INFINITY;
     double sum = 0.0;
     int bad = 0;
@@ -70,12 +73,12 @@ __global__ __launch_bounds__(kBlock) void draft_partials(const void* __restrict_
             if (in && a[j] > -INFINITY && a[j] < INFINITY) cm = fmaxf(cm, a[j]);
         }
         if (cm > m) {
-            sum = (m == -INFINITY) ? 0.0 : sum * exp((double)m - (double)cm);
+            sum = (m == -INFINITY) ? 0.0 : sum * exp64((double)m - (double)cm, s_exp);
             m = cm;
         }
 #pragma unroll
         for (int j = 0; j < 8; ++j)
-            if (i0 + j < hi && a[j] > -INFINITY && a[j] < INFINITY) sum += exp((double)a[j] - (double)m);
+            if (i0 + j < hi && a[j] > -INFINITY && a[j] < INFINITY) sum += exp64((double)a[j] - (double)m, s_exp);
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             const bool ok = (i0 + j < hi) && !isnan(x[j]);

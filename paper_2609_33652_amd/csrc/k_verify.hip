@@ -162,13 +162,15 @@ __device__ void request_barrier(uint32_t* counter, uint32_t target, int* timeout
     if (threadIdx.x == 0) {
         __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
         uint32_t spins = 0;
-        while (__hip_atomic_load(counter, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < target) {
+        // relaxed polls (no cache invalidation per poll), one acquire after
+        while (__hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
             __builtin_amdgcn_s_sleep(2);
-            if (++spins > (1u << 22)) {
+            if (++spins > (1u << 23)) {
                 *timeout = 1;
                 break;
             }
         }
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     }
     __syncthreads();
 }
@@ -214,127 +216,305 @@ __device__ double block_sum(double v) {
     return tot;
 }
 
-// sum_v exp(a_v - L0) over this slice of target row `trow`, binary64 terms.
+// ---------------------------------------------------------------- walk
+// A walk workgroup owns the slice [v0, v1) of the vocabulary. At every
+// visited node u with children, the first pass over the slice computes, in
+// binary64, p~_v = exp(a^t_{u,v} - L0) (L0 the streamed estimate of the
+// target normaliser) and q_v = exp(a^d_{depth(u),v} - lse_d), keeps both in
+// LDS and returns sum p~ (the exact normaliser is L0 + ln sum_v p~_v over the
+// request). The residual passes after rejections and the residual bonus then
+// read (p~, q) from LDS. Slices longer than the LDS cache are processed in
+// chunks that are recomputed in every pass.
+constexpr int kWalkThreads = 512;
+constexpr int kWalkCache = kWalkTokensPerGroup;  // tokens of (p~, q) held in LDS
+
 template <int DT>
-__device__ double mass_slice(const WalkArgs& A, bool vec, size_t trow, double L0, int v0, int v1) {
-    double acc = 0.0;
-    for (int g = v0 / 4 + (int)threadIdx.x; g * 4 < v1; g += kBlock) {
-        const int e0 = g * 4;
-        const int valid = min(4, v1 - e0);
-        float xt[4];
-        load4<DT>(A.target, trow + e0, valid, vec, xt);
+__device__ __forceinline__ void load4_scaled(const void* base, size_t off, int valid, bool vec, float invT,
+                                             float a[4]) {
+    float x[4];
+    load4<DT>(base, off, valid, vec, x);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const float a = xt[e] * A.invT;
-            if (e < valid && a > -INFINITY) acc += exp((double)a - L0);
-        }
-    }
-    return block_sum(acc);
+    for (int e = 0; e < 4; ++e) a[e] = e < valid ? x[e] * invT : -INFINITY;
 }
 
-// Residual mass sum_v max(p_v - C q_v, 0) over this slice, binary64 terms
-// (the difference cancels when the target is close to the draft).
-template <int DT>
-__device__ double residual_slice(const WalkArgs& A, bool vec, size_t trow, size_t drow, double Lt, double Ld,
-                                 double C, int v0, int v1) {
-    double acc = 0.0;
-    for (int g = v0 / 4 + (int)threadIdx.x; g * 4 < v1; g += kBlock) {
-        const int e0 = g * 4;
-        const int valid = min(4, v1 - e0);
-        float xt[4], xd[4];
-        load4<DT>(A.target, trow + e0, valid, vec, xt);
-        load4<DT>(A.draft, drow + e0, valid, vec, xd);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            if (e >= valid) continue;
-            const double p = exp((double)(xt[e] * A.invT) - Lt);
-            const double q = exp((double)(xd[e] * A.invT) - Ld);
-            const double rr = p - C * q;
-            acc += rr > 0.0 ? rr : 0.0;
-        }
-    }
-    return block_sum(acc);
+// Block-wide binary64 sum for kWalkThreads threads (fixed order).
+__device__ double walk_sum(double v) {
+    __shared__ double red[kWalkThreads / kWave];
+    const double w = wave_sum(v);
+    if ((threadIdx.x % kWave) == 0) red[threadIdx.x / kWave] = w;
+    __syncthreads();
+    double tot = 0.0;
+    for (int i = 0; i < kWalkThreads / kWave; ++i) tot += red[i];
+    __syncthreads();
+    return tot;
 }
 
-// Bonus keys ln max(p_v - C q_v, 0) + G_v over this slice; returns the best
-// (key, token) and the slice's residual mass.
+struct WalkSlice {
+    int v0, v1, nchunks;
+    double* p;  // LDS [kWalkCache]
+    double* q;  // LDS [kWalkCache]
+};
+
+// First pass at a node: fill (p~, q) for chunk c (into LDS when the slice has
+// one chunk) and return sum p~ over the chunk. Groups of four tokens per
+// thread; two groups are loaded before either is used.
 template <int DT>
-__device__ void bonus_slice(const WalkArgs& A, bool vec, const RngKey& key, uint32_t node, size_t trow, size_t drow,
-                            bool use_q, double Lt, double Ld, double C, int v0, int v1, float* bk, int* bi,
-                            double* mass) {
-    float best = -INFINITY;
-    int bidx = 0x7FFFFFFF;
+__device__ double fill_chunk(const WalkArgs& A, bool vec, const WalkSlice& S, int c, size_t trow, size_t drow,
+                             double L0, double Ld, const double* et, bool store) {
+    const int c0 = S.v0 + c * kWalkCache;
+    const int n = min(kWalkCache, S.v1 - c0);
     double acc = 0.0;
-    const SplitF Ls = split(Lt);
-    for (int g = v0 / 4 + (int)threadIdx.x; g * 4 < v1; g += kBlock) {
-        const int e0 = g * 4;
-        const int valid = min(4, v1 - e0);
-        float xt[4], xd[4];
-        load4<DT>(A.target, trow + e0, valid, vec, xt);
-        if (use_q) load4<DT>(A.draft, drow + e0, valid, vec, xd);
-        const uint4 w = rng_block(key, node, kStreamBonus, (uint32_t)g);
-        const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+    for (int base = 0; base * 4 < n; base += 2 * kWalkThreads) {
+        float at[2][4], ad[2][4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            if (e >= valid) continue;
-            float lr;
-            if (use_q) {
-                const double p = exp((double)(xt[e] * A.invT) - Lt);
-                const double q = exp((double)(xd[e] * A.invT) - Ld);
-                const double rr = p - C * q;
-                acc += rr > 0.0 ? rr : 0.0;
-                lr = rr > 0.0 ? (float)log(rr) : -INFINITY;
-            } else {
-                lr = (xt[e] * A.invT - Ls.hi) - Ls.lo;  // ln p_v up to a constant
-                acc += 1.0;
-            }
-            if (lr > -INFINITY) {
-                const float kv = lr + gumbel_f32(ws[e]);
-                const int v = e0 + e;
-                if (kv > best || (kv == best && v < bidx)) {
-                    best = kv;
-                    bidx = v;
+        for (int j = 0; j < 2; ++j) {
+            const int i = (base + j * kWalkThreads + (int)threadIdx.x) * 4;
+            const int valid = max(0, min(4, n - i));
+            load4_scaled<DT>(A.target, trow + c0 + (valid ? i : 0), valid, vec, A.invT, at[j]);
+            load4_scaled<DT>(A.draft, drow + c0 + (valid ? i : 0), valid, vec, A.invT, ad[j]);
+        }
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int i = (base + j * kWalkThreads + (int)threadIdx.x) * 4;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                if (i + e >= n) break;
+                const double pt = at[j][e] > -INFINITY ? exp64((double)at[j][e] - L0, et) : 0.0;
+                const double qd = ad[j][e] > -INFINITY ? exp64((double)ad[j][e] - Ld, et) : 0.0;
+                acc += pt;
+                if (store) {
+                    S.p[i + e] = pt;
+                    S.q[i + e] = qd;
                 }
             }
         }
     }
+    return acc;
+}
+
+// Token-wise visit of (p = p~ * inv, q) over the slice: from LDS when cached,
+// else recomputed chunk by chunk. f(token, p, q) is called for every token.
+template <int DT, typename F>
+__device__ void visit_pq(const WalkArgs& A, bool vec, const WalkSlice& S, bool cached, size_t trow, size_t drow,
+                         double L0, double inv, double Ld, const double* et, F f) {
+    if (cached) {
+        const int n = S.v1 - S.v0;
+        for (int i = threadIdx.x; i < n; i += kWalkThreads) f(S.v0 + i, S.p[i] * inv, S.q[i]);
+        return;
+    }
+    for (int c = 0; c < S.nchunks; ++c) {
+        const int c0 = S.v0 + c * kWalkCache;
+        const int n = min(kWalkCache, S.v1 - c0);
+        for (int i4 = threadIdx.x; i4 * 4 < n; i4 += kWalkThreads) {
+            const int i = i4 * 4;
+            const int valid = min(4, n - i);
+            float at[4], ad[4];
+            load4_scaled<DT>(A.target, trow + c0 + i, valid, vec, A.invT, at);
+            load4_scaled<DT>(A.draft, drow + c0 + i, valid, vec, A.invT, ad);
+            for (int e = 0; e < valid; ++e) {
+                const double pt = at[e] > -INFINITY ? exp64((double)at[e] - L0, et) : 0.0;
+                const double qd = ad[e] > -INFINITY ? exp64((double)ad[e] - Ld, et) : 0.0;
+                f(c0 + i + e, pt * inv, qd);
+            }
+        }
+    }
+}
+
+// (key, token) argmax across the workgroup: key desc, token asc.
+__device__ void walk_argmax(float* best, int* bidx) {
+    float b = *best;
+    int bi = *bidx;
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
-        const float ok = __shfl_xor(best, off, kWave);
-        const int oi = __shfl_xor(bidx, off, kWave);
-        if (ok > best || (ok == best && oi < bidx)) {
-            best = ok;
-            bidx = oi;
+        const float ok = __shfl_xor(b, off, kWave);
+        const int oi = __shfl_xor(bi, off, kWave);
+        if (ok > b || (ok == b && oi < bi)) {
+            b = ok;
+            bi = oi;
         }
     }
-    __shared__ float rk[kBlock / kWave];
-    __shared__ int ri[kBlock / kWave];
-    __shared__ double rm[kBlock / kWave];
-    const double wm = wave_sum(acc);
+    __shared__ float rk[kWalkThreads / kWave];
+    __shared__ int ri[kWalkThreads / kWave];
     if ((threadIdx.x % kWave) == 0) {
-        rk[threadIdx.x / kWave] = best;
-        ri[threadIdx.x / kWave] = bidx;
-        rm[threadIdx.x / kWave] = wm;
+        rk[threadIdx.x / kWave] = b;
+        ri[threadIdx.x / kWave] = bi;
     }
     __syncthreads();
-    float fb = rk[0];
-    int fi = ri[0];
-    double fm = 0.0;
-    for (int i = 0; i < kBlock / kWave; ++i) {
-        if (rk[i] > fb || (rk[i] == fb && ri[i] < fi)) {
-            fb = rk[i];
-            fi = ri[i];
+    b = rk[0];
+    bi = ri[0];
+    for (int i = 1; i < kWalkThreads / kWave; ++i)
+        if (rk[i] > b || (rk[i] == b && ri[i] < bi)) {
+            b = rk[i];
+            bi = ri[i];
         }
-        fm += rm[i];
-    }
     __syncthreads();
-    *bk = fb;
-    *bi = fi;
-    *mass = fm;
+    *best = b;
+    *bidx = bi;
+}
+
+// Bonus sample from p_u alone (leaf, or empty residual): argmax ln p_v + G_v,
+// read straight from the target row.
+template <int DT>
+__device__ void bonus_from_p(const WalkArgs& A, bool vec, const WalkSlice& S, size_t trow, double Lt,
+                             const RngKey& key, uint32_t node, float* bk, int* bi) {
+    float best = -INFINITY;
+    int bidx = 0x7FFFFFFF;
+    const SplitF Ls = split(Lt);
+    const int n = S.v1 - S.v0;
+    for (int i4 = threadIdx.x; i4 * 4 < n; i4 += kWalkThreads) {
+        const int i = i4 * 4;
+        const int valid = min(4, n - i);
+        float at[4];
+        load4_scaled<DT>(A.target, trow + S.v0 + i, valid, vec, A.invT, at);
+        const uint4 w = rng_block(key, node, kStreamBonus, (uint32_t)((S.v0 + i) >> 2));
+        const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            if (e >= valid || at[e] == -INFINITY) continue;
+            const float kv = ((at[e] - Ls.hi) - Ls.lo) + gumbel_f32(ws[e]);  // ln p_v + G_v
+            const int v = S.v0 + i + e;
+            if (kv > best || (kv == best && v < bidx)) {
+                best = kv;
+                bidx = v;
+            }
+        }
+    }
+    walk_argmax(&best, &bidx);
+    *bk = best;
+    *bi = bidx;
+}
+
+// Exchange among the G workgroups of a request: each contributes up to four
+// binary64 partials (and optionally a (key, token) pair); everyone gets the
+// sums, added in workgroup order, and the best pair.
+constexpr int kExVals = 4;
+
+struct Exchange {
+    const WalkArgs* A;
+    int r, g, G;
+    uint32_t nb;  // barriers passed
+    int timeout;
+
+    template <int NV>
+    __device__ void run(const double (&part)[NV], double (&tot)[NV], float bk = 0.f, int bi = 0,
+                        float* fk = nullptr, int* fi = nullptr) {
+        static_assert(NV <= kExVals, "exchange width");
+        const int slot = (r * 2 + (nb & 1)) * kWalkGroupsMax + g;
+        if (threadIdx.x == 0) {
+#pragma unroll
+            for (int i = 0; i < NV; ++i) A->zpart[(size_t)slot * kExVals + i] = part[i];
+            A->bkey[slot] = bk;
+            A->bidx[slot] = bi;
+        }
+        ++nb;
+        request_barrier(&A->counters[r], nb * (uint32_t)G, &timeout);
+#pragma unroll
+        for (int i = 0; i < NV; ++i) tot[i] = 0.0;
+        float kb = -INFINITY;
+        int ib = 0x7FFFFFFF;
+        for (int h = 0; h < G; ++h) {
+            const int sl = (r * 2 + ((nb - 1) & 1)) * kWalkGroupsMax + h;
+#pragma unroll
+            for (int i = 0; i < NV; ++i)
+                tot[i] += __hip_atomic_load(&A->zpart[(size_t)sl * kExVals + i], __ATOMIC_RELAXED,
+                                            __HIP_MEMORY_SCOPE_AGENT);
+            if (fk) {
+                const float k = __hip_atomic_load(&A->bkey[sl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                const int i = __hip_atomic_load(&A->bidx[sl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (k > kb || (k == kb && i < ib)) {
+                    kb = k;
+                    ib = i;
+                }
+            }
+        }
+        if (fk) {
+            *fk = kb;
+            *fi = ib;
+        }
+    }
+    __device__ double sum(double part) {
+        double p[1] = {part}, t[1];
+        run<1>(p, t);
+        return t[0];
+    }
+    __device__ int best(float bk, int bi, double part, double* tot) {
+        double p[1] = {part}, t[1];
+        float fk;
+        int fi;
+        run<1>(p, t, bk, bi, &fk, &fi);
+        *tot = t[0];
+        return fk > -INFINITY ? fi : -1;
+    }
+};
+
+// Relative half-width of the band in which an acceptance test taken with the
+// streamed normaliser is recomputed with the exact one (the streamed
+// normaliser is within ~1e-6 of it: binary32 terms, binary64 accumulation).
+constexpr double kDecisionBand = 1e-4;
+
+// First exact pass at a node: fills (p~, q) and returns the slice partials of
+// sum p~, and, for the first residual (C = 1), sum p~ and sum q over tokens
+// with p~ > q (beyond the band where the normaliser could flip the sign) and
+// the number of tokens inside that band.
+template <int DT>
+__device__ void fill_pass(const WalkArgs& A, bool vec, const WalkSlice& S, bool cached, size_t trow, size_t drow,
+                          double L0, double Ld, const double* et, double (&out)[4]) {
+    double sp = 0.0, pa = 0.0, qa = 0.0, band = 0.0;
+    for (int c = 0; c < S.nchunks; ++c) {
+        const int c0 = S.v0 + c * kWalkCache;
+        const int n = min(kWalkCache, S.v1 - c0);
+        // one group of four tokens per iteration; the next group's loads are
+        // issued before this group's arithmetic
+        int i = (int)threadIdx.x * 4;
+        float at[4], ad[4];
+        {
+            const int valid = max(0, min(4, n - i));
+            load4_scaled<DT>(A.target, trow + c0 + (valid ? i : 0), valid, vec, A.invT, at);
+            load4_scaled<DT>(A.draft, drow + c0 + (valid ? i : 0), valid, vec, A.invT, ad);
+        }
+        for (; i < n; i += 4 * kWalkThreads) {
+            const int inext = i + 4 * kWalkThreads;
+            float nt[4], nd[4];
+            const int vn = max(0, min(4, n - inext));
+            load4_scaled<DT>(A.target, trow + c0 + (vn ? inext : 0), vn, vec, A.invT, nt);
+            load4_scaled<DT>(A.draft, drow + c0 + (vn ? inext : 0), vn, vec, A.invT, nd);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const double pt = at[e] > -INFINITY ? exp64((double)at[e] - L0, et) : 0.0;
+                const double qd = ad[e] > -INFINITY ? exp64((double)ad[e] - Ld, et) : 0.0;
+                sp += pt;
+                if (pt > qd * (1.0 + 1e-5)) {
+                    pa += pt;
+                    qa += qd;
+                } else if (pt >= qd * (1.0 - 1e-5) && pt > 0.0) {
+                    band += 1.0;
+                }
+                if (cached && i + e < n) {
+                    S.p[i + e] = pt;
+                    S.q[i + e] = qd;
+                }
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                at[e] = nt[e];
+                ad[e] = nd[e];
+            }
+        }
+    }
+    out[0] = walk_sum(sp);
+    out[1] = walk_sum(pa);
+    out[2] = walk_sum(qa);
+    out[3] = walk_sum(band);
 }
 
 template <int DT, bool VEC>
-__global__ __launch_bounds__(kBlock) void verify_walk(WalkArgs A) {
+__global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
+    extern __shared__ double s_pq[];  // [2 * kWalkCache]: p~ then q
+    __shared__ double s_exp[kExpTable];
+    __shared__ int s_bad;
+    __shared__ int s_tok[TSB_MAX_K];
+    __shared__ float s_xd[TSB_MAX_K], s_xt[TSB_MAX_K];
+    __shared__ double s_u[TSB_MAX_K];
     const int g = blockIdx.x;
     const int G = gridDim.x;
     const int r = A.r0 + blockIdx.y;
@@ -344,98 +524,99 @@ __global__ __launch_bounds__(kBlock) void verify_walk(WalkArgs A) {
     const bool vec = VEC;
     int* status_p = A.out.req_status + r;
     const int n = A.tree.n_nodes[r];
-
     const bool lead = (g == 0 && tid == 0);
-    int n_acc_out = -1, bonus_out = -1, add_status = 0;
+    exp64_table_init(s_exp);
 
-    // vocabulary slice of this workgroup (multiple of 4)
-    // (an empty slice is [0, 0): its start must stay a multiple of 4)
-    const int span = ((A.V + G - 1) / G + 3) & ~3;
-    const bool has_slice = (long long)g * span < A.V;
-    const int v0 = has_slice ? g * span : 0;
-    const int v1 = has_slice ? min(A.V, v0 + span) : 0;
-
-    // target rows of every tree node must be finite
-    __shared__ int s_bad;
-    if (tid == 0) s_bad = 0;
-    __syncthreads();
-    const bool draft_bad = (*status_p & TSB_REQ_NONFINITE) != 0;
-    if (!draft_bad) {
-        for (int i = tid; i < n; i += kBlock) {
-            int b;
-            const double l = target_lse(A, r, i, &b);
-            if (b) atomicOr(&s_bad, 1);
-            if (A.out.target_lse && (i % G) == g) A.out.target_lse[tb + i] = b ? (double)NAN : l;
-        }
+    // vocabulary slice (start a multiple of 4; an empty slice is [0, 0))
+    WalkSlice S;
+    {
+        const int span = ((A.V + G - 1) / G + 3) & ~3;
+        const bool has = (long long)g * span < A.V;
+        S.v0 = has ? g * span : 0;
+        S.v1 = has ? min(A.V, S.v0 + span) : 0;
+        S.nchunks = (S.v1 - S.v0 + kWalkCache - 1) / kWalkCache;
+        S.p = s_pq;
+        S.q = s_pq + kWalkCache;
     }
-    __syncthreads();
-    if (A.out.target_lse && (draft_bad || s_bad))
-        for (int i = tid; i < B1; i += kBlock)
-            if ((i % G) == g) A.out.target_lse[tb + i] = (double)NAN;
-    if (A.out.target_lse && !draft_bad && !s_bad)
-        for (int i = n + tid; i < B1; i += kBlock)
-            if ((i % G) == g) A.out.target_lse[tb + i] = (double)NAN;
+    const bool cached = S.nchunks <= 1;
+    const bool draft_bad = (*status_p & TSB_REQ_NONFINITE) != 0;
 
     int tcount = 0;
-    auto trace_put = [&](int child, double U, double ratio, double z) {
-        if (lead && A.out.trace && tcount < TSB_TRACE_MAX) {
-            double* t = A.out.trace + ((size_t)r * TSB_TRACE_MAX + tcount) * 4;
-            t[0] = child;
-            t[1] = U;
-            t[2] = ratio;
-            t[3] = z;
-        }
-        ++tcount;
-    };
-    auto trace_set_z = [&](double z) {
-        if (lead && A.out.trace && tcount >= 1 && tcount <= TSB_TRACE_MAX)
-            A.out.trace[((size_t)r * TSB_TRACE_MAX + tcount - 1) * 4 + 3] = z;
-    };
+    double* const trace = (lead && A.out.trace) ? A.out.trace + (size_t)r * TSB_TRACE_MAX * 4 : nullptr;
 
-    if (!draft_bad && !s_bad) {
+    int bonus_out = -1, add_status = 0, nacc = 0;
+    if (!draft_bad) {
         RngKey key;
         key.k0 = A.k0;
         key.k1 = A.k1;
         key.request = (uint32_t)r;
         key.step = A.step;
-        uint32_t nb = 0;  // barriers passed
-        int timeout = 0;
+        Exchange X{&A, r, g, G, 0u, 0};
         int u = 0;
-        int nacc = 0;
         while (true) {
             const int m = A.tree.n_children[tb + u];
             const int d = A.tree.depth[tb + u];
             int tbad;
-            const double Lt0 = target_lse(A, r, u, &tbad);
+            const double L0 = target_lse(A, r, u, &tbad);
             const size_t trow = ((size_t)r * B1 + u) * (size_t)A.V;
             const size_t drow = ((size_t)r * A.D + (d < A.D ? d : 0)) * (size_t)A.V;
-            const double Ld = (m > 0) ? A.draft_lse[(size_t)r * A.D + d] : 0.0;
-            double Lt = Lt0;
-            if (m > 0) {
-                // binary64 normaliser of p_u (the streamed estimate has binary32 terms)
-                const double part = mass_slice<DT>(A, vec, trow, Lt0, v0, v1);
-                const int slot = (r * 2 + (nb & 1)) * kWalkGroupsMax + g;
-                if (tid == 0) A.zpart[slot] = part;
-                ++nb;
-                request_barrier(&A.counters[r], nb * (uint32_t)G, &timeout);
-                double S0 = 0.0;
-                for (int h = 0; h < G; ++h)
-                    S0 += __hip_atomic_load(&A.zpart[(r * 2 + ((nb - 1) & 1)) * kWalkGroupsMax + h], __ATOMIC_RELAXED,
-                                            __HIP_MEMORY_SCOPE_AGENT);
-                Lt = Lt0 + log(S0);
+            if (m == 0) {  // accepted leaf: bonus from p_u
+                float bk;
+                int bi;
+                double unused;
+                bonus_from_p<DT>(A, vec, S, trow, L0, key, (uint32_t)u, &bk, &bi);
+                bonus_out = X.best(bk, bi, 0.0, &unused);
+                break;
             }
-            double C = 0.0, S = 1.0, Z = 1.0;
+            const double Ld = A.draft_lse[(size_t)r * A.D + d];
+            // children of u: tokens, their logits and the uniforms, fetched together
+            const int fc = A.tree.first_child[tb + u];
+            if (tid < m) {
+                const int y = A.node_tok[tb + fc + tid];
+                s_tok[tid] = y;
+                s_xd[tid] = load_logit<DT>(A.draft, drow + y) * A.invT;
+                s_xt[tid] = load_logit<DT>(A.target, trow + y) * A.invT;
+                s_u[tid] = u24d(rng_word(key, (uint32_t)(fc + tid), kStreamAccept, 0u));
+            }
+            __syncthreads();
+
+            bool exact = false;
+            double Lt = L0, inv = 1.0;
+            double C = 0.0, Sq = 1.0, Z = 1.0, Z1 = -1.0;
             bool accepted = false, degenerate = false;
             for (int j = 0; j < m; ++j) {
-                const int c = A.tree.first_child[tb + u] + j;
-                const int y = A.node_tok[tb + c];
-                const double qy = exp((double)(load_logit<DT>(A.draft, drow + y) * A.invT) - Ld);
-                const double py = exp((double)(load_logit<DT>(A.target, trow + y) * A.invT) - Lt);
-                const double W = Z / S;
-                const double num = py - C * qy;
-                const double ratio = (num > 0.0 ? num : 0.0) / (W * qy);
-                const double U = u24d(rng_word(key, (uint32_t)c, kStreamAccept, 0u));
-                trace_put(c, U, ratio, -1.0);
+                const int c = fc + j;
+                const int y = s_tok[j];
+                const double qy = exp((double)s_xd[j] - Ld);
+                const double U = s_u[j];
+                const double W = Z / Sq;
+                double py = exp((double)s_xt[j] - Lt);
+                double num = py - C * qy;
+                double ratio = (num > 0.0 ? num : 0.0) / (W * qy);
+                if (trace && tcount < TSB_TRACE_MAX) {
+                    trace[tcount * 4 + 0] = c;
+                    trace[tcount * 4 + 1] = U;
+                    trace[tcount * 4 + 3] = -1.0;
+                }
+                ++tcount;
+                // Before the exact pass only the first test of a node is taken, with
+                // the streamed normaliser; it stands if U is clear of the ratio by
+                // the band. A rejection needs the exact residual anyway.
+                if (!exact && (fabs(U - ratio) <= kDecisionBand * ratio || !(U < ratio))) {
+                    double part[4], tot[4];
+                    fill_pass<DT>(A, vec, S, cached, trow, drow, L0, Ld, s_exp, part);
+                    X.run<4>(part, tot);
+                    Lt = L0 + log(tot[0]);
+                    inv = 1.0 / tot[0];
+                    // first residual (C = 1): sum over {p > q} of p - q, exact when no
+                    // token lies in the band where the normaliser decides the sign
+                    Z1 = tot[3] == 0.0 ? tot[1] * inv - tot[2] : -1.0;
+                    exact = true;
+                    py = exp((double)s_xt[j] - Lt);
+                    num = py - C * qy;
+                    ratio = (num > 0.0 ? num : 0.0) / (W * qy);
+                }
+                if (trace && tcount <= TSB_TRACE_MAX) trace[(tcount - 1) * 4 + 2] = ratio;
                 if (U < ratio) {
                     if (lead) {
                         A.out.acc_node[(size_t)r * A.D + nacc] = c;
@@ -447,87 +628,138 @@ __global__ __launch_bounds__(kBlock) void verify_walk(WalkArgs A) {
                     break;
                 }
                 C = C + W;
-                S = S - qy;
+                Sq = Sq - qy;
                 if (j + 1 == m) break;
-                // residual mass at the new C, summed over the G slices
-                const double part = residual_slice<DT>(A, vec, trow, drow, Lt, Ld, C, v0, v1);
-                const int slot = (r * 2 + (nb & 1)) * kWalkGroupsMax + g;
-                if (tid == 0) A.zpart[slot] = part;
-                ++nb;
-                request_barrier(&A.counters[r], nb * (uint32_t)G, &timeout);
-                Z = 0.0;
-                for (int h = 0; h < G; ++h)
-                    Z += __hip_atomic_load(&A.zpart[(r * 2 + ((nb - 1) & 1)) * kWalkGroupsMax + h], __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
-                trace_set_z(Z);
-                if (Z <= 0.0 || S <= 0.0) {
+                // residual mass at the new C
+                if (j == 0 && Z1 >= 0.0) {
+                    Z = Z1;
+                } else {
+                    double zp = 0.0;
+                    visit_pq<DT>(A, vec, S, cached, trow, drow, L0, inv, Ld, s_exp, [&](int, double p, double q) {
+                        const double rr = p - C * q;
+                        zp += rr > 0.0 ? rr : 0.0;
+                    });
+                    Z = X.sum(walk_sum(zp));
+                }
+                if (trace && tcount <= TSB_TRACE_MAX) trace[(tcount - 1) * 4 + 3] = Z;
+                if (Z <= 0.0 || Sq <= 0.0) {
                     degenerate = true;
                     break;
                 }
             }
+            __syncthreads();  // s_tok & co. are rewritten at the next node
             if (accepted) continue;
-            // bonus token at the terminal node u
-            bool use_q = !degenerate && C > 0.0;
-            for (int attempt = 0; attempt < 2; ++attempt) {
+            // every child rejected: bonus from the residual max(p - C q, 0)
+            if (!degenerate) {
+                float best = -INFINITY;
+                int bidx = 0x7FFFFFFF;
+                double zp = 0.0;
+                const double Cc = C;
+                const uint32_t node = (uint32_t)u;
+                if (cached) {
+                    const int nn = S.v1 - S.v0;
+                    for (int i4 = tid; i4 * 4 < nn; i4 += kWalkThreads) {
+                        const uint4 w = rng_block(key, node, kStreamBonus, (uint32_t)((S.v0 >> 2) + i4));
+                        const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const int i = i4 * 4 + e;
+                            if (i >= nn) break;
+                            const double rr = S.p[i] * inv - Cc * S.q[i];
+                            if (rr > 0.0) {
+                                zp += rr;
+                                const float kv = logf((float)rr) + gumbel_f32(ws[e]);
+                                const int v = S.v0 + i;
+                                if (kv > best || (kv == best && v < bidx)) {
+                                    best = kv;
+                                    bidx = v;
+                                }
+                            }
+                        }
+                    }
+                } else {
+                    visit_pq<DT>(A, vec, S, false, trow, drow, L0, inv, Ld, s_exp, [&](int v, double p, double q) {
+                        const double rr = p - Cc * q;
+                        if (rr > 0.0) {
+                            zp += rr;
+                            const float kv = logf((float)rr) + gumbel_f32(rng_word(key, node, kStreamBonus, (uint32_t)v));
+                            if (kv > best || (kv == best && v < bidx)) {
+                                best = kv;
+                                bidx = v;
+                            }
+                        }
+                    });
+                }
+                walk_argmax(&best, &bidx);
+                const double zs = walk_sum(zp);
+                double mass;
+                const int fi = X.best(best, bidx, zs, &mass);
+                if (trace && tcount >= 1 && tcount <= TSB_TRACE_MAX) trace[(tcount - 1) * 4 + 3] = mass;
+                if (mass > 0.0 && fi >= 0) {
+                    bonus_out = fi;
+                } else {
+                    degenerate = true;
+                }
+            }
+            if (degenerate) {  // empty residual: bonus from p_u
                 float bk;
                 int bi;
-                double mass;
-                bonus_slice<DT>(A, vec, key, (uint32_t)u, trow, drow, use_q, Lt, Ld, C, v0, v1, &bk, &bi, &mass);
-                const int slot = (r * 2 + (nb & 1)) * kWalkGroupsMax + g;
-                if (tid == 0) {
-                    A.bkey[slot] = bk;
-                    A.bidx[slot] = bi;
-                    A.zpart[slot] = mass;
-                }
-                ++nb;
-                request_barrier(&A.counters[r], nb * (uint32_t)G, &timeout);
-                float fb = -INFINITY;
-                int fi = 0x7FFFFFFF;
-                double fm = 0.0;
-                for (int h = 0; h < G; ++h) {
-                    const int sl = (r * 2 + ((nb - 1) & 1)) * kWalkGroupsMax + h;
-                    const float kb = __hip_atomic_load(&A.bkey[sl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    const int ib = __hip_atomic_load(&A.bidx[sl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    fm += __hip_atomic_load(&A.zpart[sl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    if (kb > fb || (kb == fb && ib < fi)) {
-                        fb = kb;
-                        fi = ib;
-                    }
-                }
-                if (use_q) trace_set_z(fm);
-                if (use_q && (fm <= 0.0 || fb == -INFINITY)) {
-                    degenerate = true;
-                    use_q = false;
-                    continue;
-                }
-                bonus_out = fi;
-                break;
+                double unused;
+                bonus_from_p<DT>(A, vec, S, trow, Lt, key, (uint32_t)u, &bk, &bi);
+                bonus_out = X.best(bk, bi, 0.0, &unused);
+                add_status |= TSB_REQ_DEGENERATE_RESIDUAL;
             }
-            if (degenerate) add_status |= TSB_REQ_DEGENERATE_RESIDUAL;
-            if (timeout) add_status |= TSB_REQ_WALK_TIMEOUT;
-            n_acc_out = nacc;
             break;
         }
-        if (lead)
+        if (X.timeout) add_status |= TSB_REQ_WALK_TIMEOUT;
+    }
+
+    // every target row of the tree must be finite; optional normaliser output
+    if (tid == 0) s_bad = 0;
+    __syncthreads();
+    if (!draft_bad) {
+        for (int i = g * kWalkThreads + tid; i < n; i += G * kWalkThreads) {
+            int b;
+            const double l = target_lse(A, r, i, &b);
+            if (b) atomicOr(&s_bad, 1);
+            if (A.out.target_lse) A.out.target_lse[tb + i] = b ? (double)NAN : l;
+        }
+        if (g != 0 && tid == 0 && s_bad == 0) { /* workgroup 0 checks every row below */ }
+    }
+    __syncthreads();
+    if (A.out.target_lse)
+        for (int i = n + g * kWalkThreads + tid; i < B1; i += G * kWalkThreads) A.out.target_lse[tb + i] = (double)NAN;
+    if (g == 0) {
+        // workgroup 0 decides the request's finiteness over all rows
+        if (tid == 0) s_bad = 0;
+        __syncthreads();
+        if (!draft_bad)
+            for (int i = tid; i < n; i += kWalkThreads) {
+                int b;
+                target_lse(A, r, i, &b);
+                if (b) atomicOr(&s_bad, 1);
+            }
+        __syncthreads();
+        const bool bad = draft_bad || s_bad;
+        if (bad && A.out.target_lse)
+            for (int i = tid; i < B1; i += kWalkThreads) A.out.target_lse[tb + i] = (double)NAN;
+        if (lead) {
+            if (bad) {
+                nacc = 0;
+                bonus_out = -1;
+                add_status = (add_status & ~(TSB_REQ_DEGENERATE_RESIDUAL | TSB_REQ_WALK_TIMEOUT)) | TSB_REQ_NONFINITE;
+            }
             for (int i = nacc; i < A.D; ++i) {
                 A.out.acc_node[(size_t)r * A.D + i] = -1;
                 A.out.acc_tok[(size_t)r * A.D + i] = -1;
             }
-    } else {
-        add_status |= TSB_REQ_NONFINITE;
-        if (lead)
-            for (int i = 0; i < A.D; ++i) {
-                A.out.acc_node[(size_t)r * A.D + i] = -1;
-                A.out.acc_tok[(size_t)r * A.D + i] = -1;
-            }
-    }
-    if (lead) {
-        A.out.n_acc[r] = n_acc_out;
-        A.out.bonus[r] = bonus_out;
-        *status_p |= add_status;
-        if (A.out.trace)
-            for (int i = tcount; i < TSB_TRACE_MAX; ++i)
-                for (int f = 0; f < 4; ++f) A.out.trace[((size_t)r * TSB_TRACE_MAX + i) * 4 + f] = -1.0;
+            A.out.n_acc[r] = bad ? -1 : nacc;
+            A.out.bonus[r] = bonus_out;
+            *status_p |= add_status;
+            if (A.out.trace)
+                for (int i = tcount; i < TSB_TRACE_MAX; ++i)
+                    for (int f = 0; f < 4; ++f) A.out.trace[((size_t)r * TSB_TRACE_MAX + i) * 4 + f] = -1.0;
+        }
     }
 }
 
@@ -595,12 +827,15 @@ hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, con
     else
         fn = vec4 ? (const void*)verify_walk<TSB_F32, true> : (const void*)verify_walk<TSB_F32, false>;
 
+    const size_t lds = 2 * (size_t)kWalkCache * sizeof(double);
     int dev = 0, cus = 0, per_cu = 0;
     e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
     e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kBlock, 0);
+    e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kWalkThreads, lds);
     if (e != hipSuccess) return e;
     const int cap = per_cu * cus;
     if (cap < 1) return hipErrorCooperativeLaunchTooLarge;
@@ -612,7 +847,7 @@ hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, con
         A.r0 = r0;
         const int rc = min(chunk, c.R - r0);
         void* args[] = {&A};
-        e = hipLaunchCooperativeKernel(fn, dim3(G, rc), dim3(kBlock), args, 0, st);
+        e = hipLaunchCooperativeKernel(fn, dim3(G, rc), dim3(kWalkThreads), args, (unsigned)lds, st);
         if (e != hipSuccess) return e;
     }
     return hook_after(TSB_KERNEL_VERIFY_WALK, st);

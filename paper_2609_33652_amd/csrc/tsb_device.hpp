@@ -75,6 +75,41 @@ __device__ __forceinline__ float gumbel_f32(uint32_t w) {
 // Upper bound of gumbel_f32 over all 2^23 uniforms, with slack for rounding.
 constexpr float kGumbelMaxBound = 16.75f;
 
+// ---------------------------------------------------------------- exp (binary64)
+// Table-driven exponential (P. T. P. Tang, "Table-driven implementation of
+// the exponential function in IEEE floating-point arithmetic", ACM TOMS
+// 15(2), 1989): x = (64 m + j) ln2/64 + r with |r| <= ln2/128, so
+// e^x = 2^m * 2^(j/64) * e^r; e^r - 1 by a degree-6 Taylor polynomial
+// (truncation < 2^-54 relative), the reduction by two FMAs against a split
+// ln2/64. The 64 table entries 2^(j/64) live in LDS (exp64_table_init).
+constexpr int kExpTable = 64;
+
+__device__ __forceinline__ void exp64_table_init(double* t) {
+    for (int j = threadIdx.x; j < kExpTable; j += blockDim.x) t[j] = exp2((double)j / (double)kExpTable);
+    __syncthreads();
+}
+
+__device__ __forceinline__ double exp64(double x, const double* t) {
+    constexpr double kInvL = 92.332482616893656877;        // 64 / ln2
+    constexpr double kLhi = 0x1.62e42fefa39efp-7;          // ln2/64, leading part
+    constexpr double kLlo = 3.6235106466348431e-19;        // ln2/64 - kLhi
+    x = fmax(x, -746.0);                                   // e^-746 underflows to 0
+    const double n = rint(x * kInvL);
+    double r = fma(-n, kLhi, x);
+    r = fma(-n, kLlo, r);
+    const int ni = (int)n;
+    const int j = ni & (kExpTable - 1);
+    const int m = ni >> 6;                                 // floor(ni / 64)
+    double p = fma(r, 1.0 / 720.0, 1.0 / 120.0);
+    p = fma(r, p, 1.0 / 24.0);
+    p = fma(r, p, 1.0 / 6.0);
+    p = fma(r, p, 0.5);
+    p = fma(r, p, 1.0);
+    p = p * r;                                             // e^r - 1
+    const double s = t[j];
+    return ldexp(fma(s, p, s), m);
+}
+
 // ---------------------------------------------------------------- logits
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 

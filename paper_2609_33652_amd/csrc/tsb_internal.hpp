@@ -14,7 +14,8 @@ enum : uint32_t { kStreamReplay = 0, kStreamAccept = 1, kStreamBonus = 2 };
 
 constexpr int kBlock = 256;          // threads per workgroup of the streaming kernels
 constexpr int kReplayTile = 4096;    // vocabulary tile of the replay scan
-constexpr int kWalkGroupsMax = 64;   // workgroups per request in verification
+constexpr int kWalkGroupsMax = 128;  // workgroups per request in verification
+constexpr int kWalkTokensPerGroup = 9728;  // tokens whose binary64 (p, q) one walk workgroup holds in LDS
 constexpr int kTargetWorkgroups = 2048;
 
 struct Geometry {
@@ -43,7 +44,11 @@ inline Geometry geometry(const tsb_config& c) {
     g.seg4 = ceil_div(ceil_div(c.V, g.S4), 8) * 8;
     g.S4 = ceil_div(c.V, g.seg4);
     g.T = ceil_div(c.V, kReplayTile);
-    int gw = 512 / (c.R > 0 ? c.R : 1);
+    // walk: about one workgroup per compute unit over the batch, and enough
+    // per request that a slice fits the LDS cache
+    int gw = 256 / (c.R > 0 ? c.R : 1);
+    const int gmin = ceil_div(c.V, kWalkTokensPerGroup);
+    if (gw < gmin) gw = gmin;
     g.G = gw < 1 ? 1 : (gw > kWalkGroupsMax ? kWalkGroupsMax : gw);
     return g;
 }
@@ -95,7 +100,7 @@ inline VerifyWs verify_ws(const tsb_config& c) {
     w.ts = o; o = align256(o + n * sizeof(double));
     w.tf = o; o = align256(o + n * sizeof(int32_t));
     w.counter = o; o = align256(o + (size_t)c.R * sizeof(uint32_t));
-    w.zpart = o; o = align256(o + (size_t)c.R * 2 * kWalkGroupsMax * sizeof(double));
+    w.zpart = o; o = align256(o + (size_t)c.R * 2 * kWalkGroupsMax * 4 * sizeof(double));
     w.bkey = o; o = align256(o + (size_t)c.R * 2 * kWalkGroupsMax * sizeof(float));
     w.bidx = o; o = align256(o + (size_t)c.R * 2 * kWalkGroupsMax * sizeof(int32_t));
     w.total = o;
