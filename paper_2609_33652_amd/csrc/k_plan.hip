@@ -174,6 +174,22 @@ __global__ __launch_bounds__(kWave) void draft_merge(int D, int S, int K, float 
 }
 
 // ------------------------------------------------------------------ K2
+// Frontier of the lazy best-first expansion, one wave per request. The best
+// (up to) 64 frontier entries are kept sorted across the lanes of the wave
+// (lane i holds the i-th best), so a pop is lane 0 and a whole-wave one-lane
+// DPP shift, and a push is a ballot for its position and a one-lane shift.
+// Entries that fall off the end go to a "cold" list in LDS; every cold entry
+// ranks after every hot entry (a push that ranks after the best cold entry
+// goes to the cold list too), so the hot head is always the global best.
+// When the hot list runs empty, the best cold entries are moved back.
+//
+// Entry: score (binary64); info = depth << 16 | rank << 10 | parent (pop
+// index of the committed parent, root = 0); the parent's score; and the two
+// planning log-probabilities the entry needs once popped (its first child's
+// and its next sibling's), so a pop reads no memory.
+constexpr int kInfoParentBits = 10;
+constexpr int kInfoRankBits = 6;
+
 struct PlanShared {
     float lp[TSB_MAX_D * TSB_MAX_K];
     double c_score[TSB_MAX_B + 1];
@@ -183,10 +199,9 @@ struct PlanShared {
     union {
         struct {
             double score[TSB_MAX_B + 2];
-            int parent[TSB_MAX_B + 2];
-            int rank[TSB_MAX_B + 2];
-            int depth[TSB_MAX_B + 2];
-        } f;  // frontier
+            double pscore[TSB_MAX_B + 2];
+            uint32_t info[TSB_MAX_B + 2];
+        } cold;
         struct {
             int order[TSB_MAX_B + 1];
             int bfs_of[TSB_MAX_B + 1];
@@ -196,21 +211,125 @@ struct PlanShared {
     } u;
 };
 
-// Frontier order: score desc, depth asc, rank path lexicographic asc.
-__device__ __forceinline__ bool plan_better(const PlanShared& sh, int i, int j) {
-    const double si = sh.u.f.score[i], sj = sh.u.f.score[j];
-    if (si != sj) return si > sj;
-    const int di = sh.u.f.depth[i], dj = sh.u.f.depth[j];
-    if (di != dj) return di < dj;
-    int pa = sh.u.f.parent[i], pb = sh.u.f.parent[j];
-    int ra = sh.u.f.rank[i], rb = sh.u.f.rank[j];
-    while (pa != pb) {  // equal depth: walk up to the common ancestor
+__device__ __forceinline__ int info_depth(uint32_t i) { return (int)(i >> 16); }
+__device__ __forceinline__ int info_rank(uint32_t i) { return (int)((i >> kInfoParentBits) & ((1u << kInfoRankBits) - 1)); }
+__device__ __forceinline__ int info_parent(uint32_t i) { return (int)(i & ((1u << kInfoParentBits) - 1)); }
+__device__ __forceinline__ uint32_t make_info(int depth, int rank, int parent) {
+    return ((uint32_t)depth << 16) | ((uint32_t)rank << kInfoParentBits) | (uint32_t)parent;
+}
+
+// Static order of frontier entries: score desc, depth asc, rank path
+// lexicographic asc (equal depth: walk both parents up to their common
+// ancestor and compare the ranks just below it). True if a precedes b.
+__device__ __forceinline__ bool plan_precedes(const PlanShared& sh, double sa, uint32_t ia, double sb, uint32_t ib) {
+    if (sa != sb) return sa > sb;
+    const int da = info_depth(ia), db = info_depth(ib);
+    if (da != db) return da < db;
+    int pa = info_parent(ia), pb = info_parent(ib);
+    int ra = info_rank(ia), rb = info_rank(ib);
+    for (int guard = 0; pa != pb && guard < TSB_MAX_D; ++guard) {
         ra = sh.c_rank[pa];
         rb = sh.c_rank[pb];
         pa = sh.c_parent[pa];
         pb = sh.c_parent[pb];
     }
     return ra < rb;
+}
+
+// Whole-wave one-lane shifts (lane i gets lane i-1 / i+1; the edge lane keeps its value).
+__device__ __forceinline__ uint32_t wave_shr1(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x138, 0xf, 0xf, false);
+}
+__device__ __forceinline__ uint32_t wave_shl1(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x130, 0xf, 0xf, false);
+}
+__device__ __forceinline__ double wave_shr1(double v) {
+    const uint64_t b = __double_as_longlong(v);
+    return __longlong_as_double((long long)(((uint64_t)wave_shr1((uint32_t)(b >> 32)) << 32) | wave_shr1((uint32_t)b)));
+}
+__device__ __forceinline__ double wave_shl1(double v) {
+    const uint64_t b = __double_as_longlong(v);
+    return __longlong_as_double((long long)(((uint64_t)wave_shl1((uint32_t)(b >> 32)) << 32) | wave_shl1((uint32_t)b)));
+}
+__device__ __forceinline__ uint32_t lane_u32(uint32_t v, int l) { return (uint32_t)__builtin_amdgcn_readlane((int)v, l); }
+__device__ __forceinline__ float lane_f32(float v, int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l)); }
+__device__ __forceinline__ double lane_f64(double v, int l) {
+    const uint64_t b = __double_as_longlong(v);
+    return __longlong_as_double((long long)(((uint64_t)lane_u32((uint32_t)(b >> 32), l) << 32) | lane_u32((uint32_t)b, l)));
+}
+
+struct Entry {
+    double s, ps;   // score, parent's score
+    uint32_t i;     // info
+    float lc, lsib; // first child's lp (NaN: none), next sibling's lp (NaN: none)
+};
+
+__device__ __forceinline__ Entry shr1(const Entry& e) {
+    return Entry{wave_shr1(e.s), wave_shr1(e.ps), wave_shr1(e.i), __uint_as_float(wave_shr1(__float_as_uint(e.lc))),
+                 __uint_as_float(wave_shr1(__float_as_uint(e.lsib)))};
+}
+__device__ __forceinline__ Entry shl1(const Entry& e) {
+    return Entry{wave_shl1(e.s), wave_shl1(e.ps), wave_shl1(e.i), __uint_as_float(wave_shl1(__float_as_uint(e.lc))),
+                 __uint_as_float(wave_shl1(__float_as_uint(e.lsib)))};
+}
+__device__ __forceinline__ Entry lane_entry(const Entry& e, int l) {
+    return Entry{lane_f64(e.s, l), lane_f64(e.ps, l), lane_u32(e.i, l), lane_f32(e.lc, l), lane_f32(e.lsib, l)};
+}
+
+// lp values a new entry (depth dep, rank rk) will need once popped
+__device__ __forceinline__ Entry make_entry(const PlanShared& sh, int Dp, int K, double s, double ps, int dep, int rk,
+                                            int par) {
+    Entry e;
+    e.s = s;
+    e.ps = ps;
+    e.i = make_info(dep, rk, par);
+    e.lc = dep < Dp ? sh.lp[dep * K + 0] : (float)NAN;
+    e.lsib = rk + 1 < K ? sh.lp[(dep - 1) * K + rk + 1] : (float)NAN;
+    return e;
+}
+
+struct Frontier {
+    Entry h;  // this lane's hot entry
+    int nh, ncold;
+    double cold_s;  // best cold entry (valid when ncold > 0)
+    uint32_t cold_i;
+};
+
+__device__ __forceinline__ void frontier_to_cold(PlanShared& sh, Frontier& F, const Entry& e) {
+    if (lane_id() == 0) {
+        sh.u.cold.score[F.ncold] = e.s;
+        sh.u.cold.pscore[F.ncold] = e.ps;
+        sh.u.cold.info[F.ncold] = e.i;
+    }
+    if (F.ncold == 0 || plan_precedes(sh, e.s, e.i, F.cold_s, F.cold_i)) {
+        F.cold_s = e.s;
+        F.cold_i = e.i;
+    }
+    ++F.ncold;
+}
+
+__device__ __forceinline__ void frontier_push(PlanShared& sh, Frontier& F, const Entry& e) {
+    // entries ranking after the best cold entry stay cold (invariant)
+    if (F.ncold > 0 && !plan_precedes(sh, e.s, e.i, F.cold_s, F.cold_i)) {
+        frontier_to_cold(sh, F, e);
+        return;
+    }
+    const int lane = lane_id();
+    const bool before = lane < F.nh && plan_precedes(sh, F.h.s, F.h.i, e.s, e.i);
+    const int pos = __popcll(__ballot(before));
+    if (F.nh == kWave) {  // the entry that leaves: the old tail, or e if it ranks last
+        if (pos == kWave) {
+            frontier_to_cold(sh, F, e);
+            return;
+        }
+        frontier_to_cold(sh, F, lane_entry(F.h, kWave - 1));
+    }
+    const Entry up = shr1(F.h);
+    if (lane == pos)
+        F.h = e;
+    else if (lane > pos)
+        F.h = up;
+    if (F.nh < kWave) ++F.nh;
 }
 
 __global__ __launch_bounds__(kWave) void plan_tree(int D, int K, int B, const float* __restrict__ topk_lp,
@@ -230,73 +349,114 @@ __global__ __launch_bounds__(kWave) void plan_tree(int D, int K, int B, const fl
     }
     __syncthreads();
 
-    int nf = 0;
-    if (Dp > 0 && isfinite(sh.lp[0])) {
-        if (lane == 0) {
-            sh.u.f.score[0] = 0.0 + (double)sh.lp[0];
-            sh.u.f.parent[0] = 0;
-            sh.u.f.rank[0] = 0;
-            sh.u.f.depth[0] = 1;
-        }
-        nf = 1;
-    }
-    int committed = 1;
-    __syncthreads();
+    Frontier F;
+    F.h.s = -INFINITY;
+    F.h.ps = 0.0;
+    F.h.i = 0;
+    F.h.lc = F.h.lsib = (float)NAN;
+    F.nh = 0;
+    F.ncold = 0;
+    F.cold_s = -INFINITY;
+    F.cold_i = 0;
 
-    while (committed <= B && nf > 0) {
-        int best = -1;
-        for (int i = lane; i < nf; i += kWave)
-            if (best < 0 || plan_better(sh, i, best)) best = i;
+    if (Dp > 0 && isfinite(sh.lp[0])) frontier_push(sh, F, make_entry(sh, Dp, K, 0.0 + (double)sh.lp[0], 0.0, 1, 0, 0));
+    int committed = 1;
+
+    while (committed <= B && (F.nh > 0 || F.ncold > 0)) {
+        if (F.nh == 0) {
+            // refill: move the best cold entries back, best first
+            __syncthreads();
+            const int take = F.ncold < kWave ? F.ncold : kWave;
+            for (int t = 0; t < take; ++t) {
+                double bs = -INFINITY;
+                uint32_t bi = 0;
+                int bj = -1;
+                for (int j = lane; j < F.ncold; j += kWave) {
+                    const double cs = sh.u.cold.score[j];
+                    const uint32_t ci = sh.u.cold.info[j];
+                    if (bj < 0 || plan_precedes(sh, cs, ci, bs, bi)) {
+                        bs = cs;
+                        bi = ci;
+                        bj = j;
+                    }
+                }
 #pragma unroll
-        for (int o = 32; o > 0; o >>= 1) {
-            const int other = __shfl_xor(best, o, kWave);
-            if (other >= 0 && (best < 0 || plan_better(sh, other, best))) best = other;
+                for (int o = 32; o > 0; o >>= 1) {
+                    const double os = __shfl_xor(bs, o, kWave);
+                    const uint32_t oi = (uint32_t)__shfl_xor((int)bi, o, kWave);
+                    const int oj = __shfl_xor(bj, o, kWave);
+                    if (oj >= 0 && (bj < 0 || plan_precedes(sh, os, oi, bs, bi))) {
+                        bs = os;
+                        bi = oi;
+                        bj = oj;
+                    }
+                }
+                const double bps = sh.u.cold.pscore[bj];
+                if (lane == t) F.h = make_entry(sh, Dp, K, bs, bps, info_depth(bi), info_rank(bi), info_parent(bi));
+                __syncthreads();
+                if (lane == 0) {
+                    sh.u.cold.score[bj] = sh.u.cold.score[F.ncold - 1];
+                    sh.u.cold.pscore[bj] = sh.u.cold.pscore[F.ncold - 1];
+                    sh.u.cold.info[bj] = sh.u.cold.info[F.ncold - 1];
+                }
+                --F.ncold;
+                __syncthreads();
+            }
+            F.nh = take;
+            // best remaining cold entry
+            if (F.ncold > 0) {
+                double bs = -INFINITY;
+                uint32_t bi = 0;
+                int bj = -1;
+                for (int j = lane; j < F.ncold; j += kWave) {
+                    const double cs = sh.u.cold.score[j];
+                    const uint32_t ci = sh.u.cold.info[j];
+                    if (bj < 0 || plan_precedes(sh, cs, ci, bs, bi)) {
+                        bs = cs;
+                        bi = ci;
+                        bj = j;
+                    }
+                }
+#pragma unroll
+                for (int o = 32; o > 0; o >>= 1) {
+                    const double os = __shfl_xor(bs, o, kWave);
+                    const uint32_t oi = (uint32_t)__shfl_xor((int)bi, o, kWave);
+                    const int oj = __shfl_xor(bj, o, kWave);
+                    if (oj >= 0 && (bj < 0 || plan_precedes(sh, os, oi, bs, bi))) {
+                        bs = os;
+                        bi = oi;
+                        bj = oj;
+                    }
+                }
+                F.cold_s = bs;
+                F.cold_i = bi;
+            }
         }
-        const int w = best;
-        const double s = sh.u.f.score[w];
-        const int par = sh.u.f.parent[w], rk = sh.u.f.rank[w], dep = sh.u.f.depth[w];
+        // pop the head
+        const Entry top = lane_entry(F.h, 0);
+        {
+            const Entry dn = shl1(F.h);
+            if (lane < F.nh - 1) F.h = dn;
+            --F.nh;
+        }
+        const int dep = info_depth(top.i), rk = info_rank(top.i), par = info_parent(top.i);
         const int c = committed++;
-        const bool child = dep < Dp && isfinite(sh.lp[dep * K + 0]);
-        const bool sib = rk + 1 < K && isfinite(sh.lp[(dep - 1) * K + rk + 1]);
-        __syncthreads();
-        if (lane == 0) {
+        if (lane == 0) {  // single wave: later LDS reads see these writes in order
             sh.c_parent[c] = par;
             sh.c_rank[c] = rk;
             sh.c_depth[c] = dep;
-            sh.c_score[c] = s;
-            int slot_free = 1;
-            if (child) {
-                sh.u.f.score[w] = s + (double)sh.lp[dep * K + 0];
-                sh.u.f.parent[w] = c;
-                sh.u.f.rank[w] = 0;
-                sh.u.f.depth[w] = dep + 1;
-                slot_free = 0;
-            }
-            if (sib) {
-                const int slot = slot_free ? w : nf;
-                sh.u.f.score[slot] = sh.c_score[par] + (double)sh.lp[(dep - 1) * K + rk + 1];
-                sh.u.f.parent[slot] = par;
-                sh.u.f.rank[slot] = rk + 1;
-                sh.u.f.depth[slot] = dep;
-                slot_free = 0;
-            }
-            if (slot_free && w != nf - 1) {
-                sh.u.f.score[w] = sh.u.f.score[nf - 1];
-                sh.u.f.parent[w] = sh.u.f.parent[nf - 1];
-                sh.u.f.rank[w] = sh.u.f.rank[nf - 1];
-                sh.u.f.depth[w] = sh.u.f.depth[nf - 1];
-            }
+            sh.c_score[c] = top.s;
         }
-        nf += (child && sib) ? 1 : ((!child && !sib) ? -1 : 0);
-        __syncthreads();
+        if (!isnan(top.lc) && isfinite(top.lc))
+            frontier_push(sh, F, make_entry(sh, Dp, K, top.s + (double)top.lc, top.s, dep + 1, 0, c));
+        if (!isnan(top.lsib) && isfinite(top.lsib))
+            frontier_push(sh, F, make_entry(sh, Dp, K, top.ps + (double)top.lsib, top.ps, dep, rk + 1, par));
     }
+    __syncthreads();
+    const int nf = F.nh + F.ncold;
+    // best uncommitted: the hot head (the cold list ranks after it), else the best cold entry
+    const double bestf = F.nh > 0 ? lane_f64(F.h.s, 0) : F.cold_s;
     const int n = committed;
-
-    // margin against the best uncommitted frontier node
-    double bestf = -INFINITY;
-    for (int i = lane; i < nf; i += kWave) bestf = fmax(bestf, sh.u.f.score[i]);
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) bestf = fmax(bestf, __shfl_xor(bestf, o, kWave));
     const double margin = (nf > 0 && n > 1) ? sh.c_score[n - 1] - bestf : (double)INFINITY;
     __syncthreads();
 

@@ -3,9 +3,13 @@
 // m_u largest Gumbel keys a_{d,v} + G(u, v) over the whole vocabulary
 // (Gumbel-top-k = ordered sampling without replacement).
 //
-//   replay_scan   grid (vocabulary tile, request x depth). One read of the
-//                 tile of draft row d serves every parent at depth d (they
-//                 share q_d). Per parent, tokens whose key cannot reach the
+//   replay_prep   one workgroup: flat list of the parents of the batch
+//                 (request-major, BFS order, so a depth's parents are
+//                 contiguous).
+//   replay_scan   grid (vocabulary tile, 64 rows); a row takes a contiguous
+//                 chunk of the parent list and stages the tile of draft row d
+//                 once for consecutive parents of the same (request, depth)
+//                 (they share q_d). Per parent, tokens whose key cannot reach the
 //                 parent's threshold (a lower bound of its m-th key, taken
 //                 from its planning candidates) are skipped before any
 //                 random number is drawn; the survivors are compacted per
@@ -25,127 +29,174 @@
 namespace tsb {
 
 constexpr int kTileGroups = kReplayTile / 4;  // groups of four tokens per tile
+constexpr int kTileOut = kReplayTileOut;       // candidates a (parent, tile) may hand to the merge
 
 struct ReplayShared {
     float b[kReplayTile];                         // fl32(a_v - c_d) of the tile
     int queue[kBlock / kWave][kTileGroups / (kBlock / kWave)];
     float ckey[kReplayTile];                      // candidates of the current parent
     int cidx[kReplayTile];
-    int parents[TSB_MAX_B + 1];
     int ccount;
-    int nparents;
-    int lo, hi;
     float thr;
-    float sel_key;
-    int sel_idx;
 };
+
+constexpr int kPrepThreads = 1024;
+constexpr int kScanRows = 256;  // workgroup rows of the scan grid (each takes a chunk of parents)
+
+// Flat list of every node with children, request-major, BFS order within a
+// request (so parents of one (request, depth) are contiguous): plist[i] =
+// r * (B + 1) + u; ptotal[0] = list length.
+__global__ __launch_bounds__(kPrepThreads) void replay_prep(int R, int B, tsb_tree tree, int* __restrict__ plist,
+                                                            int* __restrict__ ptotal) {
+    __shared__ int s_wave[kPrepThreads / kWave];
+    __shared__ int s_base;
+    const int tid = threadIdx.x;
+    const int lane = tid % kWave, wave = tid / kWave;
+    if (tid == 0) s_base = 0;
+    __syncthreads();
+    const int total_nodes = R * (B + 1);
+    for (int base = 0; base < total_nodes; base += kPrepThreads) {
+        const int i = base + tid;
+        int flag = 0;
+        if (i < total_nodes) {
+            const int r = i / (B + 1), u = i % (B + 1);
+            flag = (u < tree.n_nodes[r] && tree.n_children[i] > 0) ? 1 : 0;
+        }
+        const uint64_t bal = __ballot(flag);
+        const int before = __popcll(bal & ((1ull << lane) - 1ull));
+        if (lane == 0) s_wave[wave] = __popcll(bal);
+        __syncthreads();
+        int off = s_base;
+        for (int w = 0; w < wave; ++w) off += s_wave[w];
+        if (flag) plist[off + before] = i;
+        __syncthreads();
+        if (tid == 0) {
+            int t = 0;
+            for (int w = 0; w < kPrepThreads / kWave; ++w) t += s_wave[w];
+            s_base += t;
+        }
+        __syncthreads();
+    }
+    if (tid == 0) ptotal[0] = s_base;
+}
 
 __device__ __forceinline__ bool key_better(float ka, int ia, float kb, int ib) {
     return ka > kb || (ka == kb && ia < ib);
 }
 
-template <int DT, bool VEC>
-__global__ __launch_bounds__(kBlock) void replay_scan(const void* __restrict__ draft, int V, int D, int B, int K,
-                                                      int T, float invT, const int32_t* __restrict__ topk_tok,
-                                                      tsb_tree tree, uint32_t k0, uint32_t k1, uint32_t step,
-                                                      int prune, float* __restrict__ out_key,
-                                                      int* __restrict__ out_idx, int* __restrict__ out_cnt) {
-    __shared__ ReplayShared sh;
-    const int t = blockIdx.x;
-    const int r = blockIdx.y / D;
-    const int d = blockIdx.y % D;
-    const int tid = threadIdx.x;
-    const int wave = tid / kWave, lane = tid % kWave;
-    const size_t tb = (size_t)r * (B + 1);
-    const int n = tree.n_nodes[r];
-
-    // parents at depth d: contiguous BFS range with depth == d, having children
-    if (tid == 0) {
-        sh.lo = n;
-        sh.hi = 0;
-        sh.nparents = 0;
-    }
-    __syncthreads();
-    for (int i = tid; i < n; i += kBlock) {
-        const int di = tree.depth[tb + i];
-        if (di == d) {
-            atomicMin(&sh.lo, i);
-            atomicMax(&sh.hi, i + 1);
-        }
-    }
-    __syncthreads();
-    if (tid == 0) {
-        int np = 0;
-        for (int i = sh.lo; i < sh.hi; ++i)
-            if (tree.n_children[tb + i] > 0) sh.parents[np++] = i;
-        sh.nparents = np;
-    }
-    __syncthreads();
-    const int P = sh.nparents;
-    if (P == 0) return;
-
+// Per parent u (one wave each): the m_u-th largest key among the keys of
+// its planning candidates, a lower bound of its m_u-th largest key over the
+// vocabulary (the same key arithmetic as the scan). -inf without pruning.
+template <int DT>
+__global__ __launch_bounds__(kBlock) void replay_threshold(const void* __restrict__ draft, int R, int V, int D, int B,
+                                                           int K, float invT, const int32_t* __restrict__ topk_tok,
+                                                           tsb_tree tree, uint32_t k0, uint32_t k1, uint32_t step,
+                                                           int prune, float* __restrict__ thr) {
+    const int lane = threadIdx.x % kWave;
+    const int node = blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
+    if (node >= R * (B + 1)) return;
+    const int r = node / (B + 1), u = node % (B + 1);
+    if (u >= tree.n_nodes[r]) return;
+    const int m = tree.n_children[node];
+    if (m == 0) return;
+    const int d = tree.depth[node];
     const size_t rowbase = ((size_t)r * D + d) * (size_t)V;
-    const int tok0 = topk_tok[((size_t)r * D + d) * K];
-    const float cd = load_logit<DT>(draft, rowbase + tok0) * invT;
-    const int t0 = t * kReplayTile;
-    const int tn = min(kReplayTile, V - t0);
-
-    // stage b_v = fl32(a_v - c_d) for the tile
-    for (int g = tid; g < kTileGroups; g += kBlock) {
-        const int e0 = g * 4;
-        float x[4];
-        if (VEC && e0 + 4 <= tn) {
-            if (DT == TSB_BF16) {
-                const uint2 raw = *(const uint2*)((const uint16_t*)draft + rowbase + t0 + e0);
-                x[0] = __uint_as_float(raw.x << 16);
-                x[1] = __uint_as_float(raw.x & 0xFFFF0000u);
-                x[2] = __uint_as_float(raw.y << 16);
-                x[3] = __uint_as_float(raw.y & 0xFFFF0000u);
-            } else {
-                const float4 a = *(const float4*)((const float*)draft + rowbase + t0 + e0);
-                x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
-            }
-        } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) x[e] = (e0 + e < tn) ? load_logit<DT>(draft, rowbase + t0 + e0 + e) : -INFINITY;
-        }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const float a = x[e] * invT;
-            sh.b[e0 + e] = (e0 + e < tn) ? a - cd : -INFINITY;
-        }
-    }
-    __syncthreads();
-
+    const int32_t* tk = topk_tok + ((size_t)r * D + d) * K;
+    const float cd = load_logit<DT>(draft, rowbase + tk[0]) * invT;
     RngKey key;
     key.k0 = k0;
     key.k1 = k1;
     key.request = (uint32_t)r;
     key.step = step;
-    const uint32_t blk0 = (uint32_t)(t0 >> 2);
+    float kj = -INFINITY;
+    int tj = 0x7FFFFFFF;
+    if (lane < K) {
+        tj = tk[lane];
+        const float a = load_logit<DT>(draft, rowbase + tj) * invT;
+        const float bj = a - cd;
+        kj = bj + gumbel_f32(rng_word(key, (uint32_t)u, kStreamReplay, (uint32_t)tj));
+    }
+    int above = 0;
+    for (int j = 0; j < K; ++j) {
+        const float kk = __shfl(kj, j, kWave);
+        const int tt = __shfl(tj, j, kWave);
+        above += key_better(kk, tt, kj, tj) ? 1 : 0;
+    }
+    if (lane < K && above == m - 1) thr[node] = prune ? kj : -INFINITY;
+}
 
-    for (int p = 0; p < P; ++p) {
-        const int u = sh.parents[p];
+template <int DT, bool VEC>
+__global__ __launch_bounds__(kBlock) void replay_scan(const void* __restrict__ draft, int V, int D, int B, int K,
+                                                      int T, float invT, const int32_t* __restrict__ topk_tok,
+                                                      tsb_tree tree, const int* __restrict__ plist,
+                                                      const int* __restrict__ ptotal, const float* __restrict__ thr_in,
+                                                      uint32_t k0, uint32_t k1, uint32_t step,
+                                                      float* __restrict__ out_key, int* __restrict__ out_idx,
+                                                      int* __restrict__ out_cnt) {
+    __shared__ ReplayShared sh;
+    const int t = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int wave = tid / kWave, lane = tid % kWave;
+    const int total = ptotal[0];
+    const int chunk = (total + kScanRows - 1) / kScanRows;
+    const int p0 = blockIdx.y * chunk;
+    const int p1 = min(total, p0 + chunk);
+    if (p0 >= p1) return;
+    const int t0 = t * kReplayTile;
+    const int tn = min(kReplayTile, V - t0);
+    const uint32_t blk0 = (uint32_t)(t0 >> 2);
+    int staged = -1;  // r * D + d of the staged tile
+
+    for (int pi = p0; pi < p1; ++pi) {
+        const int node = plist[pi];
+        const int r = node / (B + 1);
+        const int u = node % (B + 1);
+        const size_t tb = (size_t)r * (B + 1);
+        const int d = tree.depth[tb + u];
         const int m = tree.n_children[tb + u];
-        // threshold: m-th largest key among the planning candidates (a lower
-        // bound of the m-th largest key over the vocabulary)
-        if (wave == 0) {
-            float kj = -INFINITY;
-            int tj = 0x7FFFFFFF;
-            if (lane < K) {
-                tj = topk_tok[((size_t)r * D + d) * K + lane];
-                const float a = load_logit<DT>(draft, rowbase + tj) * invT;
-                const float bj = a - cd;
-                kj = bj + gumbel_f32(rng_word(key, (uint32_t)u, kStreamReplay, (uint32_t)tj));
+        const size_t rowbase = ((size_t)r * D + d) * (size_t)V;
+        const int tok0 = topk_tok[((size_t)r * D + d) * K];
+        const float cd = load_logit<DT>(draft, rowbase + tok0) * invT;
+        if (staged != r * D + d) {
+            // stage b_v = fl32(a_v - c_d) for the tile
+            __syncthreads();
+            for (int g = tid; g < kTileGroups; g += kBlock) {
+                const int e0 = g * 4;
+                float x[4];
+                if (VEC && e0 + 4 <= tn) {
+                    if (DT == TSB_BF16) {
+                        const uint2 raw = *(const uint2*)((const uint16_t*)draft + rowbase + t0 + e0);
+                        x[0] = __uint_as_float(raw.x << 16);
+                        x[1] = __uint_as_float(raw.x & 0xFFFF0000u);
+                        x[2] = __uint_as_float(raw.y << 16);
+                        x[3] = __uint_as_float(raw.y & 0xFFFF0000u);
+                    } else {
+                        const float4 a = *(const float4*)((const float*)draft + rowbase + t0 + e0);
+                        x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+                    }
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        x[e] = (e0 + e < tn) ? load_logit<DT>(draft, rowbase + t0 + e0 + e) : -INFINITY;
+                }
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float a = x[e] * invT;
+                    sh.b[e0 + e] = (e0 + e < tn) ? a - cd : -INFINITY;
+                }
             }
-            int above = 0;
-            for (int j = 0; j < K; ++j) {
-                const float kk = __shfl(kj, j, kWave);
-                const int tt = __shfl(tj, j, kWave);
-                above += key_better(kk, tt, kj, tj) ? 1 : 0;
-            }
-            if (lane < K && above == m - 1) sh.thr = prune ? kj : -INFINITY;
-            if (lane == 0) sh.ccount = 0;
+            __syncthreads();
+            staged = r * D + d;
+        }
+
+        RngKey key;
+        key.k0 = k0;
+        key.k1 = k1;
+        key.request = (uint32_t)r;
+        key.step = step;
+        if (tid == 0) {
+            sh.thr = thr_in[node];
+            sh.ccount = 0;
         }
         __syncthreads();
         const float thr = sh.thr;
@@ -183,13 +234,14 @@ __global__ __launch_bounds__(kBlock) void replay_scan(const void* __restrict__ d
         }
         __syncthreads();
 
-        // keep this tile's best m (slot order is settled by the merge)
+        // candidates of this tile (at most kTileOut; beyond that the tile's best
+        // m are selected here); the merge settles the order
         const int c = sh.ccount;
         const size_t o = (tb + u) * (size_t)T + t;
-        if (c <= m) {
+        if (c <= kTileOut) {
             for (int j = tid; j < c; j += kBlock) {
-                out_key[o * K + j] = sh.ckey[j];
-                out_idx[o * K + j] = sh.cidx[j];
+                out_key[o * kTileOut + j] = sh.ckey[j];
+                out_idx[o * kTileOut + j] = sh.cidx[j];
             }
         } else {
             for (int j = 0; j < m; ++j) {
@@ -230,14 +282,14 @@ __global__ __launch_bounds__(kBlock) void replay_scan(const void* __restrict__ d
                             fi = wi[w2];
                             fs = wsl[w2];
                         }
-                    out_key[o * K + j] = fk;
-                    out_idx[o * K + j] = fi;
+                    out_key[o * kTileOut + j] = fk;
+                    out_idx[o * kTileOut + j] = fi;
                     sh.cidx[fs] = -1;  // taken
                 }
                 __syncthreads();
             }
         }
-        if (tid == 0) out_cnt[o] = c < m ? c : m;
+        if (tid == 0) out_cnt[o] = c <= kTileOut ? c : m;
         __syncthreads();
     }
 }
@@ -264,7 +316,7 @@ __global__ __launch_bounds__(kWave) void replay_merge(int B, int K, int T, tsb_t
         for (int base = 0; base < c; base += kWave) {
             const int j = base + lane;
             uint64_t k = 0;
-            if (j < c) k = cand_key(ck[(o + t) * K + j], (uint32_t)ci[(o + t) * K + j]);
+            if (j < c) k = cand_key(ck[(o + t) * kTileOut + j], (uint32_t)ci[(o + t) * kTileOut + j]);
             top.offer(k, j < c);
         }
     }
@@ -278,26 +330,40 @@ hipError_t launch_replay(const tsb_config& c, float invT, const void* draft, con
     float* ck = (float*)(ws + w.key);
     int* ci = (int*)(ws + w.idx);
     int* cc = (int*)(ws + w.cnt);
+    int* plist = (int*)(ws + w.plist);
+    int* ptotal = (int*)(ws + w.ptotal);
     const uint32_t k0 = (uint32_t)c.seed, k1 = (uint32_t)(c.seed >> 32);
     const int prune = (c.flags & TSB_FLAG_NO_PRUNE) ? 0 : 1;
     const bool vec = c.V % 4 == 0 && ((uintptr_t)draft & 15) == 0;
-    const dim3 grid(g.T, c.R * c.D);
     hipError_t e = hook_before(TSB_KERNEL_REPLAY_SCAN, st);
     if (e != hipSuccess) return e;
+    replay_prep<<<1, kPrepThreads, 0, st>>>(c.R, c.B, tree, plist, ptotal);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    float* thr = (float*)(ws + w.thr);
+    const int nthr = (c.R * (c.B + 1) + kBlock / kWave - 1) / (kBlock / kWave);
+    if (c.dtype == TSB_BF16)
+        replay_threshold<TSB_BF16><<<nthr, kBlock, 0, st>>>(draft, c.R, c.V, c.D, c.B, c.K, invT, topk_tok, tree, k0,
+                                                            k1, step, prune, thr);
+    else
+        replay_threshold<TSB_F32><<<nthr, kBlock, 0, st>>>(draft, c.R, c.V, c.D, c.B, c.K, invT, topk_tok, tree, k0,
+                                                           k1, step, prune, thr);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    const dim3 grid(g.T, kScanRows);
     if (c.dtype == TSB_BF16) {
         if (vec)
             replay_scan<TSB_BF16, true><<<grid, kBlock, 0, st>>>(draft, c.V, c.D, c.B, c.K, g.T, invT, topk_tok, tree,
-                                                                 k0, k1, step, prune, ck, ci, cc);
+                                                                 plist, ptotal, thr, k0, k1, step, ck, ci, cc);
         else
-            replay_scan<TSB_BF16, false><<<grid, kBlock, 0, st>>>(draft, c.V, c.D, c.B, c.K, g.T, invT, topk_tok, tree,
-                                                                  k0, k1, step, prune, ck, ci, cc);
+            replay_scan<TSB_BF16, false><<<grid, kBlock, 0, st>>>(draft, c.V, c.D, c.B, c.K, g.T, invT, topk_tok,
+                                                                  tree, plist, ptotal, thr, k0, k1, step, ck, ci,
+                                                                  cc);
     } else {
         if (vec)
             replay_scan<TSB_F32, true><<<grid, kBlock, 0, st>>>(draft, c.V, c.D, c.B, c.K, g.T, invT, topk_tok, tree,
-                                                                k0, k1, step, prune, ck, ci, cc);
+                                                                plist, ptotal, thr, k0, k1, step, ck, ci, cc);
         else
             replay_scan<TSB_F32, false><<<grid, kBlock, 0, st>>>(draft, c.V, c.D, c.B, c.K, g.T, invT, topk_tok, tree,
-                                                                 k0, k1, step, prune, ck, ci, cc);
+                                                                 plist, ptotal, thr, k0, k1, step, ck, ci, cc);
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;

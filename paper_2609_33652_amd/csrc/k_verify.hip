@@ -27,11 +27,21 @@
 namespace tsb {
 
 // ------------------------------------------------------------------ K4
+// Streamed estimate of every target row's normaliser: per thread, four
+// 16-byte loads in flight, a running maximum of the raw logits and
+// sum 2^(x c - m c) with c = invT log2(e) (one FMA and one v_exp_f32 per
+// logit; partial sums of 8 terms in binary32, accumulated in binary64).
+// The estimate only has to be within ~1e-6 of ln sum exp(a): the walk uses it
+// to take acceptance tests that are clear of U by a wide band, and computes
+// the exact normaliser (binary64 terms) for every other node it tests.
+// A NaN or +inf logit surfaces as a non-finite maximum or sum.
 template <int DT, bool VEC>
 __global__ __launch_bounds__(kBlock) void target_partials(const void* __restrict__ target, int V, int B, int seg,
                                                           int S, float invT, const int32_t* __restrict__ n_nodes,
                                                           float* __restrict__ tm, double* __restrict__ ts,
                                                           int* __restrict__ tf, uint32_t* __restrict__ counters) {
+    constexpr int kEl = 8;      // logits per 16-byte load (bf16); fp32 loads are 2 x 16 bytes
+    constexpr int kLoads = 4;   // loads in flight per thread
     const int s = blockIdx.x;
     const int row = blockIdx.y;
     const int r = row / (B + 1);
@@ -40,82 +50,81 @@ __global__ __launch_bounds__(kBlock) void target_partials(const void* __restrict
     if (s == 0 && node == 0 && tid == 0) counters[r] = 0u;
     if (node >= n_nodes[r]) return;
 
+    const float c = invT * 1.4426950408889634f;  // invT * log2(e)
     const size_t rowbase = (size_t)row * (size_t)V;
     const int lo = s * seg;
     const int hi = min(V, lo + seg);
-    float m = -INFINITY;
-    double sum = 0.0;
-    int bad = 0;
-    for (int i0 = lo + tid * 8; i0 < hi; i0 += kBlock * 8) {
-        float x[8];
-        if (VEC && i0 + 8 <= hi) {
-            if (DT == TSB_BF16) {
-                const uint4 raw = *(const uint4*)((const uint16_t*)target + rowbase + i0);
-                const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+    float m = -INFINITY;   // running max of the raw logits
+    double sum = 0.0;      // sum of 2^(x c - m c)
+    for (int base = lo; base < hi; base += kBlock * kEl * kLoads) {
+        float x[kLoads][kEl];
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    x[2 * j] = __uint_as_float(w[j] << 16);
-                    x[2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
+        for (int l = 0; l < kLoads; ++l) {
+            const int i0 = base + (l * kBlock + tid) * kEl;
+            if (VEC && i0 + kEl <= hi) {
+                if (DT == TSB_BF16) {
+                    const uint4 raw = *(const uint4*)((const uint16_t*)target + rowbase + i0);
+                    const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        x[l][2 * j] = __uint_as_float(w[j] << 16);
+                        x[l][2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
+                    }
+                } else {
+                    const float4 a = *(const float4*)((const float*)target + rowbase + i0);
+                    const float4 b = *(const float4*)((const float*)target + rowbase + i0 + 4);
+                    x[l][0] = a.x; x[l][1] = a.y; x[l][2] = a.z; x[l][3] = a.w;
+                    x[l][4] = b.x; x[l][5] = b.y; x[l][6] = b.z; x[l][7] = b.w;
                 }
             } else {
-                const float4 a = *(const float4*)((const float*)target + rowbase + i0);
-                const float4 b = *(const float4*)((const float*)target + rowbase + i0 + 4);
-                x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
-                x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
-            }
-        } else {
 #pragma unroll
-            for (int j = 0; j < 8; ++j) x[j] = (i0 + j < hi) ? load_logit<DT>(target, rowbase + i0 + j) : -INFINITY;
-        }
-        float a[8];
-        float cm = -INFINITY;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            a[j] = x[j] * invT;
-            if (isnan(a[j]) || a[j] == INFINITY) {
-                bad = 1;
-                a[j] = -INFINITY;
+                for (int j = 0; j < kEl; ++j)
+                    x[l][j] = (i0 + j < hi) ? load_logit<DT>(target, rowbase + i0 + j) : -INFINITY;
             }
-            cm = fmaxf(cm, a[j]);
         }
+        float cm = m;
+#pragma unroll
+        for (int l = 0; l < kLoads; ++l)
+#pragma unroll
+            for (int j = 0; j < kEl; ++j) cm = fmaxf(cm, x[l][j]);
         if (cm > m) {
-            sum = (m == -INFINITY) ? 0.0 : sum * (double)__expf(m - cm);
+            if (m > -INFINITY) sum *= (double)exp2f((m - cm) * c);
             m = cm;
         }
         if (m > -INFINITY) {
-            float cs = 0.f;
+            const float mc = m * c;
 #pragma unroll
-            for (int j = 0; j < 8; ++j) cs += __expf(a[j] - m);
-            sum += (double)cs;
+            for (int l = 0; l < kLoads; ++l) {
+                float cs = 0.f;
+#pragma unroll
+                for (int j = 0; j < kEl; ++j) cs += __builtin_amdgcn_exp2f(fmaf(x[l][j], c, -mc));
+                sum += (double)cs;
+            }
         }
     }
     __shared__ float s_m[kBlock / kWave];
     __shared__ double s_s[kBlock / kWave];
-    __shared__ int s_bad[kBlock / kWave];
     const int wave = tid / kWave, lane = tid % kWave;
     const float wm = wave_max(m);
-    const double contrib = (m == -INFINITY) ? 0.0 : sum * exp((double)m - (double)wm);
+    const double contrib = (m == -INFINITY) ? 0.0 : sum * (double)exp2f((m - wm) * c);
     const double wsum = wave_sum(contrib);
-    const int wb = wave_or(bad);
     if (lane == 0) {
         s_m[wave] = wm;
         s_s[wave] = wsum;
-        s_bad[wave] = wb;
     }
     __syncthreads();
     if (tid == 0) {
         float M = s_m[0];
         for (int w = 1; w < kBlock / kWave; ++w) M = fmaxf(M, s_m[w]);
         double tot = 0.0;
-        int anybad = 0;
-        for (int w = 0; w < kBlock / kWave; ++w) {
-            if (s_m[w] != -INFINITY) tot += s_s[w] * exp((double)s_m[w] - (double)M);
-            anybad |= s_bad[w];
-        }
+        for (int w = 0; w < kBlock / kWave; ++w)
+            if (s_m[w] != -INFINITY) tot += s_s[w] * (double)exp2f((s_m[w] - M) * c);
         const size_t o = (size_t)row * S + s;
-        tm[o] = M;
+        // partial as (max of a, sum exp(a - max a)), a = x invT; non-finite input
+        // leaves a NaN or infinite max/sum
+        tm[o] = M * invT;
         ts[o] = tot;
-        tf[o] = anybad;
+        tf[o] = (isnan(M) || M == INFINITY || !isfinite(tot)) ? 1 : 0;
     }
 }
 
