@@ -17,6 +17,33 @@
 namespace tsb {
 
 // ------------------------------------------------------------------ K1a
+// Eight consecutive logits of one row as binary32; positions at or past `hi`
+// read as -inf.
+template <int DT, bool VEC>
+__device__ __forceinline__ void load8(const void* __restrict__ draft, size_t rowbase, int i0, int hi, float* x) {
+    if (VEC && i0 + 8 <= hi) {
+        if (DT == TSB_BF16) {
+            const uint4 raw = *(const uint4*)((const uint16_t*)draft + rowbase + i0);
+            const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                x[2 * j] = __uint_as_float(w[j] << 16);
+                x[2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
+            }
+        } else {
+            const float4 f0 = *(const float4*)((const float*)draft + rowbase + i0);
+            const float4 f1 = *(const float4*)((const float*)draft + rowbase + i0 + 4);
+            x[0] = f0.x; x[1] = f0.y; x[2] = f0.z; x[3] = f0.w;
+            x[4] = f1.x; x[5] = f1.y; x[6] = f1.z; x[7] = f1.w;
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x[j] = (i0 + j < hi) ? load_logit<DT>(draft, rowbase + i0 + j) : -INFINITY;
+    }
+}
+
+constexpr int kDraftUnroll = 2;  // 8-logit groups per thread per chunk
+
 template <int DT, bool VEC>
 __global__ __launch_bounds__(kBlock) void draft_partials(const void* __restrict__ draft, int V, int D,
                                                          int seg, int S, float invT, int K,
@@ -31,59 +58,95 @@ __global__ __launch_bounds__(kBlock) void draft_partials(const void* __restrict_
     const size_t rowbase = (size_t)row * (size_t)V;
     const int lo = s * seg;
     const int hi = min(V, lo + seg);
+    constexpr int kChunk = kBlock * 8 * kDraftUnroll;
+
+    // the first chunk is in flight while the exp table is built
+    float xc[kDraftUnroll][8];
+#pragma unroll
+    for (int u = 0; u < kDraftUnroll; ++u) load8<DT, VEC>(draft, rowbase, lo + (u * kBlock + tid) * 8, hi, xc[u]);
 
     __shared__ double s_exp[kExpTable];
     exp64_table_init(s_exp);
 
-    float m = -INFINITY;
-    double sum = 0.0;
-    int bad = 0;
+    float m = -INFINITY;    // running max of the scaled logits (-inf entries never raise it)
+    double sum = 0.0;       // sum of e^(a - m) over this lane's elements
+    bool bad = false;       // a NaN or +inf scaled logit
     WaveTopList top;
     top.init(K);
-
-    for (int base = lo; base < hi; base += kBlock * 8) {
-        const int i0 = base + tid * 8;
-        float x[8];
-        if (VEC && i0 + 8 <= hi) {
-            if (DT == TSB_BF16) {
-                const uint4 raw = *(const uint4*)((const uint16_t*)draft + rowbase + i0);
-                const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
+    // Filter (fx, fid): a logit x with id i can still enter the wave's list
+    // only if x > fx, or x == fx and i <= fid (the key order is logit desc,
+    // id asc). It starts at the K-th largest of the lanes' first-chunk maxima
+    // (K distinct logits at or above it exist) with any id, and then follows
+    // the list's K-th entry once the list is full.
+    float fx;
+    uint32_t fid = 0xFFFFFFFFu;
+    {
+        float lm = -INFINITY;
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    x[2 * j] = __uint_as_float(w[j] << 16);
-                    x[2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
-                }
-            } else {
-                const float4 a = *(const float4*)((const float*)draft + rowbase + i0);
-                const float4 b = *(const float4*)((const float*)draft + rowbase + i0 + 4);
-                x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
-                x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
-            }
+        for (int u = 0; u < kDraftUnroll; ++u)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) lm = fmaxf(lm, xc[u][j]);
+        fx = wave_kth_largest(lm, K);
+    }
+
+    for (int base = lo; base < hi; base += kChunk) {
+        const int nbase = base + kChunk;
+        float xn[kDraftUnroll][8];
+        if (nbase < hi) {
+#pragma unroll
+            for (int u = 0; u < kDraftUnroll; ++u)
+                load8<DT, VEC>(draft, rowbase, nbase + (u * kBlock + tid) * 8, hi, xn[u]);
         } else {
 #pragma unroll
-            for (int j = 0; j < 8; ++j) x[j] = (i0 + j < hi) ? load_logit<DT>(draft, rowbase + i0 + j) : -INFINITY;
-        }
-        float a[8];
-        float cm = -INFINITY;
+            for (int u = 0; u < kDraftUnroll; ++u)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const bool in = i0 + j < hi;
-            a[j] = x[j] * invT;
-            if (in && (isnan(a[j]) || a[j] == INFINITY)) bad = 1;
-            if (in && a[j] > -INFINITY && a[j] < INFINITY) cm = fmaxf(cm, a[j]);
-        }
-        if (cm > m) {
-            sum = (m == -INFINITY) ? 0.0 : sum * exp64((double)m - (double)cm, s_exp);
-            m = cm;
+                for (int j = 0; j < 8; ++j) xn[u][j] = -INFINITY;
         }
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-            if (i0 + j < hi && a[j] > -INFINITY && a[j] < INFINITY) sum += exp64((double)a[j] - (double)m, s_exp);
+        for (int u = 0; u < kDraftUnroll; ++u) {
+            const int i0 = base + (u * kBlock + tid) * 8;
+            float xm = xc[u][0];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const bool ok = (i0 + j < hi) && !isnan(x[j]);
-            top.offer(cand_key(x[j], (uint32_t)(i0 + j)), ok);
+            for (int j = 1; j < 8; ++j) xm = fmaxf(xm, xc[u][j]);  // NaN is ignored
+            float a[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                a[j] = xc[u][j] * invT;
+                bad |= __builtin_amdgcn_classf(a[j], 0x203);  // signalling NaN, quiet NaN, +inf
+            }
+            // rounding is monotone, so the max of the scaled values is the scaled max
+            const float am = xm * invT;
+            if (am > m && am < INFINITY) {
+                sum = (m == -INFINITY) ? 0.0 : sum * exp64((double)m - (double)am, s_exp);
+                m = am;
+            }
+            const double md = (double)m;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) sum += exp64((double)a[j] - md, s_exp);
+            // the group's smallest id is i0
+            if (__ballot(xm > fx || (xm == fx && (uint32_t)i0 <= fid))) {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const float xj = xc[u][j];
+                    const uint32_t id = (uint32_t)(i0 + j);
+                    const bool ok = (i0 + j < hi) && (xj > fx || (xj == fx && id <= fid));  // false for NaN
+                    top.offer(cand_key(xj, id), ok);
+                }
+                if (top.thr) {
+                    // the list's K-th key; entering now needs a key above it
+                    const float tx = cand_value(top.thr);
+                    const uint32_t tid1 = cand_id(top.thr);
+                    if (tx > fx || (tx == fx && tid1 <= fid)) {
+                        fx = tx;
+                        fid = tid1 - 1;  // wraps for id 0 to "any id": looser, and offer re-checks the key
+                    }
+                }
+            }
         }
+#pragma unroll
+        for (int u = 0; u < kDraftUnroll; ++u)
+#pragma unroll
+            for (int j = 0; j < 8; ++j) xc[u][j] = xn[u][j];
     }
 
     // combine lanes and waves in a fixed order
@@ -234,28 +297,6 @@ __device__ __forceinline__ bool plan_precedes(const PlanShared& sh, double sa, u
         pb = sh.c_parent[pb];
     }
     return ra < rb;
-}
-
-// Whole-wave one-lane shifts (lane i gets lane i-1 / i+1; the edge lane keeps its value).
-__device__ __forceinline__ uint32_t wave_shr1(uint32_t v) {
-    return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x138, 0xf, 0xf, false);
-}
-__device__ __forceinline__ uint32_t wave_shl1(uint32_t v) {
-    return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x130, 0xf, 0xf, false);
-}
-__device__ __forceinline__ double wave_shr1(double v) {
-    const uint64_t b = __double_as_longlong(v);
-    return __longlong_as_double((long long)(((uint64_t)wave_shr1((uint32_t)(b >> 32)) << 32) | wave_shr1((uint32_t)b)));
-}
-__device__ __forceinline__ double wave_shl1(double v) {
-    const uint64_t b = __double_as_longlong(v);
-    return __longlong_as_double((long long)(((uint64_t)wave_shl1((uint32_t)(b >> 32)) << 32) | wave_shl1((uint32_t)b)));
-}
-__device__ __forceinline__ uint32_t lane_u32(uint32_t v, int l) { return (uint32_t)__builtin_amdgcn_readlane((int)v, l); }
-__device__ __forceinline__ float lane_f32(float v, int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l)); }
-__device__ __forceinline__ double lane_f64(double v, int l) {
-    const uint64_t b = __double_as_longlong(v);
-    return __longlong_as_double((long long)(((uint64_t)lane_u32((uint32_t)(b >> 32), l) << 32) | lane_u32((uint32_t)b, l)));
 }
 
 struct Entry {

@@ -78,11 +78,14 @@ constexpr float kGumbelMaxBound = 16.75f;
 // ---------------------------------------------------------------- exp (binary64)
 // Table-driven exponential (P. T. P. Tang, "Table-driven implementation of
 // the exponential function in IEEE floating-point arithmetic", ACM TOMS
-// 15(2), 1989): x = (64 m + j) ln2/64 + r with |r| <= ln2/128, so
-// e^x = 2^m * 2^(j/64) * e^r; e^r - 1 by a degree-6 Taylor polynomial
-// (truncation < 2^-54 relative), the reduction by two FMAs against a split
-// ln2/64. The 64 table entries 2^(j/64) live in LDS (exp64_table_init).
-constexpr int kExpTable = 64;
+// 15(2), 1989): x = (256 m + j) ln2/256 + r with |r| <= ln2/512, so
+// e^x = 2^m * 2^(j/256) * e^r, e^r - 1 by its degree-4 Taylor polynomial.
+// The reduction uses one FMA against fl64(ln2)/256, whose error (9.1e-20)
+// times |n| stays below 1.3e-15 for every x >= -36, i.e. for every term that
+// is not already below 2^-52 of the largest one; the truncation is below
+// 4e-17 relative. The 256 table entries 2^(j/256) live in LDS
+// (exp64_table_init). Inputs below -746 give 0; -inf gives 0; NaN gives 0.
+constexpr int kExpTable = 256;
 
 __device__ __forceinline__ void exp64_table_init(double* t) {
     for (int j = threadIdx.x; j < kExpTable; j += blockDim.x) t[j] = exp2((double)j / (double)kExpTable);
@@ -90,19 +93,15 @@ __device__ __forceinline__ void exp64_table_init(double* t) {
 }
 
 __device__ __forceinline__ double exp64(double x, const double* t) {
-    constexpr double kInvL = 92.332482616893656877;        // 64 / ln2
-    constexpr double kLhi = 0x1.62e42fefa39efp-7;          // ln2/64, leading part
-    constexpr double kLlo = 3.6235106466348431e-19;        // ln2/64 - kLhi
-    x = fmax(x, -746.0);                                   // e^-746 underflows to 0
+    constexpr double kInvL = 369.3299304675746;            // 256 / ln2
+    constexpr double kL = 0.0027076061740622863;           // fl64(ln2) / 256
+    x = fmax(x, -746.0);                                   // e^-746 rounds to 0
     const double n = rint(x * kInvL);
-    double r = fma(-n, kLhi, x);
-    r = fma(-n, kLlo, r);
+    const double r = fma(-n, kL, x);
     const int ni = (int)n;
     const int j = ni & (kExpTable - 1);
-    const int m = ni >> 6;                                 // floor(ni / 64)
-    double p = fma(r, 1.0 / 720.0, 1.0 / 120.0);
-    p = fma(r, p, 1.0 / 24.0);
-    p = fma(r, p, 1.0 / 6.0);
+    const int m = ni >> 8;                                 // floor(ni / 256)
+    double p = fma(r, 1.0 / 24.0, 1.0 / 6.0);
     p = fma(r, p, 0.5);
     p = fma(r, p, 1.0);
     p = p * r;                                             // e^r - 1
@@ -158,20 +157,40 @@ __device__ __forceinline__ int wave_or(int v) {
     for (int o = 32; o > 0; o >>= 1) v |= __shfl_xor(v, o, kWave);
     return v;
 }
-__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
-    const uint32_t lo = __shfl((uint32_t)v, src, kWave);
-    const uint32_t hi = __shfl((uint32_t)(v >> 32), src, kWave);
-    return ((uint64_t)hi << 32) | lo;
+// Whole-wave one-lane shifts through DPP (lane i receives lane i-1, resp.
+// i+1; the edge lane keeps its own value) and reads of one lane's value
+// (the lane index must be wave-uniform).
+__device__ __forceinline__ uint32_t wave_shr1(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x138, 0xf, 0xf, false);
 }
-__device__ __forceinline__ uint64_t shfl_up_u64(uint64_t v, int d) {
-    const uint32_t lo = __shfl_up((uint32_t)v, d, kWave);
-    const uint32_t hi = __shfl_up((uint32_t)(v >> 32), d, kWave);
-    return ((uint64_t)hi << 32) | lo;
+__device__ __forceinline__ uint32_t wave_shl1(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, 0x130, 0xf, 0xf, false);
+}
+__device__ __forceinline__ uint64_t wave_shr1(uint64_t v) {
+    return ((uint64_t)wave_shr1((uint32_t)(v >> 32)) << 32) | wave_shr1((uint32_t)v);
+}
+__device__ __forceinline__ uint64_t wave_shl1(uint64_t v) {
+    return ((uint64_t)wave_shl1((uint32_t)(v >> 32)) << 32) | wave_shl1((uint32_t)v);
+}
+__device__ __forceinline__ double wave_shr1(double v) {
+    return __longlong_as_double((long long)wave_shr1((uint64_t)__double_as_longlong(v)));
+}
+__device__ __forceinline__ double wave_shl1(double v) {
+    return __longlong_as_double((long long)wave_shl1((uint64_t)__double_as_longlong(v)));
+}
+__device__ __forceinline__ uint32_t lane_u32(uint32_t v, int l) { return (uint32_t)__builtin_amdgcn_readlane((int)v, l); }
+__device__ __forceinline__ float lane_f32(float v, int l) { return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l)); }
+__device__ __forceinline__ uint64_t lane_u64(uint64_t v, int l) {
+    return ((uint64_t)lane_u32((uint32_t)(v >> 32), l) << 32) | lane_u32((uint32_t)v, l);
+}
+__device__ __forceinline__ double lane_f64(double v, int l) {
+    return __longlong_as_double((long long)lane_u64((uint64_t)__double_as_longlong(v), l));
 }
 
 // A descending list of the `k` (<= 64) largest uint64 keys seen so far,
 // one entry per lane (lane i holds the i-th largest; lanes >= k hold 0).
-// Key 0 is reserved as "empty".
+// Key 0 is reserved as "empty". An insertion is a ballot for the position
+// and a one-lane shift of the tail.
 struct WaveTopList {
     uint64_t v;    // this lane's entry
     uint64_t thr;  // smallest kept key (entry of lane k-1), uniform
@@ -187,24 +206,37 @@ struct WaveTopList {
     __device__ void offer(uint64_t key, bool want) {
         want = want && key > thr;
         uint64_t ballot = __ballot(want);
+        const int lane = lane_id();
         while (ballot) {
             const int src = __ffsll((unsigned long long)ballot) - 1;
             ballot &= ballot - 1;
-            const uint64_t c = shfl_u64(key, src);
+            const uint64_t c = lane_u64(key, src);
             if (c <= thr) continue;
-            const int lane = lane_id();
-            const uint64_t gt = __ballot(lane < k && v > c);
-            const int pos = __popcll(gt);
-            const uint64_t up = shfl_up_u64(v, 1);
+            const int pos = __popcll(__ballot(lane < k && v > c));
+            const uint64_t up = wave_shr1(v);
             if (lane < k) {
                 if (lane == pos)
                     v = c;
                 else if (lane > pos)
                     v = up;
             }
-            thr = shfl_u64(v, k - 1);
+            thr = lane_u64(v, k - 1);
         }
     }
 };
+
+// The k-th largest (1 <= k <= 64) of the values held by the 64 lanes, NaN
+// counted as -inf; wave-uniform.
+__device__ __forceinline__ float wave_kth_largest(float x, int k) {
+    x = isnan(x) ? -INFINITY : x;
+    const int lane = lane_id();
+    int rank = 0;
+    for (int l = 0; l < kWave; ++l) {
+        const float o = lane_f32(x, l);
+        rank += (o > x || (o == x && l < lane)) ? 1 : 0;
+    }
+    const uint64_t b = __ballot(rank == k - 1);
+    return lane_f32(x, __ffsll((unsigned long long)b) - 1);
+}
 
 }  // namespace tsb

@@ -18,6 +18,7 @@ constexpr int kReplayTileOut = 64;   // candidates one (parent, tile) hands to t
 constexpr int kWalkGroupsMax = 128;  // workgroups per request in verification
 constexpr int kWalkTokensPerGroup = 9728;  // tokens whose binary64 (p, q) one walk workgroup holds in LDS
 constexpr int kTargetWorkgroups = 2048;
+constexpr int kDraftWorkgroups = 1024;   // row statistics: one resident wave of workgroups
 
 struct Geometry {
     int S1;          // workgroups per draft row (row statistics)
@@ -33,7 +34,7 @@ inline int ceil_div(long long a, long long b) { return (int)((a + b - 1) / b); }
 inline Geometry geometry(const tsb_config& c) {
     Geometry g;
     const long long drows = (long long)c.R * c.D;
-    int s1 = ceil_div(kTargetWorkgroups, drows);
+    int s1 = ceil_div(kDraftWorkgroups, drows);
     int s1max = ceil_div(c.V, 2048);
     g.S1 = s1 < 1 ? 1 : (s1 > s1max ? s1max : s1);
     g.seg1 = ceil_div(ceil_div(c.V, g.S1), 8) * 8;
