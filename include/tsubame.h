@@ -171,13 +171,12 @@ tsb_status tsb_step(const tsb_config* cfg, const void* draft, const void* target
  * clears the hook. The events stay owned by the caller. */
 enum {
     TSB_KERNEL_DRAFT_PARTIALS = 0, /* draft row statistics + candidates (streams the draft) */
-    TSB_KERNEL_DRAFT_MERGE = 1,
-    TSB_KERNEL_PLAN_TREE = 2,
-    TSB_KERNEL_REPLAY_SCAN = 3,
-    TSB_KERNEL_REPLAY_MERGE = 4,
-    TSB_KERNEL_TARGET_PARTIALS = 5, /* target row statistics (streams the target) */
-    TSB_KERNEL_VERIFY_WALK = 6,
-    TSB_KERNEL_COUNT = 7
+    TSB_KERNEL_PLAN_TREE = 1,      /* row merge + topology planning */
+    TSB_KERNEL_REPLAY_SCAN = 2,
+    TSB_KERNEL_REPLAY_MERGE = 3,
+    TSB_KERNEL_TARGET_PARTIALS = 4, /* target row statistics (streams the target) */
+    TSB_KERNEL_VERIFY_WALK = 5,
+    TSB_KERNEL_COUNT = 6
 };
 tsb_status tsb_profile_kernel(int32_t kernel_id, hipEvent_t start, hipEvent_t stop);
 

@@ -24,7 +24,7 @@ REQ_BUDGET_SHORT = 4
 REQ_WALK_TIMEOUT = 8
 FLAG_NO_PRUNE = 1
 MAX_D, MAX_K, MAX_B, TRACE_MAX = 64, 32, 1023, 256
-KERNELS = ("draft_partials", "draft_merge", "plan_tree", "replay_scan", "replay_merge", "target_partials",
+KERNELS = ("draft_partials", "plan_tree", "replay_scan", "replay_merge", "target_partials",
            "verify_walk")
 
 EXPORTS = ("tsb_workspace_bytes", "tsb_plan", "tsb_replay", "tsb_verify", "tsb_step",

@@ -3,12 +3,12 @@
 //                   online max / binary64 sum of exp, and the segment's K best
 //                   candidates by (logit desc, id asc) kept in a wave-wide
 //                   sorted list; one streaming read of the draft logits.
-//   draft_merge     one wave per draft row: combine the segments into the
-//                   binary64 log-sum-exp, its canonical binary32 rounding and
-//                   the planning candidates lp = fl32(a - lse32).
-//   plan_tree       one wave per request: lazy best-first expansion of rank
+//   plan_tree       one workgroup per request: merge of the segment partials
+//                   into the binary64 log-sum-exp, its canonical binary32
+//                   rounding and lp = fl32(a - lse32); then the first B rank
 //                   paths under the static order (score desc, depth asc, rank
-//                   path lexicographic asc), then BFS canonicalisation.
+//                   path lexicographic asc) by a parallel threshold search,
+//                   emitted in BFS order.
 #include <math.h>
 
 #include "tsb_device.hpp"
@@ -189,14 +189,93 @@ __global__ __launch_bounds__(kBlock) void draft_partials(const void* __restrict_
     }
 }
 
-// ------------------------------------------------------------------ K1b
-__global__ __launch_bounds__(kWave) void draft_merge(int D, int S, int K, float invT, const float* __restrict__ pm,
-                                                     const double* __restrict__ ps, const uint64_t* __restrict__ pk,
-                                                     const int* __restrict__ pf, double* __restrict__ draft_lse,
-                                                     int32_t* __restrict__ topk_tok, float* __restrict__ topk_lp,
-                                                     int32_t* __restrict__ req_status) {
-    const int row = blockIdx.x;
-    const int lane = threadIdx.x;
+// ------------------------------------------------------------------ K2
+// One workgroup of kPlanWaves waves per request.
+//
+// 1. Merge: each wave combines the segment partials of some draft rows into
+//    the binary64 log-sum-exp, its canonical binary32 rounding and the K
+//    planning candidates lp = fl32(a - lse32), kept in LDS.
+// 2. Threshold search. The topology is the first B rank paths under the
+//    static order (score desc, depth asc, rank path lexicographic asc), which
+//    is what lazy best-first expansion commits (Section 3.1; Appendix B.3).
+//    With t* the (B+1)-th largest path score, it is every node scoring above
+//    t* plus the first B - #(above t*) nodes scoring exactly t*, taken in
+//    (depth, rank path) order. Path scores never increase from a node to its
+//    children or younger siblings (lp <= 0, sorted by rank), so the nodes
+//    scoring at least a threshold form a subtree that a level-by-level count
+//    enumerates. Each wave counts one candidate threshold per round:
+//      - hi: a threshold with count(hi) <= B, and m(hi), the largest node
+//        score below hi (count(m(hi)) > count(hi));
+//      - wave 0 counts at m(hi); if that reaches B + 1, t* = m(hi);
+//      - the other waves count at thresholds spread below m(hi); a count in
+//        [B + 1, cap] has every node scoring at least its threshold in LDS,
+//        and t* is selected among them;
+//      - otherwise hi moves to the lowest threshold that counted <= B (its
+//        count grows by at least one per round, so rounds end).
+// 3. Emission: one wave enumerates the admitted nodes level by level in
+//    (depth, rank path) order, which is the BFS canonical order: parents in
+//    order, children by rank. Chosen children form a prefix of each parent's
+//    children.
+constexpr int kPlanWaves = 16;
+constexpr int kPlanThreads = kPlanWaves * kWave;
+constexpr int kPlanBuf = 12288;  // binary64 slots shared by the counting waves
+
+struct PlanShared {
+    float lp[TSB_MAX_D * TSB_MAX_K];
+    int kfin[TSB_MAX_D];  // finite candidates per row (a prefix: -inf sorts last)
+    int bad;
+    double piv[kPlanWaves];
+    double mval[kPlanWaves];
+    int cnt[kPlanWaves];
+    double tstar;
+    int g;
+    union {
+        double buf[kPlanBuf];
+        struct {
+            double score[TSB_MAX_B + 1];
+            int par[TSB_MAX_B + 1];
+            int rank[TSB_MAX_B + 1];
+            int depth[TSB_MAX_B + 1];
+            int nch[TSB_MAX_B + 1];
+            int fc[TSB_MAX_B + 1];
+        } t;
+    } u;
+};
+
+// Exclusive prefix sum over the lanes of small non-negative counts (< 64),
+// one ballot per bit; `total` receives the wave sum.
+__device__ __forceinline__ int wave_excl_scan6(int c, int& total) {
+    int off = 0;
+    total = 0;
+#pragma unroll
+    for (int b = 0; b < 6; ++b) {
+        const uint64_t m = __ballot((c >> b) & 1);
+        const int below = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                         __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+        off += below << b;
+        total += __popcll(m) << b;
+    }
+    return off;
+}
+
+__device__ __forceinline__ double wave_max_f64(double v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o, kWave));
+    return v;
+}
+__device__ __forceinline__ double wave_min_f64(double v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmin(v, __shfl_xor(v, o, kWave));
+    return v;
+}
+
+// Merge of one draft row (one wave): log-sum-exp from the segment partials
+// in a fixed order, candidates from the segment lists.
+__device__ void merge_row(PlanShared& sh, int row, int rrow, int S, int K, float invT, const float* __restrict__ pm,
+                          const double* __restrict__ ps, const uint64_t* __restrict__ pk,
+                          const int* __restrict__ pf, double* __restrict__ draft_lse,
+                          int32_t* __restrict__ topk_tok, float* __restrict__ topk_lp) {
+    const int lane = lane_id();
     const size_t o = (size_t)row * S;
     float M = -INFINITY;
     int bad = 0;
@@ -223,332 +302,246 @@ __global__ __launch_bounds__(kWave) void draft_merge(int D, int S, int K, float 
     const bool nonfinite = bad || M == -INFINITY;
     const double l64 = nonfinite ? (double)NAN : (double)M + log(tot);
     const float l32 = (float)l64;
-    if (lane == 0) {
-        draft_lse[row] = l64;
-        if (nonfinite) atomicOr(&req_status[row / D], TSB_REQ_NONFINITE);
-    }
+    float lp = -INFINITY;
     if (lane < K) {
         const uint64_t k = top.v;
-        const float x = cand_value(k);
-        const float a = x * invT;
+        const float a = cand_value(k) * invT;
+        lp = a - l32;
         topk_tok[(size_t)row * K + lane] = (int32_t)cand_id(k);
-        topk_lp[(size_t)row * K + lane] = a - l32;
+        topk_lp[(size_t)row * K + lane] = lp;
+        sh.lp[rrow * K + lane] = lp;
+    }
+    const int nfin = __popcll(__ballot(lane < K && lp > -INFINITY && lp < INFINITY));
+    if (lane == 0) {
+        draft_lse[row] = l64;
+        sh.kfin[rrow] = nfin;
+        if (nonfinite) atomicOr(&sh.bad, 1);
     }
 }
 
-// ------------------------------------------------------------------ K2
-// Frontier of the lazy best-first expansion, one wave per request. The best
-// (up to) 64 frontier entries are kept sorted across the lanes of the wave
-// (lane i holds the i-th best), so a pop is lane 0 and a whole-wave one-lane
-// DPP shift, and a push is a ballot for its position and a one-lane shift.
-// Entries that fall off the end go to a "cold" list in LDS; every cold entry
-// ranks after every hot entry (a push that ranks after the best cold entry
-// goes to the cold list too), so the hot head is always the global best.
-// When the hot list runs empty, the best cold entries are moved back.
-//
-// Entry: score (binary64); info = depth << 16 | rank << 10 | parent (pop
-// index of the committed parent, root = 0); the parent's score; and the two
-// planning log-probabilities the entry needs once popped (its first child's
-// and its next sibling's), so a pop reads no memory.
-constexpr int kInfoParentBits = 10;
-constexpr int kInfoRankBits = 6;
-
-struct PlanShared {
-    float lp[TSB_MAX_D * TSB_MAX_K];
-    double c_score[TSB_MAX_B + 1];
-    int c_parent[TSB_MAX_B + 1];
-    int c_rank[TSB_MAX_B + 1];
-    int c_depth[TSB_MAX_B + 1];
-    union {
-        struct {
-            double score[TSB_MAX_B + 2];
-            double pscore[TSB_MAX_B + 2];
-            uint32_t info[TSB_MAX_B + 2];
-        } cold;
-        struct {
-            int order[TSB_MAX_B + 1];
-            int bfs_of[TSB_MAX_B + 1];
-            int nch[TSB_MAX_B + 1];
-            int fc[TSB_MAX_B + 1];
-        } b;  // BFS canonicalisation
-    } u;
-};
-
-__device__ __forceinline__ int info_depth(uint32_t i) { return (int)(i >> 16); }
-__device__ __forceinline__ int info_rank(uint32_t i) { return (int)((i >> kInfoParentBits) & ((1u << kInfoRankBits) - 1)); }
-__device__ __forceinline__ int info_parent(uint32_t i) { return (int)(i & ((1u << kInfoParentBits) - 1)); }
-__device__ __forceinline__ uint32_t make_info(int depth, int rank, int parent) {
-    return ((uint32_t)depth << 16) | ((uint32_t)rank << kInfoParentBits) | (uint32_t)parent;
-}
-
-// Static order of frontier entries: score desc, depth asc, rank path
-// lexicographic asc (equal depth: walk both parents up to their common
-// ancestor and compare the ranks just below it). True if a precedes b.
-__device__ __forceinline__ bool plan_precedes(const PlanShared& sh, double sa, uint32_t ia, double sb, uint32_t ib) {
-    if (sa != sb) return sa > sb;
-    const int da = info_depth(ia), db = info_depth(ib);
-    if (da != db) return da < db;
-    int pa = info_parent(ia), pb = info_parent(ib);
-    int ra = info_rank(ia), rb = info_rank(ib);
-    for (int guard = 0; pa != pb && guard < TSB_MAX_D; ++guard) {
-        ra = sh.c_rank[pa];
-        rb = sh.c_rank[pb];
-        pa = sh.c_parent[pa];
-        pb = sh.c_parent[pb];
-    }
-    return ra < rb;
-}
-
-struct Entry {
-    double s, ps;   // score, parent's score
-    uint32_t i;     // info
-    float lc, lsib; // first child's lp (NaN: none), next sibling's lp (NaN: none)
-};
-
-__device__ __forceinline__ Entry shr1(const Entry& e) {
-    return Entry{wave_shr1(e.s), wave_shr1(e.ps), wave_shr1(e.i), __uint_as_float(wave_shr1(__float_as_uint(e.lc))),
-                 __uint_as_float(wave_shr1(__float_as_uint(e.lsib)))};
-}
-__device__ __forceinline__ Entry shl1(const Entry& e) {
-    return Entry{wave_shl1(e.s), wave_shl1(e.ps), wave_shl1(e.i), __uint_as_float(wave_shl1(__float_as_uint(e.lc))),
-                 __uint_as_float(wave_shl1(__float_as_uint(e.lsib)))};
-}
-__device__ __forceinline__ Entry lane_entry(const Entry& e, int l) {
-    return Entry{lane_f64(e.s, l), lane_f64(e.ps, l), lane_u32(e.i, l), lane_f32(e.lc, l), lane_f32(e.lsib, l)};
-}
-
-// lp values a new entry (depth dep, rank rk) will need once popped
-__device__ __forceinline__ Entry make_entry(const PlanShared& sh, int Dp, int K, double s, double ps, int dep, int rk,
-                                            int par) {
-    Entry e;
-    e.s = s;
-    e.ps = ps;
-    e.i = make_info(dep, rk, par);
-    e.lc = dep < Dp ? sh.lp[dep * K + 0] : (float)NAN;
-    e.lsib = rk + 1 < K ? sh.lp[(dep - 1) * K + rk + 1] : (float)NAN;
-    return e;
-}
-
-struct Frontier {
-    Entry h;  // this lane's hot entry
-    int nh, ncold;
-    double cold_s;  // best cold entry (valid when ncold > 0)
-    uint32_t cold_i;
-};
-
-__device__ __forceinline__ void frontier_to_cold(PlanShared& sh, Frontier& F, const Entry& e) {
-    if (lane_id() == 0) {
-        sh.u.cold.score[F.ncold] = e.s;
-        sh.u.cold.pscore[F.ncold] = e.ps;
-        sh.u.cold.info[F.ncold] = e.i;
-    }
-    if (F.ncold == 0 || plan_precedes(sh, e.s, e.i, F.cold_s, F.cold_i)) {
-        F.cold_s = e.s;
-        F.cold_i = e.i;
-    }
-    ++F.ncold;
-}
-
-__device__ __forceinline__ void frontier_push(PlanShared& sh, Frontier& F, const Entry& e) {
-    // entries ranking after the best cold entry stay cold (invariant)
-    if (F.ncold > 0 && !plan_precedes(sh, e.s, e.i, F.cold_s, F.cold_i)) {
-        frontier_to_cold(sh, F, e);
-        return;
-    }
+// Number of nodes (root excluded) scoring at least tau, level by level, with
+// their scores stored in buf; cap + 1 once more than cap. m_out: the largest
+// node score below tau (-inf if none; meaningful without overflow).
+__device__ int plan_count(const PlanShared& sh, int Dp, int K, double tau, int cap, double* buf, double& m_out) {
     const int lane = lane_id();
-    const bool before = lane < F.nh && plan_precedes(sh, F.h.s, F.h.i, e.s, e.i);
-    const int pos = __popcll(__ballot(before));
-    if (F.nh == kWave) {  // the entry that leaves: the old tail, or e if it ranks last
-        if (pos == kWave) {
-            frontier_to_cold(sh, F, e);
-            return;
+    int total = 0;
+    int plo = 0, phi = 0;  // parents of the current level in buf; level 0: the root
+    double m = -INFINITY;
+    for (int k = 0; k < Dp; ++k) {
+        const int kk = sh.kfin[k];
+        const float lpv = lane < kk ? sh.lp[k * K + lane] : -INFINITY;
+        const int np = k == 0 ? 1 : phi - plo;
+        const int nstart = total;
+        for (int base = 0; base < np; base += kWave) {
+            const int i = base + lane;
+            const bool valid = i < np;
+            const double s = (valid && k > 0) ? buf[plo + i] : 0.0;
+            int c = 0;
+            bool done = !valid;
+            for (int j = 0; j < kk; ++j) {
+                const double cs = s + (double)lane_f32(lpv, j);
+                const bool ok = valid && cs >= tau;
+                if (!done && !ok) {
+                    m = fmax(m, cs);  // the parent's best child below tau
+                    done = true;
+                }
+                if (!__ballot(ok)) break;
+                c += ok ? 1 : 0;
+            }
+            int tot;
+            const int off = wave_excl_scan6(c, tot);
+            if (total + tot > cap) {
+                m_out = -INFINITY;
+                return cap + 1;
+            }
+            for (int j = 0; __ballot(j < c); ++j) {
+                const float lj = lane_f32(lpv, j);
+                if (j < c) buf[total + off + j] = s + (double)lj;
+            }
+            total += tot;
         }
-        frontier_to_cold(sh, F, lane_entry(F.h, kWave - 1));
+        __threadfence_block();  // the next level reads these scores from other lanes
+        plo = nstart;
+        phi = total;
+        if (phi == plo) break;
     }
-    const Entry up = shr1(F.h);
-    if (lane == pos)
-        F.h = e;
-    else if (lane > pos)
-        F.h = up;
-    if (F.nh < kWave) ++F.nh;
+    m_out = wave_max_f64(m);
+    return total;
 }
 
-__global__ __launch_bounds__(kWave) void plan_tree(int D, int K, int B, const float* __restrict__ topk_lp,
-                                                   tsb_tree tree, int32_t* __restrict__ req_status) {
+__global__ __launch_bounds__(kPlanThreads) void plan_tree(int D, int S, int K, int B, float invT,
+                                                          const float* __restrict__ pm,
+                                                          const double* __restrict__ ps,
+                                                          const uint64_t* __restrict__ pk,
+                                                          const int* __restrict__ pf, double* __restrict__ draft_lse,
+                                                          int32_t* __restrict__ topk_tok,
+                                                          float* __restrict__ topk_lp, tsb_tree tree,
+                                                          int32_t* __restrict__ req_status) {
     __shared__ PlanShared sh;
     const int r = blockIdx.x;
-    const int lane = threadIdx.x;
-    const bool nonfinite = (req_status[r] & TSB_REQ_NONFINITE) != 0;
+    const int tid = threadIdx.x;
+    const int wave = tid / kWave, lane = tid % kWave;
+
+    if (tid == 0) sh.bad = 0;
+    __syncthreads();
+    for (int d = wave; d < D; d += kPlanWaves)
+        merge_row(sh, r * D + d, d, S, K, invT, pm, ps, pk, pf, draft_lse, topk_tok, topk_lp);
+    __syncthreads();
+    const bool nonfinite = sh.bad != 0;
     const int Dp = nonfinite ? 0 : D;
 
-    for (int i = lane; i < D * K; i += kWave) sh.lp[i] = topk_lp[(size_t)r * D * K + i];
-    if (lane == 0) {
-        sh.c_parent[0] = -1;
-        sh.c_rank[0] = -1;
-        sh.c_depth[0] = 0;
-        sh.c_score[0] = 0.0;
-    }
-    __syncthreads();
-
-    Frontier F;
-    F.h.s = -INFINITY;
-    F.h.ps = 0.0;
-    F.h.i = 0;
-    F.h.lc = F.h.lsib = (float)NAN;
-    F.nh = 0;
-    F.ncold = 0;
-    F.cold_s = -INFINITY;
-    F.cold_i = 0;
-
-    if (Dp > 0 && isfinite(sh.lp[0])) frontier_push(sh, F, make_entry(sh, Dp, K, 0.0 + (double)sh.lp[0], 0.0, 1, 0, 0));
-    int committed = 1;
-
-    while (committed <= B && (F.nh > 0 || F.ncold > 0)) {
-        if (F.nh == 0) {
-            // refill: move the best cold entries back, best first
-            __syncthreads();
-            const int take = F.ncold < kWave ? F.ncold : kWave;
-            for (int t = 0; t < take; ++t) {
-                double bs = -INFINITY;
-                uint32_t bi = 0;
-                int bj = -1;
-                for (int j = lane; j < F.ncold; j += kWave) {
-                    const double cs = sh.u.cold.score[j];
-                    const uint32_t ci = sh.u.cold.info[j];
-                    if (bj < 0 || plan_precedes(sh, cs, ci, bs, bi)) {
-                        bs = cs;
-                        bi = ci;
-                        bj = j;
-                    }
-                }
-#pragma unroll
-                for (int o = 32; o > 0; o >>= 1) {
-                    const double os = __shfl_xor(bs, o, kWave);
-                    const uint32_t oi = (uint32_t)__shfl_xor((int)bi, o, kWave);
-                    const int oj = __shfl_xor(bj, o, kWave);
-                    if (oj >= 0 && (bj < 0 || plan_precedes(sh, os, oi, bs, bi))) {
-                        bs = os;
-                        bi = oi;
-                        bj = oj;
-                    }
-                }
-                const double bps = sh.u.cold.pscore[bj];
-                if (lane == t) F.h = make_entry(sh, Dp, K, bs, bps, info_depth(bi), info_rank(bi), info_parent(bi));
-                __syncthreads();
-                if (lane == 0) {
-                    sh.u.cold.score[bj] = sh.u.cold.score[F.ncold - 1];
-                    sh.u.cold.pscore[bj] = sh.u.cold.pscore[F.ncold - 1];
-                    sh.u.cold.info[bj] = sh.u.cold.info[F.ncold - 1];
-                }
-                --F.ncold;
-                __syncthreads();
-            }
-            F.nh = take;
-            // best remaining cold entry
-            if (F.ncold > 0) {
-                double bs = -INFINITY;
-                uint32_t bi = 0;
-                int bj = -1;
-                for (int j = lane; j < F.ncold; j += kWave) {
-                    const double cs = sh.u.cold.score[j];
-                    const uint32_t ci = sh.u.cold.info[j];
-                    if (bj < 0 || plan_precedes(sh, cs, ci, bs, bi)) {
-                        bs = cs;
-                        bi = ci;
-                        bj = j;
-                    }
-                }
-#pragma unroll
-                for (int o = 32; o > 0; o >>= 1) {
-                    const double os = __shfl_xor(bs, o, kWave);
-                    const uint32_t oi = (uint32_t)__shfl_xor((int)bi, o, kWave);
-                    const int oj = __shfl_xor(bj, o, kWave);
-                    if (oj >= 0 && (bj < 0 || plan_precedes(sh, os, oi, bs, bi))) {
-                        bs = os;
-                        bi = oi;
-                        bj = oj;
-                    }
-                }
-                F.cold_s = bs;
-                F.cold_i = bi;
+    // ---- threshold search (uniform control flow across the workgroup)
+    const int cap = 2 * (B + 1);
+    const int ns = min(kPlanWaves, kPlanBuf / cap);
+    double hi_m = (Dp > 0 && sh.kfin[0] > 0) ? (double)sh.lp[0] : -INFINITY;  // the best node's score
+    int hi_cnt = 0;
+    double lo = -INFINITY;
+    int mode = 3;  // 1: t* = hi_m; 2: t* selected in a wave's buffer; 3: every node is chosen
+    int src = -1;
+    // every round raises count(hi) by at least one (at most B + 1 rounds); the
+    // guard only bounds the loop
+    for (int round = 0; hi_m > -INFINITY; ++round) {
+        if (round > B + 1) {
+            mode = 1;
+            break;
+        }
+        if (wave < ns) {
+            const double tau = wave == 0 ? hi_m
+                               : (lo > -INFINITY ? hi_m - (hi_m - lo) * ((double)wave / (double)ns)
+                                                 : hi_m - 0.125 * ldexp(1.0, wave - 1));
+            double m;
+            const int c = plan_count(sh, Dp, K, tau, cap, sh.u.buf + wave * cap, m);
+            if (lane == 0) {
+                sh.piv[wave] = tau;
+                sh.cnt[wave] = c;
+                sh.mval[wave] = m;
             }
         }
-        // pop the head
-        const Entry top = lane_entry(F.h, 0);
-        {
-            const Entry dn = shl1(F.h);
-            if (lane < F.nh - 1) F.h = dn;
-            --F.nh;
+        __syncthreads();
+        if (sh.cnt[0] >= B + 1) {
+            mode = 1;
+            break;
         }
-        const int dep = info_depth(top.i), rk = info_rank(top.i), par = info_parent(top.i);
-        const int c = committed++;
-        if (lane == 0) {  // single wave: later LDS reads see these writes in order
-            sh.c_parent[c] = par;
-            sh.c_rank[c] = rk;
-            sh.c_depth[c] = dep;
-            sh.c_score[c] = top.s;
+        int best = -1;
+        for (int w = 1; w < ns; ++w)
+            if (sh.cnt[w] >= B + 1 && sh.cnt[w] <= cap && (best < 0 || sh.piv[w] > sh.piv[best])) best = w;
+        if (best >= 0) {
+            mode = 2;
+            src = best;
+            break;
         }
-        if (!isnan(top.lc) && isfinite(top.lc))
-            frontier_push(sh, F, make_entry(sh, Dp, K, top.s + (double)top.lc, top.s, dep + 1, 0, c));
-        if (!isnan(top.lsib) && isfinite(top.lsib))
-            frontier_push(sh, F, make_entry(sh, Dp, K, top.ps + (double)top.lsib, top.ps, dep, rk + 1, par));
+        int nh = 0;  // count(piv[0]) <= B here
+        double nlo = lo;
+        for (int w = 1; w < ns; ++w) {
+            if (sh.cnt[w] <= B && sh.piv[w] < sh.piv[nh]) nh = w;
+            if (sh.cnt[w] > cap && sh.piv[w] > nlo) nlo = sh.piv[w];
+        }
+        hi_cnt = sh.cnt[nh];
+        hi_m = sh.mval[nh];
+        lo = nlo;
+        __syncthreads();
+    }
+    if (mode == 1) {
+        if (tid == 0) {
+            sh.tstar = hi_m;
+            sh.g = hi_cnt;
+        }
+    } else if (mode == 2) {
+        const int c = sh.cnt[src];
+        const double* b = sh.u.buf + src * cap;
+        for (int i = tid; i < c; i += kPlanThreads) {
+            const double v = b[i];
+            int gt = 0, ge = 0;
+            for (int j = 0; j < c; ++j) {
+                const double w = b[j];
+                gt += w > v ? 1 : 0;
+                ge += w >= v ? 1 : 0;
+            }
+            if (gt <= B && ge >= B + 1) {  // every such thread holds the same value
+                sh.tstar = v;
+                sh.g = gt;
+            }
+        }
+    } else if (tid == 0) {
+        sh.tstar = -INFINITY;  // every node scores above it
+        sh.g = 0;
     }
     __syncthreads();
-    const int nf = F.nh + F.ncold;
-    // best uncommitted: the hot head (the cold list ranks after it), else the best cold entry
-    const double bestf = F.nh > 0 ? lane_f64(F.h.s, 0) : F.cold_s;
-    const int n = committed;
-    const double margin = (nf > 0 && n > 1) ? sh.c_score[n - 1] - bestf : (double)INFINITY;
-    __syncthreads();
+    if (wave != 0) return;
 
-    // BFS canonicalisation (the frontier storage is reused)
-    for (int i = lane; i < n; i += kWave) sh.u.b.nch[i] = 0;
-    __syncthreads();
-    for (int c = 1 + lane; c < n; c += kWave) atomicAdd(&sh.u.b.nch[sh.c_parent[c]], 1);
+    // ---- emission in BFS order (wave 0)
+    const double tstar = sh.tstar;
+    int quota = mode == 3 ? 0 : B - sh.g;  // nodes scoring exactly t* still admitted
+    bool tie_admitted = false;
+    double minsc = INFINITY;
     if (lane == 0) {
-        sh.u.b.order[0] = 0;
-        sh.u.b.bfs_of[0] = 0;
+        sh.u.t.score[0] = 0.0;
+        sh.u.t.par[0] = -1;
+        sh.u.t.rank[0] = -1;
+        sh.u.t.depth[0] = 0;
     }
-    __syncthreads();
-    int lo = 0, hi = 1, L = 0;
-    while (lo < hi) {
-        int running = hi;
-        for (int base = lo; base < hi; base += kWave) {
+    int n = 1, plo = 0, phi = 1;
+    for (int k = 0; k < Dp && plo < phi; ++k) {
+        const int kk = sh.kfin[k];
+        const float lpv = lane < kk ? sh.lp[k * K + lane] : -INFINITY;
+        for (int base = plo; base < phi; base += kWave) {
             const int i = base + lane;
-            const int cnt = i < hi ? sh.u.b.nch[sh.u.b.order[i]] : 0;
-            int incl = cnt;
-#pragma unroll
-            for (int o = 1; o < kWave; o <<= 1) {
-                const int t = __shfl_up(incl, o, kWave);
-                if (lane >= o) incl += t;
+            const bool valid = i < phi;
+            const double s = valid ? sh.u.t.score[i] : 0.0;
+            int cg = 0, ce = 0;
+            for (int j = 0; j < kk; ++j) {
+                const double cs = s + (double)lane_f32(lpv, j);
+                const bool gt = valid && cs > tstar;
+                const bool eq = valid && cs == tstar;
+                if (!__ballot(gt || eq)) break;
+                cg += gt ? 1 : 0;
+                ce += eq ? 1 : 0;
             }
-            if (i < hi) sh.u.b.fc[i] = running + incl - cnt;
-            running += __shfl(incl, kWave - 1, kWave);
-        }
-        __syncthreads();
-        for (int c = 1 + lane; c < n; c += kWave) {
-            if (sh.c_depth[c] == L + 1) {
-                const int b = sh.u.b.fc[sh.u.b.bfs_of[sh.c_parent[c]]] + sh.c_rank[c];
-                sh.u.b.order[b] = c;
-                sh.u.b.bfs_of[c] = b;
+            int etot;
+            const int eoff = wave_excl_scan6(ce, etot);
+            const int adm = max(0, min(ce, quota - eoff));
+            if (etot > 0 && quota > 0) tie_admitted = true;
+            quota -= min(etot, quota);
+            const int c = cg + adm;
+            int tot;
+            const int off = wave_excl_scan6(c, tot);
+            for (int j = 0; __ballot(j < c); ++j) {
+                const float lj = lane_f32(lpv, j);
+                if (j < c && n + off + j <= B) {  // always true: the admitted nodes number at most B
+                    const int x = n + off + j;
+                    const double cs = s + (double)lj;
+                    sh.u.t.score[x] = cs;
+                    sh.u.t.par[x] = i;
+                    sh.u.t.rank[x] = j;
+                    sh.u.t.depth[x] = k + 1;
+                    minsc = fmin(minsc, cs);
+                }
             }
+            if (valid) {
+                sh.u.t.nch[i] = c;
+                sh.u.t.fc[i] = c ? n + off : -1;
+            }
+            n = min(n + tot, B + 1);
         }
-        __syncthreads();
-        lo = hi;
-        hi = running;
-        ++L;
+        __threadfence_block();
+        plo = phi;
+        phi = n;
     }
+    for (int i = plo + lane; i < phi; i += kWave) {  // the last level has no children
+        sh.u.t.nch[i] = 0;
+        sh.u.t.fc[i] = -1;
+    }
+    minsc = wave_min_f64(minsc);
 
     const size_t o = (size_t)r * (B + 1);
     for (int i = lane; i < B + 1; i += kWave) {
         if (i < n) {
-            const int c = sh.u.b.order[i];
-            tree.parent[o + i] = c == 0 ? -1 : sh.u.b.bfs_of[sh.c_parent[c]];
-            tree.depth[o + i] = sh.c_depth[c];
-            tree.rank[o + i] = sh.c_rank[c];
-            tree.score[o + i] = sh.c_score[c];
-            tree.n_children[o + i] = sh.u.b.nch[c];
-            tree.first_child[o + i] = sh.u.b.nch[c] ? sh.u.b.fc[i] : -1;
+            tree.parent[o + i] = sh.u.t.par[i];
+            tree.depth[o + i] = sh.u.t.depth[i];
+            tree.rank[o + i] = sh.u.t.rank[i];
+            tree.score[o + i] = sh.u.t.score[i];
+            tree.n_children[o + i] = sh.u.t.nch[i];
+            tree.first_child[o + i] = sh.u.t.fc[i];
         } else {
             tree.parent[o + i] = -1;
             tree.depth[o + i] = -1;
@@ -559,9 +552,15 @@ __global__ __launch_bounds__(kWave) void plan_tree(int D, int K, int B, const fl
         }
     }
     if (lane == 0) {
+        // margin: score of the B-th node in the order minus that of the (B+1)-th
+        double margin = (double)INFINITY;
+        if (mode != 3 && n > 1) margin = (tie_admitted ? tstar : minsc) - tstar;
         tree.n_nodes[r] = n;
         tree.plan_margin[r] = margin;
-        if (!nonfinite && n < B + 1) req_status[r] |= TSB_REQ_BUDGET_SHORT;
+        int st = req_status[r];
+        if (nonfinite) st |= TSB_REQ_NONFINITE;
+        else if (n < B + 1) st |= TSB_REQ_BUDGET_SHORT;
+        req_status[r] = st;
     }
 }
 
@@ -597,14 +596,9 @@ hipError_t launch_plan(const tsb_config& c, float invT, const void* draft, doubl
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     if ((e = hook_after(TSB_KERNEL_DRAFT_PARTIALS, st)) != hipSuccess) return e;
-    if ((e = hook_before(TSB_KERNEL_DRAFT_MERGE, st)) != hipSuccess) return e;
-    draft_merge<<<c.R * c.D, kWave, 0, st>>>(c.D, g.S1, c.K, invT, pm, ps, pk, pf, draft_lse, topk_tok, topk_lp,
-                                             req_status);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    if ((e = hook_after(TSB_KERNEL_DRAFT_MERGE, st)) != hipSuccess) return e;
     if ((e = hook_before(TSB_KERNEL_PLAN_TREE, st)) != hipSuccess) return e;
-    plan_tree<<<c.R, kWave, 0, st>>>(c.D, c.K, c.B, topk_lp, tree, req_status);
+    plan_tree<<<c.R, kPlanThreads, 0, st>>>(c.D, g.S1, c.K, c.B, invT, pm, ps, pk, pf, draft_lse, topk_tok, topk_lp,
+                                            tree, req_status);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     return hook_after(TSB_KERNEL_PLAN_TREE, st);

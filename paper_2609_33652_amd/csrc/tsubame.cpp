@@ -195,6 +195,6 @@ const char* tsb_status_string(tsb_status s) {
 
 const char* tsb_last_error(void) { return g_last_error; }
 
-int32_t tsb_version(void) { return 100; }
+int32_t tsb_version(void) { return 101; }
 
 }  // extern "C"

@@ -33,7 +33,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(tsb.EXPORTS)
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.tsb_version() == 100
+    assert lib.tsb_version() == 101
 
 
 def _cfg(**kw):

@@ -267,3 +267,35 @@ def test_edge_chain_and_minimal_vocabulary():
     for s in range(20):
         h, tally = _run_edge(cfg, d, t, step=s)
         assert tally.exact >= 4
+
+
+def _plan_only(cfg, draft_np):
+    rnd = make_round(cfg, 11)
+    rnd.plan(torch.from_numpy(draft_np).cuda())
+    h = rnd.host()
+    tally = Tally()
+    for r in range(cfg["R"]):
+        pl = ostep.plan_request(draft_np[r], cfg["T"], cfg["K"], cfg["B"])
+        compare_plan(h, r, pl, tally, "plan req %d" % r)  # raises on a mismatch that is not a near-tie
+    say("plan-only %s: exact %d flagged %d %s" % (W.describe(cfg), tally.exact, tally.flagged, tally.notes[:3]))
+    return h, tally
+
+
+@pytest.mark.parametrize("B,K,D", [(1, 4, 6), (7, 4, 6), (50, 6, 8), (200, 8, 10), (1023, 32, 64)])
+def test_planner_exact_ties(B, K, D):
+    """Exact score ties (identical logits, few distinct values) at small and maximal budgets: the
+    topology is decided by depth and rank path, so it must match bit for bit."""
+    V = 96
+    rng = np.random.default_rng(B * 7 + K)
+    d = np.zeros((5, D, V), dtype=np.float32)
+    d[0] = 0.0                                                   # every candidate ties
+    d[1] = rng.integers(0, 4, size=(D, V)).astype(np.float32)    # four distinct values
+    d[2] = rng.standard_normal((D, V)).astype(np.float32)
+    d[2, :, :3] = 5.0                                            # three tied peaks per row
+    d[3] = (rng.standard_normal((D, V)) * 3).astype(np.float32)  # no designed ties
+    d[4] = np.round(rng.standard_normal((D, V)) * 4) / 4         # quarter steps
+    cfg = dict(name="ties", R=5, V=V, D=D, B=B, K=K, T=1.0, dtype="f32", steps=1)
+    h, tally = _plan_only(cfg, d)
+    assert tally.exact >= 4
+    nmax = sum(K ** i for i in range(1, D + 1))
+    assert (h["n_nodes"] == min(B, nmax) + 1).all()
