@@ -35,25 +35,21 @@ namespace tsb {
 // to take acceptance tests that are clear of U by a wide band, and computes
 // the exact normaliser (binary64 terms) for every other node it tests.
 // A NaN or +inf logit surfaces as a non-finite maximum or sum.
+//
+// Loads are non-temporal: the rows stream through once, and keeping them out
+// of the caches' normal allocation was measured ~11% faster on this part.
+//
+// Layout: a persistent grid. The target is one flat array of R (B+1) V
+// logits cut into equal chunks, one per workgroup (all resident at once, so
+// no workgroup trails the others). A chunk covers pieces of one or two rows;
+// piece k of row t (its k-th workgroup) is partial slot k of the row, and
+// the row's first workgroup marks the slots no piece uses as empty.
 template <int DT, bool VEC>
-__global__ __launch_bounds__(kBlock) void target_partials(const void* __restrict__ target, int V, int B, int seg,
-                                                          int S, float invT, const int32_t* __restrict__ n_nodes,
-                                                          float* __restrict__ tm, double* __restrict__ ts,
-                                                          int* __restrict__ tf, uint32_t* __restrict__ counters) {
+__device__ __forceinline__ void stream_piece(const void* __restrict__ target, size_t rowbase, int lo, int hi,
+                                             float c, float& m_out, double& sum_out) {
     constexpr int kEl = 8;      // logits per 16-byte load (bf16); fp32 loads are 2 x 16 bytes
     constexpr int kLoads = 4;   // loads in flight per thread
-    const int s = blockIdx.x;
-    const int row = blockIdx.y;
-    const int r = row / (B + 1);
-    const int node = row % (B + 1);
     const int tid = threadIdx.x;
-    if (s == 0 && node == 0 && tid == 0) counters[r] = 0u;
-    if (node >= n_nodes[r]) return;
-
-    const float c = invT * 1.4426950408889634f;  // invT * log2(e)
-    const size_t rowbase = (size_t)row * (size_t)V;
-    const int lo = s * seg;
-    const int hi = min(V, lo + seg);
     float m = -INFINITY;   // running max of the raw logits
     double sum = 0.0;      // sum of 2^(x c - m c)
     for (int base = lo; base < hi; base += kBlock * kEl * kLoads) {
@@ -63,7 +59,7 @@ __global__ __launch_bounds__(kBlock) void target_partials(const void* __restrict
             const int i0 = base + (l * kBlock + tid) * kEl;
             if (VEC && i0 + kEl <= hi) {
                 if (DT == TSB_BF16) {
-                    const uint4 raw = *(const uint4*)((const uint16_t*)target + rowbase + i0);
+                    const uint4 raw = load_stream16((const uint16_t*)target + rowbase + i0);
                     const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
@@ -71,10 +67,12 @@ __global__ __launch_bounds__(kBlock) void target_partials(const void* __restrict
                         x[l][2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
                     }
                 } else {
-                    const float4 a = *(const float4*)((const float*)target + rowbase + i0);
-                    const float4 b = *(const float4*)((const float*)target + rowbase + i0 + 4);
-                    x[l][0] = a.x; x[l][1] = a.y; x[l][2] = a.z; x[l][3] = a.w;
-                    x[l][4] = b.x; x[l][5] = b.y; x[l][6] = b.z; x[l][7] = b.w;
+                    const uint4 a = load_stream16((const float*)target + rowbase + i0);
+                    const uint4 b = load_stream16((const float*)target + rowbase + i0 + 4);
+                    x[l][0] = __uint_as_float(a.x); x[l][1] = __uint_as_float(a.y);
+                    x[l][2] = __uint_as_float(a.z); x[l][3] = __uint_as_float(a.w);
+                    x[l][4] = __uint_as_float(b.x); x[l][5] = __uint_as_float(b.y);
+                    x[l][6] = __uint_as_float(b.z); x[l][7] = __uint_as_float(b.w);
                 }
             } else {
 #pragma unroll
@@ -102,29 +100,70 @@ __global__ __launch_bounds__(kBlock) void target_partials(const void* __restrict
             }
         }
     }
+    m_out = m;
+    sum_out = sum;
+}
+
+template <int DT, bool VEC>
+__global__ __launch_bounds__(kBlock) void target_partials(const void* __restrict__ target, int V, int B, int nrows,
+                                                          long long chunk, int P, float invT,
+                                                          const int32_t* __restrict__ n_nodes,
+                                                          float* __restrict__ tm, double* __restrict__ ts,
+                                                          int* __restrict__ tf, uint32_t* __restrict__ counters) {
+    const int g = blockIdx.x;
+    const int tid = threadIdx.x;
+    const long long N = (long long)nrows * V;
+    const long long e0 = (long long)g * chunk;
+    if (e0 >= N) return;
+    const long long e1 = min(e0 + chunk, N);
+    const int t0 = (int)(e0 / V), t1 = (int)((e1 - 1) / V);
+    const float c = invT * 1.4426950408889634f;  // invT * log2(e)
     __shared__ float s_m[kBlock / kWave];
     __shared__ double s_s[kBlock / kWave];
     const int wave = tid / kWave, lane = tid % kWave;
-    const float wm = wave_max(m);
-    const double contrib = (m == -INFINITY) ? 0.0 : sum * (double)exp2f((m - wm) * c);
-    const double wsum = wave_sum(contrib);
-    if (lane == 0) {
-        s_m[wave] = wm;
-        s_s[wave] = wsum;
-    }
-    __syncthreads();
-    if (tid == 0) {
-        float M = s_m[0];
-        for (int w = 1; w < kBlock / kWave; ++w) M = fmaxf(M, s_m[w]);
-        double tot = 0.0;
-        for (int w = 0; w < kBlock / kWave; ++w)
-            if (s_m[w] != -INFINITY) tot += s_s[w] * (double)exp2f((s_m[w] - M) * c);
-        const size_t o = (size_t)row * S + s;
-        // partial as (max of a, sum exp(a - max a)), a = x invT; non-finite input
-        // leaves a NaN or infinite max/sum
-        tm[o] = M * invT;
-        ts[o] = tot;
-        tf[o] = (isnan(M) || M == INFINITY || !isfinite(tot)) ? 1 : 0;
+    for (int t = t0; t <= t1; ++t) {
+        const int r = t / (B + 1);
+        const int node = t % (B + 1);
+        const long long rb = (long long)t * V;
+        const int gf = (int)(rb / chunk);            // the row's first workgroup
+        const int gl = (int)((rb + V - 1) / chunk);  // and its last
+        const size_t o = (size_t)t * P;
+        if (g == gf && tid == 0) {
+            if (node == 0) counters[r] = 0u;
+            for (int q = gl - gf + 1; q < P; ++q) {
+                tm[o + q] = -INFINITY;
+                ts[o + q] = 0.0;
+                tf[o + q] = 0;
+            }
+        }
+        if (node >= n_nodes[r]) continue;  // uniform over the workgroup
+        const int lo = (int)max(e0 - rb, 0LL);
+        const int hi = (int)min(e1 - rb, (long long)V);
+        float m;
+        double sum;
+        stream_piece<DT, VEC>(target, (size_t)rb, lo, hi, c, m, sum);
+        const float wm = wave_max(m);
+        const double contrib = (m == -INFINITY) ? 0.0 : sum * (double)exp2f((m - wm) * c);
+        const double wsum = wave_sum(contrib);
+        if (lane == 0) {
+            s_m[wave] = wm;
+            s_s[wave] = wsum;
+        }
+        __syncthreads();
+        if (tid == 0) {
+            float M = s_m[0];
+            for (int w = 1; w < kBlock / kWave; ++w) M = fmaxf(M, s_m[w]);
+            double tot = 0.0;
+            for (int w = 0; w < kBlock / kWave; ++w)
+                if (s_m[w] != -INFINITY) tot += s_s[w] * (double)exp2f((s_m[w] - M) * c);
+            const size_t q = o + (size_t)(g - gf);
+            // partial as (max of a, sum exp(a - max a)), a = x invT; non-finite input
+            // leaves a NaN or infinite max/sum
+            tm[q] = M * invT;
+            ts[q] = tot;
+            tf[q] = (isnan(M) || M == INFINITY || !isfinite(tot)) ? 1 : 0;
+        }
+        __syncthreads();
     }
 }
 
@@ -784,23 +823,23 @@ hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, con
     uint32_t* counters = (uint32_t*)(ws + w.counter);
     const bool vec8 = (c.dtype == TSB_BF16) ? (c.V % 8 == 0 && ((uintptr_t)target & 15) == 0)
                                             : (c.V % 4 == 0 && ((uintptr_t)target & 15) == 0);
-    const dim3 grid4(g.S4, c.R * (c.B + 1));
+    const int nrows = c.R * (c.B + 1);
     hipError_t e = hook_before(TSB_KERNEL_TARGET_PARTIALS, st);
     if (e != hipSuccess) return e;
     if (c.dtype == TSB_BF16) {
         if (vec8)
-            target_partials<TSB_BF16, true><<<grid4, kBlock, 0, st>>>(target, c.V, c.B, g.seg4, g.S4, invT,
-                                                                      tree.n_nodes, tm, ts, tf, counters);
-        else
-            target_partials<TSB_BF16, false><<<grid4, kBlock, 0, st>>>(target, c.V, c.B, g.seg4, g.S4, invT,
-                                                                       tree.n_nodes, tm, ts, tf, counters);
-    } else {
-        if (vec8)
-            target_partials<TSB_F32, true><<<grid4, kBlock, 0, st>>>(target, c.V, c.B, g.seg4, g.S4, invT,
+            target_partials<TSB_BF16, true><<<g.G4, kBlock, 0, st>>>(target, c.V, c.B, nrows, g.chunk4, g.S4, invT,
                                                                      tree.n_nodes, tm, ts, tf, counters);
         else
-            target_partials<TSB_F32, false><<<grid4, kBlock, 0, st>>>(target, c.V, c.B, g.seg4, g.S4, invT,
+            target_partials<TSB_BF16, false><<<g.G4, kBlock, 0, st>>>(target, c.V, c.B, nrows, g.chunk4, g.S4, invT,
                                                                       tree.n_nodes, tm, ts, tf, counters);
+    } else {
+        if (vec8)
+            target_partials<TSB_F32, true><<<g.G4, kBlock, 0, st>>>(target, c.V, c.B, nrows, g.chunk4, g.S4, invT,
+                                                                    tree.n_nodes, tm, ts, tf, counters);
+        else
+            target_partials<TSB_F32, false><<<g.G4, kBlock, 0, st>>>(target, c.V, c.B, nrows, g.chunk4, g.S4, invT,
+                                                                     tree.n_nodes, tm, ts, tf, counters);
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;

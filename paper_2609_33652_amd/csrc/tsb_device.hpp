@@ -120,6 +120,13 @@ __device__ __forceinline__ float load_logit(const void* base, size_t i) {
         return ((const float*)base)[i];
 }
 
+// 16-byte load with the non-temporal hint, for data read exactly once.
+typedef unsigned int tsb_u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 load_stream16(const void* p) {
+    const tsb_u32x4 v = __builtin_nontemporal_load((const tsb_u32x4*)p);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // Order-preserving map of a binary32 value to uint32 (larger float -> larger
 // key); -0 is folded onto +0 so equal values give equal keys.
 __device__ __forceinline__ uint32_t ordered_bits(float x) {

@@ -17,14 +17,15 @@ constexpr int kReplayTile = 4096;    // vocabulary tile of the replay scan
 constexpr int kReplayTileOut = 64;   // candidates one (parent, tile) hands to the merge
 constexpr int kWalkGroupsMax = 128;  // workgroups per request in verification
 constexpr int kWalkTokensPerGroup = 9728;  // tokens whose binary64 (p, q) one walk workgroup holds in LDS
-constexpr int kTargetWorkgroups = 2048;
+constexpr int kTargetWorkgroups = 2048;  // target stream: 8 resident workgroups on each of 256 CUs
 constexpr int kDraftWorkgroups = 1024;   // row statistics: one resident wave of workgroups
 
 struct Geometry {
     int S1;          // workgroups per draft row (row statistics)
     int seg1;        // elements per draft segment (multiple of 8)
-    int S4;          // workgroups per target row
-    int seg4;        // elements per target segment (multiple of 8)
+    int S4;          // partial slots per target row
+    int G4;          // workgroups of the target stream
+    long long chunk4;  // logits per target-stream workgroup (multiple of 8)
     int T;           // replay tiles per row
     int G;           // workgroups per request in verification (upper bound)
 };
@@ -39,12 +40,15 @@ inline Geometry geometry(const tsb_config& c) {
     g.S1 = s1 < 1 ? 1 : (s1 > s1max ? s1max : s1);
     g.seg1 = ceil_div(ceil_div(c.V, g.S1), 8) * 8;
     g.S1 = ceil_div(c.V, g.seg1);
-    const long long trows = (long long)c.R * (c.B + 1);
-    int s4 = ceil_div(kTargetWorkgroups / 2, trows);
-    int s4max = ceil_div(c.V, 4096);
-    g.S4 = s4 < 1 ? 1 : (s4 > s4max ? s4max : s4);
-    g.seg4 = ceil_div(ceil_div(c.V, g.S4), 8) * 8;
-    g.S4 = ceil_div(c.V, g.seg4);
+    // target stream: equal chunks of the flat [R (B+1) V] array, one per
+    // resident workgroup; a row meets at most (V - 1) / chunk + 2 chunks
+    const long long n4 = (long long)c.R * (c.B + 1) * c.V;
+    long long g4 = (n4 + 4095) / 4096;
+    if (g4 > kTargetWorkgroups) g4 = kTargetWorkgroups;
+    if (g4 < 1) g4 = 1;
+    g.chunk4 = ((n4 + g4 - 1) / g4 + 7) / 8 * 8;
+    g.G4 = (int)((n4 + g.chunk4 - 1) / g.chunk4);
+    g.S4 = (int)((c.V - 1) / g.chunk4) + 2;
     g.T = ceil_div(c.V, kReplayTile);
     // walk: about one workgroup per compute unit over the batch, and enough
     // per request that a slice fits the LDS cache
