@@ -5,7 +5,7 @@
 //   target_partials  grid (segment, request x node): one streaming read of
 //                    every target row of the tree; online max and sum of
 //                    exp per segment (binary32 terms, binary64 per lane).
-//   verify_walk      cooperative grid (G workgroups per request). All G
+//   verify_walk      resident grid (G workgroups per request). All G
 //                    workgroups of a request replay the same scalar walk;
 //                    every vocabulary-wide reduction of the walk (residual
 //                    mass after a rejection, the bonus draw) is split over
@@ -20,6 +20,8 @@
 // argmax_v ln max(p_v - C q_v, 0) + G_v (Gumbel-max of the residual; C = 0
 // at an accepted leaf).
 #include <math.h>
+
+#include <atomic>
 
 #include "tsb_device.hpp"
 #include "tsb_kernels.hpp"
@@ -434,7 +436,8 @@ __device__ void bonus_from_p(const WalkArgs& A, bool vec, const WalkSlice& S, si
 
 // Exchange among the G workgroups of a request: each contributes up to four
 // binary64 partials (and optionally a (key, token) pair); everyone gets the
-// sums, added in workgroup order, and the best pair.
+// sums (a fixed reduction tree over the workgroups, so every run adds in the
+// same order) and the best pair.
 constexpr int kExVals = 4;
 
 struct Exchange {
@@ -456,29 +459,65 @@ struct Exchange {
         }
         ++nb;
         request_barrier(&A->counters[r], nb * (uint32_t)G, &timeout);
+        // wave 0 reads the G slots in parallel (lane h: slots h and h + 64),
+        // reduces them in a fixed order and hands the result to the others
+        __shared__ double s_tot[kExVals];
+        __shared__ float s_bk;
+        __shared__ int s_bi;
+        if (threadIdx.x < kWave) {
+            const int lane = threadIdx.x;
+            double v[NV];
+            float kb = -INFINITY;
+            int ib = 0x7FFFFFFF;
 #pragma unroll
-        for (int i = 0; i < NV; ++i) tot[i] = 0.0;
-        float kb = -INFINITY;
-        int ib = 0x7FFFFFFF;
-        for (int h = 0; h < G; ++h) {
-            const int sl = (r * 2 + ((nb - 1) & 1)) * kWalkGroupsMax + h;
+            for (int i = 0; i < NV; ++i) v[i] = 0.0;
 #pragma unroll
-            for (int i = 0; i < NV; ++i)
-                tot[i] += __hip_atomic_load(&A->zpart[(size_t)sl * kExVals + i], __ATOMIC_RELAXED,
-                                            __HIP_MEMORY_SCOPE_AGENT);
-            if (fk) {
-                const float k = __hip_atomic_load(&A->bkey[sl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                const int i = __hip_atomic_load(&A->bidx[sl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                if (k > kb || (k == kb && i < ib)) {
-                    kb = k;
-                    ib = i;
+            for (int half = 0; half < kWalkGroupsMax / kWave; ++half) {
+                const int h = lane + half * kWave;
+                if (h < G) {
+                    const int sl = (r * 2 + ((nb - 1) & 1)) * kWalkGroupsMax + h;
+#pragma unroll
+                    for (int i = 0; i < NV; ++i)
+                        v[i] += __hip_atomic_load(&A->zpart[(size_t)sl * kExVals + i], __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT);
+                    if (fk) {
+                        const float k = __hip_atomic_load(&A->bkey[sl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        const int ix = __hip_atomic_load(&A->bidx[sl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        if (k > kb || (k == kb && ix < ib)) {
+                            kb = k;
+                            ib = ix;
+                        }
+                    }
                 }
             }
+#pragma unroll
+            for (int i = 0; i < NV; ++i) v[i] = wave_sum(v[i]);
+            if (fk) {
+#pragma unroll
+                for (int off = 32; off > 0; off >>= 1) {
+                    const float ok = __shfl_xor(kb, off, kWave);
+                    const int oi = __shfl_xor(ib, off, kWave);
+                    if (ok > kb || (ok == kb && oi < ib)) {
+                        kb = ok;
+                        ib = oi;
+                    }
+                }
+            }
+            if (lane == 0) {
+#pragma unroll
+                for (int i = 0; i < NV; ++i) s_tot[i] = v[i];
+                s_bk = kb;
+                s_bi = ib;
+            }
         }
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < NV; ++i) tot[i] = s_tot[i];
         if (fk) {
-            *fk = kb;
-            *fi = ib;
+            *fk = s_bk;
+            *fi = s_bi;
         }
+        __syncthreads();  // s_tot is rewritten by the next exchange
     }
     __device__ double sum(double part) {
         double p[1] = {part}, t[1];
@@ -508,28 +547,26 @@ template <int DT>
 __device__ void fill_pass(const WalkArgs& A, bool vec, const WalkSlice& S, bool cached, size_t trow, size_t drow,
                           double L0, double Ld, const double* et, double (&out)[4]) {
     double sp = 0.0, pa = 0.0, qa = 0.0, band = 0.0;
-    for (int c = 0; c < S.nchunks; ++c) {
-        const int c0 = S.v0 + c * kWalkCache;
-        const int n = min(kWalkCache, S.v1 - c0);
-        // one group of four tokens per iteration; the next group's loads are
-        // issued before this group's arithmetic
-        int i = (int)threadIdx.x * 4;
-        float at[4], ad[4];
-        {
+    if (cached) {
+        // the whole slice fits the LDS cache: every load of the thread is
+        // issued before any arithmetic (one memory latency per pass)
+        constexpr int kGroups = (kWalkCache + 4 * kWalkThreads - 1) / (4 * kWalkThreads);
+        const int n = S.v1 - S.v0;
+        float at[kGroups][4], ad[kGroups][4];
+#pragma unroll
+        for (int k = 0; k < kGroups; ++k) {
+            const int i = (k * kWalkThreads + (int)threadIdx.x) * 4;
             const int valid = max(0, min(4, n - i));
-            load4_scaled<DT>(A.target, trow + c0 + (valid ? i : 0), valid, vec, A.invT, at);
-            load4_scaled<DT>(A.draft, drow + c0 + (valid ? i : 0), valid, vec, A.invT, ad);
+            load4_scaled<DT>(A.target, trow + S.v0 + (valid ? i : 0), valid, vec, A.invT, at[k]);
+            load4_scaled<DT>(A.draft, drow + S.v0 + (valid ? i : 0), valid, vec, A.invT, ad[k]);
         }
-        for (; i < n; i += 4 * kWalkThreads) {
-            const int inext = i + 4 * kWalkThreads;
-            float nt[4], nd[4];
-            const int vn = max(0, min(4, n - inext));
-            load4_scaled<DT>(A.target, trow + c0 + (vn ? inext : 0), vn, vec, A.invT, nt);
-            load4_scaled<DT>(A.draft, drow + c0 + (vn ? inext : 0), vn, vec, A.invT, nd);
+#pragma unroll
+        for (int k = 0; k < kGroups; ++k) {
+            const int i = (k * kWalkThreads + (int)threadIdx.x) * 4;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const double pt = at[e] > -INFINITY ? exp64((double)at[e] - L0, et) : 0.0;
-                const double qd = ad[e] > -INFINITY ? exp64((double)ad[e] - Ld, et) : 0.0;
+                const double pt = at[k][e] > -INFINITY ? exp64((double)at[k][e] - L0, et) : 0.0;
+                const double qd = ad[k][e] > -INFINITY ? exp64((double)ad[k][e] - Ld, et) : 0.0;
                 sp += pt;
                 if (pt > qd * (1.0 + 1e-5)) {
                     pa += pt;
@@ -537,15 +574,48 @@ __device__ void fill_pass(const WalkArgs& A, bool vec, const WalkSlice& S, bool 
                 } else if (pt >= qd * (1.0 - 1e-5) && pt > 0.0) {
                     band += 1.0;
                 }
-                if (cached && i + e < n) {
+                if (i + e < n) {
                     S.p[i + e] = pt;
                     S.q[i + e] = qd;
                 }
             }
+        }
+    } else {
+        for (int c = 0; c < S.nchunks; ++c) {
+            const int c0 = S.v0 + c * kWalkCache;
+            const int n = min(kWalkCache, S.v1 - c0);
+            // one group of four tokens per iteration; the next group's loads are
+            // issued before this group's arithmetic
+            int i = (int)threadIdx.x * 4;
+            float at[4], ad[4];
+            {
+                const int valid = max(0, min(4, n - i));
+                load4_scaled<DT>(A.target, trow + c0 + (valid ? i : 0), valid, vec, A.invT, at);
+                load4_scaled<DT>(A.draft, drow + c0 + (valid ? i : 0), valid, vec, A.invT, ad);
+            }
+            for (; i < n; i += 4 * kWalkThreads) {
+                const int inext = i + 4 * kWalkThreads;
+                float nt[4], nd[4];
+                const int vn = max(0, min(4, n - inext));
+                load4_scaled<DT>(A.target, trow + c0 + (vn ? inext : 0), vn, vec, A.invT, nt);
+                load4_scaled<DT>(A.draft, drow + c0 + (vn ? inext : 0), vn, vec, A.invT, nd);
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                at[e] = nt[e];
-                ad[e] = nd[e];
+                for (int e = 0; e < 4; ++e) {
+                    const double pt = at[e] > -INFINITY ? exp64((double)at[e] - L0, et) : 0.0;
+                    const double qd = ad[e] > -INFINITY ? exp64((double)ad[e] - Ld, et) : 0.0;
+                    sp += pt;
+                    if (pt > qd * (1.0 + 1e-5)) {
+                        pa += pt;
+                        qa += qd;
+                    } else if (pt >= qd * (1.0 - 1e-5) && pt > 0.0) {
+                        band += 1.0;
+                    }
+                }
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    at[e] = nt[e];
+                    ad[e] = nd[e];
+                }
             }
         }
     }
@@ -812,6 +882,35 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
 }
 
 // ------------------------------------------------------------------ launch
+// Workgroups of the walk that are resident at once on the current device
+// (one per CU: the LDS cache fills a CU). Every launch of the walk stays
+// within this, in order of requests, so all workgroups of a launch run
+// together and their barriers complete; the bounded spin of the barrier
+// turns a device shared with other work (workgroups kept waiting) into
+// TSB_REQ_WALK_TIMEOUT instead of a hang. Queried once per (device,
+// kernel instance).
+static hipError_t walk_capacity(const void* fn, int dt, int vec, size_t lds, int* cap) {
+    constexpr int kDevs = 64;
+    static std::atomic<int> cached[kDevs][2][2];
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev >= 0 && dev < kDevs) {
+        const int v = cached[dev][dt][vec].load(std::memory_order_relaxed);
+        if (v > 0) {
+            *cap = v;
+            return hipSuccess;
+        }
+    }
+    int cus = 0, per_cu = 0;
+    if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess) return e;
+    if ((e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) != hipSuccess) return e;
+    if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kWalkThreads, lds)) != hipSuccess) return e;
+    *cap = per_cu * cus;
+    if (dev >= 0 && dev < kDevs && *cap > 0) cached[dev][dt][vec].store(*cap, std::memory_order_relaxed);
+    return hipSuccess;
+}
+
 hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, const double* draft_lse,
                          const void* target, const tsb_tree& tree, const int32_t* node_tok, uint32_t step,
                          const tsb_verdict& out, char* ws, hipStream_t st) {
@@ -876,17 +975,9 @@ hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, con
         fn = vec4 ? (const void*)verify_walk<TSB_F32, true> : (const void*)verify_walk<TSB_F32, false>;
 
     const size_t lds = 2 * (size_t)kWalkCache * sizeof(double);
-    int dev = 0, cus = 0, per_cu = 0;
-    e = hipGetDevice(&dev);
-    if (e != hipSuccess) return e;
-    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-    if (e != hipSuccess) return e;
-    e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kWalkThreads, lds);
-    if (e != hipSuccess) return e;
-    const int cap = per_cu * cus;
-    if (cap < 1) return hipErrorCooperativeLaunchTooLarge;
+    int cap = 0;
+    if ((e = walk_capacity(fn, c.dtype == TSB_BF16 ? 1 : 0, vec4 ? 1 : 0, lds, &cap)) != hipSuccess) return e;
+    if (cap < 1) return hipErrorLaunchOutOfResources;
     int G = g.G;
     if (G * c.R > cap) G = cap / c.R > 0 ? cap / c.R : 1;
     const int chunk = cap / G;
@@ -895,7 +986,7 @@ hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, con
         A.r0 = r0;
         const int rc = min(chunk, c.R - r0);
         void* args[] = {&A};
-        e = hipLaunchCooperativeKernel(fn, dim3(G, rc), dim3(kWalkThreads), args, (unsigned)lds, st);
+        e = hipLaunchKernel(fn, dim3(G, rc), dim3(kWalkThreads), args, lds, st);
         if (e != hipSuccess) return e;
     }
     return hook_after(TSB_KERNEL_VERIFY_WALK, st);
