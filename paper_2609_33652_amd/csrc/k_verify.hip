@@ -207,12 +207,18 @@ __device__ double target_lse(const WalkArgs& A, int r, int node, int* bad) {
 
 // Per-request barrier over the G workgroups of a request: monotone counter,
 // bounded spin (a wait that exceeds the limit sets *timeout and proceeds).
+// Only the exchange slots cross workgroups, and they are written and read
+// with agent-scope atomics (coherent without L2 maintenance), so the
+// barrier needs no cache writeback or invalidation: the slot stores have
+// completed (s_waitcnt vmcnt(0)) before the counter is incremented, and a
+// reader issues its slot loads only after it has seen the count.
 __device__ void request_barrier(uint32_t* counter, uint32_t target, int* timeout) {
     __syncthreads();
     if (threadIdx.x == 0) {
-        __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this thread's slot stores are done
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         uint32_t spins = 0;
-        // relaxed polls (no cache invalidation per poll), one acquire after
         while (__hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
             __builtin_amdgcn_s_sleep(2);
             if (++spins > (1u << 23)) {
@@ -220,7 +226,7 @@ __device__ void request_barrier(uint32_t* counter, uint32_t target, int* timeout
                 break;
             }
         }
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
     }
     __syncthreads();
 }
@@ -453,9 +459,11 @@ struct Exchange {
         const int slot = (r * 2 + (nb & 1)) * kWalkGroupsMax + g;
         if (threadIdx.x == 0) {
 #pragma unroll
-            for (int i = 0; i < NV; ++i) A->zpart[(size_t)slot * kExVals + i] = part[i];
-            A->bkey[slot] = bk;
-            A->bidx[slot] = bi;
+            for (int i = 0; i < NV; ++i)
+                __hip_atomic_store(&A->zpart[(size_t)slot * kExVals + i], part[i], __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&A->bkey[slot], bk, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&A->bidx[slot], bi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         ++nb;
         request_barrier(&A->counters[r], nb * (uint32_t)G, &timeout);
