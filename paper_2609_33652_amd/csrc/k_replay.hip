@@ -6,15 +6,16 @@
 //   replay_prep   one workgroup: flat list of the parents of the batch
 //                 (request-major, BFS order, so a depth's parents are
 //                 contiguous).
-//   replay_scan   grid (vocabulary tile, 64 rows); a row takes a contiguous
-//                 chunk of the parent list and stages the tile of draft row d
-//                 once for consecutive parents of the same (request, depth)
-//                 (they share q_d). Per parent, tokens whose key cannot reach the
+//   replay_scan   one wave per (parent, vocabulary tile) item, dealt
+//                 grid-stride over a persistent grid (parents of one (request,
+//                 depth) are adjacent, so their tiles of draft row d meet in
+//                 cache). Per item, tokens whose key cannot reach the
 //                 parent's threshold (a lower bound of its m-th key, taken
-//                 from its planning candidates) are skipped before any
-//                 random number is drawn; the survivors are compacted per
-//                 wave and only they pay for Philox and two logarithms. Each
-//                 (parent, tile) emits its best m keys.
+//                 from its planning candidates) are skipped before any random
+//                 number is drawn; the survivors are compacted within the
+//                 wave and only they pay for Philox and two logarithms; the
+//                 wave keeps the parent's m best keys of the tile in a sorted
+//                 wave-wide list.
 //   replay_merge  one wave per parent: merge the per-tile lists, keep the m
 //                 best (key desc, token asc) in slot order.
 //
@@ -23,25 +24,18 @@
 // row, so the order is that of a_v + G_v).
 #include <math.h>
 
+#include <algorithm>
+
 #include "tsb_device.hpp"
 #include "tsb_kernels.hpp"
 
 namespace tsb {
 
 constexpr int kTileGroups = kReplayTile / 4;  // groups of four tokens per tile
-constexpr int kTileOut = kReplayTileOut;       // candidates a (parent, tile) may hand to the merge
-
-struct ReplayShared {
-    float b[kReplayTile];                         // fl32(a_v - c_d) of the tile
-    int queue[kBlock / kWave][kTileGroups / (kBlock / kWave)];
-    float ckey[kReplayTile];                      // candidates of the current parent
-    int cidx[kReplayTile];
-    int ccount;
-    float thr;
-};
+constexpr int kScanWaves = kBlock / kWave;
+constexpr int kScanWorkgroups = 1536;  // resident at 6 waves per SIMD
 
 constexpr int kPrepThreads = 1024;
-constexpr int kScanRows = 256;  // workgroup rows of the scan grid (each takes a chunk of parents)
 
 // Flat list of every node with children, request-major, BFS order within a
 // request (so parents of one (request, depth) are contiguous): plist[i] =
@@ -125,178 +119,117 @@ __global__ __launch_bounds__(kBlock) void replay_threshold(const void* __restric
     if (lane < K && above == m - 1) thr[node] = prune ? kj : -INFINITY;
 }
 
+// Four logits of the draft row as b = fl32(a - c_d); positions at or past
+// `tn` (relative to the tile) read as -inf.
+template <int DT, bool VEC>
+__device__ __forceinline__ void load_b4(const void* __restrict__ draft, size_t base, int e0, int tn, float invT,
+                                        float cd, float b[4]) {
+    float x[4];
+    if (VEC && e0 + 4 <= tn) {
+        if (DT == TSB_BF16) {
+            const uint2 raw = *(const uint2*)((const uint16_t*)draft + base + e0);
+            x[0] = __uint_as_float(raw.x << 16);
+            x[1] = __uint_as_float(raw.x & 0xFFFF0000u);
+            x[2] = __uint_as_float(raw.y << 16);
+            x[3] = __uint_as_float(raw.y & 0xFFFF0000u);
+        } else {
+            const float4 a = *(const float4*)((const float*)draft + base + e0);
+            x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[e] = (e0 + e < tn) ? load_logit<DT>(draft, base + e0 + e) : -INFINITY;
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) b[e] = (e0 + e < tn) ? x[e] * invT - cd : -INFINITY;
+}
+
 template <int DT, bool VEC>
 __global__ __launch_bounds__(kBlock) void replay_scan(const void* __restrict__ draft, int V, int D, int B, int K,
                                                       int T, float invT, const int32_t* __restrict__ topk_tok,
                                                       tsb_tree tree, const int* __restrict__ plist,
                                                       const int* __restrict__ ptotal, const float* __restrict__ thr_in,
                                                       uint32_t k0, uint32_t k1, uint32_t step,
-                                                      float* __restrict__ out_key, int* __restrict__ out_idx,
-                                                      int* __restrict__ out_cnt) {
-    __shared__ ReplayShared sh;
-    const int t = blockIdx.x;
-    const int tid = threadIdx.x;
-    const int wave = tid / kWave, lane = tid % kWave;
-    const int total = ptotal[0];
-    const int chunk = (total + kScanRows - 1) / kScanRows;
-    const int p0 = blockIdx.y * chunk;
-    const int p1 = min(total, p0 + chunk);
-    if (p0 >= p1) return;
-    const int t0 = t * kReplayTile;
-    const int tn = min(kReplayTile, V - t0);
-    const uint32_t blk0 = (uint32_t)(t0 >> 2);
-    int staged = -1;  // r * D + d of the staged tile
-
-    for (int pi = p0; pi < p1; ++pi) {
+                                                      uint64_t* __restrict__ out_cand, int* __restrict__ out_cnt) {
+    __shared__ int s_queue[kScanWaves][kTileGroups];  // surviving groups, per wave
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    int* queue = s_queue[wave];
+    const long long items = (long long)ptotal[0] * T;
+    const long long nw = (long long)gridDim.x * kScanWaves;
+    for (long long it = (long long)blockIdx.x * kScanWaves + wave; it < items; it += nw) {
+        const int pi = (int)(it / T);
+        const int t = (int)(it - (long long)pi * T);
         const int node = plist[pi];
         const int r = node / (B + 1);
-        const int u = node % (B + 1);
-        const size_t tb = (size_t)r * (B + 1);
-        const int d = tree.depth[tb + u];
-        const int m = tree.n_children[tb + u];
+        const int u = node - r * (B + 1);
+        const int d = tree.depth[node];
+        const int m = tree.n_children[node];
         const size_t rowbase = ((size_t)r * D + d) * (size_t)V;
-        const int tok0 = topk_tok[((size_t)r * D + d) * K];
-        const float cd = load_logit<DT>(draft, rowbase + tok0) * invT;
-        if (staged != r * D + d) {
-            // stage b_v = fl32(a_v - c_d) for the tile
-            __syncthreads();
-            for (int g = tid; g < kTileGroups; g += kBlock) {
-                const int e0 = g * 4;
-                float x[4];
-                if (VEC && e0 + 4 <= tn) {
-                    if (DT == TSB_BF16) {
-                        const uint2 raw = *(const uint2*)((const uint16_t*)draft + rowbase + t0 + e0);
-                        x[0] = __uint_as_float(raw.x << 16);
-                        x[1] = __uint_as_float(raw.x & 0xFFFF0000u);
-                        x[2] = __uint_as_float(raw.y << 16);
-                        x[3] = __uint_as_float(raw.y & 0xFFFF0000u);
-                    } else {
-                        const float4 a = *(const float4*)((const float*)draft + rowbase + t0 + e0);
-                        x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
-                    }
-                } else {
-#pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        x[e] = (e0 + e < tn) ? load_logit<DT>(draft, rowbase + t0 + e0 + e) : -INFINITY;
-                }
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const float a = x[e] * invT;
-                    sh.b[e0 + e] = (e0 + e < tn) ? a - cd : -INFINITY;
-                }
-            }
-            __syncthreads();
-            staged = r * D + d;
-        }
+        const float cd = load_logit<DT>(draft, rowbase + topk_tok[((size_t)r * D + d) * K]) * invT;
+        const float thr = thr_in[node];
+        const float bound = thr - kGumbelMaxBound;
+        const int t0 = t * kReplayTile;
+        const int tn = min(kReplayTile, V - t0);
+        const size_t tbase = rowbase + t0;
 
+        // compact the groups with a token that can still reach thr (a quarter
+        // of the tile's loads in flight at a time)
+        constexpr int kPer = kTileGroups / kWave;  // groups per lane
+        constexpr int kBatch = kPer / 4;
+        int qn = 0;
+#pragma unroll 1
+        for (int k0b = 0; k0b < kPer; k0b += kBatch) {
+            float bq[kBatch][4];
+#pragma unroll
+            for (int k = 0; k < kBatch; ++k)
+                load_b4<DT, VEC>(draft, tbase, ((k0b + k) * kWave + lane) * 4, tn, invT, cd, bq[k]);
+#pragma unroll
+            for (int k = 0; k < kBatch; ++k) {
+                const float mx = fmaxf(fmaxf(bq[k][0], bq[k][1]), fmaxf(bq[k][2], bq[k][3]));
+                const bool live = mx >= bound && mx > -INFINITY;
+                const uint64_t bal = __ballot(live);
+                if (live) queue[qn + __popcll(bal & ((1ull << lane) - 1ull))] = (k0b + k) * kWave + lane;
+                qn += __popcll(bal);
+            }
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+        // Philox and the keys for the survivors; the m best keys >= thr
         RngKey key;
         key.k0 = k0;
         key.k1 = k1;
         key.request = (uint32_t)r;
         key.step = step;
-        if (tid == 0) {
-            sh.thr = thr_in[node];
-            sh.ccount = 0;
-        }
-        __syncthreads();
-        const float thr = sh.thr;
-        const float bound = thr - kGumbelMaxBound;
-
-        // compact surviving groups of this wave
-        int qn = 0;
-        const int gpw = kTileGroups / (kBlock / kWave);  // groups per wave
-        for (int base = 0; base < gpw; base += kWave) {
-            const int gl = wave * gpw + base + lane;
-            const float* bb = &sh.b[gl * 4];
-            const bool live = (bb[0] >= bound) | (bb[1] >= bound) | (bb[2] >= bound) | (bb[3] >= bound);
-            const uint64_t bal = __ballot(live);
-            const int pos = qn + __popcll(bal & ((1ull << lane) - 1ull));
-            if (live) sh.queue[wave][pos] = gl;
-            qn += __popcll(bal);
-        }
-        __syncthreads();
-        for (int q = lane; q < qn; q += kWave) {
-            const int gl = sh.queue[wave][q];
+        const uint32_t blk0 = (uint32_t)(t0 >> 2);
+        WaveTopList top;
+        top.init(m);
+        for (int base = 0; base < qn; base += kWave) {
+            const int q = base + lane;
+            const bool valid = q < qn;
+            const int gl = valid ? queue[q] : 0;
+            float bv[4];
+            load_b4<DT, VEC>(draft, tbase, gl * 4, valid ? tn : 0, invT, cd, bv);
             const uint4 w = rng_block(key, (uint32_t)u, kStreamReplay, blk0 + (uint32_t)gl);
             const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const float bv = sh.b[gl * 4 + e];
-                if (bv >= bound && bv > -INFINITY) {
-                    const float kv = bv + gumbel_f32(ws[e]);
-                    if (kv >= thr) {
-                        const int slot = atomicAdd(&sh.ccount, 1);
-                        sh.ckey[slot] = kv;
-                        sh.cidx[slot] = t0 + gl * 4 + e;
-                    }
-                }
+                const bool in = bv[e] >= bound && bv[e] > -INFINITY;
+                const float kv = in ? bv[e] + gumbel_f32(ws[e]) : -INFINITY;
+                top.offer(cand_key(kv, (uint32_t)(t0 + gl * 4 + e)), in && kv >= thr);
             }
         }
-        __syncthreads();
-
-        // candidates of this tile (at most kTileOut; beyond that the tile's best
-        // m are selected here); the merge settles the order
-        const int c = sh.ccount;
-        const size_t o = (tb + u) * (size_t)T + t;
-        if (c <= kTileOut) {
-            for (int j = tid; j < c; j += kBlock) {
-                out_key[o * kTileOut + j] = sh.ckey[j];
-                out_idx[o * kTileOut + j] = sh.cidx[j];
-            }
-        } else {
-            for (int j = 0; j < m; ++j) {
-                float bk = -INFINITY;
-                int bi = 0x7FFFFFFF, bs = -1;
-                for (int i = tid; i < c; i += kBlock) {
-                    if (sh.cidx[i] >= 0 && (bs < 0 || key_better(sh.ckey[i], sh.cidx[i], bk, bi))) {
-                        bk = sh.ckey[i];
-                        bi = sh.cidx[i];
-                        bs = i;
-                    }
-                }
-#pragma unroll
-                for (int off = 32; off > 0; off >>= 1) {
-                    const float ok = __shfl_xor(bk, off, kWave);
-                    const int oi = __shfl_xor(bi, off, kWave);
-                    const int os = __shfl_xor(bs, off, kWave);
-                    if (os >= 0 && (bs < 0 || key_better(ok, oi, bk, bi))) {
-                        bk = ok;
-                        bi = oi;
-                        bs = os;
-                    }
-                }
-                __shared__ float wk[kBlock / kWave];
-                __shared__ int wi[kBlock / kWave], wsl[kBlock / kWave];
-                if (lane == 0) {
-                    wk[wave] = bk;
-                    wi[wave] = bi;
-                    wsl[wave] = bs;
-                }
-                __syncthreads();
-                if (tid == 0) {
-                    float fk = wk[0];
-                    int fi = wi[0], fs = wsl[0];
-                    for (int w2 = 1; w2 < kBlock / kWave; ++w2)
-                        if (wsl[w2] >= 0 && (fs < 0 || key_better(wk[w2], wi[w2], fk, fi))) {
-                            fk = wk[w2];
-                            fi = wi[w2];
-                            fs = wsl[w2];
-                        }
-                    out_key[o * kTileOut + j] = fk;
-                    out_idx[o * kTileOut + j] = fi;
-                    sh.cidx[fs] = -1;  // taken
-                }
-                __syncthreads();
-            }
-        }
-        if (tid == 0) out_cnt[o] = c <= kTileOut ? c : m;
-        __syncthreads();
+        const size_t o = (size_t)node * (size_t)T + t;
+        const int cnt = __popcll(__ballot(lane < m && top.v != 0));
+        if (lane < cnt) out_cand[o * TSB_MAX_K + lane] = top.v;
+        if (lane == 0) out_cnt[o] = cnt;
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");  // the queue is rewritten by the next item
     }
 }
 
 __global__ __launch_bounds__(kWave) void replay_merge(int B, int K, int T, tsb_tree tree,
-                                                      const float* __restrict__ ck, const int* __restrict__ ci,
-                                                      const int* __restrict__ cc, int32_t* __restrict__ node_tok) {
+                                                      const uint64_t* __restrict__ cand, const int* __restrict__ cc,
+                                                      int32_t* __restrict__ node_tok) {
     const int r = blockIdx.y;
     const int u = blockIdx.x;
     const int lane = threadIdx.x;
@@ -311,14 +244,14 @@ __global__ __launch_bounds__(kWave) void replay_merge(int B, int K, int T, tsb_t
     WaveTopList top;
     top.init(m);
     const size_t o = (tb + u) * (size_t)T;
-    for (int t = 0; t < T; ++t) {
-        const int c = cc[o + t];
-        for (int base = 0; base < c; base += kWave) {
-            const int j = base + lane;
-            uint64_t k = 0;
-            if (j < c) k = cand_key(ck[(o + t) * kTileOut + j], (uint32_t)ci[(o + t) * kTileOut + j]);
-            top.offer(k, j < c);
-        }
+    // the tiles' lists (at most m entries each), all loads of a batch in flight together
+    const int ne = T * m;
+    for (int base = 0; base < ne; base += kWave) {
+        const int i = base + lane;
+        const int tt = i / m, j = i - tt * m;
+        uint64_t k = 0;
+        if (i < ne && j < cc[o + tt]) k = cand[(o + tt) * TSB_MAX_K + j];
+        top.offer(k, k != 0);
     }
     if (lane < m) node_tok[tb + tree.first_child[tb + u] + lane] = (int32_t)cand_id(top.v);
 }
@@ -327,8 +260,7 @@ hipError_t launch_replay(const tsb_config& c, float invT, const void* draft, con
                          const tsb_tree& tree, uint32_t step, int32_t* node_tok, char* ws, hipStream_t st) {
     const Geometry g = geometry(c);
     const ReplayWs w = replay_ws(c);
-    float* ck = (float*)(ws + w.key);
-    int* ci = (int*)(ws + w.idx);
+    uint64_t* cand = (uint64_t*)(ws + w.cand);
     int* cc = (int*)(ws + w.cnt);
     int* plist = (int*)(ws + w.plist);
     int* ptotal = (int*)(ws + w.ptotal);
@@ -348,28 +280,29 @@ hipError_t launch_replay(const tsb_config& c, float invT, const void* draft, con
         replay_threshold<TSB_F32><<<nthr, kBlock, 0, st>>>(draft, c.R, c.V, c.D, c.B, c.K, invT, topk_tok, tree, k0,
                                                            k1, step, prune, thr);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    const dim3 grid(g.T, kScanRows);
+    // a persistent grid: the item count is only known on the device
+    const long long max_items = (long long)c.R * c.B * g.T;
+    const int grid = (int)std::max<long long>(1, std::min<long long>(kScanWorkgroups, (max_items + kScanWaves - 1) / kScanWaves));
     if (c.dtype == TSB_BF16) {
         if (vec)
             replay_scan<TSB_BF16, true><<<grid, kBlock, 0, st>>>(draft, c.V, c.D, c.B, c.K, g.T, invT, topk_tok, tree,
-                                                                 plist, ptotal, thr, k0, k1, step, ck, ci, cc);
+                                                                 plist, ptotal, thr, k0, k1, step, cand, cc);
         else
             replay_scan<TSB_BF16, false><<<grid, kBlock, 0, st>>>(draft, c.V, c.D, c.B, c.K, g.T, invT, topk_tok,
-                                                                  tree, plist, ptotal, thr, k0, k1, step, ck, ci,
-                                                                  cc);
+                                                                  tree, plist, ptotal, thr, k0, k1, step, cand, cc);
     } else {
         if (vec)
             replay_scan<TSB_F32, true><<<grid, kBlock, 0, st>>>(draft, c.V, c.D, c.B, c.K, g.T, invT, topk_tok, tree,
-                                                                plist, ptotal, thr, k0, k1, step, ck, ci, cc);
+                                                                plist, ptotal, thr, k0, k1, step, cand, cc);
         else
             replay_scan<TSB_F32, false><<<grid, kBlock, 0, st>>>(draft, c.V, c.D, c.B, c.K, g.T, invT, topk_tok, tree,
-                                                                 plist, ptotal, thr, k0, k1, step, ck, ci, cc);
+                                                                 plist, ptotal, thr, k0, k1, step, cand, cc);
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     if ((e = hook_after(TSB_KERNEL_REPLAY_SCAN, st)) != hipSuccess) return e;
     if ((e = hook_before(TSB_KERNEL_REPLAY_MERGE, st)) != hipSuccess) return e;
-    replay_merge<<<dim3(c.B + 1, c.R), kWave, 0, st>>>(c.B, c.K, g.T, tree, ck, ci, cc, node_tok);
+    replay_merge<<<dim3(c.B + 1, c.R), kWave, 0, st>>>(c.B, c.K, g.T, tree, cand, cc, node_tok);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     return hook_after(TSB_KERNEL_REPLAY_MERGE, st);

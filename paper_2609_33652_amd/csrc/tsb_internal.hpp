@@ -14,7 +14,6 @@ enum : uint32_t { kStreamReplay = 0, kStreamAccept = 1, kStreamBonus = 2 };
 
 constexpr int kBlock = 256;          // threads per workgroup of the streaming kernels
 constexpr int kReplayTile = 4096;    // vocabulary tile of the replay scan
-constexpr int kReplayTileOut = 64;   // candidates one (parent, tile) hands to the merge
 constexpr int kWalkGroupsMax = 128;  // workgroups per request in verification
 constexpr int kWalkTokensPerGroup = 9728;  // tokens whose binary64 (p, q) one walk workgroup holds in LDS
 constexpr int kTargetWorkgroups = 2048;  // target stream: 8 resident workgroups on each of 256 CUs
@@ -65,8 +64,8 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 struct PlanWs {  // row statistics partials
     size_t pm, ps, pk, pf, total;
 };
-struct ReplayWs {  // per (parent, tile) candidates, flat parent list, thresholds
-    size_t key, idx, cnt, plist, ptotal, thr, total;
+struct ReplayWs {  // per (parent, tile) best keys, flat parent list, thresholds
+    size_t cand, cnt, plist, ptotal, thr, total;
 };
 struct VerifyWs {  // target partials + walk exchange
     size_t tm, ts, tf, counter, zpart, bkey, bidx, total;
@@ -90,8 +89,7 @@ inline ReplayWs replay_ws(const tsb_config& c) {
     const size_t slots = (size_t)c.R * (c.B + 1) * g.T;
     ReplayWs w;
     size_t o = 0;
-    w.key = o; o = align256(o + slots * kReplayTileOut * sizeof(float));
-    w.idx = o; o = align256(o + slots * kReplayTileOut * sizeof(int32_t));
+    w.cand = o; o = align256(o + slots * TSB_MAX_K * sizeof(uint64_t));
     w.cnt = o; o = align256(o + slots * sizeof(int32_t));
     w.plist = o; o = align256(o + (size_t)c.R * (c.B + 1) * sizeof(int32_t));
     w.ptotal = o; o = align256(o + sizeof(int32_t));
