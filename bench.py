@@ -26,6 +26,24 @@ import workloads as W  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
 
+# HBM bytes per launch of target_partials at the batched workload from the
+# FETCH_SIZE / WRITE_SIZE counter passes (KiB, scaled by a plain copy of known
+# size: FETCH x2.0, WRITE x1.0), valid for the kernel source they were taken on
+TARGET_TRAFFIC = {"config": 4, "source_sha256_16": "123781335ee822c2", "fetch_kib": 309956.1, "write_kib": 267.7,
+                  "fetch_scale": 2.0, "write_scale": 1.0}
+
+
+def target_traffic(cfg_id):
+    """Counter-measured bytes per launch, or None if the kernel or workload differs from the counted one."""
+    import hashlib
+    src = open(os.path.join(ROOT, "paper_2609_33652_amd", "csrc", "k_verify.hip")).read()
+    a = src.find("// ------------------------------------------------------------------ K4")
+    b = src.find("// ------------------------------------------------------------------ K5")
+    t = TARGET_TRAFFIC
+    if cfg_id != t["config"] or a < 0 or b < 0 or hashlib.sha256(src[a:b].encode()).hexdigest()[:16] != t["source_sha256_16"]:
+        return None
+    return int(round((t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"]) * 1024))
+
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
@@ -97,6 +115,7 @@ def main():
     ap.add_argument("--cpu-requests", type=int, default=None, help="oracle request-steps in the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown-steps", type=int, default=20)
+    ap.add_argument("--sample", type=int, default=8, help="time the target kernel on every n-th timed step")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (requests shard with no "
@@ -142,7 +161,10 @@ def main():
     torch.cuda.synchronize()
 
     K4 = tsb.KERNELS.index("target_partials")
-    ev = events(args.steps)
+    # the target kernel is bracketed by events on every `sample`-th timed step
+    # (each event pair costs a few microseconds of idle GPU)
+    sampled = list(range(0, args.steps, args.sample))
+    ev = events(len(sampled))
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -150,14 +172,17 @@ def main():
     start.record()
     for i in range(args.steps):
         s = args.warmup + i
-        tsb.profile_kernel(K4, ev[i][0], ev[i][1])
+        if i % args.sample == 0:
+            a, b = ev[i // args.sample]
+            tsb.profile_kernel(K4, a, b)
         rnd.step(drafts[s % P], targets[s % P], s)
+        if i % args.sample == 0:
+            tsb.profile_kernel(K4, None)
     stop.record()
     torch.cuda.synchronize()
     t_host1 = time.perf_counter()
-    tsb.profile_kernel(K4, None)
     ms = start.elapsed_time(stop) / args.steps
-    k4_ms = sum(a.elapsed_time(b) for a, b in ev) / args.steps
+    k4_ms = sum(a.elapsed_time(b) for a, b in ev) / len(ev)
 
     # untimed passes: per-kernel breakdown and acceptance statistics
     kern_us = {}
@@ -181,6 +206,7 @@ def main():
 
     b = 2 if cfg["dtype"] == "bf16" else 4
     k4_bytes = R * (B + 1) * V * b  # every target row of a full tree, read once
+    k1_bytes = R * D * V * b        # every draft row, read once
     achieved = k4_bytes / (k4_ms * 1e-3) / 1e9
     steps_per_s = 1000.0 / ms
     out = {
@@ -204,8 +230,16 @@ def main():
         "tau": round(tau, 4),
         "roofline": {"kernel": "target_partials", "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": None, "bytes_per_launch": k4_bytes, "avg_launch_us": round(k4_ms * 1000, 2)},
+                     "traffic": target_traffic(args.config), "bytes_per_launch": k4_bytes, "avg_launch_us": round(k4_ms * 1000, 2),
+                     "timed_launches": len(ev)},
         "kernels_us": kern_us,
+        # the other logit-streaming kernel, from the untimed per-kernel pass
+        "roofline_draft": {"kernel": "draft_partials", "bound": "hbm (binary64 exp per logit makes it VALU-bound)",
+                           "achieved": round(k1_bytes / (kern_us["draft_partials"] * 1e-6) / 1e9, 1),
+                           "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                           "frac": round(k1_bytes / (kern_us["draft_partials"] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                           "bytes_per_launch": k1_bytes, "avg_launch_us": kern_us["draft_partials"],
+                           "source": "per-kernel pass after the timed region"},
         "host_wall_s": round(t_host1 - t_host0, 3),
         "flagged_requests": flagged,
         "cpu_baseline": cpu,
