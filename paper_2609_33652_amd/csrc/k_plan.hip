@@ -42,7 +42,7 @@ __device__ __forceinline__ void load8(const void* __restrict__ draft, size_t row
     }
 }
 
-constexpr int kDraftUnroll = 2;  // 8-logit groups per thread per chunk
+constexpr int kDraftUnroll = 1;  // 8-logit groups per thread per chunk
 
 template <int DT, bool VEC>
 __global__ __launch_bounds__(kBlock) void draft_partials(const void* __restrict__ draft, int V, int D,
@@ -73,11 +73,16 @@ __global__ __launch_bounds__(kBlock) void draft_partials(const void* __restrict_
     bool bad = false;       // a NaN or +inf scaled logit
     WaveTopList top;
     top.init(K);
-    // Filter (fx, fid): a logit x with id i can still enter the wave's list
+    // Filter (fx, fid): a logit x with id i can still be among the row's K best
     // only if x > fx, or x == fx and i <= fid (the key order is logit desc,
-    // id asc). It starts at the K-th largest of the lanes' first-chunk maxima
-    // (K distinct logits at or above it exist) with any id, and then follows
-    // the list's K-th entry once the list is full.
+    // id asc). It starts at the K-th largest of the workgroup's column maxima
+    // over its first chunk (K distinct logits at or above it exist) with any
+    // id; then every wave whose list is full publishes its K-th key to s_key
+    // (an LDS maximum) and all waves filter against the best published key.
+
+    const int wave = tid / kWave, lane = tid % kWave;
+    __shared__ float s_lm[kBlock / kWave][kWave];
+    __shared__ unsigned long long s_key;
     float fx;
     uint32_t fid = 0xFFFFFFFFu;
     {
@@ -86,8 +91,15 @@ __global__ __launch_bounds__(kBlock) void draft_partials(const void* __restrict_
         for (int u = 0; u < kDraftUnroll; ++u)
 #pragma unroll
             for (int j = 0; j < 8; ++j) lm = fmaxf(lm, xc[u][j]);
-        fx = wave_kth_largest(lm, K);
+        s_lm[wave][lane] = isnan(lm) ? -INFINITY : lm;
+        if (tid == 0) s_key = 0ull;
+        __syncthreads();
+        float cm = s_lm[0][lane];
+#pragma unroll
+        for (int w = 1; w < kBlock / kWave; ++w) cm = fmaxf(cm, s_lm[w][lane]);
+        fx = wave_kth_largest(cm, K);
     }
+    uint64_t pub = 0;  // the key this wave last published
 
     for (int base = lo; base < hi; base += kChunk) {
         const int nbase = base + kChunk;
@@ -102,44 +114,63 @@ __global__ __launch_bounds__(kBlock) void draft_partials(const void* __restrict_
 #pragma unroll
                 for (int j = 0; j < 8; ++j) xn[u][j] = -INFINITY;
         }
+        // row statistics first, as one straight-line block (the exps of all
+        // groups interleave), then the candidate filter
+        float xm[kDraftUnroll];
+        float a[kDraftUnroll][8];
+        float am = -INFINITY;
+#pragma unroll
+        for (int u = 0; u < kDraftUnroll; ++u) {
+            xm[u] = xc[u][0];
+#pragma unroll
+            for (int j = 1; j < 8; ++j) xm[u] = fmaxf(xm[u], xc[u][j]);  // NaN is ignored
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                a[u][j] = xc[u][j] * invT;
+                bad |= __builtin_amdgcn_classf(a[u][j], 0x203);  // signalling NaN, quiet NaN, +inf
+            }
+            am = fmaxf(am, xm[u] * invT);  // rounding is monotone: the scaled max is the max of the scaled
+        }
+        if (am > m && am < INFINITY) {
+            sum = (m == -INFINITY) ? 0.0 : sum * exp64((double)m - (double)am, s_exp);
+            m = am;
+        }
+        {
+            const double md = (double)m;
+            double s2[2] = {0.0, 0.0};
+#pragma unroll
+            for (int u = 0; u < kDraftUnroll; ++u)
+#pragma unroll
+                for (int j = 0; j < 8; ++j) s2[j & 1] += exp64((double)a[u][j] - md, s_exp);
+            sum += s2[0] + s2[1];
+        }
 #pragma unroll
         for (int u = 0; u < kDraftUnroll; ++u) {
             const int i0 = base + (u * kBlock + tid) * 8;
-            float xm = xc[u][0];
-#pragma unroll
-            for (int j = 1; j < 8; ++j) xm = fmaxf(xm, xc[u][j]);  // NaN is ignored
-            float a[8];
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                a[j] = xc[u][j] * invT;
-                bad |= __builtin_amdgcn_classf(a[j], 0x203);  // signalling NaN, quiet NaN, +inf
-            }
-            // rounding is monotone, so the max of the scaled values is the scaled max
-            const float am = xm * invT;
-            if (am > m && am < INFINITY) {
-                sum = (m == -INFINITY) ? 0.0 : sum * exp64((double)m - (double)am, s_exp);
-                m = am;
-            }
-            const double md = (double)m;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) sum += exp64((double)a[j] - md, s_exp);
             // the group's smallest id is i0
-            if (__ballot(xm > fx || (xm == fx && (uint32_t)i0 <= fid))) {
+            if (__ballot(xm[u] > fx || (xm[u] == fx && (uint32_t)i0 <= fid))) {
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
                     const float xj = xc[u][j];
                     const uint32_t id = (uint32_t)(i0 + j);
                     const bool ok = (i0 + j < hi) && (xj > fx || (xj == fx && id <= fid));  // false for NaN
-                    top.offer(cand_key(xj, id), ok);
+                    top.offer_xid(xj, id, ok);
                 }
-                if (top.thr) {
-                    // the list's K-th key; entering now needs a key above it
-                    const float tx = cand_value(top.thr);
-                    const uint32_t tid1 = cand_id(top.thr);
-                    if (tx > fx || (tx == fx && tid1 <= fid)) {
-                        fx = tx;
-                        fid = tid1 - 1;  // wraps for id 0 to "any id": looser, and offer re-checks the key
-                    }
+                if (top.thr > pub) {  // publish this wave's K-th key
+                    pub = top.thr;
+                    if (lane == 0) atomicMax(&s_key, (unsigned long long)pub);
+                }
+            }
+        }
+        {
+            // entering needs a key above the best published K-th key
+            const uint64_t sk = *(volatile unsigned long long*)&s_key;
+            if (sk) {
+                const float tx = cand_value(sk);
+                const uint32_t tid1 = cand_id(sk);
+                if (tx > fx || (tx == fx && tid1 <= fid)) {
+                    fx = tx;
+                    fid = tid1 - 1;  // wraps for id 0 to "any id": looser, and offer re-checks the key
                 }
             }
         }
@@ -154,7 +185,6 @@ __global__ __launch_bounds__(kBlock) void draft_partials(const void* __restrict_
     __shared__ double s_s[kBlock / kWave];
     __shared__ int s_bad[kBlock / kWave];
     __shared__ uint64_t s_top[kBlock / kWave][kWave];
-    const int wave = tid / kWave, lane = tid % kWave;
     const float wm = wave_max(m);
     double contrib = (m == -INFINITY) ? 0.0 : sum * exp((double)m - (double)wm);
     const double ws = wave_sum(contrib);
@@ -241,22 +271,6 @@ struct PlanShared {
         } t;
     } u;
 };
-
-// Exclusive prefix sum over the lanes of small non-negative counts (< 64),
-// one ballot per bit; `total` receives the wave sum.
-__device__ __forceinline__ int wave_excl_scan6(int c, int& total) {
-    int off = 0;
-    total = 0;
-#pragma unroll
-    for (int b = 0; b < 6; ++b) {
-        const uint64_t m = __ballot((c >> b) & 1);
-        const int below = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
-                                                         __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-        off += below << b;
-        total += __popcll(m) << b;
-    }
-    return off;
-}
 
 __device__ __forceinline__ double wave_max_f64(double v) {
 #pragma unroll
@@ -349,7 +363,7 @@ __device__ int plan_count(const PlanShared& sh, int Dp, int K, double tau, int c
                 c += ok ? 1 : 0;
             }
             int tot;
-            const int off = wave_excl_scan6(c, tot);
+            const int off = wave_excl_scan<6>(c, tot);
             if (total + tot > cap) {
                 m_out = -INFINITY;
                 return cap + 1;
@@ -498,13 +512,13 @@ __global__ __launch_bounds__(kPlanThreads) void plan_tree(int D, int S, int K, i
                 ce += eq ? 1 : 0;
             }
             int etot;
-            const int eoff = wave_excl_scan6(ce, etot);
+            const int eoff = wave_excl_scan<6>(ce, etot);
             const int adm = max(0, min(ce, quota - eoff));
             if (etot > 0 && quota > 0) tie_admitted = true;
             quota -= min(etot, quota);
             const int c = cg + adm;
             int tot;
-            const int off = wave_excl_scan6(c, tot);
+            const int off = wave_excl_scan<6>(c, tot);
             for (int j = 0; __ballot(j < c); ++j) {
                 const float lj = lane_f32(lpv, j);
                 if (j < c && n + off + j <= B) {  // always true: the admitted nodes number at most B

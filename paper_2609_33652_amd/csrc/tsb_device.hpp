@@ -230,7 +230,45 @@ struct WaveTopList {
             thr = lane_u64(v, k - 1);
         }
     }
+    // As offer, for candidates given as (logit, id): the key is formed only
+    // for the one candidate being inserted (from wave-uniform values).
+    __device__ void offer_xid(float x, uint32_t id, bool want) {
+        uint64_t ballot = __ballot(want);
+        const int lane = lane_id();
+        while (ballot) {
+            const int src = __ffsll((unsigned long long)ballot) - 1;
+            ballot &= ballot - 1;
+            const uint64_t c = cand_key(lane_f32(x, src), lane_u32(id, src));
+            if (c <= thr) continue;
+            const int pos = __popcll(__ballot(lane < k && v > c));
+            const uint64_t up = wave_shr1(v);
+            if (lane < k) {
+                if (lane == pos)
+                    v = c;
+                else if (lane > pos)
+                    v = up;
+            }
+            thr = lane_u64(v, k - 1);
+        }
+    }
 };
+
+// Exclusive prefix sum over the lanes of small non-negative counts
+// (< 2^NB), one ballot per bit; `total` receives the wave sum.
+template <int NB>
+__device__ __forceinline__ int wave_excl_scan(int c, int& total) {
+    int off = 0;
+    total = 0;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+        const uint64_t m = __ballot((c >> b) & 1);
+        const int below = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                         __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+        off += below << b;
+        total += __popcll(m) << b;
+    }
+    return off;
+}
 
 // The k-th largest (1 <= k <= 64) of the values held by the 64 lanes, NaN
 // counted as -inf; wave-uniform.
