@@ -305,6 +305,24 @@ __device__ double walk_sum(double v) {
     return tot;
 }
 
+// Four block-wide binary64 sums in one reduction (same fixed order as walk_sum).
+__device__ void walk_sum4(double (&v)[4]) {
+    __shared__ double red4[4][kWalkThreads / kWave];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = wave_sum(v[k]);
+    if ((threadIdx.x % kWave) == 0)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) red4[k][threadIdx.x / kWave] = v[k];
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        double tot = 0.0;
+        for (int i = 0; i < kWalkThreads / kWave; ++i) tot += red4[k][i];
+        v[k] = tot;
+    }
+    __syncthreads();
+}
+
 struct WalkSlice {
     int v0, v1, nchunks;
     double* p;  // LDS [kWalkCache]
@@ -547,6 +565,78 @@ struct Exchange {
 // normaliser is within ~1e-6 of it: binary32 terms, binary64 accumulation).
 constexpr double kDecisionBand = 1e-4;
 
+// Four logits as loaded (bf16 pairs or binary32), so the loads of a pass can
+// be issued early and converted later.
+template <int DT>
+struct Raw4 {
+    uint32_t w[DT == TSB_BF16 ? 2 : 4];
+};
+
+template <int DT>
+__device__ __forceinline__ void raw_load4(const void* base, size_t off, int valid, bool vec, Raw4<DT>& g) {
+    if (vec && valid == 4) {
+        if (DT == TSB_BF16) {
+            const uint2 raw = *(const uint2*)((const uint16_t*)base + off);
+            g.w[0] = raw.x;
+            g.w[1] = raw.y;
+        } else {
+            const uint4 raw = *(const uint4*)((const float*)base + off);
+            g.w[0] = raw.x;
+            g.w[1] = raw.y;
+            g.w[2] = raw.z;
+            g.w[3] = raw.w;
+        }
+    } else {
+        float x[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[e] = e < valid ? load_logit<DT>(base, off + e) : -INFINITY;
+        if (DT == TSB_BF16) {  // a bf16 value is the top half of its binary32 value
+            g.w[0] = (__float_as_uint(x[0]) >> 16) | (__float_as_uint(x[1]) & 0xFFFF0000u);
+            g.w[1] = (__float_as_uint(x[2]) >> 16) | (__float_as_uint(x[3]) & 0xFFFF0000u);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) g.w[e] = __float_as_uint(x[e]);
+        }
+    }
+}
+
+template <int DT>
+__device__ __forceinline__ void raw_scaled4(const Raw4<DT>& g, int valid, float invT, float a[4]) {
+    float x[4];
+    if (DT == TSB_BF16) {
+        x[0] = __uint_as_float(g.w[0] << 16);
+        x[1] = __uint_as_float(g.w[0] & 0xFFFF0000u);
+        x[2] = __uint_as_float(g.w[1] << 16);
+        x[3] = __uint_as_float(g.w[1] & 0xFFFF0000u);
+    } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[e] = __uint_as_float(g.w[e]);
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) a[e] = e < valid ? x[e] * invT : -INFINITY;
+}
+
+// The target and draft logits of a cached slice, loaded ahead of the pass
+// that needs them.
+constexpr int kFillGroups = (kWalkCache + 4 * kWalkThreads - 1) / (4 * kWalkThreads);
+template <int DT>
+struct FillRaw {
+    Raw4<DT> t[kFillGroups], d[kFillGroups];
+};
+
+template <int DT>
+__device__ __forceinline__ void fill_prefetch(const WalkArgs& A, bool vec, const WalkSlice& S, size_t trow,
+                                              size_t drow, FillRaw<DT>& f) {
+    const int n = S.v1 - S.v0;
+#pragma unroll
+    for (int k = 0; k < kFillGroups; ++k) {
+        const int i = (k * kWalkThreads + (int)threadIdx.x) * 4;
+        const int valid = max(0, min(4, n - i));
+        raw_load4<DT>(A.target, trow + S.v0 + (valid ? i : 0), valid, vec, f.t[k]);
+        raw_load4<DT>(A.draft, drow + S.v0 + (valid ? i : 0), valid, vec, f.d[k]);
+    }
+}
+
 // First exact pass at a node: fills (p~, q) and returns the slice partials of
 // sum p~, and, for the first residual (C = 1), sum p~ and sum q over tokens
 // with p~ > q (beyond the band where the normaliser could flip the sign) and
@@ -558,23 +648,20 @@ __device__ void fill_pass(const WalkArgs& A, bool vec, const WalkSlice& S, bool 
     if (cached) {
         // the whole slice fits the LDS cache: every load of the thread is
         // issued before any arithmetic (one memory latency per pass)
-        constexpr int kGroups = (kWalkCache + 4 * kWalkThreads - 1) / (4 * kWalkThreads);
         const int n = S.v1 - S.v0;
-        float at[kGroups][4], ad[kGroups][4];
+        FillRaw<DT> pre;
+        fill_prefetch<DT>(A, vec, S, trow, drow, pre);
 #pragma unroll
-        for (int k = 0; k < kGroups; ++k) {
+        for (int k = 0; k < kFillGroups; ++k) {
             const int i = (k * kWalkThreads + (int)threadIdx.x) * 4;
             const int valid = max(0, min(4, n - i));
-            load4_scaled<DT>(A.target, trow + S.v0 + (valid ? i : 0), valid, vec, A.invT, at[k]);
-            load4_scaled<DT>(A.draft, drow + S.v0 + (valid ? i : 0), valid, vec, A.invT, ad[k]);
-        }
-#pragma unroll
-        for (int k = 0; k < kGroups; ++k) {
-            const int i = (k * kWalkThreads + (int)threadIdx.x) * 4;
+            float at[4], ad[4];
+            raw_scaled4<DT>(pre.t[k], valid, A.invT, at);
+            raw_scaled4<DT>(pre.d[k], valid, A.invT, ad);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const double pt = at[k][e] > -INFINITY ? exp64((double)at[k][e] - L0, et) : 0.0;
-                const double qd = ad[k][e] > -INFINITY ? exp64((double)ad[k][e] - Ld, et) : 0.0;
+                const double pt = at[e] > -INFINITY ? exp64((double)at[e] - L0, et) : 0.0;
+                const double qd = ad[e] > -INFINITY ? exp64((double)ad[e] - Ld, et) : 0.0;
                 sp += pt;
                 if (pt > qd * (1.0 + 1e-5)) {
                     pa += pt;
@@ -627,10 +714,11 @@ __device__ void fill_pass(const WalkArgs& A, bool vec, const WalkSlice& S, bool 
             }
         }
     }
-    out[0] = walk_sum(sp);
-    out[1] = walk_sum(pa);
-    out[2] = walk_sum(qa);
-    out[3] = walk_sum(band);
+    out[0] = sp;
+    out[1] = pa;
+    out[2] = qa;
+    out[3] = band;
+    walk_sum4(out);
 }
 
 template <int DT, bool VEC>
@@ -682,10 +770,10 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
         while (true) {
             const int m = A.tree.n_children[tb + u];
             const int d = A.tree.depth[tb + u];
-            int tbad;
-            const double L0 = target_lse(A, r, u, &tbad);
             const size_t trow = ((size_t)r * B1 + u) * (size_t)A.V;
             const size_t drow = ((size_t)r * A.D + (d < A.D ? d : 0)) * (size_t)A.V;
+            int tbad;
+            const double L0 = target_lse(A, r, u, &tbad);
             if (m == 0) {  // accepted leaf: bonus from p_u
                 float bk;
                 int bi;
