@@ -304,13 +304,30 @@ __device__ void merge_row(PlanShared& sh, int row, int rrow, int S, int K, float
         if (pm[o + s] != -INFINITY) tot += ps[o + s] * exp((double)pm[o + s] - (double)M);
     tot = wave_sum(tot);
 
-    WaveTopList top;
-    top.init(K);
     const int n = S * K;
-    for (int base = 0; base < n; base += kWave) {
-        const int i = base + lane;
-        const uint64_t k = i < n ? pk[o * K + i] : 0;
-        top.offer(k, i < n && k != 0);
+    uint64_t best;  // lane j < K: the j-th best candidate of the row
+    if (n <= kWave) {
+        // one candidate per lane: its rank is the number of larger keys (keys
+        // are distinct, empty slots are 0); all lanes in parallel
+        const uint64_t mine = lane < n ? pk[o * K + lane] : 0;
+        int rank = 0;
+        for (int j = 0; j < n; ++j) rank += lane_u64(mine, j) > mine ? 1 : 0;
+        __shared__ uint64_t s_rank[kPlanWaves][kWave];
+        uint64_t* sr = s_rank[threadIdx.x / kWave];
+        sr[lane] = 0;
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        if (mine != 0 && rank < K) sr[rank] = mine;
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+        best = sr[lane];
+    } else {
+        WaveTopList top;
+        top.init(K);
+        for (int base = 0; base < n; base += kWave) {
+            const int i = base + lane;
+            const uint64_t k = i < n ? pk[o * K + i] : 0;
+            top.offer(k, i < n && k != 0);
+        }
+        best = top.v;
     }
 
     const bool nonfinite = bad || M == -INFINITY;
@@ -318,7 +335,7 @@ __device__ void merge_row(PlanShared& sh, int row, int rrow, int S, int K, float
     const float l32 = (float)l64;
     float lp = -INFINITY;
     if (lane < K) {
-        const uint64_t k = top.v;
+        const uint64_t k = best;
         const float a = cand_value(k) * invT;
         lp = a - l32;
         topk_tok[(size_t)row * K + lane] = (int32_t)cand_id(k);
@@ -422,7 +439,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_tree(int D, int S, int K, i
         if (wave < ns) {
             const double tau = wave == 0 ? hi_m
                                : (lo > -INFINITY ? hi_m - (hi_m - lo) * ((double)wave / (double)ns)
-                                                 : hi_m - 0.125 * ldexp(1.0, wave - 1));
+                                                 : hi_m - 0.25 * exp2(0.5 * (double)(wave - 1)));
             double m;
             const int c = plan_count(sh, Dp, K, tau, cap, sh.u.buf + wave * cap, m);
             if (lane == 0) {
