@@ -14,6 +14,11 @@ target p(. | s), every random choice of the round is enumerated:
   * the bonus token: the normalised final residual (or p at a leaf).
 Subtrees that the walk never enters are marginalised out, which is exact
 because the draws of different parents are independent.
+
+naive_law() enumerates target-sample matching (Table 2, Naive) over a tree
+whose node tokens are fixed (the First tree of Section 3.1): at each visited
+node every token of p_u either matches a child and continues there, or ends
+the round as the bonus.
 """
 import itertools
 
@@ -116,3 +121,27 @@ def target_law(p_of_prefix, V, length):
             w *= p_of_prefix(seq[:i])[seq[i]]
         out[seq] = w
     return out
+
+
+def naive_law(tree, node_tok, p_of_prefix):
+    """Exact law of the emitted sequence under target-sample matching on fixed node tokens."""
+    law = {}
+
+    def walk(u, prefix, w):
+        p = np.asarray(p_of_prefix(prefix), dtype=np.float64)
+        m = int(tree["n_children"][u])
+        fc = int(tree["first_child"][u])
+        child_of = {}
+        for j in range(m):
+            child_of.setdefault(int(node_tok[fc + j]), fc + j)
+        for y in range(p.shape[0]):
+            if p[y] <= 0.0:
+                continue
+            if y in child_of:
+                walk(child_of[y], prefix + (y,), w * p[y])
+            else:
+                seq = prefix + (y,)
+                law[seq] = law.get(seq, 0.0) + w * p[y]
+
+    walk(0, (), 1.0)
+    return law
