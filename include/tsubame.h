@@ -17,6 +17,9 @@
  *               replayed candidates).
  *   tsb_step    plan -> replay -> verify with target logits supplied up front.
  *
+ * and the deterministic baseline of Section 3.1 with target-sample matching
+ * (Table 2, Naive): tsb_first_tokens, tsb_verify_naive, tsb_step_first.
+ *
  * Conventions shared by every entry point
  *   - Every array pointer is a DEVICE pointer owned by the caller, row-major,
  *     vocabulary index fastest. The library never allocates, frees or
@@ -164,6 +167,38 @@ tsb_status tsb_step(const tsb_config* cfg, const void* draft, const void* target
                     int32_t* node_tok, const tsb_verdict* out, void* workspace,
                     size_t workspace_bytes, hipStream_t stream);
 
+/* Planning tokens as node tokens: the first-pass tree verified directly is
+ * the deterministic baseline First (Section 3.1; Tables 3 and 4, TopK).
+ * Writes node_tok[r, i] = topk_tok[r, depth[i] - 1, rank[i]] for
+ * 0 < i < n_nodes[r]; -1 at the root, beyond n_nodes, and where depth or
+ * rank is out of range. topk_tok and tree as written by tsb_plan. Needs no
+ * workspace. */
+tsb_status tsb_first_tokens(const tsb_config* cfg, const int32_t* topk_tok, const tsb_tree* tree,
+                            int32_t* node_tok, hipStream_t stream);
+
+/* Target-sample matching (Table 2, Naive; Section 2.3): from the root, draw
+ * y ~ p_u as argmax_v a_v + G(seed, step, request, u, v) over the scaled
+ * target row a = fl32(target[r, u, :] * invT) (Gumbel-max, BONUS stream of
+ * node u; equal keys to the smaller id); the first child of u (in rank
+ * order) whose node_tok is y is accepted and the walk continues there,
+ * otherwise y is the bonus token. Lossless for any tree and node tokens
+ * (replayed or First). Only visited target rows are read; no normaliser is
+ * computed. Writes n_acc, acc_node, acc_tok, bonus and ORs into req_status
+ * (NONFINITE if a visited row holds NaN or +inf or no finite logit, or if
+ * req_status already holds NONFINITE from tsb_plan: then n_acc = bonus = -1;
+ * WALK_TIMEOUT as in tsb_verify). out->target_lse and out->trace are not
+ * written. The walk stops accepting at depth D. */
+tsb_status tsb_verify_naive(const tsb_config* cfg, const void* target, const tsb_tree* tree,
+                            const int32_t* node_tok, uint32_t step, const tsb_verdict* out,
+                            void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* plan -> first tokens -> naive verification on one stream: one round of the
+ * First + Naive baseline (target supplied up front, one row per tree node). */
+tsb_status tsb_step_first(const tsb_config* cfg, const void* draft, const void* target, uint32_t step,
+                          double* draft_lse, int32_t* topk_tok, float* topk_lp, const tsb_tree* tree,
+                          int32_t* node_tok, const tsb_verdict* out, void* workspace,
+                          size_t workspace_bytes, hipStream_t stream);
+
 /* Instrumentation (for benchmarks). On the calling thread, every later
  * launch of kernel `kernel_id` (a TSB_KERNEL_* value) is bracketed by
  * hipEventRecord(start) / hipEventRecord(stop) on the launch stream, so
@@ -176,7 +211,8 @@ enum {
     TSB_KERNEL_REPLAY_MERGE = 3,
     TSB_KERNEL_TARGET_PARTIALS = 4, /* target row statistics (streams the target) */
     TSB_KERNEL_VERIFY_WALK = 5,
-    TSB_KERNEL_COUNT = 6
+    TSB_KERNEL_VERIFY_NAIVE = 6,    /* target-sample matching walk */
+    TSB_KERNEL_COUNT = 7
 };
 tsb_status tsb_profile_kernel(int32_t kernel_id, hipEvent_t start, hipEvent_t stop);
 

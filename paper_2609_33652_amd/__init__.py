@@ -5,7 +5,8 @@ runs in the HIP kernels behind the C ABI of include/tsubame.h. PyTorch
 supplies device memory and the stream. There is no CPU fallback: if the
 library is not built, or a call fails, an exception is raised.
 
-Entry points mirror the C ABI: plan, replay, verify, step, workspace_bytes.
+Entry points mirror the C ABI: plan, replay, verify, step, workspace_bytes,
+and the First + Naive baseline: first_tokens, verify_naive, step_first.
 `Round` bundles the output buffers of one configuration.
 """
 import ctypes
@@ -25,9 +26,10 @@ REQ_WALK_TIMEOUT = 8
 FLAG_NO_PRUNE = 1
 MAX_D, MAX_K, MAX_B, TRACE_MAX = 64, 32, 1023, 256
 KERNELS = ("draft_partials", "plan_tree", "replay_scan", "replay_merge", "target_partials",
-           "verify_walk")
+           "verify_walk", "verify_naive")
 
 EXPORTS = ("tsb_workspace_bytes", "tsb_plan", "tsb_replay", "tsb_verify", "tsb_step",
+           "tsb_first_tokens", "tsb_verify_naive", "tsb_step_first",
            "tsb_status_string", "tsb_last_error", "tsb_version", "tsb_profile_kernel")
 
 
@@ -83,6 +85,13 @@ def load(path=LIB_PATH):
     lib.tsb_step.restype = ctypes.c_int
     lib.tsb_step.argtypes = [ctypes.POINTER(TsbConfig), P, P, ctypes.c_uint32, P, P, P, ctypes.POINTER(TsbTree), P,
                              ctypes.POINTER(TsbVerdict), P, ctypes.c_size_t, P]
+    lib.tsb_first_tokens.restype = ctypes.c_int
+    lib.tsb_first_tokens.argtypes = [ctypes.POINTER(TsbConfig), P, ctypes.POINTER(TsbTree), P, P]
+    lib.tsb_verify_naive.restype = ctypes.c_int
+    lib.tsb_verify_naive.argtypes = [ctypes.POINTER(TsbConfig), P, ctypes.POINTER(TsbTree), P, ctypes.c_uint32,
+                                     ctypes.POINTER(TsbVerdict), P, ctypes.c_size_t, P]
+    lib.tsb_step_first.restype = ctypes.c_int
+    lib.tsb_step_first.argtypes = lib.tsb_step.argtypes
     lib.tsb_status_string.restype = ctypes.c_char_p
     lib.tsb_status_string.argtypes = [ctypes.c_int]
     lib.tsb_last_error.restype = ctypes.c_char_p
@@ -211,6 +220,32 @@ class Round:
                              self.ws_ptr, self.ws_bytes, _stream(stream))
         if st:
             raise TsbError(st, "tsb_step")
+
+    # ------------------------------------------------- First + Naive baseline
+    def first_tokens(self, stream=None):
+        """node_tok <- planning candidates of the first-pass tree (needs plan() first)."""
+        st = load().tsb_first_tokens(ctypes.byref(self.cfg), _ptr(self.topk_tok), ctypes.byref(self._tree_c),
+                                     _ptr(self.node_tok), _stream(stream))
+        if st:
+            raise TsbError(st, "tsb_first_tokens")
+
+    def verify_naive(self, target, step, stream=None):
+        self._logits(target, self.cfg.B + 1, "target")
+        st = load().tsb_verify_naive(ctypes.byref(self.cfg), _ptr(target), ctypes.byref(self._tree_c),
+                                     _ptr(self.node_tok), int(step) & 0xFFFFFFFF, ctypes.byref(self._verdict_c),
+                                     self.ws_ptr, self.ws_bytes, _stream(stream))
+        if st:
+            raise TsbError(st, "tsb_verify_naive")
+
+    def step_first(self, draft, target, step, stream=None):
+        self._logits(draft, self.cfg.D, "draft")
+        self._logits(target, self.cfg.B + 1, "target")
+        st = load().tsb_step_first(ctypes.byref(self.cfg), _ptr(draft), _ptr(target), int(step) & 0xFFFFFFFF,
+                                   _ptr(self.draft_lse), _ptr(self.topk_tok), _ptr(self.topk_lp),
+                                   ctypes.byref(self._tree_c), _ptr(self.node_tok), ctypes.byref(self._verdict_c),
+                                   self.ws_ptr, self.ws_bytes, _stream(stream))
+        if st:
+            raise TsbError(st, "tsb_step_first")
 
     # ---------------------------------------------------------------- results
     def host(self):

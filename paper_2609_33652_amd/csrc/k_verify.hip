@@ -205,51 +205,6 @@ __device__ double target_lse(const WalkArgs& A, int r, int node, int* bad) {
     return (double)M + log(tot);
 }
 
-// Per-request barrier over the G workgroups of a request: monotone counter,
-// bounded spin (a wait that exceeds the limit sets *timeout and proceeds).
-// Only the exchange slots cross workgroups, and they are written and read
-// with agent-scope atomics (coherent without L2 maintenance), so the
-// barrier needs no cache writeback or invalidation: the slot stores have
-// completed (s_waitcnt vmcnt(0)) before the counter is incremented, and a
-// reader issues its slot loads only after it has seen the count.
-__device__ void request_barrier(uint32_t* counter, uint32_t target, int* timeout) {
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this thread's slot stores are done
-        __atomic_signal_fence(__ATOMIC_SEQ_CST);
-        __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        uint32_t spins = 0;
-        while (__hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-            __builtin_amdgcn_s_sleep(2);
-            if (++spins > (1u << 23)) {
-                *timeout = 1;
-                break;
-            }
-        }
-        __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    }
-    __syncthreads();
-}
-
-template <int DT>
-__device__ __forceinline__ void load4(const void* base, size_t off, int valid, bool vec, float x[4]) {
-    if (vec && valid == 4) {
-        if (DT == TSB_BF16) {
-            const uint2 raw = *(const uint2*)((const uint16_t*)base + off);
-            x[0] = __uint_as_float(raw.x << 16);
-            x[1] = __uint_as_float(raw.x & 0xFFFF0000u);
-            x[2] = __uint_as_float(raw.y << 16);
-            x[3] = __uint_as_float(raw.y & 0xFFFF0000u);
-        } else {
-            const float4 a = *(const float4*)((const float*)base + off);
-            x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
-        }
-    } else {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) x[e] = e < valid ? load_logit<DT>(base, off + e) : -INFINITY;
-    }
-}
-
 struct SplitF {  // binary64 value as binary32 hi + lo
     float hi, lo;
 };

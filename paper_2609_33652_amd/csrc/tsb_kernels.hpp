@@ -34,4 +34,11 @@ hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, con
                          const void* target, const tsb_tree& tree, const int32_t* node_tok, uint32_t step,
                          const tsb_verdict& out, char* ws, hipStream_t st);
 
+hipError_t launch_first_tokens(const tsb_config& c, const int32_t* topk_tok, const tsb_tree& tree, int32_t* node_tok,
+                               hipStream_t st);
+
+hipError_t launch_verify_naive(const tsb_config& c, float invT, const void* target, const tsb_tree& tree,
+                               const int32_t* node_tok, uint32_t step, const tsb_verdict& out, char* ws,
+                               hipStream_t st);
+
 }  // namespace tsb

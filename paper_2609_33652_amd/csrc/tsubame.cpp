@@ -164,6 +164,52 @@ tsb_status tsb_step(const tsb_config* cfg, const void* draft, const void* target
     return TSB_OK;
 }
 
+tsb_status tsb_first_tokens(const tsb_config* cfg, const int32_t* topk_tok, const tsb_tree* tree, int32_t* node_tok,
+                            hipStream_t stream) {
+    g_last_error[0] = 0;
+    TRY(check_config(cfg));
+    if (!topk_tok || !node_tok) return fail(TSB_E_NULL, "tsb_first_tokens: a required array is NULL");
+    TRY(check_tree(tree));
+    const hipError_t e = tsb::launch_first_tokens(*cfg, topk_tok, *tree, node_tok, stream);
+    return e == hipSuccess ? TSB_OK : hip_fail(e, "tsb_first_tokens");
+}
+
+tsb_status tsb_verify_naive(const tsb_config* cfg, const void* target, const tsb_tree* tree, const int32_t* node_tok,
+                            uint32_t step, const tsb_verdict* out, void* workspace, size_t workspace_bytes,
+                            hipStream_t stream) {
+    g_last_error[0] = 0;
+    TRY(check_config(cfg));
+    if (!target || !node_tok) return fail(TSB_E_NULL, "tsb_verify_naive: a required array is NULL");
+    TRY(check_tree(tree));
+    TRY(check_verdict(out));
+    TRY(check_ws(cfg, workspace, workspace_bytes));
+    const hipError_t e = tsb::launch_verify_naive(*cfg, inv_temperature(cfg->temperature), target, *tree, node_tok,
+                                                  step, *out, (char*)workspace, stream);
+    return e == hipSuccess ? TSB_OK : hip_fail(e, "tsb_verify_naive");
+}
+
+tsb_status tsb_step_first(const tsb_config* cfg, const void* draft, const void* target, uint32_t step,
+                          double* draft_lse, int32_t* topk_tok, float* topk_lp, const tsb_tree* tree,
+                          int32_t* node_tok, const tsb_verdict* out, void* workspace, size_t workspace_bytes,
+                          hipStream_t stream) {
+    g_last_error[0] = 0;
+    TRY(check_config(cfg));
+    if (!draft || !target || !draft_lse || !topk_tok || !topk_lp || !node_tok)
+        return fail(TSB_E_NULL, "tsb_step_first: a required array is NULL");
+    TRY(check_tree(tree));
+    TRY(check_verdict(out));
+    TRY(check_ws(cfg, workspace, workspace_bytes));
+    const float invT = inv_temperature(cfg->temperature);
+    char* ws = (char*)workspace;
+    hipError_t e = tsb::launch_plan(*cfg, invT, draft, draft_lse, topk_tok, topk_lp, *tree, out->req_status, ws, stream);
+    if (e != hipSuccess) return hip_fail(e, "tsb_step_first/plan");
+    e = tsb::launch_first_tokens(*cfg, topk_tok, *tree, node_tok, stream);
+    if (e != hipSuccess) return hip_fail(e, "tsb_step_first/first_tokens");
+    e = tsb::launch_verify_naive(*cfg, invT, target, *tree, node_tok, step, *out, ws, stream);
+    if (e != hipSuccess) return hip_fail(e, "tsb_step_first/verify_naive");
+    return TSB_OK;
+}
+
 tsb_status tsb_profile_kernel(int32_t kernel_id, hipEvent_t start, hipEvent_t stop) {
     g_last_error[0] = 0;
     tsb::ProfileHook& h = tsb::profile_hook();
@@ -195,6 +241,6 @@ const char* tsb_status_string(tsb_status s) {
 
 const char* tsb_last_error(void) { return g_last_error; }
 
-int32_t tsb_version(void) { return 101; }
+int32_t tsb_version(void) { return 102; }
 
 }  // extern "C"

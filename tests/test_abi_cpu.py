@@ -33,7 +33,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(tsb.EXPORTS)
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.tsb_version() == 101
+    assert lib.tsb_version() == 102
 
 
 def _cfg(**kw):
@@ -110,3 +110,28 @@ def test_status_strings(lib):
     for code in range(0, 8):
         assert lib.tsb_status_string(code).decode()
     assert lib.tsb_status_string(99).decode() == "unknown status"
+
+
+def test_first_naive_entry_points_validate(lib):
+    cfg = _cfg()
+    need = lib.tsb_workspace_bytes(ctypes.byref(cfg))
+    t = _tree()
+    v = _verdict()
+    bad = _cfg(K=0)
+    assert lib.tsb_first_tokens(ctypes.byref(bad), FAKE, ctypes.byref(t), FAKE, None) == 2
+    assert lib.tsb_first_tokens(ctypes.byref(cfg), None, ctypes.byref(t), FAKE, None) == 1
+    assert lib.tsb_first_tokens(ctypes.byref(cfg), FAKE, ctypes.byref(t), None, None) == 1
+    assert lib.tsb_verify_naive(ctypes.byref(_cfg(temperature=0.0)), FAKE, ctypes.byref(t), FAKE, 0,
+                                ctypes.byref(v), FAKE, need, None) == 4
+    assert lib.tsb_verify_naive(ctypes.byref(cfg), None, ctypes.byref(t), FAKE, 0, ctypes.byref(v), FAKE, need,
+                                None) == 1
+    bad_v = _verdict()
+    bad_v.req_status = None
+    assert lib.tsb_verify_naive(ctypes.byref(cfg), FAKE, ctypes.byref(t), FAKE, 0, ctypes.byref(bad_v), FAKE,
+                                need, None) == 1
+    assert lib.tsb_verify_naive(ctypes.byref(cfg), FAKE, ctypes.byref(t), FAKE, 0, ctypes.byref(v), FAKE,
+                                need - 1, None) == 5
+    assert lib.tsb_step_first(ctypes.byref(cfg), FAKE, None, 0, FAKE, FAKE, FAKE, ctypes.byref(t), FAKE,
+                              ctypes.byref(v), FAKE, need, None) == 1
+    assert lib.tsb_step_first(ctypes.byref(_cfg(dtype=9)), FAKE, FAKE, 0, FAKE, FAKE, FAKE, ctypes.byref(t),
+                              FAKE, ctypes.byref(v), FAKE, need, None) == 3
