@@ -66,13 +66,18 @@ _CPU = {}
 
 def _cpu_task(args):
     r, step = args
-    from oracle import step as ostep
     c = _CPU["cfg"]
-    out = ostep.step_request(_CPU["draft"][r], _CPU["target"][r], c["T"], c["K"], c["B"], _CPU["seed"], step, r)
+    if _CPU["path"] == "first_naive":
+        from oracle import naive as onaive
+        out = onaive.first_naive_request(_CPU["draft"][r], _CPU["target"][r], c["T"], c["K"], c["B"], _CPU["seed"],
+                                         step, r)
+    else:
+        from oracle import step as ostep
+        out = ostep.step_request(_CPU["draft"][r], _CPU["target"][r], c["T"], c["K"], c["B"], _CPU["seed"], step, r)
     return out["n_acc"]
 
 
-def cpu_baseline(cfg, seed, requests):
+def cpu_baseline(cfg, seed, requests, path="replay_rrs"):
     """Time the oracle over `requests` request-steps of one input set (runs before any GPU use)."""
     import multiprocessing as mp
 
@@ -88,7 +93,7 @@ def cpu_baseline(cfg, seed, requests):
     del base
     # plain numpy in the workers: no torch (OpenMP) use after fork
     nr = min(requests, cfg["R"])
-    _CPU.update(cfg=cfg, draft=draft[:nr].float().numpy(), target=target[:nr].float().numpy(), seed=seed)
+    _CPU.update(cfg=cfg, draft=draft[:nr].float().numpy(), target=target[:nr].float().numpy(), seed=seed, path=path)
     del draft, target
     log("cpu baseline: inputs ready")
     tasks = [(r % nr, r // nr) for r in range(requests)]
@@ -100,11 +105,65 @@ def cpu_baseline(cfg, seed, requests):
     dt = time.perf_counter() - t0
     _CPU.clear()
     return dict(value=(len(tasks) / cfg["R"]) / dt, unit="steps/s", cores=cores, kind="oracle",
-                sample="%d request-steps (%g steps) of the %s workload, CPU-generated set 0; wall %.2f s"
-                       % (len(tasks), len(tasks) / cfg["R"], cfg["name"], dt))
+                sample="%d request-steps (%g steps) of the %s workload, CPU-generated set 0, %s round; wall %.2f s"
+                       % (len(tasks), len(tasks) / cfg["R"], cfg["name"], path.replace("_", " + "), dt))
 
 
 # ---------------------------------------------------------------- GPU
+def first_naive(tsb, c, dev, drafts, targets, args, cfg):
+    """The First + Naive baseline on the same inputs: timed rounds, acceptance, and the walk's roofline."""
+    import torch
+    R, V = cfg["R"], cfg["V"]
+    P = len(drafts)
+    rnd = tsb.Round(c, dev)
+    for s in range(args.warmup):
+        rnd.step_first(drafts[s % P], targets[s % P], s)
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(args.first_steps):
+        s = args.warmup + i
+        rnd.step_first(drafts[s % P], targets[s % P], s)
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.first_steps
+    # the walk kernel alone, with the rows it visited (one read of each)
+    kern_us = {}
+    visited = 0
+    for name in ("draft_partials", "plan_tree", "verify_naive"):
+        kid = tsb.KERNELS.index(name)
+        evs = events(args.breakdown_steps)
+        for i in range(args.breakdown_steps):
+            tsb.profile_kernel(kid, evs[i][0], evs[i][1])
+            rnd.step_first(drafts[i % P], targets[i % P], i)
+            tsb.profile_kernel(kid, None)
+            if name == "verify_naive":
+                n_acc = rnd.n_acc.clamp(min=-1)
+                visited += int((n_acc + 1).sum())
+        torch.cuda.synchronize()
+        kern_us[name] = round(1000.0 * sum(a.elapsed_time(b) for a, b in evs) / args.breakdown_steps, 2)
+    acc = 0
+    for i in range(P):
+        rnd.step_first(drafts[i], targets[i], i)
+        h = rnd.host()
+        acc += int(h["n_acc"].clamp(min=0).sum()) + int((h["n_acc"] >= 0).sum())
+    tau = acc / (P * R)
+    b = 2 if cfg["dtype"] == "bf16" else 4
+    walk_bytes = visited / args.breakdown_steps * V * b
+    achieved = walk_bytes / (kern_us["verify_naive"] * 1e-6) / 1e9
+    return {
+        "steps_per_s": round(1000.0 / ms, 2), "ms_per_step": round(ms, 4), "steps": args.first_steps,
+        "tau": round(tau, 4), "accepted_tokens_per_s": round(tau * R * 1000.0 / ms, 1),
+        "kernels_us": kern_us,
+        "roofline": {"kernel": "verify_naive", "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "bytes_per_launch": int(walk_bytes), "avg_launch_us": kern_us["verify_naive"],
+                     "rows_per_launch": round(visited / args.breakdown_steps, 2),
+                     "note": "one cross-workgroup exchange per visited row; latency, not bandwidth, sets its time"},
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -116,6 +175,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--breakdown-steps", type=int, default=20)
     ap.add_argument("--sample", type=int, default=8, help="time the target kernel on every n-th timed step")
+    ap.add_argument("--first-steps", type=int, default=100, help="timed steps of the First + Naive baseline")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (requests shard with no "
@@ -132,6 +192,10 @@ def main():
         log("cpu baseline: %d oracle request-steps" % nreq)
         cpu = cpu_baseline(cfg, seed, nreq)
         log("cpu baseline:", cpu)
+        cpu_first = cpu_baseline(cfg, seed, nreq, path="first_naive")
+        log("cpu baseline (first + naive):", cpu_first)
+    else:
+        cpu_first = None
 
     import torch
     import paper_2609_33652_amd as tsb
@@ -187,6 +251,8 @@ def main():
     # untimed passes: per-kernel breakdown and acceptance statistics
     kern_us = {}
     for kid, name in enumerate(tsb.KERNELS):
+        if name == "verify_naive":
+            continue
         evs = events(args.breakdown_steps)
         for i in range(args.breakdown_steps):
             tsb.profile_kernel(kid, evs[i][0], evs[i][1])
@@ -203,6 +269,9 @@ def main():
         flagged += int((h["req_status"] & (tsb.REQ_NONFINITE | tsb.REQ_WALK_TIMEOUT)).ne(0).sum())
     tau = acc / (P * R)
     nodes_per_step = nodes / P
+
+    first = first_naive(tsb, c, dev, drafts, targets, args, cfg)
+    first["cpu_baseline"] = cpu_first
 
     b = 2 if cfg["dtype"] == "bf16" else 4
     k4_bytes = R * (B + 1) * V * b  # every target row of a full tree, read once
@@ -243,6 +312,7 @@ def main():
         "host_wall_s": round(t_host1 - t_host0, 3),
         "flagged_requests": flagged,
         "cpu_baseline": cpu,
+        "first_naive": first,
     }
     print(json.dumps(out), flush=True)
 

@@ -163,7 +163,7 @@ class Round:
         nb = workspace_bytes(cfg)
         if nb == 0:
             raise ValueError("invalid configuration")
-        self.ws = torch.empty(nb + 256, dtype=torch.uint8, device=dev)
+        self.ws = torch.zeros(nb + 256, dtype=torch.uint8, device=dev)  # zero-filled once (naive exchange tags)
         off = (-self.ws.data_ptr()) % 256
         self.ws_ptr = ctypes.c_void_p(self.ws.data_ptr() + off)
         self.ws_bytes = nb

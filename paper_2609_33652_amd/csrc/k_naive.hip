@@ -15,11 +15,10 @@
 // argmax). No normaliser is needed, so only the rows the walk visits are read.
 //
 //   first_tokens   one thread per (request, node).
-//   naive_clear    zeroes the per-request barrier counters.
 //   verify_naive   resident grid, G workgroups per request, each owning a
 //                  slice of the vocabulary; per visited node one read of its
 //                  slice, the local best key, one exchange of (key, token,
-//                  finiteness) through the per-request barrier.
+//                  finiteness) through tagged slots that the workgroups poll.
 #include <math.h>
 
 #include <atomic>
@@ -48,159 +47,229 @@ __global__ __launch_bounds__(kBlock) void first_tokens(int R, int D, int K, int 
 
 // ------------------------------------------------------------- naive walk
 constexpr int kNaiveThreads = 512;
-constexpr int kNaiveBatch = 4;  // groups of four tokens per thread in flight
+constexpr int kNaiveBatch = 3;  // groups of four tokens per thread per batch
+constexpr int kNaiveBatchTokens = kNaiveBatch * 4 * kNaiveThreads;
+constexpr int kNaiveNodes = TSB_MAX_B + 1;
 
-__global__ __launch_bounds__(kBlock) void naive_clear(uint32_t* counters, int R) {
-    for (int i = blockIdx.x * kBlock + threadIdx.x; i < R; i += gridDim.x * kBlock) counters[i] = 0u;
-}
+// Exchange slots: [R][2][kWalkGroupsMax] pairs of 64-bit words (slot
+// parity = round & 1), written by one relaxed agent-scope store each and
+// polled by the readers. Both words carry a tag of (request sequence number,
+// round), so a reader knows when it holds both words of the current round
+// with no ordering between them and no clearing between calls:
+//   v      = seq << 7 | (round + 1)            (never 0; rounds <= TSB_MAX_D)
+//   word 0 = key with its low 16 bits replaced by v & 0xFFFF
+//   word 1 = token << 33 | has << 32 | bad << 31 | (v & 0x7FFFFFFF)
+// The sequence number of request r advances by one per call; at the end of
+// a call each workgroup zeroes its slot of the round before the last, so a
+// slot holds at most the last call's final round (tag of an older sequence).
+constexpr uint64_t kTagBits0 = 0xFFFFull;
+constexpr uint64_t kTagBits1 = 0x7FFFFFFFull;
 
 struct NaiveArgs {
     const void* target;
     tsb_tree tree;
     const int32_t* node_tok;
     tsb_verdict out;
-    uint32_t* counters;
-    double* zpart;  // exchange slots: [R][2][kWalkGroupsMax][4] doubles
-    int* bidx;      // [R][2][kWalkGroupsMax]
+    uint32_t* seqs;   // [R]
+    uint64_t* slots;  // [R][2][kWalkGroupsMax][2]
     int V, D, B, r0;
     float invT;
     uint32_t k0, k1, step;
 };
 
-// Local result of one slice: best key (binary64 value of fl32(a) + G) and
-// its token (smallest id among equal keys), plus finiteness of the slice.
+// Order-preserving map of a binary64 value to uint64 (-0 folded onto +0).
+__device__ __forceinline__ uint64_t ordered_bits64(double x) {
+    uint64_t u = (uint64_t)__double_as_longlong(x);
+    if (u == 0x8000000000000000ull) u = 0ull;
+    return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
+}
+
+// Keys are compared as ordered_bits64(fl32(a) + G) with the low 16 bits
+// cleared (word 0 of a slot carries the tag there): relative resolution
+// 2^-36 of the binary64 sum; keys equal after clearing go to the smaller
+// token.
+__device__ __forceinline__ uint64_t sample_key(float a, float gumbel) {
+    return ordered_bits64((double)a + (double)gumbel) & ~kTagBits0;
+}
+
+// Local result of one slice: best key and its token (smallest id among equal
+// keys), plus finiteness of the slice.
 struct SliceBest {
-    double key;
-    int tok;
-    int bad;  // a NaN or +inf logit
-    int has;  // a finite logit
+    uint64_t key;  // 0: no candidate
+    uint32_t tok;  // < 2^31
+    int bad;       // a NaN or +inf logit
+    int has;       // a finite logit
 };
 
-// Best (key, token) of the slice [v0, v1) of one target row. A group of
-// four tokens whose largest logit cannot reach the wave's best key so far,
-// nor the smallest key the wave's largest logit of the batch can get, even
-// with the largest Gumbel value, is skipped without drawing its random
-// numbers; such tokens lose strictly to a key the wave keeps, so the result
-// is the exact argmax.
 template <int DT, bool VEC>
-__device__ SliceBest slice_sample(const NaiveArgs& A, size_t trow, int v0, int v1, const RngKey& key,
-                                  uint32_t node) {
-    SliceBest s{-INFINITY, 0x7FFFFFFF, 0, 0};
-    const int n = v1 - v0;
-    double wave_best = -INFINITY;
-    for (int base = 0; base * 4 < n; base += kNaiveBatch * kNaiveThreads) {
-        float a[kNaiveBatch][4];
+__device__ __forceinline__ void load_batch(const void* target, size_t trow, int v0, int n, int base,
+                                           Raw4<DT> (&a)[kNaiveBatch]) {
 #pragma unroll
-        for (int j = 0; j < kNaiveBatch; ++j) {
-            const int i = (base + j * kNaiveThreads + (int)threadIdx.x) * 4;
-            const int valid = max(0, min(4, n - i));
-            float x[4];
-            load4<DT>(A.target, trow + v0 + (valid ? i : 0), valid, VEC, x);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) a[j][e] = e < valid ? x[e] * A.invT : -INFINITY;
-        }
-        float gm[kNaiveBatch], bm = -INFINITY;
-#pragma unroll
-        for (int j = 0; j < kNaiveBatch; ++j) {
-            gm[j] = -INFINITY;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                s.bad |= (isnan(a[j][e]) || a[j][e] == INFINITY) ? 1 : 0;
-                s.has |= (a[j][e] > -INFINITY && a[j][e] < INFINITY) ? 1 : 0;
-                gm[j] = fmaxf(gm[j], a[j][e]);
-            }
-            bm = fmaxf(bm, gm[j]);
-        }
-        bm = wave_max(bm);
-        const double thr = fmax(wave_best, bm < INFINITY ? (double)bm + (double)kGumbelMinBound : -INFINITY);
-#pragma unroll
-        for (int j = 0; j < kNaiveBatch; ++j) {
-            const int i = (base + j * kNaiveThreads + (int)threadIdx.x) * 4;
-            if (gm[j] > -INFINITY && (double)gm[j] + (double)kGumbelMaxBound >= thr) {
-                const uint4 w = rng_block(key, node, kStreamBonus, (uint32_t)((v0 + i) >> 2));
-                const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    if (!(a[j][e] > -INFINITY)) continue;
-                    const double k = (double)a[j][e] + (double)gumbel_f32(ws[e]);
-                    const int v = v0 + i + e;
-                    if (k > s.key || (k == s.key && v < s.tok)) {
-                        s.key = k;
-                        s.tok = v;
-                    }
-                }
-            }
-        }
-        double b = s.key;
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) b = fmax(b, __shfl_xor(b, o, kWave));
-        wave_best = b;
+    for (int j = 0; j < kNaiveBatch; ++j) {
+        const int i = (base + j * kNaiveThreads + (int)threadIdx.x) * 4;
+        const int valid = max(0, min(4, n - i));
+        raw_load4<DT>(target, trow + v0 + (valid ? i : 0), valid, VEC, a[j]);
     }
-    // workgroup argmax (key desc, token asc) and flags
-    double k = s.key;
-    int t = s.tok;
+}
+
+// Inverse of ordered_bits64 (for a key with cleared low bits: a value at
+// most that of the full key).
+__device__ __forceinline__ double from_ordered_bits64(uint64_t k) {
+    const uint64_t u = (k >> 63) ? (k & 0x7FFFFFFFFFFFFFFFull) : ~k;
+    return __longlong_as_double((long long)u);
+}
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t k) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
-        const double ok = __shfl_xor(k, o, kWave);
-        const int ot = __shfl_xor(t, o, kWave);
+        const uint64_t ok = ((uint64_t)__shfl_xor((uint32_t)(k >> 32), o, kWave) << 32) |
+                            (uint32_t)__shfl_xor((uint32_t)k, o, kWave);
+        k = ok > k ? ok : k;
+    }
+    return k;
+}
+
+// Scores one batch. A group of four tokens whose largest logit, even with
+// the largest Gumbel value, stays below the wave's best key so far or below
+// the smallest key the largest logit of the batch can get, is skipped
+// without drawing its random numbers: its tokens lose strictly to a key the
+// wave keeps, so the result is the exact argmax. Groups are scored one at a
+// time (scheduling barriers keep the random numbers of one group in flight).
+template <int DT>
+__device__ __forceinline__ void score_batch(const Raw4<DT> (&raw)[kNaiveBatch], int v0, int n, int base, float invT,
+                                            const RngKey& key, uint32_t node, SliceBest& s) {
+    float gm[kNaiveBatch], bm = -INFINITY;
+#pragma unroll
+    for (int j = 0; j < kNaiveBatch; ++j) {
+        const int i = (base + j * kNaiveThreads + (int)threadIdx.x) * 4;
+        float a[4];
+        raw_scaled4<DT>(raw[j], max(0, min(4, n - i)), invT, a);
+        gm[j] = -INFINITY;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            s.bad |= (isnan(a[e]) || a[e] == INFINITY) ? 1 : 0;
+            s.has |= (a[e] > -INFINITY && a[e] < INFINITY) ? 1 : 0;
+            gm[j] = fmaxf(gm[j], a[e]);
+        }
+        bm = fmaxf(bm, gm[j]);
+    }
+    bm = wave_max(bm);
+    const uint64_t wk = wave_max_u64(s.key);
+    const double wave_best = wk ? from_ordered_bits64(wk) : -INFINITY;
+    const double thr = fmax(wave_best, bm < INFINITY ? (double)bm + (double)kGumbelMinBound : -INFINITY);
+#pragma unroll
+    for (int j = 0; j < kNaiveBatch; ++j) {
+        __builtin_amdgcn_sched_barrier(0);
+        if (!(gm[j] > -INFINITY && (double)gm[j] + (double)kGumbelMaxBound >= thr)) continue;
+        const int i = (base + j * kNaiveThreads + (int)threadIdx.x) * 4;
+        float a[4];
+        raw_scaled4<DT>(raw[j], max(0, min(4, n - i)), invT, a);
+        const uint4 w = rng_block(key, node, kStreamBonus, (uint32_t)((v0 + i) >> 2));
+        const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            if (!(a[e] > -INFINITY)) continue;
+            const uint64_t k = sample_key(a[e], gumbel_f32(ws[e]));
+            const uint32_t v = (uint32_t)(v0 + i + e);
+            if (k > s.key || (k == s.key && v < s.tok)) {
+                s.key = k;
+                s.tok = v;
+            }
+        }
+    }
+}
+
+// Workgroup-wide reduction of the per-thread results (key desc, token asc).
+__device__ SliceBest reduce_slice(const SliceBest& s) {
+    uint64_t k = s.key;
+    uint32_t t = s.tok;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const uint64_t ok = ((uint64_t)__shfl_xor((uint32_t)(k >> 32), o, kWave) << 32) |
+                            (uint32_t)__shfl_xor((uint32_t)k, o, kWave);
+        const uint32_t ot = (uint32_t)__shfl_xor((int)t, o, kWave);
         if (ok > k || (ok == k && ot < t)) {
             k = ok;
             t = ot;
         }
     }
     const int bad = wave_or(s.bad), has = wave_or(s.has);
-    __shared__ double rk[kNaiveThreads / kWave];
-    __shared__ int rt[kNaiveThreads / kWave], rb[kNaiveThreads / kWave], rh[kNaiveThreads / kWave];
+    __shared__ uint64_t rk[kNaiveThreads / kWave];
+    __shared__ uint32_t rt[kNaiveThreads / kWave];
+    __shared__ int rf[kNaiveThreads / kWave];
     const int wv = threadIdx.x / kWave;
     if ((threadIdx.x % kWave) == 0) {
         rk[wv] = k;
         rt[wv] = t;
-        rb[wv] = bad;
-        rh[wv] = has;
+        rf[wv] = bad | (has << 1);
     }
     __syncthreads();
-    SliceBest r{rk[0], rt[0], rb[0], rh[0]};
+    SliceBest r{rk[0], rt[0], rf[0] & 1, (rf[0] >> 1) & 1};
     for (int i = 1; i < kNaiveThreads / kWave; ++i) {
         if (rk[i] > r.key || (rk[i] == r.key && rt[i] < r.tok)) {
             r.key = rk[i];
             r.tok = rt[i];
         }
-        r.bad |= rb[i];
-        r.has |= rh[i];
+        r.bad |= rf[i] & 1;
+        r.has |= (rf[i] >> 1) & 1;
     }
     __syncthreads();
     return r;
 }
 
-// Exchange of the slice results among the G workgroups of request r; all
-// of them get the same reduced result (argmax in a fixed order).
-__device__ SliceBest naive_exchange(const NaiveArgs& A, int r, int g, int G, uint32_t* nb, int* timeout,
-                                    const SliceBest& mine) {
-    const int slot = (r * 2 + (*nb & 1)) * kWalkGroupsMax + g;
-    if (threadIdx.x == 0) {
-        __hip_atomic_store(&A.zpart[(size_t)slot * 4 + 0], mine.key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&A.zpart[(size_t)slot * 4 + 1], (double)(mine.bad | (mine.has << 1)), __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&A.bidx[slot], mine.tok, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    ++*nb;
-    request_barrier(&A.counters[r], *nb * (uint32_t)G, timeout);
+__device__ __forceinline__ uint64_t* naive_slot(const NaiveArgs& A, int r, int parity, int g) {
+    return A.slots + ((size_t)(r * 2 + parity) * kWalkGroupsMax + g) * 2;
+}
+
+__device__ __forceinline__ uint32_t round_tag(uint32_t seq, uint32_t e) { return (seq << 7) | (e + 1u); }
+
+// Publishes this workgroup's result of round e (thread 0).
+__device__ __forceinline__ void naive_publish(const NaiveArgs& A, int r, int g, uint32_t seq, uint32_t e,
+                                              const SliceBest& mine) {
+    if (threadIdx.x != 0) return;
+    const uint64_t v = round_tag(seq, e);
+    uint64_t* s = naive_slot(A, r, e & 1, g);
+    __hip_atomic_store(&s[0], (mine.key & ~kTagBits0) | (v & kTagBits0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&s[1],
+                       ((uint64_t)mine.tok << 33) | ((uint64_t)mine.has << 32) | ((uint64_t)mine.bad << 31) |
+                           (v & kTagBits1),
+                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Collects round e from the G workgroups of request r: wave 0 polls the
+// slots (lane h: slots h and h + 64) until both words of each carry the
+// round's tag (bounded: a wait past the limit sets *timeout), reduces them
+// in a fixed order and hands the result to the other waves.
+__device__ SliceBest naive_collect(const NaiveArgs& A, int r, int G, uint32_t seq, uint32_t e, int* timeout) {
     __shared__ SliceBest s_res;
+    __shared__ int s_to;
     if (threadIdx.x < kWave) {
         const int lane = threadIdx.x;
-        double k = -INFINITY;
-        int t = 0x7FFFFFFF, fl = 0;
+        const uint64_t v = round_tag(seq, e);
+        uint64_t k = 0ull;
+        uint32_t t = 0xFFFFFFFFu;
+        int bad = 0, has = 0, to = 0;
 #pragma unroll
         for (int half = 0; half < kWalkGroupsMax / kWave; ++half) {
             const int h = lane + half * kWave;
             if (h < G) {
-                const int sl = (r * 2 + ((*nb - 1) & 1)) * kWalkGroupsMax + h;
-                const double kk = __hip_atomic_load(&A.zpart[(size_t)sl * 4 + 0], __ATOMIC_RELAXED,
-                                                    __HIP_MEMORY_SCOPE_AGENT);
-                const double ff = __hip_atomic_load(&A.zpart[(size_t)sl * 4 + 1], __ATOMIC_RELAXED,
-                                                    __HIP_MEMORY_SCOPE_AGENT);
-                const int tt = __hip_atomic_load(&A.bidx[sl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                fl |= (int)ff;
+                const uint64_t* s = naive_slot(A, r, e & 1, h);
+                uint64_t w0, w1;
+                uint32_t spins = 0;
+                while (true) {
+                    w0 = __hip_atomic_load(&s[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    w1 = __hip_atomic_load(&s[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if ((w0 & kTagBits0) == (v & kTagBits0) && (w1 & kTagBits1) == (v & kTagBits1)) break;
+                    if (++spins > (1u << 20)) {
+                        to = 1;
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(1);
+                }
+                const uint64_t kk = w0 & ~kTagBits0;
+                const uint32_t tt = (uint32_t)(w1 >> 33);
+                bad |= (int)((w1 >> 31) & 1ull);
+                has |= (int)((w1 >> 32) & 1ull);
                 if (kk > k || (kk == k && tt < t)) {
                     k = kk;
                     t = tt;
@@ -209,24 +278,32 @@ __device__ SliceBest naive_exchange(const NaiveArgs& A, int r, int g, int G, uin
         }
 #pragma unroll
         for (int o = 32; o > 0; o >>= 1) {
-            const double ok = __shfl_xor(k, o, kWave);
-            const int ot = __shfl_xor(t, o, kWave);
+            const uint64_t ok = ((uint64_t)__shfl_xor((uint32_t)(k >> 32), o, kWave) << 32) |
+                                (uint32_t)__shfl_xor((uint32_t)k, o, kWave);
+            const uint32_t ot = (uint32_t)__shfl_xor((int)t, o, kWave);
             if (ok > k || (ok == k && ot < t)) {
                 k = ok;
                 t = ot;
             }
         }
-        fl = wave_or(fl);
-        if (lane == 0) s_res = SliceBest{k, t, fl & 1, (fl >> 1) & 1};
+        bad = wave_or(bad);
+        has = wave_or(has);
+        to = wave_or(to);
+        if (lane == 0) {
+            s_res = SliceBest{k, t, bad, has};
+            s_to = to;
+        }
     }
     __syncthreads();
     const SliceBest res = s_res;
-    __syncthreads();  // s_res is rewritten by the next exchange
+    if (s_to) *timeout = 1;
+    __syncthreads();  // s_res is rewritten by the next round
     return res;
 }
 
 template <int DT, bool VEC>
 __global__ __launch_bounds__(kNaiveThreads) void verify_naive(NaiveArgs A) {
+    __shared__ int s_nc[kNaiveNodes], s_fc[kNaiveNodes], s_tok[kNaiveNodes];
     const int g = blockIdx.x;
     const int G = gridDim.x;
     const int r = A.r0 + blockIdx.y;
@@ -242,6 +319,8 @@ __global__ __launch_bounds__(kNaiveThreads) void verify_naive(NaiveArgs A) {
     const bool has_slice = (long long)g * span < A.V;
     const int v0 = has_slice ? g * span : 0;
     const int v1 = has_slice ? min(A.V, v0 + span) : 0;
+    const int ns = v1 - v0;
+    const bool single = ns <= kNaiveBatchTokens;  // the slice is one batch: its loads are issued at once
 
     const bool plan_bad = (*status_p & TSB_REQ_NONFINITE) != 0;
     int nacc = 0, bonus = -1, add_status = 0;
@@ -251,24 +330,44 @@ __global__ __launch_bounds__(kNaiveThreads) void verify_naive(NaiveArgs A) {
         key.k1 = A.k1;
         key.request = (uint32_t)r;
         key.step = A.step;
-        uint32_t nb = 0;
         int timeout = 0;
+        const uint32_t seq = A.seqs[r];
+        Raw4<DT> cur[kNaiveBatch];
+        if (single) load_batch<DT, VEC>(A.target, tb * (size_t)A.V, v0, ns, 0, cur);
+        // the request's tree (children and node tokens) in LDS
+        for (int i = tid; i < n; i += kNaiveThreads) {
+            s_nc[i] = A.tree.n_children[tb + i];
+            s_fc[i] = A.tree.first_child[tb + i];
+            s_tok[i] = A.node_tok[tb + i];
+        }
+        __syncthreads();
         int u = 0;
-        while (true) {
+        uint32_t e = 0;
+        for (;; ++e) {
             const size_t trow = ((size_t)r * B1 + u) * (size_t)A.V;
-            const SliceBest mine = slice_sample<DT, VEC>(A, trow, v0, v1, key, (uint32_t)u);
-            const SliceBest all = naive_exchange(A, r, g, G, &nb, &timeout, mine);
+            SliceBest mine{0ull, 0xFFFFFFFFu, 0, 0};
+            if (single) {
+                score_batch<DT>(cur, v0, ns, 0, A.invT, key, (uint32_t)u, mine);
+            } else {
+                for (int base = 0; base * 4 < ns; base += kNaiveBatch * kNaiveThreads) {
+                    load_batch<DT, VEC>(A.target, trow, v0, ns, base, cur);
+                    score_batch<DT>(cur, v0, ns, base, A.invT, key, (uint32_t)u, mine);
+                }
+            }
+            naive_publish(A, r, g, seq, e, reduce_slice(mine));
+            const int m = s_nc[u];
+            const int fc = s_fc[u];
+            const bool may_descend = m > 0 && fc > u && fc + m <= n && nacc < A.D;
+            const SliceBest all = naive_collect(A, r, G, seq, e, &timeout);
             if (all.bad || !all.has) {
                 add_status |= TSB_REQ_NONFINITE;
                 break;
             }
-            const int y = all.tok;
-            const int m = A.tree.n_children[tb + u];
-            const int fc = A.tree.first_child[tb + u];
+            const int y = (int)all.tok;
             int match = -1;
-            if (m > 0 && fc > u && fc + m <= n && nacc < A.D)
+            if (may_descend)
                 for (int j = 0; j < m; ++j)
-                    if (A.node_tok[tb + fc + j] == y) {
+                    if (s_tok[fc + j] == y) {
                         match = fc + j;
                         break;
                     }
@@ -282,7 +381,16 @@ __global__ __launch_bounds__(kNaiveThreads) void verify_naive(NaiveArgs A) {
             }
             ++nacc;
             u = match;
+            if (single) load_batch<DT, VEC>(A.target, ((size_t)r * B1 + u) * (size_t)A.V, v0, ns, 0, cur);
         }
+        // every workgroup has read round e - 1: clear this workgroup's slot of
+        // that parity; the next call of this request uses the next sequence
+        if (tid == 0) {
+            uint64_t* sl = naive_slot(A, r, (e + 1) & 1, g);
+            __hip_atomic_store(&sl[0], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&sl[1], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        if (lead) A.seqs[r] = seq + 1u;
         if (timeout) add_status |= TSB_REQ_WALK_TIMEOUT;
     } else {
         add_status |= TSB_REQ_NONFINITE;
@@ -336,16 +444,14 @@ static hipError_t naive_capacity(const void* fn, int dt, int vec, int* cap) {
 hipError_t launch_verify_naive(const tsb_config& c, float invT, const void* target, const tsb_tree& tree,
                                const int32_t* node_tok, uint32_t step, const tsb_verdict& out, char* ws,
                                hipStream_t st) {
-    const Geometry geo = geometry(c);
-    const VerifyWs w = verify_ws(c);
     NaiveArgs A;
     A.target = target;
     A.tree = tree;
     A.node_tok = node_tok;
     A.out = out;
-    A.counters = (uint32_t*)(ws + w.counter);
-    A.zpart = (double*)(ws + w.zpart);
-    A.bidx = (int*)(ws + w.bidx);
+    const NaiveWs nw = naive_ws(c);
+    A.seqs = (uint32_t*)(ws + nw.seq);
+    A.slots = (uint64_t*)(ws + nw.slots);
     A.V = c.V;
     A.D = c.D;
     A.B = c.B;
@@ -364,13 +470,15 @@ hipError_t launch_verify_naive(const tsb_config& c, float invT, const void* targ
     hipError_t e = naive_capacity(fn, c.dtype == TSB_BF16 ? 1 : 0, vec ? 1 : 0, &cap);
     if (e != hipSuccess) return e;
     if (cap < 1) return hipErrorLaunchOutOfResources;
-    int G = geo.G;
-    if (G > cap) G = cap;
+    // workgroups per request: enough that a slice is one batch, within what
+    // keeps the whole batch resident (then one launch covers every request)
+    const int need = (c.V + kNaiveBatchTokens - 1) / kNaiveBatchTokens;
+    int G = cap / c.R;
+    if (G > need) G = need;
+    if (G > kWalkGroupsMax) G = kWalkGroupsMax;
+    if (G < 1) G = 1;
     const int chunk = cap / G;
 
-    naive_clear<<<(c.R + kBlock - 1) / kBlock < 64 ? (c.R + kBlock - 1) / kBlock : 64, kBlock, 0, st>>>(A.counters,
-                                                                                                      c.R);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = hook_before(TSB_KERNEL_VERIFY_NAIVE, st)) != hipSuccess) return e;
     for (int r0 = 0; r0 < c.R; r0 += chunk) {
         A.r0 = r0;

@@ -242,6 +242,57 @@ __device__ __forceinline__ void load4(const void* base, size_t off, int valid, b
     }
 }
 
+// Four logits as loaded (bf16 pairs or binary32), so the loads of a pass can
+// be issued early and converted later.
+template <int DT>
+struct Raw4 {
+    uint32_t w[DT == TSB_BF16 ? 2 : 4];
+};
+
+template <int DT>
+__device__ __forceinline__ void raw_load4(const void* base, size_t off, int valid, bool vec, Raw4<DT>& g) {
+    if (vec && valid == 4) {
+        if (DT == TSB_BF16) {
+            const uint2 raw = *(const uint2*)((const uint16_t*)base + off);
+            g.w[0] = raw.x;
+            g.w[1] = raw.y;
+        } else {
+            const uint4 raw = *(const uint4*)((const float*)base + off);
+            g.w[0] = raw.x;
+            g.w[1] = raw.y;
+            g.w[2] = raw.z;
+            g.w[3] = raw.w;
+        }
+    } else {
+        float x[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[e] = e < valid ? load_logit<DT>(base, off + e) : -INFINITY;
+        if (DT == TSB_BF16) {  // a bf16 value is the top half of its binary32 value
+            g.w[0] = (__float_as_uint(x[0]) >> 16) | (__float_as_uint(x[1]) & 0xFFFF0000u);
+            g.w[1] = (__float_as_uint(x[2]) >> 16) | (__float_as_uint(x[3]) & 0xFFFF0000u);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) g.w[e] = __float_as_uint(x[e]);
+        }
+    }
+}
+
+template <int DT>
+__device__ __forceinline__ void raw_scaled4(const Raw4<DT>& g, int valid, float invT, float a[4]) {
+    float x[4];
+    if (DT == TSB_BF16) {
+        x[0] = __uint_as_float(g.w[0] << 16);
+        x[1] = __uint_as_float(g.w[0] & 0xFFFF0000u);
+        x[2] = __uint_as_float(g.w[1] << 16);
+        x[3] = __uint_as_float(g.w[1] & 0xFFFF0000u);
+    } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[e] = __uint_as_float(g.w[e]);
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) a[e] = e < valid ? x[e] * invT : -INFINITY;
+}
+
 // A descending list of the `k` (<= 64) largest uint64 keys seen so far,
 // one entry per lane (lane i holds the i-th largest; lanes >= k hold 0).
 // Key 0 is reserved as "empty". An insertion is a ballot for the position

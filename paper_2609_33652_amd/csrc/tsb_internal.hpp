@@ -114,4 +114,27 @@ inline VerifyWs verify_ws(const tsb_config& c) {
     return w;
 }
 
+// Region that naive verification keeps across calls, after every stage's
+// scratch (no other stage writes it): a sequence number per request and the
+// exchange slots, [R][2][kWalkGroupsMax] pairs of 64-bit words.
+struct NaiveWs {
+    size_t seq, slots, total;
+};
+
+inline size_t stage_ws_bytes(const tsb_config& c) {
+    size_t m = plan_ws(c).total;
+    const size_t b = replay_ws(c).total, v = verify_ws(c).total;
+    m = m > b ? m : b;
+    return m > v ? m : v;
+}
+
+inline NaiveWs naive_ws(const tsb_config& c) {
+    NaiveWs w;
+    size_t o = align256(stage_ws_bytes(c));
+    w.seq = o; o = align256(o + (size_t)c.R * sizeof(uint32_t));
+    w.slots = o; o = align256(o + (size_t)c.R * 2 * kWalkGroupsMax * 2 * sizeof(uint64_t));
+    w.total = o;
+    return w;
+}
+
 }  // namespace tsb

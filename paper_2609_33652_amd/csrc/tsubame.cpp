@@ -95,11 +95,7 @@ size_t tsb_workspace_bytes(const tsb_config* cfg) {
     const tsb_status s = check_config(cfg);
     memcpy(g_last_error, saved, sizeof saved);
     if (s != TSB_OK) return 0;
-    const size_t a = tsb::plan_ws(*cfg).total;
-    const size_t b = tsb::replay_ws(*cfg).total;
-    const size_t c = tsb::verify_ws(*cfg).total;
-    size_t m = a > b ? a : b;
-    m = m > c ? m : c;
+    const size_t m = tsb::naive_ws(*cfg).total;
     return m < 256 ? 256 : m;
 }
 
