@@ -18,12 +18,13 @@
 //   verify_naive   resident grid, G workgroups per request, each owning a
 //                  slice of the vocabulary; per visited node one read of its
 //                  slice, the local best key, one exchange of (key, token,
-//                  finiteness) through tagged slots that the workgroups poll.
+//                  finiteness) through the tagged slots of the request.
 #include <math.h>
 
 #include <atomic>
 
 #include "tsb_device.hpp"
+#include "tsb_exchange.hpp"
 #include "tsb_kernels.hpp"
 
 namespace tsb {
@@ -51,27 +52,12 @@ constexpr int kNaiveBatch = 3;  // groups of four tokens per thread per batch
 constexpr int kNaiveBatchTokens = kNaiveBatch * 4 * kNaiveThreads;
 constexpr int kNaiveNodes = TSB_MAX_B + 1;
 
-// Exchange slots: [R][2][kWalkGroupsMax] pairs of 64-bit words (slot
-// parity = round & 1), written by one relaxed agent-scope store each and
-// polled by the readers. Both words carry a tag of (request sequence number,
-// round), so a reader knows when it holds both words of the current round
-// with no ordering between them and no clearing between calls:
-//   v      = seq << 7 | (round + 1)            (never 0; rounds <= TSB_MAX_D)
-//   word 0 = key with its low 16 bits replaced by v & 0xFFFF
-//   word 1 = token << 33 | has << 32 | bad << 31 | (v & 0x7FFFFFFF)
-// The sequence number of request r advances by one per call; at the end of
-// a call each workgroup zeroes its slot of the round before the last, so a
-// slot holds at most the last call's final round (tag of an older sequence).
-constexpr uint64_t kTagBits0 = 0xFFFFull;
-constexpr uint64_t kTagBits1 = 0x7FFFFFFFull;
-
 struct NaiveArgs {
     const void* target;
     tsb_tree tree;
     const int32_t* node_tok;
     tsb_verdict out;
-    uint32_t* seqs;   // [R]
-    uint64_t* slots;  // [R][2][kWalkGroupsMax][2]
+    XRegion X;  // exchange slots and per-request sequence numbers
     int V, D, B, r0;
     float invT;
     uint32_t k0, k1, step;
@@ -84,12 +70,12 @@ __device__ __forceinline__ uint64_t ordered_bits64(double x) {
     return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
 }
 
-// Keys are compared as ordered_bits64(fl32(a) + G) with the low 16 bits
-// cleared (word 0 of a slot carries the tag there): relative resolution
-// 2^-36 of the binary64 sum; keys equal after clearing go to the smaller
+// Keys are compared as ordered_bits64(fl32(a) + G) with the low 8 bits
+// cleared (an exchanged word carries its tag there): relative resolution
+// 2^-44 of the binary64 sum; keys equal after clearing go to the smaller
 // token.
 __device__ __forceinline__ uint64_t sample_key(float a, float gumbel) {
-    return ordered_bits64((double)a + (double)gumbel) & ~kTagBits0;
+    return ordered_bits64((double)a + (double)gumbel) & ~kTagMask;
 }
 
 // Local result of one slice: best key and its token (smallest id among equal
@@ -217,35 +203,18 @@ __device__ SliceBest reduce_slice(const SliceBest& s) {
     return r;
 }
 
-__device__ __forceinline__ uint64_t* naive_slot(const NaiveArgs& A, int r, int parity, int g) {
-    return A.slots + ((size_t)(r * 2 + parity) * kWalkGroupsMax + g) * 2;
-}
-
-__device__ __forceinline__ uint32_t round_tag(uint32_t seq, uint32_t e) { return (seq << 7) | (e + 1u); }
-
-// Publishes this workgroup's result of round e (thread 0).
-__device__ __forceinline__ void naive_publish(const NaiveArgs& A, int r, int g, uint32_t seq, uint32_t e,
-                                              const SliceBest& mine) {
-    if (threadIdx.x != 0) return;
-    const uint64_t v = round_tag(seq, e);
-    uint64_t* s = naive_slot(A, r, e & 1, g);
-    __hip_atomic_store(&s[0], (mine.key & ~kTagBits0) | (v & kTagBits0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(&s[1],
-                       ((uint64_t)mine.tok << 33) | ((uint64_t)mine.has << 32) | ((uint64_t)mine.bad << 31) |
-                           (v & kTagBits1),
-                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// Collects round e from the G workgroups of request r: wave 0 polls the
-// slots (lane h: slots h and h + 64) until both words of each carry the
-// round's tag (bounded: a wait past the limit sets *timeout), reduces them
-// in a fixed order and hands the result to the other waves.
-__device__ SliceBest naive_collect(const NaiveArgs& A, int r, int G, uint32_t seq, uint32_t e, int* timeout) {
+// Round e of request r: publish this workgroup's result, then wave 0 polls
+// the G slots (lane h: slots h and h + 64), reduces them in a fixed order
+// (key desc, token asc; flags or-ed) and hands the result to the other waves.
+// Slot words: key, token << 32 | has << 9 | bad << 8.
+__device__ SliceBest naive_round(const NaiveArgs& A, int r, int g, int G, uint32_t seq, uint32_t e,
+                                 const SliceBest& mine, int* timeout) {
+    const uint64_t w[2] = {mine.key, xpack_u32(mine.tok) | ((uint64_t)mine.has << 9) | ((uint64_t)mine.bad << 8)};
+    xpublish<2>(A.X, r, g, seq, e, w);
     __shared__ SliceBest s_res;
     __shared__ int s_to;
     if (threadIdx.x < kWave) {
         const int lane = threadIdx.x;
-        const uint64_t v = round_tag(seq, e);
         uint64_t k = 0ull;
         uint32_t t = 0xFFFFFFFFu;
         int bad = 0, has = 0, to = 0;
@@ -253,23 +222,12 @@ __device__ SliceBest naive_collect(const NaiveArgs& A, int r, int G, uint32_t se
         for (int half = 0; half < kWalkGroupsMax / kWave; ++half) {
             const int h = lane + half * kWave;
             if (h < G) {
-                const uint64_t* s = naive_slot(A, r, e & 1, h);
-                uint64_t w0, w1;
-                uint32_t spins = 0;
-                while (true) {
-                    w0 = __hip_atomic_load(&s[0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    w1 = __hip_atomic_load(&s[1], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    if ((w0 & kTagBits0) == (v & kTagBits0) && (w1 & kTagBits1) == (v & kTagBits1)) break;
-                    if (++spins > (1u << 20)) {
-                        to = 1;
-                        break;
-                    }
-                    __builtin_amdgcn_s_sleep(1);
-                }
-                const uint64_t kk = w0 & ~kTagBits0;
-                const uint32_t tt = (uint32_t)(w1 >> 33);
-                bad |= (int)((w1 >> 31) & 1ull);
-                has |= (int)((w1 >> 32) & 1ull);
+                uint64_t q[2];
+                if (!xpoll<2>(A.X, r, h, seq, e, q)) to = 1;
+                const uint64_t kk = q[0] & ~kTagMask;
+                const uint32_t tt = xunpack_u32(q[1]);
+                bad |= (int)((q[1] >> 8) & 1ull);
+                has |= (int)((q[1] >> 9) & 1ull);
                 if (kk > k || (kk == k && tt < t)) {
                     k = kk;
                     t = tt;
@@ -331,7 +289,7 @@ __global__ __launch_bounds__(kNaiveThreads) void verify_naive(NaiveArgs A) {
         key.request = (uint32_t)r;
         key.step = A.step;
         int timeout = 0;
-        const uint32_t seq = A.seqs[r];
+        const uint32_t seq = A.X.seqs[r];
         Raw4<DT> cur[kNaiveBatch];
         if (single) load_batch<DT, VEC>(A.target, tb * (size_t)A.V, v0, ns, 0, cur);
         // the request's tree (children and node tokens) in LDS
@@ -354,11 +312,10 @@ __global__ __launch_bounds__(kNaiveThreads) void verify_naive(NaiveArgs A) {
                     score_batch<DT>(cur, v0, ns, base, A.invT, key, (uint32_t)u, mine);
                 }
             }
-            naive_publish(A, r, g, seq, e, reduce_slice(mine));
             const int m = s_nc[u];
             const int fc = s_fc[u];
             const bool may_descend = m > 0 && fc > u && fc + m <= n && nacc < A.D;
-            const SliceBest all = naive_collect(A, r, G, seq, e, &timeout);
+            const SliceBest all = naive_round(A, r, g, G, seq, e, reduce_slice(mine), &timeout);
             if (all.bad || !all.has) {
                 add_status |= TSB_REQ_NONFINITE;
                 break;
@@ -383,14 +340,7 @@ __global__ __launch_bounds__(kNaiveThreads) void verify_naive(NaiveArgs A) {
             u = match;
             if (single) load_batch<DT, VEC>(A.target, ((size_t)r * B1 + u) * (size_t)A.V, v0, ns, 0, cur);
         }
-        // every workgroup has read round e - 1: clear this workgroup's slot of
-        // that parity; the next call of this request uses the next sequence
-        if (tid == 0) {
-            uint64_t* sl = naive_slot(A, r, (e + 1) & 1, g);
-            __hip_atomic_store(&sl[0], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(&sl[1], 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-        if (lead) A.seqs[r] = seq + 1u;
+        xfinish(A.X, r, g, G, seq, e + 1);
         if (timeout) add_status |= TSB_REQ_WALK_TIMEOUT;
     } else {
         add_status |= TSB_REQ_NONFINITE;
@@ -419,7 +369,7 @@ hipError_t launch_first_tokens(const tsb_config& c, const int32_t* topk_tok, con
 
 // Workgroups of verify_naive resident at once on the current device, queried
 // once per (device, kernel instance); every launch stays within it so the
-// barriers of a request complete.
+// exchanges of a request complete.
 static hipError_t naive_capacity(const void* fn, int dt, int vec, int* cap) {
     constexpr int kDevs = 64;
     static std::atomic<int> cached[kDevs][2][2];
@@ -449,9 +399,9 @@ hipError_t launch_verify_naive(const tsb_config& c, float invT, const void* targ
     A.tree = tree;
     A.node_tok = node_tok;
     A.out = out;
-    const NaiveWs nw = naive_ws(c);
-    A.seqs = (uint32_t*)(ws + nw.seq);
-    A.slots = (uint64_t*)(ws + nw.slots);
+    const XchgWs xw = xchg_ws(c);
+    A.X.seqs = (uint32_t*)(ws + xw.seq);
+    A.X.slots = (uint64_t*)(ws + xw.slots);
     A.V = c.V;
     A.D = c.D;
     A.B = c.B;

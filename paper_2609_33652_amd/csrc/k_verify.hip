@@ -9,7 +9,8 @@
 //                    workgroups of a request replay the same scalar walk;
 //                    every vocabulary-wide reduction of the walk (residual
 //                    mass after a rejection, the bonus draw) is split over
-//                    them and exchanged through a per-request barrier.
+//                    them and exchanged through the request's tagged slots
+//                    (each workgroup polls the others' slots).
 //
 // Closed form of WoR-RRS used by the walk (equal to the literal recursion
 // of residuals; derived from eq. (1) and the without-replacement update):
@@ -24,6 +25,7 @@
 #include <atomic>
 
 #include "tsb_device.hpp"
+#include "tsb_exchange.hpp"
 #include "tsb_kernels.hpp"
 
 namespace tsb {
@@ -111,7 +113,7 @@ __global__ __launch_bounds__(kBlock) void target_partials(const void* __restrict
                                                           long long chunk, int P, float invT,
                                                           const int32_t* __restrict__ n_nodes,
                                                           float* __restrict__ tm, double* __restrict__ ts,
-                                                          int* __restrict__ tf, uint32_t* __restrict__ counters) {
+                                                          int* __restrict__ tf) {
     const int g = blockIdx.x;
     const int tid = threadIdx.x;
     const long long N = (long long)nrows * V;
@@ -131,7 +133,6 @@ __global__ __launch_bounds__(kBlock) void target_partials(const void* __restrict
         const int gl = (int)((rb + V - 1) / chunk);  // and its last
         const size_t o = (size_t)t * P;
         if (g == gf && tid == 0) {
-            if (node == 0) counters[r] = 0u;
             for (int q = gl - gf + 1; q < P; ++q) {
                 tm[o + q] = -INFINITY;
                 ts[o + q] = 0.0;
@@ -180,10 +181,7 @@ struct WalkArgs {
     const float* tm;
     const double* ts;
     const int* tf;
-    uint32_t* counters;
-    double* zpart;
-    float* bkey;
-    int* bidx;
+    XRegion X;  // exchange slots and per-request sequence numbers
     int V, D, B, S4, r0;
     float invT;
     uint32_t k0, k1, step;
@@ -413,57 +411,54 @@ __device__ void bonus_from_p(const WalkArgs& A, bool vec, const WalkSlice& S, si
     *bi = bidx;
 }
 
-// Exchange among the G workgroups of a request: each contributes up to four
-// binary64 partials (and optionally a (key, token) pair); everyone gets the
-// sums (a fixed reduction tree over the workgroups, so every run adds in the
-// same order) and the best pair.
+// Exchange among the G workgroups of a request through the request's
+// tagged slots: each contributes up to four binary64 partials (and
+// optionally a (key, token) pair); everyone gets the sums (a fixed reduction
+// tree over the workgroups, so every run adds in the same order) and the
+// best pair. Partials travel with 2^-44 relative resolution.
 constexpr int kExVals = 4;
 
 struct Exchange {
     const WalkArgs* A;
     int r, g, G;
-    uint32_t nb;  // barriers passed
+    uint32_t seq;
+    uint32_t nb;  // rounds run
     int timeout;
 
-    template <int NV>
-    __device__ void run(const double (&part)[NV], double (&tot)[NV], float bk = 0.f, int bi = 0,
-                        float* fk = nullptr, int* fi = nullptr) {
+    template <int NV, bool BEST>
+    __device__ void run(const double (&part)[NV], double (&tot)[NV], float bk, int bi, float* fk, int* fi) {
         static_assert(NV <= kExVals, "exchange width");
-        const int slot = (r * 2 + (nb & 1)) * kWalkGroupsMax + g;
-        if (threadIdx.x == 0) {
+        constexpr int NW = NV + (BEST ? 2 : 0);
+        uint64_t w[NW];
 #pragma unroll
-            for (int i = 0; i < NV; ++i)
-                __hip_atomic_store(&A->zpart[(size_t)slot * kExVals + i], part[i], __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(&A->bkey[slot], bk, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            __hip_atomic_store(&A->bidx[slot], bi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        for (int i = 0; i < NV; ++i) w[i] = xpack_f64(part[i]);
+        if (BEST) {
+            w[NV] = xpack_u32(ordered_bits(bk));
+            w[NW - 1] = xpack_u32((uint32_t)bi);
         }
-        ++nb;
-        request_barrier(&A->counters[r], nb * (uint32_t)G, &timeout);
-        // wave 0 reads the G slots in parallel (lane h: slots h and h + 64),
-        // reduces them in a fixed order and hands the result to the others
+        xpublish<NW>(A->X, r, g, seq, nb, w);
+        // wave 0 polls the G slots (lane h: slots h and h + 64), reduces them
+        // in a fixed order and hands the result to the others
         __shared__ double s_tot[kExVals];
         __shared__ float s_bk;
-        __shared__ int s_bi;
+        __shared__ int s_bi, s_to;
         if (threadIdx.x < kWave) {
             const int lane = threadIdx.x;
             double v[NV];
-            float kb = -INFINITY;
-            int ib = 0x7FFFFFFF;
+            uint32_t kb = 0u, ib = 0xFFFFFFFFu;
+            int to = 0;
 #pragma unroll
             for (int i = 0; i < NV; ++i) v[i] = 0.0;
 #pragma unroll
             for (int half = 0; half < kWalkGroupsMax / kWave; ++half) {
                 const int h = lane + half * kWave;
                 if (h < G) {
-                    const int sl = (r * 2 + ((nb - 1) & 1)) * kWalkGroupsMax + h;
+                    uint64_t q[NW];
+                    if (!xpoll<NW>(A->X, r, h, seq, nb, q)) to = 1;
 #pragma unroll
-                    for (int i = 0; i < NV; ++i)
-                        v[i] += __hip_atomic_load(&A->zpart[(size_t)sl * kExVals + i], __ATOMIC_RELAXED,
-                                                  __HIP_MEMORY_SCOPE_AGENT);
-                    if (fk) {
-                        const float k = __hip_atomic_load(&A->bkey[sl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        const int ix = __hip_atomic_load(&A->bidx[sl], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    for (int i = 0; i < NV; ++i) v[i] += xunpack_f64(q[i]);
+                    if (BEST) {
+                        const uint32_t k = xunpack_u32(q[NV]), ix = xunpack_u32(q[NW - 1]);
                         if (k > kb || (k == kb && ix < ib)) {
                             kb = k;
                             ib = ix;
@@ -473,32 +468,40 @@ struct Exchange {
             }
 #pragma unroll
             for (int i = 0; i < NV; ++i) v[i] = wave_sum(v[i]);
-            if (fk) {
+            if (BEST) {
 #pragma unroll
                 for (int off = 32; off > 0; off >>= 1) {
-                    const float ok = __shfl_xor(kb, off, kWave);
-                    const int oi = __shfl_xor(ib, off, kWave);
+                    const uint32_t ok = (uint32_t)__shfl_xor((int)kb, off, kWave);
+                    const uint32_t oi = (uint32_t)__shfl_xor((int)ib, off, kWave);
                     if (ok > kb || (ok == kb && oi < ib)) {
                         kb = ok;
                         ib = oi;
                     }
                 }
             }
+            to = wave_or(to);
             if (lane == 0) {
 #pragma unroll
                 for (int i = 0; i < NV; ++i) s_tot[i] = v[i];
-                s_bk = kb;
-                s_bi = ib;
+                s_bk = kb ? from_ordered_bits(kb) : -INFINITY;
+                s_bi = (int)ib;
+                s_to = to;
             }
         }
         __syncthreads();
 #pragma unroll
         for (int i = 0; i < NV; ++i) tot[i] = s_tot[i];
-        if (fk) {
+        if (BEST) {
             *fk = s_bk;
             *fi = s_bi;
         }
+        if (s_to) timeout = 1;
+        ++nb;
         __syncthreads();  // s_tot is rewritten by the next exchange
+    }
+    template <int NV>
+    __device__ void run(const double (&part)[NV], double (&tot)[NV]) {
+        run<NV, false>(part, tot, 0.f, 0, nullptr, nullptr);
     }
     __device__ double sum(double part) {
         double p[1] = {part}, t[1];
@@ -509,7 +512,7 @@ struct Exchange {
         double p[1] = {part}, t[1];
         float fk;
         int fi;
-        run<1>(p, t, bk, bi, &fk, &fi);
+        run<1, true>(p, t, bk, bi, &fk, &fi);
         *tot = t[0];
         return fk > -INFINITY ? fi : -1;
     }
@@ -669,7 +672,7 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
         key.k1 = A.k1;
         key.request = (uint32_t)r;
         key.step = A.step;
-        Exchange X{&A, r, g, G, 0u, 0};
+        Exchange X{&A, r, g, G, A.X.seqs[r], 0u, 0};
         int u = 0;
         while (true) {
             const int m = A.tree.n_children[tb + u];
@@ -829,6 +832,7 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
             }
             break;
         }
+        if (X.nb > 0) xfinish(A.X, r, g, G, X.seq, X.nb);
         if (X.timeout) add_status |= TSB_REQ_WALK_TIMEOUT;
     }
 
@@ -885,7 +889,7 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
 // Workgroups of the walk that are resident at once on the current device
 // (one per CU: the LDS cache fills a CU). Every launch of the walk stays
 // within this, in order of requests, so all workgroups of a launch run
-// together and their barriers complete; the bounded spin of the barrier
+// together and every exchange completes; the bounded polling of an exchange
 // turns a device shared with other work (workgroups kept waiting) into
 // TSB_REQ_WALK_TIMEOUT instead of a hang. Queried once per (device,
 // kernel instance).
@@ -919,7 +923,6 @@ hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, con
     float* tm = (float*)(ws + w.tm);
     double* ts = (double*)(ws + w.ts);
     int* tf = (int*)(ws + w.tf);
-    uint32_t* counters = (uint32_t*)(ws + w.counter);
     const bool vec8 = (c.dtype == TSB_BF16) ? (c.V % 8 == 0 && ((uintptr_t)target & 15) == 0)
                                             : (c.V % 4 == 0 && ((uintptr_t)target & 15) == 0);
     const int nrows = c.R * (c.B + 1);
@@ -928,17 +931,17 @@ hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, con
     if (c.dtype == TSB_BF16) {
         if (vec8)
             target_partials<TSB_BF16, true><<<g.G4, kBlock, 0, st>>>(target, c.V, c.B, nrows, g.chunk4, g.S4, invT,
-                                                                     tree.n_nodes, tm, ts, tf, counters);
+                                                                     tree.n_nodes, tm, ts, tf);
         else
             target_partials<TSB_BF16, false><<<g.G4, kBlock, 0, st>>>(target, c.V, c.B, nrows, g.chunk4, g.S4, invT,
-                                                                      tree.n_nodes, tm, ts, tf, counters);
+                                                                      tree.n_nodes, tm, ts, tf);
     } else {
         if (vec8)
             target_partials<TSB_F32, true><<<g.G4, kBlock, 0, st>>>(target, c.V, c.B, nrows, g.chunk4, g.S4, invT,
-                                                                    tree.n_nodes, tm, ts, tf, counters);
+                                                                    tree.n_nodes, tm, ts, tf);
         else
             target_partials<TSB_F32, false><<<g.G4, kBlock, 0, st>>>(target, c.V, c.B, nrows, g.chunk4, g.S4, invT,
-                                                                     tree.n_nodes, tm, ts, tf, counters);
+                                                                     tree.n_nodes, tm, ts, tf);
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -954,10 +957,9 @@ hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, con
     A.tm = tm;
     A.ts = ts;
     A.tf = tf;
-    A.counters = counters;
-    A.zpart = (double*)(ws + w.zpart);
-    A.bkey = (float*)(ws + w.bkey);
-    A.bidx = (int*)(ws + w.bidx);
+    const XchgWs xw = xchg_ws(c);
+    A.X.seqs = (uint32_t*)(ws + xw.seq);
+    A.X.slots = (uint64_t*)(ws + xw.slots);
     A.V = c.V;
     A.D = c.D;
     A.B = c.B;

@@ -197,32 +197,6 @@ __device__ __forceinline__ double lane_f64(double v, int l) {
 }
 
 // ---------------------------------------------------------------- walk support
-// Per-request barrier over the G workgroups of a request: monotone counter,
-// bounded spin (a wait that exceeds the limit sets *timeout and proceeds).
-// Only the exchange slots cross workgroups, and they are written and read
-// with agent-scope atomics (coherent without L2 maintenance), so the
-// barrier needs no cache writeback or invalidation: the slot stores have
-// completed (s_waitcnt vmcnt(0)) before the counter is incremented, and a
-// reader issues its slot loads only after it has seen the count.
-__device__ inline void request_barrier(uint32_t* counter, uint32_t target, int* timeout) {
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this thread's slot stores are done
-        __atomic_signal_fence(__ATOMIC_SEQ_CST);
-        __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        uint32_t spins = 0;
-        while (__hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-            __builtin_amdgcn_s_sleep(2);
-            if (++spins > (1u << 23)) {
-                *timeout = 1;
-                break;
-            }
-        }
-        __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    }
-    __syncthreads();
-}
-
 template <int DT>
 __device__ __forceinline__ void load4(const void* base, size_t off, int valid, bool vec, float x[4]) {
     if (vec && valid == 4) {

@@ -67,8 +67,8 @@ struct PlanWs {  // row statistics partials
 struct ReplayWs {  // per (parent, tile) best keys, flat parent list, thresholds
     size_t cand, cnt, plist, ptotal, thr, total;
 };
-struct VerifyWs {  // target partials + walk exchange
-    size_t tm, ts, tf, counter, zpart, bkey, bidx, total;
+struct VerifyWs {  // target partials
+    size_t tm, ts, tf, total;
 };
 
 inline PlanWs plan_ws(const tsb_config& c) {
@@ -106,18 +106,15 @@ inline VerifyWs verify_ws(const tsb_config& c) {
     w.tm = o; o = align256(o + n * sizeof(float));
     w.ts = o; o = align256(o + n * sizeof(double));
     w.tf = o; o = align256(o + n * sizeof(int32_t));
-    w.counter = o; o = align256(o + (size_t)c.R * sizeof(uint32_t));
-    w.zpart = o; o = align256(o + (size_t)c.R * 2 * kWalkGroupsMax * 4 * sizeof(double));
-    w.bkey = o; o = align256(o + (size_t)c.R * 2 * kWalkGroupsMax * sizeof(float));
-    w.bidx = o; o = align256(o + (size_t)c.R * 2 * kWalkGroupsMax * sizeof(int32_t));
     w.total = o;
     return w;
 }
 
-// Region that naive verification keeps across calls, after every stage's
-// scratch (no other stage writes it): a sequence number per request and the
-// exchange slots, [R][2][kWalkGroupsMax] pairs of 64-bit words.
-struct NaiveWs {
+// Region that verification keeps across calls, after every stage's scratch
+// (no other stage writes it): a sequence number per request and the
+// exchange slots of the workgroups of a request, [R][2][kWalkGroupsMax][8]
+// 64-bit words.
+struct XchgWs {
     size_t seq, slots, total;
 };
 
@@ -128,11 +125,11 @@ inline size_t stage_ws_bytes(const tsb_config& c) {
     return m > v ? m : v;
 }
 
-inline NaiveWs naive_ws(const tsb_config& c) {
-    NaiveWs w;
+inline XchgWs xchg_ws(const tsb_config& c) {
+    XchgWs w;
     size_t o = align256(stage_ws_bytes(c));
     w.seq = o; o = align256(o + (size_t)c.R * sizeof(uint32_t));
-    w.slots = o; o = align256(o + (size_t)c.R * 2 * kWalkGroupsMax * 2 * sizeof(uint64_t));
+    w.slots = o; o = align256(o + (size_t)c.R * 2 * kWalkGroupsMax * 8 * sizeof(uint64_t));
     w.total = o;
     return w;
 }

@@ -95,7 +95,7 @@ size_t tsb_workspace_bytes(const tsb_config* cfg) {
     const tsb_status s = check_config(cfg);
     memcpy(g_last_error, saved, sizeof saved);
     if (s != TSB_OK) return 0;
-    const size_t m = tsb::naive_ws(*cfg).total;
+    const size_t m = tsb::xchg_ws(*cfg).total;
     return m < 256 ? 256 : m;
 }
 

@@ -259,3 +259,21 @@ def test_naive_deterministic_repeat():
         outs.append(rnd.host())
     for k in ("node_tok", "n_acc", "acc_tok", "bonus", "req_status"):
         assert torch.equal(outs[0][k], outs[1][k]), k
+
+
+def test_exchange_state_across_calls():
+    """Verification keeps exchange state in the workspace between calls: alternating RRS and naive
+    rounds on one workspace must give the same results as a fresh workspace for every call."""
+    cfg = W.config(2, R=4, V=20000, D=6, B=24, K=4, name="xstate")
+    base, sigma = W.base_rows(cfg, 0)
+    draft = W.draft_from_base(cfg, base).cuda()
+    target = W.target_from_base(cfg, base, sigma, torch.ones(4, 25, dtype=torch.int64)).cuda()
+    reused = make_round(cfg, 21, trace=False)
+    for i in range(12):
+        fresh = make_round(cfg, 21, trace=False)
+        kind = "step" if i % 3 != 2 else "step_first"
+        getattr(reused, kind)(draft, target, i)
+        getattr(fresh, kind)(draft, target, i)
+        a, b = reused.host(), fresh.host()
+        for k in ("node_tok", "n_acc", "acc_node", "acc_tok", "bonus", "req_status"):
+            assert torch.equal(a[k], b[k]), (i, kind, k)
