@@ -31,8 +31,9 @@
  *     tsb_workspace_bytes(cfg) bytes, 256-byte aligned. One workspace may be
  *     reused by successive calls on one stream; calls that overlap in time
  *     need separate workspaces. Zero-fill a workspace once, before its first
- *     use: its last part holds state that tsb_verify_naive keeps between
- *     calls (a sequence number per request and tagged exchange slots).
+ *     use, and again after any request reported TSB_REQ_WALK_TIMEOUT: its
+ *     last part holds state that verification keeps between calls (a
+ *     sequence number per request and tagged exchange slots).
  *   - Results are a deterministic function of (inputs, cfg.seed, step): the
  *     randomness is Philox4x32-10 (Salmon et al., SC'11) keyed by
  *     (seed, step, request, node, draw), independent of launch shapes.

@@ -11,11 +11,14 @@
 // never 0, different for rounds e and e - 2 of one slot, and different for
 // the previous call of the request (seq - 1).
 //
-// Invariant between calls: every slot of a request is zero or holds a
-// word of the previous call's last round. A call that ran rounds keeps it
-// with finish(): each workgroup zeroes its slot of the round before the
-// last (all workgroups have read it), the request's first workgroup zeroes
-// the slots of workgroups g >= G, and the sequence number advances.
+// Invariant between calls: every word of every slot of a request is zero
+// or belongs to the previous call's last round (a publish writes all words
+// of its slot). A call that ran rounds keeps it with xfinish(): each
+// workgroup zeroes its slot of the round before the last (all workgroups
+// have read it), the request's first workgroup zeroes the slots of
+// workgroups g >= G, and the sequence number advances. A wait that was
+// abandoned (TSB_REQ_WALK_TIMEOUT) voids the invariant for that request until
+// the caller zero-fills the workspace again.
 #pragma once
 
 #include "tsb_device.hpp"
@@ -46,16 +49,20 @@ __device__ __forceinline__ double xunpack_f64(uint64_t w) { return __longlong_as
 __device__ __forceinline__ uint64_t xpack_u32(uint32_t x) { return (uint64_t)x << 32; }
 __device__ __forceinline__ uint32_t xunpack_u32(uint64_t w) { return (uint32_t)(w >> 32); }
 
-// Thread 0 publishes NW payload words of round e.
+// Thread 0 publishes NW payload words of round e. The slot's other words get
+// the bare tag: every word of a slot then belongs to the round last written,
+// whatever the width of the exchanges before it (a word left from an older
+// round could otherwise carry a tag that matches again two calls later).
 template <int NW>
 __device__ __forceinline__ void xpublish(const XRegion& X, int r, int g, uint32_t seq, uint32_t e,
                                          const uint64_t (&w)[NW]) {
+    static_assert(NW <= kSlotWords, "slot width");
     if (threadIdx.x != 0) return;
     const uint64_t t = xtag(seq, e);
     uint64_t* s = xslot(X, r, e, g);
 #pragma unroll
-    for (int i = 0; i < NW; ++i)
-        __hip_atomic_store(&s[i], (w[i] & ~kTagMask) | t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    for (int i = 0; i < kSlotWords; ++i)
+        __hip_atomic_store(&s[i], i < NW ? ((w[i] & ~kTagMask) | t) : t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Polls the NW words of workgroup h's slot of round e until all carry the

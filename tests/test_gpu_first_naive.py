@@ -277,3 +277,29 @@ def test_exchange_state_across_calls():
         a, b = reused.host(), fresh.host()
         for k in ("node_tok", "n_acc", "acc_node", "acc_tok", "bonus", "req_status"):
             assert torch.equal(a[k], b[k]), (i, kind, k)
+
+
+def test_exchange_state_many_calls_full_size():
+    """Hundreds of rounds on one workspace (mixed exchange widths in the walk) against a workspace
+    zero-filled before every call: identical results and no abandoned wait. A stale slot word
+    accepted as current makes the workgroups of a request diverge, which shows up here."""
+    cfg = W.config(4)
+    base, sigma = W.base_rows(cfg, 0, device="cuda")
+    draft = W.draft_from_base(cfg, base)
+    a = make_round(cfg, W.replay_seed(4), trace=False)
+    b = make_round(cfg, W.replay_seed(4), trace=False)
+    a.plan(draft)
+    target = W.target_from_base(cfg, base, sigma, a.tree["depth"].long().clamp(min=0))
+    del base
+    flags = 0
+    for s in range(240):
+        kind = "step" if s % 5 else "step_first"
+        getattr(a, kind)(draft, target, s)
+        b.ws.zero_()
+        getattr(b, kind)(draft, target, s)
+        if s % 40 == 39:
+            say("exchange state: %d calls" % (s + 1))
+        flags |= int((a.req_status & tsb.REQ_WALK_TIMEOUT).any())
+        for k in ("n_acc", "acc_tok", "bonus", "req_status"):
+            assert torch.equal(getattr(a, k), getattr(b, k)), (s, kind, k)
+    assert flags == 0
