@@ -29,7 +29,7 @@ HBM_PEAK_GBS = 8000.0
 # HBM bytes per launch of target_partials at the batched workload from the
 # FETCH_SIZE / WRITE_SIZE counter passes (KiB, scaled by a plain copy of known
 # size: FETCH x2.0, WRITE x1.0), valid for the kernel source they were taken on
-TARGET_TRAFFIC = {"config": 4, "source_sha256_16": "123781335ee822c2", "fetch_kib": 309956.1, "write_kib": 267.7,
+TARGET_TRAFFIC = {"config": 4, "source_sha256_16": "d1240d8a06bfe313", "fetch_kib": 309788.3, "write_kib": 268.0,
                   "fetch_scale": 2.0, "write_scale": 1.0}
 
 
