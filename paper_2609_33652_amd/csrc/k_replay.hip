@@ -212,12 +212,19 @@ __global__ __launch_bounds__(kBlock) void replay_scan(const void* __restrict__ d
             load_b4<DT, VEC>(draft, tbase, gl * 4, valid ? tn : 0, invT, cd, bv);
             const uint4 w = rng_block(key, (uint32_t)u, kStreamReplay, blk0 + (uint32_t)gl);
             const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+            float kv[4];
+            bool hit = false;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const bool in = bv[e] >= bound && bv[e] > -INFINITY;
-                const float kv = in ? bv[e] + gumbel_f32(ws[e]) : -INFINITY;
-                top.offer(cand_key(kv, (uint32_t)(t0 + gl * 4 + e)), in && kv >= thr);
+                kv[e] = in ? bv[e] + gumbel_f32(ws[e]) : -INFINITY;
+                hit = hit || kv[e] >= thr;
             }
+            // most keys stay below thr: the list is touched only when one does not
+            if (__ballot(hit) == 0) continue;
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                top.offer(cand_key(kv[e], (uint32_t)(t0 + gl * 4 + e)), kv[e] >= thr && kv[e] > -INFINITY);
         }
         const size_t o = (size_t)node * (size_t)T + t;
         const int cnt = __popcll(__ballot(lane < m && top.v != 0));
