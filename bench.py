@@ -164,6 +164,33 @@ def first_naive(tsb, c, dev, drafts, targets, args, cfg):
     }
 
 
+def planner_ep(tsb, c, dev, drafts, targets, args, cfg, frontier=10):
+    """The expand-then-prune first pass (frontier 10) on the same inputs: planner latency and acceptance."""
+    import torch
+    R = cfg["R"]
+    P = len(drafts)
+    rnd = tsb.Round(c, dev)
+    kid = tsb.KERNELS.index("plan_tree")
+    for s in range(3):
+        rnd.plan_ep(drafts[s % P], frontier)
+    evs = events(args.breakdown_steps)
+    for i in range(args.breakdown_steps):
+        tsb.profile_kernel(kid, evs[i][0], evs[i][1])
+        rnd.plan_ep(drafts[i % P], frontier)
+        tsb.profile_kernel(kid, None)
+    torch.cuda.synchronize()
+    us = 1000.0 * sum(a.elapsed_time(b) for a, b in evs) / args.breakdown_steps
+    acc = 0
+    for i in range(P):
+        rnd.plan_ep(drafts[i], frontier)
+        rnd.replay(drafts[i], i)
+        rnd.verify(drafts[i], targets[i], i)
+        h = rnd.host()
+        acc += int(h["n_acc"].clamp(min=0).sum()) + int((h["n_acc"] >= 0).sum())
+    return {"frontier": frontier, "kernel": "plan_ep", "avg_launch_us": round(us, 2),
+            "tau_replay_rrs": round(acc / (P * R), 4)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -272,6 +299,7 @@ def main():
 
     first = first_naive(tsb, c, dev, drafts, targets, args, cfg)
     first["cpu_baseline"] = cpu_first
+    ep = planner_ep(tsb, c, dev, drafts, targets, args, cfg)
 
     b = 2 if cfg["dtype"] == "bf16" else 4
     k4_bytes = R * (B + 1) * V * b  # every target row of a full tree, read once
@@ -313,6 +341,7 @@ def main():
         "flagged_requests": flagged,
         "cpu_baseline": cpu,
         "first_naive": first,
+        "planner_expand_prune": ep,
     }
     print(json.dumps(out), flush=True)
 

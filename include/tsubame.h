@@ -7,6 +7,8 @@
  *   tsb_plan    first pass: row normalisers, planning candidates and a frozen
  *               topology by best-first expansion of draft path scores under a
  *               node budget B (Section 3.1; Appendix B.3; Figure 1).
+ *   tsb_plan_ep the same first pass by expand-then-prune with a frontier
+ *               width (Section 3.1; Appendix B.3).
  *   tsb_replay  second pass: refill every node of the frozen topology with
  *               fresh samples drawn without replacement from the draft
  *               distribution of its depth (Section 3.2, eq. (2); Appendix A).
@@ -146,6 +148,21 @@ size_t tsb_workspace_bytes(const tsb_config* cfg);
 tsb_status tsb_plan(const tsb_config* cfg, const void* draft, double* draft_lse, int32_t* topk_tok,
                     float* topk_lp, const tsb_tree* tree, int32_t* req_status, void* workspace,
                     size_t workspace_bytes, hipStream_t stream);
+
+/* First pass by expand-then-prune (Section 3.1; Appendix B.3: the EAGLE-2
+ * style planner the paper uses for drafters that correct per prefix, with a
+ * frontier of 10). Same inputs and outputs as tsb_plan. Layer 1 is the
+ * root's K candidates; the frontier of each layer is its `frontier` best
+ * nodes (score desc, rank path lexicographic asc); the next layer holds every
+ * child of every frontier node; the tree is the first B generated nodes
+ * under tsb_plan's order (score desc, depth asc, rank path asc), in BFS
+ * order. plan_margin = score of the last chosen node - score of the first
+ * generated node left out (+inf if none). With frontier >= B the tree equals
+ * tsb_plan's. TSB_E_SHAPE if frontier is outside [1, 64] or the generated
+ * nodes, K + sum over depths of min(layer, frontier) * K, exceed 6144. */
+tsb_status tsb_plan_ep(const tsb_config* cfg, int32_t frontier, const void* draft, double* draft_lse,
+                       int32_t* topk_tok, float* topk_lp, const tsb_tree* tree, int32_t* req_status,
+                       void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* Second pass (Section 3.2, eq. (2)). For every node u with m children at
  * depth d the children receive, in rank order, the m largest keys of

@@ -5,7 +5,7 @@ runs in the HIP kernels behind the C ABI of include/tsubame.h. PyTorch
 supplies device memory and the stream. There is no CPU fallback: if the
 library is not built, or a call fails, an exception is raised.
 
-Entry points mirror the C ABI: plan, replay, verify, step, workspace_bytes,
+Entry points mirror the C ABI: plan, plan_ep, replay, verify, step, workspace_bytes,
 and the First + Naive baseline: first_tokens, verify_naive, step_first.
 `Round` bundles the output buffers of one configuration.
 """
@@ -28,7 +28,7 @@ MAX_D, MAX_K, MAX_B, TRACE_MAX = 64, 32, 1023, 256
 KERNELS = ("draft_partials", "plan_tree", "replay_scan", "replay_merge", "target_partials",
            "verify_walk", "verify_naive")
 
-EXPORTS = ("tsb_workspace_bytes", "tsb_plan", "tsb_replay", "tsb_verify", "tsb_step",
+EXPORTS = ("tsb_workspace_bytes", "tsb_plan", "tsb_plan_ep", "tsb_replay", "tsb_verify", "tsb_step",
            "tsb_first_tokens", "tsb_verify_naive", "tsb_step_first",
            "tsb_status_string", "tsb_last_error", "tsb_version", "tsb_profile_kernel")
 
@@ -76,6 +76,9 @@ def load(path=LIB_PATH):
     lib.tsb_plan.restype = ctypes.c_int
     lib.tsb_plan.argtypes = [ctypes.POINTER(TsbConfig), P, P, P, P, ctypes.POINTER(TsbTree), P, P,
                              ctypes.c_size_t, P]
+    lib.tsb_plan_ep.restype = ctypes.c_int
+    lib.tsb_plan_ep.argtypes = [ctypes.POINTER(TsbConfig), ctypes.c_int32, P, P, P, P, ctypes.POINTER(TsbTree), P, P,
+                                ctypes.c_size_t, P]
     lib.tsb_replay.restype = ctypes.c_int
     lib.tsb_replay.argtypes = [ctypes.POINTER(TsbConfig), P, P, ctypes.POINTER(TsbTree), ctypes.c_uint32, P, P,
                                ctypes.c_size_t, P]
@@ -193,6 +196,15 @@ class Round:
                              self.ws_bytes, _stream(stream))
         if st:
             raise TsbError(st, "tsb_plan")
+
+    def plan_ep(self, draft, frontier, stream=None):
+        """First pass by expand-then-prune with the given frontier width."""
+        self._logits(draft, self.cfg.D, "draft")
+        st = load().tsb_plan_ep(ctypes.byref(self.cfg), int(frontier), _ptr(draft), _ptr(self.draft_lse),
+                                _ptr(self.topk_tok), _ptr(self.topk_lp), ctypes.byref(self._tree_c),
+                                _ptr(self.req_status), self.ws_ptr, self.ws_bytes, _stream(stream))
+        if st:
+            raise TsbError(st, "tsb_plan_ep")
 
     def replay(self, draft, step, stream=None):
         self._logits(draft, self.cfg.D, "draft")

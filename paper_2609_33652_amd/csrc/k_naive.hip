@@ -63,13 +63,6 @@ struct NaiveArgs {
     uint32_t k0, k1, step;
 };
 
-// Order-preserving map of a binary64 value to uint64 (-0 folded onto +0).
-__device__ __forceinline__ uint64_t ordered_bits64(double x) {
-    uint64_t u = (uint64_t)__double_as_longlong(x);
-    if (u == 0x8000000000000000ull) u = 0ull;
-    return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
-}
-
 // Keys are compared as ordered_bits64(fl32(a) + G) with the low 8 bits
 // cleared (an exchanged word carries its tag there): relative resolution
 // 2^-44 of the binary64 sum; keys equal after clearing go to the smaller
@@ -96,13 +89,6 @@ __device__ __forceinline__ void load_batch(const void* target, size_t trow, int 
         const int valid = max(0, min(4, n - i));
         raw_load4<DT>(target, trow + v0 + (valid ? i : 0), valid, VEC, a[j]);
     }
-}
-
-// Inverse of ordered_bits64 (for a key with cleared low bits: a value at
-// most that of the full key).
-__device__ __forceinline__ double from_ordered_bits64(uint64_t k) {
-    const uint64_t u = (k >> 63) ? (k & 0x7FFFFFFFFFFFFFFFull) : ~k;
-    return __longlong_as_double((long long)u);
 }
 
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t k) {

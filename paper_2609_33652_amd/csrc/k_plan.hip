@@ -285,7 +285,8 @@ __device__ __forceinline__ double wave_min_f64(double v) {
 
 // Merge of one draft row (one wave): log-sum-exp from the segment partials
 // in a fixed order, candidates from the segment lists.
-__device__ void merge_row(PlanShared& sh, int row, int rrow, int S, int K, float invT, const float* __restrict__ pm,
+template <typename SH>
+__device__ void merge_row(SH& sh, int row, int rrow, int S, int K, float invT, const float* __restrict__ pm,
                           const double* __restrict__ ps, const uint64_t* __restrict__ pk,
                           const int* __restrict__ pf, double* __restrict__ draft_lse,
                           int32_t* __restrict__ topk_tok, float* __restrict__ topk_lp) {
@@ -595,9 +596,309 @@ __global__ __launch_bounds__(kPlanThreads) void plan_tree(int D, int S, int K, i
     }
 }
 
+// ------------------------------------------------------------------ K2b
+// Expand-then-prune first pass (Section 3.1; Appendix B.3), one workgroup of
+// kPlanWaves waves per request. Layer 1 is the root's children; the frontier
+// of a layer is its W best nodes (score desc, rank path lex asc); the next
+// layer holds every child of every frontier node; the tree is the first B of
+// all generated nodes (score desc, depth asc, rank path lex asc).
+//
+// Layers are stored one after another, each in rank-path lexicographic order
+// (a child of the frontier node that is f-th in lexicographic order, rank j,
+// sits at f * K_d + j), so the storage order is the order of (depth, path):
+// ties on score are resolved by storage index, and the chosen nodes in
+// storage order are the BFS order of the tree.
+constexpr int kEpMax = 6144;  // generated nodes held in LDS
+
+struct EpShared {
+    float lp[TSB_MAX_D * TSB_MAX_K];
+    int kfin[TSB_MAX_D];
+    int bad;
+    double score[kEpMax];
+    int16_t par[kEpMax];  // storage index of the parent, -1 for the root
+    int16_t pos[kEpMax];  // scratch positions, then BFS index
+    int16_t nch[kEpMax];
+    int16_t fc[kEpMax];
+    uint8_t rank[kEpMax];
+    uint8_t depth[kEpMax];
+    uint8_t flag[kEpMax];
+    int16_t front[kEpFrontierLimit];
+    int lstart[TSB_MAX_D + 1];
+    uint64_t lists[kPlanWaves][kWave];
+    uint32_t hist[256];
+    int wsum[kPlanWaves];
+    double wmax[kPlanWaves];
+    int cnt;
+    uint64_t tkey;
+    int root_nch, root_fc;
+};
+
+constexpr uint8_t kEpFront = 1, kEpTie = 2, kEpChosen = 4, kEpAbove = 8;
+
+// Positions of the elements of [lo, hi) whose flag has `bit`, in index order
+// (pos[i] for those elements); returns their number. Called by all threads.
+__device__ int ep_scan(EpShared& sh, uint8_t bit, int lo, int hi) {
+    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const int per = (hi - lo + kPlanThreads - 1) / kPlanThreads;
+    const int b = lo + tid * per, e = min(hi, b + per);
+    int c = 0;
+    for (int i = b; i < e; ++i) c += (sh.flag[i] & bit) ? 1 : 0;
+    int incl = c;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const int t = __shfl_up(incl, o, kWave);
+        if (lane >= o) incl += t;
+    }
+    if (lane == kWave - 1) sh.wsum[wave] = incl;
+    __syncthreads();
+    int base = 0, total = 0;
+    for (int w = 0; w < kPlanWaves; ++w) {
+        base += w < wave ? sh.wsum[w] : 0;
+        total += sh.wsum[w];
+    }
+    int run = base + incl - c;
+    for (int i = b; i < e; ++i)
+        if (sh.flag[i] & bit) sh.pos[i] = (int16_t)run++;
+    __syncthreads();
+    return total;
+}
+
+// Number of elements of [lo, hi) whose flag has `bit` (all threads).
+__device__ int ep_count(EpShared& sh, uint8_t bit, int lo, int hi) {
+    int c = 0;
+    for (int i = lo + (int)threadIdx.x; i < hi; i += kPlanThreads) c += (sh.flag[i] & bit) ? 1 : 0;
+    if (threadIdx.x == 0) sh.cnt = 0;
+    __syncthreads();
+    for (int o = 32; o > 0; o >>= 1) c += __shfl_xor(c, o, kWave);
+    if ((threadIdx.x % kWave) == 0 && c) atomicAdd(&sh.cnt, c);
+    __syncthreads();
+    const int t = sh.cnt;
+    __syncthreads();
+    return t;
+}
+
+__global__ __launch_bounds__(kPlanThreads) void plan_ep(int D, int S, int K, int B, int W, float invT,
+                                                        const float* __restrict__ pm, const double* __restrict__ ps,
+                                                        const uint64_t* __restrict__ pk, const int* __restrict__ pf,
+                                                        double* __restrict__ draft_lse, int32_t* __restrict__ topk_tok,
+                                                        float* __restrict__ topk_lp, tsb_tree tree,
+                                                        int32_t* __restrict__ req_status) {
+    __shared__ EpShared sh;
+    const int r = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int wave = tid / kWave, lane = tid % kWave;
+
+    if (tid == 0) sh.bad = 0;
+    __syncthreads();
+    for (int d = wave; d < D; d += kPlanWaves)
+        merge_row(sh, r * D + d, d, S, K, invT, pm, ps, pk, pf, draft_lse, topk_tok, topk_lp);
+    __syncthreads();
+    const bool nonfinite = sh.bad != 0;
+    const int Dp = nonfinite ? 0 : D;
+
+    // layer of depth 1: the root's candidates
+    const int k0 = Dp > 0 ? sh.kfin[0] : 0;
+    for (int i = tid; i < k0; i += kPlanThreads) {
+        sh.score[i] = (double)sh.lp[i];
+        sh.par[i] = -1;
+        sh.rank[i] = (uint8_t)i;
+        sh.depth[i] = 1;
+        sh.flag[i] = 0;
+    }
+    if (tid == 0) {
+        sh.lstart[0] = 0;
+        sh.lstart[1] = k0;
+    }
+    int ntot = k0, layers = k0 > 0 ? 1 : 0;
+    __syncthreads();
+
+    // expansion: frontier of each layer, then its children
+    for (int d = 1; d < Dp; ++d) {
+        const int lb = sh.lstart[d - 1], le = sh.lstart[d], nl = le - lb, kd = sh.kfin[d];
+        if (nl == 0 || kd == 0) break;
+        if (nl <= W) {
+            for (int i = lb + tid; i < le; i += kPlanThreads) sh.flag[i] = kEpFront;
+            __syncthreads();
+        } else {
+            // the W-th largest score of the layer (with multiplicity): per-wave
+            // lists of the W largest keys, merged by wave 0
+            WaveTopList tl;
+            tl.init(W);
+            for (int base = lb + wave * kWave; base < le; base += kPlanThreads) {
+                const int i = base + lane;
+                tl.offer(i < le ? ordered_bits64(sh.score[i]) : 0ull, i < le);
+            }
+            sh.lists[wave][lane] = tl.v;
+            __syncthreads();
+            if (wave == 0) {
+                for (int v = 1; v < kPlanWaves; ++v) {
+                    const uint64_t k = sh.lists[v][lane];
+                    tl.offer(k, lane < W && k != 0);
+                }
+                if (lane == 0) sh.tkey = lane_u64(tl.v, W - 1);
+            }
+            __syncthreads();
+            const uint64_t tk = sh.tkey;
+            for (int i = lb + tid; i < le; i += kPlanThreads) {
+                const uint64_t k = ordered_bits64(sh.score[i]);
+                sh.flag[i] = k > tk ? kEpFront : (k == tk ? kEpTie : 0);
+            }
+            __syncthreads();
+            const int above = ep_count(sh, kEpFront, lb, le);
+            ep_scan(sh, kEpTie, lb, le);  // ties in lexicographic order
+            const int need = W - above;
+            for (int i = lb + tid; i < le; i += kPlanThreads)
+                if ((sh.flag[i] & kEpTie) && sh.pos[i] < need) sh.flag[i] |= kEpFront;
+            __syncthreads();
+        }
+        // the frontier in lexicographic order
+        const int f = ep_scan(sh, kEpFront, lb, le);
+        for (int i = lb + tid; i < le; i += kPlanThreads)
+            if (sh.flag[i] & kEpFront) sh.front[sh.pos[i]] = (int16_t)i;
+        __syncthreads();
+        if (le + f * kd > kEpMax) break;  // the host bounds the generated nodes; never taken
+        for (int t = tid; t < f * kd; t += kPlanThreads) {
+            const int p = sh.front[t / kd], j = t % kd;
+            const int c = le + t;
+            sh.score[c] = sh.score[p] + (double)sh.lp[d * K + j];
+            sh.par[c] = (int16_t)p;
+            sh.rank[c] = (uint8_t)j;
+            sh.depth[c] = (uint8_t)(d + 1);
+            sh.flag[c] = 0;
+        }
+        if (tid == 0) sh.lstart[d + 1] = le + f * kd;
+        ntot = le + f * kd;
+        layers = d + 1;
+        __syncthreads();
+    }
+    for (int i = tid; i < ntot; i += kPlanThreads) sh.flag[i] &= (uint8_t)~(kEpFront | kEpTie);
+    __syncthreads();
+
+    // prune: the first B generated nodes
+    double margin = (double)INFINITY;
+    if (ntot <= B || B == 0) {
+        if (B > 0)
+            for (int i = tid; i < ntot; i += kPlanThreads) sh.flag[i] = kEpChosen;
+        __syncthreads();
+    } else {
+        // t* = the B-th largest score, by radix selection on the ordered keys
+        uint64_t prefix = 0ull;
+        int remaining = B;
+        for (int shift = 56; shift >= 0; shift -= 8) {
+            for (int b = tid; b < 256; b += kPlanThreads) sh.hist[b] = 0u;
+            __syncthreads();
+            for (int i = tid; i < ntot; i += kPlanThreads) {
+                const uint64_t k = ordered_bits64(sh.score[i]);
+                if (shift == 56 || (k >> (shift + 8)) == prefix) atomicAdd(&sh.hist[(k >> shift) & 255u], 1u);
+            }
+            __syncthreads();
+            if (tid == 0) {
+                int acc = 0, b = 255;
+                for (; b > 0; --b) {
+                    if (acc + (int)sh.hist[b] >= remaining) break;
+                    acc += (int)sh.hist[b];
+                }
+                sh.cnt = remaining - acc;
+                sh.tkey = (prefix << 8) | (uint64_t)b;
+            }
+            __syncthreads();
+            remaining = sh.cnt;
+            prefix = sh.tkey;
+            __syncthreads();
+        }
+        const uint64_t tk = prefix;
+        double below = -INFINITY;
+        for (int i = tid; i < ntot; i += kPlanThreads) {
+            const uint64_t k = ordered_bits64(sh.score[i]);
+            sh.flag[i] = k > tk ? (uint8_t)(kEpChosen | kEpAbove) : (k == tk ? kEpTie : 0);
+            if (k < tk) below = fmax(below, sh.score[i]);
+        }
+        below = wave_max_f64(below);
+        if (lane == 0) sh.wmax[wave] = below;
+        __syncthreads();
+        const int above = ep_count(sh, kEpAbove, 0, ntot);
+        const int ties = ep_scan(sh, kEpTie, 0, ntot);
+        const int need = B - above;
+        for (int i = tid; i < ntot; i += kPlanThreads)
+            if ((sh.flag[i] & kEpTie) && sh.pos[i] < need) sh.flag[i] |= kEpChosen;
+        double bmax = -INFINITY;
+        for (int w = 0; w < kPlanWaves; ++w) bmax = fmax(bmax, sh.wmax[w]);
+        // the last chosen node scores t*; the next one ties or is the best below
+        margin = ties > need ? 0.0 : from_ordered_bits64(tk) - bmax;
+        __syncthreads();
+    }
+
+    // BFS positions: the chosen nodes in storage order
+    const int n = ep_scan(sh, kEpChosen, 0, ntot) + 1;
+    if (tid == 0) {
+        sh.root_nch = 0;
+        sh.root_fc = -1;
+    }
+    __syncthreads();
+    // children of a node are a rank prefix stored together: the rank-0 child
+    // gives the first child, the last chosen one the count
+    for (int i = tid; i < ntot; i += kPlanThreads) {
+        sh.nch[i] = 0;
+        sh.fc[i] = -1;
+    }
+    __syncthreads();
+    for (int i = tid; i < ntot; i += kPlanThreads) {
+        if (!(sh.flag[i] & kEpChosen)) continue;
+        const int p = sh.par[i];
+        const int j = sh.rank[i];
+        const int kd = sh.kfin[sh.depth[i] - 1];
+        const bool last = j + 1 >= kd || !(sh.flag[i + 1] & kEpChosen);
+        if (p >= 0) {
+            if (j == 0) sh.fc[p] = (int16_t)(sh.pos[i] + 1);
+            if (last) sh.nch[p] = (int16_t)(j + 1);
+        } else {
+            if (j == 0) sh.root_fc = sh.pos[i] + 1;
+            if (last) sh.root_nch = j + 1;
+        }
+    }
+    __syncthreads();
+
+    const size_t o = (size_t)r * (B + 1);
+    for (int i = tid; i < ntot; i += kPlanThreads) {
+        if (!(sh.flag[i] & kEpChosen)) continue;
+        const size_t x = o + sh.pos[i] + 1;
+        const int p = sh.par[i];
+        tree.parent[x] = p >= 0 ? sh.pos[p] + 1 : 0;
+        tree.depth[x] = sh.depth[i];
+        tree.rank[x] = sh.rank[i];
+        tree.score[x] = sh.score[i];
+        tree.n_children[x] = sh.nch[i];
+        tree.first_child[x] = sh.fc[i];
+    }
+    for (int i = n + tid; i < B + 1; i += kPlanThreads) {
+        tree.parent[o + i] = -1;
+        tree.depth[o + i] = -1;
+        tree.rank[o + i] = -1;
+        tree.score[o + i] = 0.0;
+        tree.n_children[o + i] = 0;
+        tree.first_child[o + i] = -1;
+    }
+    if (tid == 0) {
+        tree.parent[o] = -1;
+        tree.depth[o] = 0;
+        tree.rank[o] = -1;
+        tree.score[o] = 0.0;
+        tree.n_children[o] = sh.root_nch;
+        tree.first_child[o] = sh.root_fc;
+        tree.n_nodes[r] = n;
+        tree.plan_margin[r] = n > 1 ? margin : (double)INFINITY;
+        int st = req_status[r];
+        if (nonfinite) st |= TSB_REQ_NONFINITE;
+        else if (n < B + 1) st |= TSB_REQ_BUDGET_SHORT;
+        req_status[r] = st;
+    }
+    (void)layers;
+}
+
 // ------------------------------------------------------------------ launch
 hipError_t launch_plan(const tsb_config& c, float invT, const void* draft, double* draft_lse, int32_t* topk_tok,
-                       float* topk_lp, const tsb_tree& tree, int32_t* req_status, char* ws, hipStream_t st) {
+                       float* topk_lp, const tsb_tree& tree, int32_t* req_status, char* ws, hipStream_t st,
+                       int frontier) {
     const Geometry g = geometry(c);
     const PlanWs w = plan_ws(c);
     float* pm = (float*)(ws + w.pm);
@@ -628,11 +929,25 @@ hipError_t launch_plan(const tsb_config& c, float invT, const void* draft, doubl
     if (e != hipSuccess) return e;
     if ((e = hook_after(TSB_KERNEL_DRAFT_PARTIALS, st)) != hipSuccess) return e;
     if ((e = hook_before(TSB_KERNEL_PLAN_TREE, st)) != hipSuccess) return e;
-    plan_tree<<<c.R, kPlanThreads, 0, st>>>(c.D, g.S1, c.K, c.B, invT, pm, ps, pk, pf, draft_lse, topk_tok, topk_lp,
-                                            tree, req_status);
+    if (frontier > 0)
+        plan_ep<<<c.R, kPlanThreads, 0, st>>>(c.D, g.S1, c.K, c.B, frontier, invT, pm, ps, pk, pf, draft_lse,
+                                              topk_tok, topk_lp, tree, req_status);
+    else
+        plan_tree<<<c.R, kPlanThreads, 0, st>>>(c.D, g.S1, c.K, c.B, invT, pm, ps, pk, pf, draft_lse, topk_tok,
+                                                topk_lp, tree, req_status);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     return hook_after(TSB_KERNEL_PLAN_TREE, st);
+}
+
+int ep_generated_bound(const tsb_config& c, int frontier) {
+    long long n = c.K, layer = c.K;
+    for (int d = 1; d < c.D; ++d) {
+        layer = (layer < frontier ? layer : frontier) * (long long)c.K;
+        n += layer;
+        if (n > (1ll << 30)) break;
+    }
+    return n > kEpMax ? -1 : (int)n;
 }
 
 }  // namespace tsb

@@ -141,6 +141,20 @@ __device__ __forceinline__ float from_ordered_bits(uint32_t k) {
     return __uint_as_float(u);
 }
 
+// Order-preserving map of a binary64 value to uint64 (-0 folded onto +0).
+__device__ __forceinline__ uint64_t ordered_bits64(double x) {
+    uint64_t u = (uint64_t)__double_as_longlong(x);
+    if (u == 0x8000000000000000ull) u = 0ull;
+    return (u >> 63) ? ~u : (u | 0x8000000000000000ull);
+}
+
+// Inverse of ordered_bits64 (for a key with cleared low bits: a value at
+// most that of the full key).
+__device__ __forceinline__ double from_ordered_bits64(uint64_t k) {
+    const uint64_t u = (k >> 63) ? (k & 0x7FFFFFFFFFFFFFFFull) : ~k;
+    return __longlong_as_double((long long)u);
+}
+
 // Candidate key: logit desc, then token id asc.
 __device__ __forceinline__ uint64_t cand_key(float x, uint32_t id) {
     return ((uint64_t)ordered_bits(x) << 32) | (uint32_t)(~id);

@@ -24,8 +24,16 @@ inline hipError_t hook_after(int kernel, hipStream_t st) {
     return h.kernel == kernel ? hipEventRecord(h.stop, st) : hipSuccess;
 }
 
+// frontier > 0: the expand-then-prune first pass with that frontier width;
+// 0: the max-heap first pass.
 hipError_t launch_plan(const tsb_config& c, float invT, const void* draft, double* draft_lse, int32_t* topk_tok,
-                       float* topk_lp, const tsb_tree& tree, int32_t* req_status, char* ws, hipStream_t st);
+                       float* topk_lp, const tsb_tree& tree, int32_t* req_status, char* ws, hipStream_t st,
+                       int frontier = 0);
+
+// Nodes the expand-then-prune pass generates for this shape and frontier
+// width, or -1 if they exceed what a workgroup holds.
+int ep_generated_bound(const tsb_config& c, int frontier);
+constexpr int kEpFrontierLimit = 64;
 
 hipError_t launch_replay(const tsb_config& c, float invT, const void* draft, const int32_t* topk_tok,
                          const tsb_tree& tree, uint32_t step, int32_t* node_tok, char* ws, hipStream_t st);

@@ -113,6 +113,25 @@ tsb_status tsb_plan(const tsb_config* cfg, const void* draft, double* draft_lse,
     return e == hipSuccess ? TSB_OK : hip_fail(e, "tsb_plan");
 }
 
+tsb_status tsb_plan_ep(const tsb_config* cfg, int32_t frontier, const void* draft, double* draft_lse,
+                       int32_t* topk_tok, float* topk_lp, const tsb_tree* tree, int32_t* req_status,
+                       void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    g_last_error[0] = 0;
+    TRY(check_config(cfg));
+    if (frontier < 1 || frontier > tsb::kEpFrontierLimit)
+        return fail(TSB_E_SHAPE, "frontier=%d must be in [1, %d]", frontier, tsb::kEpFrontierLimit);
+    if (tsb::ep_generated_bound(*cfg, frontier) < 0)
+        return fail(TSB_E_SHAPE, "expand-then-prune with K=%d, D=%d, frontier=%d generates more nodes than a "
+                    "workgroup holds", cfg->K, cfg->D, frontier);
+    if (!draft || !draft_lse || !topk_tok || !topk_lp || !req_status)
+        return fail(TSB_E_NULL, "tsb_plan_ep: a required array is NULL");
+    TRY(check_tree(tree));
+    TRY(check_ws(cfg, workspace, workspace_bytes));
+    const hipError_t e = tsb::launch_plan(*cfg, inv_temperature(cfg->temperature), draft, draft_lse, topk_tok,
+                                          topk_lp, *tree, req_status, (char*)workspace, stream, frontier);
+    return e == hipSuccess ? TSB_OK : hip_fail(e, "tsb_plan_ep");
+}
+
 tsb_status tsb_replay(const tsb_config* cfg, const void* draft, const int32_t* topk_tok, const tsb_tree* tree,
                       uint32_t step, int32_t* node_tok, void* workspace, size_t workspace_bytes, hipStream_t stream) {
     g_last_error[0] = 0;
@@ -237,6 +256,6 @@ const char* tsb_status_string(tsb_status s) {
 
 const char* tsb_last_error(void) { return g_last_error; }
 
-int32_t tsb_version(void) { return 102; }
+int32_t tsb_version(void) { return 103; }
 
 }  // extern "C"

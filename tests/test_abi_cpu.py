@@ -33,7 +33,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(tsb.EXPORTS)
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.tsb_version() == 102
+    assert lib.tsb_version() == 103
 
 
 def _cfg(**kw):
@@ -135,3 +135,21 @@ def test_first_naive_entry_points_validate(lib):
                               ctypes.byref(v), FAKE, need, None) == 1
     assert lib.tsb_step_first(ctypes.byref(_cfg(dtype=9)), FAKE, FAKE, 0, FAKE, FAKE, FAKE, ctypes.byref(t),
                               FAKE, ctypes.byref(v), FAKE, need, None) == 3
+
+
+def test_plan_ep_validates_frontier_and_size(lib):
+    cfg = _cfg()
+    need = lib.tsb_workspace_bytes(ctypes.byref(cfg))
+    t = _tree()
+    for w in (0, -1, 65):
+        assert lib.tsb_plan_ep(ctypes.byref(cfg), w, FAKE, FAKE, FAKE, FAKE, ctypes.byref(t), FAKE, FAKE, need,
+                               None) == 2
+    big = _cfg(K=32, D=64, B=100)
+    nb = lib.tsb_workspace_bytes(ctypes.byref(big))
+    assert lib.tsb_plan_ep(ctypes.byref(big), 64, FAKE, FAKE, FAKE, FAKE, ctypes.byref(t), FAKE, FAKE, nb,
+                           None) == 2
+    assert "generates more nodes" in lib.tsb_last_error().decode()
+    assert lib.tsb_plan_ep(ctypes.byref(cfg), 4, None, FAKE, FAKE, FAKE, ctypes.byref(t), FAKE, FAKE, need,
+                           None) == 1
+    assert lib.tsb_plan_ep(ctypes.byref(cfg), 4, FAKE, FAKE, FAKE, FAKE, ctypes.byref(t), FAKE, FAKE, need - 1,
+                           None) == 5
