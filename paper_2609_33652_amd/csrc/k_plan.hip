@@ -712,65 +712,71 @@ __global__ __launch_bounds__(kPlanThreads) void plan_ep(int D, int S, int K, int
     int ntot = k0, layers = k0 > 0 ? 1 : 0;
     __syncthreads();
 
-    // expansion: frontier of each layer, then its children
-    for (int d = 1; d < Dp; ++d) {
-        const int lb = sh.lstart[d - 1], le = sh.lstart[d], nl = le - lb, kd = sh.kfin[d];
-        if (nl == 0 || kd == 0) break;
-        if (nl <= W) {
-            for (int i = lb + tid; i < le; i += kPlanThreads) sh.flag[i] = kEpFront;
-            __syncthreads();
-        } else {
-            // the W-th largest score of the layer (with multiplicity): per-wave
-            // lists of the W largest keys, merged by wave 0
-            WaveTopList tl;
-            tl.init(W);
-            for (int base = lb + wave * kWave; base < le; base += kPlanThreads) {
-                const int i = base + lane;
-                tl.offer(i < le ? ordered_bits64(sh.score[i]) : 0ull, i < le);
-            }
-            sh.lists[wave][lane] = tl.v;
-            __syncthreads();
-            if (wave == 0) {
-                for (int v = 1; v < kPlanWaves; ++v) {
-                    const uint64_t k = sh.lists[v][lane];
-                    tl.offer(k, lane < W && k != 0);
+    // expansion (wave 0 alone: a layer holds at most frontier * K nodes):
+    // frontier of each layer, then its children
+    if (wave == 0) {
+        for (int d = 1; d < Dp; ++d) {
+            const int lb = sh.lstart[d - 1], le = sh.lstart[d], nl = le - lb, kd = sh.kfin[d];
+            if (nl == 0 || kd == 0) break;
+            int f = 0;  // frontier nodes, listed in lexicographic (storage) order
+            if (nl <= W) {
+                for (int base = lb; base < le; base += kWave) {
+                    const int i = base + lane;
+                    if (i < le) sh.front[i - lb] = (int16_t)i;
                 }
-                if (lane == 0) sh.tkey = lane_u64(tl.v, W - 1);
+                f = nl;
+            } else {
+                // the W-th largest score of the layer (with multiplicity)
+                WaveTopList tl;
+                tl.init(W);
+                for (int base = lb; base < le; base += kWave) {
+                    const int i = base + lane;
+                    tl.offer(i < le ? ordered_bits64(sh.score[i]) : 0ull, i < le);
+                }
+                const uint64_t tk = lane_u64(tl.v, W - 1);
+                int above = 0;
+                for (int base = lb; base < le; base += kWave) {
+                    const int i = base + lane;
+                    above += __popcll(__ballot(i < le && ordered_bits64(sh.score[i]) > tk));
+                }
+                // nodes above the W-th score, then ties in lexicographic order
+                int ties = 0;
+                for (int base = lb; base < le; base += kWave) {
+                    const int i = base + lane;
+                    const uint64_t k = i < le ? ordered_bits64(sh.score[i]) : 0ull;
+                    const bool tie = i < le && k == tk;
+                    const uint64_t tb = __ballot(tie);
+                    const int trank = ties + __popcll(tb & ((1ull << lane) - 1ull));
+                    const bool in = (i < le && k > tk) || (tie && trank < W - above);
+                    const uint64_t ib = __ballot(in);
+                    if (in) sh.front[f + __popcll(ib & ((1ull << lane) - 1ull))] = (int16_t)i;
+                    f += __popcll(ib);
+                    ties += __popcll(tb);
+                }
             }
-            __syncthreads();
-            const uint64_t tk = sh.tkey;
-            for (int i = lb + tid; i < le; i += kPlanThreads) {
-                const uint64_t k = ordered_bits64(sh.score[i]);
-                sh.flag[i] = k > tk ? kEpFront : (k == tk ? kEpTie : 0);
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            if (le + f * kd > kEpMax) break;  // the host bounds the generated nodes; never taken
+            for (int t = lane; t < f * kd; t += kWave) {
+                const int p = sh.front[t / kd], j = t % kd;
+                const int c = le + t;
+                sh.score[c] = sh.score[p] + (double)sh.lp[d * K + j];
+                sh.par[c] = (int16_t)p;
+                sh.rank[c] = (uint8_t)j;
+                sh.depth[c] = (uint8_t)(d + 1);
+                sh.flag[c] = 0;
             }
-            __syncthreads();
-            const int above = ep_count(sh, kEpFront, lb, le);
-            ep_scan(sh, kEpTie, lb, le);  // ties in lexicographic order
-            const int need = W - above;
-            for (int i = lb + tid; i < le; i += kPlanThreads)
-                if ((sh.flag[i] & kEpTie) && sh.pos[i] < need) sh.flag[i] |= kEpFront;
-            __syncthreads();
+            if (lane == 0) sh.lstart[d + 1] = le + f * kd;
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            ntot = le + f * kd;
+            layers = d + 1;
         }
-        // the frontier in lexicographic order
-        const int f = ep_scan(sh, kEpFront, lb, le);
-        for (int i = lb + tid; i < le; i += kPlanThreads)
-            if (sh.flag[i] & kEpFront) sh.front[sh.pos[i]] = (int16_t)i;
-        __syncthreads();
-        if (le + f * kd > kEpMax) break;  // the host bounds the generated nodes; never taken
-        for (int t = tid; t < f * kd; t += kPlanThreads) {
-            const int p = sh.front[t / kd], j = t % kd;
-            const int c = le + t;
-            sh.score[c] = sh.score[p] + (double)sh.lp[d * K + j];
-            sh.par[c] = (int16_t)p;
-            sh.rank[c] = (uint8_t)j;
-            sh.depth[c] = (uint8_t)(d + 1);
-            sh.flag[c] = 0;
-        }
-        if (tid == 0) sh.lstart[d + 1] = le + f * kd;
-        ntot = le + f * kd;
-        layers = d + 1;
-        __syncthreads();
+        if (lane == 0) sh.cnt = ntot;
     }
+    __syncthreads();
+    ntot = sh.cnt;
+    __syncthreads();
     for (int i = tid; i < ntot; i += kPlanThreads) sh.flag[i] &= (uint8_t)~(kEpFront | kEpTie);
     __syncthreads();
 
@@ -792,14 +798,31 @@ __global__ __launch_bounds__(kPlanThreads) void plan_ep(int D, int S, int K, int
                 if (shift == 56 || (k >> (shift + 8)) == prefix) atomicAdd(&sh.hist[(k >> shift) & 255u], 1u);
             }
             __syncthreads();
-            if (tid == 0) {
-                int acc = 0, b = 255;
-                for (; b > 0; --b) {
-                    if (acc + (int)sh.hist[b] >= remaining) break;
-                    acc += (int)sh.hist[b];
+            if (wave == 0) {
+                // lane l holds bins 255 - 4l .. 252 - 4l: counts from the top
+                int c4[4], ls = 0;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    c4[q] = (int)sh.hist[255 - 4 * lane - q];
+                    ls += c4[q];
                 }
-                sh.cnt = remaining - acc;
-                sh.tkey = (prefix << 8) | (uint64_t)b;
+                int incl = ls;
+#pragma unroll
+                for (int o = 1; o < kWave; o <<= 1) {
+                    const int t = __shfl_up(incl, o, kWave);
+                    if (lane >= o) incl += t;
+                }
+                const uint64_t hit = __ballot(incl >= remaining);
+                const int l0 = hit ? __ffsll((unsigned long long)hit) - 1 : kWave - 1;
+                if (lane == l0) {
+                    int acc = incl - ls, q = 0;
+                    for (; q < 3; ++q) {
+                        if (acc + c4[q] >= remaining) break;
+                        acc += c4[q];
+                    }
+                    sh.cnt = remaining - acc;
+                    sh.tkey = (prefix << 8) | (uint64_t)(255 - 4 * lane - q);
+                }
             }
             __syncthreads();
             remaining = sh.cnt;
