@@ -3,8 +3,9 @@
 TEST INFRASTRUCTURE ONLY: used by the tests to check the losslessness claim
 (Section 3.3, Proposition 1) with no random numbers at all.
 
-For a fixed topology, a context-free draft table q[d] and a prefix-keyed
-target p(. | s), every random choice of the round is enumerated:
+For a fixed topology, a draft table q[d] (or a draft distribution keyed by
+the replayed prefix) and a prefix-keyed target p(. | s), every random choice
+of the round is enumerated:
   * replay draws at each parent u: ordered samples without replacement from
     q[depth(u)] with Plackett-Luce weight prod_j q(y_j) / (1 - sum_{i<j} q(y_i))
     (Appendix A, sampling without replacement);
@@ -48,7 +49,10 @@ def emitted_law(tree, q, p_of_prefix):
     """Exact distribution of the emitted sequence (accepted tokens + bonus).
 
     tree: BFS topology dict (n_children, first_child, depth).
-    q: array [D, V] of draft distributions per depth.
+    q: array [D, V] of draft distributions per depth, or a callable
+       q(prefix) -> draft distribution of the children of the node reached
+       by that token prefix (a drafter conditioned on the replayed prefix,
+       eq. (2)).
     p_of_prefix(tuple) -> target distribution after that token prefix.
     Returns dict {tuple(sequence): probability}.
     """
@@ -65,7 +69,7 @@ def emitted_law(tree, q, p_of_prefix):
                 if p_u[v] > 0:
                     add(prefix + (v,), weight * p_u[v])
             return
-        qd = np.asarray(q[int(tree["depth"][u])], dtype=np.float64)
+        qd = np.asarray(q(prefix) if callable(q) else q[int(tree["depth"][u])], dtype=np.float64)
         fc = int(tree["first_child"][u])
         for seq, w_draw in _wor_orders(qd, m):
             P, Q = p_u.copy(), qd.copy()

@@ -69,11 +69,14 @@ def bonus_sample(P, seed, step, request, node):
     return int(order[0]), margin
 
 
-def verify(p_rows, q_rows, tree, node_tok, seed, step, request):
+def verify(p_rows, q_rows, tree, node_tok, seed, step, request, q_node=None):
     """Walk the replayed tree.
 
     p_rows(u) -> float64 target distribution at node u (length V)
     q_rows(d) -> float64 draft distribution of position d
+    q_node(u) -> float64 draft distribution q_u of the children of node u;
+                 when given it replaces q_rows (drafters whose q_u depends on
+                 the replayed prefix, eq. (2))
     Returns dict: n_acc, acc_node, acc_tok, bonus, status, tests (list of
     (child, U, ratio, accepted)), residual_Z (list), margins (list of
     (kind, id, margin)).
@@ -87,7 +90,12 @@ def verify(p_rows, q_rows, tree, node_tok, seed, step, request):
     while True:
         m = int(n_children[u])
         P = p_rows(u)
-        Q = q_rows(int(depth[u])) if m > 0 else None
+        if m == 0:
+            Q = None
+        elif q_node is not None:
+            Q = q_node(u)
+        else:
+            Q = q_rows(int(depth[u]))
         accepted = False
         degenerate = False
         for j in range(m):

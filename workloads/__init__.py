@@ -22,6 +22,10 @@ Five workloads (sizes, distributions and temperatures):
                   noise sd sigma_r ~ U[0.3, 1.5] per request
   5 large_budget  R=64, V=151936, D=32, B=256, K=16, bf16, T=1.0, as 4
 
+Pool workloads add transition scores between the candidates of consecutive
+positions (transitions(): i.i.d. 1.5 * N(0, 1), binary32), as a drafter that
+looks its corrections up in a table would hold.
+
 Per request the generator draws D+1 base rows (binary32). Draft row d is base
 row d. The target row of tree node n is base row depth(n) (the distribution of
 the token that follows node n) plus Gaussian noise, so the target needs the
@@ -123,6 +127,20 @@ def target_from_base(cfg, base, sigma, depth, set_idx=0, seed=None, out=None):
     return out
 
 
+def transitions(cfg, P, scale=1.5, set_idx=0, device="cpu", seed=None):
+    """Transition scores [R, D-1, P, P] (binary32): scale * N(0, 1) per entry.
+
+    They stand in for a drafter's precomputed scores between the pool
+    candidates of consecutive positions (the correction of pool slot j of
+    position d after slot i of position d-1).
+    """
+    R, D = cfg["R"], cfg["D"]
+    seed = GEN_SEED_BASE + cfg.get("id", 0) if seed is None else seed
+    g = _gen(device, seed * 1000003 + 104729 + set_idx)
+    t = torch.randn(R, max(D - 1, 0), P, P, generator=g, device=device, dtype=torch.float32)
+    return t.mul_(scale).contiguous()
+
+
 def bytes_per_step(cfg):
     """Algorithmic bytes of one round: every draft row and every target row read once."""
     b = 4 if cfg["dtype"] == "f32" else 2
@@ -134,5 +152,5 @@ def describe(cfg):
                                                 cfg["T"], cfg["dtype"])
 
 
-__all__ = ["CONFIGS", "config", "base_rows", "draft_from_base", "target_from_base",
+__all__ = ["CONFIGS", "config", "base_rows", "draft_from_base", "target_from_base", "transitions",
            "replay_seed", "bytes_per_step", "describe"]
