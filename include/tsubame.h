@@ -20,7 +20,11 @@
  *   tsb_step    plan -> replay -> verify with target logits supplied up front.
  *
  * and the deterministic baseline of Section 3.1 with target-sample matching
- * (Table 2, Naive): tsb_first_tokens, tsb_verify_naive, tsb_step_first.
+ * (Table 2, Naive): tsb_first_tokens, tsb_verify_naive, tsb_step_first;
+ * and the same round over sparse candidate pools with a drafter whose
+ * distribution depends on the replayed prefix (Section 3.1; Section 3.2,
+ * eq. (2); Section 3.3): tsb_pool_plan, tsb_pool_replay, tsb_pool_verify,
+ * tsb_pool_step.
  *
  * Conventions shared by every entry point
  *   - Every array pointer is a DEVICE pointer owned by the caller, row-major,
@@ -34,8 +38,9 @@
  *     reused by successive calls on one stream; calls that overlap in time
  *     need separate workspaces. Zero-fill a workspace once, before its first
  *     use, and again after any request reported TSB_REQ_WALK_TIMEOUT: its
- *     last part holds state that verification keeps between calls (a
- *     sequence number per request and tagged exchange slots).
+ *     first part holds state that verification keeps between calls (a
+ *     sequence number per request and tagged exchange slots), at the same
+ *     place for every entry point of one cfg.
  *   - Results are a deterministic function of (inputs, cfg.seed, step): the
  *     randomness is Philox4x32-10 (Salmon et al., SC'11) keyed by
  *     (seed, step, request, node, draw), independent of launch shapes.
@@ -84,7 +89,8 @@ enum {
     TSB_REQ_NONFINITE = 1,           /* NaN/+inf logit, or a row with no finite logit */
     TSB_REQ_DEGENERATE_RESIDUAL = 2, /* empty residual after a rejection: bonus drawn from p at that node */
     TSB_REQ_BUDGET_SHORT = 4,        /* fewer than B nodes exist: n_nodes < B + 1 */
-    TSB_REQ_WALK_TIMEOUT = 8         /* a cross-workgroup wait in verification hit its spin limit */
+    TSB_REQ_WALK_TIMEOUT = 8,        /* a cross-workgroup wait in verification hit its spin limit */
+    TSB_REQ_BAD_TOKEN = 16           /* tsb_pool_verify: a visited node token is not in its position's pool */
 };
 
 /* cfg.flags */
@@ -219,6 +225,74 @@ tsb_status tsb_step_first(const tsb_config* cfg, const void* draft, const void* 
                           int32_t* node_tok, const tsb_verdict* out, void* workspace,
                           size_t workspace_bytes, hipStream_t stream);
 
+/* ---------------------------------------------------------------- pools
+ * Sparse candidate pools with a drafter conditioned on the replayed prefix
+ * (Section 3.1: the draft vocabulary of each position is restricted to a
+ * pool of the backbone's P top-scoring tokens, the drafter's correction is
+ * computed inside the pool and the corrected logits are normalised over the
+ * pool; drafters that look their conditionals up in a table of transition
+ * scores are planned by max-heap expansion. Section 3.2, eq. (2): replay
+ * recomputes q_u under the replayed prefix with the same pools. Section 3.3:
+ * verification uses these pool-normalised probabilities; the target stays
+ * vocabulary-wide). The paper's pools hold 16 or 64 tokens.
+ *
+ *   pool_tok [R, D, P]   pool d: the P best tokens of draft row d by (logit
+ *                        desc, id asc), in that order (pool slot j).
+ *   trans [R, D-1, P, P] binary32 transition scores: trans[r, d-1, i, j]
+ *                        corrects slot j of pool d after a token in slot i of
+ *                        pool d - 1 (NULL allowed when D = 1). Every entry
+ *                        must be finite, else the request is NONFINITE.
+ *   For a node u at depth d >= 1 whose token holds slot s of pool d - 1:
+ *     z_u(j) = fl32(a_{d,j} + fl32(trans[r, d-1, s, j] * invT)),
+ *     a_{d,j} = fl32(draft[r, d, pool_tok[r, d, j]] * invT); z_root = a_0.
+ *     q_u(j) = exp(z_u(j) - L_u), L_u the binary64 log-sum-exp of z_u;
+ *     lp_u(j) = fl32(z_u(j) - fl32(L_u)); u's candidates are the slots by
+ *     (lp desc, slot asc) with lp > -inf, at most K; child rank k of u is
+ *     its k-th candidate.
+ *   P must satisfy K <= P <= min(64, V). Workspaces of these entry points are
+ *   tsb_pool_workspace_bytes(cfg, P) bytes (the zero-fill rule above holds).
+ */
+size_t tsb_pool_workspace_bytes(const tsb_config* cfg, int32_t P);
+
+/* First pass over the pools. Writes pool_tok, the tree (the first B rank
+ * paths under the order of tsb_plan: score desc, depth asc, rank path asc,
+ * with score the binary64 sum of lp_u along the path; plan_margin as in
+ * tsb_plan) and, if plan_tok is not NULL, the planning token of every node
+ * ([R, B+1], -1 at the root and beyond n_nodes: the First tree of Section
+ * 3.1 over the pools). Clears and sets req_status (NONFINITE: a non-finite
+ * draft row or transition score; BUDGET_SHORT). */
+tsb_status tsb_pool_plan(const tsb_config* cfg, int32_t P, const void* draft, const float* trans,
+                         int32_t* pool_tok, const tsb_tree* tree, int32_t* plan_tok, int32_t* req_status,
+                         void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* Second pass over the pools, layer by layer: the m children of u receive,
+ * in rank order, the pool tokens with the m largest keys
+ * z_u(j) + G(seed, step, request, u, pool_tok[r, d, j]) in binary64 (G from
+ * the REPLAY stream, draw = token id; equal keys to the smaller id), with
+ * z_u built from the slot of u's replayed token. Writes node_tok [R, B+1]
+ * (-1 at the root and beyond n_nodes). Needs no workspace. */
+tsb_status tsb_pool_replay(const tsb_config* cfg, int32_t P, const void* draft, const float* trans,
+                           const int32_t* pool_tok, const tsb_tree* tree, uint32_t step, int32_t* node_tok,
+                           hipStream_t stream);
+
+/* Verification as tsb_verify with q_u of the pools (zero outside pool d):
+ * acceptance U < max(p(y) - C q_u(y), 0) / (W q_u(y)), residual
+ * max(p - C q_u, 0), bonus by Gumbel-max of the residual or of p. Node
+ * tokens are looked up in their position's pool; one that is not there is
+ * tested with q = 0 (accepted iff p(y) > 0), its children are built from slot
+ * 0, and the request gets TSB_REQ_BAD_TOKEN. out->target_lse and out->trace
+ * as in tsb_verify. */
+tsb_status tsb_pool_verify(const tsb_config* cfg, int32_t P, const void* draft, const float* trans,
+                           const int32_t* pool_tok, const void* target, const tsb_tree* tree,
+                           const int32_t* node_tok, uint32_t step, const tsb_verdict* out, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream);
+
+/* pool plan -> pool replay -> pool verify back to back on one stream. */
+tsb_status tsb_pool_step(const tsb_config* cfg, int32_t P, const void* draft, const float* trans,
+                         const void* target, uint32_t step, int32_t* pool_tok, const tsb_tree* tree,
+                         int32_t* node_tok, const tsb_verdict* out, void* workspace, size_t workspace_bytes,
+                         hipStream_t stream);
+
 /* Instrumentation (for benchmarks). On the calling thread, every later
  * launch of kernel `kernel_id` (a TSB_KERNEL_* value) is bracketed by
  * hipEventRecord(start) / hipEventRecord(stop) on the launch stream, so
@@ -232,7 +306,12 @@ enum {
     TSB_KERNEL_TARGET_PARTIALS = 4, /* target row statistics (streams the target) */
     TSB_KERNEL_VERIFY_WALK = 5,
     TSB_KERNEL_VERIFY_NAIVE = 6,    /* target-sample matching walk */
-    TSB_KERNEL_COUNT = 7
+    TSB_KERNEL_POOL_PARTIALS = 7,   /* pool selection (streams the draft) */
+    TSB_KERNEL_POOL_LISTS = 8,      /* pools and candidate lists of every context */
+    TSB_KERNEL_POOL_PLAN = 9,       /* best-first topology over per-node candidate lists */
+    TSB_KERNEL_POOL_REPLAY = 10,
+    TSB_KERNEL_POOL_WALK = 11,      /* verification with pool-restricted q_u */
+    TSB_KERNEL_COUNT = 12
 };
 tsb_status tsb_profile_kernel(int32_t kernel_id, hipEvent_t start, hipEvent_t stop);
 

@@ -6,7 +6,9 @@ supplies device memory and the stream. There is no CPU fallback: if the
 library is not built, or a call fails, an exception is raised.
 
 Entry points mirror the C ABI: plan, plan_ep, replay, verify, step, workspace_bytes,
-and the First + Naive baseline: first_tokens, verify_naive, step_first.
+the First + Naive baseline: first_tokens, verify_naive, step_first, and the
+round over sparse candidate pools with context-dependent draft distributions:
+pool_plan, pool_replay, pool_verify, pool_step, pool_workspace_bytes.
 `Round` bundles the output buffers of one configuration.
 """
 import ctypes
@@ -23,13 +25,16 @@ REQ_NONFINITE = 1
 REQ_DEGENERATE_RESIDUAL = 2
 REQ_BUDGET_SHORT = 4
 REQ_WALK_TIMEOUT = 8
+REQ_BAD_TOKEN = 16
+POOL_MAX = 64
 FLAG_NO_PRUNE = 1
 MAX_D, MAX_K, MAX_B, TRACE_MAX = 64, 32, 1023, 256
 KERNELS = ("draft_partials", "plan_tree", "replay_scan", "replay_merge", "target_partials",
-           "verify_walk", "verify_naive")
+           "verify_walk", "verify_naive", "pool_partials", "pool_lists", "pool_plan", "pool_replay", "pool_walk")
 
 EXPORTS = ("tsb_workspace_bytes", "tsb_plan", "tsb_plan_ep", "tsb_replay", "tsb_verify", "tsb_step",
            "tsb_first_tokens", "tsb_verify_naive", "tsb_step_first",
+           "tsb_pool_workspace_bytes", "tsb_pool_plan", "tsb_pool_replay", "tsb_pool_verify", "tsb_pool_step",
            "tsb_status_string", "tsb_last_error", "tsb_version", "tsb_profile_kernel")
 
 
@@ -95,6 +100,18 @@ def load(path=LIB_PATH):
                                      ctypes.POINTER(TsbVerdict), P, ctypes.c_size_t, P]
     lib.tsb_step_first.restype = ctypes.c_int
     lib.tsb_step_first.argtypes = lib.tsb_step.argtypes
+    I = ctypes.c_int32
+    cfgp, treep, verdp = ctypes.POINTER(TsbConfig), ctypes.POINTER(TsbTree), ctypes.POINTER(TsbVerdict)
+    lib.tsb_pool_workspace_bytes.restype = ctypes.c_size_t
+    lib.tsb_pool_workspace_bytes.argtypes = [cfgp, I]
+    lib.tsb_pool_plan.restype = ctypes.c_int
+    lib.tsb_pool_plan.argtypes = [cfgp, I, P, P, P, treep, P, P, P, ctypes.c_size_t, P]
+    lib.tsb_pool_replay.restype = ctypes.c_int
+    lib.tsb_pool_replay.argtypes = [cfgp, I, P, P, P, treep, ctypes.c_uint32, P, P]
+    lib.tsb_pool_verify.restype = ctypes.c_int
+    lib.tsb_pool_verify.argtypes = [cfgp, I, P, P, P, P, treep, P, ctypes.c_uint32, verdp, P, ctypes.c_size_t, P]
+    lib.tsb_pool_step.restype = ctypes.c_int
+    lib.tsb_pool_step.argtypes = [cfgp, I, P, P, P, ctypes.c_uint32, P, treep, P, verdp, P, ctypes.c_size_t, P]
     lib.tsb_status_string.restype = ctypes.c_char_p
     lib.tsb_status_string.argtypes = [ctypes.c_int]
     lib.tsb_last_error.restype = ctypes.c_char_p
@@ -115,6 +132,10 @@ def make_config(R, D, V, B, K, temperature, dtype, seed, flags=0):
 
 def workspace_bytes(cfg):
     return int(load().tsb_workspace_bytes(ctypes.byref(cfg)))
+
+
+def pool_workspace_bytes(cfg, P):
+    return int(load().tsb_pool_workspace_bytes(ctypes.byref(cfg), int(P)))
 
 
 def _ptr(t):
@@ -142,8 +163,10 @@ def _check(t, shape, dtype, name):
 class Round:
     """Output buffers and workspace of one configuration on one device."""
 
-    def __init__(self, cfg, device="cuda", target_lse=False, trace=False):
+    def __init__(self, cfg, device="cuda", target_lse=False, trace=False, pool=None):
+        """pool: pool size P to also hold the buffers of the pool entry points."""
         self.cfg = cfg
+        self.pool = None if pool is None else int(pool)
         R, D, B, K = cfg.R, cfg.D, cfg.B, cfg.K
         dev = torch.device(device)
         i32, f64 = torch.int32, torch.float64
@@ -166,6 +189,14 @@ class Round:
         nb = workspace_bytes(cfg)
         if nb == 0:
             raise ValueError("invalid configuration")
+        self.pool_tok = self.plan_tok = None
+        if self.pool is not None:
+            nbp = pool_workspace_bytes(cfg, self.pool)
+            if nbp == 0:
+                raise ValueError("invalid pool size %d" % self.pool)
+            nb = max(nb, nbp)
+            self.pool_tok = torch.empty(R, D, self.pool, dtype=i32, device=dev)
+            self.plan_tok = torch.empty(R, B + 1, dtype=i32, device=dev)
         self.ws = torch.zeros(nb + 256, dtype=torch.uint8, device=dev)  # zero-filled once (naive exchange tags)
         off = (-self.ws.data_ptr()) % 256
         self.ws_ptr = ctypes.c_void_p(self.ws.data_ptr() + off)
@@ -259,12 +290,61 @@ class Round:
         if st:
             raise TsbError(st, "tsb_step_first")
 
+    # ------------------------------------------------------------- pools
+    def _trans(self, trans):
+        cfg = self.cfg
+        if cfg.D == 1 and trans is None:
+            return None
+        _check(trans, (cfg.R, cfg.D - 1, self.pool, self.pool), torch.float32, "trans")
+        return trans
+
+    def pool_plan(self, draft, trans, plan_tokens=True, stream=None):
+        """First pass over pools of P tokens; plan_tok receives the planning tokens."""
+        self._logits(draft, self.cfg.D, "draft")
+        tr = self._trans(trans)
+        st = load().tsb_pool_plan(ctypes.byref(self.cfg), self.pool, _ptr(draft), _ptr(tr), _ptr(self.pool_tok),
+                                  ctypes.byref(self._tree_c), _ptr(self.plan_tok if plan_tokens else None),
+                                  _ptr(self.req_status), self.ws_ptr, self.ws_bytes, _stream(stream))
+        if st:
+            raise TsbError(st, "tsb_pool_plan")
+
+    def pool_replay(self, draft, trans, step, stream=None):
+        self._logits(draft, self.cfg.D, "draft")
+        tr = self._trans(trans)
+        st = load().tsb_pool_replay(ctypes.byref(self.cfg), self.pool, _ptr(draft), _ptr(tr), _ptr(self.pool_tok),
+                                    ctypes.byref(self._tree_c), int(step) & 0xFFFFFFFF, _ptr(self.node_tok),
+                                    _stream(stream))
+        if st:
+            raise TsbError(st, "tsb_pool_replay")
+
+    def pool_verify(self, draft, trans, target, step, stream=None):
+        self._logits(draft, self.cfg.D, "draft")
+        self._logits(target, self.cfg.B + 1, "target")
+        tr = self._trans(trans)
+        st = load().tsb_pool_verify(ctypes.byref(self.cfg), self.pool, _ptr(draft), _ptr(tr), _ptr(self.pool_tok),
+                                    _ptr(target), ctypes.byref(self._tree_c), _ptr(self.node_tok),
+                                    int(step) & 0xFFFFFFFF, ctypes.byref(self._verdict_c), self.ws_ptr,
+                                    self.ws_bytes, _stream(stream))
+        if st:
+            raise TsbError(st, "tsb_pool_verify")
+
+    def pool_step(self, draft, trans, target, step, stream=None):
+        self._logits(draft, self.cfg.D, "draft")
+        self._logits(target, self.cfg.B + 1, "target")
+        tr = self._trans(trans)
+        st = load().tsb_pool_step(ctypes.byref(self.cfg), self.pool, _ptr(draft), _ptr(tr), _ptr(target),
+                                  int(step) & 0xFFFFFFFF, _ptr(self.pool_tok), ctypes.byref(self._tree_c),
+                                  _ptr(self.node_tok), ctypes.byref(self._verdict_c), self.ws_ptr, self.ws_bytes,
+                                  _stream(stream))
+        if st:
+            raise TsbError(st, "tsb_pool_step")
+
     # ---------------------------------------------------------------- results
     def host(self):
         """Copy every output to host memory (synchronises the current stream)."""
         out = {k: v.cpu() for k, v in self.tree.items()}
         for k in ("draft_lse", "topk_tok", "topk_lp", "node_tok", "n_acc", "acc_node", "acc_tok", "bonus",
-                  "req_status", "target_lse", "trace"):
+                  "req_status", "target_lse", "trace", "pool_tok", "plan_tok"):
             v = getattr(self, k)
             out[k] = v.cpu() if v is not None else None
         return out

@@ -44,7 +44,9 @@ __device__ __forceinline__ void load8(const void* __restrict__ draft, size_t row
 
 constexpr int kDraftUnroll = 1;  // 8-logit groups per thread per chunk
 
-template <int DT, bool VEC>
+// STATS = false is the pool selection: the same candidate lists (K = pool
+// size) and finiteness flags without the normaliser (pm, ps unused).
+template <int DT, bool VEC, bool STATS>
 __global__ __launch_bounds__(kBlock) void draft_partials(const void* __restrict__ draft, int V, int D,
                                                          int seg, int S, float invT, int K,
                                                          float* __restrict__ pm, double* __restrict__ ps,
@@ -66,7 +68,7 @@ __global__ __launch_bounds__(kBlock) void draft_partials(const void* __restrict_
     for (int u = 0; u < kDraftUnroll; ++u) load8<DT, VEC>(draft, rowbase, lo + (u * kBlock + tid) * 8, hi, xc[u]);
 
     __shared__ double s_exp[kExpTable];
-    exp64_table_init(s_exp);
+    if (STATS) exp64_table_init(s_exp);
 
     float m = -INFINITY;    // running max of the scaled logits (-inf entries never raise it)
     double sum = 0.0;       // sum of e^(a - m) over this lane's elements
@@ -131,11 +133,11 @@ __global__ __launch_bounds__(kBlock) void draft_partials(const void* __restrict_
             }
             am = fmaxf(am, xm[u] * invT);  // rounding is monotone: the scaled max is the max of the scaled
         }
-        if (am > m && am < INFINITY) {
+        if (STATS && am > m && am < INFINITY) {
             sum = (m == -INFINITY) ? 0.0 : sum * exp64((double)m - (double)am, s_exp);
             m = am;
         }
-        {
+        if (STATS) {
             const double md = (double)m;
             double s2[2] = {0.0, 0.0};
 #pragma unroll
@@ -187,7 +189,7 @@ __global__ __launch_bounds__(kBlock) void draft_partials(const void* __restrict_
     __shared__ uint64_t s_top[kBlock / kWave][kWave];
     const float wm = wave_max(m);
     double contrib = (m == -INFINITY) ? 0.0 : sum * exp((double)m - (double)wm);
-    const double ws = wave_sum(contrib);
+    const double ws = STATS ? wave_sum(contrib) : 0.0;
     const int wb = wave_or(bad);
     if (lane == 0) {
         s_m[wave] = wm;
@@ -211,8 +213,10 @@ __global__ __launch_bounds__(kBlock) void draft_partials(const void* __restrict_
                 anybad |= s_bad[w];
             }
             const size_t o = (size_t)row * S + s;
-            pm[o] = M;
-            ps[o] = tot;
+            if (STATS) {
+                pm[o] = M;
+                ps[o] = tot;
+            }
             pf[o] = anybad;
         }
         if (lane < K) pk[((size_t)row * S + s) * K + lane] = top.v;
@@ -935,17 +939,17 @@ hipError_t launch_plan(const tsb_config& c, float invT, const void* draft, doubl
                                            : (c.V % 4 == 0 && ((uintptr_t)draft & 15) == 0);
     if (c.dtype == TSB_BF16) {
         if (vec)
-            draft_partials<TSB_BF16, true><<<grid1, kBlock, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT, c.K, pm, ps,
+            draft_partials<TSB_BF16, true, true><<<grid1, kBlock, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT, c.K, pm, ps,
                                                                      pk, pf, req_status);
         else
-            draft_partials<TSB_BF16, false><<<grid1, kBlock, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT, c.K, pm, ps,
+            draft_partials<TSB_BF16, false, true><<<grid1, kBlock, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT, c.K, pm, ps,
                                                                       pk, pf, req_status);
     } else {
         if (vec)
-            draft_partials<TSB_F32, true><<<grid1, kBlock, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT, c.K, pm, ps,
+            draft_partials<TSB_F32, true, true><<<grid1, kBlock, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT, c.K, pm, ps,
                                                                     pk, pf, req_status);
         else
-            draft_partials<TSB_F32, false><<<grid1, kBlock, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT, c.K, pm, ps,
+            draft_partials<TSB_F32, false, true><<<grid1, kBlock, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT, c.K, pm, ps,
                                                                      pk, pf, req_status);
     }
     e = hipGetLastError();
@@ -961,6 +965,34 @@ hipError_t launch_plan(const tsb_config& c, float invT, const void* draft, doubl
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     return hook_after(TSB_KERNEL_PLAN_TREE, st);
+}
+
+hipError_t launch_pool_partials(const tsb_config& c, int P, float invT, const void* draft, uint64_t* pk, int* pf,
+                                int32_t* req_status, hipStream_t st) {
+    const Geometry g = geometry(c);
+    const dim3 grid1(g.S1, c.R * c.D);
+    hipError_t e = hook_before(TSB_KERNEL_POOL_PARTIALS, st);
+    if (e != hipSuccess) return e;
+    const bool vec = (c.dtype == TSB_BF16) ? (c.V % 8 == 0 && ((uintptr_t)draft & 15) == 0)
+                                           : (c.V % 4 == 0 && ((uintptr_t)draft & 15) == 0);
+    if (c.dtype == TSB_BF16) {
+        if (vec)
+            draft_partials<TSB_BF16, true, false><<<grid1, kBlock, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT, P,
+                                                                            nullptr, nullptr, pk, pf, req_status);
+        else
+            draft_partials<TSB_BF16, false, false><<<grid1, kBlock, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT, P,
+                                                                             nullptr, nullptr, pk, pf, req_status);
+    } else {
+        if (vec)
+            draft_partials<TSB_F32, true, false><<<grid1, kBlock, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT, P,
+                                                                           nullptr, nullptr, pk, pf, req_status);
+        else
+            draft_partials<TSB_F32, false, false><<<grid1, kBlock, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT, P,
+                                                                            nullptr, nullptr, pk, pf, req_status);
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return hook_after(TSB_KERNEL_POOL_PARTIALS, st);
 }
 
 int ep_generated_bound(const tsb_config& c, int frontier) {

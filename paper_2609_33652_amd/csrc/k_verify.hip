@@ -185,6 +185,10 @@ struct WalkArgs {
     int V, D, B, S4, r0;
     float invT;
     uint32_t k0, k1, step;
+    // pool walk only: pools [R, D, P] and transition scores [R, D-1, P, P]
+    const int32_t* pool_tok;
+    const float* trans;
+    int P;
 };
 
 // binary64 log-sum-exp of target row (r, node) from its segment partials
@@ -628,11 +632,68 @@ __device__ void fill_pass(const WalkArgs& A, bool vec, const WalkSlice& S, bool 
     walk_sum4(out);
 }
 
+// End of a walk, for every workgroup of the request: every target row of
+// the tree must be finite (workgroup 0 decides); outputs of the request.
+__device__ void walk_tail(const WalkArgs& A, int r, int g, int G, int n, bool draft_bad, int nacc, int bonus_out,
+                          int add_status, int tcount) {
+    __shared__ int s_bad;
+    const int tid = threadIdx.x;
+    const int B1 = A.B + 1;
+    const size_t tb = (size_t)r * B1;
+    const bool lead = (g == 0 && tid == 0);
+    int* status_p = A.out.req_status + r;
+    // every target row of the tree must be finite; optional normaliser output
+    if (tid == 0) s_bad = 0;
+    __syncthreads();
+    if (!draft_bad) {
+        for (int i = g * kWalkThreads + tid; i < n; i += G * kWalkThreads) {
+            int b;
+            const double l = target_lse(A, r, i, &b);
+            if (b) atomicOr(&s_bad, 1);
+            if (A.out.target_lse) A.out.target_lse[tb + i] = b ? (double)NAN : l;
+        }
+    }
+    __syncthreads();
+    if (A.out.target_lse)
+        for (int i = n + g * kWalkThreads + tid; i < B1; i += G * kWalkThreads) A.out.target_lse[tb + i] = (double)NAN;
+    if (g == 0) {
+        // workgroup 0 decides the request's finiteness over all rows
+        if (tid == 0) s_bad = 0;
+        __syncthreads();
+        if (!draft_bad)
+            for (int i = tid; i < n; i += kWalkThreads) {
+                int b;
+                target_lse(A, r, i, &b);
+                if (b) atomicOr(&s_bad, 1);
+            }
+        __syncthreads();
+        const bool bad = draft_bad || s_bad;
+        if (bad && A.out.target_lse)
+            for (int i = tid; i < B1; i += kWalkThreads) A.out.target_lse[tb + i] = (double)NAN;
+        if (lead) {
+            if (bad) {
+                nacc = 0;
+                bonus_out = -1;
+                add_status = (add_status & ~(TSB_REQ_DEGENERATE_RESIDUAL | TSB_REQ_WALK_TIMEOUT)) | TSB_REQ_NONFINITE;
+            }
+            for (int i = nacc; i < A.D; ++i) {
+                A.out.acc_node[(size_t)r * A.D + i] = -1;
+                A.out.acc_tok[(size_t)r * A.D + i] = -1;
+            }
+            A.out.n_acc[r] = bad ? -1 : nacc;
+            A.out.bonus[r] = bonus_out;
+            *status_p |= add_status;
+            if (A.out.trace)
+                for (int i = tcount; i < TSB_TRACE_MAX; ++i)
+                    for (int f = 0; f < 4; ++f) A.out.trace[((size_t)r * TSB_TRACE_MAX + i) * 4 + f] = -1.0;
+        }
+    }
+}
+
 template <int DT, bool VEC>
 __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
     extern __shared__ double s_pq[];  // [2 * kWalkCache]: p~ then q
     __shared__ double s_exp[kExpTable];
-    __shared__ int s_bad;
     __shared__ int s_tok[TSB_MAX_K];
     __shared__ float s_xd[TSB_MAX_K], s_xt[TSB_MAX_K];
     __shared__ double s_u[TSB_MAX_K];
@@ -836,53 +897,320 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
         if (X.timeout) add_status |= TSB_REQ_WALK_TIMEOUT;
     }
 
-    // every target row of the tree must be finite; optional normaliser output
-    if (tid == 0) s_bad = 0;
-    __syncthreads();
+    walk_tail(A, r, g, G, n, draft_bad, nacc, bonus_out, add_status, tcount);
+}
+
+
+// ---------------------------------------------------------------- pool walk
+// Verification with pool-restricted, context-dependent q_u (Section 3.1;
+// Section 3.3: the probabilities of the replayed candidates, normalised in
+// the pool). At node u (depth d, token in slot s_u of pool d - 1) wave 0
+// rebuilds q_u over pool d from the draft logits and the transition scores,
+// z_j = fl32(a_j + fl32(c[d-1][s_u][j] invT)), q_j = exp(z_j - L_u), and
+// reads the target logits at the pool tokens. q vanishes off the pool, so
+// after a rejection the residual mass needs no vocabulary pass:
+//   Z = sum_{v off pool} p_v + sum_{v in pool} max(p_v - C q_v, 0)
+//     = (S~ - sum_{pool} p~_v) / S~ + sum_{pool} max(p~_v / S~ - C q_v, 0)
+// with p~_v = exp(a^t_v - L0) and S~ = sum_v p~_v from the one exact pass
+// over the target row (L0 the streamed normaliser). The residual bonus is a
+// Gumbel-max over the slice with the pool tokens left out (a bitmap of the
+// slice in LDS), merged with the pool tokens' residual keys.
+
+// Exact pass over the target row of the slice: sum of exp(a^t_v - L0).
+template <int DT>
+__device__ double target_pass(const WalkArgs& A, bool vec, const WalkSlice& S, size_t trow, double L0,
+                              const double* et) {
+    double sp = 0.0;
+    const int n = S.v1 - S.v0;
+    int i = (int)threadIdx.x * 4;
+    float at[4];
+    {
+        const int valid = max(0, min(4, n - i));
+        load4_scaled<DT>(A.target, trow + S.v0 + (valid ? i : 0), valid, vec, A.invT, at);
+    }
+    for (; i < n; i += 4 * kWalkThreads) {
+        const int inext = i + 4 * kWalkThreads;
+        float nt[4];
+        const int vn = max(0, min(4, n - inext));
+        load4_scaled<DT>(A.target, trow + S.v0 + (vn ? inext : 0), vn, vec, A.invT, nt);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sp += at[e] > -INFINITY ? exp64((double)at[e] - L0, et) : 0.0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) at[e] = nt[e];
+    }
+    return walk_sum(sp);
+}
+
+// Gumbel-max of ln p_v over the slice's tokens outside the pool.
+template <int DT>
+__device__ void bonus_off_pool(const WalkArgs& A, bool vec, const WalkSlice& S, size_t trow, double Lt,
+                               const RngKey& key, uint32_t node, const uint32_t* bits, float* bk, int* bi) {
+    float best = -INFINITY;
+    int bidx = 0x7FFFFFFF;
+    const SplitF Ls = split(Lt);
+    const int n = S.v1 - S.v0;
+    for (int i4 = threadIdx.x; i4 * 4 < n; i4 += kWalkThreads) {
+        const int i = i4 * 4;
+        const int valid = min(4, n - i);
+        float at[4];
+        load4_scaled<DT>(A.target, trow + S.v0 + i, valid, vec, A.invT, at);
+        const uint4 w = rng_block(key, node, kStreamBonus, (uint32_t)((S.v0 + i) >> 2));
+        const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            if (e >= valid || at[e] == -INFINITY) continue;
+            if ((bits[(i + e) >> 5] >> ((i + e) & 31)) & 1u) continue;  // a pool token
+            const float kv = ((at[e] - Ls.hi) - Ls.lo) + gumbel_f32(ws[e]);
+            const int v = S.v0 + i + e;
+            if (kv > best || (kv == best && v < bidx)) {
+                best = kv;
+                bidx = v;
+            }
+        }
+    }
+    *bk = best;
+    *bi = bidx;
+}
+
+template <int DT, bool VEC>
+__global__ __launch_bounds__(kWalkThreads) void verify_pool_walk(WalkArgs A) {
+    extern __shared__ uint32_t s_bits[];  // pool membership over the slice
+    __shared__ double s_exp[kExpTable];
+    __shared__ int s_ptok[kPoolMax];
+    __shared__ double s_q[kPoolMax], s_pp[kPoolMax];
+    __shared__ float s_pat[kPoolMax];
+    __shared__ int s_tok[TSB_MAX_K], s_cslot[TSB_MAX_K];
+    __shared__ float s_xt[TSB_MAX_K];
+    __shared__ double s_u[TSB_MAX_K];
+    __shared__ double s_z;
+    __shared__ int s_badtok;
+    const int g = blockIdx.x;
+    const int G = gridDim.x;
+    const int r = A.r0 + blockIdx.y;
+    const int tid = threadIdx.x;
+    const int lane = tid % kWave;
+    const int B1 = A.B + 1;
+    const int P = A.P;
+    const size_t tb = (size_t)r * B1;
+    const bool vec = VEC;
+    const int n = A.tree.n_nodes[r];
+    const bool lead = (g == 0 && tid == 0);
+    exp64_table_init(s_exp);
+    if (tid == 0) s_badtok = 0;
+
+    WalkSlice S;
+    {
+        const int span = ((A.V + G - 1) / G + 3) & ~3;
+        const bool has = (long long)g * span < A.V;
+        S.v0 = has ? g * span : 0;
+        S.v1 = has ? min(A.V, S.v0 + span) : 0;
+        S.nchunks = 1;
+        S.p = nullptr;
+        S.q = nullptr;
+    }
+    const int nwords = (S.v1 - S.v0 + 31) / 32;
+    const bool draft_bad = (A.out.req_status[r] & TSB_REQ_NONFINITE) != 0;
+
+    int tcount = 0;
+    double* const trace = (lead && A.out.trace) ? A.out.trace + (size_t)r * TSB_TRACE_MAX * 4 : nullptr;
+
+    int bonus_out = -1, add_status = 0, nacc = 0;
     if (!draft_bad) {
-        for (int i = g * kWalkThreads + tid; i < n; i += G * kWalkThreads) {
-            int b;
-            const double l = target_lse(A, r, i, &b);
-            if (b) atomicOr(&s_bad, 1);
-            if (A.out.target_lse) A.out.target_lse[tb + i] = b ? (double)NAN : l;
+        RngKey key;
+        key.k0 = A.k0;
+        key.k1 = A.k1;
+        key.request = (uint32_t)r;
+        key.step = A.step;
+        Exchange X{&A, r, g, G, A.X.seqs[r], 0u, 0};
+        int u = 0, su = 0;
+        while (true) {
+            const int m = A.tree.n_children[tb + u];
+            const int d = A.tree.depth[tb + u];
+            const size_t trow = ((size_t)r * B1 + u) * (size_t)A.V;
+            int tbad;
+            const double L0 = target_lse(A, r, u, &tbad);
+            if (m == 0) {  // accepted leaf: bonus from p_u
+                float bk;
+                int bi;
+                double unused;
+                bonus_from_p<DT>(A, vec, S, trow, L0, key, (uint32_t)u, &bk, &bi);
+                bonus_out = X.best(bk, bi, 0.0, &unused);
+                break;
+            }
+            // q_u over pool d, target logits at the pool tokens
+            if (tid < kWave) {
+                float z = -INFINITY, at = -INFINITY;
+                int tok = -1;
+                if (lane < P) {
+                    tok = A.pool_tok[((size_t)r * A.D + d) * P + lane];
+                    if (tok >= 0 && tok < A.V) {
+                        z = load_logit<DT>(A.draft, ((size_t)r * A.D + d) * A.V + tok) * A.invT;
+                        if (d > 0) {
+                            const float c = A.trans[(((size_t)r * (A.D - 1) + (d - 1)) * P + su) * (size_t)P + lane];
+                            const float cs = c * A.invT;
+                            z = z + cs;
+                        }
+                        at = load_logit<DT>(A.target, trow + tok) * A.invT;
+                    }
+                }
+                const float zm = wave_max(z);
+                double q = 0.0;
+                if (zm > -INFINITY) {
+                    const double e = z > -INFINITY ? exp64((double)z - (double)zm, s_exp) : 0.0;
+                    const double Lz = (double)zm + log(wave_sum(e));
+                    q = z > -INFINITY ? exp64((double)z - Lz, s_exp) : 0.0;
+                }
+                if (lane < P) {
+                    s_ptok[lane] = tok;
+                    s_q[lane] = q;
+                    s_pat[lane] = at;
+                }
+            }
+            const int fc = A.tree.first_child[tb + u];
+            if (tid < m) {
+                const int y = A.node_tok[tb + fc + tid];
+                s_tok[tid] = y;
+                s_xt[tid] = (y >= 0 && y < A.V) ? load_logit<DT>(A.target, trow + y) * A.invT : -INFINITY;
+                s_u[tid] = u24d(rng_word(key, (uint32_t)(fc + tid), kStreamAccept, 0u));
+            }
+            __syncthreads();
+            if (tid < m) {  // pool slot of each child's token
+                const int y = s_tok[tid];
+                int sl = -1;
+                for (int j = 0; j < P; ++j)
+                    if (s_ptok[j] == y) {
+                        sl = j;
+                        break;
+                    }
+                s_cslot[tid] = sl;
+                if (sl < 0) s_badtok = 1;
+            }
+            __syncthreads();
+
+            bool exact = false;
+            double Lt = L0, inv = 1.0, Stot = 1.0;
+            double C = 0.0, Sq = 1.0, Z = 1.0;
+            bool accepted = false, degenerate = false;
+            for (int j = 0; j < m; ++j) {
+                const int c = fc + j;
+                const int y = s_tok[j];
+                const int sl = s_cslot[j];
+                const double qy = sl >= 0 ? s_q[sl] : 0.0;
+                const double U = s_u[j];
+                const double W = Z / Sq;
+                double py = s_xt[j] > -INFINITY ? exp((double)s_xt[j] - Lt) : 0.0;
+                double num = py - C * qy;
+                double ratio = qy > 0.0 ? (num > 0.0 ? num : 0.0) / (W * qy) : (py > 0.0 ? INFINITY : 0.0);
+                if (trace && tcount < TSB_TRACE_MAX) {
+                    trace[tcount * 4 + 0] = c;
+                    trace[tcount * 4 + 1] = U;
+                    trace[tcount * 4 + 3] = -1.0;
+                }
+                ++tcount;
+                if (!exact && (fabs(U - ratio) <= kDecisionBand * ratio || !(U < ratio))) {
+                    Stot = X.sum(target_pass<DT>(A, vec, S, trow, L0, s_exp));
+                    Lt = L0 + log(Stot);
+                    inv = 1.0 / Stot;
+                    exact = true;
+                    // pool probabilities p~_v with the same exponential as the pass
+                    if (tid < kWave) {
+                        const double pp = lane < P && s_pat[lane] > -INFINITY ? exp64((double)s_pat[lane] - L0, s_exp)
+                                                                              : 0.0;
+                        if (lane < P) s_pp[lane] = pp;
+                    }
+                    __syncthreads();
+                    py = s_xt[j] > -INFINITY ? exp((double)s_xt[j] - Lt) : 0.0;
+                    num = py - C * qy;
+                    ratio = qy > 0.0 ? (num > 0.0 ? num : 0.0) / (W * qy) : (py > 0.0 ? INFINITY : 0.0);
+                }
+                if (trace && tcount <= TSB_TRACE_MAX) trace[(tcount - 1) * 4 + 2] = ratio;
+                if (U < ratio) {
+                    if (lead) {
+                        A.out.acc_node[(size_t)r * A.D + nacc] = c;
+                        A.out.acc_tok[(size_t)r * A.D + nacc] = y;
+                    }
+                    ++nacc;
+                    u = c;
+                    su = sl >= 0 ? sl : 0;
+                    accepted = true;
+                    break;
+                }
+                C = C + W;
+                Sq = Sq - qy;
+                // residual mass at the new C, from the pool alone
+                if (tid < kWave) {
+                    double pin = 0.0, res = 0.0;
+                    if (lane < P) {
+                        pin = s_pp[lane];
+                        const double rr = s_pp[lane] * inv - C * s_q[lane];
+                        res = rr > 0.0 ? rr : 0.0;
+                    }
+                    pin = wave_sum(pin);
+                    res = wave_sum(res);
+                    if (lane == 0) s_z = (Stot - pin) * inv + res;
+                }
+                __syncthreads();
+                Z = s_z;
+                __syncthreads();
+                if (trace && tcount <= TSB_TRACE_MAX) trace[(tcount - 1) * 4 + 3] = Z;
+                if (Z <= 0.0 || (j + 1 < m && Sq <= 0.0)) {
+                    degenerate = true;
+                    break;
+                }
+            }
+            __syncthreads();  // s_tok & co. are rewritten at the next node
+            if (accepted) continue;
+            // every child rejected: bonus from the residual max(p - C q, 0)
+            if (!degenerate) {
+                for (int w = tid; w < nwords; w += kWalkThreads) s_bits[w] = 0u;
+                __syncthreads();
+                if (tid < P) {
+                    const int t = s_ptok[tid];
+                    if (t >= S.v0 && t < S.v1) atomicOr(&s_bits[(t - S.v0) >> 5], 1u << ((t - S.v0) & 31));
+                }
+                __syncthreads();
+                float best;
+                int bidx;
+                bonus_off_pool<DT>(A, vec, S, trow, Lt, key, (uint32_t)u, s_bits, &best, &bidx);
+                if (tid < P) {
+                    const int t = s_ptok[tid];
+                    if (t >= S.v0 && t < S.v1) {
+                        const double rr = s_pp[tid] * inv - C * s_q[tid];
+                        if (rr > 0.0) {
+                            const float kv = logf((float)rr) +
+                                             gumbel_f32(rng_word(key, (uint32_t)u, kStreamBonus, (uint32_t)t));
+                            if (kv > best || (kv == best && t < bidx)) {
+                                best = kv;
+                                bidx = t;
+                            }
+                        }
+                    }
+                }
+                walk_argmax(&best, &bidx);
+                double unused;
+                const int fi = X.best(best, bidx, 0.0, &unused);
+                if (fi >= 0) {
+                    bonus_out = fi;
+                } else {
+                    degenerate = true;
+                }
+            }
+            if (degenerate) {  // empty residual: bonus from p_u
+                float bk;
+                int bi;
+                double unused;
+                bonus_from_p<DT>(A, vec, S, trow, Lt, key, (uint32_t)u, &bk, &bi);
+                bonus_out = X.best(bk, bi, 0.0, &unused);
+                add_status |= TSB_REQ_DEGENERATE_RESIDUAL;
+            }
+            break;
         }
-        if (g != 0 && tid == 0 && s_bad == 0) { /* workgroup 0 checks every row below */ }
-    }
-    __syncthreads();
-    if (A.out.target_lse)
-        for (int i = n + g * kWalkThreads + tid; i < B1; i += G * kWalkThreads) A.out.target_lse[tb + i] = (double)NAN;
-    if (g == 0) {
-        // workgroup 0 decides the request's finiteness over all rows
-        if (tid == 0) s_bad = 0;
+        if (X.nb > 0) xfinish(A.X, r, g, G, X.seq, X.nb);
+        if (X.timeout) add_status |= TSB_REQ_WALK_TIMEOUT;
         __syncthreads();
-        if (!draft_bad)
-            for (int i = tid; i < n; i += kWalkThreads) {
-                int b;
-                target_lse(A, r, i, &b);
-                if (b) atomicOr(&s_bad, 1);
-            }
-        __syncthreads();
-        const bool bad = draft_bad || s_bad;
-        if (bad && A.out.target_lse)
-            for (int i = tid; i < B1; i += kWalkThreads) A.out.target_lse[tb + i] = (double)NAN;
-        if (lead) {
-            if (bad) {
-                nacc = 0;
-                bonus_out = -1;
-                add_status = (add_status & ~(TSB_REQ_DEGENERATE_RESIDUAL | TSB_REQ_WALK_TIMEOUT)) | TSB_REQ_NONFINITE;
-            }
-            for (int i = nacc; i < A.D; ++i) {
-                A.out.acc_node[(size_t)r * A.D + i] = -1;
-                A.out.acc_tok[(size_t)r * A.D + i] = -1;
-            }
-            A.out.n_acc[r] = bad ? -1 : nacc;
-            A.out.bonus[r] = bonus_out;
-            *status_p |= add_status;
-            if (A.out.trace)
-                for (int i = tcount; i < TSB_TRACE_MAX; ++i)
-                    for (int f = 0; f < 4; ++f) A.out.trace[((size_t)r * TSB_TRACE_MAX + i) * 4 + f] = -1.0;
-        }
+        if (s_badtok) add_status |= TSB_REQ_BAD_TOKEN;
     }
+    walk_tail(A, r, g, G, n, draft_bad, nacc, bonus_out, add_status, tcount);
 }
 
 // ------------------------------------------------------------------ launch
@@ -893,14 +1221,14 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
 // turns a device shared with other work (workgroups kept waiting) into
 // TSB_REQ_WALK_TIMEOUT instead of a hang. Queried once per (device,
 // kernel instance).
-static hipError_t walk_capacity(const void* fn, int dt, int vec, size_t lds, int* cap) {
+static hipError_t walk_capacity(const void* fn, int kind, int dt, int vec, size_t lds, int* cap) {
     constexpr int kDevs = 64;
-    static std::atomic<int> cached[kDevs][2][2];
+    static std::atomic<int> cached[kDevs][2][2][2];
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
     if (dev >= 0 && dev < kDevs) {
-        const int v = cached[dev][dt][vec].load(std::memory_order_relaxed);
+        const int v = cached[dev][kind][dt][vec].load(std::memory_order_relaxed);
         if (v > 0) {
             *cap = v;
             return hipSuccess;
@@ -911,13 +1239,12 @@ static hipError_t walk_capacity(const void* fn, int dt, int vec, size_t lds, int
     if ((e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds)) != hipSuccess) return e;
     if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kWalkThreads, lds)) != hipSuccess) return e;
     *cap = per_cu * cus;
-    if (dev >= 0 && dev < kDevs && *cap > 0) cached[dev][dt][vec].store(*cap, std::memory_order_relaxed);
+    if (dev >= 0 && dev < kDevs && *cap > 0) cached[dev][kind][dt][vec].store(*cap, std::memory_order_relaxed);
     return hipSuccess;
 }
 
-hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, const double* draft_lse,
-                         const void* target, const tsb_tree& tree, const int32_t* node_tok, uint32_t step,
-                         const tsb_verdict& out, char* ws, hipStream_t st) {
+static hipError_t launch_target_partials(const tsb_config& c, float invT, const void* target, const tsb_tree& tree,
+                                         char* ws, hipStream_t st) {
     const Geometry g = geometry(c);
     const VerifyWs w = verify_ws(c);
     float* tm = (float*)(ws + w.tm);
@@ -945,8 +1272,15 @@ hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, con
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if ((e = hook_after(TSB_KERNEL_TARGET_PARTIALS, st)) != hipSuccess) return e;
+    return hook_after(TSB_KERNEL_TARGET_PARTIALS, st);
+}
 
+// Walk arguments shared by both walks.
+static WalkArgs walk_args(const tsb_config& c, float invT, const void* draft, const double* draft_lse,
+                          const void* target, const tsb_tree& tree, const int32_t* node_tok, uint32_t step,
+                          const tsb_verdict& out, char* ws) {
+    const Geometry g = geometry(c);
+    const VerifyWs w = verify_ws(c);
     WalkArgs A;
     A.draft = draft;
     A.draft_lse = draft_lse;
@@ -954,9 +1288,9 @@ hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, con
     A.tree = tree;
     A.node_tok = node_tok;
     A.out = out;
-    A.tm = tm;
-    A.ts = ts;
-    A.tf = tf;
+    A.tm = (const float*)(ws + w.tm);
+    A.ts = (const double*)(ws + w.ts);
+    A.tf = (const int*)(ws + w.tf);
     const XchgWs xw = xchg_ws(c);
     A.X.seqs = (uint32_t*)(ws + xw.seq);
     A.X.slots = (uint64_t*)(ws + xw.slots);
@@ -964,34 +1298,84 @@ hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, con
     A.D = c.D;
     A.B = c.B;
     A.S4 = g.S4;
+    A.r0 = 0;
     A.invT = invT;
     A.k0 = (uint32_t)c.seed;
     A.k1 = (uint32_t)(c.seed >> 32);
     A.step = step;
+    A.pool_tok = nullptr;
+    A.trans = nullptr;
+    A.P = 0;
+    return A;
+}
 
+// Launches of a walk grid (G workgroups per request) within the resident
+// capacity, in order of requests.
+static hipError_t launch_walk_grid(const void* fn, WalkArgs& A, int R, int G0, int cap, size_t lds, hipStream_t st) {
+    int G = G0;
+    if (G * R > cap) G = cap / R > 0 ? cap / R : 1;
+    const int chunk = cap / G;
+    for (int r0 = 0; r0 < R; r0 += chunk) {
+        A.r0 = r0;
+        const int rc = min(chunk, R - r0);
+        void* args[] = {&A};
+        const hipError_t e = hipLaunchKernel(fn, dim3(G, rc), dim3(kWalkThreads), args, lds, st);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, const double* draft_lse,
+                         const void* target, const tsb_tree& tree, const int32_t* node_tok, uint32_t step,
+                         const tsb_verdict& out, char* ws, hipStream_t st) {
+    hipError_t e = launch_target_partials(c, invT, target, tree, ws, st);
+    if (e != hipSuccess) return e;
+    WalkArgs A = walk_args(c, invT, draft, draft_lse, target, tree, node_tok, step, out, ws);
     const bool vec4 = c.V % 4 == 0 && ((uintptr_t)target & 15) == 0 && ((uintptr_t)draft & 15) == 0;
     const void* fn = nullptr;
     if (c.dtype == TSB_BF16)
         fn = vec4 ? (const void*)verify_walk<TSB_BF16, true> : (const void*)verify_walk<TSB_BF16, false>;
     else
         fn = vec4 ? (const void*)verify_walk<TSB_F32, true> : (const void*)verify_walk<TSB_F32, false>;
-
     const size_t lds = 2 * (size_t)kWalkCache * sizeof(double);
     int cap = 0;
-    if ((e = walk_capacity(fn, c.dtype == TSB_BF16 ? 1 : 0, vec4 ? 1 : 0, lds, &cap)) != hipSuccess) return e;
+    if ((e = walk_capacity(fn, 0, c.dtype == TSB_BF16 ? 1 : 0, vec4 ? 1 : 0, lds, &cap)) != hipSuccess) return e;
     if (cap < 1) return hipErrorLaunchOutOfResources;
-    int G = g.G;
-    if (G * c.R > cap) G = cap / c.R > 0 ? cap / c.R : 1;
-    const int chunk = cap / G;
     if ((e = hook_before(TSB_KERNEL_VERIFY_WALK, st)) != hipSuccess) return e;
-    for (int r0 = 0; r0 < c.R; r0 += chunk) {
-        A.r0 = r0;
-        const int rc = min(chunk, c.R - r0);
-        void* args[] = {&A};
-        e = hipLaunchKernel(fn, dim3(G, rc), dim3(kWalkThreads), args, lds, st);
-        if (e != hipSuccess) return e;
-    }
+    if ((e = launch_walk_grid(fn, A, c.R, geometry(c).G, cap, lds, st)) != hipSuccess) return e;
     return hook_after(TSB_KERNEL_VERIFY_WALK, st);
+}
+
+hipError_t launch_pool_verify(const tsb_config& c, int P, float invT, const void* draft, const float* trans,
+                              const int32_t* pool_tok, const void* target, const tsb_tree& tree,
+                              const int32_t* node_tok, uint32_t step, const tsb_verdict& out, char* ws,
+                              hipStream_t st) {
+    hipError_t e = launch_target_partials(c, invT, target, tree, ws, st);
+    if (e != hipSuccess) return e;
+    WalkArgs A = walk_args(c, invT, draft, nullptr, target, tree, node_tok, step, out, ws);
+    A.pool_tok = pool_tok;
+    A.trans = trans;
+    A.P = P;
+    const bool vec4 = c.V % 4 == 0 && ((uintptr_t)target & 15) == 0;
+    const void* fn = nullptr;
+    if (c.dtype == TSB_BF16)
+        fn = vec4 ? (const void*)verify_pool_walk<TSB_BF16, true> : (const void*)verify_pool_walk<TSB_BF16, false>;
+    else
+        fn = vec4 ? (const void*)verify_pool_walk<TSB_F32, true> : (const void*)verify_pool_walk<TSB_F32, false>;
+    // the slice bitmap: one bit per token of the widest slice at the fewest
+    // workgroups per request the capacity allows
+    const size_t lds_max = kPoolBitmapBytes;
+    int cap = 0;
+    if ((e = walk_capacity(fn, 1, c.dtype == TSB_BF16 ? 1 : 0, vec4 ? 1 : 0, lds_max, &cap)) != hipSuccess) return e;
+    if (cap < 1) return hipErrorLaunchOutOfResources;
+    int G = geometry(c).G;
+    if (G * c.R > cap) G = cap / c.R > 0 ? cap / c.R : 1;
+    const long long span = (((long long)c.V + G - 1) / G + 3) & ~3ll;
+    const size_t lds = (size_t)((span + 31) / 32) * sizeof(uint32_t);
+    if (lds > lds_max) return hipErrorInvalidConfiguration;  // vocabulary too wide for the slice bitmap
+    if ((e = hook_before(TSB_KERNEL_POOL_WALK, st)) != hipSuccess) return e;
+    if ((e = launch_walk_grid(fn, A, c.R, G, cap, lds, st)) != hipSuccess) return e;
+    return hook_after(TSB_KERNEL_POOL_WALK, st);
 }
 
 }  // namespace tsb

@@ -71,11 +71,28 @@ struct VerifyWs {  // target partials
     size_t tm, ts, tf, total;
 };
 
+// The region that verification keeps across calls comes first (no stage
+// writes it): a sequence number per request and the exchange slots of the
+// workgroups of a request, [R][2][kWalkGroupsMax][8] 64-bit words. Every
+// stage's scratch starts after it, so all entry points agree on where it is.
+struct XchgWs {
+    size_t seq, slots, total;
+};
+
+inline XchgWs xchg_ws(const tsb_config& c) {
+    XchgWs w;
+    size_t o = 0;
+    w.seq = o; o = align256(o + (size_t)c.R * sizeof(uint32_t));
+    w.slots = o; o = align256(o + (size_t)c.R * 2 * kWalkGroupsMax * 8 * sizeof(uint64_t));
+    w.total = o;
+    return w;
+}
+
 inline PlanWs plan_ws(const tsb_config& c) {
     const Geometry g = geometry(c);
     const size_t n = (size_t)c.R * c.D * g.S1;
     PlanWs w;
-    size_t o = 0;
+    size_t o = xchg_ws(c).total;
     w.pm = o; o = align256(o + n * sizeof(float));
     w.ps = o; o = align256(o + n * sizeof(double));
     w.pk = o; o = align256(o + n * (size_t)c.K * sizeof(uint64_t));
@@ -88,7 +105,7 @@ inline ReplayWs replay_ws(const tsb_config& c) {
     const Geometry g = geometry(c);
     const size_t slots = (size_t)c.R * (c.B + 1) * g.T;
     ReplayWs w;
-    size_t o = 0;
+    size_t o = xchg_ws(c).total;
     w.cand = o; o = align256(o + slots * TSB_MAX_K * sizeof(uint64_t));
     w.cnt = o; o = align256(o + slots * sizeof(int32_t));
     w.plist = o; o = align256(o + (size_t)c.R * (c.B + 1) * sizeof(int32_t));
@@ -102,7 +119,7 @@ inline VerifyWs verify_ws(const tsb_config& c) {
     const Geometry g = geometry(c);
     const size_t n = (size_t)c.R * (c.B + 1) * g.S4;
     VerifyWs w;
-    size_t o = 0;
+    size_t o = xchg_ws(c).total;
     w.tm = o; o = align256(o + n * sizeof(float));
     w.ts = o; o = align256(o + n * sizeof(double));
     w.tf = o; o = align256(o + n * sizeof(int32_t));
@@ -110,28 +127,48 @@ inline VerifyWs verify_ws(const tsb_config& c) {
     return w;
 }
 
-// Region that verification keeps across calls, after every stage's scratch
-// (no other stage writes it): a sequence number per request and the
-// exchange slots of the workgroups of a request, [R][2][kWalkGroupsMax][8]
-// 64-bit words.
-struct XchgWs {
-    size_t seq, slots, total;
-};
-
-inline size_t stage_ws_bytes(const tsb_config& c) {
-    size_t m = plan_ws(c).total;
-    const size_t b = replay_ws(c).total, v = verify_ws(c).total;
-    m = m > b ? m : b;
-    return m > v ? m : v;
+inline size_t max3(size_t a, size_t b, size_t c) {
+    const size_t m = a > b ? a : b;
+    return m > c ? m : c;
 }
 
-inline XchgWs xchg_ws(const tsb_config& c) {
-    XchgWs w;
-    size_t o = align256(stage_ws_bytes(c));
-    w.seq = o; o = align256(o + (size_t)c.R * sizeof(uint32_t));
-    w.slots = o; o = align256(o + (size_t)c.R * 2 * kWalkGroupsMax * 8 * sizeof(uint64_t));
+// Whole workspace of the vocabulary-wide entry points.
+inline size_t ws_bytes(const tsb_config& c) {
+    return max3(plan_ws(c).total, replay_ws(c).total, verify_ws(c).total);
+}
+
+// Pools of P tokens per draft position: segment candidate lists of the pool
+// selection, then the candidate lists of every (position, parent slot):
+// list 0 is the root's, list 1 + (d - 1) P + i that of a node at depth d >= 1
+// whose token holds slot i of pool d - 1; entries pack (lp bits << 32 | slot).
+constexpr int kPoolMax = 64;
+// LDS bitmap of the pool tokens in a walk workgroup's vocabulary slice
+// (slices up to 262144 tokens).
+constexpr size_t kPoolBitmapBytes = 32768;
+
+inline int pool_lists_per_request(const tsb_config& c, int P) { return 1 + (c.D - 1) * P; }
+
+struct PoolWs {
+    size_t pk, pf, lists, nfin, total;
+};
+
+inline PoolWs pool_ws(const tsb_config& c, int P) {
+    const Geometry g = geometry(c);
+    const size_t n = (size_t)c.R * c.D * g.S1;
+    const size_t nl = (size_t)c.R * pool_lists_per_request(c, P);
+    PoolWs w;
+    size_t o = xchg_ws(c).total;
+    w.pk = o; o = align256(o + n * (size_t)P * sizeof(uint64_t));
+    w.pf = o; o = align256(o + n * sizeof(int32_t));
+    w.lists = o; o = align256(o + nl * (size_t)c.K * sizeof(uint64_t));
+    w.nfin = o; o = align256(o + nl * sizeof(int32_t));
     w.total = o;
     return w;
+}
+
+inline size_t pool_ws_bytes(const tsb_config& c, int P) {
+    const size_t a = pool_ws(c, P).total, v = verify_ws(c).total;
+    return a > v ? a : v;
 }
 
 }  // namespace tsb

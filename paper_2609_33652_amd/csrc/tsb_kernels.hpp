@@ -42,6 +42,20 @@ hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, con
                          const void* target, const tsb_tree& tree, const int32_t* node_tok, uint32_t step,
                          const tsb_verdict& out, char* ws, hipStream_t st);
 
+// Sparse candidate pools of P tokens with context-dependent q_u.
+hipError_t launch_pool_partials(const tsb_config& c, int P, float invT, const void* draft, uint64_t* pk, int* pf,
+                                int32_t* req_status, hipStream_t st);
+hipError_t launch_pool_plan(const tsb_config& c, int P, float invT, const void* draft, const float* trans,
+                            int32_t* pool_tok, const tsb_tree& tree, int32_t* plan_tok, int32_t* req_status,
+                            char* ws, hipStream_t st);
+hipError_t launch_pool_replay(const tsb_config& c, int P, float invT, const void* draft, const float* trans,
+                              const int32_t* pool_tok, const tsb_tree& tree, uint32_t step, int32_t* node_tok,
+                              hipStream_t st);
+hipError_t launch_pool_verify(const tsb_config& c, int P, float invT, const void* draft, const float* trans,
+                              const int32_t* pool_tok, const void* target, const tsb_tree& tree,
+                              const int32_t* node_tok, uint32_t step, const tsb_verdict& out, char* ws,
+                              hipStream_t st);
+
 hipError_t launch_first_tokens(const tsb_config& c, const int32_t* topk_tok, const tsb_tree& tree, int32_t* node_tok,
                                hipStream_t st);
 

@@ -66,6 +66,21 @@ tsb_status check_verdict(const tsb_verdict* o) {
     return TSB_OK;
 }
 
+tsb_status check_pool(const tsb_config* c, int P, const float* trans) {
+    const int pmax = c->V < tsb::kPoolMax ? c->V : tsb::kPoolMax;
+    if (P < c->K || P > pmax) return fail(TSB_E_SHAPE, "P=%d must be in [K=%d, %d]", P, c->K, pmax);
+    if (c->D > 1 && !trans) return fail(TSB_E_NULL, "trans is NULL with D=%d", c->D);
+    return TSB_OK;
+}
+
+tsb_status check_pool_ws(const tsb_config* c, int P, void* ws, size_t bytes) {
+    const size_t need = tsb::pool_ws_bytes(*c, P);
+    if (!ws) return fail(TSB_E_NULL, "workspace is NULL");
+    if (((uintptr_t)ws & 255) != 0) return fail(TSB_E_WORKSPACE, "workspace not 256-byte aligned");
+    if (bytes < need) return fail(TSB_E_WORKSPACE, "workspace has %zu bytes, needs %zu", bytes, need);
+    return TSB_OK;
+}
+
 float inv_temperature(float T) {
     volatile float one = 1.0f;  // binary32 division, correctly rounded
     return one / T;
@@ -95,7 +110,7 @@ size_t tsb_workspace_bytes(const tsb_config* cfg) {
     const tsb_status s = check_config(cfg);
     memcpy(g_last_error, saved, sizeof saved);
     if (s != TSB_OK) return 0;
-    const size_t m = tsb::xchg_ws(*cfg).total;
+    const size_t m = tsb::ws_bytes(*cfg);
     return m < 256 ? 256 : m;
 }
 
@@ -225,6 +240,85 @@ tsb_status tsb_step_first(const tsb_config* cfg, const void* draft, const void* 
     return TSB_OK;
 }
 
+size_t tsb_pool_workspace_bytes(const tsb_config* cfg, int32_t P) {
+    if (!cfg) return 0;
+    char saved[sizeof g_last_error];
+    memcpy(saved, g_last_error, sizeof saved);
+    tsb_status s = check_config(cfg);
+    if (s == TSB_OK) s = check_pool(cfg, P, (const float*)cfg /* any non-NULL */);
+    memcpy(g_last_error, saved, sizeof saved);
+    if (s != TSB_OK) return 0;
+    const size_t m = tsb::pool_ws_bytes(*cfg, P);
+    return m < 256 ? 256 : m;
+}
+
+tsb_status tsb_pool_plan(const tsb_config* cfg, int32_t P, const void* draft, const float* trans, int32_t* pool_tok,
+                         const tsb_tree* tree, int32_t* plan_tok, int32_t* req_status, void* workspace,
+                         size_t workspace_bytes, hipStream_t stream) {
+    g_last_error[0] = 0;
+    TRY(check_config(cfg));
+    TRY(check_pool(cfg, P, trans));
+    if (!draft || !pool_tok || !req_status) return fail(TSB_E_NULL, "tsb_pool_plan: a required array is NULL");
+    TRY(check_tree(tree));
+    TRY(check_pool_ws(cfg, P, workspace, workspace_bytes));
+    const hipError_t e = tsb::launch_pool_plan(*cfg, P, inv_temperature(cfg->temperature), draft, trans, pool_tok,
+                                               *tree, plan_tok, req_status, (char*)workspace, stream);
+    return e == hipSuccess ? TSB_OK : hip_fail(e, "tsb_pool_plan");
+}
+
+tsb_status tsb_pool_replay(const tsb_config* cfg, int32_t P, const void* draft, const float* trans,
+                           const int32_t* pool_tok, const tsb_tree* tree, uint32_t step, int32_t* node_tok,
+                           hipStream_t stream) {
+    g_last_error[0] = 0;
+    TRY(check_config(cfg));
+    TRY(check_pool(cfg, P, trans));
+    if (!draft || !pool_tok || !node_tok) return fail(TSB_E_NULL, "tsb_pool_replay: a required array is NULL");
+    TRY(check_tree(tree));
+    const hipError_t e = tsb::launch_pool_replay(*cfg, P, inv_temperature(cfg->temperature), draft, trans, pool_tok,
+                                                 *tree, step, node_tok, stream);
+    return e == hipSuccess ? TSB_OK : hip_fail(e, "tsb_pool_replay");
+}
+
+tsb_status tsb_pool_verify(const tsb_config* cfg, int32_t P, const void* draft, const float* trans,
+                           const int32_t* pool_tok, const void* target, const tsb_tree* tree, const int32_t* node_tok,
+                           uint32_t step, const tsb_verdict* out, void* workspace, size_t workspace_bytes,
+                           hipStream_t stream) {
+    g_last_error[0] = 0;
+    TRY(check_config(cfg));
+    TRY(check_pool(cfg, P, trans));
+    if (!draft || !pool_tok || !target || !node_tok)
+        return fail(TSB_E_NULL, "tsb_pool_verify: a required array is NULL");
+    TRY(check_tree(tree));
+    TRY(check_verdict(out));
+    TRY(check_pool_ws(cfg, P, workspace, workspace_bytes));
+    const hipError_t e = tsb::launch_pool_verify(*cfg, P, inv_temperature(cfg->temperature), draft, trans, pool_tok,
+                                                 target, *tree, node_tok, step, *out, (char*)workspace, stream);
+    return e == hipSuccess ? TSB_OK : hip_fail(e, "tsb_pool_verify");
+}
+
+tsb_status tsb_pool_step(const tsb_config* cfg, int32_t P, const void* draft, const float* trans, const void* target,
+                         uint32_t step, int32_t* pool_tok, const tsb_tree* tree, int32_t* node_tok,
+                         const tsb_verdict* out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    g_last_error[0] = 0;
+    TRY(check_config(cfg));
+    TRY(check_pool(cfg, P, trans));
+    if (!draft || !target || !pool_tok || !node_tok) return fail(TSB_E_NULL, "tsb_pool_step: a required array is NULL");
+    TRY(check_tree(tree));
+    TRY(check_verdict(out));
+    TRY(check_pool_ws(cfg, P, workspace, workspace_bytes));
+    const float invT = inv_temperature(cfg->temperature);
+    char* ws = (char*)workspace;
+    hipError_t e = tsb::launch_pool_plan(*cfg, P, invT, draft, trans, pool_tok, *tree, nullptr, out->req_status, ws,
+                                         stream);
+    if (e != hipSuccess) return hip_fail(e, "tsb_pool_step/plan");
+    e = tsb::launch_pool_replay(*cfg, P, invT, draft, trans, pool_tok, *tree, step, node_tok, stream);
+    if (e != hipSuccess) return hip_fail(e, "tsb_pool_step/replay");
+    e = tsb::launch_pool_verify(*cfg, P, invT, draft, trans, pool_tok, target, *tree, node_tok, step, *out, ws,
+                                stream);
+    if (e != hipSuccess) return hip_fail(e, "tsb_pool_step/verify");
+    return TSB_OK;
+}
+
 tsb_status tsb_profile_kernel(int32_t kernel_id, hipEvent_t start, hipEvent_t stop) {
     g_last_error[0] = 0;
     tsb::ProfileHook& h = tsb::profile_hook();
@@ -256,6 +350,6 @@ const char* tsb_status_string(tsb_status s) {
 
 const char* tsb_last_error(void) { return g_last_error; }
 
-int32_t tsb_version(void) { return 103; }
+int32_t tsb_version(void) { return 104; }
 
 }  // extern "C"

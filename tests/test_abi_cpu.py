@@ -33,7 +33,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(tsb.EXPORTS)
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.tsb_version() == 103
+    assert lib.tsb_version() == 104
 
 
 def _cfg(**kw):
@@ -153,3 +153,35 @@ def test_plan_ep_validates_frontier_and_size(lib):
                            None) == 1
     assert lib.tsb_plan_ep(ctypes.byref(cfg), 4, FAKE, FAKE, FAKE, FAKE, ctypes.byref(t), FAKE, FAKE, need - 1,
                            None) == 5
+
+
+def test_pool_entry_points_validate(lib):
+    cfg = _cfg()
+    need = lib.tsb_pool_workspace_bytes(ctypes.byref(cfg), 16)
+    assert need >= 256 and need % 256 == 0
+    assert lib.tsb_pool_workspace_bytes(ctypes.byref(cfg), 64) > need
+    # pool size outside [K, min(64, V)]
+    for P in (3, 65, 0):
+        assert lib.tsb_pool_workspace_bytes(ctypes.byref(cfg), P) == 0
+    assert lib.tsb_pool_workspace_bytes(ctypes.byref(_cfg(V=20, K=4)), 21) == 0
+    t = _tree()
+    v = _verdict()
+    for P in (3, 65):
+        assert lib.tsb_pool_plan(ctypes.byref(cfg), P, FAKE, FAKE, FAKE, ctypes.byref(t), None, FAKE, FAKE,
+                                 need, None) == 2
+    # transition table required with D > 1, optional with D = 1
+    assert lib.tsb_pool_plan(ctypes.byref(cfg), 16, FAKE, None, FAKE, ctypes.byref(t), None, FAKE, FAKE, need,
+                             None) == 1
+    assert lib.tsb_pool_replay(ctypes.byref(cfg), 16, FAKE, None, FAKE, ctypes.byref(t), 0, FAKE, None) == 1
+    assert lib.tsb_pool_plan(ctypes.byref(cfg), 16, FAKE, FAKE, None, ctypes.byref(t), None, FAKE, FAKE, need,
+                             None) == 1
+    assert lib.tsb_pool_plan(ctypes.byref(cfg), 16, FAKE, FAKE, FAKE, ctypes.byref(t), None, FAKE, FAKE,
+                             need - 1, None) == 5
+    assert lib.tsb_pool_verify(ctypes.byref(cfg), 16, FAKE, FAKE, FAKE, None, ctypes.byref(t), FAKE, 0,
+                               ctypes.byref(v), FAKE, need, None) == 1
+    assert lib.tsb_pool_verify(ctypes.byref(_cfg(temperature=0.0)), 16, FAKE, FAKE, FAKE, FAKE, ctypes.byref(t),
+                               FAKE, 0, ctypes.byref(v), FAKE, need, None) == 4
+    assert lib.tsb_pool_step(ctypes.byref(cfg), 16, FAKE, FAKE, FAKE, 0, FAKE, ctypes.byref(t), FAKE,
+                             ctypes.byref(v), FAKE, need - 256, None) == 5
+    assert lib.tsb_pool_step(ctypes.byref(_cfg(dtype=5)), 16, FAKE, FAKE, FAKE, 0, FAKE, ctypes.byref(t), FAKE,
+                             ctypes.byref(v), FAKE, need, None) == 3
