@@ -25,6 +25,9 @@ sys.path.insert(0, ROOT)
 import workloads as W  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
+# kernels launched by one replay + RRS round, and by one round over sparse pools
+STEP_KERNELS = ("draft_partials", "plan_tree", "replay_scan", "replay_merge", "target_partials", "verify_walk")
+POOL_KERNELS = ("pool_partials", "pool_lists", "pool_plan", "pool_replay", "target_partials", "pool_walk")
 
 # HBM bytes per launch of target_partials at the batched workload from the
 # FETCH_SIZE / WRITE_SIZE counter passes (KiB, scaled by a plain copy of known
@@ -71,13 +74,17 @@ def _cpu_task(args):
         from oracle import naive as onaive
         out = onaive.first_naive_request(_CPU["draft"][r], _CPU["target"][r], c["T"], c["K"], c["B"], _CPU["seed"],
                                          step, r)
+    elif _CPU["path"] == "pool":
+        from oracle import pool as opool
+        out = opool.step_pool_request(_CPU["draft"][r], _CPU["target"][r], _CPU["trans"][r], c["T"], c["K"],
+                                      _CPU["P"], c["B"], _CPU["seed"], step, r)
     else:
         from oracle import step as ostep
         out = ostep.step_request(_CPU["draft"][r], _CPU["target"][r], c["T"], c["K"], c["B"], _CPU["seed"], step, r)
     return out["n_acc"]
 
 
-def cpu_baseline(cfg, seed, requests, path="replay_rrs"):
+def cpu_baseline(cfg, seed, requests, path="replay_rrs", P=None):
     """Time the oracle over `requests` request-steps of one input set (runs before any GPU use)."""
     import multiprocessing as mp
 
@@ -85,15 +92,21 @@ def cpu_baseline(cfg, seed, requests, path="replay_rrs"):
     from oracle import step as ostep
     base, sigma = W.base_rows(cfg, 0, device="cpu")
     draft = W.draft_from_base(cfg, base)
+    trans = W.transitions(cfg, P, set_idx=0) if path == "pool" else None
     dep = torch.zeros(cfg["R"], cfg["B"] + 1, dtype=torch.int64)
     for r in range(min(requests, cfg["R"])):
-        pl = ostep.plan_request(draft[r].float().numpy(), cfg["T"], cfg["K"], cfg["B"])
-        dep[r, :pl["tree"]["n_nodes"]] = torch.from_numpy(pl["tree"]["depth"])
+        if path == "pool":
+            from oracle import pool as opool
+            tree = pool_plan_cpu(opool, draft[r].float().numpy(), trans[r].numpy(), cfg, P)
+        else:
+            tree = ostep.plan_request(draft[r].float().numpy(), cfg["T"], cfg["K"], cfg["B"])["tree"]
+        dep[r, :tree["n_nodes"]] = torch.from_numpy(tree["depth"])
     target = W.target_from_base(cfg, base, sigma, dep)
     del base
     # plain numpy in the workers: no torch (OpenMP) use after fork
     nr = min(requests, cfg["R"])
-    _CPU.update(cfg=cfg, draft=draft[:nr].float().numpy(), target=target[:nr].float().numpy(), seed=seed, path=path)
+    _CPU.update(cfg=cfg, draft=draft[:nr].float().numpy(), target=target[:nr].float().numpy(), seed=seed, path=path,
+                trans=None if trans is None else trans[:nr].numpy(), P=P)
     del draft, target
     log("cpu baseline: inputs ready")
     tasks = [(r % nr, r // nr) for r in range(requests)]
@@ -104,9 +117,19 @@ def cpu_baseline(cfg, seed, requests, path="replay_rrs"):
         pool.map(_cpu_task, tasks, chunksize=1)
     dt = time.perf_counter() - t0
     _CPU.clear()
+    what = "pools of %d tokens" % P if path == "pool" else path.replace("_", " + ")
     return dict(value=(len(tasks) / cfg["R"]) / dt, unit="steps/s", cores=cores, kind="oracle",
                 sample="%d request-steps (%g steps) of the %s workload, CPU-generated set 0, %s round; wall %.2f s"
-                       % (len(tasks), len(tasks) / cfg["R"], cfg["name"], path.replace("_", " + "), dt))
+                       % (len(tasks), len(tasks) / cfg["R"], cfg["name"], what, dt))
+
+
+def pool_plan_cpu(opool, draft, trans, cfg, P):
+    """The pool oracle's first pass for one request (only its depths key the target rows)."""
+    from oracle.rowstats import inv_temperature
+    invT = inv_temperature(cfg["T"])
+    pl = opool.pools(draft, P)
+    return opool.plan_ctx(opool.pool_logits(draft, invT, pl), opool.scaled_corrections(trans, invT), cfg["K"],
+                          cfg["B"])
 
 
 # ---------------------------------------------------------------- GPU
@@ -191,6 +214,60 @@ def planner_ep(tsb, c, dev, drafts, targets, args, cfg, frontier=10):
             "tau_replay_rrs": round(acc / (P * R), 4)}
 
 
+def pool_block(tsb, c, dev, drafts, args, cfg, P):
+    """The round over sparse pools of P tokens with transition-score corrections: its own targets (keyed by
+    the pool plan's depths), timed rounds, per-kernel times, acceptance."""
+    import torch
+    R = cfg["R"]
+    NS = len(drafts)
+    rnd = tsb.Round(c, dev, pool=P)
+    trans, targets = [], []
+    for p in range(NS):
+        base, sigma = W.base_rows(cfg, p, device=dev)
+        tr = W.transitions(cfg, P, set_idx=p, device=dev)
+        rnd.pool_plan(drafts[p], tr)
+        dep = rnd.tree["depth"].long().clamp(min=0)
+        targets.append(W.target_from_base(cfg, base, sigma, dep, set_idx=p))
+        trans.append(tr)
+        del base
+    torch.cuda.synchronize()
+    for s in range(args.warmup):
+        rnd.pool_step(drafts[s % NS], trans[s % NS], targets[s % NS], s)
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(args.first_steps):
+        s = args.warmup + i
+        rnd.pool_step(drafts[s % NS], trans[s % NS], targets[s % NS], s)
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.first_steps
+    kern_us = {}
+    for name in POOL_KERNELS:
+        kid = tsb.KERNELS.index(name)
+        evs = events(args.breakdown_steps)
+        for i in range(args.breakdown_steps):
+            tsb.profile_kernel(kid, evs[i][0], evs[i][1])
+            rnd.pool_step(drafts[i % NS], trans[i % NS], targets[i % NS], i)
+            tsb.profile_kernel(kid, None)
+        torch.cuda.synchronize()
+        kern_us[name] = round(1000.0 * sum(a.elapsed_time(b) for a, b in evs) / args.breakdown_steps, 2)
+    acc, flagged = 0, 0
+    for i in range(NS):
+        rnd.pool_step(drafts[i], trans[i], targets[i], i)
+        h = rnd.host()
+        acc += int(h["n_acc"].clamp(min=0).sum()) + int((h["n_acc"] >= 0).sum())
+        flagged += int(h["req_status"].ne(0).logical_and(h["n_acc"] < 0).sum())
+    tau = acc / (NS * R)
+    del targets, trans
+    torch.cuda.empty_cache()
+    return {"pool_size": P, "steps_per_s": round(1000.0 / ms, 2), "ms_per_step": round(ms, 4),
+            "steps": args.first_steps, "tau": round(tau, 4), "accepted_tokens_per_s": round(tau * R * 1000.0 / ms, 1),
+            "kernels_us": kern_us, "flagged_requests": flagged,
+            "transitions": "i.i.d. 1.5 * N(0, 1) binary32 scores [R, D-1, P, P]"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -203,6 +280,7 @@ def main():
     ap.add_argument("--breakdown-steps", type=int, default=20)
     ap.add_argument("--sample", type=int, default=8, help="time the target kernel on every n-th timed step")
     ap.add_argument("--first-steps", type=int, default=100, help="timed steps of the First + Naive baseline")
+    ap.add_argument("--pool-size", type=int, default=64, help="tokens per pool in the sparse-pool round (0: skip)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (requests shard with no "
@@ -221,8 +299,10 @@ def main():
         log("cpu baseline:", cpu)
         cpu_first = cpu_baseline(cfg, seed, nreq, path="first_naive")
         log("cpu baseline (first + naive):", cpu_first)
+        cpu_pool = cpu_baseline(cfg, seed, nreq, path="pool", P=args.pool_size) if args.pool_size else None
+        log("cpu baseline (pools):", cpu_pool)
     else:
-        cpu_first = None
+        cpu_first = cpu_pool = None
 
     import torch
     import paper_2609_33652_amd as tsb
@@ -277,9 +357,8 @@ def main():
 
     # untimed passes: per-kernel breakdown and acceptance statistics
     kern_us = {}
-    for kid, name in enumerate(tsb.KERNELS):
-        if name == "verify_naive":
-            continue
+    for name in STEP_KERNELS:
+        kid = tsb.KERNELS.index(name)
         evs = events(args.breakdown_steps)
         for i in range(args.breakdown_steps):
             tsb.profile_kernel(kid, evs[i][0], evs[i][1])
@@ -300,6 +379,12 @@ def main():
     first = first_naive(tsb, c, dev, drafts, targets, args, cfg)
     first["cpu_baseline"] = cpu_first
     ep = planner_ep(tsb, c, dev, drafts, targets, args, cfg)
+    del targets
+    torch.cuda.empty_cache()
+    pool = None
+    if args.pool_size:
+        pool = pool_block(tsb, c, dev, drafts, args, cfg, args.pool_size)
+        pool["cpu_baseline"] = cpu_pool
 
     b = 2 if cfg["dtype"] == "bf16" else 4
     k4_bytes = R * (B + 1) * V * b  # every target row of a full tree, read once
@@ -342,6 +427,7 @@ def main():
         "cpu_baseline": cpu,
         "first_naive": first,
         "planner_expand_prune": ep,
+        "sparse_pools": pool,
     }
     print(json.dumps(out), flush=True)
 

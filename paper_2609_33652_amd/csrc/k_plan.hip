@@ -17,209 +17,537 @@
 namespace tsb {
 
 // ------------------------------------------------------------------ K1a
-// Eight consecutive logits of one row as binary32; positions at or past `hi`
-// read as -inf.
+// Row statistics of the draft: one workgroup of kDraftThreads threads per
+// (draft row, vocabulary segment), one streaming read of the segment. The
+// next chunk's loads are issued before the current chunk is processed and
+// are kept as raw words until then.
+//
+// Normaliser. For bf16 logits at a temperature whose scaled logits stay in
+// range, e^a is looked up per logit instead of evaluated: a = fl32(x invT)
+// depends only on the 16-bit pattern of x, so a binary64 table of e^a over
+// every pattern with 2^-16 <= |x| < 64 (22 binades, both signs) is built in
+// LDS per workgroup and the segment sum is a binary64 sum of table entries
+// (no running maximum: the entries stay within binary64's normal range).
+// Logits outside the table (zero, tiny, large, non-finite) and every logit of
+// binary32 rows take the evaluated path: a running maximum m per lane and a
+// binary64 sum of e^(a - m) by the table-driven exp64. The two parts of a
+// lane (reference 0 and reference m) are combined at the end.
+//
+// Candidates. A group of 8 logits whose maximum passes a filter (x > fx, or
+// x == fx with id <= fid) is only recorded (its offset, in a short per-lane
+// list in LDS); the stream does no other candidate work. When some lane's
+// list is full, and at the end, the wave re-reads the recorded groups, one
+// per lane per round, and appends the logits that pass to its LDS buffer; a
+// buffer that runs full keeps its K best keys and the filter rises to the
+// K-th of them (shared with the other waves of the workgroup through an LDS
+// maximum). The filter starts at the K-th largest of the first chunk's
+// column maxima: K distinct logits at least that large exist, so nothing
+// below it can be among the segment's K best. At the end one wave selects
+// the K best of all buffers.
+constexpr int kDraftThreads = 512;
+constexpr int kDraftWaves = kDraftThreads / kWave;
+constexpr int kDraftU = 4;     // 8-logit groups per thread per chunk
+// candidate buffer entries per wave (the pool selection, with no table in
+// LDS, keeps more: its K reaches 64)
+template <bool STATS>
+constexpr int cand_cap() { return STATS ? 128 : 256; }
+constexpr int kDraftChunk = kDraftThreads * 8 * kDraftU;
+constexpr int kFinalRegs = 8;  // keys per lane in the final selection (512 in all)
+constexpr int kRecSlots = 8;   // recorded groups per lane before the wave flushes
+constexpr int kRecBatch = 4;   // recorded groups re-read at once
+
+// Exponential table over bf16 patterns: biased exponent field in
+// [kTabExpLo, kTabExpLo + kTabBinades), both signs; entry 2 * t + sign for
+// t = (pattern & 0x7FFF) - kTabBase, and a last entry 0.0 that patterns
+// outside the table read.
+constexpr uint32_t kTabExpLo = 111;  // 2^-16
+constexpr int kTabBinades = 22;      // up to 2^6 (exclusive)
+constexpr int kTabHalf = kTabBinades * 128;
+constexpr int kTabEntries = 2 * kTabHalf + 1;
+constexpr uint32_t kTabBase = kTabExpLo << 7;
+
+// Whether the table may be used at this inverse temperature: every entry
+// e^(fl32(x invT)), |x| < 64, is a normal binary64 number (and a sum of up
+// to 2^31 of them stays finite).
+inline bool draft_table_ok(float invT) { return 63.75f * invT < 680.0f; }
+// Segments shorter than this evaluate every exponential (the table would
+// cost more to build than it saves).
+constexpr int kTableMinSeg = 32768;
+
+// Raw words of one 8-logit group: four words of bf16 pairs, or eight binary32.
+template <int DT>
+struct Raw8 {
+    uint32_t w[DT == TSB_BF16 ? 4 : 8];
+};
+
+// Loads one group; positions at or past `hi` read as -inf. Issues the loads
+// only: nothing here waits for them.
 template <int DT, bool VEC>
-__device__ __forceinline__ void load8(const void* __restrict__ draft, size_t rowbase, int i0, int hi, float* x) {
+__device__ __forceinline__ void load_raw8(const void* __restrict__ draft, size_t rowbase, int i0, int hi,
+                                          Raw8<DT>& g) {
     if (VEC && i0 + 8 <= hi) {
         if (DT == TSB_BF16) {
-            const uint4 raw = *(const uint4*)((const uint16_t*)draft + rowbase + i0);
-            const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                x[2 * j] = __uint_as_float(w[j] << 16);
-                x[2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
-            }
+            const uint4 r = load_stream16((const uint16_t*)draft + rowbase + i0);
+            g.w[0] = r.x; g.w[1] = r.y; g.w[2] = r.z; g.w[3] = r.w;
         } else {
-            const float4 f0 = *(const float4*)((const float*)draft + rowbase + i0);
-            const float4 f1 = *(const float4*)((const float*)draft + rowbase + i0 + 4);
-            x[0] = f0.x; x[1] = f0.y; x[2] = f0.z; x[3] = f0.w;
-            x[4] = f1.x; x[5] = f1.y; x[6] = f1.z; x[7] = f1.w;
+            const uint4 r0 = load_stream16((const float*)draft + rowbase + i0);
+            const uint4 r1 = load_stream16((const float*)draft + rowbase + i0 + 4);
+            g.w[0] = r0.x; g.w[1] = r0.y; g.w[2] = r0.z; g.w[3] = r0.w;
+            g.w[4] = r1.x; g.w[5] = r1.y; g.w[6] = r1.z; g.w[7] = r1.w;
         }
     } else {
+        if (DT == TSB_BF16) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) x[j] = (i0 + j < hi) ? load_logit<DT>(draft, rowbase + i0 + j) : -INFINITY;
+            for (int j = 0; j < 4; ++j) {
+                const uint32_t a = (i0 + 2 * j < hi) ? (uint32_t)((const uint16_t*)draft)[rowbase + i0 + 2 * j] : 0xFF80u;
+                const uint32_t b = (i0 + 2 * j + 1 < hi) ? (uint32_t)((const uint16_t*)draft)[rowbase + i0 + 2 * j + 1]
+                                                         : 0xFF80u;
+                g.w[j] = a | (b << 16);
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                g.w[j] = (i0 + j < hi) ? __float_as_uint(((const float*)draft)[rowbase + i0 + j]) : 0xFF800000u;
+        }
     }
 }
 
-constexpr int kDraftUnroll = 1;  // 8-logit groups per thread per chunk
+template <int DT>
+__device__ __forceinline__ void raw8_values(const Raw8<DT>& g, float* x) {
+    if (DT == TSB_BF16) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            x[2 * j] = __uint_as_float(g.w[j] << 16);
+            x[2 * j + 1] = __uint_as_float(g.w[j] & 0xFFFF0000u);
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x[j] = __uint_as_float(g.w[j]);
+    }
+}
+
+// The k-th largest (1 <= k <= 64) of the values held by the 64 lanes (NaN
+// counted as -inf), wave-uniform: a bitonic sort across the lanes.
+__device__ __forceinline__ float wave_kth_largest_sorted(float x, int k) {
+    x = isnan(x) ? -INFINITY : x;
+    const int lane = lane_id();
+#pragma unroll
+    for (int kk = 2; kk <= kWave; kk <<= 1) {
+#pragma unroll
+        for (int j = kk >> 1; j > 0; j >>= 1) {
+            const float o = __shfl_xor(x, j, kWave);
+            const bool keep_max = ((lane & j) == 0) == ((lane & kk) == 0);  // descending overall
+            x = keep_max ? fmaxf(x, o) : fminf(x, o);
+        }
+    }
+    return lane_f32(x, k - 1);
+}
+
+// One step of a wave maximum through DPP: lanes of the rows in ROWMASK take
+// the larger of their key and the key DPP control CTRL moves to them.
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ uint64_t dpp_max_step(uint64_t v) {
+    const int h = (int)(uint32_t)(v >> 32), l = (int)(uint32_t)v;
+    const uint32_t oh = (uint32_t)__builtin_amdgcn_update_dpp(h, h, CTRL, ROWMASK, 0xf, false);
+    const uint32_t ol = (uint32_t)__builtin_amdgcn_update_dpp(l, l, CTRL, ROWMASK, 0xf, false);
+    const uint64_t o = ((uint64_t)oh << 32) | ol;
+    return o > v ? o : v;
+}
+
+// Wave-uniform maximum of a uint64 key: within quads, half rows and rows by
+// DPP permutations, then row broadcasts carry the running maximum to lane 63.
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+    v = dpp_max_step<0xB1, 0xF>(v);   // quad_perm [1, 0, 3, 2]
+    v = dpp_max_step<0x4E, 0xF>(v);   // quad_perm [2, 3, 0, 1]
+    v = dpp_max_step<0x141, 0xF>(v);  // row_half_mirror
+    v = dpp_max_step<0x140, 0xF>(v);  // row_mirror
+    v = dpp_max_step<0x142, 0xA>(v);  // row_bcast:15 into rows 1 and 3
+    v = dpp_max_step<0x143, 0xC>(v);  // row_bcast:31 into rows 2 and 3
+    return lane_u64(v, kWave - 1);
+}
+
+// The K (<= 64) largest of the NR * 64 keys held NR per lane (0 = empty;
+// keys are distinct): lane r receives the r-th largest, lanes >= K and lanes
+// past the number of non-empty keys receive 0. Destroys v.
+template <int NR>
+__device__ uint64_t wave_select_top(uint64_t (&v)[NR], int K) {
+    const int lane = lane_id();
+    uint64_t out = 0;
+    for (int r = 0; r < K; ++r) {
+        uint64_t m = v[0];
+#pragma unroll
+        for (int i = 1; i < NR; ++i) m = v[i] > m ? v[i] : m;
+        const uint64_t w = wave_max_u64(m);
+        if (w == 0) break;
+        if (lane == r) out = w;
+#pragma unroll
+        for (int i = 0; i < NR; ++i)
+            if (v[i] == w) v[i] = 0;
+    }
+    return out;
+}
+
+__device__ __forceinline__ void wave_lds_fence() {
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+}
+
+// Per-wave candidate buffer with its filter.
+template <int CAP>
+struct CandBuf {
+    uint64_t* buf;  // CAP entries in LDS
+    int n;          // entries in use (wave-uniform)
+    float fx;       // filter value
+    uint32_t fid;   // filter id bound for x == fx
+
+    __device__ bool pass(float x, uint32_t id) const { return x > fx || (x == fx && id <= fid); }
+    // Tighten the filter to key k (the K-th best of some set of distinct
+    // logits): entering needs a larger key.
+    __device__ void raise_to(uint64_t k) {
+        const float tx = cand_value(k);
+        const uint32_t ti = cand_id(k);
+        if (tx > fx || (tx == fx && ti <= fid)) {
+            fx = tx;
+            fid = ti - 1;  // wraps for id 0 to "any id": looser, and the keys still order correctly
+        }
+    }
+    // Keep the K best keys at the front; when K keys are kept, raise the
+    // filter to the K-th and publish it to s_key.
+    __device__ void compact(int K, unsigned long long* s_key) {
+        const int lane = lane_id();
+        wave_lds_fence();
+        uint64_t v[CAP / kWave];
+#pragma unroll
+        for (int i = 0; i < CAP / kWave; ++i) {
+            const int j = i * kWave + lane;
+            v[i] = j < n ? buf[j] : 0ull;
+        }
+        const uint64_t t = wave_select_top<CAP / kWave>(v, K);
+        wave_lds_fence();
+        if (lane < K) buf[lane] = t;
+        wave_lds_fence();
+        n = __popcll(__ballot(t != 0ull));
+        if (n == K) {
+            const uint64_t kth = lane_u64(t, K - 1);
+            raise_to(kth);
+            if (lane == 0) atomicMax(s_key, (unsigned long long)kth);
+        }
+    }
+    // Append the logits of one group (lane's x[0..8) with ids i0..i0+7)
+    // that pass, one per lane per round.
+    __device__ void offer8(const float* x, int i0, int hi, bool live, int K, unsigned long long* s_key) {
+        uint32_t mask = 0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+            if (live && i0 + j < hi && pass(x[j], (uint32_t)(i0 + j))) mask |= 1u << j;
+        for (;;) {
+            const uint64_t b = __ballot(mask != 0u);
+            if (!b) break;
+            if (n + kWave > CAP) compact(K, s_key);
+            const int j = mask ? (int)__builtin_ctz(mask) : 0;
+            // x[j] by a select tree on the bits of j (no indexed register access)
+            const bool b0 = j & 1, b1 = j & 2, b2 = j & 4;
+            const float t0 = b0 ? x[1] : x[0], t1 = b0 ? x[3] : x[2];
+            const float t2 = b0 ? x[5] : x[4], t3 = b0 ? x[7] : x[6];
+            const float u0 = b1 ? t1 : t0, u1 = b1 ? t3 : t2;
+            const float xv = b2 ? u1 : u0;
+            const int pos = n + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(b >> 32),
+                                                               __builtin_amdgcn_mbcnt_lo((uint32_t)b, 0u));
+            if (mask) buf[pos] = cand_key(xv, (uint32_t)(i0 + j));
+            n += __popcll(b);
+            mask &= mask - 1u;
+        }
+    }
+};
+
+// Re-reads the groups this wave's lanes recorded (nrec per lane, offsets in
+// s_rec[.][tid]) and offers their logits, one group per lane per round.
+template <int DT, bool VEC, int CAP>
+__device__ void flush_recorded(CandBuf<CAP>& cb, const void* __restrict__ draft, size_t rowbase, int hi, int K,
+                               int (*s_rec)[kDraftThreads], int nrec, unsigned long long* s_key) {
+    const int tid = threadIdx.x;
+    int rounds = nrec;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) rounds = max(rounds, __shfl_xor(rounds, o, kWave));
+    for (int r0 = 0; r0 < rounds; r0 += kRecBatch) {
+        Raw8<DT> g[kRecBatch];
+        int off[kRecBatch];
+#pragma unroll
+        for (int r = 0; r < kRecBatch; ++r) {
+            off[r] = r0 + r < nrec ? s_rec[r0 + r][tid] : 0;
+            if (r0 + r < nrec) load_raw8<DT, VEC>(draft, rowbase, off[r], hi, g[r]);
+        }
+#pragma unroll
+        for (int r = 0; r < kRecBatch; ++r) {
+            if (r0 + r >= rounds) break;
+            float x[8];
+            raw8_values<DT>(g[r], x);
+            cb.offer8(x, off[r], hi, r0 + r < nrec, K, s_key);
+        }
+    }
+}
+
+// The entries of the wave buffers as one flat list (buffer 0's n[0], then
+// buffer 1's, ...), NR per lane: entry r * 64 + lane goes to v[r], 0 past
+// the end.
+template <int NR, int CAP>
+__device__ __forceinline__ void gather_flat(const uint64_t (*buf)[CAP], const int* n, uint64_t (&v)[NR]) {
+    const int lane = lane_id();
+    int w = 0, start = 0;
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+        const int i = r * kWave + lane;
+        while (w < kDraftWaves && i >= start + n[w]) {
+            start += n[w];
+            ++w;
+        }
+        v[r] = w < kDraftWaves ? buf[w][i - start] : 0ull;
+    }
+}
+
+// Evaluated path of the normaliser for one logit (scaled value a): running
+// maximum m and sum of e^(a - m); NaN and +inf set bad, -inf adds nothing.
+__device__ __forceinline__ void eval_term(float a, float& m, double& sum, bool& bad, const double* et) {
+    if (__builtin_amdgcn_classf(a, 0x203)) {  // signalling NaN, quiet NaN, +inf
+        bad = true;
+        return;
+    }
+    if (a == -INFINITY) return;
+    if (a > m) {
+        sum = (m == -INFINITY) ? 1.0 : sum * exp64((double)m - (double)a, et) + 1.0;
+        m = a;
+    } else {
+        sum += exp64((double)a - (double)m, et);
+    }
+}
+
+// Table part of the normaliser for one bf16 pattern (in the low 16 bits of
+// hw, upper bits ignored): adds its entry (0.0 outside the table) and
+// reports whether it is outside.
+__device__ __forceinline__ bool tab_term(uint32_t hw, const double* tab, double& sumF) {
+    const uint32_t t = (hw & 0x7FFFu) - kTabBase;
+    const bool f = t < (uint32_t)kTabHalf;
+    const uint32_t idx = f ? ((t << 1) | ((hw >> 15) & 1u)) : (uint32_t)(kTabEntries - 1);
+    sumF += tab[idx];
+    return !f;
+}
 
 // STATS = false is the pool selection: the same candidate lists (K = pool
 // size) and finiteness flags without the normaliser (pm, ps unused).
 template <int DT, bool VEC, bool STATS>
-__global__ __launch_bounds__(kBlock) void draft_partials(const void* __restrict__ draft, int V, int D,
-                                                         int seg, int S, float invT, int K,
-                                                         float* __restrict__ pm, double* __restrict__ ps,
-                                                         uint64_t* __restrict__ pk, int* __restrict__ pf,
-                                                         int32_t* __restrict__ req_status) {
+__global__ __launch_bounds__(kDraftThreads) void draft_partials(const void* __restrict__ draft, int V, int D,
+                                                                int seg, int S, float invT, int K, int use_table,
+                                                                float* __restrict__ pm, double* __restrict__ ps,
+                                                                uint64_t* __restrict__ pk, int* __restrict__ pf,
+                                                                int32_t* __restrict__ req_status) {
     const int s = blockIdx.x;
     const int row = blockIdx.y;
     const int tid = threadIdx.x;
+    const int wave = tid / kWave, lane = tid % kWave;
     if (s == 0 && (row % D) == 0 && tid == 0) req_status[row / D] = 0;
 
     const size_t rowbase = (size_t)row * (size_t)V;
     const int lo = s * seg;
     const int hi = min(V, lo + seg);
-    constexpr int kChunk = kBlock * 8 * kDraftUnroll;
+    const bool tab = DT == TSB_BF16 && STATS && use_table;
 
-    // the first chunk is in flight while the exp table is built
-    float xc[kDraftUnroll][8];
+    // the first chunk is in flight while the tables are built
+    Raw8<DT> rc[kDraftU];
 #pragma unroll
-    for (int u = 0; u < kDraftUnroll; ++u) load8<DT, VEC>(draft, rowbase, lo + (u * kBlock + tid) * 8, hi, xc[u]);
+    for (int u = 0; u < kDraftU; ++u) load_raw8<DT, VEC>(draft, rowbase, lo + (u * kDraftThreads + tid) * 8, hi, rc[u]);
 
+    constexpr int kTab = (DT == TSB_BF16 && STATS) ? kTabEntries : 1;
+    __shared__ double s_tab[kTab];
     __shared__ double s_exp[kExpTable];
-    if (STATS) exp64_table_init(s_exp);
-
-    float m = -INFINITY;    // running max of the scaled logits (-inf entries never raise it)
-    double sum = 0.0;       // sum of e^(a - m) over this lane's elements
-    bool bad = false;       // a NaN or +inf scaled logit
-    WaveTopList top;
-    top.init(K);
-    // Filter (fx, fid): a logit x with id i can still be among the row's K best
-    // only if x > fx, or x == fx and i <= fid (the key order is logit desc,
-    // id asc). It starts at the K-th largest of the workgroup's column maxima
-    // over its first chunk (K distinct logits at or above it exist) with any
-    // id; then every wave whose list is full publishes its K-th key to s_key
-    // (an LDS maximum) and all waves filter against the best published key.
-
-    const int wave = tid / kWave, lane = tid % kWave;
-    __shared__ float s_lm[kBlock / kWave][kWave];
+    constexpr int CAP = cand_cap<STATS>();
+    __shared__ uint64_t s_buf[kDraftWaves][CAP];
+    __shared__ float s_lm[kDraftWaves][kWave];
     __shared__ unsigned long long s_key;
-    float fx;
-    uint32_t fid = 0xFFFFFFFFu;
+    if (STATS) {
+        for (int j = tid; j < kExpTable; j += kDraftThreads) s_exp[j] = exp2((double)j / (double)kExpTable);
+        __syncthreads();
+        if (tab) {
+            for (int i = tid; i < kTabEntries - 1; i += kDraftThreads) {
+                const uint32_t h = (kTabBase + (uint32_t)(i >> 1)) | ((uint32_t)(i & 1) << 15);
+                s_tab[i] = exp64((double)(__uint_as_float(h << 16) * invT), s_exp);
+            }
+            if (tid == 0) s_tab[kTabEntries - 1] = 0.0;
+        }
+    }
+
+    __shared__ int s_rec[kRecSlots][kDraftThreads];
+    int nrec = 0;  // groups recorded by this lane
+    CandBuf<CAP> cb;
+    cb.buf = s_buf[wave];
+    cb.n = 0;
+    cb.fid = 0xFFFFFFFFu;
     {
         float lm = -INFINITY;
 #pragma unroll
-        for (int u = 0; u < kDraftUnroll; ++u)
+        for (int u = 0; u < kDraftU; ++u) {
+            float x[8];
+            raw8_values<DT>(rc[u], x);
 #pragma unroll
-            for (int j = 0; j < 8; ++j) lm = fmaxf(lm, xc[u][j]);
+            for (int j = 0; j < 8; ++j) lm = fmaxf(lm, x[j]);
+        }
         s_lm[wave][lane] = isnan(lm) ? -INFINITY : lm;
         if (tid == 0) s_key = 0ull;
         __syncthreads();
         float cm = s_lm[0][lane];
 #pragma unroll
-        for (int w = 1; w < kBlock / kWave; ++w) cm = fmaxf(cm, s_lm[w][lane]);
-        fx = wave_kth_largest(cm, K);
+        for (int w = 1; w < kDraftWaves; ++w) cm = fmaxf(cm, s_lm[w][lane]);
+        cb.fx = wave_kth_largest_sorted(cm, K);
     }
-    uint64_t pub = 0;  // the key this wave last published
 
-    for (int base = lo; base < hi; base += kChunk) {
-        const int nbase = base + kChunk;
-        float xn[kDraftUnroll][8];
+    double sumF = 0.0;      // sum of table entries (reference 0)
+    float m = -INFINITY;    // evaluated path: running maximum of the scaled logits
+    double sum = 0.0;       // evaluated path: sum of e^(a - m)
+    bool bad = false;       // a NaN or +inf scaled logit
+
+    for (int base = lo; base < hi; base += kDraftChunk) {
+        const int nbase = base + kDraftChunk;
+        Raw8<DT> rn[kDraftU];
         if (nbase < hi) {
 #pragma unroll
-            for (int u = 0; u < kDraftUnroll; ++u)
-                load8<DT, VEC>(draft, rowbase, nbase + (u * kBlock + tid) * 8, hi, xn[u]);
-        } else {
-#pragma unroll
-            for (int u = 0; u < kDraftUnroll; ++u)
-#pragma unroll
-                for (int j = 0; j < 8; ++j) xn[u][j] = -INFINITY;
+            for (int u = 0; u < kDraftU; ++u)
+                load_raw8<DT, VEC>(draft, rowbase, nbase + (u * kDraftThreads + tid) * 8, hi, rn[u]);
         }
-        // row statistics first, as one straight-line block (the exps of all
-        // groups interleave), then the candidate filter
-        float xm[kDraftUnroll];
-        float a[kDraftUnroll][8];
-        float am = -INFINITY;
 #pragma unroll
-        for (int u = 0; u < kDraftUnroll; ++u) {
-            xm[u] = xc[u][0];
+        for (int u = 0; u < kDraftU; ++u) {
+            const int i0 = base + (u * kDraftThreads + tid) * 8;
+            float x[8];
+            raw8_values<DT>(rc[u], x);
+            if (STATS) {
+                if (tab) {
+                    bool slow = false;
 #pragma unroll
-            for (int j = 1; j < 8; ++j) xm[u] = fmaxf(xm[u], xc[u][j]);  // NaN is ignored
+                    for (int j = 0; j < 4; ++j) {
+                        slow |= tab_term(rc[u].w[j], s_tab, sumF);
+                        slow |= tab_term(rc[u].w[j] >> 16, s_tab, sumF);
+                    }
+                    if (__ballot(slow)) {
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                a[u][j] = xc[u][j] * invT;
-                bad |= __builtin_amdgcn_classf(a[u][j], 0x203);  // signalling NaN, quiet NaN, +inf
+                        for (int j = 0; j < 8; ++j) {
+                            const uint32_t hw = (j & 1) ? (rc[u].w[j >> 1] >> 16) : rc[u].w[j >> 1];
+                            const bool f = ((hw & 0x7FFFu) - kTabBase) < (uint32_t)kTabHalf;
+                            if (__ballot(!f) && !f) eval_term(x[j] * invT, m, sum, bad, s_exp);
+                        }
+                    }
+                } else {
+                    // evaluated path for every logit: rescale once per group
+                    float a[8];
+                    float am = -INFINITY;
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        a[j] = x[j] * invT;
+                        bad |= __builtin_amdgcn_classf(a[j], 0x203);
+                        am = fmaxf(am, a[j]);  // NaN is ignored
+                    }
+                    if (am > m && am < INFINITY) {
+                        sum = (m == -INFINITY) ? 0.0 : sum * exp64((double)m - (double)am, s_exp);
+                        m = am;
+                    }
+                    const double md = (double)m;
+                    double s2[2] = {0.0, 0.0};
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) s2[j & 1] += exp64((double)a[j] - md, s_exp);
+                    sum += s2[0] + s2[1];
+                }
+            } else {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) bad |= __builtin_amdgcn_classf(x[j] * invT, 0x203);
             }
-            am = fmaxf(am, xm[u] * invT);  // rounding is monotone: the scaled max is the max of the scaled
-        }
-        if (STATS && am > m && am < INFINITY) {
-            sum = (m == -INFINITY) ? 0.0 : sum * exp64((double)m - (double)am, s_exp);
-            m = am;
-        }
-        if (STATS) {
-            const double md = (double)m;
-            double s2[2] = {0.0, 0.0};
+            // candidates: record the group if its maximum passes (its
+            // smallest id is i0)
+            float xm = x[0];
 #pragma unroll
-            for (int u = 0; u < kDraftUnroll; ++u)
-#pragma unroll
-                for (int j = 0; j < 8; ++j) s2[j & 1] += exp64((double)a[u][j] - md, s_exp);
-            sum += s2[0] + s2[1];
-        }
-#pragma unroll
-        for (int u = 0; u < kDraftUnroll; ++u) {
-            const int i0 = base + (u * kBlock + tid) * 8;
-            // the group's smallest id is i0
-            if (__ballot(xm[u] > fx || (xm[u] == fx && (uint32_t)i0 <= fid))) {
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const float xj = xc[u][j];
-                    const uint32_t id = (uint32_t)(i0 + j);
-                    const bool ok = (i0 + j < hi) && (xj > fx || (xj == fx && id <= fid));  // false for NaN
-                    top.offer_xid(xj, id, ok);
-                }
-                if (top.thr > pub) {  // publish this wave's K-th key
-                    pub = top.thr;
-                    if (lane == 0) atomicMax(&s_key, (unsigned long long)pub);
-                }
+            for (int j = 1; j < 8; ++j) xm = fmaxf(xm, x[j]);  // NaN is ignored
+            if (cb.pass(xm, (uint32_t)i0)) {
+                s_rec[nrec][tid] = i0;
+                ++nrec;
             }
         }
         {
-            // entering needs a key above the best published K-th key
             const uint64_t sk = *(volatile unsigned long long*)&s_key;
-            if (sk) {
-                const float tx = cand_value(sk);
-                const uint32_t tid1 = cand_id(sk);
-                if (tx > fx || (tx == fx && tid1 <= fid)) {
-                    fx = tx;
-                    fid = tid1 - 1;  // wraps for id 0 to "any id": looser, and offer re-checks the key
-                }
-            }
+            if (sk) cb.raise_to(sk);
+        }
+        if (__ballot(nrec > kRecSlots - kDraftU)) {
+            flush_recorded<DT, VEC, CAP>(cb, draft, rowbase, hi, K, s_rec, nrec, &s_key);
+            nrec = 0;
         }
 #pragma unroll
-        for (int u = 0; u < kDraftUnroll; ++u)
-#pragma unroll
-            for (int j = 0; j < 8; ++j) xc[u][j] = xn[u][j];
+        for (int u = 0; u < kDraftU; ++u) rc[u] = rn[u];
     }
+    flush_recorded<DT, VEC, CAP>(cb, draft, rowbase, hi, K, s_rec, nrec, &s_key);
 
-    // combine lanes and waves in a fixed order
-    __shared__ float s_m[kBlock / kWave];
-    __shared__ double s_s[kBlock / kWave];
-    __shared__ int s_bad[kBlock / kWave];
-    __shared__ uint64_t s_top[kBlock / kWave][kWave];
-    const float wm = wave_max(m);
-    double contrib = (m == -INFINITY) ? 0.0 : sum * exp((double)m - (double)wm);
+    __shared__ int s_n[kDraftWaves];
+    __shared__ float s_m[kDraftWaves];
+    __shared__ double s_s[kDraftWaves];
+    __shared__ int s_bad[kDraftWaves];
+    // lane partial: reference M (0 for the table part) and the sum relative
+    // to it; exponentials only where references differ
+    const bool anyF = sumF > 0.0;  // table entries are positive
+    float Ml;
+    double sl;
+    if (m == -INFINITY) {
+        Ml = anyF ? 0.0f : -INFINITY;
+        sl = sumF;
+    } else {
+        Ml = anyF ? fmaxf(0.0f, m) : m;
+        sl = (anyF ? (Ml == 0.0f ? sumF : sumF * exp(-(double)Ml)) : 0.0) +
+             (m == Ml ? sum : sum * exp((double)m - (double)Ml));
+    }
+    const float wm = wave_max(Ml);
+    const double contrib = (Ml == -INFINITY) ? 0.0 : (Ml == wm ? sl : sl * exp((double)Ml - (double)wm));
     const double ws = STATS ? wave_sum(contrib) : 0.0;
     const int wb = wave_or(bad);
     if (lane == 0) {
+        s_n[wave] = cb.n;
         s_m[wave] = wm;
         s_s[wave] = ws;
         s_bad[wave] = wb;
     }
-    s_top[wave][lane] = top.v;
     __syncthreads();
+    // the K best over all buffers: by one wave when they fit its registers,
+    // else after every wave has kept its own K best
+    int total = 0;
+#pragma unroll
+    for (int w = 0; w < kDraftWaves; ++w) total += s_n[w];
+    if (total > kFinalRegs * kWave) {
+        cb.compact(K, &s_key);
+        if (lane == 0) s_n[wave] = cb.n;
+        __syncthreads();
+        total = 0;
+#pragma unroll
+        for (int w = 0; w < kDraftWaves; ++w) total += s_n[w];
+    }
     if (wave == 0) {
-        for (int w = 1; w < kBlock / kWave; ++w) {
-            const uint64_t k = s_top[w][lane];
-            top.offer(k, lane < K && k != 0);
+        uint64_t best;
+        if (total <= 2 * kWave) {
+            uint64_t v[2];
+            gather_flat<2, CAP>(s_buf, s_n, v);
+            best = wave_select_top<2>(v, K);
+        } else {
+            uint64_t v[kFinalRegs];
+            gather_flat<kFinalRegs, CAP>(s_buf, s_n, v);
+            best = wave_select_top<kFinalRegs>(v, K);
         }
+        // segment normaliser: lanes w < kDraftWaves hold wave w's partial
+        const float mw = lane < kDraftWaves ? s_m[lane] : -INFINITY;
+        const float M = wave_max(mw);
+        const double sw = lane < kDraftWaves && mw != -INFINITY
+                              ? (mw == M ? s_s[lane] : s_s[lane] * exp((double)mw - (double)M)) : 0.0;
+        const double tot = STATS ? wave_sum(sw) : 0.0;
+        const int anybad = wave_or(lane < kDraftWaves ? s_bad[lane] : 0);
+        const size_t o = (size_t)row * S + s;
         if (lane == 0) {
-            float M = s_m[0];
-            for (int w = 1; w < kBlock / kWave; ++w) M = fmaxf(M, s_m[w]);
-            double tot = 0.0;
-            int anybad = 0;
-            for (int w = 0; w < kBlock / kWave; ++w) {
-                if (s_m[w] != -INFINITY) tot += s_s[w] * exp((double)s_m[w] - (double)M);
-                anybad |= s_bad[w];
-            }
-            const size_t o = (size_t)row * S + s;
             if (STATS) {
                 pm[o] = M;
                 ps[o] = tot;
             }
             pf[o] = anybad;
         }
-        if (lane < K) pk[((size_t)row * S + s) * K + lane] = top.v;
+        if (lane < K) pk[o * K + lane] = best;
     }
 }
 
@@ -923,6 +1251,32 @@ __global__ __launch_bounds__(kPlanThreads) void plan_ep(int D, int S, int K, int
 }
 
 // ------------------------------------------------------------------ launch
+template <bool STATS>
+hipError_t launch_draft_partials(const tsb_config& c, int K, float invT, const void* draft, float* pm, double* ps,
+                                 uint64_t* pk, int* pf, int32_t* req_status, hipStream_t st) {
+    const Geometry g = geometry(c);
+    const dim3 grid1(g.S1, c.R * c.D);
+    const bool vec = (c.dtype == TSB_BF16) ? (c.V % 8 == 0 && ((uintptr_t)draft & 15) == 0)
+                                           : (c.V % 4 == 0 && ((uintptr_t)draft & 15) == 0);
+    const int tab = (c.dtype == TSB_BF16 && draft_table_ok(invT) && g.seg1 >= kTableMinSeg) ? 1 : 0;
+    if (c.dtype == TSB_BF16) {
+        if (vec)
+            draft_partials<TSB_BF16, true, STATS><<<grid1, kDraftThreads, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT,
+                                                                                  K, tab, pm, ps, pk, pf, req_status);
+        else
+            draft_partials<TSB_BF16, false, STATS><<<grid1, kDraftThreads, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT,
+                                                                                   K, tab, pm, ps, pk, pf, req_status);
+    } else {
+        if (vec)
+            draft_partials<TSB_F32, true, STATS><<<grid1, kDraftThreads, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT,
+                                                                                 K, 0, pm, ps, pk, pf, req_status);
+        else
+            draft_partials<TSB_F32, false, STATS><<<grid1, kDraftThreads, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT,
+                                                                                  K, 0, pm, ps, pk, pf, req_status);
+    }
+    return hipGetLastError();
+}
+
 hipError_t launch_plan(const tsb_config& c, float invT, const void* draft, double* draft_lse, int32_t* topk_tok,
                        float* topk_lp, const tsb_tree& tree, int32_t* req_status, char* ws, hipStream_t st,
                        int frontier) {
@@ -932,28 +1286,9 @@ hipError_t launch_plan(const tsb_config& c, float invT, const void* draft, doubl
     double* ps = (double*)(ws + w.ps);
     uint64_t* pk = (uint64_t*)(ws + w.pk);
     int* pf = (int*)(ws + w.pf);
-    const dim3 grid1(g.S1, c.R * c.D);
     hipError_t e = hook_before(TSB_KERNEL_DRAFT_PARTIALS, st);
     if (e != hipSuccess) return e;
-    const bool vec = (c.dtype == TSB_BF16) ? (c.V % 8 == 0 && ((uintptr_t)draft & 15) == 0)
-                                           : (c.V % 4 == 0 && ((uintptr_t)draft & 15) == 0);
-    if (c.dtype == TSB_BF16) {
-        if (vec)
-            draft_partials<TSB_BF16, true, true><<<grid1, kBlock, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT, c.K, pm, ps,
-                                                                     pk, pf, req_status);
-        else
-            draft_partials<TSB_BF16, false, true><<<grid1, kBlock, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT, c.K, pm, ps,
-                                                                      pk, pf, req_status);
-    } else {
-        if (vec)
-            draft_partials<TSB_F32, true, true><<<grid1, kBlock, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT, c.K, pm, ps,
-                                                                    pk, pf, req_status);
-        else
-            draft_partials<TSB_F32, false, true><<<grid1, kBlock, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT, c.K, pm, ps,
-                                                                     pk, pf, req_status);
-    }
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    if ((e = launch_draft_partials<true>(c, c.K, invT, draft, pm, ps, pk, pf, req_status, st)) != hipSuccess) return e;
     if ((e = hook_after(TSB_KERNEL_DRAFT_PARTIALS, st)) != hipSuccess) return e;
     if ((e = hook_before(TSB_KERNEL_PLAN_TREE, st)) != hipSuccess) return e;
     if (frontier > 0)
@@ -969,29 +1304,10 @@ hipError_t launch_plan(const tsb_config& c, float invT, const void* draft, doubl
 
 hipError_t launch_pool_partials(const tsb_config& c, int P, float invT, const void* draft, uint64_t* pk, int* pf,
                                 int32_t* req_status, hipStream_t st) {
-    const Geometry g = geometry(c);
-    const dim3 grid1(g.S1, c.R * c.D);
     hipError_t e = hook_before(TSB_KERNEL_POOL_PARTIALS, st);
     if (e != hipSuccess) return e;
-    const bool vec = (c.dtype == TSB_BF16) ? (c.V % 8 == 0 && ((uintptr_t)draft & 15) == 0)
-                                           : (c.V % 4 == 0 && ((uintptr_t)draft & 15) == 0);
-    if (c.dtype == TSB_BF16) {
-        if (vec)
-            draft_partials<TSB_BF16, true, false><<<grid1, kBlock, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT, P,
-                                                                            nullptr, nullptr, pk, pf, req_status);
-        else
-            draft_partials<TSB_BF16, false, false><<<grid1, kBlock, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT, P,
-                                                                             nullptr, nullptr, pk, pf, req_status);
-    } else {
-        if (vec)
-            draft_partials<TSB_F32, true, false><<<grid1, kBlock, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT, P,
-                                                                           nullptr, nullptr, pk, pf, req_status);
-        else
-            draft_partials<TSB_F32, false, false><<<grid1, kBlock, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT, P,
-                                                                            nullptr, nullptr, pk, pf, req_status);
-    }
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    if ((e = launch_draft_partials<false>(c, P, invT, draft, nullptr, nullptr, pk, pf, req_status, st)) != hipSuccess)
+        return e;
     return hook_after(TSB_KERNEL_POOL_PARTIALS, st);
 }
 

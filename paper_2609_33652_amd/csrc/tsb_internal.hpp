@@ -17,7 +17,8 @@ constexpr int kReplayTile = 4096;    // vocabulary tile of the replay scan
 constexpr int kWalkGroupsMax = 128;  // workgroups per request in verification
 constexpr int kWalkTokensPerGroup = 9728;  // tokens whose binary64 (p, q) one walk workgroup holds in LDS
 constexpr int kTargetWorkgroups = 2048;  // target stream: 8 resident workgroups on each of 256 CUs
-constexpr int kDraftWorkgroups = 1024;   // row statistics: one resident wave of workgroups
+constexpr int kDraftWorkgroups = 512;    // row statistics: two 512-thread workgroups on each of 256 CUs
+constexpr int kDraftMinSeg = 16384;      // shortest draft segment (elements), unless the row is shorter
 
 struct Geometry {
     int S1;          // workgroups per draft row (row statistics)
@@ -35,7 +36,7 @@ inline Geometry geometry(const tsb_config& c) {
     Geometry g;
     const long long drows = (long long)c.R * c.D;
     int s1 = ceil_div(kDraftWorkgroups, drows);
-    int s1max = ceil_div(c.V, 2048);
+    int s1max = ceil_div(c.V, kDraftMinSeg);
     g.S1 = s1 < 1 ? 1 : (s1 > s1max ? s1max : s1);
     g.seg1 = ceil_div(ceil_div(c.V, g.S1), 8) * 8;
     g.S1 = ceil_div(c.V, g.seg1);
