@@ -19,8 +19,8 @@ namespace tsb {
 // ------------------------------------------------------------------ K1a
 // Row statistics of the draft: one workgroup of kDraftThreads threads per
 // (draft row, vocabulary segment), one streaming read of the segment. The
-// next chunk's loads are issued before the current chunk is processed and
-// are kept as raw words until then.
+// next chunk's loads are issued before the current chunk is processed, and
+// chunks stay raw words until then.
 //
 // Normaliser. For bf16 logits at a temperature whose scaled logits stay in
 // range, e^a is looked up per logit instead of evaluated: a = fl32(x invT)
@@ -57,13 +57,13 @@ constexpr int kRecSlots = 8;   // recorded groups per lane before the wave flush
 constexpr int kRecBatch = 4;   // recorded groups re-read at once
 
 // Exponential table over bf16 patterns: biased exponent field in
-// [kTabExpLo, kTabExpLo + kTabBinades), both signs; entry 2 * t + sign for
-// t = (pattern & 0x7FFF) - kTabBase, and a last entry 0.0 that patterns
-// outside the table read.
+// [kTabExpLo, kTabExpLo + kTabBinades), both signs; entry 2 t + sign for
+// t = (pattern & 0x7FFF) - kTabBase, and two last entries 0.0 that patterns
+// outside the table read (t clamped to kTabHalf).
 constexpr uint32_t kTabExpLo = 111;  // 2^-16
 constexpr int kTabBinades = 22;      // up to 2^6 (exclusive)
 constexpr int kTabHalf = kTabBinades * 128;
-constexpr int kTabEntries = 2 * kTabHalf + 1;
+constexpr int kTabEntries = 2 * kTabHalf + 2;
 constexpr uint32_t kTabBase = kTabExpLo << 7;
 
 // Whether the table may be used at this inverse temperature: every entry
@@ -110,6 +110,34 @@ __device__ __forceinline__ void load_raw8(const void* __restrict__ draft, size_t
                 g.w[j] = (i0 + j < hi) ? __float_as_uint(((const float*)draft)[rowbase + i0 + j]) : 0xFF800000u;
         }
     }
+}
+
+// A chunk (kDraftU groups per thread) that lies inside the segment: vector
+// loads with no bounds test.
+template <int DT>
+__device__ __forceinline__ void load_chunk(const void* __restrict__ draft, size_t rowbase, int base, int tid,
+                                           Raw8<DT> (&r)[kDraftU]) {
+#pragma unroll
+    for (int u = 0; u < kDraftU; ++u) {
+        const size_t i0 = rowbase + (size_t)(base + (u * kDraftThreads + tid) * 8);
+        if (DT == TSB_BF16) {
+            const uint4 v = load_stream16((const uint16_t*)draft + i0);
+            r[u].w[0] = v.x; r[u].w[1] = v.y; r[u].w[2] = v.z; r[u].w[3] = v.w;
+        } else {
+            const uint4 v0 = load_stream16((const float*)draft + i0);
+            const uint4 v1 = load_stream16((const float*)draft + i0 + 4);
+            r[u].w[0] = v0.x; r[u].w[1] = v0.y; r[u].w[2] = v0.z; r[u].w[3] = v0.w;
+            r[u].w[4] = v1.x; r[u].w[5] = v1.y; r[u].w[6] = v1.z; r[u].w[7] = v1.w;
+        }
+    }
+}
+
+// A chunk that may reach past `hi` (positions there read as -inf).
+template <int DT, bool VEC>
+__device__ __forceinline__ void load_chunk_masked(const void* __restrict__ draft, size_t rowbase, int base, int hi,
+                                                  int tid, Raw8<DT> (&r)[kDraftU]) {
+#pragma unroll
+    for (int u = 0; u < kDraftU; ++u) load_raw8<DT, VEC>(draft, rowbase, base + (u * kDraftThreads + tid) * 8, hi, r[u]);
 }
 
 template <int DT>
@@ -170,7 +198,7 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
 // keys are distinct): lane r receives the r-th largest, lanes >= K and lanes
 // past the number of non-empty keys receive 0. Destroys v.
 template <int NR>
-__device__ uint64_t wave_select_top(uint64_t (&v)[NR], int K) {
+__device__ __forceinline__ uint64_t wave_select_top(uint64_t (&v)[NR], int K) {
     const int lane = lane_id();
     uint64_t out = 0;
     for (int r = 0; r < K; ++r) {
@@ -213,7 +241,7 @@ struct CandBuf {
     }
     // Keep the K best keys at the front; when K keys are kept, raise the
     // filter to the K-th and publish it to s_key.
-    __device__ void compact(int K, unsigned long long* s_key) {
+    __device__ __forceinline__ void compact(int K, unsigned long long* s_key) {
         const int lane = lane_id();
         wave_lds_fence();
         uint64_t v[CAP / kWave];
@@ -235,7 +263,7 @@ struct CandBuf {
     }
     // Append the logits of one group (lane's x[0..8) with ids i0..i0+7)
     // that pass, one per lane per round.
-    __device__ void offer8(const float* x, int i0, int hi, bool live, int K, unsigned long long* s_key) {
+    __device__ __forceinline__ void offer8(const float* x, int i0, int hi, bool live, int K, unsigned long long* s_key) {
         uint32_t mask = 0;
 #pragma unroll
         for (int j = 0; j < 8; ++j)
@@ -263,7 +291,7 @@ struct CandBuf {
 // Re-reads the groups this wave's lanes recorded (nrec per lane, offsets in
 // s_rec[.][tid]) and offers their logits, one group per lane per round.
 template <int DT, bool VEC, int CAP>
-__device__ void flush_recorded(CandBuf<CAP>& cb, const void* __restrict__ draft, size_t rowbase, int hi, int K,
+__device__ __forceinline__ void flush_recorded(CandBuf<CAP>& cb, const void* __restrict__ draft, size_t rowbase, int hi, int K,
                                int (*s_rec)[kDraftThreads], int nrec, unsigned long long* s_key) {
     const int tid = threadIdx.x;
     int rounds = nrec;
@@ -321,15 +349,110 @@ __device__ __forceinline__ void eval_term(float a, float& m, double& sum, bool& 
     }
 }
 
-// Table part of the normaliser for one bf16 pattern (in the low 16 bits of
-// hw, upper bits ignored): adds its entry (0.0 outside the table) and
-// reports whether it is outside.
-__device__ __forceinline__ bool tab_term(uint32_t hw, const double* tab, double& sumF) {
-    const uint32_t t = (hw & 0x7FFFu) - kTabBase;
-    const bool f = t < (uint32_t)kTabHalf;
-    const uint32_t idx = f ? ((t << 1) | ((hw >> 15) & 1u)) : (uint32_t)(kTabEntries - 1);
-    sumF += tab[idx];
-    return !f;
+// Table part of the normaliser for the two bf16 patterns of a word, with
+// packed 16-bit arithmetic: adds their entries (0.0 outside the table) and
+// reports whether either is outside. The byte offset of an entry is
+// 16 t + 8 sign, below 2^16.
+typedef unsigned short tsb_u16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ bool tab_pair(uint32_t w, const double* tab, double& sumF) {
+    const tsb_u16x2 base = {(unsigned short)kTabBase, (unsigned short)kTabBase};
+    const tsb_u16x2 lim = {(unsigned short)kTabHalf, (unsigned short)kTabHalf};
+    const tsb_u16x2 t = __builtin_bit_cast(tsb_u16x2, w & 0x7FFF7FFFu) - base;  // wraps below the table
+    const tsb_u16x2 tc = __builtin_elementwise_min(t, lim);
+    const tsb_u16x2 a = tc << (tsb_u16x2){4, 4};
+    const uint32_t off = __builtin_bit_cast(uint32_t, a) | ((w >> 12) & 0x00080008u);
+    sumF += *(const double*)((const char*)tab + (off & 0xFFFFu));
+    sumF += *(const double*)((const char*)tab + (off >> 16));
+    return __builtin_bit_cast(uint32_t, tc) != __builtin_bit_cast(uint32_t, t);
+}
+
+// Per-workgroup-lane state of the draft stream: candidate buffer, recorded
+// groups, normaliser parts and the LDS tables.
+template <int CAP>
+struct DraftState {
+    CandBuf<CAP>& cb;
+    const void* draft;
+    size_t rowbase;
+    int hi, K;
+    float invT;
+    bool use_tab;
+    const double* tab_lds;
+    const double* exp_lds;
+    int (*rec)[kDraftThreads];
+    unsigned long long* key;
+    int nrec = 0;           // groups recorded by this lane
+    double sumF = 0.0;      // sum of table entries (reference 0)
+    float m = -INFINITY;    // evaluated path: running maximum of the scaled logits
+    double sum = 0.0;       // evaluated path: sum of e^(a - m)
+    bool bad = false;       // a NaN or +inf scaled logit
+};
+
+// One chunk held in r, starting at base: normaliser terms, finiteness and
+// the recording of candidate groups.
+template <int DT, bool VEC, bool STATS, int CAP>
+__device__ __forceinline__ void draft_chunk(const Raw8<DT> (&r)[kDraftU], int base, DraftState<CAP>& St) {
+#pragma unroll
+    for (int u = 0; u < kDraftU; ++u) {
+        const int i0 = base + (u * kDraftThreads + (int)threadIdx.x) * 8;
+        float x[8];
+        raw8_values<DT>(r[u], x);
+        if (STATS) {
+            if (St.use_tab) {
+                bool slow = false;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) slow |= tab_pair(r[u].w[j], St.tab_lds, St.sumF);
+                if (__ballot(slow)) {
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        const uint32_t hw = (j & 1) ? (r[u].w[j >> 1] >> 16) : r[u].w[j >> 1];
+                        const bool f = ((hw & 0x7FFFu) - kTabBase) < (uint32_t)kTabHalf;
+                        if (__ballot(!f) && !f) eval_term(x[j] * St.invT, St.m, St.sum, St.bad, St.exp_lds);
+                    }
+                }
+            } else {
+                // evaluated path for every logit: rescale once per group
+                float a[8];
+                float am = -INFINITY;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    a[j] = x[j] * St.invT;
+                    St.bad |= __builtin_amdgcn_classf(a[j], 0x203);
+                    am = fmaxf(am, a[j]);  // NaN is ignored
+                }
+                if (am > St.m && am < INFINITY) {
+                    St.sum = (St.m == -INFINITY) ? 0.0 : St.sum * exp64((double)St.m - (double)am, St.exp_lds);
+                    St.m = am;
+                }
+                const double md = (double)St.m;
+                double s2[2] = {0.0, 0.0};
+#pragma unroll
+                for (int j = 0; j < 8; ++j) s2[j & 1] += exp64((double)a[j] - md, St.exp_lds);
+                St.sum += s2[0] + s2[1];
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) St.bad |= __builtin_amdgcn_classf(x[j] * St.invT, 0x203);
+        }
+        // candidates: record the group if its maximum passes (its
+        // smallest id is i0)
+        float xm = x[0];
+#pragma unroll
+        for (int j = 1; j < 8; ++j) xm = fmaxf(xm, x[j]);  // NaN is ignored
+        if (St.cb.pass(xm, (uint32_t)i0)) {
+            St.rec[St.nrec][threadIdx.x] = i0;
+            ++St.nrec;
+        }
+    }
+    {
+        // an LDS load (a generic volatile load would also wait for the
+        // chunks in flight)
+        const uint64_t sk = __hip_atomic_load(St.key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        if (sk) St.cb.raise_to(sk);
+    }
+    if (__ballot(St.nrec > kRecSlots - kDraftU)) {
+        flush_recorded<DT, VEC, CAP>(St.cb, St.draft, St.rowbase, St.hi, St.K, St.rec, St.nrec, St.key);
+        St.nrec = 0;
+    }
 }
 
 // STATS = false is the pool selection: the same candidate lists (K = pool
@@ -351,10 +474,15 @@ __global__ __launch_bounds__(kDraftThreads) void draft_partials(const void* __re
     const int hi = min(V, lo + seg);
     const bool tab = DT == TSB_BF16 && STATS && use_table;
 
-    // the first chunk is in flight while the tables are built
-    Raw8<DT> rc[kDraftU];
-#pragma unroll
-    for (int u = 0; u < kDraftU; ++u) load_raw8<DT, VEC>(draft, rowbase, lo + (u * kDraftThreads + tid) * 8, hi, rc[u]);
+    // a chunk that lies wholly inside the segment is read with unconditional
+    // vector loads (a wave-uniform choice), a last partial chunk with
+    // per-position bounds
+    const bool full0 = VEC && lo + kDraftChunk <= hi;
+    Raw8<DT> rA[kDraftU];
+    if (full0)
+        load_chunk<DT>(draft, rowbase, lo, tid, rA);
+    else
+        load_chunk_masked<DT, VEC>(draft, rowbase, lo, hi, tid, rA);
 
     constexpr int kTab = (DT == TSB_BF16 && STATS) ? kTabEntries : 1;
     __shared__ double s_tab[kTab];
@@ -367,16 +495,15 @@ __global__ __launch_bounds__(kDraftThreads) void draft_partials(const void* __re
         for (int j = tid; j < kExpTable; j += kDraftThreads) s_exp[j] = exp2((double)j / (double)kExpTable);
         __syncthreads();
         if (tab) {
-            for (int i = tid; i < kTabEntries - 1; i += kDraftThreads) {
+            for (int i = tid; i < kTabEntries - 2; i += kDraftThreads) {
                 const uint32_t h = (kTabBase + (uint32_t)(i >> 1)) | ((uint32_t)(i & 1) << 15);
                 s_tab[i] = exp64((double)(__uint_as_float(h << 16) * invT), s_exp);
             }
-            if (tid == 0) s_tab[kTabEntries - 1] = 0.0;
+            if (tid < 2) s_tab[kTabEntries - 2 + tid] = 0.0;
         }
     }
 
     __shared__ int s_rec[kRecSlots][kDraftThreads];
-    int nrec = 0;  // groups recorded by this lane
     CandBuf<CAP> cb;
     cb.buf = s_buf[wave];
     cb.n = 0;
@@ -386,7 +513,7 @@ __global__ __launch_bounds__(kDraftThreads) void draft_partials(const void* __re
 #pragma unroll
         for (int u = 0; u < kDraftU; ++u) {
             float x[8];
-            raw8_values<DT>(rc[u], x);
+            raw8_values<DT>(rA[u], x);
 #pragma unroll
             for (int j = 0; j < 8; ++j) lm = fmaxf(lm, x[j]);
         }
@@ -399,86 +526,26 @@ __global__ __launch_bounds__(kDraftThreads) void draft_partials(const void* __re
         cb.fx = wave_kth_largest_sorted(cm, K);
     }
 
-    double sumF = 0.0;      // sum of table entries (reference 0)
-    float m = -INFINITY;    // evaluated path: running maximum of the scaled logits
-    double sum = 0.0;       // evaluated path: sum of e^(a - m)
-    bool bad = false;       // a NaN or +inf scaled logit
+    DraftState<CAP> St{cb, draft, rowbase, hi, K, invT, tab, s_tab, s_exp, s_rec, &s_key};
+
 
     for (int base = lo; base < hi; base += kDraftChunk) {
-        const int nbase = base + kDraftChunk;
-        Raw8<DT> rn[kDraftU];
-        if (nbase < hi) {
+        // the next chunk's loads are issued before this one is processed
+        const int nb = base + kDraftChunk;
+        Raw8<DT> rB[kDraftU];
+        if (VEC && nb + kDraftChunk <= hi)
+            load_chunk<DT>(draft, rowbase, nb, tid, rB);
+        else if (nb < hi)
+            load_chunk_masked<DT, VEC>(draft, rowbase, nb, hi, tid, rB);
+        draft_chunk<DT, VEC, STATS, CAP>(rA, base, St);
 #pragma unroll
-            for (int u = 0; u < kDraftU; ++u)
-                load_raw8<DT, VEC>(draft, rowbase, nbase + (u * kDraftThreads + tid) * 8, hi, rn[u]);
-        }
-#pragma unroll
-        for (int u = 0; u < kDraftU; ++u) {
-            const int i0 = base + (u * kDraftThreads + tid) * 8;
-            float x[8];
-            raw8_values<DT>(rc[u], x);
-            if (STATS) {
-                if (tab) {
-                    bool slow = false;
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        slow |= tab_term(rc[u].w[j], s_tab, sumF);
-                        slow |= tab_term(rc[u].w[j] >> 16, s_tab, sumF);
-                    }
-                    if (__ballot(slow)) {
-#pragma unroll
-                        for (int j = 0; j < 8; ++j) {
-                            const uint32_t hw = (j & 1) ? (rc[u].w[j >> 1] >> 16) : rc[u].w[j >> 1];
-                            const bool f = ((hw & 0x7FFFu) - kTabBase) < (uint32_t)kTabHalf;
-                            if (__ballot(!f) && !f) eval_term(x[j] * invT, m, sum, bad, s_exp);
-                        }
-                    }
-                } else {
-                    // evaluated path for every logit: rescale once per group
-                    float a[8];
-                    float am = -INFINITY;
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        a[j] = x[j] * invT;
-                        bad |= __builtin_amdgcn_classf(a[j], 0x203);
-                        am = fmaxf(am, a[j]);  // NaN is ignored
-                    }
-                    if (am > m && am < INFINITY) {
-                        sum = (m == -INFINITY) ? 0.0 : sum * exp64((double)m - (double)am, s_exp);
-                        m = am;
-                    }
-                    const double md = (double)m;
-                    double s2[2] = {0.0, 0.0};
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) s2[j & 1] += exp64((double)a[j] - md, s_exp);
-                    sum += s2[0] + s2[1];
-                }
-            } else {
-#pragma unroll
-                for (int j = 0; j < 8; ++j) bad |= __builtin_amdgcn_classf(x[j] * invT, 0x203);
-            }
-            // candidates: record the group if its maximum passes (its
-            // smallest id is i0)
-            float xm = x[0];
-#pragma unroll
-            for (int j = 1; j < 8; ++j) xm = fmaxf(xm, x[j]);  // NaN is ignored
-            if (cb.pass(xm, (uint32_t)i0)) {
-                s_rec[nrec][tid] = i0;
-                ++nrec;
-            }
-        }
-        {
-            const uint64_t sk = *(volatile unsigned long long*)&s_key;
-            if (sk) cb.raise_to(sk);
-        }
-        if (__ballot(nrec > kRecSlots - kDraftU)) {
-            flush_recorded<DT, VEC, CAP>(cb, draft, rowbase, hi, K, s_rec, nrec, &s_key);
-            nrec = 0;
-        }
-#pragma unroll
-        for (int u = 0; u < kDraftU; ++u) rc[u] = rn[u];
+        for (int u = 0; u < kDraftU; ++u) rA[u] = rB[u];
     }
-    flush_recorded<DT, VEC, CAP>(cb, draft, rowbase, hi, K, s_rec, nrec, &s_key);
+    flush_recorded<DT, VEC, CAP>(St.cb, draft, rowbase, hi, K, s_rec, St.nrec, &s_key);
+    const double sumF = St.sumF;
+    const float m = St.m;
+    const double sum = St.sum;
+    const bool bad = St.bad;
 
     __shared__ int s_n[kDraftWaves];
     __shared__ float s_m[kDraftWaves];
