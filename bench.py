@@ -32,7 +32,7 @@ POOL_KERNELS = ("pool_partials", "pool_lists", "pool_plan", "pool_replay", "targ
 # HBM bytes per launch of target_partials at the batched workload from the
 # FETCH_SIZE / WRITE_SIZE counter passes (KiB, scaled by a plain copy of known
 # size: FETCH x2.0, WRITE x1.0), valid for the kernel source they were taken on
-TARGET_TRAFFIC = {"config": 4, "source_sha256_16": "d1240d8a06bfe313", "fetch_kib": 309788.3, "write_kib": 268.0,
+TARGET_TRAFFIC = {"config": 4, "source_sha256_16": "d1240d8a06bfe313", "fetch_kib": 309815.6, "write_kib": 266.6,
                   "fetch_scale": 2.0, "write_scale": 1.0}
 
 
@@ -416,7 +416,7 @@ def main():
                      "timed_launches": len(ev)},
         "kernels_us": kern_us,
         # the other logit-streaming kernel, from the untimed per-kernel pass
-        "roofline_draft": {"kernel": "draft_partials", "bound": "hbm (binary64 exp per logit makes it VALU-bound)",
+        "roofline_draft": {"kernel": "draft_partials", "bound": "hbm (VALU-bound: a table lookup and a binary64 add per logit)",
                            "achieved": round(k1_bytes / (kern_us["draft_partials"] * 1e-6) / 1e9, 1),
                            "peak": HBM_PEAK_GBS, "unit": "GB/s",
                            "frac": round(k1_bytes / (kern_us["draft_partials"] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
