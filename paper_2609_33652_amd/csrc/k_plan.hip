@@ -752,44 +752,41 @@ __device__ void merge_row(SH& sh, int row, int rrow, int S, int K, float invT, c
 
 // Number of nodes (root excluded) scoring at least tau, level by level, with
 // their scores stored in buf; cap + 1 once more than cap. m_out: the largest
-// node score below tau (-inf if none; meaningful without overflow).
+// node score below tau (-inf if none; meaningful without overflow). Lane l
+// takes candidate l % K of parent l / K, so a pass covers 64 / K parents and
+// one ballot compacts the children that reach tau in (parent, rank) order.
+__device__ __forceinline__ int lanes_below(uint64_t b) {
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(b >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b, 0u));
+}
+
 __device__ int plan_count(const PlanShared& sh, int Dp, int K, double tau, int cap, double* buf, double& m_out) {
     const int lane = lane_id();
+    const int per = kWave / K;  // parents per pass
+    const int pp = lane / K, pj = lane - pp * K;
     int total = 0;
     int plo = 0, phi = 0;  // parents of the current level in buf; level 0: the root
     double m = -INFINITY;
     for (int k = 0; k < Dp; ++k) {
         const int kk = sh.kfin[k];
-        const float lpv = lane < kk ? sh.lp[k * K + lane] : -INFINITY;
+        const bool cand = pp < per && pj < kk;
+        const double lpj = cand ? (double)sh.lp[k * K + pj] : -INFINITY;
         const int np = k == 0 ? 1 : phi - plo;
         const int nstart = total;
-        for (int base = 0; base < np; base += kWave) {
-            const int i = base + lane;
-            const bool valid = i < np;
+        for (int base = 0; base < np; base += per) {
+            const int i = base + pp;
+            const bool valid = cand && i < np;
             const double s = (valid && k > 0) ? buf[plo + i] : 0.0;
-            int c = 0;
-            bool done = !valid;
-            for (int j = 0; j < kk; ++j) {
-                const double cs = s + (double)lane_f32(lpv, j);
-                const bool ok = valid && cs >= tau;
-                if (!done && !ok) {
-                    m = fmax(m, cs);  // the parent's best child below tau
-                    done = true;
-                }
-                if (!__ballot(ok)) break;
-                c += ok ? 1 : 0;
-            }
-            int tot;
-            const int off = wave_excl_scan<6>(c, tot);
-            if (total + tot > cap) {
+            const double cs = s + lpj;
+            const bool ok = valid && cs >= tau;
+            if (valid && !ok) m = fmax(m, cs);  // children below tau (the best of them counts)
+            const uint64_t b = __ballot(ok);
+            const int cnt = __popcll(b);
+            if (total + cnt > cap) {
                 m_out = -INFINITY;
                 return cap + 1;
             }
-            for (int j = 0; __ballot(j < c); ++j) {
-                const float lj = lane_f32(lpv, j);
-                if (j < c) buf[total + off + j] = s + (double)lj;
-            }
-            total += tot;
+            if (ok) buf[total + lanes_below(b)] = cs;
+            total += cnt;
         }
         __threadfence_block();  // the next level reads these scores from other lanes
         plo = nstart;
@@ -911,48 +908,48 @@ __global__ __launch_bounds__(kPlanThreads) void plan_tree(int D, int S, int K, i
         sh.u.t.rank[0] = -1;
         sh.u.t.depth[0] = 0;
     }
+    // lane l takes candidate l % K of parent l / K (as in plan_count); the
+    // admitted children of a parent are a prefix of its candidates
+    const int per = kWave / K;
+    const int pp = lane / K, pj = lane - pp * K;
     int n = 1, plo = 0, phi = 1;
     for (int k = 0; k < Dp && plo < phi; ++k) {
         const int kk = sh.kfin[k];
-        const float lpv = lane < kk ? sh.lp[k * K + lane] : -INFINITY;
-        for (int base = plo; base < phi; base += kWave) {
-            const int i = base + lane;
-            const bool valid = i < phi;
-            const double s = valid ? sh.u.t.score[i] : 0.0;
-            int cg = 0, ce = 0;
-            for (int j = 0; j < kk; ++j) {
-                const double cs = s + (double)lane_f32(lpv, j);
-                const bool gt = valid && cs > tstar;
-                const bool eq = valid && cs == tstar;
-                if (!__ballot(gt || eq)) break;
-                cg += gt ? 1 : 0;
-                ce += eq ? 1 : 0;
-            }
-            int etot;
-            const int eoff = wave_excl_scan<6>(ce, etot);
-            const int adm = max(0, min(ce, quota - eoff));
+        const bool cand = pp < per && pj < kk;
+        const double lpj = cand ? (double)sh.lp[k * K + pj] : -INFINITY;
+        for (int base = plo; base < phi; base += per) {
+            const int i = base + pp;
+            const bool par_ok = pp < per && i < phi;
+            const bool valid = cand && i < phi;
+            const double s = par_ok ? sh.u.t.score[i] : 0.0;
+            const double cs = s + lpj;
+            const bool gt = valid && cs > tstar;
+            const bool eq = valid && cs == tstar;
+            // nodes scoring exactly t* are admitted in (depth, rank path) order,
+            // which is lane order here
+            const uint64_t beq = __ballot(eq);
+            const int etot = __popcll(beq);
+            const bool adm = gt || (eq && lanes_below(beq) < quota);
             if (etot > 0 && quota > 0) tie_admitted = true;
             quota -= min(etot, quota);
-            const int c = cg + adm;
-            int tot;
-            const int off = wave_excl_scan<6>(c, tot);
-            for (int j = 0; __ballot(j < c); ++j) {
-                const float lj = lane_f32(lpv, j);
-                if (j < c && n + off + j <= B) {  // always true: the admitted nodes number at most B
-                    const int x = n + off + j;
-                    const double cs = s + (double)lj;
+            const uint64_t b = __ballot(adm);
+            if (adm) {
+                const int x = n + lanes_below(b);
+                if (x <= B) {  // always true: the admitted nodes number at most B
                     sh.u.t.score[x] = cs;
                     sh.u.t.par[x] = i;
-                    sh.u.t.rank[x] = j;
+                    sh.u.t.rank[x] = pj;
                     sh.u.t.depth[x] = k + 1;
                     minsc = fmin(minsc, cs);
                 }
             }
-            if (valid) {
+            if (par_ok && pj == 0) {
+                const uint64_t seg = (K >= 64 ? ~0ull : ((1ull << K) - 1ull)) << (pp * K);
+                const int c = __popcll(b & seg);
                 sh.u.t.nch[i] = c;
-                sh.u.t.fc[i] = c ? n + off : -1;
+                sh.u.t.fc[i] = c ? n + __popcll(b & ((1ull << (pp * K)) - 1ull)) : -1;
             }
-            n = min(n + tot, B + 1);
+            n = min(n + __popcll(b), B + 1);
         }
         __threadfence_block();
         plo = phi;
