@@ -53,7 +53,10 @@ template <bool STATS>
 constexpr int cand_cap() { return STATS ? 128 : 256; }
 constexpr int kDraftChunk = kDraftThreads * 8 * kDraftU;
 constexpr int kFinalRegs = 8;  // keys per lane in the final selection (512 in all)
-constexpr int kRecSlots = 8;   // recorded groups per lane before the wave flushes
+// recorded groups per lane before the wave flushes (the pool selection, with
+// no table in LDS and a weaker first filter at K = 64, keeps more)
+template <bool STATS>
+constexpr int rec_slots() { return STATS ? 8 : 24; }
 constexpr int kRecBatch = 4;   // recorded groups re-read at once
 
 // Exponential table over bf16 patterns: biased exponent field in
@@ -215,6 +218,58 @@ __device__ __forceinline__ uint64_t wave_select_top(uint64_t (&v)[NR], int K) {
     return out;
 }
 
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int j) {
+    const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), j, kWave);
+    const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, j, kWave);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Sorts the NR * 64 keys held NR per lane in descending order (element
+// r * 64 + lane in v[r]): a bitonic network, lane exchanges for distances
+// below 64 and register exchanges above. Cheaper than K selection rounds
+// once K is large.
+template <int NR>
+__device__ __forceinline__ void wave_sort_desc(uint64_t (&v)[NR]) {
+    const int lane = lane_id();
+    constexpr int N = NR * kWave;
+#pragma unroll
+    for (int k = 2; k <= N; k <<= 1) {
+#pragma unroll
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            if (j >= kWave) {
+                const int rj = j / kWave;
+#pragma unroll
+                for (int r = 0; r < NR; ++r) {
+                    if (r & rj) continue;  // each register pair (r, r | rj) once
+                    const bool desc = ((r * kWave + lane) & k) == 0;
+                    const uint64_t a = v[r], b = v[r | rj];
+                    const bool sw = desc ? (a < b) : (a > b);  // the lower element keeps the max when descending
+                    v[r] = sw ? b : a;
+                    v[r | rj] = sw ? a : b;
+                }
+            } else {
+#pragma unroll
+                for (int r = 0; r < NR; ++r) {
+                    const uint64_t o = shfl_xor_u64(v[r], j);
+                    const bool lower = (lane & j) == 0;
+                    const bool desc = ((r * kWave + lane) & k) == 0;
+                    const bool keep_max = lower == desc;
+                    v[r] = keep_max ? (v[r] > o ? v[r] : o) : (v[r] < o ? v[r] : o);
+                }
+            }
+        }
+    }
+}
+
+// The K (<= 64) largest keys in lanes 0..K-1 (sorted; 0 past them), by
+// selection rounds for small K and by a sort for large K. Destroys v.
+template <int NR>
+__device__ __forceinline__ uint64_t wave_top(uint64_t (&v)[NR], int K) {
+    if (K <= 16) return wave_select_top<NR>(v, K);
+    wave_sort_desc<NR>(v);
+    return lane_id() < K ? v[0] : 0ull;
+}
+
 __device__ __forceinline__ void wave_lds_fence() {
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -250,7 +305,7 @@ struct CandBuf {
             const int j = i * kWave + lane;
             v[i] = j < n ? buf[j] : 0ull;
         }
-        const uint64_t t = wave_select_top<CAP / kWave>(v, K);
+        const uint64_t t = wave_top<CAP / kWave>(v, K);
         wave_lds_fence();
         if (lane < K) buf[lane] = t;
         wave_lds_fence();
@@ -449,7 +504,7 @@ __device__ __forceinline__ void draft_chunk(const Raw8<DT> (&r)[kDraftU], int ba
         const uint64_t sk = __hip_atomic_load(St.key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         if (sk) St.cb.raise_to(sk);
     }
-    if (__ballot(St.nrec > kRecSlots - kDraftU)) {
+    if (__ballot(St.nrec > rec_slots<STATS>() - kDraftU)) {
         flush_recorded<DT, VEC, CAP>(St.cb, St.draft, St.rowbase, St.hi, St.K, St.rec, St.nrec, St.key);
         St.nrec = 0;
     }
@@ -458,7 +513,7 @@ __device__ __forceinline__ void draft_chunk(const Raw8<DT> (&r)[kDraftU], int ba
 // STATS = false is the pool selection: the same candidate lists (K = pool
 // size) and finiteness flags without the normaliser (pm, ps unused).
 template <int DT, bool VEC, bool STATS>
-__global__ __launch_bounds__(kDraftThreads) void draft_partials(const void* __restrict__ draft, int V, int D,
+__global__ __launch_bounds__(kDraftThreads) __attribute__((amdgpu_waves_per_eu(4))) void draft_partials(const void* __restrict__ draft, int V, int D,
                                                                 int seg, int S, float invT, int K, int use_table,
                                                                 float* __restrict__ pm, double* __restrict__ ps,
                                                                 uint64_t* __restrict__ pk, int* __restrict__ pf,
@@ -503,7 +558,7 @@ __global__ __launch_bounds__(kDraftThreads) void draft_partials(const void* __re
         }
     }
 
-    __shared__ int s_rec[kRecSlots][kDraftThreads];
+    __shared__ int s_rec[rec_slots<STATS>()][kDraftThreads];
     CandBuf<CAP> cb;
     cb.buf = s_buf[wave];
     cb.n = 0;
@@ -593,11 +648,11 @@ __global__ __launch_bounds__(kDraftThreads) void draft_partials(const void* __re
         if (total <= 2 * kWave) {
             uint64_t v[2];
             gather_flat<2, CAP>(s_buf, s_n, v);
-            best = wave_select_top<2>(v, K);
+            best = wave_top<2>(v, K);
         } else {
             uint64_t v[kFinalRegs];
             gather_flat<kFinalRegs, CAP>(s_buf, s_n, v);
-            best = wave_select_top<kFinalRegs>(v, K);
+            best = wave_top<kFinalRegs>(v, K);
         }
         // segment normaliser: lanes w < kDraftWaves hold wave w's partial
         const float mw = lane < kDraftWaves ? s_m[lane] : -INFINITY;
