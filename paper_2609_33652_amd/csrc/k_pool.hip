@@ -14,11 +14,14 @@
 //                the segment lists of the pool selection into pool d, then
 //                builds the candidate list of every context that draws from
 //                pool d (the root's for d = 0, one per parent slot otherwise).
-//   pool_plan    one workgroup per request: best-first expansion over the
-//                per-node candidate lists. One wave pops: the fringe (every
-//                uncommitted node whose predecessor is committed) sits in
-//                LDS and every pop is a wave-wide argmax over it; then the
-//                committed nodes are laid out in BFS order level by level.
+//   pool_plan    one workgroup per request: the first B rank paths under the
+//                static order over the per-node candidate lists, found by
+//                the threshold search of the vocabulary-wide planner (path
+//                scores never grow toward children or younger siblings, so
+//                the nodes scoring at least a threshold form a subtree that
+//                a level-by-level count enumerates; here a node's children
+//                come from its own list, and nodes carry their pool slot),
+//                then emitted in BFS order.
 //   pool_replay  one workgroup per request: layer by layer, one wave per
 //                parent, lane j scores pool slot j; the children get the m
 //                largest Gumbel keys in rank order.
@@ -150,58 +153,50 @@ __global__ __launch_bounds__(kPoolThreads) void pool_lists(int D, int S, int P, 
 // workspace).
 constexpr int kPoolListLds = 16384;
 constexpr int kPoolListsMax = 1 + (TSB_MAX_D - 1) * kPoolMax;
-constexpr int kFringeMax = TSB_MAX_B + 2;
-constexpr int kPlanPoolThreads = 256;
+constexpr int kPlanPoolWaves = 16;
+constexpr int kPlanPoolThreads = kPlanPoolWaves * kWave;
+constexpr int kPoolPlanBuf = 6144;  // (score, slot) records shared by the counting waves
 
 struct PoolPlanShared {
     float llp[kPoolListLds];
     uint8_t lslot[kPoolListLds];
     uint8_t lnf[kPoolListsMax];
-    // committed nodes by pop index (0 = root)
-    double cscore[TSB_MAX_B + 1];
-    int16_t cpar[TSB_MAX_B + 1];
-    uint8_t crank[TSB_MAX_B + 1], cdepth[TSB_MAX_B + 1], cslot[TSB_MAX_B + 1], cnch[TSB_MAX_B + 1];
-    // fringe: (score, depth, parent pop index, rank)
-    double fscore[kFringeMax];
-    int16_t fpar[kFringeMax];
-    uint8_t frank[kFringeMax], fdepth[kFringeMax];
-    // BFS layout
-    int16_t order[TSB_MAX_B + 1], bfs_of_pop[TSB_MAX_B + 1], fcb[TSB_MAX_B + 1], bucket[TSB_MAX_B + 1];
-    int dcnt[TSB_MAX_D + 2], dstart[TSB_MAX_D + 2];
+    double piv[kPlanPoolWaves];
+    double mval[kPlanPoolWaves];
+    int cnt[kPlanPoolWaves];
+    double tstar;
+    int g;
+    union {
+        struct {
+            double score[kPoolPlanBuf];
+            uint8_t slot[kPoolPlanBuf];
+        } b;
+        struct {
+            double score[TSB_MAX_B + 1];
+            int par[TSB_MAX_B + 1];
+            int rank[TSB_MAX_B + 1];
+            int depth[TSB_MAX_B + 1];
+            int nch[TSB_MAX_B + 1];
+            int fc[TSB_MAX_B + 1];
+            uint8_t slot[TSB_MAX_B + 1];
+        } t;
+    } u;
 };
 
-struct ListView {
-    const PoolPlanShared* sh;
-    const uint64_t* g;  // this request's lists in the workspace
-    int K, P;
-    __device__ float lp(int li, int k) const {
-        const int i = li * K + k;
-        return i < kPoolListLds ? sh->llp[i] : entry_lp(g[i]);
-    }
-    __device__ int slot(int li, int k) const {
-        const int i = li * K + k;
-        return i < kPoolListLds ? (int)sh->lslot[i] : entry_slot(g[i]);
-    }
-    // list of the children of a committed node
-    __device__ int of(int depth, int slot) const { return depth == 0 ? 0 : 1 + (depth - 1) * P + slot; }
-};
-
-__device__ __forceinline__ void wave_lds_sync() {
-    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-    __builtin_amdgcn_wave_barrier();
+// Entry k of list li (LDS, or the workspace beyond the LDS copy).
+__device__ __forceinline__ float list_lp(const PoolPlanShared& sh, const uint64_t* g, int K, int li, int k) {
+    const int i = li * K + k;
+    return i < kPoolListLds ? sh.llp[i] : entry_lp(g[i]);
 }
+__device__ __forceinline__ int list_slot(const PoolPlanShared& sh, const uint64_t* g, int K, int li, int k) {
+    const int i = li * K + k;
+    return i < kPoolListLds ? (int)sh.lslot[i] : entry_slot(g[i]);
+}
+// list of the children of a node at `depth` whose token holds `slot`
+__device__ __forceinline__ int list_of(int P, int depth, int slot) { return depth == 0 ? 0 : 1 + (depth - 1) * P + slot; }
 
-// Rank paths of two fringe entries at the same depth, lexicographically:
-// true if entry a comes first. Walks up the committed parents to the first
-// common one.
-__device__ bool fringe_lex_less(const PoolPlanShared& sh, int a, int b) {
-    int pa = sh.fpar[a], pb = sh.fpar[b];
-    if (pa == pb) return sh.frank[a] < sh.frank[b];
-    while (sh.cpar[pa] != sh.cpar[pb]) {
-        pa = sh.cpar[pa];
-        pb = sh.cpar[pb];
-    }
-    return sh.crank[pa] < sh.crank[pb];
+__device__ __forceinline__ int lanes_below(uint64_t b) {
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(b >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b, 0u));
 }
 
 __device__ __forceinline__ double wave_max_d(double v) {
@@ -209,10 +204,56 @@ __device__ __forceinline__ double wave_max_d(double v) {
     for (int o = 32; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o, kWave));
     return v;
 }
-__device__ __forceinline__ int wave_min_i(int v) {
+__device__ __forceinline__ double wave_min_d(double v) {
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o, kWave));
+    for (int o = 32; o > 0; o >>= 1) v = fmin(v, __shfl_xor(v, o, kWave));
     return v;
+}
+
+// Number of nodes (root excluded) scoring at least tau, level by level, with
+// their (score, slot) stored in (bs, bsl); cap + 1 once more than cap.
+// m_out: the largest node score below tau (-inf if none; meaningful without
+// overflow). Lane l takes candidate l % K of parent l / K.
+__device__ int pool_count(const PoolPlanShared& sh, const uint64_t* G, int P, int Dp, int K, double tau, int cap,
+                          double* bs, uint8_t* bsl, double& m_out) {
+    const int lane = lane_id();
+    const int per = kWave / K;
+    const int pp = lane / K, pj = lane - pp * K;
+    int total = 0;
+    int plo = 0, phi = 0;  // parents of the current level in the buffer; level 0: the root
+    double m = -INFINITY;
+    for (int k = 0; k < Dp; ++k) {
+        const int np = k == 0 ? 1 : phi - plo;
+        const int nstart = total;
+        for (int base = 0; base < np; base += per) {
+            const int i = base + pp;
+            const bool par_ok = pp < per && i < np;
+            const double s = (par_ok && k > 0) ? bs[plo + i] : 0.0;
+            const int li = list_of(P, k, (par_ok && k > 0) ? (int)bsl[plo + i] : 0);
+            const bool valid = par_ok && pj < (int)sh.lnf[li];
+            const double cs = valid ? s + (double)list_lp(sh, G, K, li, pj) : -INFINITY;
+            const bool ok = valid && cs >= tau;
+            if (valid && !ok) m = fmax(m, cs);  // children below tau (the best of them counts)
+            const uint64_t b = __ballot(ok);
+            const int cnt = __popcll(b);
+            if (total + cnt > cap) {
+                m_out = -INFINITY;
+                return cap + 1;
+            }
+            if (ok) {
+                const int x = total + lanes_below(b);
+                bs[x] = cs;
+                bsl[x] = (uint8_t)list_slot(sh, G, K, li, pj);
+            }
+            total += cnt;
+        }
+        __threadfence_block();  // the next level reads these records from other lanes
+        plo = nstart;
+        phi = total;
+        if (phi == plo) break;
+    }
+    m_out = wave_max_d(m);
+    return total;
 }
 
 __global__ __launch_bounds__(kPlanPoolThreads) void pool_plan(int D, int P, int K, int B,
@@ -223,12 +264,13 @@ __global__ __launch_bounds__(kPlanPoolThreads) void pool_plan(int D, int P, int 
                                                               int32_t* __restrict__ req_status) {
     __shared__ PoolPlanShared sh;
     const int r = blockIdx.x;
-    const int tid = threadIdx.x, lane = tid % kWave;
+    const int tid = threadIdx.x;
+    const int wave = tid / kWave, lane = tid % kWave;
     const int NL = 1 + (D - 1) * P;
     const uint64_t* G = lists + (size_t)r * NL * K;
     const bool bad = (req_status[r] & TSB_REQ_NONFINITE) != 0;
 
-    // lists into LDS (all threads)
+    // lists into LDS
     const int nent = min(NL * K, kPoolListLds);
     for (int i = tid; i < nent; i += kPlanPoolThreads) {
         const int li = i / K, k = i % K;
@@ -238,191 +280,162 @@ __global__ __launch_bounds__(kPlanPoolThreads) void pool_plan(int D, int P, int 
     }
     for (int i = tid; i < NL; i += kPlanPoolThreads) sh.lnf[i] = (uint8_t)nfin[(size_t)r * NL + i];
     __syncthreads();
-    if (tid >= kWave) return;
+    const int Dp = (bad || B == 0) ? 0 : D;
 
-    const ListView LV{&sh, G, K, P};
-    // root committed; its first child enters the fringe
-    int ncom = 1, nf = 0;
+    // ---- threshold search (uniform control flow across the workgroup), as
+    // in the vocabulary-wide planner
+    const int cap = 2 * (B + 1);
+    const int ns = min(kPlanPoolWaves, kPoolPlanBuf / cap);
+    double hi_m = (Dp > 0 && sh.lnf[0] > 0) ? (double)sh.llp[0] : -INFINITY;  // the best node's score
+    int hi_cnt = 0;
+    double lo = -INFINITY;
+    int mode = 3;  // 1: t* = hi_m; 2: t* selected in a wave's buffer; 3: every node is chosen
+    int src = -1;
+    for (int round = 0; hi_m > -INFINITY; ++round) {
+        if (round > B + 1) {
+            mode = 1;
+            break;
+        }
+        if (wave < ns) {
+            const double tau = wave == 0 ? hi_m
+                               : (lo > -INFINITY ? hi_m - (hi_m - lo) * ((double)wave / (double)ns)
+                                                 : hi_m - 0.25 * exp2(0.5 * (double)(wave - 1)));
+            double m;
+            const int c = pool_count(sh, G, P, Dp, K, tau, cap, sh.u.b.score + wave * cap, sh.u.b.slot + wave * cap, m);
+            if (lane == 0) {
+                sh.piv[wave] = tau;
+                sh.cnt[wave] = c;
+                sh.mval[wave] = m;
+            }
+        }
+        __syncthreads();
+        if (sh.cnt[0] >= B + 1) {
+            mode = 1;
+            break;
+        }
+        int best = -1;
+        for (int w = 1; w < ns; ++w)
+            if (sh.cnt[w] >= B + 1 && sh.cnt[w] <= cap && (best < 0 || sh.piv[w] > sh.piv[best])) best = w;
+        if (best >= 0) {
+            mode = 2;
+            src = best;
+            break;
+        }
+        int nh = 0;  // count(piv[0]) <= B here
+        double nlo = lo;
+        for (int w = 1; w < ns; ++w) {
+            if (sh.cnt[w] <= B && sh.piv[w] < sh.piv[nh]) nh = w;
+            if (sh.cnt[w] > cap && sh.piv[w] > nlo) nlo = sh.piv[w];
+        }
+        hi_cnt = sh.cnt[nh];
+        hi_m = sh.mval[nh];
+        lo = nlo;
+        __syncthreads();
+    }
+    if (mode == 1) {
+        if (tid == 0) {
+            sh.tstar = hi_m;
+            sh.g = hi_cnt;
+        }
+    } else if (mode == 2) {
+        const int c = sh.cnt[src];
+        const double* b = sh.u.b.score + src * cap;
+        for (int i = tid; i < c; i += kPlanPoolThreads) {
+            const double v = b[i];
+            int gt = 0, ge = 0;
+            for (int j = 0; j < c; ++j) {
+                const double w = b[j];
+                gt += w > v ? 1 : 0;
+                ge += w >= v ? 1 : 0;
+            }
+            if (gt <= B && ge >= B + 1) {  // every such thread holds the same value
+                sh.tstar = v;
+                sh.g = gt;
+            }
+        }
+    } else if (tid == 0) {
+        sh.tstar = -INFINITY;  // every node scores above it
+        sh.g = 0;
+    }
+    __syncthreads();
+    if (wave != 0) return;
+
+    // ---- emission in BFS order (wave 0): lane l takes candidate l % K of
+    // parent l / K; the admitted children of a parent are a prefix of its list
+    const double tstar = sh.tstar;
+    int quota = mode == 3 ? 0 : B - sh.g;  // nodes scoring exactly t* still admitted
+    bool tie_admitted = false;
+    double minsc = INFINITY;
     if (lane == 0) {
-        sh.cscore[0] = 0.0;
-        sh.cpar[0] = -1;
-        sh.crank[0] = 0;
-        sh.cdepth[0] = 0;
-        sh.cslot[0] = 0;
-        sh.cnch[0] = 0;
+        sh.u.t.score[0] = 0.0;
+        sh.u.t.par[0] = -1;
+        sh.u.t.rank[0] = -1;
+        sh.u.t.depth[0] = 0;
+        sh.u.t.slot[0] = 0;
     }
-    if (!bad && D > 0 && B > 0 && sh.lnf[0] > 0) {
-        if (lane == 0) {
-            sh.fscore[0] = 0.0 + (double)LV.lp(0, 0);
-            sh.fpar[0] = 0;
-            sh.frank[0] = 0;
-            sh.fdepth[0] = 1;
-        }
-        nf = 1;
-    }
-    wave_lds_sync();
-
-    while (ncom - 1 < B && nf > 0) {
-        // best fringe entry: score desc, depth asc, rank path asc
-        double bs = -INFINITY;
-        int bd = 255, bi = -1, bc = 0;
-        for (int i = lane; i < nf; i += kWave) {
-            const double s = sh.fscore[i];
-            const int dd = sh.fdepth[i];
-            if (bi < 0 || s > bs || (s == bs && dd < bd)) {
-                bs = s;
-                bd = dd;
-                bi = i;
-                bc = 1;
-            } else if (s == bs && dd == bd) {
-                ++bc;
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    const int per = kWave / K;
+    const int pp = lane / K, pj = lane - pp * K;
+    int n = 1, plo = 0, phi = 1;
+    for (int k = 0; k < Dp && plo < phi; ++k) {
+        for (int base = plo; base < phi; base += per) {
+            const int i = base + pp;
+            const bool par_ok = pp < per && i < phi;
+            const double s = par_ok ? sh.u.t.score[i] : 0.0;
+            const int li = list_of(P, k, par_ok ? (int)sh.u.t.slot[i] : 0);
+            const bool valid = par_ok && pj < (int)sh.lnf[li];
+            const double cs = valid ? s + (double)list_lp(sh, G, K, li, pj) : -INFINITY;
+            const bool gt = valid && cs > tstar;
+            const bool eq = valid && cs == tstar;
+            // nodes scoring exactly t* are admitted in (depth, rank path)
+            // order, which is lane order here
+            const uint64_t beq = __ballot(eq);
+            const int etot = __popcll(beq);
+            const bool adm = gt || (eq && lanes_below(beq) < quota);
+            if (etot > 0 && quota > 0) tie_admitted = true;
+            quota -= min(etot, quota);
+            const uint64_t b = __ballot(adm);
+            if (adm) {
+                const int x = n + lanes_below(b);
+                if (x <= B) {  // always true: the admitted nodes number at most B
+                    sh.u.t.score[x] = cs;
+                    sh.u.t.par[x] = i;
+                    sh.u.t.rank[x] = pj;
+                    sh.u.t.depth[x] = k + 1;
+                    sh.u.t.slot[x] = (uint8_t)list_slot(sh, G, K, li, pj);
+                    minsc = fmin(minsc, cs);
+                }
             }
-        }
-        const double ws = wave_max_d(bi >= 0 ? bs : -INFINITY);
-        const int wd = wave_min_i(bi >= 0 && bs == ws ? bd : 255);
-        const bool mine = bi >= 0 && bs == ws && bd == wd;
-        const uint64_t m1 = __ballot(mine), m2 = __ballot(mine && bc >= 2);
-        int b;
-        if (__popcll(m1) == 1 && m2 == 0) {
-            b = __builtin_amdgcn_readlane(bi, __ffsll((unsigned long long)m1) - 1);
-        } else {  // equal score and depth: the lexicographically smaller rank path
-            int best = -1;
-            if (lane == 0)
-                for (int i = 0; i < nf; ++i)
-                    if (sh.fscore[i] == ws && sh.fdepth[i] == wd && (best < 0 || fringe_lex_less(sh, i, best)))
-                        best = i;
-            b = __builtin_amdgcn_readlane(best, 0);
-        }
-        // commit entry b
-        const double s = sh.fscore[b];
-        const int dd = sh.fdepth[b], p = sh.fpar[b], k = sh.frank[b];
-        const int lip = LV.of(sh.cdepth[p], sh.cslot[p]);
-        const int slot = LV.slot(lip, k);
-        const int c = ncom++;
-        // successors: c's first child, then its next younger sibling
-        bool has_a = false, has_b = false;
-        double sa = 0.0, sb = 0.0;
-        if (dd < D) {
-            const int lic = LV.of(dd, slot);
-            if (sh.lnf[lic] > 0) {
-                has_a = true;
-                sa = s + (double)LV.lp(lic, 0);
+            if (par_ok && pj == 0) {
+                const uint64_t seg = (K >= 64 ? ~0ull : ((1ull << K) - 1ull)) << (pp * K);
+                const int c = __popcll(b & seg);
+                sh.u.t.nch[i] = c;
+                sh.u.t.fc[i] = c ? n + __popcll(b & ((1ull << (pp * K)) - 1ull)) : -1;
             }
+            n = min(n + __popcll(b), B + 1);
         }
-        if (k + 1 < sh.lnf[lip]) {
-            has_b = true;
-            sb = sh.cscore[p] + (double)LV.lp(lip, k + 1);
-        }
-        wave_lds_sync();
-        if (lane == 0) {
-            sh.cscore[c] = s;
-            sh.cpar[c] = (int16_t)p;
-            sh.crank[c] = (uint8_t)k;
-            sh.cdepth[c] = (uint8_t)dd;
-            sh.cslot[c] = (uint8_t)slot;
-            sh.cnch[c] = 0;
-            sh.cnch[p] = (uint8_t)(k + 1);  // children are committed in rank order
-            int at = b;
-            if (has_a) {
-                sh.fscore[at] = sa;
-                sh.fpar[at] = (int16_t)c;
-                sh.frank[at] = 0;
-                sh.fdepth[at] = (uint8_t)(dd + 1);
-                at = nf;
-            }
-            if (has_b) {
-                sh.fscore[at] = sb;
-                sh.fpar[at] = (int16_t)p;
-                sh.frank[at] = (uint8_t)(k + 1);
-                sh.fdepth[at] = (uint8_t)dd;
-                at = nf;
-            }
-            if (!has_a && !has_b && b != nf - 1) {  // fill the hole with the last entry
-                sh.fscore[b] = sh.fscore[nf - 1];
-                sh.fpar[b] = sh.fpar[nf - 1];
-                sh.frank[b] = sh.frank[nf - 1];
-                sh.fdepth[b] = sh.fdepth[nf - 1];
-            }
-        }
-        nf += (has_a && has_b) ? 1 : ((!has_a && !has_b) ? -1 : 0);
-        wave_lds_sync();
+        __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+        plo = phi;
+        phi = n;
     }
-
-    // plan margin: last committed score - best uncommitted score
-    double margin = INFINITY;
-    {
-        double m = -INFINITY;
-        for (int i = lane; i < nf; i += kWave) m = fmax(m, sh.fscore[i]);
-        m = wave_max_d(m);
-        if (ncom > 1 && nf > 0) margin = sh.cscore[ncom - 1] - m;
+    for (int i = plo + lane; i < phi; i += kWave) {  // the last level has no children
+        sh.u.t.nch[i] = 0;
+        sh.u.t.fc[i] = -1;
     }
-
-    // BFS layout: nodes bucketed by depth, then level by level the first
-    // child of every node (prefix sums of the children counts in BFS order)
-    const int n = ncom;
-    for (int d = lane; d < TSB_MAX_D + 2; d += kWave) sh.dcnt[d] = 0;
-    wave_lds_sync();
-    for (int c = lane; c < n; c += kWave) atomicAdd(&sh.dcnt[sh.cdepth[c]], 1);
-    wave_lds_sync();
-    if (lane == 0) {
-        int acc = 0;
-        for (int d = 0; d <= D; ++d) {
-            sh.dstart[d] = acc;
-            acc += sh.dcnt[d];
-            sh.dcnt[d] = 0;
-        }
-    }
-    wave_lds_sync();
-    for (int c = lane; c < n; c += kWave) {
-        const int d = sh.cdepth[c];
-        const int pos = atomicAdd(&sh.dcnt[d], 1);
-        sh.bucket[sh.dstart[d] + pos] = (int16_t)c;
-    }
-    if (lane == 0) {
-        sh.order[0] = 0;
-        sh.bfs_of_pop[0] = 0;
-    }
-    wave_lds_sync();
-    int lo = 0, hi = 1;
-    for (int d = 0; d < D && hi > lo; ++d) {
-        int next = hi;
-        for (int base = lo; base < hi; base += kWave) {
-            const int i = base + lane;
-            const int cnt = i < hi ? (int)sh.cnch[sh.order[i]] : 0;
-            int tot;
-            const int off = wave_excl_scan<6>(cnt, tot);
-            if (i < hi) sh.fcb[i] = (int16_t)(cnt > 0 ? next + off : -1);
-            next += tot;
-        }
-        wave_lds_sync();
-        const int b0 = sh.dstart[d + 1], b1 = b0 + (next - hi);
-        for (int j = b0 + lane; j < b1; j += kWave) {
-            const int c = sh.bucket[j];
-            const int bp = sh.bfs_of_pop[sh.cpar[c]];
-            const int bc = sh.fcb[bp] + sh.crank[c];
-            sh.order[bc] = (int16_t)c;
-            sh.bfs_of_pop[c] = (int16_t)bc;
-        }
-        wave_lds_sync();
-        lo = hi;
-        hi = next;
-    }
-    for (int i = lo + lane; i < hi; i += kWave) sh.fcb[i] = -1;  // the deepest level has no children
-    wave_lds_sync();
+    minsc = wave_min_d(minsc);
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
 
     const size_t tb = (size_t)r * (B + 1);
     for (int i = lane; i <= B; i += kWave) {
         if (i < n) {
-            const int c = sh.order[i];
-            tree.parent[tb + i] = i == 0 ? -1 : (int32_t)sh.bfs_of_pop[sh.cpar[c]];
-            tree.depth[tb + i] = sh.cdepth[c];
-            tree.rank[tb + i] = i == 0 ? -1 : (int32_t)sh.crank[c];
-            tree.n_children[tb + i] = sh.cnch[c];
-            tree.first_child[tb + i] = sh.fcb[i];
-            tree.score[tb + i] = sh.cscore[c];
+            tree.parent[tb + i] = sh.u.t.par[i];
+            tree.depth[tb + i] = sh.u.t.depth[i];
+            tree.rank[tb + i] = sh.u.t.rank[i];
+            tree.n_children[tb + i] = sh.u.t.nch[i];
+            tree.first_child[tb + i] = sh.u.t.fc[i];
+            tree.score[tb + i] = sh.u.t.score[i];
             if (plan_tok)
-                plan_tok[tb + i] = i == 0 ? -1
-                                          : pool_tok[((size_t)r * D + (sh.cdepth[c] - 1)) * P + sh.cslot[c]];
+                plan_tok[tb + i] = i == 0 ? -1 : pool_tok[((size_t)r * D + (sh.u.t.depth[i] - 1)) * P + sh.u.t.slot[i]];
         } else {
             tree.parent[tb + i] = -1;
             tree.depth[tb + i] = -1;
@@ -434,6 +447,9 @@ __global__ __launch_bounds__(kPlanPoolThreads) void pool_plan(int D, int P, int 
         }
     }
     if (lane == 0) {
+        // margin: score of the B-th node in the order minus that of the (B+1)-th
+        double margin = (double)INFINITY;
+        if (mode != 3 && n > 1) margin = (tie_admitted ? tstar : minsc) - tstar;
         tree.n_nodes[r] = n;
         tree.plan_margin[r] = margin;
         if (!bad && n < B + 1) req_status[r] |= TSB_REQ_BUDGET_SHORT;
