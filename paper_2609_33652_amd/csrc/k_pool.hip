@@ -105,6 +105,16 @@ __global__ __launch_bounds__(kPoolThreads) void pool_lists(int D, int S, int P, 
                 const int rj = __builtin_amdgcn_readlane(rank, j);
                 if (kj != 0ull && rj == lane) best = kj;
             }
+        } else if (n <= 4 * kWave) {
+            // a bitonic sort of up to 256 keys: the pool is the first P
+            uint64_t v[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int i = q * kWave + lane;
+                v[q] = i < n ? pk[o * P + i] : 0ull;
+            }
+            wave_sort_desc<4>(v);
+            best = lane < P ? v[0] : 0ull;
         } else {
             WaveTopList top;
             top.init(P);

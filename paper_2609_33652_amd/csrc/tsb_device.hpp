@@ -340,6 +340,49 @@ struct WaveTopList {
     }
 };
 
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int j) {
+    const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), j, kWave);
+    const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, j, kWave);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Sorts the NR * 64 keys held NR per lane in descending order (element
+// r * 64 + lane in v[r]): a bitonic network, lane exchanges for distances
+// below 64 and register exchanges above. Cheaper than K selection rounds
+// once K is large.
+template <int NR>
+__device__ __forceinline__ void wave_sort_desc(uint64_t (&v)[NR]) {
+    const int lane = lane_id();
+    constexpr int N = NR * kWave;
+#pragma unroll
+    for (int k = 2; k <= N; k <<= 1) {
+#pragma unroll
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            if (j >= kWave) {
+                const int rj = j / kWave;
+#pragma unroll
+                for (int r = 0; r < NR; ++r) {
+                    if (r & rj) continue;  // each register pair (r, r | rj) once
+                    const bool desc = ((r * kWave + lane) & k) == 0;
+                    const uint64_t a = v[r], b = v[r | rj];
+                    const bool sw = desc ? (a < b) : (a > b);  // the lower element keeps the max when descending
+                    v[r] = sw ? b : a;
+                    v[r | rj] = sw ? a : b;
+                }
+            } else {
+#pragma unroll
+                for (int r = 0; r < NR; ++r) {
+                    const uint64_t o = shfl_xor_u64(v[r], j);
+                    const bool lower = (lane & j) == 0;
+                    const bool desc = ((r * kWave + lane) & k) == 0;
+                    const bool keep_max = lower == desc;
+                    v[r] = keep_max ? (v[r] > o ? v[r] : o) : (v[r] < o ? v[r] : o);
+                }
+            }
+        }
+    }
+}
+
 // Exclusive prefix sum over the lanes of small non-negative counts
 // (< 2^NB), one ballot per bit; `total` receives the wave sum.
 template <int NB>
