@@ -14,7 +14,7 @@ import torch
 
 import workloads as W
 from oracle import replay as oreplay, step as ostep
-from oracle.rowstats import inv_temperature, scaled
+from oracle.rowstats import STATUS_NONFINITE, inv_temperature, scaled
 import paper_2609_33652_amd as tsb
 from parity_util import (Tally, compare_plan, compare_replay, compare_verify, make_round, to_np, tree_dict_np)
 
@@ -299,3 +299,61 @@ def test_planner_exact_ties(B, K, D):
     assert tally.exact >= 4
     nmax = sum(K ** i for i in range(1, D + 1))
     assert (h["n_nodes"] == min(B, nmax) + 1).all()
+
+
+def _special_rows(rng, R, D, V):
+    """bf16-exact draft rows [R, D, V] with values outside the exponential table planted: exact zeros,
+    values below its smallest binade (+-2^-20 and bf16 subnormals), values at or beyond 64 (some the
+    row maximum), masked -inf entries, and one row whose every value lies outside the table."""
+    d = (rng.standard_normal((R, D, V)) * 2.5).astype(np.float32)
+    d[:, :, rng.integers(0, V, 16)] += 6.0
+    for r in range(R):
+        for j in range(D):
+            kind = (r * D + j) % 6
+            pos = rng.choice(V, 4000, replace=False)
+            if kind == 0:
+                d[r, j, pos] = 0.0
+            elif kind == 1:
+                d[r, j, pos[:2000]] = 2.0 ** -20
+                d[r, j, pos[2000:]] = -(2.0 ** -20)
+            elif kind == 2:
+                d[r, j, pos[:50]] = np.float32(np.ldexp(1.0, -130))  # a bf16 subnormal
+                d[r, j, pos[50:60]] = 64.0
+                d[r, j, pos[60:63]] = 100.0
+                d[r, j, pos[63:80]] = -100.0
+            elif kind == 3:
+                d[r, j, pos] = -np.inf
+            elif kind == 4:
+                d[r, j, pos[:20]] = 70.0
+                d[r, j, pos[20:40]] = -70.0
+    d[1, 4] = 64.0 + (rng.random(V).astype(np.float32) * 30.0)  # every value outside the table
+    return torch.from_numpy(d).to(torch.bfloat16).float().numpy()
+
+
+@pytest.mark.parametrize("T", [1.0, 0.05])
+def test_draft_table_path_special_values(T):
+    """Row statistics on full-vocabulary bf16 rows whose segments are long enough for the exponential
+    table (T = 1; at T = 0.05 the scaled logits leave the table's range and every logit is evaluated):
+    zeros, tiny, subnormal, large and masked logits must give the oracle's binary64 normaliser to 1e-12,
+    its canonical binary32 rounding, the same candidates and the same topology; NaN and +inf rows flag
+    only their own request."""
+    R, D, V = 4, 32, 151936  # 128 draft rows: four segments of 37984 logits each
+    rng = np.random.default_rng(31 if T == 1.0 else 32)
+    d = _special_rows(rng, R, D, V)
+    d[2, 7, 12345] = np.nan
+    d[3, 30, 777] = np.inf
+    cfg = dict(name="special", R=R, V=V, D=D, B=20, K=8, T=T, dtype="bf16", steps=1)
+    rnd = make_round(cfg, 11)
+    rnd.plan(torch.from_numpy(d).to(torch.bfloat16).cuda())
+    h = rnd.host()
+    st = h["req_status"].numpy()
+    tally = Tally()
+    for r in range(R):
+        pl = ostep.plan_request(d[r], T, cfg["K"], cfg["B"])
+        if r >= 2:
+            assert pl["status"] & STATUS_NONFINITE and st[r] & tsb.REQ_NONFINITE, r
+            continue
+        assert not st[r] & tsb.REQ_NONFINITE, r
+        compare_plan(h, r, pl, tally, "special T=%g req %d" % (T, r))
+    say("special rows T=%g: exact %d flagged %d %s" % (T, tally.exact, tally.flagged, tally.notes[:3]))
+    assert tally.exact >= 1
