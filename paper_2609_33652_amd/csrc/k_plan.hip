@@ -227,11 +227,6 @@ __device__ __forceinline__ uint64_t wave_top(uint64_t (&v)[NR], int K) {
     return lane_id() < K ? v[0] : 0ull;
 }
 
-__device__ __forceinline__ void wave_lds_fence() {
-    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-}
-
 // Per-wave candidate buffer with its filter.
 template <int CAP>
 struct CandBuf {
@@ -532,10 +527,27 @@ __global__ __launch_bounds__(kDraftThreads) __attribute__((amdgpu_waves_per_eu(4
         s_lm[wave][lane] = isnan(lm) ? -INFINITY : lm;
         if (tid == 0) s_key = 0ull;
         __syncthreads();
-        float cm = s_lm[0][lane];
+        if (K <= 16) {
+            float cm = s_lm[0][lane];
 #pragma unroll
-        for (int w = 1; w < kDraftWaves; ++w) cm = fmaxf(cm, s_lm[w][lane]);
-        cb.fx = wave_kth_largest_sorted(cm, K);
+            for (int w = 1; w < kDraftWaves; ++w) cm = fmaxf(cm, s_lm[w][lane]);
+            cb.fx = wave_kth_largest_sorted(cm, K);
+        } else {
+            // large K: the K-th largest of the 512 lane maxima (each over
+            // distinct logits), by a radix selection on their ordered bits
+            uint32_t kb[kDraftWaves];
+#pragma unroll
+            for (int w = 0; w < kDraftWaves; ++w) kb[w] = ordered_bits(s_lm[w][lane]);
+            uint32_t t = 0;
+            for (int bit = 31; bit >= 0; --bit) {
+                const uint32_t cand = t | (1u << bit);
+                int cnt = 0;
+#pragma unroll
+                for (int w = 0; w < kDraftWaves; ++w) cnt += __popcll(__ballot(kb[w] >= cand));
+                if (cnt >= K) t = cand;
+            }
+            cb.fx = from_ordered_bits(t);
+        }
     }
 
     DraftState<CAP> St{cb, draft, rowbase, hi, K, invT, tab, s_tab, s_exp, s_rec, &s_key};

@@ -469,6 +469,104 @@ __global__ __launch_bounds__(kPlanPoolThreads) void pool_plan(int D, int P, int 
 // ------------------------------------------------------------------ replay
 __device__ __forceinline__ double gumbel_f64(uint32_t w) { return -log(-log(u24d(w))); }
 
+// Internal nodes whose Gumbel draws are computed before the layer walk.
+constexpr int kReplayGCap = 128;
+
+// Exact rank of lane's key under (key desc, token asc) among the wave's 64
+// keys (invalid lanes carry -inf); used when two valid keys are equal.
+__device__ __forceinline__ int rank_exact(double kv, int tok) {
+    int rank = 0;
+    for (int k = 0; k < kWave; ++k) {
+        const double ok = lane_f64(kv, k);
+        const int ot = __builtin_amdgcn_readlane(tok, k);
+        rank += (ok > kv || (ok == kv && ot < tok)) ? 1 : 0;
+    }
+    return rank;
+}
+
+constexpr int kReplayMatRegs = (kPoolMax * kPoolMax) / kPoolThreads;
+
+// LDS state of the pool replay walk.
+struct PoolReplayLds {
+    const int* tok;        // [D][P] pool tokens
+    const float* a;        // [D][P] tempered draft logits
+    const double* g;       // [kReplayGCap][kPoolMax] Gumbel draws of internal nodes
+    const uint16_t* in;    // internal nodes: node | depth << 10
+    const int16_t* m;      // child count of internal node q
+    const int16_t* fc;     // first child of internal node q
+    int16_t* slot;         // pool slot of every node's replayed token
+    int* ntok;             // replayed token of every node
+    uint64_t* key;         // [waves][64] keys of a wave's parent
+    int8_t* pos;           // [waves][64] rank claims
+};
+
+// Transition matrix j of a request into registers; every thread loads every
+// time (the index is clamped into the matrix, entries past its end land in
+// the unused tail of the LDS buffer), so the loads are issued unconditionally.
+__device__ __forceinline__ void fetch_matrix(float (&v)[kReplayMatRegs], const float* src, size_t base, int mat,
+                                             int tid) {
+#pragma unroll
+    for (int k = 0; k < kReplayMatRegs; ++k) v[k] = src[base + min(tid + k * kPoolThreads, mat - 1)];
+}
+__device__ __forceinline__ void store_matrix(float* buf, const float (&v)[kReplayMatRegs], int tid) {
+#pragma unroll
+    for (int k = 0; k < kReplayMatRegs; ++k) buf[tid + k * kPoolThreads] = v[k];
+}
+
+// The parents of layer d (internal nodes lo..hi-1), one wave each: lane j
+// scores pool slot j under the parent's replayed slot (matrix tr of position
+// d - 1), and the m largest keys give the children in rank order.
+__device__ __forceinline__ void replay_parents(const PoolReplayLds& L, int d, int lo, int hi, int P, float invT,
+                                               const float* tr, const RngKey& key, int wave, int lane) {
+    for (int g = lo + wave; g < hi; g += kPoolWaves) {
+        const int u = L.in[g] & 1023;
+        const int m = L.m[g], fc = L.fc[g];
+        float z = -INFINITY;
+        int tok = 0x7FFFFFFF;
+        if (lane < P) {
+            tok = L.tok[d * P + lane];
+            z = L.a[d * P + lane];
+            if (d > 0) z = corrected_logit(z, tr[L.slot[u] * P + lane], invT);
+        }
+        const bool valid = lane < P && z > -INFINITY;
+        double kv = -INFINITY;
+        if (valid) {
+            const double G = g < kReplayGCap ? L.g[g * kPoolMax + lane]
+                                             : gumbel_f64(rng_word(key, (uint32_t)u, kStreamReplay, (uint32_t)tok));
+            kv = (double)z + G;
+        }
+        const uint64_t kb = valid ? ordered_bits64(kv) : 0ull;
+        uint64_t* wk = L.key + wave * kWave;
+        wk[lane] = kb;
+        wave_lds_fence();
+        int rank = 0;
+#pragma unroll 16
+        for (int k = 0; k < kWave; ++k) rank += wk[k] > kb ? 1 : 0;
+        // equal keys among the first m share a count: each claims its
+        // position, and a lane that lost its claim sends the wave to the exact
+        // ranking
+        wave_lds_fence();
+        int8_t* wp = L.pos + wave * kWave;
+        const bool top = valid && rank < m;
+        if (top) wp[rank] = (int8_t)lane;
+        wave_lds_fence();
+        if (__ballot(top && wp[rank] != lane)) rank = rank_exact(kv, valid ? tok : 0x7FFFFFFF);
+        wave_lds_fence();
+        if (valid && rank < m) {
+            L.ntok[fc + rank] = tok;
+            L.slot[fc + rank] = (int16_t)lane;
+        }
+    }
+}
+
+// One workgroup per request. Set-up, all waves at once: the pool tokens and
+// their tempered draft logits, the internal nodes in BFS order with their
+// depth, first child and child count, and the Gumbel draws of the first
+// kReplayGCap internal nodes (the draws depend on the node and the pool token
+// only). Then layer by layer, one wave per parent: the transition matrix of
+// the layer sits in LDS, fetched into registers two layers ahead (two
+// register sets, the walk unrolled by two), and a lane's rank is the count of
+// larger keys, read back from LDS. Replayed tokens stay in LDS until the end.
 template <int DT>
 __global__ __launch_bounds__(kPoolThreads) void pool_replay(int D, int V, int P, int B, float invT, const void* draft,
                                                             const float* __restrict__ trans,
@@ -477,12 +575,31 @@ __global__ __launch_bounds__(kPoolThreads) void pool_replay(int D, int V, int P,
                                                             int32_t* __restrict__ node_tok) {
     __shared__ int s_tok[TSB_MAX_D * kPoolMax];
     __shared__ float s_a[TSB_MAX_D * kPoolMax];
+    __shared__ float s_tr[2][kPoolMax * kPoolMax];
+    __shared__ double s_g[kReplayGCap * kPoolMax];
+    __shared__ uint64_t s_key[kPoolWaves][kWave];
+    __shared__ int8_t s_pos[kPoolWaves][kWave];
     __shared__ int16_t s_slot[TSB_MAX_B + 1];
-    __shared__ int s_lvl[TSB_MAX_D + 2];
+    __shared__ int s_ntok[TSB_MAX_B + 1];
+    __shared__ uint16_t s_int[TSB_MAX_B + 1];  // node | depth << 10
+    __shared__ int16_t s_fc[TSB_MAX_B + 1];
+    __shared__ int16_t s_m[TSB_MAX_B + 1];
+    __shared__ int s_ilvl[TSB_MAX_D + 2];
+    __shared__ int s_wcnt[kPoolWaves];
+    static_assert(TSB_MAX_B + 1 <= kPoolThreads, "one thread per node");
+    static_assert(TSB_MAX_B + 1 <= 1024 && TSB_MAX_D <= 64, "node | depth << 10 fits 16 bits");
+    static_assert(kReplayMatRegs * kPoolThreads == kPoolMax * kPoolMax, "matrix split over the threads");
     const int r = blockIdx.x;
     const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
     const size_t tb = (size_t)r * (B + 1);
     const int n = tree.n_nodes[r];
+    // transition matrices of the request (with D = 1 there are none: the
+    // fetches then read pool_tok[0] and their values are never used)
+    const bool has_t = D > 1;
+    const float* tsrc = has_t ? trans : (const float*)pool_tok;
+    const int mat = has_t ? P * P : 1;
+    const size_t trb = has_t ? (size_t)r * (D - 1) * mat : 0;
+    const int jmax = has_t ? D - 2 : 0;
 
     for (int i = tid; i < D * P; i += kPoolThreads) {
         const int d = i / P;
@@ -490,55 +607,81 @@ __global__ __launch_bounds__(kPoolThreads) void pool_replay(int D, int V, int P,
         s_tok[i] = t;
         s_a[i] = (t >= 0 && t < V) ? load_logit<DT>(draft, ((size_t)r * D + d) * V + t) * invT : -INFINITY;
     }
-    for (int d = tid; d < TSB_MAX_D + 2; d += kPoolThreads) s_lvl[d] = n;
-    if (tid == 0) {
-        s_lvl[0] = 0;
-        s_slot[0] = -1;
+    for (int i = tid; i <= B; i += kPoolThreads) {
+        s_ntok[i] = -1;
+        s_slot[i] = 0;  // every node below the root gets its slot from its parent's layer
     }
+    // internal nodes in BFS order (their depths are contiguous from 0)
+    const int nc = tid < n ? tree.n_children[tb + tid] : 0;
+    const bool internal = nc > 0;
+    const uint64_t bal = __ballot(internal);
+    const int below = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+    if (lane == 0) s_wcnt[wave] = __popcll(bal);
     __syncthreads();
-    for (int i = 1 + tid; i < n; i += kPoolThreads) {
-        const int di = tree.depth[tb + i];
-        if (di != tree.depth[tb + i - 1]) s_lvl[di] = i;
+    int q = below, n_int = 0;
+    for (int w = 0; w < kPoolWaves; ++w) {
+        const int c = s_wcnt[w];
+        q += w < wave ? c : 0;
+        n_int += c;
     }
-    for (int i = tid; i <= B; i += kPoolThreads) node_tok[tb + i] = -1;
+    if (internal) {
+        const int dep = tree.depth[tb + tid];
+        s_int[q] = (uint16_t)(tid | (dep << 10));
+        s_fc[q] = (int16_t)tree.first_child[tb + tid];
+        s_m[q] = (int16_t)nc;
+    }
+    for (int d = tid; d < TSB_MAX_D + 2; d += kPoolThreads) s_ilvl[d] = n_int;
     __syncthreads();
+    if (tid < n_int) {
+        const int dep = s_int[tid] >> 10;
+        if (tid == 0 || (s_int[tid - 1] >> 10) != dep) s_ilvl[dep] = tid;
+    }
 
     RngKey key;
     key.k0 = k0;
     key.k1 = k1;
     key.request = (uint32_t)r;
     key.step = step;
-    for (int d = 0; d < D; ++d) {
-        const int lo = s_lvl[d], hi = s_lvl[d + 1];
+    float ra[kReplayMatRegs], rb[kReplayMatRegs];
+    fetch_matrix(rb, tsrc, trb, mat, tid);  // position 0, stored after layer 0
+    const int ng = n_int < kReplayGCap ? n_int : kReplayGCap;
+    for (int g = wave; g < ng; g += kPoolWaves) {
+        const int u = s_int[g] & 1023, d = s_int[g] >> 10;
+        if (lane < P) s_g[g * kPoolMax + lane] = gumbel_f64(rng_word(key, (uint32_t)u, kStreamReplay,
+                                                                       (uint32_t)s_tok[d * P + lane]));
+    }
+    __syncthreads();
+
+    PoolReplayLds L;
+    L.tok = s_tok;
+    L.a = s_a;
+    L.g = s_g;
+    L.in = s_int;
+    L.m = s_m;
+    L.fc = s_fc;
+    L.slot = s_slot;
+    L.ntok = s_ntok;
+    L.key = &s_key[0][0];
+    L.pos = &s_pos[0][0];
+    // layer d reads the matrix of position d - 1 from buffer (d - 1) & 1 and
+    // stores that of position d (fetched during layer d - 1) into buffer d & 1
+    for (int d = 0; d < D; d += 2) {
+        int lo = s_ilvl[d], hi = s_ilvl[d + 1];
         if (lo >= hi) break;
-        for (int u = lo + wave; u < hi; u += kPoolWaves) {
-            const int m = tree.n_children[tb + u];
-            if (m <= 0) continue;
-            const int fc = tree.first_child[tb + u];
-            float z = -INFINITY;
-            int tok = 0x7FFFFFFF;
-            if (lane < P) {
-                tok = s_tok[d * P + lane];
-                z = s_a[d * P + lane];
-                if (d > 0) z = corrected_logit(z, trans[trans_row(r, D, d, s_slot[u], P) + lane], invT);
-            }
-            const bool valid = lane < P && z > -INFINITY;
-            const double kv =
-                valid ? (double)z + gumbel_f64(rng_word(key, (uint32_t)u, kStreamReplay, (uint32_t)tok)) : -INFINITY;
-            // rank under (key desc, token asc) among valid lanes
-            int rank = 0;
-            for (int k = 0; k < kWave; ++k) {
-                const double ok = lane_f64(kv, k);
-                const int ot = __builtin_amdgcn_readlane(tok, k);
-                rank += (ok > kv || (ok == kv && ot < tok)) ? 1 : 0;
-            }
-            if (valid && rank < m) {
-                node_tok[tb + fc + rank] = tok;
-                s_slot[fc + rank] = (int16_t)lane;
-            }
-        }
+        fetch_matrix(ra, tsrc, trb + (size_t)min(d + 1, jmax) * mat, mat, tid);
+        replay_parents(L, d, lo, hi, P, invT, s_tr[1], key, wave, lane);
+        store_matrix(s_tr[0], rb, tid);
+        __syncthreads();
+        if (d + 1 >= D) break;
+        lo = s_ilvl[d + 1];
+        hi = s_ilvl[d + 2];
+        if (lo >= hi) break;
+        fetch_matrix(rb, tsrc, trb + (size_t)min(d + 2, jmax) * mat, mat, tid);
+        replay_parents(L, d + 1, lo, hi, P, invT, s_tr[0], key, wave, lane);
+        store_matrix(s_tr[1], ra, tid);
         __syncthreads();
     }
+    for (int i = tid; i <= B; i += kPoolThreads) node_tok[tb + i] = s_ntok[i];
 }
 
 // ------------------------------------------------------------------ launch

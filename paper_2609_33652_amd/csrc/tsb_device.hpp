@@ -340,6 +340,13 @@ struct WaveTopList {
     }
 };
 
+// Orders a wave's LDS accesses before and after this point (for lanes that
+// read what other lanes of the same wave wrote).
+__device__ __forceinline__ void wave_lds_fence() {
+    __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+}
+
 __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int j) {
     const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), j, kWave);
     const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, j, kWave);

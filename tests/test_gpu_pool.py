@@ -214,6 +214,14 @@ def test_pool_batched_full_size(P):
     assert v.exact >= 15
 
 
+def test_pool_full_budget_many_internal_nodes():
+    # B = 1023 with K = 2: a 1024-node tree with several hundred internal
+    # nodes, beyond those whose Gumbel draws the replay computes ahead
+    cfg = W.config(2, R=2, V=4096, D=12, B=1023, K=2, T=1.0, name="deep")
+    p, rp, v = run_pool(cfg, 8, 4242, steps=2, name="deep")
+    assert rp.exact + rp.flagged == 4 and rp.exact >= 3
+
+
 def test_pool_large_budget_sampled():
     cfg = W.config(5)
     p, rp, v = run_pool(cfg, 64, W.replay_seed(5), steps=1, sets=1, requests=[0, 21, 63], gen_device="cuda",
