@@ -248,9 +248,63 @@ __global__ __launch_bounds__(kWave) void replay_merge(int B, int K, int T, tsb_t
     if (u >= n) return;
     const int m = tree.n_children[tb + u];
     if (m == 0) return;
+    const size_t o = (tb + u) * (size_t)T;
+    if (T <= kWave) {
+        // lane t holds tile t's count; the keys of all lists are gathered
+        // contiguously, rank-major (every tile's best key, then every second
+        // best, ...: each list is sorted, so the best keys come first), their
+        // indices placed through LDS. At most 64 keys: one per lane, sorted,
+        // and the first m are the children. More: in batches of 64 against
+        // the running list, a batch sorted first when more than m of its keys
+        // beat the list's smallest, so that at most m are inserted
+        __shared__ int s_idx[kWave * TSB_MAX_K];
+        const int ct = lane < T ? cc[o + lane] : 0;
+        int nv = 0;
+        for (int j = 0;; ++j) {
+            const uint64_t bj = __ballot(j < ct);
+            if (!bj) break;
+            if (j < ct) s_idx[nv + lanes_below_u64(bj)] = lane * TSB_MAX_K + j;
+            nv += __popcll(bj);
+        }
+        wave_lds_fence();
+        const uint64_t* cb = cand + o * TSB_MAX_K;
+        if (nv <= kWave) {
+            uint64_t v[1];
+            v[0] = lane < nv ? cb[s_idx[lane]] : 0ull;
+            wave_sort_desc<1>(v);
+            if (lane < m) node_tok[tb + tree.first_child[tb + u] + lane] = (int32_t)cand_id(v[0]);
+            return;
+        }
+        WaveTopList top;
+        top.init(m);
+        constexpr int kMergeBatches = 8;  // batches whose loads are in flight together
+        const int nb = (nv + kWave - 1) / kWave;
+        for (int b0 = 0; b0 < nb; b0 += kMergeBatches) {
+            uint64_t kb[kMergeBatches];
+#pragma unroll
+            for (int q = 0; q < kMergeBatches; ++q) {
+                const int e = (b0 + q) * kWave + lane;
+                kb[q] = e < nv ? cb[s_idx[e]] : 0ull;
+            }
+#pragma unroll
+            for (int q = 0; q < kMergeBatches; ++q) {
+                if (b0 + q >= nb) break;
+                const bool want = kb[q] > top.thr;
+                if (__popcll(__ballot(want)) > m) {
+                    uint64_t v[1];
+                    v[0] = want ? kb[q] : 0ull;
+                    wave_sort_desc<1>(v);
+                    top.offer(v[0], lane < m && v[0] != 0);
+                } else {
+                    top.offer(kb[q], want);
+                }
+            }
+        }
+        if (lane < m) node_tok[tb + tree.first_child[tb + u] + lane] = (int32_t)cand_id(top.v);
+        return;
+    }
     WaveTopList top;
     top.init(m);
-    const size_t o = (tb + u) * (size_t)T;
     // the tiles' lists (at most m entries each), all loads of a batch in flight together
     const int ne = T * m;
     for (int base = 0; base < ne; base += kWave) {

@@ -390,6 +390,11 @@ __device__ __forceinline__ void wave_sort_desc(uint64_t (&v)[NR]) {
     }
 }
 
+// Number of lanes below this one whose bit is set in b.
+__device__ __forceinline__ int lanes_below_u64(uint64_t b) {
+    return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(b >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)b, 0u));
+}
+
 // Exclusive prefix sum over the lanes of small non-negative counts
 // (< 2^NB), one ballot per bit; `total` receives the wave sum.
 template <int NB>
