@@ -3,9 +3,10 @@
 // m_u largest Gumbel keys a_{d,v} + G(u, v) over the whole vocabulary
 // (Gumbel-top-k = ordered sampling without replacement).
 //
-//   replay_prep   one workgroup: flat list of the parents of the batch
-//                 (request-major, BFS order, so a depth's parents are
-//                 contiguous).
+//   replay_threshold  one wave per parent: a lower bound of its m-th key
+//                 from its planning candidates; one more workgroup writes
+//                 the flat list of the parents of the batch (request-major,
+//                 BFS order, so a depth's parents are contiguous).
 //   replay_scan   one wave per (parent, vocabulary tile) item, dealt
 //                 grid-stride over a persistent grid (parents of one (request,
 //                 depth) are adjacent, so their tiles of draft row d meet in
@@ -35,43 +36,46 @@ constexpr int kTileGroups = kReplayTile / 4;  // groups of four tokens per tile
 constexpr int kScanWaves = kBlock / kWave;
 constexpr int kScanWorkgroups = 1536;  // resident at 6 waves per SIMD
 
-constexpr int kPrepThreads = 1024;
-
 // Flat list of every node with children, request-major, BFS order within a
 // request (so parents of one (request, depth) are contiguous): plist[i] =
-// r * (B + 1) + u; ptotal[0] = list length.
-__global__ __launch_bounds__(kPrepThreads) void replay_prep(int R, int B, tsb_tree tree, int* __restrict__ plist,
-                                                            int* __restrict__ ptotal) {
-    __shared__ int s_wave[kPrepThreads / kWave];
-    __shared__ int s_base;
-    const int tid = threadIdx.x;
-    const int lane = tid % kWave, wave = tid / kWave;
-    if (tid == 0) s_base = 0;
-    __syncthreads();
+// r * (B + 1) + u; ptotal[0] = list length. One workgroup of kBlock threads:
+// a thread takes eight consecutive nodes of a chunk (their loads in flight
+// together) and a block scan places them.
+__device__ void prep_list(int R, int B, const tsb_tree& tree, int* __restrict__ plist, int* __restrict__ ptotal) {
+    constexpr int kPer = 8;
+    __shared__ int s_w[kBlock / kWave];
+    const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
     const int total_nodes = R * (B + 1);
-    for (int base = 0; base < total_nodes; base += kPrepThreads) {
-        const int i = base + tid;
-        int flag = 0;
-        if (i < total_nodes) {
-            const int r = i / (B + 1), u = i % (B + 1);
-            flag = (u < tree.n_nodes[r] && tree.n_children[i] > 0) ? 1 : 0;
+    int out = 0;
+    for (int c0 = 0; c0 < total_nodes; c0 += kBlock * kPer) {
+        int flags = 0;  // bit k: node c0 + tid * kPer + k has children
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int i = c0 + tid * kPer + k;
+            if (i < total_nodes) {
+                const int r = i / (B + 1), u = i - r * (B + 1);
+                const int nn = tree.n_nodes[r], ch = tree.n_children[i];
+                if (u < nn && ch > 0) flags |= 1 << k;
+            }
         }
-        const uint64_t bal = __ballot(flag);
-        const int before = __popcll(bal & ((1ull << lane) - 1ull));
-        if (lane == 0) s_wave[wave] = __popcll(bal);
+        int wt;
+        const int off = wave_excl_scan<4>(__popc(flags), wt);
+        if (lane == 0) s_w[wave] = wt;
         __syncthreads();
-        int off = s_base;
-        for (int w = 0; w < wave; ++w) off += s_wave[w];
-        if (flag) plist[off + before] = i;
-        __syncthreads();
-        if (tid == 0) {
-            int t = 0;
-            for (int w = 0; w < kPrepThreads / kWave; ++w) t += s_wave[w];
-            s_base += t;
+        int o = out, tot = 0;
+        for (int w = 0; w < kBlock / kWave; ++w) {
+            const int x = s_w[w];
+            o += w < wave ? x : 0;
+            tot += x;
         }
-        __syncthreads();
+        o += off;
+#pragma unroll
+        for (int k = 0; k < kPer; ++k)
+            if ((flags >> k) & 1) plist[o++] = c0 + tid * kPer + k;
+        out += tot;
+        __syncthreads();  // s_w is rewritten by the next chunk
     }
-    if (tid == 0) ptotal[0] = s_base;
+    if (tid == 0) ptotal[0] = out;
 }
 
 __device__ __forceinline__ bool key_better(float ka, int ia, float kb, int ib) {
@@ -81,19 +85,25 @@ __device__ __forceinline__ bool key_better(float ka, int ia, float kb, int ib) {
 // Per parent u (one wave each): the m_u-th largest key among the keys of
 // its planning candidates, a lower bound of its m_u-th largest key over the
 // vocabulary (the same key arithmetic as the scan). -inf without pruning.
+// The grid's last workgroup builds the parent list instead.
 template <int DT>
 __global__ __launch_bounds__(kBlock) void replay_threshold(const void* __restrict__ draft, int R, int V, int D, int B,
                                                            int K, float invT, const int32_t* __restrict__ topk_tok,
                                                            tsb_tree tree, uint32_t k0, uint32_t k1, uint32_t step,
-                                                           int prune, float* __restrict__ thr) {
+                                                           int prune, float* __restrict__ thr,
+                                                           int* __restrict__ plist, int* __restrict__ ptotal) {
+    if (blockIdx.x == gridDim.x - 1) {
+        prep_list(R, B, tree, plist, ptotal);
+        return;
+    }
     const int lane = threadIdx.x % kWave;
     const int node = blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
     if (node >= R * (B + 1)) return;
     const int r = node / (B + 1), u = node % (B + 1);
-    if (u >= tree.n_nodes[r]) return;
-    const int m = tree.n_children[node];
-    if (m == 0) return;
-    const int d = tree.depth[node];
+    // the three loads are issued together (entries past n_nodes are read but
+    // not used)
+    const int nn = tree.n_nodes[r], m = tree.n_children[node], d = tree.depth[node];
+    if (u >= nn || m <= 0) return;
     const size_t rowbase = ((size_t)r * D + d) * (size_t)V;
     const int32_t* tk = topk_tok + ((size_t)r * D + d) * K;
     const float cd = load_logit<DT>(draft, rowbase + tk[0]) * invT;
@@ -330,16 +340,15 @@ hipError_t launch_replay(const tsb_config& c, float invT, const void* draft, con
     const bool vec = c.V % 4 == 0 && ((uintptr_t)draft & 15) == 0;
     hipError_t e = hook_before(TSB_KERNEL_REPLAY_SCAN, st);
     if (e != hipSuccess) return e;
-    replay_prep<<<1, kPrepThreads, 0, st>>>(c.R, c.B, tree, plist, ptotal);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
     float* thr = (float*)(ws + w.thr);
-    const int nthr = (c.R * (c.B + 1) + kBlock / kWave - 1) / (kBlock / kWave);
+    // one workgroup per four nodes, and one more for the parent list
+    const int nthr = (c.R * (c.B + 1) + kBlock / kWave - 1) / (kBlock / kWave) + 1;
     if (c.dtype == TSB_BF16)
         replay_threshold<TSB_BF16><<<nthr, kBlock, 0, st>>>(draft, c.R, c.V, c.D, c.B, c.K, invT, topk_tok, tree, k0,
-                                                            k1, step, prune, thr);
+                                                            k1, step, prune, thr, plist, ptotal);
     else
         replay_threshold<TSB_F32><<<nthr, kBlock, 0, st>>>(draft, c.R, c.V, c.D, c.B, c.K, invT, topk_tok, tree, k0,
-                                                           k1, step, prune, thr);
+                                                           k1, step, prune, thr, plist, ptotal);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // a persistent grid: the item count is only known on the device
     const long long max_items = (long long)c.R * c.B * g.T;
