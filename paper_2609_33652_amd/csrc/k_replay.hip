@@ -84,13 +84,15 @@ __device__ __forceinline__ bool key_better(float ka, int ia, float kb, int ib) {
 
 // Per parent u (one wave each): the m_u-th largest key among the keys of
 // its planning candidates, a lower bound of its m_u-th largest key over the
-// vocabulary (the same key arithmetic as the scan). -inf without pruning.
-// The grid's last workgroup builds the parent list instead.
+// vocabulary (the same key arithmetic as the scan; -inf without pruning),
+// stored with what the scan needs of the parent in one record
+// (c_d, thr, depth, m_u). The grid's last workgroup builds the parent list
+// instead.
 template <int DT>
 __global__ __launch_bounds__(kBlock) void replay_threshold(const void* __restrict__ draft, int R, int V, int D, int B,
                                                            int K, float invT, const int32_t* __restrict__ topk_tok,
                                                            tsb_tree tree, uint32_t k0, uint32_t k1, uint32_t step,
-                                                           int prune, float* __restrict__ thr,
+                                                           int prune, float4* __restrict__ rec,
                                                            int* __restrict__ plist, int* __restrict__ ptotal) {
     if (blockIdx.x == gridDim.x - 1) {
         prep_list(R, B, tree, plist, ptotal);
@@ -126,7 +128,9 @@ __global__ __launch_bounds__(kBlock) void replay_threshold(const void* __restric
         const int tt = __shfl(tj, j, kWave);
         above += key_better(kk, tt, kj, tj) ? 1 : 0;
     }
-    if (lane < K && above == m - 1) thr[node] = prune ? kj : -INFINITY;
+    const uint64_t at = __ballot(lane < K && above == m - 1);  // exactly one lane
+    const float thr = prune ? lane_f32(kj, (int)__ffsll((unsigned long long)at) - 1) : -INFINITY;
+    if (lane == 0) rec[node] = make_float4(cd, thr, __int_as_float(d), __int_as_float(m));
 }
 
 // Four logits of the draft row as b = fl32(a - c_d); positions at or past
@@ -158,7 +162,7 @@ template <int DT, bool VEC>
 __global__ __launch_bounds__(kBlock) void replay_scan(const void* __restrict__ draft, int V, int D, int B, int K,
                                                       int T, float invT, const int32_t* __restrict__ topk_tok,
                                                       tsb_tree tree, const int* __restrict__ plist,
-                                                      const int* __restrict__ ptotal, const float* __restrict__ thr_in,
+                                                      const int* __restrict__ ptotal, const float4* __restrict__ rec,
                                                       uint32_t k0, uint32_t k1, uint32_t step,
                                                       uint64_t* __restrict__ out_cand, int* __restrict__ out_cnt) {
     __shared__ int s_queue[kScanWaves][kTileGroups];  // surviving groups, per wave
@@ -170,13 +174,14 @@ __global__ __launch_bounds__(kBlock) void replay_scan(const void* __restrict__ d
         const int pi = (int)(it / T);
         const int t = (int)(it - (long long)pi * T);
         const int node = plist[pi];
+        const float4 pr = rec[node];  // (c_d, thr, depth, m) of the parent
         const int r = node / (B + 1);
         const int u = node - r * (B + 1);
-        const int d = tree.depth[node];
-        const int m = tree.n_children[node];
+        const int d = __float_as_int(pr.z);
+        const int m = __float_as_int(pr.w);
         const size_t rowbase = ((size_t)r * D + d) * (size_t)V;
-        const float cd = load_logit<DT>(draft, rowbase + topk_tok[((size_t)r * D + d) * K]) * invT;
-        const float thr = thr_in[node];
+        const float cd = pr.x;
+        const float thr = pr.y;
         const float bound = thr - kGumbelMaxBound;
         const int t0 = t * kReplayTile;
         const int tn = min(kReplayTile, V - t0);
@@ -340,15 +345,15 @@ hipError_t launch_replay(const tsb_config& c, float invT, const void* draft, con
     const bool vec = c.V % 4 == 0 && ((uintptr_t)draft & 15) == 0;
     hipError_t e = hook_before(TSB_KERNEL_REPLAY_SCAN, st);
     if (e != hipSuccess) return e;
-    float* thr = (float*)(ws + w.thr);
+    float4* rec = (float4*)(ws + w.thr);
     // one workgroup per four nodes, and one more for the parent list
     const int nthr = (c.R * (c.B + 1) + kBlock / kWave - 1) / (kBlock / kWave) + 1;
     if (c.dtype == TSB_BF16)
         replay_threshold<TSB_BF16><<<nthr, kBlock, 0, st>>>(draft, c.R, c.V, c.D, c.B, c.K, invT, topk_tok, tree, k0,
-                                                            k1, step, prune, thr, plist, ptotal);
+                                                            k1, step, prune, rec, plist, ptotal);
     else
         replay_threshold<TSB_F32><<<nthr, kBlock, 0, st>>>(draft, c.R, c.V, c.D, c.B, c.K, invT, topk_tok, tree, k0,
-                                                           k1, step, prune, thr, plist, ptotal);
+                                                           k1, step, prune, rec, plist, ptotal);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     // a persistent grid: the item count is only known on the device
     const long long max_items = (long long)c.R * c.B * g.T;
@@ -356,17 +361,17 @@ hipError_t launch_replay(const tsb_config& c, float invT, const void* draft, con
     if (c.dtype == TSB_BF16) {
         if (vec)
             replay_scan<TSB_BF16, true><<<grid, kBlock, 0, st>>>(draft, c.V, c.D, c.B, c.K, g.T, invT, topk_tok, tree,
-                                                                 plist, ptotal, thr, k0, k1, step, cand, cc);
+                                                                 plist, ptotal, rec, k0, k1, step, cand, cc);
         else
             replay_scan<TSB_BF16, false><<<grid, kBlock, 0, st>>>(draft, c.V, c.D, c.B, c.K, g.T, invT, topk_tok,
-                                                                  tree, plist, ptotal, thr, k0, k1, step, cand, cc);
+                                                                  tree, plist, ptotal, rec, k0, k1, step, cand, cc);
     } else {
         if (vec)
             replay_scan<TSB_F32, true><<<grid, kBlock, 0, st>>>(draft, c.V, c.D, c.B, c.K, g.T, invT, topk_tok, tree,
-                                                                plist, ptotal, thr, k0, k1, step, cand, cc);
+                                                                plist, ptotal, rec, k0, k1, step, cand, cc);
         else
             replay_scan<TSB_F32, false><<<grid, kBlock, 0, st>>>(draft, c.V, c.D, c.B, c.K, g.T, invT, topk_tok, tree,
-                                                                 plist, ptotal, thr, k0, k1, step, cand, cc);
+                                                                 plist, ptotal, rec, k0, k1, step, cand, cc);
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -65,7 +65,7 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 struct PlanWs {  // row statistics partials
     size_t pm, ps, pk, pf, total;
 };
-struct ReplayWs {  // per (parent, tile) best keys, flat parent list, thresholds
+struct ReplayWs {  // per (parent, tile) best keys, flat parent list, per-parent records
     size_t cand, cnt, plist, ptotal, thr, total;
 };
 struct VerifyWs {  // target partials
@@ -111,7 +111,7 @@ inline ReplayWs replay_ws(const tsb_config& c) {
     w.cnt = o; o = align256(o + slots * sizeof(int32_t));
     w.plist = o; o = align256(o + (size_t)c.R * (c.B + 1) * sizeof(int32_t));
     w.ptotal = o; o = align256(o + sizeof(int32_t));
-    w.thr = o; o = align256(o + (size_t)c.R * (c.B + 1) * sizeof(float));
+    w.thr = o; o = align256(o + (size_t)c.R * (c.B + 1) * 4 * sizeof(float));  // per node (c_d, thr, d, m)
     w.total = o;
     return w;
 }
