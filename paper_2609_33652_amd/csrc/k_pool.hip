@@ -54,7 +54,7 @@ __device__ __forceinline__ size_t trans_row(int r, int D, int d, int slot, int P
 // ------------------------------------------------------------------ lists
 // Candidate list of one context from z (lane j < P holds z_j, -inf beyond):
 // binary64 log-sum-exp over the pool (lanes summed in a fixed order), lp,
-// and the rank of each slot under (lp desc, slot asc).
+// and the slots in (lp desc, slot asc) order by a sort of the 64 keys.
 __device__ void build_list(float z, int P, int K, const double* et, uint64_t* out, int* nfin_out) {
     const int lane = lane_id();
     const float m = wave_max(z);
@@ -65,10 +65,13 @@ __device__ void build_list(float z, int P, int K, const double* et, uint64_t* ou
         const float L32 = (float)L;
         const float lp = (float)((double)z - (double)L32);
         const bool valid = lane < P && lp > -INFINITY;
-        const uint64_t key = valid ? ((uint64_t)ordered_bits(lp) << 32) | (uint32_t)(~lane) : 0ull;
-        int rank = 0;
-        for (int k = 0; k < kWave; ++k) rank += lane_u64(key, k) > key ? 1 : 0;
-        if (valid && rank < K) out[rank] = pack_entry(lp, lane);
+        uint64_t v[1];
+        v[0] = valid ? ((uint64_t)ordered_bits(lp) << 32) | (uint32_t)(~lane) : 0ull;
+        wave_sort_desc<1>(v);
+        // lane k holds the k-th slot; its lp bits are taken from that slot's lane
+        const int slot = (int)(~(uint32_t)v[0]) & (kWave - 1);
+        const float lps = __shfl(lp, slot, kWave);
+        if (lane < K && v[0] != 0ull) out[lane] = pack_entry(lps, slot);
         nf = __popcll(__ballot(valid));
     }
     if (lane == 0) *nfin_out = nf < K ? nf : K;
@@ -85,6 +88,14 @@ __global__ __launch_bounds__(kPoolThreads) void pool_lists(int D, int S, int P, 
     __shared__ double s_exp[kExpTable];
     __shared__ float s_a[kPoolMax];
     exp64_table_init(s_exp);
+    // the transition rows of this wave's lists are fetched before the merge
+    constexpr int kListsPerWave = (kPoolMax + kPoolWaves - 1) / kPoolWaves;
+    float cv[kListsPerWave];
+#pragma unroll
+    for (int q = 0; q < kListsPerWave; ++q) {
+        const int i = wave + q * kPoolWaves;
+        cv[q] = (d > 0 && i < P && lane < P) ? trans[trans_row(r, D, d, i, P) + lane] : 0.0f;
+    }
 
     if (wave == 0) {
         // merge of the row's segment lists into the pool (keys are distinct;
@@ -105,6 +116,15 @@ __global__ __launch_bounds__(kPoolThreads) void pool_lists(int D, int S, int P, 
                 const int rj = __builtin_amdgcn_readlane(rank, j);
                 if (kj != 0ull && rj == lane) best = kj;
             }
+        } else if (n <= 2 * kWave) {
+            uint64_t v[2];
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+                const int i = q * kWave + lane;
+                v[q] = i < n ? pk[o * P + i] : 0ull;
+            }
+            wave_sort_desc<2>(v);
+            best = lane < P ? v[0] : 0ull;
         } else if (n <= 4 * kWave) {
             // a bitonic sort of up to 256 keys: the pool is the first P
             uint64_t v[4];
@@ -144,10 +164,13 @@ __global__ __launch_bounds__(kPoolThreads) void pool_lists(int D, int S, int P, 
         return;
     }
     int tbad = 0;
-    for (int i = wave; i < P; i += kPoolWaves) {
+#pragma unroll
+    for (int q = 0; q < kListsPerWave; ++q) {
+        const int i = wave + q * kPoolWaves;
+        if (i >= P) break;
         float z = -INFINITY;
         if (lane < P) {
-            const float c = trans[trans_row(r, D, d, i, P) + lane];
+            const float c = cv[q];
             tbad |= !isfinite(c);
             z = corrected_logit(s_a[lane], c, invT);
         }
