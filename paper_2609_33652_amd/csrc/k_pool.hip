@@ -317,7 +317,10 @@ __global__ __launch_bounds__(kPlanPoolThreads) void pool_plan(int D, int P, int 
 
     // ---- threshold search (uniform control flow across the workgroup), as
     // in the vocabulary-wide planner
-    const int cap = 2 * (B + 1);
+    // a count succeeds when it lands in [B + 1, cap]: a narrow window keeps
+    // every count short (measured best at 1.25 (B + 1) over the workloads),
+    // at the price of a round more now and then
+    const int cap = (5 * (B + 1) + 3) / 4;
     const int ns = min(kPlanPoolWaves, kPoolPlanBuf / cap);
     double hi_m = (Dp > 0 && sh.lnf[0] > 0) ? (double)sh.llp[0] : -INFINITY;  // the best node's score
     int hi_cnt = 0;
