@@ -166,6 +166,14 @@ def test_large_budget_full_size_sampled():
     assert t.exact >= 4
 
 
+def test_vocab_beyond_64_replay_tiles():
+    # V = 300001: 74 replay tiles of 4096 (more than one per lane in the merge,
+    # which then inserts key by key) with a ragged last tile, scalar loads
+    cfg = W.config(2, R=2, V=300001, D=4, B=24, K=6, T=1.0, name="wide")
+    t = run_case(cfg, 31337, steps=2, name="wide")
+    assert t.exact >= 3 and t.flagged <= 1
+
+
 def test_pruning_does_not_change_replay():
     cfg = W.config(2, R=2, V=32000, D=6, B=40, K=8, name="prune")
     seed = 99
