@@ -1149,14 +1149,27 @@ __global__ __launch_bounds__(kPlanThreads) void plan_ep(int D, int S, int K, int
                 }
                 f = nl;
             } else {
-                // the W-th largest score of the layer (with multiplicity)
-                WaveTopList tl;
-                tl.init(W);
-                for (int base = lb; base < le; base += kWave) {
-                    const int i = base + lane;
-                    tl.offer(i < le ? ordered_bits64(sh.score[i]) : 0ull, i < le);
+                // the W-th largest score of the layer (with multiplicity): a
+                // sort of the layer's keys when it holds at most 128 nodes
+                uint64_t tk;
+                if (nl <= 2 * kWave && W <= kWave) {
+                    uint64_t v[2];
+#pragma unroll
+                    for (int q = 0; q < 2; ++q) {
+                        const int i = lb + q * kWave + lane;
+                        v[q] = i < le ? ordered_bits64(sh.score[i]) : 0ull;
+                    }
+                    wave_sort_desc<2>(v);
+                    tk = lane_u64(v[0], W - 1);
+                } else {  // inserts (measured no slower than a 256-key sort)
+                    WaveTopList tl;
+                    tl.init(W);
+                    for (int base = lb; base < le; base += kWave) {
+                        const int i = base + lane;
+                        tl.offer(i < le ? ordered_bits64(sh.score[i]) : 0ull, i < le);
+                    }
+                    tk = lane_u64(tl.v, W - 1);
                 }
-                const uint64_t tk = lane_u64(tl.v, W - 1);
                 int above = 0;
                 for (int base = lb; base < le; base += kWave) {
                     const int i = base + lane;
