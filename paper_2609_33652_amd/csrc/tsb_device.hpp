@@ -352,9 +352,22 @@ __device__ __forceinline__ void wave_lds_fence() {
     __builtin_amdgcn_wave_barrier();
 }
 
+// The value of lane (lane ^ j). Distances 1 and 2 are DPP quad permutations
+// ([1, 0, 3, 2] and [2, 3, 0, 1]: no LDS round trip); the others go through
+// ds_bpermute. j is a compile-time constant wherever the sorts unroll.
 __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int j) {
-    const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), j, kWave);
-    const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, j, kWave);
+    const int h = (int)(uint32_t)(v >> 32), l = (int)(uint32_t)v;
+    uint32_t hi, lo;
+    if (j == 1) {
+        hi = (uint32_t)__builtin_amdgcn_update_dpp(h, h, 0xB1, 0xF, 0xF, false);
+        lo = (uint32_t)__builtin_amdgcn_update_dpp(l, l, 0xB1, 0xF, 0xF, false);
+    } else if (j == 2) {
+        hi = (uint32_t)__builtin_amdgcn_update_dpp(h, h, 0x4E, 0xF, 0xF, false);
+        lo = (uint32_t)__builtin_amdgcn_update_dpp(l, l, 0x4E, 0xF, 0xF, false);
+    } else {
+        hi = (uint32_t)__shfl_xor(h, j, kWave);
+        lo = (uint32_t)__shfl_xor(l, j, kWave);
+    }
     return ((uint64_t)hi << 32) | lo;
 }
 
