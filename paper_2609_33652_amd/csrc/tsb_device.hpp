@@ -353,22 +353,28 @@ __device__ __forceinline__ void wave_lds_fence() {
 }
 
 // The value of lane (lane ^ j). Distances 1 and 2 are DPP quad permutations
-// ([1, 0, 3, 2] and [2, 3, 0, 1]: no LDS round trip); the others go through
-// ds_bpermute. j is a compile-time constant wherever the sorts unroll.
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int j) {
-    const int h = (int)(uint32_t)(v >> 32), l = (int)(uint32_t)v;
-    uint32_t hi, lo;
-    if (j == 1) {
-        hi = (uint32_t)__builtin_amdgcn_update_dpp(h, h, 0xB1, 0xF, 0xF, false);
-        lo = (uint32_t)__builtin_amdgcn_update_dpp(l, l, 0xB1, 0xF, 0xF, false);
-    } else if (j == 2) {
-        hi = (uint32_t)__builtin_amdgcn_update_dpp(h, h, 0x4E, 0xF, 0xF, false);
-        lo = (uint32_t)__builtin_amdgcn_update_dpp(l, l, 0x4E, 0xF, 0xF, false);
-    } else {
-        hi = (uint32_t)__shfl_xor(h, j, kWave);
-        lo = (uint32_t)__shfl_xor(l, j, kWave);
+// ([1, 0, 3, 2] and [2, 3, 0, 1]); 16 and 32 are the row and half swaps of
+// v_permlane16_swap / v_permlane32_swap applied to two copies of the value
+// (the first result holds the partner's value in the odd rows / upper half,
+// the second in the even rows / lower half); none of them goes through LDS.
+// 4 and 8 use ds_bpermute. j is a compile-time constant wherever the sorts
+// unroll.
+__device__ __forceinline__ uint32_t xor_lane_u32(uint32_t x, int j) {
+    if (j == 1) return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0xB1, 0xF, 0xF, false);
+    if (j == 2) return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x4E, 0xF, 0xF, false);
+    if (j == 16) {
+        const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+        return (lane_id() & 16) ? r[0] : r[1];
     }
-    return ((uint64_t)hi << 32) | lo;
+    if (j == 32) {
+        const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+        return (lane_id() & 32) ? r[0] : r[1];
+    }
+    return (uint32_t)__shfl_xor((int)x, j, kWave);
+}
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int j) {
+    return ((uint64_t)xor_lane_u32((uint32_t)(v >> 32), j) << 32) | xor_lane_u32((uint32_t)v, j);
 }
 
 // Sorts the NR * 64 keys held NR per lane in descending order (element
