@@ -32,7 +32,7 @@ POOL_KERNELS = ("pool_partials", "pool_lists", "pool_plan", "pool_replay", "targ
 # HBM bytes per launch of target_partials at the batched workload from the
 # FETCH_SIZE / WRITE_SIZE counter passes (KiB, scaled by a plain copy of known
 # size: FETCH x2.0, WRITE x1.0), valid for the kernel source they were taken on
-TARGET_TRAFFIC = {"config": 4, "source_sha256_16": "d1240d8a06bfe313", "fetch_kib": 309823.6, "write_kib": 266.8,
+TARGET_TRAFFIC = {"config": 4, "source_sha256_16": "d1240d8a06bfe313", "fetch_kib": 309857.9, "write_kib": 266.8,
                   "fetch_scale": 2.0, "write_scale": 1.0}
 
 
