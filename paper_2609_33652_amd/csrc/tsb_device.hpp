@@ -357,11 +357,15 @@ __device__ __forceinline__ void wave_lds_fence() {
 // v_permlane16_swap / v_permlane32_swap applied to two copies of the value
 // (the first result holds the partner's value in the odd rows / upper half,
 // the second in the even rows / lower half); none of them goes through LDS.
-// 4 and 8 use ds_bpermute. j is a compile-time constant wherever the sorts
+// 4 and 8 use ds_swizzle in bit-mask mode (no address operand); other
+// distances ds_bpermute. j is a compile-time constant wherever the sorts
 // unroll.
 __device__ __forceinline__ uint32_t xor_lane_u32(uint32_t x, int j) {
     if (j == 1) return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0xB1, 0xF, 0xF, false);
     if (j == 2) return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x4E, 0xF, 0xF, false);
+    // bit-mask swizzle within 32 lanes: and 0x1F, or 0, xor j
+    if (j == 4) return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x1F | (4 << 10));
+    if (j == 8) return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x1F | (8 << 10));
     if (j == 16) {
         const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
         return (lane_id() & 16) ? r[0] : r[1];
