@@ -170,19 +170,56 @@ __device__ __forceinline__ float cand_value(uint64_t k) { return from_ordered_bi
 // ---------------------------------------------------------------- wave ops
 __device__ __forceinline__ int lane_id() { return (int)__lane_id(); }
 
+// The value of lane (lane ^ j). Distances 1 and 2 are DPP quad permutations
+// ([1, 0, 3, 2] and [2, 3, 0, 1]); 16 and 32 are the row and half swaps of
+// v_permlane16_swap / v_permlane32_swap applied to two copies of the value
+// (the first result holds the partner's value in the odd rows / upper half,
+// the second in the even rows / lower half); none of them goes through LDS.
+// 4 and 8 use ds_swizzle in bit-mask mode (no address operand); other
+// distances ds_bpermute. j is a compile-time constant wherever the sorts
+// unroll.
+__device__ __forceinline__ uint32_t xor_lane_u32(uint32_t x, int j) {
+    if (j == 1) return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0xB1, 0xF, 0xF, false);
+    if (j == 2) return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x4E, 0xF, 0xF, false);
+    // bit-mask swizzle within 32 lanes: and 0x1F, or 0, xor j
+    if (j == 4) return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x1F | (4 << 10));
+    if (j == 8) return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x1F | (8 << 10));
+    if (j == 16) {
+        const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+        return (lane_id() & 16) ? r[0] : r[1];
+    }
+    if (j == 32) {
+        const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+        return (lane_id() & 32) ? r[0] : r[1];
+    }
+    return (uint32_t)__shfl_xor((int)x, j, kWave);
+}
+
+// As xor_lane_u32 for the butterfly reductions, with distances 16 and 32 on
+// ds_bpermute (the permlane swaps measured slower there).
+__device__ __forceinline__ uint32_t xor_lane_red_u32(uint32_t x, int j) {
+    return (j >= 16) ? (uint32_t)__shfl_xor((int)x, j, kWave) : xor_lane_u32(x, j);
+}
+
+// Butterfly reductions over the wave (partners lane ^ 32, ^ 16, ..., ^ 1:
+// every lane ends with the same value, added in the same order).
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __uint_as_float(xor_lane_red_u32(__float_as_uint(v), o)));
     return v;
 }
 __device__ __forceinline__ double wave_sum(double v) {
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+    for (int o = 32; o > 0; o >>= 1) {
+        const uint64_t u = (uint64_t)__double_as_longlong(v);
+        const uint64_t p = ((uint64_t)xor_lane_red_u32((uint32_t)(u >> 32), o) << 32) | xor_lane_red_u32((uint32_t)u, o);
+        v += __longlong_as_double((long long)p);
+    }
     return v;
 }
 __device__ __forceinline__ int wave_or(int v) {
 #pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v |= __shfl_xor(v, o, kWave);
+    for (int o = 32; o > 0; o >>= 1) v |= (int)xor_lane_red_u32((uint32_t)v, o);
     return v;
 }
 // Whole-wave one-lane shifts through DPP (lane i receives lane i-1, resp.
@@ -350,31 +387,6 @@ struct WaveTopList {
 __device__ __forceinline__ void wave_lds_fence() {
     __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
     __builtin_amdgcn_wave_barrier();
-}
-
-// The value of lane (lane ^ j). Distances 1 and 2 are DPP quad permutations
-// ([1, 0, 3, 2] and [2, 3, 0, 1]); 16 and 32 are the row and half swaps of
-// v_permlane16_swap / v_permlane32_swap applied to two copies of the value
-// (the first result holds the partner's value in the odd rows / upper half,
-// the second in the even rows / lower half); none of them goes through LDS.
-// 4 and 8 use ds_swizzle in bit-mask mode (no address operand); other
-// distances ds_bpermute. j is a compile-time constant wherever the sorts
-// unroll.
-__device__ __forceinline__ uint32_t xor_lane_u32(uint32_t x, int j) {
-    if (j == 1) return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0xB1, 0xF, 0xF, false);
-    if (j == 2) return (uint32_t)__builtin_amdgcn_update_dpp((int)x, (int)x, 0x4E, 0xF, 0xF, false);
-    // bit-mask swizzle within 32 lanes: and 0x1F, or 0, xor j
-    if (j == 4) return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x1F | (4 << 10));
-    if (j == 8) return (uint32_t)__builtin_amdgcn_ds_swizzle((int)x, 0x1F | (8 << 10));
-    if (j == 16) {
-        const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
-        return (lane_id() & 16) ? r[0] : r[1];
-    }
-    if (j == 32) {
-        const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
-        return (lane_id() & 32) ? r[0] : r[1];
-    }
-    return (uint32_t)__shfl_xor((int)x, j, kWave);
 }
 
 __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int j) {
