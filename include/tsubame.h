@@ -34,13 +34,22 @@
  *     non-zero status means nothing was enqueued (except TSB_E_HIP, where a
  *     launch failed part-way; tsb_last_error() has the detail).
  *   - Scratch memory comes from the caller's `workspace` of at least
- *     tsb_workspace_bytes(cfg) bytes, 256-byte aligned. One workspace may be
- *     reused by successive calls on one stream; calls that overlap in time
- *     need separate workspaces. Zero-fill a workspace once, before its first
- *     use, and again after any request reported TSB_REQ_WALK_TIMEOUT: its
- *     first part holds state that verification keeps between calls (a
- *     sequence number per request and tagged exchange slots), at the same
- *     place for every entry point of one cfg.
+ *     tsb_workspace_bytes(cfg) bytes, 256-byte aligned. Its content before a
+ *     call does not matter (it need not be initialised) and nothing in it is
+ *     kept between calls: the entry points are stateless. One workspace may
+ *     be reused by successive calls on one stream; calls that overlap in time
+ *     need separate workspaces.
+ *   - Topologies and node tokens passed in by the caller are checked on the
+ *     device before any entry becomes an address. A node with m > 0
+ *     children is well formed when m <= TSB_MAX_K, its children occupy
+ *     [first_child, first_child + m) with node < first_child and
+ *     first_child + m <= n_nodes, and its depth is in [0, D); n_nodes must
+ *     lie in [1, B + 1]; node tokens must lie in [0, V). Violations never
+ *     fault: verification flags the request (TSB_REQ_BAD_TREE, n_acc =
+ *     bonus = -1; a token outside [0, V): TSB_REQ_BAD_TOKEN, with the outputs
+ *     each verifier states) and replay skips the parent (its child slots are
+ *     not written). Candidate tokens given to tsb_replay that are outside
+ *     [0, V) or repeated switch the pruning of their parents off.
  *   - Results are a deterministic function of (inputs, cfg.seed, step): the
  *     randomness is Philox4x32-10 (Salmon et al., SC'11) keyed by
  *     (seed, step, request, node, draw), independent of launch shapes.
@@ -90,7 +99,10 @@ enum {
     TSB_REQ_DEGENERATE_RESIDUAL = 2, /* empty residual after a rejection: bonus drawn from p at that node */
     TSB_REQ_BUDGET_SHORT = 4,        /* fewer than B nodes exist: n_nodes < B + 1 */
     TSB_REQ_WALK_TIMEOUT = 8,        /* a cross-workgroup wait in verification hit its spin limit */
-    TSB_REQ_BAD_TOKEN = 16           /* tsb_pool_verify: a visited node token is not in its position's pool */
+    TSB_REQ_BAD_TOKEN = 16,          /* a visited node token is outside [0, V) (tsb_pool_verify: outside its
+                                        position's pool) */
+    TSB_REQ_BAD_TREE = 32            /* a visited node's topology entries are out of range (see the conventions
+                                        above), or n_nodes is outside [1, B + 1] */
 };
 
 /* cfg.flags */
@@ -181,7 +193,8 @@ tsb_status tsb_replay(const tsb_config* cfg, const void* draft, const int32_t* t
 
 /* Verification (eq. (1); Appendix A). target: [R, B+1, V] logits, row i is
  * the target's next-token logits at tree node i (rows >= n_nodes unread).
- * draft_lse as written by tsb_plan. */
+ * draft_lse as written by tsb_plan. A visited node token outside [0, V)
+ * stops the walk with TSB_REQ_BAD_TOKEN and n_acc = bonus = -1. */
 tsb_status tsb_verify(const tsb_config* cfg, const void* draft, const double* draft_lse,
                       const void* target, const tsb_tree* tree, const int32_t* node_tok,
                       uint32_t step, const tsb_verdict* out, void* workspace,
@@ -250,7 +263,7 @@ tsb_status tsb_step_first(const tsb_config* cfg, const void* draft, const void* 
  *     (lp desc, slot asc) with lp > -inf, at most K; child rank k of u is
  *     its k-th candidate.
  *   P must satisfy K <= P <= min(64, V). Workspaces of these entry points are
- *   tsb_pool_workspace_bytes(cfg, P) bytes (the zero-fill rule above holds).
+ *   tsb_pool_workspace_bytes(cfg, P) bytes (stateless, as above).
  */
 size_t tsb_pool_workspace_bytes(const tsb_config* cfg, int32_t P);
 

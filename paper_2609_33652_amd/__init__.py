@@ -26,6 +26,7 @@ REQ_DEGENERATE_RESIDUAL = 2
 REQ_BUDGET_SHORT = 4
 REQ_WALK_TIMEOUT = 8
 REQ_BAD_TOKEN = 16
+REQ_BAD_TREE = 32
 POOL_MAX = 64
 FLAG_NO_PRUNE = 1
 MAX_D, MAX_K, MAX_B, TRACE_MAX = 64, 32, 1023, 256
@@ -197,7 +198,7 @@ class Round:
             nb = max(nb, nbp)
             self.pool_tok = torch.empty(R, D, self.pool, dtype=i32, device=dev)
             self.plan_tok = torch.empty(R, B + 1, dtype=i32, device=dev)
-        self.ws = torch.zeros(nb + 256, dtype=torch.uint8, device=dev)  # zero-filled once (naive exchange tags)
+        self.ws = torch.empty(nb + 256, dtype=torch.uint8, device=dev)  # no initial content needed
         off = (-self.ws.data_ptr()) % 256
         self.ws_ptr = ctypes.c_void_p(self.ws.data_ptr() + off)
         self.ws_bytes = nb

@@ -21,6 +21,7 @@
 //                  finiteness) through the tagged slots of the request.
 #include <math.h>
 
+#include <algorithm>
 #include <atomic>
 
 #include "tsb_device.hpp"
@@ -57,7 +58,7 @@ struct NaiveArgs {
     tsb_tree tree;
     const int32_t* node_tok;
     tsb_verdict out;
-    XRegion X;  // exchange slots and per-request sequence numbers
+    XRegion X;  // exchange slots of the requests
     int V, D, B, r0;
     float invT;
     uint32_t k0, k1, step;
@@ -193,10 +194,10 @@ __device__ SliceBest reduce_slice(const SliceBest& s) {
 // the G slots (lane h: slots h and h + 64), reduces them in a fixed order
 // (key desc, token asc; flags or-ed) and hands the result to the other waves.
 // Slot words: key, token << 32 | has << 9 | bad << 8.
-__device__ SliceBest naive_round(const NaiveArgs& A, int r, int g, int G, uint32_t seq, uint32_t e,
-                                 const SliceBest& mine, int* timeout) {
+__device__ SliceBest naive_round(const NaiveArgs& A, int r, int g, int G, uint32_t e, const SliceBest& mine,
+                                 int* timeout) {
     const uint64_t w[2] = {mine.key, xpack_u32(mine.tok) | ((uint64_t)mine.has << 9) | ((uint64_t)mine.bad << 8)};
-    xpublish<2>(A.X, r, g, seq, e, w);
+    xpublish<2>(A.X, r, g, e, w);
     __shared__ SliceBest s_res;
     __shared__ int s_to;
     if (threadIdx.x < kWave) {
@@ -209,7 +210,7 @@ __device__ SliceBest naive_round(const NaiveArgs& A, int r, int g, int G, uint32
             const int h = lane + half * kWave;
             if (h < G) {
                 uint64_t q[2];
-                if (!xpoll<2>(A.X, r, h, seq, e, q)) to = 1;
+                if (!xpoll<2>(A.X, r, h, e, q)) to = 1;
                 const uint64_t kk = q[0] & ~kTagMask;
                 const uint32_t tt = xunpack_u32(q[1]);
                 bad |= (int)((q[1] >> 8) & 1ull);
@@ -256,7 +257,9 @@ __global__ __launch_bounds__(kNaiveThreads) void verify_naive(NaiveArgs A) {
     const size_t tb = (size_t)r * B1;
     const bool lead = (g == 0 && tid == 0);
     int* status_p = A.out.req_status + r;
-    const int n = A.tree.n_nodes[r];
+    const int n_raw = A.tree.n_nodes[r];
+    const bool count_ok = tree_count_ok(n_raw, A.B);
+    const int n = count_ok ? n_raw : 0;
 
     // vocabulary slice (start a multiple of 4; an empty slice is [0, 0))
     const int span = ((A.V + G - 1) / G + 3) & ~3;
@@ -267,15 +270,14 @@ __global__ __launch_bounds__(kNaiveThreads) void verify_naive(NaiveArgs A) {
     const bool single = ns <= kNaiveBatchTokens;  // the slice is one batch: its loads are issued at once
 
     const bool plan_bad = (*status_p & TSB_REQ_NONFINITE) != 0;
-    int nacc = 0, bonus = -1, add_status = 0;
-    if (!plan_bad && n >= 1 && n <= B1) {
+    int nacc = 0, bonus = -1, add_status = count_ok ? 0 : TSB_REQ_BAD_TREE;
+    if (!plan_bad && count_ok) {
         RngKey key;
         key.k0 = A.k0;
         key.k1 = A.k1;
         key.request = (uint32_t)r;
         key.step = A.step;
         int timeout = 0;
-        const uint32_t seq = A.X.seqs[r];
         Raw4<DT> cur[kNaiveBatch];
         if (single) load_batch<DT, VEC>(A.target, tb * (size_t)A.V, v0, ns, 0, cur);
         // the request's tree (children and node tokens) in LDS
@@ -298,22 +300,27 @@ __global__ __launch_bounds__(kNaiveThreads) void verify_naive(NaiveArgs A) {
                     score_batch<DT>(cur, v0, ns, base, A.invT, key, (uint32_t)u, mine);
                 }
             }
+            // children of u (a well-formed node: m <= TSB_MAX_K, inside the
+            // tree after u, and u not deeper than D - 1 on the accepted path)
             const int m = s_nc[u];
             const int fc = s_fc[u];
-            const bool may_descend = m > 0 && fc > u && fc + m <= n && nacc < A.D;
-            const SliceBest all = naive_round(A, r, g, G, seq, e, reduce_slice(mine), &timeout);
+            const bool well_formed = m == 0 || (m > 0 && m <= TSB_MAX_K && fc > u && fc <= n - m && nacc < A.D);
+            const SliceBest all = naive_round(A, r, g, G, e, reduce_slice(mine), &timeout);
             if (all.bad || !all.has) {
                 add_status |= TSB_REQ_NONFINITE;
                 break;
             }
+            if (!well_formed) {
+                add_status |= TSB_REQ_BAD_TREE;
+                break;
+            }
             const int y = (int)all.tok;
             int match = -1;
-            if (may_descend)
-                for (int j = 0; j < m; ++j)
-                    if (s_tok[fc + j] == y) {
-                        match = fc + j;
-                        break;
-                    }
+            for (int j = 0; j < m; ++j)
+                if (s_tok[fc + j] == y) {
+                    match = fc + j;
+                    break;
+                }
             if (match < 0) {
                 bonus = y;
                 break;
@@ -326,13 +333,12 @@ __global__ __launch_bounds__(kNaiveThreads) void verify_naive(NaiveArgs A) {
             u = match;
             if (single) load_batch<DT, VEC>(A.target, ((size_t)r * B1 + u) * (size_t)A.V, v0, ns, 0, cur);
         }
-        xfinish(A.X, r, g, G, seq, e + 1);
         if (timeout) add_status |= TSB_REQ_WALK_TIMEOUT;
-    } else {
+    } else if (plan_bad) {
         add_status |= TSB_REQ_NONFINITE;
     }
     if (lead) {
-        const bool bad = (add_status & TSB_REQ_NONFINITE) != 0;
+        const bool bad = (add_status & (TSB_REQ_NONFINITE | TSB_REQ_BAD_TREE)) != 0;
         if (bad) nacc = 0;
         for (int i = nacc; i < A.D; ++i) {
             A.out.acc_node[(size_t)r * A.D + i] = -1;
@@ -342,6 +348,12 @@ __global__ __launch_bounds__(kNaiveThreads) void verify_naive(NaiveArgs A) {
         A.out.bonus[r] = bad ? -1 : bonus;
         *status_p |= add_status;
     }
+}
+
+// Zeroes the exchange slots of the requests before a walk that no stream
+// kernel precedes.
+__global__ __launch_bounds__(kBlock) void xchg_clear(XRegion X, int R) {
+    xclear(X, R, (size_t)blockIdx.x * kBlock + threadIdx.x, (size_t)gridDim.x * kBlock);
 }
 
 // ------------------------------------------------------------------ launch
@@ -385,9 +397,7 @@ hipError_t launch_verify_naive(const tsb_config& c, float invT, const void* targ
     A.tree = tree;
     A.node_tok = node_tok;
     A.out = out;
-    const XchgWs xw = xchg_ws(c);
-    A.X.seqs = (uint32_t*)(ws + xw.seq);
-    A.X.slots = (uint64_t*)(ws + xw.slots);
+    A.X.slots = (uint64_t*)(ws + xchg_ws(c).slots);
     A.V = c.V;
     A.D = c.D;
     A.B = c.B;
@@ -415,12 +425,17 @@ hipError_t launch_verify_naive(const tsb_config& c, float invT, const void* targ
     if (G < 1) G = 1;
     const int chunk = cap / G;
 
+    const int nclear = (int)std::min<size_t>(1024, (xwords(c.R) + kBlock - 1) / kBlock);
+    xchg_clear<<<nclear, kBlock, 0, st>>>(A.X, c.R);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = hook_before(TSB_KERNEL_VERIFY_NAIVE, st)) != hipSuccess) return e;
+    // cooperative launches: every workgroup of a launch is resident at once
+    // (or the launch fails), so the exchanges of a request complete
     for (int r0 = 0; r0 < c.R; r0 += chunk) {
         A.r0 = r0;
         const int rc = min(chunk, c.R - r0);
         void* args[] = {&A};
-        e = hipLaunchKernel(fn, dim3(G, rc), dim3(kNaiveThreads), args, 0, st);
+        e = hipLaunchCooperativeKernel(fn, dim3(G, rc), dim3(kNaiveThreads), args, 0, st);
         if (e != hipSuccess) return e;
     }
     return hook_after(TSB_KERNEL_VERIFY_NAIVE, st);

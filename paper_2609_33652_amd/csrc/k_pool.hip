@@ -618,7 +618,8 @@ __global__ __launch_bounds__(kPoolThreads) void pool_replay(int D, int V, int P,
     const int r = blockIdx.x;
     const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
     const size_t tb = (size_t)r * (B + 1);
-    const int n = tree.n_nodes[r];
+    const int nn = tree.n_nodes[r];
+    const int n = tree_count_ok(nn, B) ? nn : 0;  // a request with an unusable count is not replayed
     // transition matrices of the request (with D = 1 there are none: the
     // fetches then read pool_tok[0] and their values are never used)
     const bool has_t = D > 1;
@@ -637,9 +638,11 @@ __global__ __launch_bounds__(kPoolThreads) void pool_replay(int D, int V, int P,
         s_ntok[i] = -1;
         s_slot[i] = 0;  // every node below the root gets its slot from its parent's layer
     }
-    // internal nodes in BFS order (their depths are contiguous from 0)
-    const int nc = tid < n ? tree.n_children[tb + tid] : 0;
-    const bool internal = nc > 0;
+    // internal nodes in BFS order (their depths are contiguous from 0); a
+    // malformed node (entries out of range, see tree_node) is not replayed
+    TreeNode nd{0, 0, 0, false};
+    if (tid < n) nd = tree_node(tree, tb, tid, n, D);
+    const bool internal = nd.ok && nd.m > 0;
     const uint64_t bal = __ballot(internal);
     const int below = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
     if (lane == 0) s_wcnt[wave] = __popcll(bal);
@@ -651,10 +654,9 @@ __global__ __launch_bounds__(kPoolThreads) void pool_replay(int D, int V, int P,
         n_int += c;
     }
     if (internal) {
-        const int dep = tree.depth[tb + tid];
-        s_int[q] = (uint16_t)(tid | (dep << 10));
-        s_fc[q] = (int16_t)tree.first_child[tb + tid];
-        s_m[q] = (int16_t)nc;
+        s_int[q] = (uint16_t)(tid | (nd.d << 10));
+        s_fc[q] = (int16_t)nd.fc;
+        s_m[q] = (int16_t)nd.m;
     }
     for (int d = tid; d < TSB_MAX_D + 2; d += kPoolThreads) s_ilvl[d] = n_int;
     __syncthreads();

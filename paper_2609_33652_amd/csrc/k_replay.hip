@@ -36,12 +36,25 @@ constexpr int kTileGroups = kReplayTile / 4;  // groups of four tokens per tile
 constexpr int kScanWaves = kBlock / kWave;
 constexpr int kScanWorkgroups = 1536;  // resident at 6 waves per SIMD
 
-// Flat list of every node with children, request-major, BFS order within a
-// request (so parents of one (request, depth) are contiguous): plist[i] =
+// A parent that replay fills: a well-formed node of the caller's topology
+// (entries in range, see tree_node) with 1 <= m <= K children. Malformed
+// parents, and every node of a request whose n_nodes lies outside
+// [1, B + 1], are skipped: their child slots are not written.
+__device__ __forceinline__ bool replay_parent(const tsb_tree& tree, int r, int u, int B, int D, int K, TreeNode* nd) {
+    const int nn = tree.n_nodes[r];
+    const int n = tree_count_ok(nn, B) ? nn : 0;
+    if (u >= n) return false;
+    *nd = tree_node(tree, (size_t)r * (B + 1), u, n, D);
+    return nd->ok && nd->m > 0 && nd->m <= K;
+}
+
+// Flat list of every parent, request-major, BFS order within a request (so
+// parents of one (request, depth) are contiguous): plist[i] =
 // r * (B + 1) + u; ptotal[0] = list length. One workgroup of kBlock threads:
 // a thread takes eight consecutive nodes of a chunk (their loads in flight
 // together) and a block scan places them.
-__device__ void prep_list(int R, int B, const tsb_tree& tree, int* __restrict__ plist, int* __restrict__ ptotal) {
+__device__ void prep_list(int R, int B, int D, int K, const tsb_tree& tree, int* __restrict__ plist,
+                          int* __restrict__ ptotal) {
     constexpr int kPer = 8;
     __shared__ int s_w[kBlock / kWave];
     const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
@@ -54,8 +67,8 @@ __device__ void prep_list(int R, int B, const tsb_tree& tree, int* __restrict__ 
             const int i = c0 + tid * kPer + k;
             if (i < total_nodes) {
                 const int r = i / (B + 1), u = i - r * (B + 1);
-                const int nn = tree.n_nodes[r], ch = tree.n_children[i];
-                if (u < nn && ch > 0) flags |= 1 << k;
+                TreeNode nd;
+                if (replay_parent(tree, r, u, B, D, K, &nd)) flags |= 1 << k;
             }
         }
         int wt;
@@ -95,20 +108,23 @@ __global__ __launch_bounds__(kBlock) void replay_threshold(const void* __restric
                                                            int prune, float4* __restrict__ rec,
                                                            int* __restrict__ plist, int* __restrict__ ptotal) {
     if (blockIdx.x == gridDim.x - 1) {
-        prep_list(R, B, tree, plist, ptotal);
+        prep_list(R, B, D, K, tree, plist, ptotal);
         return;
     }
     const int lane = threadIdx.x % kWave;
     const int node = blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
     if (node >= R * (B + 1)) return;
     const int r = node / (B + 1), u = node % (B + 1);
-    // the three loads are issued together (entries past n_nodes are read but
-    // not used)
-    const int nn = tree.n_nodes[r], m = tree.n_children[node], d = tree.depth[node];
-    if (u >= nn || m <= 0) return;
+    TreeNode nd;
+    if (!replay_parent(tree, r, u, B, D, K, &nd)) return;
+    const int m = nd.m, d = nd.d;
     const size_t rowbase = ((size_t)r * D + d) * (size_t)V;
     const int32_t* tk = topk_tok + ((size_t)r * D + d) * K;
-    const float cd = load_logit<DT>(draft, rowbase + tk[0]) * invT;
+    // candidate tokens are checked before they become addresses; the
+    // threshold is a lower bound of the m-th key only over K distinct tokens
+    // of the row, so an out-of-range or repeated candidate turns pruning off
+    const int t0 = tk[0];
+    const float cd = (t0 >= 0 && t0 < V) ? load_logit<DT>(draft, rowbase + t0) * invT : 0.f;
     RngKey key;
     key.k0 = k0;
     key.k1 = k1;
@@ -116,9 +132,11 @@ __global__ __launch_bounds__(kBlock) void replay_threshold(const void* __restric
     key.step = step;
     float kj = -INFINITY;
     int tj = 0x7FFFFFFF;
+    bool tok_ok = true;
     if (lane < K) {
         tj = tk[lane];
-        const float a = load_logit<DT>(draft, rowbase + tj) * invT;
+        tok_ok = tj >= 0 && tj < V;
+        const float a = tok_ok ? load_logit<DT>(draft, rowbase + tj) * invT : -INFINITY;
         const float bj = a - cd;
         kj = bj + gumbel_f32(rng_word(key, (uint32_t)u, kStreamReplay, (uint32_t)tj));
     }
@@ -127,9 +145,12 @@ __global__ __launch_bounds__(kBlock) void replay_threshold(const void* __restric
         const float kk = __shfl(kj, j, kWave);
         const int tt = __shfl(tj, j, kWave);
         above += key_better(kk, tt, kj, tj) ? 1 : 0;
+        tok_ok = tok_ok && !(lane < K && j < lane && tt == tj);
     }
-    const uint64_t at = __ballot(lane < K && above == m - 1);  // exactly one lane
-    const float thr = prune ? lane_f32(kj, (int)__ffsll((unsigned long long)at) - 1) : -INFINITY;
+    const bool cands_ok = __ballot(!tok_ok) == 0ull && t0 >= 0 && t0 < V;
+    const uint64_t at = __ballot(lane < K && above == m - 1);  // one lane for distinct finite keys
+    const float thr = (prune && cands_ok && at != 0ull) ? lane_f32(kj, (int)__ffsll((unsigned long long)at) - 1)
+                                                        : -INFINITY;
     if (lane == 0) rec[node] = make_float4(cd, thr, __int_as_float(d), __int_as_float(m));
 }
 
@@ -249,20 +270,22 @@ __global__ __launch_bounds__(kBlock) void replay_scan(const void* __restrict__ d
     }
 }
 
-__global__ __launch_bounds__(kWave) void replay_merge(int B, int K, int T, tsb_tree tree,
+__global__ __launch_bounds__(kWave) void replay_merge(int B, int D, int K, int T, tsb_tree tree,
                                                       const uint64_t* __restrict__ cand, const int* __restrict__ cc,
                                                       int32_t* __restrict__ node_tok) {
     const int r = blockIdx.y;
     const int u = blockIdx.x;
     const int lane = threadIdx.x;
     const size_t tb = (size_t)r * (B + 1);
-    const int n = tree.n_nodes[r];
+    const int nn = tree.n_nodes[r];
+    const int n = tree_count_ok(nn, B) ? nn : 0;
     if (u == 0 || u >= n) {
         if (lane == 0) node_tok[tb + u] = -1;
     }
-    if (u >= n) return;
-    const int m = tree.n_children[tb + u];
-    if (m == 0) return;
+    TreeNode nd;
+    if (!replay_parent(tree, r, u, B, D, K, &nd)) return;
+    const int m = nd.m;
+    const int fc = nd.fc;
     const size_t o = (tb + u) * (size_t)T;
     if (T <= kWave) {
         // lane t holds tile t's count; the keys of all lists are gathered
@@ -287,7 +310,7 @@ __global__ __launch_bounds__(kWave) void replay_merge(int B, int K, int T, tsb_t
             uint64_t v[1];
             v[0] = lane < nv ? cb[s_idx[lane]] : 0ull;
             wave_sort_desc<1>(v);
-            if (lane < m) node_tok[tb + tree.first_child[tb + u] + lane] = (int32_t)cand_id(v[0]);
+            if (lane < m) node_tok[tb + fc + lane] = (int32_t)cand_id(v[0]);
             return;
         }
         WaveTopList top;
@@ -315,7 +338,7 @@ __global__ __launch_bounds__(kWave) void replay_merge(int B, int K, int T, tsb_t
                 }
             }
         }
-        if (lane < m) node_tok[tb + tree.first_child[tb + u] + lane] = (int32_t)cand_id(top.v);
+        if (lane < m) node_tok[tb + fc + lane] = (int32_t)cand_id(top.v);
         return;
     }
     WaveTopList top;
@@ -329,7 +352,7 @@ __global__ __launch_bounds__(kWave) void replay_merge(int B, int K, int T, tsb_t
         if (i < ne && j < cc[o + tt]) k = cand[(o + tt) * TSB_MAX_K + j];
         top.offer(k, k != 0);
     }
-    if (lane < m) node_tok[tb + tree.first_child[tb + u] + lane] = (int32_t)cand_id(top.v);
+    if (lane < m) node_tok[tb + fc + lane] = (int32_t)cand_id(top.v);
 }
 
 hipError_t launch_replay(const tsb_config& c, float invT, const void* draft, const int32_t* topk_tok,
@@ -377,7 +400,7 @@ hipError_t launch_replay(const tsb_config& c, float invT, const void* draft, con
     if (e != hipSuccess) return e;
     if ((e = hook_after(TSB_KERNEL_REPLAY_SCAN, st)) != hipSuccess) return e;
     if ((e = hook_before(TSB_KERNEL_REPLAY_MERGE, st)) != hipSuccess) return e;
-    replay_merge<<<dim3(c.B + 1, c.R), kWave, 0, st>>>(c.B, c.K, g.T, tree, cand, cc, node_tok);
+    replay_merge<<<dim3(c.B + 1, c.R), kWave, 0, st>>>(c.B, c.D, c.K, g.T, tree, cand, cc, node_tok);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     return hook_after(TSB_KERNEL_REPLAY_MERGE, st);

@@ -47,7 +47,8 @@ namespace tsb {
 // logits cut into equal chunks, one per workgroup (all resident at once, so
 // no workgroup trails the others). A chunk covers pieces of one or two rows;
 // piece k of row t (its k-th workgroup) is partial slot k of the row, and
-// the row's first workgroup marks the slots no piece uses as empty.
+// the row's first workgroup marks the slots no piece uses as empty. The grid
+// also zeroes the exchange slots of the walk launched after it.
 template <int DT, bool VEC>
 __device__ __forceinline__ void stream_piece(const void* __restrict__ target, size_t rowbase, int lo, int hi,
                                              float c, float& m_out, double& sum_out) {
@@ -113,9 +114,11 @@ __global__ __launch_bounds__(kBlock) void target_partials(const void* __restrict
                                                           long long chunk, int P, float invT,
                                                           const int32_t* __restrict__ n_nodes,
                                                           float* __restrict__ tm, double* __restrict__ ts,
-                                                          int* __restrict__ tf) {
+                                                          int* __restrict__ tf, XRegion X, int R) {
     const int g = blockIdx.x;
     const int tid = threadIdx.x;
+    // the walk that follows starts from cleared exchange slots
+    xclear(X, R, (size_t)g * kBlock + tid, (size_t)gridDim.x * kBlock);
     const long long N = (long long)nrows * V;
     const long long e0 = (long long)g * chunk;
     if (e0 >= N) return;
@@ -181,7 +184,7 @@ struct WalkArgs {
     const float* tm;
     const double* ts;
     const int* tf;
-    XRegion X;  // exchange slots and per-request sequence numbers
+    XRegion X;  // exchange slots of the requests
     int V, D, B, S4, r0;
     float invT;
     uint32_t k0, k1, step;
@@ -425,7 +428,6 @@ constexpr int kExVals = 4;
 struct Exchange {
     const WalkArgs* A;
     int r, g, G;
-    uint32_t seq;
     uint32_t nb;  // rounds run
     int timeout;
 
@@ -440,7 +442,7 @@ struct Exchange {
             w[NV] = xpack_u32(ordered_bits(bk));
             w[NW - 1] = xpack_u32((uint32_t)bi);
         }
-        xpublish<NW>(A->X, r, g, seq, nb, w);
+        xpublish<NW>(A->X, r, g, nb, w);
         // wave 0 polls the G slots (lane h: slots h and h + 64), reduces them
         // in a fixed order and hands the result to the others
         __shared__ double s_tot[kExVals];
@@ -458,7 +460,7 @@ struct Exchange {
                 const int h = lane + half * kWave;
                 if (h < G) {
                     uint64_t q[NW];
-                    if (!xpoll<NW>(A->X, r, h, seq, nb, q)) to = 1;
+                    if (!xpoll<NW>(A->X, r, h, nb, q)) to = 1;
 #pragma unroll
                     for (int i = 0; i < NV; ++i) v[i] += xunpack_f64(q[i]);
                     if (BEST) {
@@ -634,8 +636,8 @@ __device__ void fill_pass(const WalkArgs& A, bool vec, const WalkSlice& S, bool 
 
 // End of a walk, for every workgroup of the request: every target row of
 // the tree must be finite (workgroup 0 decides); outputs of the request.
-__device__ void walk_tail(const WalkArgs& A, int r, int g, int G, int n, bool draft_bad, int nacc, int bonus_out,
-                          int add_status, int tcount) {
+__device__ void walk_tail(const WalkArgs& A, int r, int g, int G, int n, bool draft_bad, bool invalid, int nacc,
+                          int bonus_out, int add_status, int tcount) {
     __shared__ int s_bad;
     const int tid = threadIdx.x;
     const int B1 = A.B + 1;
@@ -675,12 +677,15 @@ __device__ void walk_tail(const WalkArgs& A, int r, int g, int G, int n, bool dr
                 nacc = 0;
                 bonus_out = -1;
                 add_status = (add_status & ~(TSB_REQ_DEGENERATE_RESIDUAL | TSB_REQ_WALK_TIMEOUT)) | TSB_REQ_NONFINITE;
+            } else if (invalid) {  // a malformed tree or token: outputs defined, without meaning
+                nacc = 0;
+                bonus_out = -1;
             }
             for (int i = nacc; i < A.D; ++i) {
                 A.out.acc_node[(size_t)r * A.D + i] = -1;
                 A.out.acc_tok[(size_t)r * A.D + i] = -1;
             }
-            A.out.n_acc[r] = bad ? -1 : nacc;
+            A.out.n_acc[r] = (bad || invalid) ? -1 : nacc;
             A.out.bonus[r] = bonus_out;
             *status_p |= add_status;
             if (A.out.trace)
@@ -697,6 +702,7 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
     __shared__ int s_tok[TSB_MAX_K];
     __shared__ float s_xd[TSB_MAX_K], s_xt[TSB_MAX_K];
     __shared__ double s_u[TSB_MAX_K];
+    __shared__ int s_badtok;
     const int g = blockIdx.x;
     const int G = gridDim.x;
     const int r = A.r0 + blockIdx.y;
@@ -705,8 +711,11 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
     const size_t tb = (size_t)r * B1;
     const bool vec = VEC;
     int* status_p = A.out.req_status + r;
-    const int n = A.tree.n_nodes[r];
+    const int n_raw = A.tree.n_nodes[r];
+    const bool count_ok = tree_count_ok(n_raw, A.B);
+    const int n = count_ok ? n_raw : 0;
     const bool lead = (g == 0 && tid == 0);
+    if (tid == 0) s_badtok = 0;
     exp64_table_init(s_exp);
 
     // vocabulary slice (start a multiple of 4; an empty slice is [0, 0))
@@ -726,20 +735,27 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
     int tcount = 0;
     double* const trace = (lead && A.out.trace) ? A.out.trace + (size_t)r * TSB_TRACE_MAX * 4 : nullptr;
 
-    int bonus_out = -1, add_status = 0, nacc = 0;
-    if (!draft_bad) {
+    int bonus_out = -1, add_status = count_ok ? 0 : TSB_REQ_BAD_TREE, nacc = 0;
+    bool invalid = !count_ok;
+    if (!draft_bad && count_ok) {
         RngKey key;
         key.k0 = A.k0;
         key.k1 = A.k1;
         key.request = (uint32_t)r;
         key.step = A.step;
-        Exchange X{&A, r, g, G, A.X.seqs[r], 0u, 0};
+        Exchange X{&A, r, g, G, 0u, 0};
         int u = 0;
         while (true) {
-            const int m = A.tree.n_children[tb + u];
-            const int d = A.tree.depth[tb + u];
+            // every workgroup reads the same entries, so all take the same exit
+            const TreeNode nd = tree_node(A.tree, tb, u, n, A.D);
+            if (!nd.ok || (nd.m > 0 && nacc >= A.D)) {
+                add_status |= TSB_REQ_BAD_TREE;
+                invalid = true;
+                break;
+            }
+            const int m = nd.m, d = nd.d;
             const size_t trow = ((size_t)r * B1 + u) * (size_t)A.V;
-            const size_t drow = ((size_t)r * A.D + (d < A.D ? d : 0)) * (size_t)A.V;
+            const size_t drow = ((size_t)r * A.D + (m > 0 ? d : 0)) * (size_t)A.V;
             int tbad;
             const double L0 = target_lse(A, r, u, &tbad);
             if (m == 0) {  // accepted leaf: bonus from p_u
@@ -751,16 +767,24 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
                 break;
             }
             const double Ld = A.draft_lse[(size_t)r * A.D + d];
-            // children of u: tokens, their logits and the uniforms, fetched together
-            const int fc = A.tree.first_child[tb + u];
+            // children of u: tokens, their logits and the uniforms, fetched
+            // together; a token outside [0, V) is never used as an address
+            const int fc = nd.fc;
             if (tid < m) {
                 const int y = A.node_tok[tb + fc + tid];
+                const bool yok = y >= 0 && y < A.V;
                 s_tok[tid] = y;
-                s_xd[tid] = load_logit<DT>(A.draft, drow + y) * A.invT;
-                s_xt[tid] = load_logit<DT>(A.target, trow + y) * A.invT;
+                s_xd[tid] = yok ? load_logit<DT>(A.draft, drow + y) * A.invT : 0.f;
+                s_xt[tid] = yok ? load_logit<DT>(A.target, trow + y) * A.invT : 0.f;
                 s_u[tid] = u24d(rng_word(key, (uint32_t)(fc + tid), kStreamAccept, 0u));
+                if (!yok) s_badtok = 1;
             }
             __syncthreads();
+            if (s_badtok) {
+                add_status |= TSB_REQ_BAD_TOKEN;
+                invalid = true;
+                break;
+            }
 
             bool exact = false;
             double Lt = L0, inv = 1.0;
@@ -893,11 +917,10 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
             }
             break;
         }
-        if (X.nb > 0) xfinish(A.X, r, g, G, X.seq, X.nb);
         if (X.timeout) add_status |= TSB_REQ_WALK_TIMEOUT;
     }
 
-    walk_tail(A, r, g, G, n, draft_bad, nacc, bonus_out, add_status, tcount);
+    walk_tail(A, r, g, G, n, draft_bad, invalid, nacc, bonus_out, add_status, tcount);
 }
 
 
@@ -993,7 +1016,9 @@ __global__ __launch_bounds__(kWalkThreads) void verify_pool_walk(WalkArgs A) {
     const int P = A.P;
     const size_t tb = (size_t)r * B1;
     const bool vec = VEC;
-    const int n = A.tree.n_nodes[r];
+    const int n_raw = A.tree.n_nodes[r];
+    const bool count_ok = tree_count_ok(n_raw, A.B);
+    const int n = count_ok ? n_raw : 0;
     const bool lead = (g == 0 && tid == 0);
     exp64_table_init(s_exp);
     if (tid == 0) s_badtok = 0;
@@ -1014,18 +1039,25 @@ __global__ __launch_bounds__(kWalkThreads) void verify_pool_walk(WalkArgs A) {
     int tcount = 0;
     double* const trace = (lead && A.out.trace) ? A.out.trace + (size_t)r * TSB_TRACE_MAX * 4 : nullptr;
 
-    int bonus_out = -1, add_status = 0, nacc = 0;
-    if (!draft_bad) {
+    int bonus_out = -1, add_status = count_ok ? 0 : TSB_REQ_BAD_TREE, nacc = 0;
+    bool invalid = !count_ok;
+    if (!draft_bad && count_ok) {
         RngKey key;
         key.k0 = A.k0;
         key.k1 = A.k1;
         key.request = (uint32_t)r;
         key.step = A.step;
-        Exchange X{&A, r, g, G, A.X.seqs[r], 0u, 0};
+        Exchange X{&A, r, g, G, 0u, 0};
         int u = 0, su = 0;
         while (true) {
-            const int m = A.tree.n_children[tb + u];
-            const int d = A.tree.depth[tb + u];
+            // every workgroup reads the same entries, so all take the same exit
+            const TreeNode nd = tree_node(A.tree, tb, u, n, A.D);
+            if (!nd.ok || (nd.m > 0 && nacc >= A.D)) {
+                add_status |= TSB_REQ_BAD_TREE;
+                invalid = true;
+                break;
+            }
+            const int m = nd.m, d = nd.d;
             const size_t trow = ((size_t)r * B1 + u) * (size_t)A.V;
             int tbad;
             const double L0 = target_lse(A, r, u, &tbad);
@@ -1066,7 +1098,7 @@ __global__ __launch_bounds__(kWalkThreads) void verify_pool_walk(WalkArgs A) {
                     s_pat[lane] = at;
                 }
             }
-            const int fc = A.tree.first_child[tb + u];
+            const int fc = nd.fc;
             if (tid < m) {
                 const int y = A.node_tok[tb + fc + tid];
                 s_tok[tid] = y;
@@ -1205,12 +1237,11 @@ __global__ __launch_bounds__(kWalkThreads) void verify_pool_walk(WalkArgs A) {
             }
             break;
         }
-        if (X.nb > 0) xfinish(A.X, r, g, G, X.seq, X.nb);
         if (X.timeout) add_status |= TSB_REQ_WALK_TIMEOUT;
         __syncthreads();
         if (s_badtok) add_status |= TSB_REQ_BAD_TOKEN;
     }
-    walk_tail(A, r, g, G, n, draft_bad, nacc, bonus_out, add_status, tcount);
+    walk_tail(A, r, g, G, n, draft_bad, invalid, nacc, bonus_out, add_status, tcount);
 }
 
 // ------------------------------------------------------------------ launch
@@ -1250,26 +1281,16 @@ static hipError_t launch_target_partials(const tsb_config& c, float invT, const 
     float* tm = (float*)(ws + w.tm);
     double* ts = (double*)(ws + w.ts);
     int* tf = (int*)(ws + w.tf);
+    XRegion X;
+    X.slots = (uint64_t*)(ws + xchg_ws(c).slots);
     const bool vec8 = (c.dtype == TSB_BF16) ? (c.V % 8 == 0 && ((uintptr_t)target & 15) == 0)
                                             : (c.V % 4 == 0 && ((uintptr_t)target & 15) == 0);
     const int nrows = c.R * (c.B + 1);
     hipError_t e = hook_before(TSB_KERNEL_TARGET_PARTIALS, st);
     if (e != hipSuccess) return e;
-    if (c.dtype == TSB_BF16) {
-        if (vec8)
-            target_partials<TSB_BF16, true><<<g.G4, kBlock, 0, st>>>(target, c.V, c.B, nrows, g.chunk4, g.S4, invT,
-                                                                     tree.n_nodes, tm, ts, tf);
-        else
-            target_partials<TSB_BF16, false><<<g.G4, kBlock, 0, st>>>(target, c.V, c.B, nrows, g.chunk4, g.S4, invT,
-                                                                      tree.n_nodes, tm, ts, tf);
-    } else {
-        if (vec8)
-            target_partials<TSB_F32, true><<<g.G4, kBlock, 0, st>>>(target, c.V, c.B, nrows, g.chunk4, g.S4, invT,
-                                                                    tree.n_nodes, tm, ts, tf);
-        else
-            target_partials<TSB_F32, false><<<g.G4, kBlock, 0, st>>>(target, c.V, c.B, nrows, g.chunk4, g.S4, invT,
-                                                                     tree.n_nodes, tm, ts, tf);
-    }
+    auto fn = c.dtype == TSB_BF16 ? (vec8 ? target_partials<TSB_BF16, true> : target_partials<TSB_BF16, false>)
+                                  : (vec8 ? target_partials<TSB_F32, true> : target_partials<TSB_F32, false>);
+    fn<<<g.G4, kBlock, 0, st>>>(target, c.V, c.B, nrows, g.chunk4, g.S4, invT, tree.n_nodes, tm, ts, tf, X, c.R);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     return hook_after(TSB_KERNEL_TARGET_PARTIALS, st);
@@ -1291,9 +1312,7 @@ static WalkArgs walk_args(const tsb_config& c, float invT, const void* draft, co
     A.tm = (const float*)(ws + w.tm);
     A.ts = (const double*)(ws + w.ts);
     A.tf = (const int*)(ws + w.tf);
-    const XchgWs xw = xchg_ws(c);
-    A.X.seqs = (uint32_t*)(ws + xw.seq);
-    A.X.slots = (uint64_t*)(ws + xw.slots);
+    A.X.slots = (uint64_t*)(ws + xchg_ws(c).slots);
     A.V = c.V;
     A.D = c.D;
     A.B = c.B;
@@ -1310,7 +1329,9 @@ static WalkArgs walk_args(const tsb_config& c, float invT, const void* draft, co
 }
 
 // Launches of a walk grid (G workgroups per request) within the resident
-// capacity, in order of requests.
+// capacity, in order of requests. The launches are cooperative: every
+// workgroup of a launch is resident at once (or the launch fails), so the
+// exchanges of a request always complete.
 static hipError_t launch_walk_grid(const void* fn, WalkArgs& A, int R, int G0, int cap, size_t lds, hipStream_t st) {
     int G = G0;
     if (G * R > cap) G = cap / R > 0 ? cap / R : 1;
@@ -1319,7 +1340,7 @@ static hipError_t launch_walk_grid(const void* fn, WalkArgs& A, int R, int G0, i
         A.r0 = r0;
         const int rc = min(chunk, R - r0);
         void* args[] = {&A};
-        const hipError_t e = hipLaunchKernel(fn, dim3(G, rc), dim3(kWalkThreads), args, lds, st);
+        const hipError_t e = hipLaunchCooperativeKernel(fn, dim3(G, rc), dim3(kWalkThreads), args, lds, st);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;

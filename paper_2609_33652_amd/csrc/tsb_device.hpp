@@ -167,6 +167,31 @@ __device__ __forceinline__ uint64_t cand_key(float x, uint32_t id) {
 __device__ __forceinline__ uint32_t cand_id(uint64_t k) { return ~(uint32_t)k; }
 __device__ __forceinline__ float cand_value(uint64_t k) { return from_ordered_bits((uint32_t)(k >> 32)); }
 
+// ---------------------------------------------------------------- caller trees
+// One node of a caller-supplied topology, checked before any of its entries
+// becomes an address. A node with m > 0 children is well formed when
+// m <= TSB_MAX_K, its children occupy [fc, fc + m) with u < fc and
+// fc + m <= n (so every descent moves to a larger index and stays inside the
+// tree) and its depth d lies in [0, D) (its children read draft row d). A
+// node with m == 0 is a leaf whatever its other entries hold.
+struct TreeNode {
+    int m, fc, d;
+    bool ok;
+};
+
+__device__ __forceinline__ TreeNode tree_node(const tsb_tree& t, size_t tb, int u, int n, int D) {
+    TreeNode v;
+    v.m = t.n_children[tb + u];
+    v.fc = t.first_child[tb + u];
+    v.d = t.depth[tb + u];
+    v.ok = v.m == 0 || (v.m > 0 && v.m <= TSB_MAX_K && v.fc > u && v.fc <= n - v.m && v.d >= 0 && v.d < D);
+    if (!v.ok || v.m == 0) v.m = 0;
+    return v;
+}
+
+// n_nodes of a caller-supplied topology is usable when it lies in [1, B + 1].
+__device__ __forceinline__ bool tree_count_ok(int n, int B) { return n >= 1 && n <= B + 1; }
+
 // ---------------------------------------------------------------- wave ops
 __device__ __forceinline__ int lane_id() { return (int)__lane_id(); }
 

@@ -72,18 +72,17 @@ struct VerifyWs {  // target partials
     size_t tm, ts, tf, total;
 };
 
-// The region that verification keeps across calls comes first (no stage
-// writes it): a sequence number per request and the exchange slots of the
-// workgroups of a request, [R][2][kWalkGroupsMax][8] 64-bit words. Every
-// stage's scratch starts after it, so all entry points agree on where it is.
+// The exchange slots of the walks come first: [R][2][kWalkGroupsMax][8]
+// 64-bit words that the workgroups of a request poll (cleared by the kernel
+// enqueued right before each walk; nothing is kept between calls). Every
+// stage's scratch starts after them.
 struct XchgWs {
-    size_t seq, slots, total;
+    size_t slots, total;
 };
 
 inline XchgWs xchg_ws(const tsb_config& c) {
     XchgWs w;
     size_t o = 0;
-    w.seq = o; o = align256(o + (size_t)c.R * sizeof(uint32_t));
     w.slots = o; o = align256(o + (size_t)c.R * 2 * kWalkGroupsMax * 8 * sizeof(uint64_t));
     w.total = o;
     return w;

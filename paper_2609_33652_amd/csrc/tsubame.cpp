@@ -350,6 +350,6 @@ const char* tsb_status_string(tsb_status s) {
 
 const char* tsb_last_error(void) { return g_last_error; }
 
-int32_t tsb_version(void) { return 104; }
+int32_t tsb_version(void) { return 200; }
 
 }  // extern "C"

@@ -33,7 +33,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(tsb.EXPORTS)
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.tsb_version() == 104
+    assert lib.tsb_version() == 200
 
 
 def _cfg(**kw):
@@ -185,3 +185,4 @@ def test_pool_entry_points_validate(lib):
                              ctypes.byref(v), FAKE, need - 256, None) == 5
     assert lib.tsb_pool_step(ctypes.byref(_cfg(dtype=5)), 16, FAKE, FAKE, FAKE, 0, FAKE, ctypes.byref(t), FAKE,
                              ctypes.byref(v), FAKE, need, None) == 3
+
