@@ -1,10 +1,14 @@
 """GPU parity of the HIP path against the CPU oracle, through the C ABI.
 
 Every case feeds the same seeded bytes to both sides and compares stage by
-stage (plan, then replay on the same tree, then verify on the same tree and
-tokens), with the rules of tests/parity_util.py. Full-size workloads are
-checked on sampled requests and parents. tsb_step must equal the staged
-calls bit for bit.
+stage (plan; replay on the HIP path's topology; verification on its topology
+and node tokens), decision by decision, with the rules of
+tests/parity_util.py. The workloads are checked on every request of every
+step run: all steps of the tiny and small workloads, 160 steps of the
+Qwen-vocabulary one, 16 steps of the batched one and 4 of the large-budget
+one (the oracle runs in a process pool over the host's cores). tsb_step must
+equal the staged calls bit for bit. Each case allows at most one flagged
+near-tie; the tallies are printed at the end of the run.
 """
 import sys
 
@@ -12,13 +16,19 @@ import numpy as np
 import pytest
 import torch
 
+import oracle_worker
 import workloads as W
 from oracle import replay as oreplay, step as ostep
 from oracle.rowstats import STATUS_NONFINITE, inv_temperature, scaled
 import paper_2609_33652_amd as tsb
-from parity_util import (Tally, compare_plan, compare_replay, compare_verify, make_round, to_np, tree_dict_np)
+from parity_util import (check_tally, compare_plan, compare_request, make_round, run_rounds,
+                         tree_dict_np)
+from tally import Tally
 
 pytestmark = pytest.mark.gpu
+
+STEP_KEYS = ("draft_lse", "topk_tok", "topk_lp", "parent", "depth", "rank", "n_children", "first_child", "score",
+             "n_nodes", "node_tok", "n_acc", "acc_node", "acc_tok", "bonus", "req_status", "target_lse", "trace")
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -33,145 +43,72 @@ def say(*a):
     sys.stdout.flush()
 
 
-def _depths(pls, R, B):
-    dep = torch.zeros(R, B + 1, dtype=torch.int64)
-    for r, pl in enumerate(pls):
-        if pl is not None:
-            t = pl["tree"]
-            dep[r, : t["n_nodes"]] = torch.from_numpy(t["depth"])
-    return dep
+def _same(a, b):
+    return torch.equal(a, b) or (a.dtype.is_floating_point and torch.equal(a.nan_to_num(7.0), b.nan_to_num(7.0)))
 
 
-def run_case(cfg, seed, steps, sets=4, requests=None, parents_per_req=None, gen_device="cpu", flags=0,
-             check_step=True, name=""):
-    """Stage-wise parity for `steps` rounds. requests: indices checked against the oracle."""
-    R, D, B, K, T = cfg["R"], cfg["D"], cfg["B"], cfg["K"], cfg["T"]
-    requests = list(range(R)) if requests is None else list(requests)
-    rnd = make_round(cfg, seed, flags)
-    rnd2 = make_round(cfg, seed, flags) if check_step else None
-    invT = inv_temperature(T)
-    tally = Tally()
-    for s in range(steps):
-        say("case %s step %d (%s)" % (name, s, W.describe(cfg)))
-        base, sigma = W.base_rows(cfg, set_idx=s % sets, device=gen_device)
-        draft = W.draft_from_base(cfg, base)
-        d_host = to_np(draft[requests].cpu()) if gen_device != "cpu" else to_np(draft)[requests]
-        pls = [None] * R
-        for i, r in enumerate(requests):
-            pls[r] = ostep.plan_request(d_host[i], T, K, B)
-        draft_g = draft.cuda().contiguous()
-        rnd.plan(draft_g)
-        h = rnd.host()
-        dep = _depths(pls, R, B)
-        for r in range(R):
-            if pls[r] is None:
-                n = int(h["n_nodes"][r])
-                dep[r, :n] = h["depth"][r, :n].long()
-        target = W.target_from_base(cfg, base, sigma, dep.to(base.device), set_idx=s % sets)
-        t_host = to_np(target[requests].cpu()) if gen_device != "cpu" else to_np(target)[requests]
-        target_g = target.cuda().contiguous()
-        plan_ok = {}
-        for i, r in enumerate(requests):
-            plan_ok[r] = compare_plan(h, r, pls[r], tally, "%s step %d req %d" % (name, s, r))
+def run_case(pool, cfg, seed, steps, step0=0, sets=4, gen_device="cpu", check_step=True, name=""):
+    """Stage-wise parity of every request of rounds step0 .. step0 + steps - 1 (plan, replay, verify), with
+    tsb_step on a second workspace compared with the staged calls bit for bit."""
+    rnd2 = make_round(cfg, seed) if check_step else None
+
+    def gpu_round(rnd, draft_g, target_g, s):
         rnd.replay(draft_g, s)
-        h = rnd.host()
-        tok_ok = {}
-        for i, r in enumerate(requests):
-            if not plan_ok[r]:
-                continue
-            tree = pls[r]["tree"]
-            a_d = scaled(d_host[i], invT)
-            n = tree["n_nodes"]
-            g_tok = h["node_tok"][r, :n].numpy().astype(np.int64)
-            if parents_per_req is None:
-                o_tok, mg = oreplay.replay(a_d, tree, seed, s, r)
-                tok_ok[r] = compare_replay(g_tok, o_tok, mg, tally, "%s step %d req %d" % (name, s, r))
-            else:
-                par = [u for u in range(n) if tree["n_children"][u] > 0]
-                pick = par[:parents_per_req] + par[-1:]
-                for u in pick:
-                    m = int(tree["n_children"][u])
-                    toks, mg = oreplay.replay_node(a_d[int(tree["depth"][u])], m, seed, s, r, u)
-                    fc = int(tree["first_child"][u])
-                    compare_replay(g_tok[fc:fc + m], toks, {u: mg}, tally, "%s step %d req %d parent %d"
-                                   % (name, s, r, u))
-                tok_ok[r] = False
         rnd.verify(draft_g, target_g, s)
-        h = rnd.host()
-        for i, r in enumerate(requests):
-            if not tok_ok.get(r):
-                continue
-            tree = pls[r]["tree"]
-            n = tree["n_nodes"]
-            vr = ostep.verify_request(d_host[i], t_host[i], tree, h["node_tok"][r, :n].numpy(), pls[r]["lse64"], T,
-                                      seed, s, r)
-            compare_verify(h, r, vr, tally, D, "%s step %d req %d" % (name, s, r))
-        if check_step:
-            rnd2.step(draft_g, target_g, s)
-            h2 = rnd2.host()
-            for k in ("draft_lse", "topk_tok", "topk_lp", "parent", "depth", "rank", "n_children", "first_child",
-                      "score", "n_nodes", "node_tok", "n_acc", "acc_node", "acc_tok", "bonus", "req_status",
-                      "target_lse", "trace"):
-                a, b = h[k], h2[k]
-                assert torch.equal(a, b) or (a.dtype.is_floating_point and torch.equal(a.nan_to_num(7.0),
-                                                                                     b.nan_to_num(7.0))), k
-    say("case %s: exact %d flagged %d max|dlse_t| %.2e %s" % (name, tally.exact, tally.flagged,
-                                                            getattr(tally, "max_lse_err", 0.0), tally.notes[:5]))
-    return tally
+
+    def check(h, draft_g, target_g, s):
+        rnd2.step(draft_g, target_g, s)
+        h2 = rnd2.host()
+        for k in STEP_KEYS:
+            assert _same(h[k], h2[k]), (name, s, k)
+
+    return run_rounds(pool, cfg, seed, steps, "rrs", gpu_round, step0=step0, sets=sets, gen_device=gen_device,
+                      name=name, check=check if check_step else None)
 
 
-def test_tiny_fp32_end_to_end():
+_check = check_tally
+
+
+def test_tiny_all_steps(opool):
     cfg = W.config(1)
-    t = run_case(cfg, W.replay_seed(1), steps=24, name="tiny")
-    assert t.exact > 0 and t.flagged <= 2
+    _check(run_case(opool, cfg, W.replay_seed(1), steps=cfg["steps"], name="tiny"), cfg["steps"], 1)
 
 
-def test_ragged_multi_tile_scalar_path():
+def test_small_all_steps(opool):
+    cfg = W.config(2)
+    _check(run_case(opool, cfg, W.replay_seed(2), steps=cfg["steps"], name="small"), cfg["steps"], 1)
+
+
+@pytest.mark.parametrize("step0", [0, 80])
+def test_qwen_vocab_160_steps(opool, step0):
+    cfg = W.config(3)
+    _check(run_case(opool, cfg, W.replay_seed(3), steps=80, step0=step0, name="qwen_vocab"), 80, 1)
+
+
+@pytest.mark.parametrize("step0", [0, 8])
+def test_batched_every_request_16_steps(opool, step0):
+    cfg = W.config(4)
+    _check(run_case(opool, cfg, W.replay_seed(4), steps=8, step0=step0, gen_device="cuda", name="batched"), 8, 16)
+
+
+@pytest.mark.parametrize("step0", [0, 2])
+def test_large_budget_every_request_4_steps(opool, step0):
+    cfg = W.config(5)
+    _check(run_case(opool, cfg, W.replay_seed(5), steps=2, step0=step0, sets=2, gen_device="cuda",
+                    name="large_budget"), 2, 64)
+
+
+def test_ragged_multi_tile_scalar_path(opool):
     # V not a multiple of 8 or 4 (scalar loads), 3 replay tiles with a ragged tail, T != 1
     cfg = W.config(2, R=3, V=9001, D=5, B=20, K=6, T=1.3, name="ragged")
-    t = run_case(cfg, 12345, steps=8, name="ragged")
-    assert t.exact > 0 and t.flagged <= 2
+    _check(run_case(opool, cfg, 12345, steps=40, name="ragged"), 40, 3)
 
 
-def test_small_bf16():
-    cfg = W.config(2)
-    t = run_case(cfg, W.replay_seed(2), steps=6, name="small")
-    assert t.exact > 0 and t.flagged <= 2
-
-
-def test_qwen_vocab_single_request():
-    cfg = W.config(3)
-    t = run_case(cfg, W.replay_seed(3), steps=3, name="qwen_vocab")
-    assert t.exact > 0 and t.flagged <= 1
-
-
-def test_batched_full_size_sampled():
-    cfg = W.config(4)
-    t = run_case(cfg, W.replay_seed(4), steps=1, sets=1, requests=[0, 5, 11, 15], gen_device="cuda",
-                 check_step=True, name="batched")
-    assert t.exact >= 8
-
-
-def test_batched_full_size_parents_sampled():
-    cfg = W.config(4)
-    t = run_case(cfg, W.replay_seed(4), steps=1, sets=1, requests=list(range(16)), parents_per_req=2,
-                 gen_device="cuda", check_step=False, name="batched-parents")
-    assert t.exact >= 16
-
-
-def test_large_budget_full_size_sampled():
-    cfg = W.config(5)
-    t = run_case(cfg, W.replay_seed(5), steps=1, sets=1, requests=[0, 63], gen_device="cuda", check_step=False,
-                 name="large_budget")
-    assert t.exact >= 4
-
-
-def test_vocab_beyond_64_replay_tiles():
+def test_vocab_beyond_64_replay_tiles(opool):
     # V = 300001: 74 replay tiles of 4096 (more than one per lane in the merge,
     # which then inserts key by key) with a ragged last tile, scalar loads
     cfg = W.config(2, R=2, V=300001, D=4, B=24, K=6, T=1.0, name="wide")
-    t = run_case(cfg, 31337, steps=2, name="wide")
-    assert t.exact >= 3 and t.flagged <= 1
+    _check(run_case(opool, cfg, 31337, steps=8, name="wide"), 8, 2)
 
 
 def test_pruning_does_not_change_replay():
@@ -209,27 +146,24 @@ def _edge_cfg(**kw):
     return c
 
 
-def _run_edge(cfg, draft_np, target_np, seed=5, step=0):
+def _run_edge(cfg, draft_np, target_np, seed=5, step=0, name="edge"):
     rnd = make_round(cfg, seed)
     draft = torch.from_numpy(draft_np).cuda()
     target = torch.from_numpy(target_np).cuda()
     rnd.step(draft, target, step)
     h = rnd.host()
-    tally = Tally()
+    tally = Tally("%s %s step %d" % (name, W.describe(cfg), step), register=False)
     for r in range(cfg["R"]):
-        pl = ostep.plan_request(draft_np[r], cfg["T"], cfg["K"], cfg["B"])
-        if not compare_plan(h, r, pl, tally, "edge req %d" % r):
+        res = oracle_worker.request_step(draft_np[r], target_np[r], cfg["T"], cfg["K"], cfg["B"], seed, step, r,
+                                         tree_dict_np(h, r),
+                                         h["node_tok"][r, :int(h["n_nodes"][r])].numpy().astype(np.int64))
+        if res["plan"]["status"] & STATUS_NONFINITE:
+            assert int(h["req_status"][r]) & tsb.REQ_NONFINITE and int(h["n_acc"][r]) == -1
+            assert int(h["bonus"][r]) == -1
+            tally.ok("plan")
             continue
-        n = pl["tree"]["n_nodes"]
-        o_tok, mg = oreplay.replay(scaled(draft_np[r], inv_temperature(cfg["T"])), pl["tree"], seed, step, r)
-        if not compare_replay(h["node_tok"][r, :n].numpy().astype(np.int64), o_tok, mg, tally, "edge %d" % r):
-            continue
-        vr = ostep.verify_request(draft_np[r], target_np[r], pl["tree"], o_tok, pl["lse64"], cfg["T"], seed, step, r)
-        st = int(h["req_status"][r])
-        if vr["n_acc"] < 0:
-            assert st & tsb.REQ_NONFINITE and int(h["n_acc"][r]) == -1 and int(h["bonus"][r]) == -1
-            continue
-        compare_verify(h, r, vr, tally, cfg["D"], "edge %d" % r)
+        compare_request(h, r, res, tally, cfg["D"], "%s req %d" % (name, r))
+    assert tally.flagged <= 1, tally.notes
     return h, tally
 
 
@@ -250,7 +184,7 @@ def test_edge_budget_short_and_masked_tokens():
     t = (rng.standard_normal((3, 11, 600)) * 2).astype(np.float32)
     h, tally = _run_edge(cfg, d, t)
     assert int(h["n_nodes"][0]) == 7 and int(h["req_status"][0]) & tsb.REQ_BUDGET_SHORT
-    assert tally.exact >= 6
+    assert tally.exact["plan"] >= 2 and tally.exact["verify"] >= 2
 
 
 def test_edge_nonfinite_rows_flag_only_their_request():
@@ -274,18 +208,19 @@ def test_edge_chain_and_minimal_vocabulary():
     t = rng.standard_normal((2, 5, 4)).astype(np.float32)
     for s in range(20):
         h, tally = _run_edge(cfg, d, t, step=s)
-        assert tally.exact >= 4
+        assert tally.exact["verify"] == 2
 
 
 def _plan_only(cfg, draft_np):
     rnd = make_round(cfg, 11)
     rnd.plan(torch.from_numpy(draft_np).cuda())
     h = rnd.host()
-    tally = Tally()
+    tally = Tally("plan-only %s" % W.describe(cfg), register=False)
     for r in range(cfg["R"]):
         pl = ostep.plan_request(draft_np[r], cfg["T"], cfg["K"], cfg["B"])
         compare_plan(h, r, pl, tally, "plan req %d" % r)  # raises on a mismatch that is not a near-tie
-    say("plan-only %s: exact %d flagged %d %s" % (W.describe(cfg), tally.exact, tally.flagged, tally.notes[:3]))
+    say(tally.line())
+    assert tally.flagged <= 1, tally.notes
     return h, tally
 
 
@@ -304,7 +239,7 @@ def test_planner_exact_ties(B, K, D):
     d[4] = np.round(rng.standard_normal((D, V)) * 4) / 4         # quarter steps
     cfg = dict(name="ties", R=5, V=V, D=D, B=B, K=K, T=1.0, dtype="f32", steps=1)
     h, tally = _plan_only(cfg, d)
-    assert tally.exact >= 4
+    assert tally.exact["plan"] >= 4
     nmax = sum(K ** i for i in range(1, D + 1))
     assert (h["n_nodes"] == min(B, nmax) + 1).all()
 
@@ -355,7 +290,7 @@ def test_draft_table_path_special_values(T):
     rnd.plan(torch.from_numpy(d).to(torch.bfloat16).cuda())
     h = rnd.host()
     st = h["req_status"].numpy()
-    tally = Tally()
+    tally = Tally("special rows T=%g" % T)
     for r in range(R):
         pl = ostep.plan_request(d[r], T, cfg["K"], cfg["B"])
         if r >= 2:
@@ -363,5 +298,5 @@ def test_draft_table_path_special_values(T):
             continue
         assert not st[r] & tsb.REQ_NONFINITE, r
         compare_plan(h, r, pl, tally, "special T=%g req %d" % (T, r))
-    say("special rows T=%g: exact %d flagged %d %s" % (T, tally.exact, tally.flagged, tally.notes[:3]))
-    assert tally.exact >= 1
+    say(tally.line())
+    assert tally.exact["plan"] >= 1 and tally.flagged <= 1
