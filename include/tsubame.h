@@ -206,6 +206,23 @@ tsb_status tsb_step(const tsb_config* cfg, const void* draft, const void* target
                     int32_t* node_tok, const tsb_verdict* out, void* workspace,
                     size_t workspace_bytes, hipStream_t stream);
 
+/* tsb_step without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops that must not
+ * call hipMalloc, harnesses that forbid it). The scratch is a file-scope
+ * device array of TSB_NOALLOC_SCRATCH_BYTES inside the library, one per GPU,
+ * held until the process ends; its address is taken once per device on the
+ * first call there. The call itself allocates and frees nothing. Every call
+ * on one GPU shares that GPU's array: calls that overlap in time on one GPU
+ * (other streams, other host threads) race and must be serialised by the
+ * caller. Nothing in the array is carried from one call to the next (the
+ * stages rewrite or clear what they read). TSB_E_WORKSPACE if
+ * tsb_workspace_bytes(cfg) exceeds TSB_NOALLOC_SCRATCH_BYTES (the batched
+ * workload, R = 16, V = 151936, B = 128, needs about 20 MiB). */
+#define TSB_NOALLOC_SCRATCH_BYTES (32u << 20)
+tsb_status tsb_step_noalloc(const tsb_config* cfg, const void* draft, const void* target, uint32_t step,
+                            double* draft_lse, int32_t* topk_tok, float* topk_lp, const tsb_tree* tree,
+                            int32_t* node_tok, const tsb_verdict* out, hipStream_t stream);
+
 /* Planning tokens as node tokens: the first-pass tree verified directly is
  * the deterministic baseline First (Section 3.1; Tables 3 and 4, TopK).
  * Writes node_tok[r, i] = topk_tok[r, depth[i] - 1, rank[i]] for

@@ -36,7 +36,8 @@ KERNELS = ("draft_partials", "plan_tree", "replay_scan", "replay_merge", "target
 EXPORTS = ("tsb_workspace_bytes", "tsb_plan", "tsb_plan_ep", "tsb_replay", "tsb_verify", "tsb_step",
            "tsb_first_tokens", "tsb_verify_naive", "tsb_step_first",
            "tsb_pool_workspace_bytes", "tsb_pool_plan", "tsb_pool_replay", "tsb_pool_verify", "tsb_pool_step",
-           "tsb_status_string", "tsb_last_error", "tsb_version", "tsb_profile_kernel")
+           "tsb_status_string", "tsb_last_error", "tsb_version", "tsb_profile_kernel", "tsb_step_noalloc")
+NOALLOC_SCRATCH_BYTES = 32 << 20
 
 
 class TsbConfig(ctypes.Structure):
@@ -99,6 +100,9 @@ def load(path=LIB_PATH):
     lib.tsb_verify_naive.restype = ctypes.c_int
     lib.tsb_verify_naive.argtypes = [ctypes.POINTER(TsbConfig), P, ctypes.POINTER(TsbTree), P, ctypes.c_uint32,
                                      ctypes.POINTER(TsbVerdict), P, ctypes.c_size_t, P]
+    lib.tsb_step_noalloc.restype = ctypes.c_int
+    lib.tsb_step_noalloc.argtypes = [ctypes.POINTER(TsbConfig), P, P, ctypes.c_uint32, P, P, P,
+                                     ctypes.POINTER(TsbTree), P, ctypes.POINTER(TsbVerdict), P]
     lib.tsb_step_first.restype = ctypes.c_int
     lib.tsb_step_first.argtypes = lib.tsb_step.argtypes
     I = ctypes.c_int32
@@ -264,6 +268,17 @@ class Round:
                              self.ws_ptr, self.ws_bytes, _stream(stream))
         if st:
             raise TsbError(st, "tsb_step")
+
+    def step_noalloc(self, draft, target, step, stream=None):
+        """tsb_step with the library's own per-device scratch instead of this Round's workspace."""
+        self._logits(draft, self.cfg.D, "draft")
+        self._logits(target, self.cfg.B + 1, "target")
+        st = load().tsb_step_noalloc(ctypes.byref(self.cfg), _ptr(draft), _ptr(target), int(step) & 0xFFFFFFFF,
+                                     _ptr(self.draft_lse), _ptr(self.topk_tok), _ptr(self.topk_lp),
+                                     ctypes.byref(self._tree_c), _ptr(self.node_tok), ctypes.byref(self._verdict_c),
+                                     _stream(stream))
+        if st:
+            raise TsbError(st, "tsb_step_noalloc")
 
     # ------------------------------------------------- First + Naive baseline
     def first_tokens(self, stream=None):

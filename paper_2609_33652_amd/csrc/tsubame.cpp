@@ -6,6 +6,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include <hip/hip_runtime.h>
 
 #include "tsb_internal.hpp"
@@ -91,6 +93,33 @@ float inv_temperature(float T) {
         const tsb_status s__ = (x);         \
         if (s__ != TSB_OK) return s__;      \
     } while (0)
+
+// Scratch of tsb_step_noalloc: a file-scope device array, one copy per GPU
+// the library runs on, held until the process ends. In host code `scratch`
+// only names the symbol; its device address on the current GPU comes from
+// hipGetSymbolAddress, taken once per device on the first call there.
+__device__ __align__(256) unsigned char scratch[TSB_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+tsb_status scratch_address(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "tsb_step_noalloc/hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(TSB_E_DEVICE, "device %d beyond the %d the library tracks", dev, kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "tsb_step_noalloc/hipGetSymbolAddress(scratch)");
+        if (!p || ((uintptr_t)p & 255) != 0) return fail(TSB_E_DEVICE, "scratch symbol has no aligned device address");
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return TSB_OK;
+}
 
 }  // namespace
 
@@ -192,6 +221,26 @@ tsb_status tsb_step(const tsb_config* cfg, const void* draft, const void* target
     e = tsb::launch_verify(*cfg, invT, draft, draft_lse, target, *tree, node_tok, step, *out, ws, stream);
     if (e != hipSuccess) return hip_fail(e, "tsb_step/verify");
     return TSB_OK;
+}
+
+tsb_status tsb_step_noalloc(const tsb_config* cfg, const void* draft, const void* target, uint32_t step,
+                            double* draft_lse, int32_t* topk_tok, float* topk_lp, const tsb_tree* tree,
+                            int32_t* node_tok, const tsb_verdict* out, hipStream_t stream) {
+    g_last_error[0] = 0;
+    TRY(check_config(cfg));
+    const size_t need = tsb_workspace_bytes(cfg);
+    if (need > (size_t)TSB_NOALLOC_SCRATCH_BYTES)
+        return fail(TSB_E_WORKSPACE, "tsb_step_noalloc: this configuration needs %zu bytes of scratch, more than the "
+                    "%zu the library holds per device (use tsb_step with a workspace)", need,
+                    (size_t)TSB_NOALLOC_SCRATCH_BYTES);
+    if (!draft || !target || !draft_lse || !topk_tok || !topk_lp || !node_tok)
+        return fail(TSB_E_NULL, "tsb_step_noalloc: a required array is NULL");
+    TRY(check_tree(tree));
+    TRY(check_verdict(out));
+    void* ws = nullptr;
+    TRY(scratch_address(&ws));
+    return tsb_step(cfg, draft, target, step, draft_lse, topk_tok, topk_lp, tree, node_tok, out, ws,
+                    (size_t)TSB_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 tsb_status tsb_first_tokens(const tsb_config* cfg, const int32_t* topk_tok, const tsb_tree* tree, int32_t* node_tok,

@@ -186,3 +186,24 @@ def test_pool_entry_points_validate(lib):
     assert lib.tsb_pool_step(ctypes.byref(_cfg(dtype=5)), 16, FAKE, FAKE, FAKE, 0, FAKE, ctypes.byref(t), FAKE,
                              ctypes.byref(v), FAKE, need, None) == 3
 
+
+def test_step_noalloc_validates_before_any_device_call(lib):
+    """tsb_step_noalloc rejects a configuration whose scratch exceeds the library's fixed per-device array, and
+    invalid arguments, on the host (no HIP call is made, so these run without a GPU)."""
+    t = _tree()
+    v = _verdict()
+    big = _cfg(R=64, D=32, V=151936, B=256, K=16)  # about 156 MiB of scratch
+    assert lib.tsb_workspace_bytes(ctypes.byref(big)) > tsb.NOALLOC_SCRATCH_BYTES
+    assert lib.tsb_step_noalloc(ctypes.byref(big), FAKE, FAKE, 0, FAKE, FAKE, FAKE, ctypes.byref(t), FAKE,
+                                ctypes.byref(v), None) == 5
+    assert "scratch" in lib.tsb_last_error().decode()
+    batched = _cfg(R=16, D=16, V=151936, B=128, K=10)
+    assert lib.tsb_workspace_bytes(ctypes.byref(batched)) <= tsb.NOALLOC_SCRATCH_BYTES
+    assert lib.tsb_step_noalloc(ctypes.byref(_cfg(K=0)), FAKE, FAKE, 0, FAKE, FAKE, FAKE, ctypes.byref(t), FAKE,
+                                ctypes.byref(v), None) == 2
+    assert lib.tsb_step_noalloc(ctypes.byref(batched), None, FAKE, 0, FAKE, FAKE, FAKE, ctypes.byref(t), FAKE,
+                                ctypes.byref(v), None) == 1
+    bad_v = _verdict()
+    bad_v.n_acc = None
+    assert lib.tsb_step_noalloc(ctypes.byref(batched), FAKE, FAKE, 0, FAKE, FAKE, FAKE, ctypes.byref(t), FAKE,
+                                ctypes.byref(bad_v), None) == 1
