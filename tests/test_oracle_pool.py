@@ -321,3 +321,21 @@ def test_status_bits():
     assert out["status"] & STATUS_NONFINITE and out["n_acc"] == -1 and out["tree"]["n_nodes"] == 1
     out = pool.step_pool_request(draft, np.zeros((40, V), np.float32), trans, 1.0, 2, P, 30, 1, 0, 0)
     assert out["status"] & STATUS_BUDGET_SHORT and out["tree"]["n_nodes"] == 1 + 2 + 4
+
+
+def test_target_row_slip_below_the_root_breaks_the_law(monkeypatch):
+    """A node other than the root verified against its parent's target row (a row-selection mistake below the
+    root) must be caught by the sampled law of the whole emitted sequence."""
+    draft, trans, K, P, B, p_of_rows, law = _round_law_case()
+    real = pool.verify_mod.verify
+
+    def slipped(p_rows, q_rows, tree, node_tok, seed, step_, request, q_node=None):
+        par = tree["parent"]
+        return real(lambda u: p_rows(int(par[u]) if u > 0 else 0), q_rows, tree, node_tok, seed, step_, request,
+                    q_node)
+
+    monkeypatch.setattr(pool.verify_mod, "verify", slipped)
+    n = 3000
+    counts = _empirical(draft, trans, K, P, B, p_of_rows, n)
+    impossible = not set(counts) <= set(law)
+    assert impossible or _chi2_pvalue(counts, law, n) < 1e-3
