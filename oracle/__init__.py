@@ -15,6 +15,8 @@ the paper (Tsubame: Tree Replay for Diffusion-Based Speculative Decoding):
   planner   lazy best-first topology planning (Section 3.1, Appendix B.3)
   replay    Gumbel-top-k refill of the frozen topology (Section 3.2, eq. (2))
   verify    WoR recursive rejection sampling + bonus (eq. (1), Appendix A)
+  traversal traversal verification: sequence-level RRS over the tree
+            (Appendix A, Table 2)
   step      one full round per request
   exact     exact law of a round by enumeration (Section 3.3, Proposition 1)
 

@@ -20,11 +20,18 @@ naive_law() enumerates target-sample matching (Table 2, Naive) over a tree
 whose node tokens are fixed (the First tree of Section 3.1): at each visited
 node every token of p_u either matches a child and continues there, or ends
 the round as the bonus.
+
+traversal_law() enumerates a round verified by traversal (Appendix A; Table
+2): the traversal starts below the root and can visit every node, so the
+replay draws of every parent are enumerated (Plackett-Luce weights as
+above), and for each complete assignment every accept/reject branch of the
+traversal, with the updates taken from oracle.traversal.
 """
 import itertools
 
 import numpy as np
 
+from . import traversal as trav_mod
 from . import verify as verify_mod
 
 
@@ -148,4 +155,86 @@ def naive_law(tree, node_tok, p_of_prefix):
                 law[seq] = law.get(seq, 0.0) + w * p[y]
 
     walk(0, (), 1.0)
+    return law
+
+
+def traversal_law(tree, q, p_of_prefix):
+    """Exact distribution of the emitted sequence of a round verified by traversal.
+
+    tree, q, p_of_prefix as in emitted_law (q: [D, V] per depth or a callable
+    of the replayed prefix). Returns dict {tuple(sequence): probability}.
+    """
+    n = int(tree["n_nodes"])
+    n_children, first_child, parent, depth = (tree["n_children"], tree["first_child"], tree["parent"],
+                                             tree["depth"])
+    internal = [u for u in range(n) if int(n_children[u]) > 0]
+    law = {}
+
+    def add(seq, w):
+        law[seq] = law.get(seq, 0.0) + w
+
+    def prefix_of(u, tok):
+        path = []
+        while u > 0:
+            path.append(int(tok[u]))
+            u = int(parent[u])
+        return tuple(reversed(path))
+
+    def q_at(u, tok):
+        return np.asarray(q(prefix_of(u, tok)) if callable(q) else q[int(depth[u])], dtype=np.float64)
+
+    def p_at(u, tok):
+        return np.asarray(p_of_prefix(prefix_of(u, tok)), dtype=np.float64)
+
+    def emit(u, P, tok, w):
+        pre = prefix_of(u, tok)
+        tot = P.sum()
+        for v in range(P.shape[0]):
+            if P[v] > 0:
+                add(pre + (v,), w * P[v] / tot)
+
+    def branch(tok, Mb, Ms, alpha, left, path, w):
+        """Continue the traversal from the current state with probability weight w."""
+        while True:
+            u = path[-1]
+            if left[u] < int(n_children[u]):
+                c = int(first_child[u]) + left[u]
+                alpha[c] = trav_mod.child_alpha(alpha[u], Mb[u], Ms[u], int(tok[c]))
+                Mb[c] = p_at(c, tok)
+                Ms[c] = q_at(c, tok) if int(n_children[c]) > 0 else None
+                left[c] = 0
+                path.append(c)
+                continue
+            if u == 0:
+                emit(0, Mb[0], tok, w)
+                return
+            a = alpha[u]
+            if a > 0.0:
+                emit(u, Mb[u], tok, w * a)
+            if a >= 1.0:
+                return
+            w *= 1.0 - a
+            path.pop()
+            v = path[-1]
+            a_new, Mb_new, Ms_new, T, S = trav_mod.reject_child(alpha[v], Mb[v], Ms[v], int(tok[u]))
+            left[v] += 1
+            if (T <= 0.0 and alpha[v] >= 1.0) or (S <= 0.0 and left[v] < int(n_children[v])):
+                emit(v, p_at(v, tok), tok, w)
+                return
+            alpha[v], Mb[v], Ms[v] = a_new, Mb_new, Ms_new
+
+    def assign(i, tok, w):
+        if i == len(internal):
+            root_q = q_at(0, tok) if int(n_children[0]) > 0 else None
+            branch(tok, {0: p_at(0, tok)}, {0: root_q}, {0: 1.0}, {0: 0}, [0], w)
+            return
+        u = internal[i]
+        m = int(n_children[u])
+        fc = int(first_child[u])
+        for seq, w_draw in _wor_orders(q_at(u, tok), m):
+            t2 = tok.copy()
+            t2[fc:fc + m] = seq
+            assign(i + 1, t2, w * w_draw)
+
+    assign(0, np.full(n, -1, np.int64), 1.0)
     return law

@@ -16,7 +16,7 @@ Row d of the draft is the distribution of the tokens at depth d + 1.
 """
 import numpy as np
 
-from . import planner, replay as replay_mod, verify as verify_mod
+from . import planner, replay as replay_mod, traversal as traversal_mod, verify as verify_mod
 from .rowstats import (STATUS_BUDGET_SHORT, STATUS_NONFINITE, draft_rowstats,
                        inv_temperature, lse64, probs, row_ok, scaled)
 
@@ -48,8 +48,12 @@ def plan_request(draft, T, K, B):
                 tree=tree, status=status)
 
 
-def verify_request(draft, target, tree, node_tok, lse_draft64, T, seed, step, request):
-    """Target normalisers + WoR-RRS walk for one request."""
+VERIFIERS = ("rrs", "traversal")
+
+
+def verify_request(draft, target, tree, node_tok, lse_draft64, T, seed, step, request, verifier="rrs"):
+    """Target normalisers + the verification walk for one request: WoR-RRS (eq. (1); Appendix A) or
+    traversal verification (Appendix A; Table 2), both with the replayed candidates' probabilities."""
     invT = inv_temperature(T)
     n = tree["n_nodes"]
     a_t = [scaled(target[u], invT) for u in range(n)]
@@ -59,14 +63,14 @@ def verify_request(draft, target, tree, node_tok, lse_draft64, T, seed, step, re
                     lse_t=np.full(n, np.nan))
     lse_t = np.array([lse64(a) for a in a_t])
     a_d = scaled(draft, invT)
-    res = verify_mod.verify(lambda u: probs(a_t[u], lse_t[u]),
-                            lambda d: probs(a_d[d], lse_draft64[d]),
-                            tree, node_tok, seed, step, request)
+    walk = verify_mod.verify if verifier == "rrs" else traversal_mod.verify_traversal
+    res = walk(lambda u: probs(a_t[u], lse_t[u]), lambda d: probs(a_d[d], lse_draft64[d]),
+               tree, node_tok, seed, step, request)
     res["lse_t"] = lse_t
     return res
 
 
-def step_request(draft, target, T, K, B, seed, step, request, target_fn=None):
+def step_request(draft, target, T, K, B, seed, step, request, target_fn=None, verifier="rrs"):
     """Full round for one request.
 
     target: array [B+1, V] (slot-keyed rows), or None with target_fn(tree,
@@ -86,7 +90,7 @@ def step_request(draft, target, T, K, B, seed, step, request, target_fn=None):
     margins += [("replay", u, m) for u, m in rmg.items()]
     if target is None:
         target = target_fn(tree, node_tok)
-    vr = verify_request(draft, target, tree, node_tok, pl["lse64"], T, seed, step, request)
+    vr = verify_request(draft, target, tree, node_tok, pl["lse64"], T, seed, step, request, verifier)
     margins += vr["margins"]
     out.update(node_tok=node_tok, n_acc=vr["n_acc"], acc_node=vr["acc_node"],
                acc_tok=vr["acc_tok"], bonus=vr["bonus"], status=pl["status"] | vr["status"],

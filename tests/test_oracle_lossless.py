@@ -138,11 +138,11 @@ def parent_row_slip(monkeypatch):
     target row (the root's own row is untouched, so every first emitted token keeps its law)."""
     real = step.verify_request
 
-    def slipped(draft, target, tree, node_tok, lse, T, seed, step_, request):
+    def slipped(draft, target, tree, node_tok, lse, T, seed, step_, request, verifier="rrs"):
         t = np.array(target, copy=True)
         for u in range(1, tree["n_nodes"]):
             t[u] = target[int(tree["parent"][u])]
-        return real(draft, t, tree, node_tok, lse, T, seed, step_, request)
+        return real(draft, t, tree, node_tok, lse, T, seed, step_, request, verifier)
     monkeypatch.setattr(step, "verify_request", slipped)
 
 
