@@ -74,6 +74,10 @@ def _cpu_task(args):
         from oracle import naive as onaive
         out = onaive.first_naive_request(_CPU["draft"][r], _CPU["target"][r], c["T"], c["K"], c["B"], _CPU["seed"],
                                          step, r)
+    elif _CPU["path"] == "traversal":
+        from oracle import step as ostep
+        out = ostep.step_request(_CPU["draft"][r], _CPU["target"][r], c["T"], c["K"], c["B"], _CPU["seed"], step, r,
+                                 verifier="traversal")
     elif _CPU["path"] == "pool":
         from oracle import pool as opool
         out = opool.step_pool_request(_CPU["draft"][r], _CPU["target"][r], _CPU["trans"][r], c["T"], c["K"],
@@ -185,6 +189,48 @@ def first_naive(tsb, c, dev, drafts, targets, args, cfg):
                      "rows_per_launch": round(visited / args.breakdown_steps, 2),
                      "note": "one cross-workgroup exchange per visited row; latency, not bandwidth, sets its time"},
     }
+
+
+def traversal_block(tsb, c, dev, drafts, targets, args, cfg):
+    """Replay + traversal verification on the same inputs: timed rounds, the walk's time and acceptance."""
+    import torch
+    R = cfg["R"]
+    P = len(drafts)
+    rnd = tsb.Round(c, dev)
+    for s in range(args.warmup):
+        rnd.step_traversal(drafts[s % P], targets[s % P], s)
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for i in range(args.first_steps):
+        s = args.warmup + i
+        rnd.step_traversal(drafts[s % P], targets[s % P], s)
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.first_steps
+    kid = tsb.KERNELS.index("traversal_walk")
+    evs = events(args.breakdown_steps)
+    for i in range(args.breakdown_steps):
+        tsb.profile_kernel(kid, evs[i][0], evs[i][1])
+        rnd.step_traversal(drafts[i % P], targets[i % P], i)
+        tsb.profile_kernel(kid, None)
+    torch.cuda.synchronize()
+    walk_us = 1000.0 * sum(a.elapsed_time(b) for a, b in evs) / args.breakdown_steps
+    acc, tests = 0, 0
+    trnd = tsb.Round(c, dev, trace=True)
+    for i in range(P):
+        trnd.step_traversal(drafts[i], targets[i], i)
+        h = trnd.host()
+        acc += int(h["n_acc"].clamp(min=0).sum()) + int((h["n_acc"] >= 0).sum())
+        tests += int((h["trace"][:, :, 0] >= 0).sum())
+    tau = acc / (P * R)
+    return {"steps_per_s": round(1000.0 / ms, 2), "ms_per_step": round(ms, 4), "steps": args.first_steps,
+            "tau": round(tau, 4), "accepted_tokens_per_s": round(tau * R * 1000.0 / ms, 1),
+            "walk_kernel": "traversal_walk", "walk_avg_launch_us": round(walk_us, 2),
+            "tests_per_request": round(tests / (P * R), 2),
+            "note": "one vocabulary-wide pass and one cross-workgroup exchange per rejected node and per internal "
+                    "node entered; latency, not bandwidth, sets the walk's time"}
 
 
 def planner_ep(tsb, c, dev, drafts, targets, args, cfg, frontier=10):
@@ -299,10 +345,12 @@ def main():
         log("cpu baseline:", cpu)
         cpu_first = cpu_baseline(cfg, seed, nreq, path="first_naive")
         log("cpu baseline (first + naive):", cpu_first)
+        cpu_trav = cpu_baseline(cfg, seed, nreq, path="traversal")
+        log("cpu baseline (traversal):", cpu_trav)
         cpu_pool = cpu_baseline(cfg, seed, nreq, path="pool", P=args.pool_size) if args.pool_size else None
         log("cpu baseline (pools):", cpu_pool)
     else:
-        cpu_first = cpu_pool = None
+        cpu_first = cpu_pool = cpu_trav = None
 
     import torch
     import paper_2609_33652_amd as tsb
@@ -378,6 +426,8 @@ def main():
 
     first = first_naive(tsb, c, dev, drafts, targets, args, cfg)
     first["cpu_baseline"] = cpu_first
+    trav = traversal_block(tsb, c, dev, drafts, targets, args, cfg)
+    trav["cpu_baseline"] = cpu_trav
     ep = planner_ep(tsb, c, dev, drafts, targets, args, cfg)
     del targets
     torch.cuda.empty_cache()
@@ -426,6 +476,7 @@ def main():
         "flagged_requests": flagged,
         "cpu_baseline": cpu,
         "first_naive": first,
+        "traversal": trav,
         "planner_expand_prune": ep,
         "sparse_pools": pool,
     }

@@ -18,6 +18,10 @@
  *               Proposition 1: the probabilities used are those of the
  *               replayed candidates).
  *   tsb_step    plan -> replay -> verify with target logits supplied up front.
+ *   tsb_verify_traversal, tsb_step_traversal
+ *               the same round verified by traversal verification, the
+ *               sequence-level verifier for trees drawn without replacement
+ *               (Appendix A; Table 2).
  *
  * and the deterministic baseline of Section 3.1 with target-sample matching
  * (Table 2, Naive): tsb_first_tokens, tsb_verify_naive, tsb_step_first;
@@ -223,6 +227,35 @@ tsb_status tsb_step_noalloc(const tsb_config* cfg, const void* draft, const void
                             double* draft_lse, int32_t* topk_tok, float* topk_lp, const tsb_tree* tree,
                             int32_t* node_tok, const tsb_verdict* out, hipStream_t stream);
 
+/* Traversal verification (Appendix A; Table 2: the sequence-level verifier
+ * paired with sampling without replacement; compared with layer-wise RRS on
+ * replayed trees in Section 4.2). Same arguments and outputs as tsb_verify.
+ * The replayed tree is traversed in post-order (the first remaining child
+ * first, down to a node with no children left); the node reached is
+ * accepted, with the path from the root, with probability alpha, where
+ * alpha_root = 1 and a child c with token y of node u gets
+ * alpha_c = min(1, alpha_u Mb_u(y) / Ms_u(y)); Mb_u starts as p_u and Ms_u as
+ * u's draft distribution. When c is rejected, u updates with the
+ * distributions c was drawn from: T = sum_v max(alpha_u Mb_u - Ms_u, 0),
+ * Mb_u <- max(alpha_u Mb_u - Ms_u, 0) / T, alpha_u <- T / (T + 1 - alpha_u),
+ * y leaves Ms_u (renormalised). The root is accepted once its children are
+ * all rejected. The bonus token is a Gumbel-max sample of Mb at the accepted
+ * node (BONUS stream of that node); U of a tested node comes from its
+ * ACCEPT stream. An empty residual (T <= 0 with alpha_u = 1, or an
+ * exhausted Ms_u with children left) ends the round at u with a bonus from
+ * p_u and TSB_REQ_DEGENERATE_RESIDUAL. trace rows are (tested node, U,
+ * alpha, T after its rejection or -1). */
+tsb_status tsb_verify_traversal(const tsb_config* cfg, const void* draft, const double* draft_lse,
+                                const void* target, const tsb_tree* tree, const int32_t* node_tok, uint32_t step,
+                                const tsb_verdict* out, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream);
+
+/* plan -> replay -> traversal verification on one stream (target supplied up front). */
+tsb_status tsb_step_traversal(const tsb_config* cfg, const void* draft, const void* target, uint32_t step,
+                              double* draft_lse, int32_t* topk_tok, float* topk_lp, const tsb_tree* tree,
+                              int32_t* node_tok, const tsb_verdict* out, void* workspace, size_t workspace_bytes,
+                              hipStream_t stream);
+
 /* Planning tokens as node tokens: the first-pass tree verified directly is
  * the deterministic baseline First (Section 3.1; Tables 3 and 4, TopK).
  * Writes node_tok[r, i] = topk_tok[r, depth[i] - 1, rank[i]] for
@@ -341,7 +374,8 @@ enum {
     TSB_KERNEL_POOL_PLAN = 9,       /* best-first topology over per-node candidate lists */
     TSB_KERNEL_POOL_REPLAY = 10,
     TSB_KERNEL_POOL_WALK = 11,      /* verification with pool-restricted q_u */
-    TSB_KERNEL_COUNT = 12
+    TSB_KERNEL_TRAVERSAL_WALK = 12, /* traversal verification */
+    TSB_KERNEL_COUNT = 13
 };
 tsb_status tsb_profile_kernel(int32_t kernel_id, hipEvent_t start, hipEvent_t stop);
 

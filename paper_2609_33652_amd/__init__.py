@@ -6,6 +6,7 @@ supplies device memory and the stream. There is no CPU fallback: if the
 library is not built, or a call fails, an exception is raised.
 
 Entry points mirror the C ABI: plan, plan_ep, replay, verify, step, workspace_bytes,
+verify_traversal, step_traversal (traversal verification), step_noalloc,
 the First + Naive baseline: first_tokens, verify_naive, step_first, and the
 round over sparse candidate pools with context-dependent draft distributions:
 pool_plan, pool_replay, pool_verify, pool_step, pool_workspace_bytes.
@@ -31,12 +32,14 @@ POOL_MAX = 64
 FLAG_NO_PRUNE = 1
 MAX_D, MAX_K, MAX_B, TRACE_MAX = 64, 32, 1023, 256
 KERNELS = ("draft_partials", "plan_tree", "replay_scan", "replay_merge", "target_partials",
-           "verify_walk", "verify_naive", "pool_partials", "pool_lists", "pool_plan", "pool_replay", "pool_walk")
+           "verify_walk", "verify_naive", "pool_partials", "pool_lists", "pool_plan", "pool_replay", "pool_walk",
+           "traversal_walk")
 
 EXPORTS = ("tsb_workspace_bytes", "tsb_plan", "tsb_plan_ep", "tsb_replay", "tsb_verify", "tsb_step",
            "tsb_first_tokens", "tsb_verify_naive", "tsb_step_first",
            "tsb_pool_workspace_bytes", "tsb_pool_plan", "tsb_pool_replay", "tsb_pool_verify", "tsb_pool_step",
-           "tsb_status_string", "tsb_last_error", "tsb_version", "tsb_profile_kernel", "tsb_step_noalloc")
+           "tsb_status_string", "tsb_last_error", "tsb_version", "tsb_profile_kernel", "tsb_step_noalloc",
+           "tsb_verify_traversal", "tsb_step_traversal")
 NOALLOC_SCRATCH_BYTES = 32 << 20
 
 
@@ -100,6 +103,10 @@ def load(path=LIB_PATH):
     lib.tsb_verify_naive.restype = ctypes.c_int
     lib.tsb_verify_naive.argtypes = [ctypes.POINTER(TsbConfig), P, ctypes.POINTER(TsbTree), P, ctypes.c_uint32,
                                      ctypes.POINTER(TsbVerdict), P, ctypes.c_size_t, P]
+    lib.tsb_verify_traversal.restype = ctypes.c_int
+    lib.tsb_verify_traversal.argtypes = lib.tsb_verify.argtypes
+    lib.tsb_step_traversal.restype = ctypes.c_int
+    lib.tsb_step_traversal.argtypes = lib.tsb_step.argtypes
     lib.tsb_step_noalloc.restype = ctypes.c_int
     lib.tsb_step_noalloc.argtypes = [ctypes.POINTER(TsbConfig), P, P, ctypes.c_uint32, P, P, P,
                                      ctypes.POINTER(TsbTree), P, ctypes.POINTER(TsbVerdict), P]
@@ -268,6 +275,26 @@ class Round:
                              self.ws_ptr, self.ws_bytes, _stream(stream))
         if st:
             raise TsbError(st, "tsb_step")
+
+    def verify_traversal(self, draft, target, step, stream=None):
+        """Traversal verification of the replayed tree (instead of WoR-RRS)."""
+        self._logits(draft, self.cfg.D, "draft")
+        self._logits(target, self.cfg.B + 1, "target")
+        st = load().tsb_verify_traversal(ctypes.byref(self.cfg), _ptr(draft), _ptr(self.draft_lse), _ptr(target),
+                                         ctypes.byref(self._tree_c), _ptr(self.node_tok), int(step) & 0xFFFFFFFF,
+                                         ctypes.byref(self._verdict_c), self.ws_ptr, self.ws_bytes, _stream(stream))
+        if st:
+            raise TsbError(st, "tsb_verify_traversal")
+
+    def step_traversal(self, draft, target, step, stream=None):
+        self._logits(draft, self.cfg.D, "draft")
+        self._logits(target, self.cfg.B + 1, "target")
+        st = load().tsb_step_traversal(ctypes.byref(self.cfg), _ptr(draft), _ptr(target), int(step) & 0xFFFFFFFF,
+                                       _ptr(self.draft_lse), _ptr(self.topk_tok), _ptr(self.topk_lp),
+                                       ctypes.byref(self._tree_c), _ptr(self.node_tok), ctypes.byref(self._verdict_c),
+                                       self.ws_ptr, self.ws_bytes, _stream(stream))
+        if st:
+            raise TsbError(st, "tsb_step_traversal")
 
     def step_noalloc(self, draft, target, step, stream=None):
         """tsb_step with the library's own per-device scratch instead of this Round's workspace."""

@@ -1244,6 +1244,303 @@ __global__ __launch_bounds__(kWalkThreads) void verify_pool_walk(WalkArgs A) {
     walk_tail(A, r, g, G, n, draft_bad, invalid, nacc, bonus_out, add_status, tcount);
 }
 
+// ---------------------------------------------------------- traversal walk
+// Traversal verification (Appendix A; Table 2): sequence-level recursive
+// rejection sampling over the replayed tree. All G workgroups of a request
+// replay the same scalar traversal over a stack of the current path (in
+// LDS); every vocabulary-wide quantity is split over their slices and
+// exchanged:
+//   * the binary64 target normaliser of an internal node when the traversal
+//     first descends from it (its children's acceptance probabilities need
+//     p_u);
+//   * the residual mass T = sum_v max(A' p_v - C' q_v, 0) at a node after one
+//     of its children was rejected;
+//   * the bonus draw at the node that ends the round.
+// Closed form of a node's state (equal to the literal updates): Mb_u =
+// max(A p - C q, 0) / Z is the bonus distribution at u, Ms_u = q / S over
+// the tokens not yet removed the draft distribution of its remaining
+// children; a node enters with alpha from its parent and (A, C, Z, S) =
+// (1, 0, 1, 1). The child of u with token y has
+//   alpha_c = min(1, alpha_u max(A p(y) - C q(y), 0) / Z * S / q(y));
+// rejecting it maps u's state to A' = alpha A / Z, C' = alpha C / Z + 1 / S,
+// Z' = T, alpha' = T / (T + 1 - alpha), S' = S - q(y).
+// The traversal is post-order (the first remaining child first, down to a
+// node with none left, which is tested with U < alpha); the root has
+// alpha = 1 and is accepted once its children are all rejected. One
+// (p~, q) slice is kept in LDS: that of the node the last pass was over, so
+// consecutive rejections among the children of one node reuse it.
+struct TravEntry {
+    int node, left;
+    double alpha, A, C, Z, S, L;  // L: binary64 log normaliser of the node's target row, NaN until computed
+};
+constexpr int kTravStack = TSB_MAX_D + 1;  // root .. depth D
+
+// (p~, q) of a node's slice into the LDS cache when the slice fits, and the
+// block sum of p~ = exp(a^t - L0) over the slice.
+template <int DT>
+__device__ double trav_fill(const WalkArgs& A, bool vec, const WalkSlice& S, bool cached, size_t trow, size_t drow,
+                            double L0, double Ld, const double* et) {
+    double acc = 0.0;
+    for (int c = 0; c < S.nchunks; ++c) acc += fill_chunk<DT>(A, vec, S, c, trow, drow, L0, Ld, et, cached);
+    return walk_sum(acc);
+}
+
+template <int DT, bool VEC>
+__global__ __launch_bounds__(kWalkThreads) void verify_traversal(WalkArgs A) {
+    extern __shared__ double s_pq[];  // [2 * kWalkCache]: p~ then q of the cached node
+    __shared__ double s_exp[kExpTable];
+    __shared__ TravEntry s_stk[kTravStack];
+    __shared__ int s_cache;  // node whose slice is in the cache, -1 for none
+    const int g = blockIdx.x;
+    const int G = gridDim.x;
+    const int r = A.r0 + blockIdx.y;
+    const int tid = threadIdx.x;
+    const int B1 = A.B + 1;
+    const size_t tb = (size_t)r * B1;
+    const bool vec = VEC;
+    int* status_p = A.out.req_status + r;
+    const int n_raw = A.tree.n_nodes[r];
+    const bool count_ok = tree_count_ok(n_raw, A.B);
+    const int n = count_ok ? n_raw : 0;
+    const bool lead = (g == 0 && tid == 0);
+    if (tid == 0) s_cache = -1;
+    exp64_table_init(s_exp);
+
+    WalkSlice S;
+    {
+        const int span = ((A.V + G - 1) / G + 3) & ~3;
+        const bool has = (long long)g * span < A.V;
+        S.v0 = has ? g * span : 0;
+        S.v1 = has ? min(A.V, S.v0 + span) : 0;
+        S.nchunks = (S.v1 - S.v0 + kWalkCache - 1) / kWalkCache;
+        S.p = s_pq;
+        S.q = s_pq + kWalkCache;
+    }
+    const bool cached = S.nchunks <= 1;
+    const bool draft_bad = (*status_p & TSB_REQ_NONFINITE) != 0;
+
+    int tcount = 0;
+    double* const trace = (lead && A.out.trace) ? A.out.trace + (size_t)r * TSB_TRACE_MAX * 4 : nullptr;
+    int bonus_out = -1, add_status = count_ok ? 0 : TSB_REQ_BAD_TREE, nacc = 0;
+    bool invalid = !count_ok;
+    if (!draft_bad && count_ok) {
+        RngKey key;
+        key.k0 = A.k0;
+        key.k1 = A.k1;
+        key.request = (uint32_t)r;
+        key.step = A.step;
+        Exchange X{&A, r, g, G, 0u, 0};
+        if (tid == 0) s_stk[0] = TravEntry{0, 0, 1.0, 1.0, 0.0, 1.0, 1.0, (double)NAN};
+        __syncthreads();
+        int top = 0;
+        // end of the round at the node on top of the stack: bonus from Mb (or
+        // from p on an empty residual) and the accepted path = stack[1 .. top]
+        int end_kind = 0;  // 1: bonus from Mb of the top node, 2: degenerate (bonus from p)
+        while (true) {
+            const TravEntry E = s_stk[top];
+            const int u = E.node;
+            // every workgroup reads the same entries, so all take the same exits
+            const TreeNode nd = tree_node(A.tree, tb, u, n, A.D);
+            if (!nd.ok) {
+                add_status |= TSB_REQ_BAD_TREE;
+                invalid = true;
+                break;
+            }
+            const size_t trow = ((size_t)r * B1 + u) * (size_t)A.V;
+            if (E.left < nd.m) {  // descend to the next remaining child of u
+                if (top + 1 > A.D) {
+                    add_status |= TSB_REQ_BAD_TREE;
+                    invalid = true;
+                    break;
+                }
+                const size_t drow = ((size_t)r * A.D + nd.d) * (size_t)A.V;
+                const double Ld = A.draft_lse[(size_t)r * A.D + nd.d];
+                double L = E.L;
+                if (isnan(L)) {  // first descent from u: binary64 normaliser of its target row
+                    int tbad;
+                    const double L0 = target_lse(A, r, u, &tbad);
+                    const double tot = X.sum(trav_fill<DT>(A, vec, S, cached, trow, drow, L0, Ld, s_exp));
+                    L = L0 + log(tot);
+                    if (tid == 0) {
+                        s_stk[top].L = L;
+                        s_cache = cached ? u : -1;
+                    }
+                }
+                const int c = nd.fc + E.left;
+                const int y = A.node_tok[tb + c];
+                if (y < 0 || y >= A.V) {
+                    add_status |= TSB_REQ_BAD_TOKEN;
+                    invalid = true;
+                    break;
+                }
+                const double py = exp((double)(load_logit<DT>(A.target, trow + y) * A.invT) - L);
+                const double qy = exp((double)(load_logit<DT>(A.draft, drow + y) * A.invT) - Ld);
+                const double num = E.A * py - E.C * qy;  // Z Mb_u(y) before the max
+                const double ms = qy / E.S;             // Ms_u(y)
+                double ac;
+                if (!(ms > 0.0))
+                    ac = (num > 0.0 && E.alpha > 0.0) ? 1.0 : 0.0;
+                else
+                    ac = num > 0.0 ? fmin(1.0, E.alpha * (num / E.Z) / ms) : 0.0;
+                __syncthreads();  // every thread has read s_stk[top] and s_cache
+                if (tid == 0) s_stk[top + 1] = TravEntry{c, 0, ac, 1.0, 0.0, 1.0, 1.0, (double)NAN};
+                __syncthreads();
+                ++top;
+                continue;
+            }
+            if (top == 0) {  // every child of the root rejected: the root is accepted
+                end_kind = 1;
+                break;
+            }
+            // test u: accept the path root .. u with probability alpha_u
+            const double U = u24d(rng_word(key, (uint32_t)u, kStreamAccept, 0u));
+            if (trace && tcount < TSB_TRACE_MAX) {
+                trace[tcount * 4 + 0] = u;
+                trace[tcount * 4 + 1] = U;
+                trace[tcount * 4 + 2] = E.alpha;
+                trace[tcount * 4 + 3] = -1.0;
+            }
+            ++tcount;
+            if (U < E.alpha) {
+                end_kind = 1;
+                break;
+            }
+            // u rejected: update its parent w with the quantities u was drawn from
+            const TravEntry W = s_stk[top - 1];
+            const int w = W.node;
+            const TreeNode nw = tree_node(A.tree, tb, w, n, A.D);  // checked when it was descended from
+            const size_t trow_w = ((size_t)r * B1 + w) * (size_t)A.V;
+            const size_t drow_w = ((size_t)r * A.D + nw.d) * (size_t)A.V;
+            const double Ld = A.draft_lse[(size_t)r * A.D + nw.d];
+            int tbad;
+            const double L0 = target_lse(A, r, w, &tbad);
+            const int yu = A.node_tok[tb + u];
+            const double qy = exp((double)(load_logit<DT>(A.draft, drow_w + yu) * A.invT) - Ld);
+            const double A2 = W.alpha * W.A / W.Z;
+            const double C2 = W.alpha * W.C / W.Z + 1.0 / W.S;
+            const bool hit = cached && s_cache == w;
+            __syncthreads();  // every thread has read s_stk and s_cache
+            if (cached && !hit) {
+                trav_fill<DT>(A, vec, S, true, trow_w, drow_w, L0, Ld, s_exp);
+                if (tid == 0) s_cache = w;
+            }
+            const double inv = exp(L0 - W.L);
+            double zp = 0.0;
+            visit_pq<DT>(A, vec, S, cached, trow_w, drow_w, L0, inv, Ld, s_exp, [&](int, double p, double q) {
+                const double rr = A2 * p - C2 * q;
+                zp += rr > 0.0 ? rr : 0.0;
+            });
+            const double T = X.sum(walk_sum(zp));
+            if (trace && tcount <= TSB_TRACE_MAX) trace[(tcount - 1) * 4 + 3] = T;
+            const int left = W.left + 1;
+            const double S2 = W.S - qy;
+            --top;
+            if ((T <= 0.0 && W.alpha >= 1.0) || (S2 <= 0.0 && left < nw.m)) {
+                end_kind = 2;
+                break;
+            }
+            if (tid == 0) {
+                TravEntry& e = s_stk[top];
+                e.left = left;
+                e.S = S2;
+                if (T > 0.0) {
+                    e.alpha = T / (T + (1.0 - W.alpha));
+                    e.A = A2;
+                    e.C = C2;
+                    e.Z = T;
+                } else {
+                    e.alpha = 0.0;
+                    e.A = 0.0;
+                    e.C = 0.0;
+                    e.Z = 1.0;
+                }
+            }
+            __syncthreads();
+        }
+        if (end_kind != 0) {
+            const TravEntry E = s_stk[top];
+            const int u = E.node;
+            const TreeNode nd = tree_node(A.tree, tb, u, n, A.D);
+            const size_t trow = ((size_t)r * B1 + u) * (size_t)A.V;
+            int tbad;
+            const double L0 = target_lse(A, r, u, &tbad);
+            bool from_p = end_kind == 2 || E.left == 0;  // a node whose residual was never formed: Mb = p
+            if (!from_p) {
+                // Gumbel-max of ln max(p - (C / A) q, 0) (the positive factor A and the normaliser Z shift
+                // every key alike)
+                const size_t drow = ((size_t)r * A.D + nd.d) * (size_t)A.V;
+                const double Ld = A.draft_lse[(size_t)r * A.D + nd.d];
+                const double lam = E.C / E.A;
+                const bool hit = cached && s_cache == u;
+                __syncthreads();
+                if (cached && !hit) trav_fill<DT>(A, vec, S, true, trow, drow, L0, Ld, s_exp);
+                const double inv = exp(L0 - E.L);
+                float best = -INFINITY;
+                int bidx = 0x7FFFFFFF;
+                const uint32_t node = (uint32_t)u;
+                if (cached) {
+                    const int nn = S.v1 - S.v0;
+                    for (int i4 = tid; i4 * 4 < nn; i4 += kWalkThreads) {
+                        const uint4 wv = rng_block(key, node, kStreamBonus, (uint32_t)((S.v0 >> 2) + i4));
+                        const uint32_t ws[4] = {wv.x, wv.y, wv.z, wv.w};
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const int i = i4 * 4 + e;
+                            if (i >= nn) break;
+                            const double rr = S.p[i] * inv - lam * S.q[i];
+                            if (rr > 0.0) {
+                                const float kv = logf((float)rr) + gumbel_f32(ws[e]);
+                                const int v = S.v0 + i;
+                                if (kv > best || (kv == best && v < bidx)) {
+                                    best = kv;
+                                    bidx = v;
+                                }
+                            }
+                        }
+                    }
+                } else {
+                    visit_pq<DT>(A, vec, S, false, trow, drow, L0, inv, Ld, s_exp, [&](int v, double p, double q) {
+                        const double rr = p - lam * q;
+                        if (rr > 0.0) {
+                            const float kv = logf((float)rr) + gumbel_f32(rng_word(key, node, kStreamBonus, (uint32_t)v));
+                            if (kv > best || (kv == best && v < bidx)) {
+                                best = kv;
+                                bidx = v;
+                            }
+                        }
+                    });
+                }
+                walk_argmax(&best, &bidx);
+                double unused;
+                const int fi = X.best(best, bidx, 0.0, &unused);
+                if (fi >= 0) {
+                    bonus_out = fi;
+                } else {
+                    from_p = true;
+                    end_kind = 2;
+                }
+            }
+            if (from_p) {
+                float bk;
+                int bi;
+                double unused;
+                bonus_from_p<DT>(A, vec, S, trow, isnan(E.L) ? L0 : E.L, key, (uint32_t)u, &bk, &bi);
+                bonus_out = X.best(bk, bi, 0.0, &unused);
+            }
+            if (end_kind == 2) add_status |= TSB_REQ_DEGENERATE_RESIDUAL;
+            nacc = top;
+            if (lead)
+                for (int i = 1; i <= top; ++i) {
+                    const int c = s_stk[i].node;
+                    A.out.acc_node[(size_t)r * A.D + i - 1] = c;
+                    A.out.acc_tok[(size_t)r * A.D + i - 1] = A.node_tok[tb + c];
+                }
+        }
+        if (X.timeout) add_status |= TSB_REQ_WALK_TIMEOUT;
+    }
+    walk_tail(A, r, g, G, n, draft_bad, invalid, nacc, bonus_out, add_status, tcount);
+}
+
 // ------------------------------------------------------------------ launch
 // Workgroups of the walk that are resident at once on the current device
 // (one per CU: the LDS cache fills a CU). Every launch of the walk stays
@@ -1254,7 +1551,7 @@ __global__ __launch_bounds__(kWalkThreads) void verify_pool_walk(WalkArgs A) {
 // kernel instance).
 static hipError_t walk_capacity(const void* fn, int kind, int dt, int vec, size_t lds, int* cap) {
     constexpr int kDevs = 64;
-    static std::atomic<int> cached[kDevs][2][2][2];
+    static std::atomic<int> cached[kDevs][3][2][2];
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
@@ -1365,6 +1662,27 @@ hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, con
     if ((e = hook_before(TSB_KERNEL_VERIFY_WALK, st)) != hipSuccess) return e;
     if ((e = launch_walk_grid(fn, A, c.R, geometry(c).G, cap, lds, st)) != hipSuccess) return e;
     return hook_after(TSB_KERNEL_VERIFY_WALK, st);
+}
+
+hipError_t launch_verify_traversal(const tsb_config& c, float invT, const void* draft, const double* draft_lse,
+                                   const void* target, const tsb_tree& tree, const int32_t* node_tok, uint32_t step,
+                                   const tsb_verdict& out, char* ws, hipStream_t st) {
+    hipError_t e = launch_target_partials(c, invT, target, tree, ws, st);
+    if (e != hipSuccess) return e;
+    WalkArgs A = walk_args(c, invT, draft, draft_lse, target, tree, node_tok, step, out, ws);
+    const bool vec4 = c.V % 4 == 0 && ((uintptr_t)target & 15) == 0 && ((uintptr_t)draft & 15) == 0;
+    const void* fn = nullptr;
+    if (c.dtype == TSB_BF16)
+        fn = vec4 ? (const void*)verify_traversal<TSB_BF16, true> : (const void*)verify_traversal<TSB_BF16, false>;
+    else
+        fn = vec4 ? (const void*)verify_traversal<TSB_F32, true> : (const void*)verify_traversal<TSB_F32, false>;
+    const size_t lds = 2 * (size_t)kWalkCache * sizeof(double);
+    int cap = 0;
+    if ((e = walk_capacity(fn, 2, c.dtype == TSB_BF16 ? 1 : 0, vec4 ? 1 : 0, lds, &cap)) != hipSuccess) return e;
+    if (cap < 1) return hipErrorLaunchOutOfResources;
+    if ((e = hook_before(TSB_KERNEL_TRAVERSAL_WALK, st)) != hipSuccess) return e;
+    if ((e = launch_walk_grid(fn, A, c.R, geometry(c).G, cap, lds, st)) != hipSuccess) return e;
+    return hook_after(TSB_KERNEL_TRAVERSAL_WALK, st);
 }
 
 hipError_t launch_pool_verify(const tsb_config& c, int P, float invT, const void* draft, const float* trans,

@@ -42,6 +42,11 @@ hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, con
                          const void* target, const tsb_tree& tree, const int32_t* node_tok, uint32_t step,
                          const tsb_verdict& out, char* ws, hipStream_t st);
 
+// Traversal verification (sequence-level RRS over the tree) instead of WoR-RRS.
+hipError_t launch_verify_traversal(const tsb_config& c, float invT, const void* draft, const double* draft_lse,
+                                   const void* target, const tsb_tree& tree, const int32_t* node_tok, uint32_t step,
+                                   const tsb_verdict& out, char* ws, hipStream_t st);
+
 // Sparse candidate pools of P tokens with context-dependent q_u.
 hipError_t launch_pool_partials(const tsb_config& c, int P, float invT, const void* draft, uint64_t* pk, int* pf,
                                 int32_t* req_status, hipStream_t st);

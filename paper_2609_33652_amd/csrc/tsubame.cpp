@@ -223,6 +223,43 @@ tsb_status tsb_step(const tsb_config* cfg, const void* draft, const void* target
     return TSB_OK;
 }
 
+tsb_status tsb_verify_traversal(const tsb_config* cfg, const void* draft, const double* draft_lse,
+                                const void* target, const tsb_tree* tree, const int32_t* node_tok, uint32_t step,
+                                const tsb_verdict* out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    g_last_error[0] = 0;
+    TRY(check_config(cfg));
+    if (!draft || !draft_lse || !target || !node_tok)
+        return fail(TSB_E_NULL, "tsb_verify_traversal: a required array is NULL");
+    TRY(check_tree(tree));
+    TRY(check_verdict(out));
+    TRY(check_ws(cfg, workspace, workspace_bytes));
+    const hipError_t e = tsb::launch_verify_traversal(*cfg, inv_temperature(cfg->temperature), draft, draft_lse,
+                                                      target, *tree, node_tok, step, *out, (char*)workspace, stream);
+    return e == hipSuccess ? TSB_OK : hip_fail(e, "tsb_verify_traversal");
+}
+
+tsb_status tsb_step_traversal(const tsb_config* cfg, const void* draft, const void* target, uint32_t step,
+                              double* draft_lse, int32_t* topk_tok, float* topk_lp, const tsb_tree* tree,
+                              int32_t* node_tok, const tsb_verdict* out, void* workspace, size_t workspace_bytes,
+                              hipStream_t stream) {
+    g_last_error[0] = 0;
+    TRY(check_config(cfg));
+    if (!draft || !target || !draft_lse || !topk_tok || !topk_lp || !node_tok)
+        return fail(TSB_E_NULL, "tsb_step_traversal: a required array is NULL");
+    TRY(check_tree(tree));
+    TRY(check_verdict(out));
+    TRY(check_ws(cfg, workspace, workspace_bytes));
+    const float invT = inv_temperature(cfg->temperature);
+    char* ws = (char*)workspace;
+    hipError_t e = tsb::launch_plan(*cfg, invT, draft, draft_lse, topk_tok, topk_lp, *tree, out->req_status, ws, stream);
+    if (e != hipSuccess) return hip_fail(e, "tsb_step_traversal/plan");
+    e = tsb::launch_replay(*cfg, invT, draft, topk_tok, *tree, step, node_tok, ws, stream);
+    if (e != hipSuccess) return hip_fail(e, "tsb_step_traversal/replay");
+    e = tsb::launch_verify_traversal(*cfg, invT, draft, draft_lse, target, *tree, node_tok, step, *out, ws, stream);
+    if (e != hipSuccess) return hip_fail(e, "tsb_step_traversal/verify");
+    return TSB_OK;
+}
+
 tsb_status tsb_step_noalloc(const tsb_config* cfg, const void* draft, const void* target, uint32_t step,
                             double* draft_lse, int32_t* topk_tok, float* topk_lp, const tsb_tree* tree,
                             int32_t* node_tok, const tsb_verdict* out, hipStream_t stream) {
@@ -399,6 +436,6 @@ const char* tsb_status_string(tsb_status s) {
 
 const char* tsb_last_error(void) { return g_last_error; }
 
-int32_t tsb_version(void) { return 200; }
+int32_t tsb_version(void) { return 201; }
 
 }  // extern "C"

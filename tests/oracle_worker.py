@@ -54,6 +54,19 @@ def request_step(d, t, T, K, B, seed, step, r, gtree, gtok):
     return out
 
 
+def request_step_traversal(d, t, T, K, B, seed, step, r, gtree, gtok):
+    """As request_step with traversal verification on the HIP path's topology and tokens."""
+    pl = ostep.plan_request(d, T, K, B)
+    out = dict(plan=pl, replay=None, verify=None)
+    if gtree is None or pl["status"] & STATUS_NONFINITE:
+        return out
+    tok, mg = oreplay.replay(scaled(d, inv_temperature(T)), gtree, seed, step, r)
+    out["replay"] = (tok, mg)
+    if t is not None:
+        out["verify"] = ostep.verify_request(d, t, gtree, gtok, pl["lse64"], T, seed, step, r, verifier="traversal")
+    return out
+
+
 def request_step_naive(d, t, T, K, B, seed, step, r, gtree, gtok):
     """First + Naive oracle outputs of one request-step: the plan and First tokens from the draft, and
     target-sample matching on the HIP path's topology and node tokens."""
@@ -108,7 +121,8 @@ def request_step_pool(d, t, T, K, B, seed, step, r, gtree, gtok, trans, P):
     return out
 
 
-KINDS = {"rrs": request_step, "naive": request_step_naive, "pool": request_step_pool}
+KINDS = {"rrs": request_step, "naive": request_step_naive, "pool": request_step_pool,
+         "traversal": request_step_traversal}
 
 
 def run(task):

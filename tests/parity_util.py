@@ -252,6 +252,77 @@ def compare_request_naive(h, r, res, tally, D, where):
         compare_naive(h, r, res["naive"], tally, D, where)
 
 
+def compare_traversal(h, r, vr, tree, tally, D, where=""):
+    """The traversal of request r test by test (trace rows: tested node, U, alpha, T after its rejection),
+    then its outputs. The first test whose outcome differs is excused only at its own oracle margin."""
+    n_acc = int(h["n_acc"][r])
+    st = int(h["req_status"][r])
+    if vr["n_acc"] < 0:
+        assert n_acc == -1 and st & tsb.REQ_NONFINITE and int(h["bonus"][r]) == -1, where
+        tally.ok("verify")
+        return "exact"
+    tr = h["trace"][r].numpy()
+    tests, Ts = vr["tests"], vr["residual_T"]
+    zi = 0
+    for i in range(min(len(tests), tr.shape[0])):
+        u, U, alpha, ok = tests[i]
+        gu, gU, ga, gT = tr[i]
+        if int(gu) != u:
+            raise AssertionError("traversal tests node %d where the oracle tests %d %s (test %d)"
+                                 % (int(gu), u, where, i))
+        assert gU == U, (where, i, gU, U)
+        assert _close(ga, alpha), (where, i, "alpha", ga, alpha)
+        g_ok = gU < ga
+        if g_ok != ok:
+            mg = abs(U - alpha)
+            if 0 < mg < NEAR_TIE:
+                tally.flag("verify", "traversal near-tie %.2e at test %d %s" % (mg, i, where))
+                return "flagged"
+            raise AssertionError("acceptance of node %d differs %s: gpu U %r alpha %r, oracle alpha %r"
+                                 % (u, where, gU, ga, alpha))
+        if not ok:
+            if zi < len(Ts):
+                assert _close(gT, Ts[zi]), (where, i, "residual mass", gT, Ts[zi])
+            zi += 1
+    if len(tests) <= tr.shape[0]:
+        assert int((tr[:, 0] >= 0).sum()) == len(tests), (where, "trace length")
+    exp_path = ([int(x) for x in vr["acc_node"]], [int(x) for x in vr["acc_tok"]])
+    got_path = (list(h["acc_node"][r, :max(n_acc, 0)].numpy()), list(h["acc_tok"][r, :max(n_acc, 0)].numpy()))
+    if n_acc != vr["n_acc"] or got_path != exp_path:
+        raise AssertionError("accepted path differs with every test agreeing %s: gpu %s oracle %s"
+                             % (where, (n_acc, got_path), (vr["n_acc"], exp_path)))
+    assert list(h["acc_node"][r, n_acc:].numpy()) == [-1] * (D - n_acc), where
+    assert bool(st & tsb.REQ_DEGENERATE_RESIDUAL) == bool(vr["status"] & STATUS_DEGENERATE_RESIDUAL), where
+    assert not st & (tsb.REQ_WALK_TIMEOUT | tsb.REQ_BAD_TREE | tsb.REQ_BAD_TOKEN), where
+    lt = h["target_lse"][r].numpy()[: len(vr["lse_t"])]
+    tally.max_lse_err = max(tally.max_lse_err, float(np.abs(lt - vr["lse_t"]).max()))
+    np.testing.assert_allclose(lt, vr["lse_t"], rtol=0, atol=LSE_T_ATOL, err_msg=where)
+    if int(h["bonus"][r]) != vr["bonus"]:
+        mg = [m for m in vr["margins"] if m[0] == "bonus"][-1][2]
+        if 0 < mg < NEAR_TIE:
+            tally.flag("verify", "traversal bonus near-tie %.2e %s" % (mg, where))
+            return "flagged"
+        raise AssertionError("bonus differs %s: gpu %d oracle %d (margin %g)" % (where, int(h["bonus"][r]),
+                                                                                  vr["bonus"], mg))
+    tally.ok("verify")
+    return "exact"
+
+
+def compare_request_traversal(h, r, res, tally, D, where):
+    """Plan, replay and traversal verification of one request-step."""
+    compare_plan(h, r, res["plan"], tally, where)
+    tally.request_steps += 1
+    if res["replay"] is None:
+        assert int(h["req_status"][r]) & tsb.REQ_NONFINITE or int(h["n_nodes"][r]) == 1, where
+        return
+    tree = tree_dict_np(h, r)
+    n = tree["n_nodes"]
+    o_tok, mg = res["replay"]
+    compare_replay(h["node_tok"][r, :n].numpy().astype(np.int64), o_tok, mg, tree, tally, where)
+    if res["verify"] is not None:
+        compare_traversal(h, r, res["verify"], tree, tally, D, where)
+
+
 def compare_request(h, r, res, tally, D, where):
     """All three stages of one request-step (res: oracle_worker.request_step output)."""
     compare_plan(h, r, res["plan"], tally, where)
@@ -341,7 +412,8 @@ def compare_request_pool(h, r, res, tally, D, where):
         compare_verify(h, r, res["verify"], g, tally, D, where)
 
 
-COMPARE = {"rrs": compare_request, "naive": compare_request_naive, "pool": compare_request_pool}
+COMPARE = {"rrs": compare_request, "naive": compare_request_naive, "pool": compare_request_pool,
+           "traversal": compare_request_traversal}
 
 
 def run_rounds(pool, cfg, seed, steps, kind, gpu_round, step0=0, sets=4, gen_device="cpu", name="", check=None,

@@ -33,7 +33,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == set(tsb.EXPORTS)
     for n in names:
         assert hasattr(lib, n), n
-    assert lib.tsb_version() == 200
+    assert lib.tsb_version() == 201
 
 
 def _cfg(**kw):
@@ -207,3 +207,20 @@ def test_step_noalloc_validates_before_any_device_call(lib):
     bad_v.n_acc = None
     assert lib.tsb_step_noalloc(ctypes.byref(batched), FAKE, FAKE, 0, FAKE, FAKE, FAKE, ctypes.byref(t), FAKE,
                                 ctypes.byref(bad_v), None) == 1
+
+
+def test_traversal_entry_points_validate(lib):
+    cfg = _cfg()
+    need = lib.tsb_workspace_bytes(ctypes.byref(cfg))
+    t = _tree()
+    v = _verdict()
+    assert lib.tsb_verify_traversal(ctypes.byref(_cfg(K=0)), FAKE, FAKE, FAKE, ctypes.byref(t), FAKE, 0,
+                                    ctypes.byref(v), FAKE, need, None) == 2
+    assert lib.tsb_verify_traversal(ctypes.byref(cfg), FAKE, None, FAKE, ctypes.byref(t), FAKE, 0, ctypes.byref(v),
+                                    FAKE, need, None) == 1
+    assert lib.tsb_verify_traversal(ctypes.byref(cfg), FAKE, FAKE, FAKE, ctypes.byref(t), FAKE, 0, ctypes.byref(v),
+                                    FAKE, need - 1, None) == 5
+    assert lib.tsb_step_traversal(ctypes.byref(_cfg(temperature=-2.0)), FAKE, FAKE, 0, FAKE, FAKE, FAKE,
+                                  ctypes.byref(t), FAKE, ctypes.byref(v), FAKE, need, None) == 4
+    assert lib.tsb_step_traversal(ctypes.byref(cfg), FAKE, FAKE, 0, FAKE, FAKE, FAKE, ctypes.byref(t), None,
+                                  ctypes.byref(v), FAKE, need, None) == 1
