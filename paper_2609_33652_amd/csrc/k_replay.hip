@@ -33,6 +33,7 @@
 namespace tsb {
 
 constexpr int kTileGroups = kReplayTile / 4;  // groups of four tokens per tile
+constexpr int kPassGroups = kTileGroups / 2;  // groups per compaction pass
 constexpr int kScanWaves = kBlock / kWave;
 constexpr int kScanWorkgroups = 1536;  // resident at 6 waves per SIMD
 
@@ -179,6 +180,48 @@ __device__ __forceinline__ void load_b4(const void* __restrict__ draft, size_t b
     for (int e = 0; e < 4; ++e) b[e] = (e0 + e < tn) ? x[e] * invT - cd : -INFINITY;
 }
 
+// Raw logits of four consecutive tokens of a tile; positions at or past `tn`
+// read as -inf. FULL: the whole tile exists and rows are vector-aligned, so
+// the four are one unconditional load.
+template <int DT, bool VEC, bool FULL>
+__device__ __forceinline__ void load_x4(const void* __restrict__ draft, size_t base, int e0, int tn, float x[4]) {
+    if (FULL || (VEC && e0 + 4 <= tn)) {
+        if (DT == TSB_BF16) {
+            const uint2 raw = *(const uint2*)((const uint16_t*)draft + base + e0);
+            x[0] = __uint_as_float(raw.x << 16);
+            x[1] = __uint_as_float(raw.x & 0xFFFF0000u);
+            x[2] = __uint_as_float(raw.y << 16);
+            x[3] = __uint_as_float(raw.y & 0xFFFF0000u);
+        } else {
+            const float4 a = *(const float4*)((const float*)draft + base + e0);
+            x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[e] = (e0 + e < tn) ? load_logit<DT>(draft, base + e0 + e) : -INFINITY;
+    }
+}
+
+// Smallest raw Philox word a token may hold for its key to reach thr when its
+// b = fl32(a - c_d) is at most `bmax`: a necessary condition only (words
+// below it are certain misses, words at or above it are evaluated exactly).
+// With x = thr - bmax, the key can reach thr only if G(u) >= x - s for a
+// slack s that covers the rounding of the binary32 Gumbel map and of the key
+// sum; G(u) >= y means -ln u <= e^-y, and -ln u >= 1 - u, so it needs
+// 1 - u <= e^(s - x), i.e. k = w >> 9 >= 2^23 (1 - e^(s - x)) - 1/2 for
+// u = (2k + 1) 2^-24. s = 1/4 plus a few units in the last place of thr
+// (far above the Gumbel map's error, which stays near 1e-6). e^(s - x) comes
+// from the hardware base-2 exponential (about one unit in the last place;
+// a result flushed to zero only drops the bound by less than the margin);
+// the floor and the margin of two keep the result below the exact bound
+// despite the rounding of the binary32 arithmetic here. An infinite or NaN
+// gap gives 0 (every word is evaluated exactly).
+__device__ __forceinline__ uint32_t gumbel_word_floor(float thr, float bmax, float slack) {
+    const float E = __builtin_amdgcn_exp2f((slack - (thr - bmax)) * 1.44269504088896341f);
+    const float k = floorf(8388608.0f - E * 8388608.0f) - 2.0f;
+    return (uint32_t)fmaxf(k, 0.0f) << 9;
+}
+
 template <int DT, bool VEC>
 __global__ __launch_bounds__(kBlock) void replay_scan(const void* __restrict__ draft, int V, int D, int B, int K,
                                                       int T, float invT, const int32_t* __restrict__ topk_tok,
@@ -186,9 +229,10 @@ __global__ __launch_bounds__(kBlock) void replay_scan(const void* __restrict__ d
                                                       const int* __restrict__ ptotal, const float4* __restrict__ rec,
                                                       uint32_t k0, uint32_t k1, uint32_t step,
                                                       uint64_t* __restrict__ out_cand, int* __restrict__ out_cnt) {
-    __shared__ int s_queue[kScanWaves][kTileGroups];  // surviving groups, per wave
+    // surviving groups of the current pass, per wave: (group, largest b)
+    __shared__ uint2 s_queue[kScanWaves][kPassGroups];
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    int* queue = s_queue[wave];
+    uint2* queue = s_queue[wave];
     const long long items = (long long)ptotal[0] * T;
     const long long nw = (long long)gridDim.x * kScanWaves;
     for (long long it = (long long)blockIdx.x * kScanWaves + wave; it < items; it += nw) {
@@ -207,31 +251,8 @@ __global__ __launch_bounds__(kBlock) void replay_scan(const void* __restrict__ d
         const int t0 = t * kReplayTile;
         const int tn = min(kReplayTile, V - t0);
         const size_t tbase = rowbase + t0;
-
-        // compact the groups with a token that can still reach thr (a quarter
-        // of the tile's loads in flight at a time)
-        constexpr int kPer = kTileGroups / kWave;  // groups per lane
-        constexpr int kBatch = kPer / 4;
-        int qn = 0;
-#pragma unroll 1
-        for (int k0b = 0; k0b < kPer; k0b += kBatch) {
-            float bq[kBatch][4];
-#pragma unroll
-            for (int k = 0; k < kBatch; ++k)
-                load_b4<DT, VEC>(draft, tbase, ((k0b + k) * kWave + lane) * 4, tn, invT, cd, bq[k]);
-#pragma unroll
-            for (int k = 0; k < kBatch; ++k) {
-                const float mx = fmaxf(fmaxf(bq[k][0], bq[k][1]), fmaxf(bq[k][2], bq[k][3]));
-                const bool live = mx >= bound && mx > -INFINITY;
-                const uint64_t bal = __ballot(live);
-                if (live) queue[qn + __popcll(bal & ((1ull << lane) - 1ull))] = (k0b + k) * kWave + lane;
-                qn += __popcll(bal);
-            }
-        }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
-        // Philox and the keys for the survivors; the m best keys >= thr
+        const bool full = VEC && tn == kReplayTile;
+        const float slack = 0.25f + fabsf(thr) * 0x1p-20f;
         RngKey key;
         key.k0 = k0;
         key.k1 = k1;
@@ -240,33 +261,73 @@ __global__ __launch_bounds__(kBlock) void replay_scan(const void* __restrict__ d
         const uint32_t blk0 = (uint32_t)(t0 >> 2);
         WaveTopList top;
         top.init(m);
-        for (int base = 0; base < qn; base += kWave) {
-            const int q = base + lane;
-            const bool valid = q < qn;
-            const int gl = valid ? queue[q] : 0;
-            float bv[4];
-            load_b4<DT, VEC>(draft, tbase, gl * 4, valid ? tn : 0, invT, cd, bv);
-            const uint4 w = rng_block(key, (uint32_t)u, kStreamReplay, blk0 + (uint32_t)gl);
-            const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
-            float kv[4];
-            bool hit = false;
+#pragma unroll 1
+        for (int g0 = 0; g0 < kTileGroups; g0 += kPassGroups) {
+            // 1. largest b of each group of four (b = fl32(x invT - c_d) is
+            // non-decreasing in x, so it is that of the largest raw logit);
+            // groups whose largest b cannot reach thr are dropped, the rest
+            // are compacted within the wave
+            constexpr int kPer = kPassGroups / kWave;  // groups per lane
+            float gx[kPer];
+            if (full) {
+                float x[kPer][4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const bool in = bv[e] >= bound && bv[e] > -INFINITY;
-                kv[e] = in ? bv[e] + gumbel_f32(ws[e]) : -INFINITY;
-                hit = hit || kv[e] >= thr;
+                for (int k = 0; k < kPer; ++k) load_x4<DT, VEC, true>(draft, tbase, (g0 + k * kWave + lane) * 4, tn, x[k]);
+#pragma unroll
+                for (int k = 0; k < kPer; ++k) gx[k] = fmaxf(fmaxf(x[k][0], x[k][1]), fmaxf(x[k][2], x[k][3]));
+            } else {
+#pragma unroll
+                for (int k = 0; k < kPer; ++k) {
+                    float x[4];
+                    load_x4<DT, VEC, false>(draft, tbase, (g0 + k * kWave + lane) * 4, tn, x);
+                    gx[k] = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+                }
             }
-            // most keys stay below thr: the list is touched only when one does not
-            if (__ballot(hit) == 0) continue;
+            int qn = 0;
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
-                top.offer(cand_key(kv[e], (uint32_t)(t0 + gl * 4 + e)), kv[e] >= thr && kv[e] > -INFINITY);
+            for (int k = 0; k < kPer; ++k) {
+                const float bmax = gx[k] * invT - cd;
+                const bool live = bmax >= bound && bmax > -INFINITY;
+                const uint64_t bal = __ballot(live);
+                if (live)
+                    queue[qn + __popcll(bal & ((1ull << lane) - 1ull))] =
+                        make_uint2((uint32_t)(g0 + k * kWave + lane), __float_as_uint(bmax));
+                qn += __popcll(bal);
+            }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+            // 2. Philox for the survivors; a word below its group's floor is a
+            // certain miss; groups holding a word at or above it get their
+            // exact keys, and the m best keys >= thr are kept
+            for (int base = 0; base < qn; base += kWave) {
+                const int q = base + lane;
+                const bool valid = q < qn;
+                const uint2 ent = queue[valid ? q : 0];
+                const int gl = (int)ent.x;
+                const uint4 w = rng_block(key, (uint32_t)u, kStreamReplay, blk0 + (uint32_t)gl);
+                const uint32_t wf = gumbel_word_floor(thr, __uint_as_float(ent.y), slack);
+                const bool pass = valid && max(max(w.x, w.y), max(w.z, w.w)) >= wf;
+                if (__ballot(pass) == 0) continue;
+                float bv[4];
+                load_b4<DT, VEC>(draft, tbase, gl * 4, pass ? tn : 0, invT, cd, bv);
+                const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+                float kv[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const bool in = bv[e] >= bound && bv[e] > -INFINITY;
+                    kv[e] = in ? bv[e] + gumbel_f32(ws[e]) : -INFINITY;
+                }
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    top.offer(cand_key(kv[e], (uint32_t)(t0 + gl * 4 + e)), kv[e] >= thr && kv[e] > -INFINITY);
+            }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");  // the queue is rewritten by the next pass
         }
         const size_t o = (size_t)node * (size_t)T + t;
         const int cnt = __popcll(__ballot(lane < m && top.v != 0));
         if (lane < cnt) out_cand[o * TSB_MAX_K + lane] = top.v;
         if (lane == 0) out_cnt[o] = cnt;
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");  // the queue is rewritten by the next item
     }
 }
 

@@ -67,6 +67,8 @@ def test_workspace_content_does_not_matter(kind):
         for k in OUT_KEYS:
             if kind == "step_first" and k in ("trace", "target_lse"):
                 continue  # the Naive walk writes neither
+            if kind != "pool_step" and k == "pool_tok":
+                continue  # written by the pool round only (an unwritten output buffer)
             assert _same(a[k], b[k]), (kind, s, hex(fill), k)
         assert int((a["req_status"] & tsb.REQ_WALK_TIMEOUT).sum()) == 0
 
