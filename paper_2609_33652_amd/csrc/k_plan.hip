@@ -52,22 +52,29 @@ constexpr int kDraftU = 4;     // 8-logit groups per thread per chunk
 template <bool STATS>
 constexpr int cand_cap() { return STATS ? 128 : 256; }
 constexpr int kDraftChunk = kDraftThreads * 8 * kDraftU;
-constexpr int kFinalRegs = 8;  // keys per lane in the final selection (512 in all)
 // recorded groups per lane before the wave flushes (the pool selection, with
 // no table in LDS and a weaker first filter at K = 64, keeps more)
 template <bool STATS>
 constexpr int rec_slots() { return STATS ? 8 : 24; }
 constexpr int kRecBatch = 4;   // recorded groups re-read at once
 
-// Exponential table over bf16 patterns: biased exponent field in
-// [kTabExpLo, kTabExpLo + kTabBinades), both signs; entry 2 t + sign for
-// t = (pattern & 0x7FFF) - kTabBase, and two last entries 0.0 that patterns
-// outside the table read (t clamped to kTabHalf).
+// Exponential table over bf16 patterns with biased exponent field in
+// [kTabExpLo, kTabExpLo + kTabBinades) (2^-16 <= |x| < 64): the entry of
+// magnitude index t = (pattern & 0x7FFF) - kTabBase and sign bit s sits at
+// byte offset 8 t + 32768 s, so that the offsets of both halves of a word of
+// two patterns come from one shift of the clamped indices and one OR of the
+// sign bits. Index kTabHalf holds 0.0 for both signs: patterns outside the
+// table are clamped onto it. The gap between the positive half and the
+// negative half holds other LDS data of the workgroup.
 constexpr uint32_t kTabExpLo = 111;  // 2^-16
 constexpr int kTabBinades = 22;      // up to 2^6 (exclusive)
 constexpr int kTabHalf = kTabBinades * 128;
-constexpr int kTabEntries = 2 * kTabHalf + 2;
 constexpr uint32_t kTabBase = kTabExpLo << 7;
+constexpr int kTabNeg = 32768 / 8;               // first binary64 slot of the negative half
+constexpr int kTabDoubles = kTabNeg + kTabHalf + 1;
+constexpr int kTabGap = kTabHalf + 1;            // first free slot of the gap
+constexpr int kSpecialCap = 256;                 // deferred out-of-table patterns per wave
+static_assert(8 * kTabHalf < 32768, "the positive half must end below the sign bit of an offset");
 
 // Whether the table may be used at this inverse temperature: every entry
 // e^(fl32(x invT)), |x| < 64, is a normal binary64 number (and a sum of up
@@ -75,7 +82,7 @@ constexpr uint32_t kTabBase = kTabExpLo << 7;
 inline bool draft_table_ok(float invT) { return 63.75f * invT < 680.0f; }
 // Segments shorter than this evaluate every exponential (the table would
 // cost more to build than it saves).
-constexpr int kTableMinSeg = 32768;
+constexpr int kTableMinSeg = 8192;
 
 // Raw words of one 8-logit group: four words of bf16 pairs, or eight binary32.
 template <int DT>
@@ -297,46 +304,28 @@ struct CandBuf {
 
 // Re-reads the groups this wave's lanes recorded (nrec per lane, offsets in
 // s_rec[.][tid]) and offers their logits, one group per lane per round.
-template <int DT, bool VEC, int CAP>
+template <int DT, bool VEC, int CAP, int BATCH = kRecBatch>
 __device__ __forceinline__ void flush_recorded(CandBuf<CAP>& cb, const void* __restrict__ draft, size_t rowbase, int hi, int K,
                                int (*s_rec)[kDraftThreads], int nrec, unsigned long long* s_key) {
     const int tid = threadIdx.x;
     int rounds = nrec;
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) rounds = max(rounds, __shfl_xor(rounds, o, kWave));
-    for (int r0 = 0; r0 < rounds; r0 += kRecBatch) {
-        Raw8<DT> g[kRecBatch];
-        int off[kRecBatch];
+    for (int r0 = 0; r0 < rounds; r0 += BATCH) {
+        Raw8<DT> g[BATCH];
+        int off[BATCH];
 #pragma unroll
-        for (int r = 0; r < kRecBatch; ++r) {
+        for (int r = 0; r < BATCH; ++r) {
             off[r] = r0 + r < nrec ? s_rec[r0 + r][tid] : 0;
             if (r0 + r < nrec) load_raw8<DT, VEC>(draft, rowbase, off[r], hi, g[r]);
         }
 #pragma unroll
-        for (int r = 0; r < kRecBatch; ++r) {
+        for (int r = 0; r < BATCH; ++r) {
             if (r0 + r >= rounds) break;
             float x[8];
             raw8_values<DT>(g[r], x);
             cb.offer8(x, off[r], hi, r0 + r < nrec, K, s_key);
         }
-    }
-}
-
-// The entries of the wave buffers as one flat list (buffer 0's n[0], then
-// buffer 1's, ...), NR per lane: entry r * 64 + lane goes to v[r], 0 past
-// the end.
-template <int NR, int CAP>
-__device__ __forceinline__ void gather_flat(const uint64_t (*buf)[CAP], const int* n, uint64_t (&v)[NR]) {
-    const int lane = lane_id();
-    int w = 0, start = 0;
-#pragma unroll
-    for (int r = 0; r < NR; ++r) {
-        const int i = r * kWave + lane;
-        while (w < kDraftWaves && i >= start + n[w]) {
-            start += n[w];
-            ++w;
-        }
-        v[r] = w < kDraftWaves ? buf[w][i - start] : 0ull;
     }
 }
 
@@ -357,20 +346,49 @@ __device__ __forceinline__ void eval_term(float a, float& m, double& sum, bool& 
 }
 
 // Table part of the normaliser for the two bf16 patterns of a word, with
-// packed 16-bit arithmetic: adds their entries (0.0 outside the table) and
-// reports whether either is outside. The byte offset of an entry is
-// 16 t + 8 sign, below 2^16.
+// packed 16-bit arithmetic: adds their entries to s0 and s1 (0.0 outside the
+// table) and keeps the running packed maximum of the unclamped indices
+// (a half at or above kTabHalf is a pattern outside the table; patterns below
+// it wrap to large indices). Clamped indices stay below 2^12, so one 32-bit
+// shift by 3 scales both halves.
 typedef unsigned short tsb_u16x2 __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ bool tab_pair(uint32_t w, const double* tab, double& sumF) {
+typedef short tsb_i16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ void tab_word(uint32_t w, const double* tab, double& s0, double& s1, tsb_u16x2& tmax) {
     const tsb_u16x2 base = {(unsigned short)kTabBase, (unsigned short)kTabBase};
     const tsb_u16x2 lim = {(unsigned short)kTabHalf, (unsigned short)kTabHalf};
-    const tsb_u16x2 t = __builtin_bit_cast(tsb_u16x2, w & 0x7FFF7FFFu) - base;  // wraps below the table
+    const tsb_u16x2 t = __builtin_bit_cast(tsb_u16x2, w & 0x7FFF7FFFu) - base;
+    tmax = __builtin_elementwise_max(tmax, t);
     const tsb_u16x2 tc = __builtin_elementwise_min(t, lim);
-    const tsb_u16x2 a = tc << (tsb_u16x2){4, 4};
-    const uint32_t off = __builtin_bit_cast(uint32_t, a) | ((w >> 12) & 0x00080008u);
-    sumF += *(const double*)((const char*)tab + (off & 0xFFFFu));
-    sumF += *(const double*)((const char*)tab + (off >> 16));
-    return __builtin_bit_cast(uint32_t, tc) != __builtin_bit_cast(uint32_t, t);
+    const uint32_t off = (__builtin_bit_cast(uint32_t, tc) << 3) | (w & 0x80008000u);
+    s0 += *(const double*)((const char*)tab + (off & 0xFFFFu));
+    s1 += *(const double*)((const char*)tab + (off >> 16));
+}
+
+// Order-preserving signed 16-bit keys of the two bf16 patterns of a word
+// (a larger value has a larger key; -0 sits just below +0; NaN patterns sit
+// above +inf or below -inf by their sign).
+__device__ __forceinline__ tsb_i16x2 bf16_keys(uint32_t w) {
+    const tsb_i16x2 v = __builtin_bit_cast(tsb_i16x2, w);
+    const tsb_i16x2 sgn = v >> (tsb_i16x2){15, 15};  // 0 or -1 per half
+    return v ^ (sgn & (tsb_i16x2){0x7FFF, 0x7FFF});
+}
+
+// Key of the smallest bf16 value at least x (x not NaN): the pattern of a
+// positive x rounded up, of a negative x truncated toward zero.
+__device__ __forceinline__ int bf16_key_at_least(float x) {
+    const uint32_t b = __float_as_uint(x);
+    const uint32_t p = (b >> 31) ? (b >> 16) : ((b + 0xFFFFu) >> 16);
+    const int v = (int)(short)(uint16_t)p;
+    return v < 0 ? v ^ 0x7FFF : v;
+}
+
+// Whether some logit of the group (four words of bf16 pairs) has a key above
+// kf (k2 = kf in both halves).
+__device__ __forceinline__ bool group_reaches(const uint32_t (&w)[4], tsb_i16x2 k2) {
+    const tsb_i16x2 a = __builtin_elementwise_max(bf16_keys(w[0]), bf16_keys(w[1]));
+    const tsb_i16x2 b = __builtin_elementwise_max(bf16_keys(w[2]), bf16_keys(w[3]));
+    const tsb_i16x2 m = __builtin_elementwise_max(__builtin_elementwise_max(a, b), k2);
+    return __builtin_bit_cast(uint32_t, m) != __builtin_bit_cast(uint32_t, k2);
 }
 
 // Per-workgroup-lane state of the draft stream: candidate buffer, recorded
@@ -387,55 +405,103 @@ struct DraftState {
     const double* exp_lds;
     int (*rec)[kDraftThreads];
     unsigned long long* key;
+    uint16_t* special;      // table path: the wave's deferred patterns outside the table
     int nrec = 0;           // groups recorded by this lane
+    int nspecial = 0;       // deferred patterns (wave-uniform; past kSpecialCap: the list overflowed)
+    bool rec_full = false;  // table path: a group passed with this lane's list full
     double sumF = 0.0;      // sum of table entries (reference 0)
     float m = -INFINITY;    // evaluated path: running maximum of the scaled logits
     double sum = 0.0;       // evaluated path: sum of e^(a - m)
     bool bad = false;       // a NaN or +inf scaled logit
 };
 
+// Records a candidate group in this lane's list. With the normaliser the
+// stream never flushes (the stream's registers are taken): a lane whose list
+// is full marks itself and offers its part of the segment again at the end.
+// The pool selection flushes between chunks instead (its first filter is
+// weak, so its lists fill).
+template <bool STATS, int CAP>
+__device__ __forceinline__ void record_group(DraftState<CAP>& St, int i0) {
+    if (!STATS || St.nrec < rec_slots<STATS>()) {
+        St.rec[St.nrec][threadIdx.x] = i0;
+        ++St.nrec;
+    } else {
+        St.rec_full = true;
+    }
+}
+
 // One chunk held in r, starting at base: normaliser terms, finiteness and
 // the recording of candidate groups.
-template <int DT, bool VEC, bool STATS, int CAP>
+template <int DT, bool VEC, bool STATS, bool TAB, int CAP>
 __device__ __forceinline__ void draft_chunk(const Raw8<DT> (&r)[kDraftU], int base, DraftState<CAP>& St) {
+    if constexpr (TAB) {
+      {
+        // table sum on packed pairs, four independent binary64 chains
+        tsb_u16x2 tmax = {0, 0};
+        double s4[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+        for (int u = 0; u < kDraftU; ++u)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int c = 2 * ((u * 4 + j) & 1);
+                tab_word(r[u].w[j], St.tab_lds, s4[c], s4[c + 1], tmax);
+                // eight table lookups in flight at a time (a whole chunk's
+                // would not fit the registers)
+                if (j == 3) __builtin_amdgcn_sched_barrier(0);
+            }
+        St.sumF += (s4[0] + s4[1]) + (s4[2] + s4[3]);
+        // patterns outside the table (rare; -inf adds nothing) are deferred
+        // to the wave's list and evaluated after the stream
+        const bool slow = (uint32_t)__builtin_elementwise_max(tmax.x, tmax.y) >= (uint32_t)kTabHalf;
+        if (__ballot(slow)) {
+#pragma unroll
+            for (int q = 0; q < 4 * kDraftU; ++q)
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const uint32_t p = (r[q >> 2].w[q & 3] >> (16 * h)) & 0xFFFFu;
+                    const bool out = ((p & 0x7FFFu) - kTabBase) >= (uint32_t)kTabHalf && p != 0xFF80u;
+                    const uint64_t b = __ballot(out);
+                    if (b) {
+                        if (out && St.nspecial + __popcll(b) <= kSpecialCap)
+                            St.special[St.nspecial + lanes_below_u64(b)] = (uint16_t)p;
+                        St.nspecial = min(St.nspecial + __popcll(b), kSpecialCap + 1);
+                    }
+                }
+        }
+        // candidates: a group is recorded when one of its logits reaches the
+        // filter, by order-preserving 16-bit keys
+        const int kf = bf16_key_at_least(St.cb.fx) - 1;
+        const tsb_i16x2 k2 = {(short)kf, (short)kf};
+#pragma unroll
+        for (int u = 0; u < kDraftU; ++u)
+            if (group_reaches(r[u].w, k2)) record_group<STATS>(St, base + (u * kDraftThreads + (int)threadIdx.x) * 8);
+        return;
+      }
+    }
 #pragma unroll
     for (int u = 0; u < kDraftU; ++u) {
         const int i0 = base + (u * kDraftThreads + (int)threadIdx.x) * 8;
         float x[8];
         raw8_values<DT>(r[u], x);
         if (STATS) {
-            if (St.use_tab) {
-                bool slow = false;
+            // evaluated path for every logit: rescale once per group
+            float a[8];
+            float am = -INFINITY;
 #pragma unroll
-                for (int j = 0; j < 4; ++j) slow |= tab_pair(r[u].w[j], St.tab_lds, St.sumF);
-                if (__ballot(slow)) {
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        const uint32_t hw = (j & 1) ? (r[u].w[j >> 1] >> 16) : r[u].w[j >> 1];
-                        const bool f = ((hw & 0x7FFFu) - kTabBase) < (uint32_t)kTabHalf;
-                        if (__ballot(!f) && !f) eval_term(x[j] * St.invT, St.m, St.sum, St.bad, St.exp_lds);
-                    }
-                }
-            } else {
-                // evaluated path for every logit: rescale once per group
-                float a[8];
-                float am = -INFINITY;
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    a[j] = x[j] * St.invT;
-                    St.bad |= __builtin_amdgcn_classf(a[j], 0x203);
-                    am = fmaxf(am, a[j]);  // NaN is ignored
-                }
-                if (am > St.m && am < INFINITY) {
-                    St.sum = (St.m == -INFINITY) ? 0.0 : St.sum * exp64((double)St.m - (double)am, St.exp_lds);
-                    St.m = am;
-                }
-                const double md = (double)St.m;
-                double s2[2] = {0.0, 0.0};
-#pragma unroll
-                for (int j = 0; j < 8; ++j) s2[j & 1] += exp64((double)a[j] - md, St.exp_lds);
-                St.sum += s2[0] + s2[1];
+            for (int j = 0; j < 8; ++j) {
+                a[j] = x[j] * St.invT;
+                St.bad |= __builtin_amdgcn_classf(a[j], 0x203);
+                am = fmaxf(am, a[j]);  // NaN is ignored
             }
+            if (am > St.m && am < INFINITY) {
+                St.sum = (St.m == -INFINITY) ? 0.0 : St.sum * exp64((double)St.m - (double)am, St.exp_lds);
+                St.m = am;
+            }
+            const double md = (double)St.m;
+            double s2[2] = {0.0, 0.0};
+#pragma unroll
+            for (int j = 0; j < 8; ++j) s2[j & 1] += exp64((double)a[j] - md, St.exp_lds);
+            St.sum += s2[0] + s2[1];
         } else {
 #pragma unroll
             for (int j = 0; j < 8; ++j) St.bad |= __builtin_amdgcn_classf(x[j] * St.invT, 0x203);
@@ -445,28 +511,55 @@ __device__ __forceinline__ void draft_chunk(const Raw8<DT> (&r)[kDraftU], int ba
         float xm = x[0];
 #pragma unroll
         for (int j = 1; j < 8; ++j) xm = fmaxf(xm, x[j]);  // NaN is ignored
-        if (St.cb.pass(xm, (uint32_t)i0)) {
-            St.rec[St.nrec][threadIdx.x] = i0;
-            ++St.nrec;
-        }
+        if (St.cb.pass(xm, (uint32_t)i0)) record_group<STATS>(St, i0);
     }
+}
+
+// Per chunk, after draft_chunk: the filter shared by the other waves and the
+// flush of the recorded groups when some lane's list is nearly full.
+template <int DT, bool VEC, bool STATS, bool TAB, int CAP>
+__device__ __forceinline__ void draft_chunk_tail(DraftState<CAP>& St) {
     {
         // an LDS load (a generic volatile load would also wait for the
         // chunks in flight)
         const uint64_t sk = __hip_atomic_load(St.key, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
         if (sk) St.cb.raise_to(sk);
     }
-    if (__ballot(St.nrec > rec_slots<STATS>() - kDraftU)) {
-        flush_recorded<DT, VEC, CAP>(St.cb, St.draft, St.rowbase, St.hi, St.K, St.rec, St.nrec, St.key);
-        St.nrec = 0;
+    if constexpr (!STATS) {
+        if (__ballot(St.nrec > rec_slots<STATS>() - kDraftU)) {
+            flush_recorded<DT, VEC, CAP>(St.cb, St.draft, St.rowbase, St.hi, St.K, St.rec, St.nrec, St.key);
+            St.nrec = 0;
+        }
     }
+}
+
+// Issues the loads of the chunk at `base` (nothing at or past hi): a chunk
+// that lies wholly inside the segment is read with unconditional vector loads
+// (a wave-uniform choice), a last partial chunk with per-position bounds.
+template <int DT, bool VEC>
+__device__ __forceinline__ void issue_chunk(const void* __restrict__ draft, size_t rowbase, int base, int hi, int tid,
+                                            Raw8<DT> (&r)[kDraftU]) {
+    if (VEC && base + kDraftChunk <= hi)
+        load_chunk<DT>(draft, rowbase, base, tid, r);
+    else if (base < hi)
+        load_chunk_masked<DT, VEC>(draft, rowbase, base, hi, tid, r);
+}
+
+// Number of keys of a descending list of n (<= 64) distinct keys in LDS that
+// are larger than k.
+__device__ __forceinline__ int count_larger(const uint64_t* list, int n, uint64_t k) {
+    int pos = 0;
+#pragma unroll
+    for (int step = 64; step > 0; step >>= 1)
+        if (pos + step <= n && list[pos + step - 1] > k) pos += step;
+    return pos;
 }
 
 // STATS = false is the pool selection: the same candidate lists (K = pool
 // size) and finiteness flags without the normaliser (pm, ps unused).
-template <int DT, bool VEC, bool STATS>
+template <int DT, bool VEC, bool STATS, bool TAB>
 __global__ __launch_bounds__(kDraftThreads) __attribute__((amdgpu_waves_per_eu(4))) void draft_partials(const void* __restrict__ draft, int V, int D,
-                                                                int seg, int S, float invT, int K, int use_table,
+                                                                int seg, int S, float invT, int K,
                                                                 float* __restrict__ pm, double* __restrict__ ps,
                                                                 uint64_t* __restrict__ pk, int* __restrict__ pf,
                                                                 int32_t* __restrict__ req_status) {
@@ -479,43 +572,56 @@ __global__ __launch_bounds__(kDraftThreads) __attribute__((amdgpu_waves_per_eu(4
     const size_t rowbase = (size_t)row * (size_t)V;
     const int lo = s * seg;
     const int hi = min(V, lo + seg);
-    const bool tab = DT == TSB_BF16 && STATS && use_table;
+    static_assert(!TAB || (DT == TSB_BF16 && STATS), "the table path is for bf16 rows with the normaliser");
 
-    // a chunk that lies wholly inside the segment is read with unconditional
-    // vector loads (a wave-uniform choice), a last partial chunk with
-    // per-position bounds
-    const bool full0 = VEC && lo + kDraftChunk <= hi;
+    // the first chunk is in flight before anything else is done
     Raw8<DT> rA[kDraftU];
-    if (full0)
-        load_chunk<DT>(draft, rowbase, lo, tid, rA);
-    else
-        load_chunk_masked<DT, VEC>(draft, rowbase, lo, hi, tid, rA);
+    issue_chunk<DT, VEC>(draft, rowbase, lo, hi, tid, rA);
 
-    constexpr int kTab = (DT == TSB_BF16 && STATS) ? kTabEntries : 1;
-    __shared__ double s_tab[kTab];
-    __shared__ double s_exp[kExpTable];
+    // bf16 rows with the normaliser: the exponential table, with the exp64
+    // table and the column maxima in its gap; otherwise the exp64 table and
+    // the column maxima on their own. One LDS block with the table first, so
+    // that table offsets fit the immediate offset of an LDS load.
+    constexpr bool kTabbed = TAB;
     constexpr int CAP = cand_cap<STATS>();
-    __shared__ uint64_t s_buf[kDraftWaves][CAP];
-    __shared__ float s_lm[kDraftWaves][kWave];
-    __shared__ unsigned long long s_key;
+    static_assert(!kTabbed || kTabGap + kExpTable + kDraftThreads / 2 + kDraftWaves * kSpecialCap / 4 <= kTabNeg,
+                  "the gap holds the exp64 table, the column maxima and the deferred patterns");
+    struct Lds {
+        double tab[kTabbed ? kTabDoubles : kExpTable + kDraftThreads / 2];
+        uint64_t buf[kDraftWaves][CAP];
+        int rec[rec_slots<STATS>()][kDraftThreads];
+        int n[kDraftWaves];
+        float m[kDraftWaves];
+        double s[kDraftWaves];
+        int bad[kDraftWaves];
+        unsigned long long key;
+    };
+    __shared__ Lds L;
+    double* const s_tab = L.tab;
+    double* const s_exp = kTabbed ? s_tab + kTabGap : s_tab;
+    float (*const s_lm)[kWave] = (float (*)[kWave])(s_exp + kExpTable);
+    // (the table path only: its deferred out-of-table patterns, in the gap)
+    uint16_t* const s_special = (uint16_t*)(s_exp + kExpTable + kDraftThreads / 2) + wave * kSpecialCap;
     if (STATS) {
         for (int j = tid; j < kExpTable; j += kDraftThreads) s_exp[j] = exp2((double)j / (double)kExpTable);
         __syncthreads();
-        if (tab) {
-            for (int i = tid; i < kTabEntries - 2; i += kDraftThreads) {
-                const uint32_t h = (kTabBase + (uint32_t)(i >> 1)) | ((uint32_t)(i & 1) << 15);
-                s_tab[i] = exp64((double)(__uint_as_float(h << 16) * invT), s_exp);
+        if (TAB) {
+            for (int i = tid; i < 2 * (kTabHalf + 1); i += kDraftThreads) {
+                const int sg = i >= kTabHalf + 1;
+                const int t = i - sg * (kTabHalf + 1);
+                const uint32_t h = (kTabBase + (uint32_t)t) | ((uint32_t)sg << 15);
+                s_tab[sg * kTabNeg + t] = t < kTabHalf ? exp64((double)(__uint_as_float(h << 16) * invT), s_exp) : 0.0;
             }
-            if (tid < 2) s_tab[kTabEntries - 2 + tid] = 0.0;
         }
     }
 
-    __shared__ int s_rec[rec_slots<STATS>()][kDraftThreads];
     CandBuf<CAP> cb;
-    cb.buf = s_buf[wave];
+    cb.buf = L.buf[wave];
     cb.n = 0;
     cb.fid = 0xFFFFFFFFu;
     {
+        // the first filter, from the first chunk's column maxima (the barrier
+        // also orders the tables before their first use)
         float lm = -INFINITY;
 #pragma unroll
         for (int u = 0; u < kDraftU; ++u) {
@@ -525,7 +631,7 @@ __global__ __launch_bounds__(kDraftThreads) __attribute__((amdgpu_waves_per_eu(4
             for (int j = 0; j < 8; ++j) lm = fmaxf(lm, x[j]);
         }
         s_lm[wave][lane] = isnan(lm) ? -INFINITY : lm;
-        if (tid == 0) s_key = 0ull;
+        if (tid == 0) L.key = 0ull;
         __syncthreads();
         if (K <= 16) {
             float cm = s_lm[0][lane];
@@ -550,87 +656,159 @@ __global__ __launch_bounds__(kDraftThreads) __attribute__((amdgpu_waves_per_eu(4
         }
     }
 
-    DraftState<CAP> St{cb, draft, rowbase, hi, K, invT, tab, s_tab, s_exp, s_rec, &s_key};
-
-
+    DraftState<CAP> St{cb, draft, rowbase, hi, K, invT, TAB, s_tab, s_exp, L.rec, &L.key, s_special};
     for (int base = lo; base < hi; base += kDraftChunk) {
         // the next chunk's loads are issued before this one is processed
-        const int nb = base + kDraftChunk;
         Raw8<DT> rB[kDraftU];
-        if (VEC && nb + kDraftChunk <= hi)
-            load_chunk<DT>(draft, rowbase, nb, tid, rB);
-        else if (nb < hi)
-            load_chunk_masked<DT, VEC>(draft, rowbase, nb, hi, tid, rB);
-        draft_chunk<DT, VEC, STATS, CAP>(rA, base, St);
+        issue_chunk<DT, VEC>(draft, rowbase, base + kDraftChunk, hi, tid, rB);
+        draft_chunk<DT, VEC, STATS, TAB, CAP>(rA, base, St);
+        draft_chunk_tail<DT, VEC, STATS, TAB, CAP>(St);
 #pragma unroll
         for (int u = 0; u < kDraftU; ++u) rA[u] = rB[u];
     }
-    flush_recorded<DT, VEC, CAP>(St.cb, draft, rowbase, hi, K, s_rec, St.nrec, &s_key);
-    const double sumF = St.sumF;
-    const float m = St.m;
-    const double sum = St.sum;
-    const bool bad = St.bad;
+    flush_recorded<DT, VEC, CAP, STATS ? 8 : kRecBatch>(St.cb, draft, rowbase, hi, K, L.rec, St.nrec, &L.key);
+    if constexpr (STATS) {
+        if (__ballot(St.rec_full)) {
+            // a lane whose list ran full offers every group of its part of
+            // the segment again (the filter only rose since)
+            for (int base = lo; base < hi; base += kDraftChunk) {
+#pragma unroll
+                for (int u = 0; u < kDraftU; ++u) {
+                    const int i0 = base + (u * kDraftThreads + tid) * 8;
+                    Raw8<DT> g;
+                    const bool live = St.rec_full && i0 < hi;
+                    if (live) {
+                        load_raw8<DT, VEC>(draft, rowbase, i0, hi, g);
+                    } else {
+#pragma unroll
+                        for (int j = 0; j < (DT == TSB_BF16 ? 4 : 8); ++j)
+                            g.w[j] = DT == TSB_BF16 ? 0xFF80FF80u : 0xFF800000u;
+                    }
+                    float x[8];
+                    raw8_values<DT>(g, x);
+                    St.cb.offer8(x, i0, hi, live, K, &L.key);
+                }
+            }
+        }
+        if (TAB && St.nspecial > 0) {
+            // the deferred patterns, one per lane at a time; a wave whose list
+            // overflowed reads its part of the segment again instead
+            wave_lds_fence();
+            if (St.nspecial <= kSpecialCap) {
+                for (int i = lane; i < St.nspecial; i += kWave)
+                    eval_term(__uint_as_float((uint32_t)s_special[i] << 16) * invT, St.m, St.sum, St.bad, s_exp);
+            } else {
+                for (int base = lo; base < hi; base += kDraftChunk) {
+                    Raw8<DT> rr[kDraftU];
+                    issue_chunk<DT, VEC>(draft, rowbase, base, hi, tid, rr);
+#pragma unroll
+                    for (int u = 0; u < kDraftU; ++u)
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) {
+                            const uint32_t p = (rr[u].w[j >> 1] >> (16 * (j & 1))) & 0xFFFFu;
+                            const bool out = ((p & 0x7FFFu) - kTabBase) >= (uint32_t)kTabHalf && p != 0xFF80u &&
+                                             base + (u * kDraftThreads + tid) * 8 + j < hi;
+                            if (out) eval_term(__uint_as_float(p << 16) * invT, St.m, St.sum, St.bad, s_exp);
+                        }
+                }
+            }
+        }
+    }
 
-    __shared__ int s_n[kDraftWaves];
-    __shared__ float s_m[kDraftWaves];
-    __shared__ double s_s[kDraftWaves];
-    __shared__ int s_bad[kDraftWaves];
-    // lane partial: reference M (0 for the table part) and the sum relative
+    // lane partial: reference Ml (0 for the table part) and the sum relative
     // to it; exponentials only where references differ
-    const bool anyF = sumF > 0.0;  // table entries are positive
+    const bool anyF = St.sumF > 0.0;  // table entries are positive
     float Ml;
     double sl;
-    if (m == -INFINITY) {
+    if (St.m == -INFINITY) {
         Ml = anyF ? 0.0f : -INFINITY;
-        sl = sumF;
+        sl = St.sumF;
+    } else if (!anyF) {
+        Ml = St.m;
+        sl = St.sum;
     } else {
-        Ml = anyF ? fmaxf(0.0f, m) : m;
-        sl = (anyF ? (Ml == 0.0f ? sumF : sumF * exp(-(double)Ml)) : 0.0) +
-             (m == Ml ? sum : sum * exp((double)m - (double)Ml));
+        Ml = fmaxf(0.0f, St.m);
+        sl = (Ml == 0.0f ? St.sumF : St.sumF * exp(-(double)Ml)) +
+             (St.m == Ml ? St.sum : St.sum * exp((double)St.m - (double)Ml));
     }
     const float wm = wave_max(Ml);
-    const double contrib = (Ml == -INFINITY) ? 0.0 : (Ml == wm ? sl : sl * exp((double)Ml - (double)wm));
-    const double ws = STATS ? wave_sum(contrib) : 0.0;
-    const int wb = wave_or(bad);
+    double contrib = 0.0;
+    if (Ml != -INFINITY) {
+        if (Ml == wm)
+            contrib = sl;
+        else
+            contrib = sl * exp((double)Ml - (double)wm);
+    }
+    const double wsum = STATS ? wave_sum(contrib) : 0.0;
+    const int wb = wave_or(St.bad);
+
+    const int n = cb.n;
     if (lane == 0) {
-        s_n[wave] = cb.n;
-        s_m[wave] = wm;
-        s_s[wave] = ws;
-        s_bad[wave] = wb;
+        L.n[wave] = n;
+        L.m[wave] = wm;
+        L.s[wave] = wsum;
+        L.bad[wave] = wb;
     }
     __syncthreads();
-    // the K best over all buffers: by one wave when they fit its registers,
-    // else after every wave has kept its own K best
     int total = 0;
 #pragma unroll
-    for (int w = 0; w < kDraftWaves; ++w) total += s_n[w];
-    if (total > kFinalRegs * kWave) {
-        cb.compact(K, &s_key);
-        if (lane == 0) s_n[wave] = cb.n;
+    for (int w = 0; w < kDraftWaves; ++w) total += L.n[w];
+    const size_t o = (size_t)row * S + s;
+    if (total <= 2 * kWave) {
+        // few entries: the rank of a key is the number of larger keys over
+        // all the buffers; the segment's K best go to their slots
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int i = h * kWave + lane;
+            if (i < n) {
+                const uint64_t mine = cb.buf[i];
+                int rank = 0;
+                for (int w = 0; w < kDraftWaves; ++w) {
+                    const int nw = L.n[w];
+                    for (int j = 0; j < nw; ++j) rank += L.buf[w][j] > mine ? 1 : 0;
+                }
+                if (rank < K) pk[o * K + rank] = mine;
+            }
+        }
+    } else {
+        // every wave keeps its K best, sorted; a key's rank is its place in
+        // its own list plus the number of larger keys in every other list
+        uint64_t v[CAP / kWave];
+#pragma unroll
+        for (int i = 0; i < CAP / kWave; ++i) v[i] = i * kWave + lane < n ? cb.buf[i * kWave + lane] : 0ull;
+        wave_sort_desc<CAP / kWave>(v);
+        const uint64_t top = v[0];
+        const int c = min(n, K);
         __syncthreads();
+        if (lane < c) cb.buf[lane] = top;
+        if (lane == 0) L.n[wave] = c;
+        __syncthreads();
+        if (lane < c) {
+            int rank = lane;
+#pragma unroll
+            for (int w = 0; w < kDraftWaves; ++w)
+                if (w != wave) rank += count_larger(L.buf[w], L.n[w], top);
+            if (rank < K) pk[o * K + rank] = top;
+        }
         total = 0;
 #pragma unroll
-        for (int w = 0; w < kDraftWaves; ++w) total += s_n[w];
+        for (int w = 0; w < kDraftWaves; ++w) total += L.n[w];
     }
+    // empty slots get 0
+    if (tid >= total && tid < K) pk[o * K + tid] = 0ull;
     if (wave == 0) {
-        uint64_t best;
-        if (total <= 2 * kWave) {
-            uint64_t v[2];
-            gather_flat<2, CAP>(s_buf, s_n, v);
-            best = wave_top<2>(v, K);
-        } else {
-            uint64_t v[kFinalRegs];
-            gather_flat<kFinalRegs, CAP>(s_buf, s_n, v);
-            best = wave_top<kFinalRegs>(v, K);
-        }
         // segment normaliser: lanes w < kDraftWaves hold wave w's partial
-        const float mw = lane < kDraftWaves ? s_m[lane] : -INFINITY;
+        const float mw = lane < kDraftWaves ? L.m[lane] : -INFINITY;
         const float M = wave_max(mw);
-        const double sw = lane < kDraftWaves && mw != -INFINITY
-                              ? (mw == M ? s_s[lane] : s_s[lane] * exp((double)mw - (double)M)) : 0.0;
+        double sw = 0.0;
+        if (lane < kDraftWaves && mw != -INFINITY) {
+            if (mw == M)
+                sw = L.s[lane];
+            else
+                sw = L.s[lane] * exp((double)mw - (double)M);
+        }
         const double tot = STATS ? wave_sum(sw) : 0.0;
-        const int anybad = wave_or(lane < kDraftWaves ? s_bad[lane] : 0);
-        const size_t o = (size_t)row * S + s;
+        const int anybad = wave_or(lane < kDraftWaves ? L.bad[lane] : 0);
         if (lane == 0) {
             if (STATS) {
                 pm[o] = M;
@@ -638,7 +816,6 @@ __global__ __launch_bounds__(kDraftThreads) __attribute__((amdgpu_waves_per_eu(4
             }
             pf[o] = anybad;
         }
-        if (lane < K) pk[o * K + lane] = best;
     }
 }
 
@@ -1362,22 +1539,30 @@ hipError_t launch_draft_partials(const tsb_config& c, int K, float invT, const v
     const dim3 grid1(g.S1, c.R * c.D);
     const bool vec = (c.dtype == TSB_BF16) ? (c.V % 8 == 0 && ((uintptr_t)draft & 15) == 0)
                                            : (c.V % 4 == 0 && ((uintptr_t)draft & 15) == 0);
-    const int tab = (c.dtype == TSB_BF16 && draft_table_ok(invT) && g.seg1 >= kTableMinSeg) ? 1 : 0;
+    const bool tab = STATS && c.dtype == TSB_BF16 && draft_table_ok(invT) && g.seg1 >= kTableMinSeg;
+#define TSB_DRAFT_LAUNCH(DT, VEC, TAB)                                                                          \
+    draft_partials<DT, VEC, STATS, (TAB) && STATS><<<grid1, kDraftThreads, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, \
+                                                                                invT, K, pm, ps, pk, pf,       \
+                                                                                req_status)
     if (c.dtype == TSB_BF16) {
-        if (vec)
-            draft_partials<TSB_BF16, true, STATS><<<grid1, kDraftThreads, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT,
-                                                                                  K, tab, pm, ps, pk, pf, req_status);
-        else
-            draft_partials<TSB_BF16, false, STATS><<<grid1, kDraftThreads, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT,
-                                                                                   K, tab, pm, ps, pk, pf, req_status);
+        if (tab) {
+            if (vec)
+                TSB_DRAFT_LAUNCH(TSB_BF16, true, true);
+            else
+                TSB_DRAFT_LAUNCH(TSB_BF16, false, true);
+        } else {
+            if (vec)
+                TSB_DRAFT_LAUNCH(TSB_BF16, true, false);
+            else
+                TSB_DRAFT_LAUNCH(TSB_BF16, false, false);
+        }
     } else {
         if (vec)
-            draft_partials<TSB_F32, true, STATS><<<grid1, kDraftThreads, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT,
-                                                                                 K, 0, pm, ps, pk, pf, req_status);
+            TSB_DRAFT_LAUNCH(TSB_F32, true, false);
         else
-            draft_partials<TSB_F32, false, STATS><<<grid1, kDraftThreads, 0, st>>>(draft, c.V, c.D, g.seg1, g.S1, invT,
-                                                                                  K, 0, pm, ps, pk, pf, req_status);
+            TSB_DRAFT_LAUNCH(TSB_F32, false, false);
     }
+#undef TSB_DRAFT_LAUNCH
     return hipGetLastError();
 }
 

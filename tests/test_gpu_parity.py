@@ -247,7 +247,8 @@ def test_planner_exact_ties(B, K, D):
 def _special_rows(rng, R, D, V):
     """bf16-exact draft rows [R, D, V] with values outside the exponential table planted: exact zeros,
     values below its smallest binade (+-2^-20 and bf16 subnormals), values at or beyond 64 (some the
-    row maximum), masked -inf entries, and one row whose every value lies outside the table."""
+    row maximum), masked -inf entries, one row whose every value lies outside the table, and rows
+    rising along the vocabulary (every late group passes the first candidate filter)."""
     d = (rng.standard_normal((R, D, V)) * 2.5).astype(np.float32)
     d[:, :, rng.integers(0, V, 16)] += 6.0
     for r in range(R):
@@ -270,6 +271,11 @@ def _special_rows(rng, R, D, V):
                 d[r, j, pos[:20]] = 70.0
                 d[r, j, pos[20:40]] = -70.0
     d[1, 4] = 64.0 + (rng.random(V).astype(np.float32) * 30.0)  # every value outside the table
+    # rising along the vocabulary: every group after the first chunk passes
+    # the first filter (the per-lane lists of candidate groups run full),
+    # with long runs of equal bf16 values
+    d[0, 5] = np.linspace(-5.0, 15.0, V, dtype=np.float32)
+    d[1, 9] = np.linspace(20.0, -5.0, V, dtype=np.float32)[::-1].copy()
     return torch.from_numpy(d).to(torch.bfloat16).float().numpy()
 
 
