@@ -59,7 +59,8 @@ struct NaiveArgs {
     const int32_t* node_tok;
     tsb_verdict out;
     XRegion X;  // exchange slots of the requests
-    int V, D, B, r0;
+    int V, D, B;
+    int R, G;   // requests and workgroups per request of the launch (tickets)
     float invT;
     uint32_t k0, k1, step;
 };
@@ -249,9 +250,10 @@ __device__ SliceBest naive_round(const NaiveArgs& A, int r, int g, int G, uint32
 template <int DT, bool VEC>
 __global__ __launch_bounds__(kNaiveThreads) void verify_naive(NaiveArgs A) {
     __shared__ int s_nc[kNaiveNodes], s_fc[kNaiveNodes], s_tok[kNaiveNodes];
-    const int g = blockIdx.x;
-    const int G = gridDim.x;
-    const int r = A.r0 + blockIdx.y;
+    const int G = A.G;
+    const int ticket = xticket(A.X, A.R);
+    const int g = ticket % G;
+    const int r = ticket / G;
     const int tid = threadIdx.x;
     const int B1 = A.B + 1;
     const size_t tb = (size_t)r * B1;
@@ -417,27 +419,23 @@ hipError_t launch_verify_naive(const tsb_config& c, float invT, const void* targ
     if (e != hipSuccess) return e;
     if (cap < 1) return hipErrorLaunchOutOfResources;
     // workgroups per request: enough that a slice is one batch, within what
-    // keeps the whole batch resident (then one launch covers every request)
+    // keeps the whole batch resident (the launch itself needs only G
+    // workgroups to fit at once: tickets)
     const int need = (c.V + kNaiveBatchTokens - 1) / kNaiveBatchTokens;
     int G = cap / c.R;
     if (G > need) G = need;
     if (G > kWalkGroupsMax) G = kWalkGroupsMax;
     if (G < 1) G = 1;
-    const int chunk = cap / G;
+    A.R = c.R;
+    A.G = G;
 
     const int nclear = (int)std::min<size_t>(1024, (xwords(c.R) + kBlock - 1) / kBlock);
     xchg_clear<<<nclear, kBlock, 0, st>>>(A.X, c.R);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if ((e = hook_before(TSB_KERNEL_VERIFY_NAIVE, st)) != hipSuccess) return e;
-    // cooperative launches: every workgroup of a launch is resident at once
-    // (or the launch fails), so the exchanges of a request complete
-    for (int r0 = 0; r0 < c.R; r0 += chunk) {
-        A.r0 = r0;
-        const int rc = min(chunk, c.R - r0);
-        void* args[] = {&A};
-        e = hipLaunchCooperativeKernel(fn, dim3(G, rc), dim3(kNaiveThreads), args, 0, st);
-        if (e != hipSuccess) return e;
-    }
+    void* args[] = {&A};
+    e = hipLaunchKernel(fn, dim3((unsigned)(G * c.R)), dim3(kNaiveThreads), args, 0, st);
+    if (e != hipSuccess) return e;
     return hook_after(TSB_KERNEL_VERIFY_NAIVE, st);
 }
 

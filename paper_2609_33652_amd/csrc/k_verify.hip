@@ -185,7 +185,8 @@ struct WalkArgs {
     const double* ts;
     const int* tf;
     XRegion X;  // exchange slots of the requests
-    int V, D, B, S4, r0;
+    int V, D, B, S4;
+    int R, G;   // requests and workgroups per request of the launch (tickets)
     float invT;
     uint32_t k0, k1, step;
     // pool walk only: pools [R, D, P] and transition scores [R, D-1, P, P]
@@ -703,9 +704,10 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
     __shared__ float s_xd[TSB_MAX_K], s_xt[TSB_MAX_K];
     __shared__ double s_u[TSB_MAX_K];
     __shared__ int s_badtok;
-    const int g = blockIdx.x;
-    const int G = gridDim.x;
-    const int r = A.r0 + blockIdx.y;
+    const int G = A.G;
+    const int ticket = xticket(A.X, A.R);
+    const int g = ticket % G;
+    const int r = ticket / G;
     const int tid = threadIdx.x;
     const int B1 = A.B + 1;
     const size_t tb = (size_t)r * B1;
@@ -1007,9 +1009,10 @@ __global__ __launch_bounds__(kWalkThreads) void verify_pool_walk(WalkArgs A) {
     __shared__ double s_u[TSB_MAX_K];
     __shared__ double s_z;
     __shared__ int s_badtok;
-    const int g = blockIdx.x;
-    const int G = gridDim.x;
-    const int r = A.r0 + blockIdx.y;
+    const int G = A.G;
+    const int ticket = xticket(A.X, A.R);
+    const int g = ticket % G;
+    const int r = ticket / G;
     const int tid = threadIdx.x;
     const int lane = tid % kWave;
     const int B1 = A.B + 1;
@@ -1291,9 +1294,10 @@ __global__ __launch_bounds__(kWalkThreads) void verify_traversal(WalkArgs A) {
     __shared__ double s_exp[kExpTable];
     __shared__ TravEntry s_stk[kTravStack];
     __shared__ int s_cache;  // node whose slice is in the cache, -1 for none
-    const int g = blockIdx.x;
-    const int G = gridDim.x;
-    const int r = A.r0 + blockIdx.y;
+    const int G = A.G;
+    const int ticket = xticket(A.X, A.R);
+    const int g = ticket % G;
+    const int r = ticket / G;
     const int tid = threadIdx.x;
     const int B1 = A.B + 1;
     const size_t tb = (size_t)r * B1;
@@ -1614,7 +1618,8 @@ static WalkArgs walk_args(const tsb_config& c, float invT, const void* draft, co
     A.D = c.D;
     A.B = c.B;
     A.S4 = g.S4;
-    A.r0 = 0;
+    A.R = c.R;
+    A.G = 1;
     A.invT = invT;
     A.k0 = (uint32_t)c.seed;
     A.k1 = (uint32_t)(c.seed >> 32);
@@ -1625,22 +1630,14 @@ static WalkArgs walk_args(const tsb_config& c, float invT, const void* draft, co
     return A;
 }
 
-// Launches of a walk grid (G workgroups per request) within the resident
-// capacity, in order of requests. The launches are cooperative: every
-// workgroup of a launch is resident at once (or the launch fails), so the
-// exchanges of a request always complete.
+// One launch of a walk grid: G workgroups per request, each taking its
+// (request, slice) from a ticket (xticket), so only G workgroups need to fit
+// on the device at once (cap: resident workgroups of this kernel).
 static hipError_t launch_walk_grid(const void* fn, WalkArgs& A, int R, int G0, int cap, size_t lds, hipStream_t st) {
-    int G = G0;
-    if (G * R > cap) G = cap / R > 0 ? cap / R : 1;
-    const int chunk = cap / G;
-    for (int r0 = 0; r0 < R; r0 += chunk) {
-        A.r0 = r0;
-        const int rc = min(chunk, R - r0);
-        void* args[] = {&A};
-        const hipError_t e = hipLaunchCooperativeKernel(fn, dim3(G, rc), dim3(kWalkThreads), args, lds, st);
-        if (e != hipSuccess) return e;
-    }
-    return hipSuccess;
+    A.R = R;
+    A.G = G0 < cap ? G0 : cap;
+    void* args[] = {&A};
+    return hipLaunchKernel(fn, dim3((unsigned)(A.G * R)), dim3(kWalkThreads), args, lds, st);
 }
 
 hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, const double* draft_lse,
@@ -1708,7 +1705,7 @@ hipError_t launch_pool_verify(const tsb_config& c, int P, float invT, const void
     if ((e = walk_capacity(fn, 1, c.dtype == TSB_BF16 ? 1 : 0, vec4 ? 1 : 0, lds_max, &cap)) != hipSuccess) return e;
     if (cap < 1) return hipErrorLaunchOutOfResources;
     int G = geometry(c).G;
-    if (G * c.R > cap) G = cap / c.R > 0 ? cap / c.R : 1;
+    if (G > cap) G = cap;
     const long long span = (((long long)c.V + G - 1) / G + 3) & ~3ll;
     const size_t lds = (size_t)((span + 31) / 32) * sizeof(uint32_t);
     if (lds > lds_max) return hipErrorInvalidConfiguration;  // vocabulary too wide for the slice bitmap

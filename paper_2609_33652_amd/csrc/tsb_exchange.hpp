@@ -13,7 +13,8 @@
 // round e - 1 from every workgroup, each of which had read round e - 2).
 //
 // Nothing persists between calls: the kernel enqueued right before a walk
-// clears the slots of every request of the call (xclear), and stream order
+// clears the slots of every request of the call and the ticket counter
+// (xclear), and stream order
 // makes the zeros visible before the walk starts. Whatever the workspace
 // held before the call (another entry point's scratch, an abandoned wait of
 // an earlier call, uninitialised memory) can therefore never be taken for a
@@ -40,10 +41,32 @@ __device__ __forceinline__ uint64_t* xslot(const XRegion& X, int r, uint32_t e, 
     return X.slots + (((size_t)r * 2 + (e & 1u)) * kWalkGroupsMax + g) * kSlotWords;
 }
 
-// Words of the exchange region of R requests.
-__host__ __device__ inline size_t xwords(int R) { return (size_t)R * 2 * kWalkGroupsMax * kSlotWords; }
+// Words of the slots of R requests; one more 64-byte line after them holds
+// the walk's ticket counter.
+constexpr int kTicketWords = 8;
+__host__ __device__ inline size_t xslot_words(int R) { return (size_t)R * 2 * kWalkGroupsMax * kSlotWords; }
+// Words of the exchange region of R requests (slots and ticket counter).
+__host__ __device__ inline size_t xwords(int R) { return xslot_words(R) + kTicketWords; }
 
-// Zeroes the exchange slots of R requests; thread `i` of `n` threads
+// Tickets. A walk is one launch of R * G workgroups; each workgroup, once it
+// runs, takes the next ticket t from a counter cleared before the launch and
+// serves request t / G, slice t % G. Tickets go only to running workgroups,
+// in order, so every request below the highest ticket taken has all its
+// workgroups running or done, and its exchanges complete; as they finish,
+// waiting workgroups start and take the next tickets. The launch therefore
+// needs only G workgroups to fit on the device at once, whatever else runs
+// there and however the hardware orders the dispatch of the grid.
+__device__ __forceinline__ int xticket(const XRegion& X, int R) {
+    __shared__ int s_ticket;
+    if (threadIdx.x == 0)
+        s_ticket = (int)__hip_atomic_fetch_add((uint32_t*)(X.slots + xslot_words(R)), 1u, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    return s_ticket;
+}
+
+// Zeroes the exchange slots of R requests and the ticket counter; thread `i`
+// of `n` threads
 // (grid-stride) takes every n-th word.
 __device__ __forceinline__ void xclear(const XRegion& X, int R, size_t i, size_t n) {
     const size_t nw = xwords(R);

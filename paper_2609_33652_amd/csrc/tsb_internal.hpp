@@ -83,7 +83,8 @@ struct XchgWs {
 inline XchgWs xchg_ws(const tsb_config& c) {
     XchgWs w;
     size_t o = 0;
-    w.slots = o; o = align256(o + (size_t)c.R * 2 * kWalkGroupsMax * 8 * sizeof(uint64_t));
+    // slots [R][2][kWalkGroupsMax][8] words, then one line for the ticket counter
+    w.slots = o; o = align256(o + ((size_t)c.R * 2 * kWalkGroupsMax * 8 + 8) * sizeof(uint64_t));
     w.total = o;
     return w;
 }
