@@ -36,6 +36,33 @@ TARGET_TRAFFIC = {"config": 4, "source_sha256_16": "d1240d8a06bfe313", "fetch_ki
                   "fetch_scale": 2.0, "write_scale": 1.0}
 
 
+# VALU wave-instructions per launch of replay_scan at the batched workload from
+# an SQ_INSTS_VALU counter pass, valid for the scan source it was taken on
+REPLAY_COUNTERS = {"config": 4, "source_sha256_16": None, "insts_valu": None}
+# peak VALU issue: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = 39.3e12 lane
+# operations/s, i.e. 614.4e9 wave64 instructions/s
+VALU_PEAK_WAVE_INSTS = 256 * 2.4e9
+
+
+def _section_hash(path, start, end):
+    import hashlib
+    src = open(os.path.join(ROOT, "paper_2609_33652_amd", "csrc", path)).read()
+    a, b = src.find(start), src.find(end)
+    if a < 0 or b < 0:
+        return None
+    return hashlib.sha256(src[a:b].encode()).hexdigest()[:16]
+
+
+def replay_insts(cfg_id):
+    """Counter-measured VALU wave-instructions per replay_scan launch, or None if the scan or workload differs."""
+    t = REPLAY_COUNTERS
+    h = _section_hash("k_replay.hip", "__global__ __launch_bounds__(kBlock) void replay_scan(",
+                      "__global__ __launch_bounds__(kWave) void replay_merge(")
+    if cfg_id != t["config"] or t["insts_valu"] is None or h != t["source_sha256_16"]:
+        return None
+    return t["insts_valu"]
+
+
 def target_traffic(cfg_id):
     """Counter-measured bytes per launch, or None if the kernel or workload differs from the counted one."""
     import hashlib
@@ -88,6 +115,11 @@ def _cpu_task(args):
     return out["n_acc"]
 
 
+def host_cores():
+    """Worker processes of the CPU baseline: the host's CPUs, at most the 16 a one-GPU share has."""
+    return min(16, len(os.sched_getaffinity(0)))
+
+
 def cpu_baseline(cfg, seed, requests, path="replay_rrs", P=None):
     """Time the oracle over `requests` request-steps of one input set (runs before any GPU use)."""
     import multiprocessing as mp
@@ -114,7 +146,7 @@ def cpu_baseline(cfg, seed, requests, path="replay_rrs", P=None):
     del draft, target
     log("cpu baseline: inputs ready")
     tasks = [(r % nr, r // nr) for r in range(requests)]
-    cores = min(16, len(os.sched_getaffinity(0)), len(tasks))
+    cores = min(host_cores(), len(tasks))
     ctx = mp.get_context("fork")
     t0 = time.perf_counter()
     with ctx.Pool(cores) as pool:
@@ -122,7 +154,8 @@ def cpu_baseline(cfg, seed, requests, path="replay_rrs", P=None):
     dt = time.perf_counter() - t0
     _CPU.clear()
     what = "pools of %d tokens" % P if path == "pool" else path.replace("_", " + ")
-    return dict(value=(len(tasks) / cfg["R"]) / dt, unit="steps/s", cores=cores, kind="oracle",
+    return dict(value=(len(tasks) / cfg["R"]) / dt, unit="steps/s", cores=cores, host_cpus=len(os.sched_getaffinity(0)),
+                kind="oracle",
                 sample="%d request-steps (%g steps) of the %s workload, CPU-generated set 0, %s round; wall %.2f s"
                        % (len(tasks), len(tasks) / cfg["R"], cfg["name"], what, dt))
 
@@ -314,6 +347,70 @@ def pool_block(tsb, c, dev, drafts, args, cfg, P):
             "transitions": "i.i.d. 1.5 * N(0, 1) binary32 scores [R, D-1, P, P]"}
 
 
+def latency_block(tsb, cfg_id, args, n=200):
+    """Latency of one replay + RRS round of a small workload (one request): back-to-back rounds launched
+    eagerly, the same round captured once as a graph and replayed, and eager rounds each followed by a
+    synchronisation (what a caller waiting on every round sees)."""
+    import torch
+    cfg = W.config(cfg_id)
+    c = tsb.make_config(cfg["R"], cfg["D"], cfg["V"], cfg["B"], cfg["K"], cfg["T"], cfg["dtype"],
+                        W.replay_seed(cfg_id))
+    dev = torch.device("cuda:0")
+    rnd = tsb.Round(c, dev)
+    base, sigma = W.base_rows(cfg, 0, device=dev)
+    draft = W.draft_from_base(cfg, base)
+    rnd.plan(draft)
+    dep = rnd.tree["depth"].long().clamp(min=0)
+    target = W.target_from_base(cfg, base, sigma, dep)
+    del base
+    for s in range(20):
+        rnd.step(draft, target, s)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for s in range(n):
+        rnd.step(draft, target, s)
+    b.record()
+    torch.cuda.synchronize()
+    eager_us = 1000.0 * a.elapsed_time(b) / n
+    t0 = time.perf_counter()
+    for s in range(n):
+        rnd.step(draft, target, s)
+        torch.cuda.synchronize()
+    sync_us = 1e6 * (time.perf_counter() - t0) / n
+    # one round captured as a graph (the step index is fixed in it); its outputs must equal the eager round's
+    rnd.step(draft, target, 7)
+    ref = {k: rnd.host()[k].clone() for k in ("node_tok", "n_acc", "bonus", "acc_tok")}
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        rnd.step(draft, target, 7)  # warm-up on the capture stream
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        rnd.step(draft, target, 7)
+    g.replay()
+    torch.cuda.synchronize()
+    h = rnd.host()
+    same = all(torch.equal(h[k], ref[k]) for k in ref)
+    a.record()
+    for s in range(n):
+        g.replay()
+    b.record()
+    torch.cuda.synchronize()
+    graph_us = 1000.0 * a.elapsed_time(b) / n
+    t0 = time.perf_counter()
+    for s in range(n):
+        g.replay()
+        torch.cuda.synchronize()
+    gsync_us = 1e6 * (time.perf_counter() - t0) / n
+    del g
+    return {"workload": W.describe(cfg), "eager_us_per_round": round(eager_us, 2),
+            "graph_us_per_round": round(graph_us, 2), "eager_synced_us": round(sync_us, 2),
+            "graph_synced_us": round(gsync_us, 2), "graph_matches_eager": bool(same), "rounds": n}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -327,6 +424,8 @@ def main():
     ap.add_argument("--sample", type=int, default=8, help="time the target kernel on every n-th timed step")
     ap.add_argument("--first-steps", type=int, default=100, help="timed steps of the First + Naive baseline")
     ap.add_argument("--pool-size", type=int, default=64, help="tokens per pool in the sparse-pool round (0: skip)")
+    ap.add_argument("--latency", type=int, default=1, help="per-round latency of the small workloads, eager and "
+                                                               "as a captured graph (0: skip)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (requests shard with no "
@@ -339,7 +438,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        nreq = args.cpu_requests if args.cpu_requests is not None else R
+        nreq = args.cpu_requests if args.cpu_requests is not None else max(R, host_cores())
         log("cpu baseline: %d oracle request-steps" % nreq)
         cpu = cpu_baseline(cfg, seed, nreq)
         log("cpu baseline:", cpu)
@@ -414,6 +513,13 @@ def main():
         torch.cuda.synchronize()
         tsb.profile_kernel(kid, None)
         kern_us[name] = round(1000.0 * sum(a.elapsed_time(b) for a, b in evs) / args.breakdown_steps, 2)
+    # untimed pass with the work counters on: replay pruning, walk and planner
+    tsb.stats_read(reset=True)
+    tsb.stats_enable(True)
+    for i in range(args.breakdown_steps):
+        rnd.step(drafts[i % P], targets[i % P], i)
+    work = tsb.stats_read(reset=True)
+    tsb.stats_enable(False)
     acc, nodes, flagged = 0, 0, 0
     for i in range(P):
         rnd.step(drafts[i], targets[i], i)
@@ -436,8 +542,45 @@ def main():
         pool = pool_block(tsb, c, dev, drafts, args, cfg, args.pool_size)
         pool["cpu_baseline"] = cpu_pool
 
+    latency = None
+    if args.latency:
+        del drafts
+        torch.cuda.empty_cache()
+        latency = {W.config(i)["name"]: latency_block(tsb, i, args) for i in (1, 2, 3)}
+
     b = 2 if cfg["dtype"] == "bf16" else 4
     k4_bytes = R * (B + 1) * V * b  # every target row of a full tree, read once
+    nst = max(1, args.breakdown_steps)
+    insts = replay_insts(args.config)
+    replay = {
+        "kernel": "replay_scan", "bound": "alu", "avg_launch_us": kern_us["replay_scan"],
+        "items_per_launch": round(work["replay_items"] / nst, 1),
+        "tokens_per_launch": round(work["replay_tokens"] / nst, 1),
+        "live_fraction": round(4 * work["replay_groups_live"] / max(1, work["replay_tokens"]), 5),
+        "keyed_fraction": round(4 * work["replay_groups_keyed"] / max(1, work["replay_tokens"]), 5),
+        "valu_insts_per_launch": insts,
+        "achieved": None if insts is None else round(insts / (kern_us["replay_scan"] * 1e-6) / 1e9, 1),
+        "peak": VALU_PEAK_WAVE_INSTS / 1e9, "unit": "G wave64 VALU instructions/s",
+        "frac": None if insts is None else round(insts / (kern_us["replay_scan"] * 1e-6) / VALU_PEAK_WAVE_INSTS, 4),
+        "note": "fractions are of the scanned tiles' tokens, in groups of four: live = the group's largest key bound "
+                "reaches the parent's threshold (its Philox words are drawn), keyed = a word passes the floor "
+                "(its Gumbel keys are evaluated)"}
+    wr = max(1, work["walk_requests"])
+    walk = {"kernel": "verify_walk", "avg_launch_us": kern_us["verify_walk"],
+            "nodes_per_request": round(work["walk_nodes"] / wr, 3),
+            "tests_per_request": round(work["walk_tests"] / wr, 3),
+            "exchanges_per_request": round(work["walk_exchanges"] / wr, 3),
+            "us_per_node": round(kern_us["verify_walk"] / max(1e-9, work["walk_nodes"] / wr), 2),
+            "us_per_exchange": round(kern_us["verify_walk"] / max(1e-9, work["walk_exchanges"] / wr), 2),
+            "note": "per-node and per-exchange times divide the launch time by the mean count of one request "
+                    "(the requests run side by side)"}
+    pr = max(1, work["plan_requests"])
+    plan = {"kernel": "plan_tree", "avg_launch_us": kern_us["plan_tree"],
+            "merge_us": round(work["plan_merge_ticks"] / pr * 0.01, 2),
+            "search_us": round(work["plan_search_ticks"] / pr * 0.01, 2),
+            "emit_us": round(work["plan_emit_ticks"] / pr * 0.01, 2),
+            "rounds_per_request": round(work["plan_rounds"] / pr, 2),
+            "note": "phase times of one request's workgroup from the 100 MHz real-time counter"}
     k1_bytes = R * D * V * b        # every draft row, read once
     achieved = k4_bytes / (k4_ms * 1e-3) / 1e9
     steps_per_s = 1000.0 / ms
@@ -472,6 +615,10 @@ def main():
                            "frac": round(k1_bytes / (kern_us["draft_partials"] * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
                            "bytes_per_launch": k1_bytes, "avg_launch_us": kern_us["draft_partials"],
                            "source": "per-kernel pass after the timed region"},
+        "replay_roofline": replay,
+        "walk_breakdown": walk,
+        "plan_breakdown": plan,
+        "latency": latency,
         "host_wall_s": round(t_host1 - t_host0, 3),
         "flagged_requests": flagged,
         "cpu_baseline": cpu,

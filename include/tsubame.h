@@ -379,6 +379,35 @@ enum {
 };
 tsb_status tsb_profile_kernel(int32_t kernel_id, hipEvent_t start, hipEvent_t stop);
 
+/* Work counters (for benchmarks). While counting is enabled on the calling
+ * thread, the replay scan, the WoR-RRS walk and the max-heap planner of
+ * every later call on the current device add what they did to a counter
+ * block held on that device (a file-scope array, one per device, kept until
+ * the process ends; calls that overlap on one device add into the same
+ * block). Counting costs a few atomic additions per wave and per request.
+ * tsb_stats_read copies the block of the current device to *out after the
+ * device has finished its work (a synchronous copy: not for use under stream
+ * capture) and zeroes it when reset != 0. Ticks are of the 100 MHz
+ * real-time counter, summed over requests. */
+typedef struct tsb_stats {
+    uint64_t replay_items;        /* (parent, vocabulary tile) items scanned */
+    uint64_t replay_tokens;       /* tokens of the scanned tiles */
+    uint64_t replay_groups_live;  /* groups of four tokens whose largest key bound reaches the parent's threshold */
+    uint64_t replay_groups_keyed; /* of those, groups whose largest uniform word passes the word floor */
+    uint64_t walk_requests;       /* requests walked */
+    uint64_t walk_nodes;          /* nodes entered (children tested, or the bonus drawn there) */
+    uint64_t walk_tests;          /* acceptance tests */
+    uint64_t walk_exchanges;      /* cross-workgroup exchange rounds */
+    uint64_t plan_requests;       /* requests planned */
+    uint64_t plan_merge_ticks;    /* merge of the draft row partials */
+    uint64_t plan_search_ticks;   /* threshold search */
+    uint64_t plan_emit_ticks;     /* emission of the topology */
+    uint64_t plan_rounds;         /* threshold counting rounds */
+    uint64_t reserved[3];
+} tsb_stats;
+tsb_status tsb_stats_enable(int32_t on);
+tsb_status tsb_stats_read(tsb_stats* out, int32_t reset);
+
 const char* tsb_status_string(tsb_status status);
 /* Detail of the last failure on the calling thread ("" if none). */
 const char* tsb_last_error(void);

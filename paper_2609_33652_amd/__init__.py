@@ -39,7 +39,7 @@ EXPORTS = ("tsb_workspace_bytes", "tsb_plan", "tsb_plan_ep", "tsb_replay", "tsb_
            "tsb_first_tokens", "tsb_verify_naive", "tsb_step_first",
            "tsb_pool_workspace_bytes", "tsb_pool_plan", "tsb_pool_replay", "tsb_pool_verify", "tsb_pool_step",
            "tsb_status_string", "tsb_last_error", "tsb_version", "tsb_profile_kernel", "tsb_step_noalloc",
-           "tsb_verify_traversal", "tsb_step_traversal")
+           "tsb_verify_traversal", "tsb_step_traversal", "tsb_stats_enable", "tsb_stats_read")
 NOALLOC_SCRATCH_BYTES = 32 << 20
 
 
@@ -52,6 +52,15 @@ class TsbConfig(ctypes.Structure):
 class TsbTree(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in ("parent", "depth", "rank", "n_children", "first_child",
                                                "score", "n_nodes", "plan_margin")]
+
+
+STATS_FIELDS = ("replay_items", "replay_tokens", "replay_groups_live", "replay_groups_keyed", "walk_requests",
+                "walk_nodes", "walk_tests", "walk_exchanges", "plan_requests", "plan_merge_ticks",
+                "plan_search_ticks", "plan_emit_ticks", "plan_rounds")
+
+
+class TsbStats(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_uint64) for n in STATS_FIELDS] + [("reserved", ctypes.c_uint64 * 3)]
 
 
 class TsbVerdict(ctypes.Structure):
@@ -132,6 +141,10 @@ def load(path=LIB_PATH):
     lib.tsb_version.argtypes = []
     lib.tsb_profile_kernel.restype = ctypes.c_int
     lib.tsb_profile_kernel.argtypes = [ctypes.c_int32, P, P]
+    lib.tsb_stats_enable.restype = ctypes.c_int
+    lib.tsb_stats_enable.argtypes = [ctypes.c_int32]
+    lib.tsb_stats_read.restype = ctypes.c_int
+    lib.tsb_stats_read.argtypes = [ctypes.POINTER(TsbStats), ctypes.c_int32]
     _LIB = lib
     return lib
 
@@ -402,3 +415,19 @@ def profile_kernel(kernel, start=None, stop=None):
         st = load().tsb_profile_kernel(kid, ctypes.c_void_p(start.cuda_event), ctypes.c_void_p(stop.cuda_event))
     if st:
         raise TsbError(st, "tsb_profile_kernel")
+
+
+def stats_enable(on=True):
+    """Turn the work counters of the replay scan, the walk and the planner on or off (calling thread)."""
+    st = load().tsb_stats_enable(1 if on else 0)
+    if st:
+        raise TsbError(st, "tsb_stats_enable")
+
+
+def stats_read(reset=True):
+    """The current device's work counters as a dict (waits for the device); reset zeroes them."""
+    out = TsbStats()
+    st = load().tsb_stats_read(ctypes.byref(out), 1 if reset else 0)
+    if st:
+        raise TsbError(st, "tsb_stats_read")
+    return {n: int(getattr(out, n)) for n in STATS_FIELDS}

@@ -1005,17 +1005,22 @@ __global__ __launch_bounds__(kPlanThreads) void plan_tree(int D, int S, int K, i
                                                           const int* __restrict__ pf, double* __restrict__ draft_lse,
                                                           int32_t* __restrict__ topk_tok,
                                                           float* __restrict__ topk_lp, tsb_tree tree,
-                                                          int32_t* __restrict__ req_status) {
+                                                          int32_t* __restrict__ req_status,
+                                                          unsigned long long* __restrict__ stats) {
     __shared__ PlanShared sh;
     const int r = blockIdx.x;
     const int tid = threadIdx.x;
     const int wave = tid / kWave, lane = tid % kWave;
+    unsigned long long t_start = 0, t_merge = 0, t_search = 0;  // work counters (thread 0)
+    int n_rounds = 0;
+    if (stats && tid == 0) t_start = __builtin_amdgcn_s_memrealtime();
 
     if (tid == 0) sh.bad = 0;
     __syncthreads();
     for (int d = wave; d < D; d += kPlanWaves)
         merge_row(sh, r * D + d, d, S, K, invT, pm, ps, pk, pf, draft_lse, topk_tok, topk_lp);
     __syncthreads();
+    if (stats && tid == 0) t_merge = __builtin_amdgcn_s_memrealtime();
     const bool nonfinite = sh.bad != 0;
     const int Dp = nonfinite ? 0 : D;
 
@@ -1033,6 +1038,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_tree(int D, int S, int K, i
     // every round raises count(hi) by at least one (at most B + 1 rounds); the
     // guard only bounds the loop
     for (int round = 0; hi_m > -INFINITY; ++round) {
+        n_rounds = round + 1;
         if (round > B + 1) {
             mode = 1;
             break;
@@ -1100,6 +1106,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_tree(int D, int S, int K, i
     }
     __syncthreads();
     if (wave != 0) return;
+    if (stats && tid == 0) t_search = __builtin_amdgcn_s_memrealtime();
 
     // ---- emission in BFS order (wave 0)
     const double tstar = sh.tstar;
@@ -1193,6 +1200,14 @@ __global__ __launch_bounds__(kPlanThreads) void plan_tree(int D, int S, int K, i
         if (nonfinite) st |= TSB_REQ_NONFINITE;
         else if (n < B + 1) st |= TSB_REQ_BUDGET_SHORT;
         req_status[r] = st;
+        if (stats) {
+            const unsigned long long t_end = __builtin_amdgcn_s_memrealtime();
+            atomicAdd(&stats[kStPlanRequests], 1ull);
+            atomicAdd(&stats[kStPlanMergeTicks], t_merge - t_start);
+            atomicAdd(&stats[kStPlanSearchTicks], t_search - t_merge);
+            atomicAdd(&stats[kStPlanEmitTicks], t_end - t_search);
+            atomicAdd(&stats[kStPlanRounds], (unsigned long long)n_rounds);
+        }
     }
 }
 
@@ -1585,7 +1600,7 @@ hipError_t launch_plan(const tsb_config& c, float invT, const void* draft, doubl
                                               topk_tok, topk_lp, tree, req_status);
     else
         plan_tree<<<c.R, kPlanThreads, 0, st>>>(c.D, g.S1, c.K, c.B, invT, pm, ps, pk, pf, draft_lse, topk_tok,
-                                                topk_lp, tree, req_status);
+                                                topk_lp, tree, req_status, stats_ptr());
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     return hook_after(TSB_KERNEL_PLAN_TREE, st);

@@ -33,7 +33,7 @@
 namespace tsb {
 
 constexpr int kTileGroups = kReplayTile / 4;  // groups of four tokens per tile
-constexpr int kPassGroups = kTileGroups / 2;  // groups per compaction pass
+constexpr int kPassGroups = kTileGroups / 4;  // groups per compaction pass
 constexpr int kScanWaves = kBlock / kWave;
 constexpr int kScanWorkgroups = 1536;  // resident at 6 waves per SIMD
 
@@ -228,13 +228,17 @@ __global__ __launch_bounds__(kBlock) void replay_scan(const void* __restrict__ d
                                                       tsb_tree tree, const int* __restrict__ plist,
                                                       const int* __restrict__ ptotal, const float4* __restrict__ rec,
                                                       uint32_t k0, uint32_t k1, uint32_t step,
-                                                      uint64_t* __restrict__ out_cand, int* __restrict__ out_cnt) {
-    // surviving groups of the current pass, per wave: (group, largest b)
-    __shared__ uint2 s_queue[kScanWaves][kPassGroups];
+                                                      uint64_t* __restrict__ out_cand, int* __restrict__ out_cnt,
+                                                      unsigned long long* __restrict__ stats) {
+    // surviving groups of the current pass, per wave: (group, its four bf16
+    // logits as two words, largest b); binary32 rows keep (group, largest b)
+    // and read the group again
+    __shared__ uint4 s_queue[kScanWaves][kPassGroups];
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    uint2* queue = s_queue[wave];
+    uint4* queue = s_queue[wave];
     const long long items = (long long)ptotal[0] * T;
     const long long nw = (long long)gridDim.x * kScanWaves;
+    unsigned long long n_items = 0, n_tokens = 0, n_live = 0, n_keyed = 0;  // work counters (wave-uniform)
     for (long long it = (long long)blockIdx.x * kScanWaves + wave; it < items; it += nw) {
         const int pi = (int)(it / T);
         const int t = (int)(it - (long long)pi * T);
@@ -261,41 +265,40 @@ __global__ __launch_bounds__(kBlock) void replay_scan(const void* __restrict__ d
         const uint32_t blk0 = (uint32_t)(t0 >> 2);
         WaveTopList top;
         top.init(m);
+        constexpr int kPer = kPassGroups / kWave;  // groups per lane and pass
 #pragma unroll 1
         for (int g0 = 0; g0 < kTileGroups; g0 += kPassGroups) {
             // 1. largest b of each group of four (b = fl32(x invT - c_d) is
             // non-decreasing in x, so it is that of the largest raw logit);
             // groups whose largest b cannot reach thr are dropped, the rest
             // are compacted within the wave
-            constexpr int kPer = kPassGroups / kWave;  // groups per lane
-            float gx[kPer];
+            float x[kPer][4];
             if (full) {
-                float x[kPer][4];
 #pragma unroll
                 for (int k = 0; k < kPer; ++k) load_x4<DT, VEC, true>(draft, tbase, (g0 + k * kWave + lane) * 4, tn, x[k]);
-#pragma unroll
-                for (int k = 0; k < kPer; ++k) gx[k] = fmaxf(fmaxf(x[k][0], x[k][1]), fmaxf(x[k][2], x[k][3]));
             } else {
 #pragma unroll
-                for (int k = 0; k < kPer; ++k) {
-                    float x[4];
-                    load_x4<DT, VEC, false>(draft, tbase, (g0 + k * kWave + lane) * 4, tn, x);
-                    gx[k] = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
-                }
+                for (int k = 0; k < kPer; ++k) load_x4<DT, VEC, false>(draft, tbase, (g0 + k * kWave + lane) * 4, tn, x[k]);
             }
             int qn = 0;
 #pragma unroll
             for (int k = 0; k < kPer; ++k) {
-                const float bmax = gx[k] * invT - cd;
+                const float gx = fmaxf(fmaxf(x[k][0], x[k][1]), fmaxf(x[k][2], x[k][3]));
+                const float bmax = gx * invT - cd;
                 const bool live = bmax >= bound && bmax > -INFINITY;
                 const uint64_t bal = __ballot(live);
-                if (live)
+                if (live) {
+                    // a bf16 logit is the top half of its binary32 value (-inf past tn included)
+                    const uint32_t w0 = (__float_as_uint(x[k][0]) >> 16) | (__float_as_uint(x[k][1]) & 0xFFFF0000u);
+                    const uint32_t w1 = (__float_as_uint(x[k][2]) >> 16) | (__float_as_uint(x[k][3]) & 0xFFFF0000u);
                     queue[qn + __popcll(bal & ((1ull << lane) - 1ull))] =
-                        make_uint2((uint32_t)(g0 + k * kWave + lane), __float_as_uint(bmax));
+                        make_uint4((uint32_t)(g0 + k * kWave + lane), w0, w1, __float_as_uint(bmax));
+                }
                 qn += __popcll(bal);
             }
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            n_live += (unsigned)qn;
 
             // 2. Philox for the survivors; a word below its group's floor is a
             // certain miss; groups holding a word at or above it get their
@@ -303,14 +306,24 @@ __global__ __launch_bounds__(kBlock) void replay_scan(const void* __restrict__ d
             for (int base = 0; base < qn; base += kWave) {
                 const int q = base + lane;
                 const bool valid = q < qn;
-                const uint2 ent = queue[valid ? q : 0];
+                const uint4 ent = queue[valid ? q : 0];
                 const int gl = (int)ent.x;
                 const uint4 w = rng_block(key, (uint32_t)u, kStreamReplay, blk0 + (uint32_t)gl);
-                const uint32_t wf = gumbel_word_floor(thr, __uint_as_float(ent.y), slack);
+                const uint32_t wf = gumbel_word_floor(thr, __uint_as_float(ent.w), slack);
                 const bool pass = valid && max(max(w.x, w.y), max(w.z, w.w)) >= wf;
-                if (__ballot(pass) == 0) continue;
+                const uint64_t pb = __ballot(pass);
+                n_keyed += (unsigned)__popcll(pb);
+                if (pb == 0) continue;
                 float bv[4];
-                load_b4<DT, VEC>(draft, tbase, gl * 4, pass ? tn : 0, invT, cd, bv);
+                if constexpr (DT == TSB_BF16) {
+                    // the group's logits come from the queue (no second read)
+                    const float xq[4] = {__uint_as_float(ent.y << 16), __uint_as_float(ent.y & 0xFFFF0000u),
+                                         __uint_as_float(ent.z << 16), __uint_as_float(ent.z & 0xFFFF0000u)};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) bv[e] = (pass && gl * 4 + e < tn) ? xq[e] * invT - cd : -INFINITY;
+                } else {
+                    load_b4<DT, VEC>(draft, tbase, gl * 4, pass ? tn : 0, invT, cd, bv);
+                }
                 const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
                 float kv[4];
 #pragma unroll
@@ -328,6 +341,14 @@ __global__ __launch_bounds__(kBlock) void replay_scan(const void* __restrict__ d
         const int cnt = __popcll(__ballot(lane < m && top.v != 0));
         if (lane < cnt) out_cand[o * TSB_MAX_K + lane] = top.v;
         if (lane == 0) out_cnt[o] = cnt;
+        n_items += 1;
+        n_tokens += (unsigned)tn;
+    }
+    if (stats && lane == 0 && n_items) {
+        atomicAdd(&stats[kStReplayItems], n_items);
+        atomicAdd(&stats[kStReplayTokens], n_tokens);
+        atomicAdd(&stats[kStReplayLive], n_live);
+        atomicAdd(&stats[kStReplayKeyed], n_keyed);
     }
 }
 
@@ -439,23 +460,24 @@ hipError_t launch_replay(const tsb_config& c, float invT, const void* draft, con
         replay_threshold<TSB_F32><<<nthr, kBlock, 0, st>>>(draft, c.R, c.V, c.D, c.B, c.K, invT, topk_tok, tree, k0,
                                                            k1, step, prune, rec, plist, ptotal);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+    unsigned long long* const stats = stats_ptr();
     // a persistent grid: the item count is only known on the device
     const long long max_items = (long long)c.R * c.B * g.T;
     const int grid = (int)std::max<long long>(1, std::min<long long>(kScanWorkgroups, (max_items + kScanWaves - 1) / kScanWaves));
     if (c.dtype == TSB_BF16) {
         if (vec)
             replay_scan<TSB_BF16, true><<<grid, kBlock, 0, st>>>(draft, c.V, c.D, c.B, c.K, g.T, invT, topk_tok, tree,
-                                                                 plist, ptotal, rec, k0, k1, step, cand, cc);
+                                                                 plist, ptotal, rec, k0, k1, step, cand, cc, stats);
         else
             replay_scan<TSB_BF16, false><<<grid, kBlock, 0, st>>>(draft, c.V, c.D, c.B, c.K, g.T, invT, topk_tok,
-                                                                  tree, plist, ptotal, rec, k0, k1, step, cand, cc);
+                                                                  tree, plist, ptotal, rec, k0, k1, step, cand, cc, stats);
     } else {
         if (vec)
             replay_scan<TSB_F32, true><<<grid, kBlock, 0, st>>>(draft, c.V, c.D, c.B, c.K, g.T, invT, topk_tok, tree,
-                                                                plist, ptotal, rec, k0, k1, step, cand, cc);
+                                                                plist, ptotal, rec, k0, k1, step, cand, cc, stats);
         else
             replay_scan<TSB_F32, false><<<grid, kBlock, 0, st>>>(draft, c.V, c.D, c.B, c.K, g.T, invT, topk_tok, tree,
-                                                                 plist, ptotal, rec, k0, k1, step, cand, cc);
+                                                                 plist, ptotal, rec, k0, k1, step, cand, cc, stats);
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;

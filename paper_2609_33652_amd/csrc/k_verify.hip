@@ -187,6 +187,7 @@ struct WalkArgs {
     XRegion X;  // exchange slots of the requests
     int V, D, B, S4;
     int R, G;   // requests and workgroups per request of the launch (tickets)
+    unsigned long long* stats;  // work counters (null: none)
     float invT;
     uint32_t k0, k1, step;
     // pool walk only: pools [R, D, P] and transition scores [R, D-1, P, P]
@@ -735,6 +736,7 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
     const bool draft_bad = (*status_p & TSB_REQ_NONFINITE) != 0;
 
     int tcount = 0;
+    int n_entered = 0;  // nodes entered (work counter)
     double* const trace = (lead && A.out.trace) ? A.out.trace + (size_t)r * TSB_TRACE_MAX * 4 : nullptr;
 
     int bonus_out = -1, add_status = count_ok ? 0 : TSB_REQ_BAD_TREE, nacc = 0;
@@ -748,6 +750,7 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
         Exchange X{&A, r, g, G, 0u, 0};
         int u = 0;
         while (true) {
+            ++n_entered;
             // every workgroup reads the same entries, so all take the same exit
             const TreeNode nd = tree_node(A.tree, tb, u, n, A.D);
             if (!nd.ok || (nd.m > 0 && nacc >= A.D)) {
@@ -920,6 +923,12 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
             break;
         }
         if (X.timeout) add_status |= TSB_REQ_WALK_TIMEOUT;
+        if (A.stats && lead) {
+            atomicAdd(&A.stats[kStWalkRequests], 1ull);
+            atomicAdd(&A.stats[kStWalkNodes], (unsigned long long)n_entered);
+            atomicAdd(&A.stats[kStWalkTests], (unsigned long long)tcount);
+            atomicAdd(&A.stats[kStWalkExchanges], (unsigned long long)X.nb);
+        }
     }
 
     walk_tail(A, r, g, G, n, draft_bad, invalid, nacc, bonus_out, add_status, tcount);
@@ -1620,6 +1629,7 @@ static WalkArgs walk_args(const tsb_config& c, float invT, const void* draft, co
     A.S4 = g.S4;
     A.R = c.R;
     A.G = 1;
+    A.stats = stats_ptr();
     A.invT = invT;
     A.k0 = (uint32_t)c.seed;
     A.k1 = (uint32_t)(c.seed >> 32);

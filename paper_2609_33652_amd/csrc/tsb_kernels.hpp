@@ -24,6 +24,16 @@ inline hipError_t hook_after(int kernel, hipStream_t st) {
     return h.kernel == kernel ? hipEventRecord(h.stop, st) : hipSuccess;
 }
 
+// Device counter block of tsb_stats on the current device while counting is
+// enabled on the calling thread, else null (kernels then count nothing).
+unsigned long long* stats_ptr();
+enum : int {
+    kStReplayItems = 0, kStReplayTokens, kStReplayLive, kStReplayKeyed,
+    kStWalkRequests, kStWalkNodes, kStWalkTests, kStWalkExchanges,
+    kStPlanRequests, kStPlanMergeTicks, kStPlanSearchTicks, kStPlanEmitTicks, kStPlanRounds,
+    kStCount = 16
+};
+
 // frontier > 0: the expand-then-prune first pass with that frontier width;
 // 0: the max-heap first pass.
 hipError_t launch_plan(const tsb_config& c, float invT, const void* draft, double* draft_lse, int32_t* topk_tok,

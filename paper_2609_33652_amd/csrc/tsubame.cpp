@@ -128,6 +128,37 @@ ProfileHook& profile_hook() {
     static thread_local ProfileHook h;
     return h;
 }
+
+// The tsb_stats counter block: one per device (a file-scope array; in host
+// code its name is not a device address: the address comes from
+// hipGetSymbolAddress, taken once per device).
+__device__ __align__(256) unsigned long long counters[kStCount];
+static_assert(sizeof(tsb_stats) == kStCount * sizeof(unsigned long long), "tsb_stats layout");
+thread_local bool g_stats_on = false;
+std::mutex g_counters_mu;
+void* g_counters_ptr[kMaxDevices];
+
+hipError_t counters_address(void** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_counters_mu);
+    if (!g_counters_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(counters));
+        if (e != hipSuccess) return e;
+        g_counters_ptr[dev] = p;
+    }
+    *out = g_counters_ptr[dev];
+    return hipSuccess;
+}
+
+unsigned long long* stats_ptr() {
+    if (!g_stats_on) return nullptr;
+    void* p = nullptr;
+    return counters_address(&p) == hipSuccess ? (unsigned long long*)p : nullptr;
+}
 }  // namespace tsb
 
 extern "C" {
@@ -417,6 +448,32 @@ tsb_status tsb_profile_kernel(int32_t kernel_id, hipEvent_t start, hipEvent_t st
     h.kernel = kernel_id;
     h.start = start;
     h.stop = stop;
+    return TSB_OK;
+}
+
+tsb_status tsb_stats_enable(int32_t on) {
+    g_last_error[0] = 0;
+    void* p = nullptr;
+    const hipError_t e = tsb::counters_address(&p);
+    if (e != hipSuccess) return hip_fail(e, "tsb_stats_enable/hipGetSymbolAddress(counters)");
+    tsb::g_stats_on = on != 0;
+    return TSB_OK;
+}
+
+tsb_status tsb_stats_read(tsb_stats* out, int32_t reset) {
+    g_last_error[0] = 0;
+    if (!out) return fail(TSB_E_NULL, "out is NULL");
+    void* p = nullptr;
+    hipError_t e = tsb::counters_address(&p);
+    if (e != hipSuccess) return hip_fail(e, "tsb_stats_read/hipGetSymbolAddress(counters)");
+    if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(e, "tsb_stats_read/hipDeviceSynchronize");
+    if ((e = hipMemcpy(out, p, sizeof(tsb_stats), hipMemcpyDeviceToHost)) != hipSuccess)
+        return hip_fail(e, "tsb_stats_read/hipMemcpy");
+    if (reset) {
+        const tsb_stats zero = {};
+        if ((e = hipMemcpy(p, &zero, sizeof(tsb_stats), hipMemcpyHostToDevice)) != hipSuccess)
+            return hip_fail(e, "tsb_stats_read/hipMemcpy(reset)");
+    }
     return TSB_OK;
 }
 
