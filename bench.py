@@ -32,13 +32,13 @@ POOL_KERNELS = ("pool_partials", "pool_lists", "pool_plan", "pool_replay", "targ
 # HBM bytes per launch of target_partials at the batched workload from the
 # FETCH_SIZE / WRITE_SIZE counter passes (KiB, scaled by a plain copy of known
 # size: FETCH x2.0, WRITE x1.0), valid for the kernel source they were taken on
-TARGET_TRAFFIC = {"config": 4, "source_sha256_16": "d1240d8a06bfe313", "fetch_kib": 309857.9, "write_kib": 266.8,
+TARGET_TRAFFIC = {"config": 4, "source_sha256_16": "21c2780168091d03", "fetch_kib": 309880.6, "write_kib": 522.3,
                   "fetch_scale": 2.0, "write_scale": 1.0}
 
 
 # VALU wave-instructions per launch of replay_scan at the batched workload from
 # an SQ_INSTS_VALU counter pass, valid for the scan source it was taken on
-REPLAY_COUNTERS = {"config": 4, "source_sha256_16": None, "insts_valu": None}
+REPLAY_COUNTERS = {"config": 4, "source_sha256_16": "28b0e18fdeb2b7fe", "insts_valu": 30551478.7}
 # peak VALU issue: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = 39.3e12 lane
 # operations/s, i.e. 614.4e9 wave64 instructions/s
 VALU_PEAK_WAVE_INSTS = 256 * 2.4e9
