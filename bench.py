@@ -9,8 +9,9 @@ are synthetic (workloads package), resident in HBM before timing starts; a
 pool of P distinct input sets is rotated so that no step reuses cached rows.
 
 Prints one JSON line: steps/s as `value`, verified tree nodes/s, the
-roofline of the dominant (target-streaming) kernel measured live with HIP
-events on the launch stream, a per-kernel breakdown, and the CPU oracle
+roofline of the dominant kernel (the replay scan, whose grid also streams
+the target's row normalisers) measured live with HIP events on the launch
+stream, the target stream alone, a per-kernel breakdown, and the CPU oracle
 timed on a bounded sample of the same workload on the host cores.
 """
 import argparse
@@ -25,54 +26,76 @@ sys.path.insert(0, ROOT)
 import workloads as W  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
-# kernels launched by one replay + RRS round, and by one round over sparse pools
-STEP_KERNELS = ("draft_partials", "plan_tree", "replay_scan", "replay_merge", "target_partials", "verify_walk")
+# kernels launched by one replay + RRS round (the replay scan's grid also
+# streams the target), and by one round over sparse pools
+STEP_KERNELS = ("draft_partials", "plan_tree", "scan_target", "replay_merge", "verify_walk")
 POOL_KERNELS = ("pool_partials", "pool_lists", "pool_plan", "pool_replay", "target_partials", "pool_walk")
 
-# HBM bytes per launch of target_partials at the batched workload from the
-# FETCH_SIZE / WRITE_SIZE counter passes (KiB, scaled by a plain copy of known
-# size: FETCH x2.0, WRITE x1.0), valid for the kernel source they were taken on
-TARGET_TRAFFIC = {"config": 4, "source_sha256_16": "21c2780168091d03", "fetch_kib": 309880.6, "write_kib": 522.3,
-                  "fetch_scale": 2.0, "write_scale": 1.0}
-
-
-# VALU wave-instructions per launch of replay_scan at the batched workload from
-# an SQ_INSTS_VALU counter pass, valid for the scan source it was taken on
-REPLAY_COUNTERS = {"config": 4, "source_sha256_16": "28b0e18fdeb2b7fe", "insts_valu": 30551478.7}
+# Counter passes per launch at the batched workload, valid for the kernel
+# source they were taken on: HBM traffic from FETCH_SIZE / WRITE_SIZE (KiB,
+# scaled by a plain copy of known size: FETCH x2.0, WRITE x1.0) and VALU
+# wave-instructions from SQ_INSTS_VALU.
+COUNTERS = {
+    "scan_target": {"config": 4, "source_sha256_16": None, "fetch_kib": None, "write_kib": None,
+                    "insts_valu": None},
+    "target_partials": {"config": 4, "source_sha256_16": None, "fetch_kib": None, "write_kib": None,
+                        "insts_valu": None},
+}
+FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 # peak VALU issue: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = 39.3e12 lane
 # operations/s, i.e. 614.4e9 wave64 instructions/s
 VALU_PEAK_WAVE_INSTS = 256 * 2.4e9
 
 
-def _section_hash(path, start, end):
-    import hashlib
-    src = open(os.path.join(ROOT, "paper_2609_33652_amd", "csrc", path)).read()
+def _read(path):
+    return open(os.path.join(ROOT, "paper_2609_33652_amd", "csrc", path)).read()
+
+
+def _section(path, start, end):
+    src = _read(path)
     a, b = src.find(start), src.find(end)
-    if a < 0 or b < 0:
-        return None
-    return hashlib.sha256(src[a:b].encode()).hexdigest()[:16]
+    return None if a < 0 or b < 0 else src[a:b]
 
 
-def replay_insts(cfg_id):
-    """Counter-measured VALU wave-instructions per replay_scan launch, or None if the scan or workload differs."""
-    t = REPLAY_COUNTERS
-    h = _section_hash("k_replay.hip", "__global__ __launch_bounds__(kBlock) void replay_scan(",
-                      "__global__ __launch_bounds__(kWave) void replay_merge(")
-    if cfg_id != t["config"] or t["insts_valu"] is None or h != t["source_sha256_16"]:
-        return None
-    return t["insts_valu"]
-
-
-def target_traffic(cfg_id):
-    """Counter-measured bytes per launch, or None if the kernel or workload differs from the counted one."""
+def source_hash(kernel):
+    """Hash of the source a kernel is built from (its device code), to tie counter figures to it."""
     import hashlib
-    src = open(os.path.join(ROOT, "paper_2609_33652_amd", "csrc", "k_verify.hip")).read()
-    a = src.find("// ------------------------------------------------------------------ K4")
-    b = src.find("// ------------------------------------------------------------------ K5")
-    t = TARGET_TRAFFIC
-    if cfg_id != t["config"] or a < 0 or b < 0 or hashlib.sha256(src[a:b].encode()).hexdigest()[:16] != t["source_sha256_16"]:
+    if kernel == "scan_target":
+        parts = [_section("k_replay.hip", "struct ScanArgs {", "__global__ __launch_bounds__(kWave) void replay_merge("),
+                 _read("tsb_target.hpp")]
+    elif kernel == "target_partials":
+        parts = [_section("k_verify.hip", "// ------------------------------------------------------------------ K4",
+                          "// ------------------------------------------------------------------ K5"),
+                 _read("tsb_target.hpp")]
+    else:
         return None
-    return int(round((t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"]) * 1024))
+    if any(p is None for p in parts):
+        return None
+    return hashlib.sha256("".join(parts).encode()).hexdigest()[:16]
+
+
+def counted(kernel, cfg_id):
+    """Counter figures of a kernel at this workload: (traffic bytes or None, VALU wave-instructions or None)."""
+    t = COUNTERS.get(kernel)
+    if t is None or cfg_id != t["config"] or t["source_sha256_16"] is None or source_hash(kernel) != t["source_sha256_16"]:
+        return None, None
+    traffic = None
+    if t["fetch_kib"] is not None and t["write_kib"] is not None:
+        traffic = int(round((t["fetch_kib"] * FETCH_SCALE + t["write_kib"] * WRITE_SCALE) * 1024))
+    return traffic, t["insts_valu"]
+
+
+def parent_rows(h, B):
+    """Distinct (request, depth) draft rows that hold at least one parent of a round's tree."""
+    import torch
+    n = h["n_nodes"].long()
+    idx = torch.arange(B + 1).unsqueeze(0)
+    par = (idx < n.unsqueeze(1)) & (h["n_children"].long() > 0)
+    dep = h["depth"].long().clamp(min=0)
+    rows = set()
+    for r, u in par.nonzero().tolist():
+        rows.add((r, int(dep[r, u])))
+    return len(rows)
 
 
 def log(*a):
@@ -478,9 +501,10 @@ def main():
         rnd.step(drafts[s % P], targets[s % P], s)
     torch.cuda.synchronize()
 
-    K4 = tsb.KERNELS.index("target_partials")
-    # the target kernel is bracketed by events on every `sample`-th timed step
-    # (each event pair costs a few microseconds of idle GPU)
+    K4 = tsb.KERNELS.index("scan_target")
+    # the dominant kernel (replay scan + target stream) is bracketed by events
+    # on every `sample`-th timed step (each event pair costs a few
+    # microseconds of idle GPU)
     sampled = list(range(0, args.steps, args.sample))
     ev = events(len(sampled))
     start = torch.cuda.Event(enable_timing=True)
@@ -520,15 +544,28 @@ def main():
         rnd.step(drafts[i % P], targets[i % P], i)
     work = tsb.stats_read(reset=True)
     tsb.stats_enable(False)
-    acc, nodes, flagged = 0, 0, 0
+    acc, nodes, flagged, trows, drows = 0, 0, 0, 0, 0
     for i in range(P):
         rnd.step(drafts[i], targets[i], i)
         h = rnd.host()
         acc += int(h["n_acc"].clamp(min=0).sum()) + int((h["n_acc"] >= 0).sum())
         nodes += int((h["n_nodes"] - 1).sum())
         flagged += int((h["req_status"] & (tsb.REQ_NONFINITE | tsb.REQ_WALK_TIMEOUT)).ne(0).sum())
+        trows += int(h["n_nodes"].sum())
+        drows += parent_rows(h, B)
     tau = acc / (P * R)
     nodes_per_step = nodes / P
+    # the target stream alone (the verification entry point launches it on
+    # its own grid), for its own roofline
+    KT = tsb.KERNELS.index("target_partials")
+    evt = events(args.breakdown_steps)
+    for i in range(args.breakdown_steps):
+        rnd.step(drafts[i % P], targets[i % P], i)
+        tsb.profile_kernel(KT, evt[i][0], evt[i][1])
+        rnd.verify(drafts[i % P], targets[i % P], i)
+        tsb.profile_kernel(KT, None)
+    torch.cuda.synchronize()
+    kt_us = 1000.0 * sum(a.elapsed_time(b) for a, b in evt) / args.breakdown_steps
 
     first = first_naive(tsb, c, dev, drafts, targets, args, cfg)
     first["cpu_baseline"] = cpu_first
@@ -549,22 +586,32 @@ def main():
         latency = {W.config(i)["name"]: latency_block(tsb, i, args) for i in (1, 2, 3)}
 
     b = 2 if cfg["dtype"] == "bf16" else 4
-    k4_bytes = R * (B + 1) * V * b  # every target row of a full tree, read once
+    # algorithmic bytes of one scan_target launch: every target row of the
+    # tree and every draft row that holds parents, each read once
+    t_bytes = trows * V * b // P
+    d_bytes = drows * V * b // P
+    k4_bytes = t_bytes + d_bytes
     nst = max(1, args.breakdown_steps)
-    insts = replay_insts(args.config)
+    traffic, insts = counted("scan_target", args.config)
     replay = {
-        "kernel": "replay_scan", "bound": "alu", "avg_launch_us": kern_us["replay_scan"],
+        "kernel": "scan_target", "bound": "alu", "avg_launch_us": kern_us["scan_target"],
         "items_per_launch": round(work["replay_items"] / nst, 1),
         "tokens_per_launch": round(work["replay_tokens"] / nst, 1),
         "live_fraction": round(4 * work["replay_groups_live"] / max(1, work["replay_tokens"]), 5),
         "keyed_fraction": round(4 * work["replay_groups_keyed"] / max(1, work["replay_tokens"]), 5),
         "valu_insts_per_launch": insts,
-        "achieved": None if insts is None else round(insts / (kern_us["replay_scan"] * 1e-6) / 1e9, 1),
+        "achieved": None if insts is None else round(insts / (kern_us["scan_target"] * 1e-6) / 1e9, 1),
         "peak": VALU_PEAK_WAVE_INSTS / 1e9, "unit": "G wave64 VALU instructions/s",
-        "frac": None if insts is None else round(insts / (kern_us["replay_scan"] * 1e-6) / VALU_PEAK_WAVE_INSTS, 4),
-        "note": "fractions are of the scanned tiles' tokens, in groups of four: live = the group's largest key bound "
-                "reaches the parent's threshold (its Philox words are drawn), keyed = a word passes the floor "
-                "(its Gumbel keys are evaluated)"}
+        "frac": None if insts is None else round(insts / (kern_us["scan_target"] * 1e-6) / VALU_PEAK_WAVE_INSTS, 4),
+        "note": "VALU issue of the whole launch (scan and target stream); fractions are of the scanned tiles' "
+                "tokens, in groups of four: live = the group's largest key bound reaches the parent's threshold "
+                "(its Philox words are drawn), keyed = a word passes the floor (its Gumbel keys are evaluated)"}
+    t_traffic, t_insts = counted("target_partials", args.config)
+    target_stream = {"kernel": "target_partials", "bound": "hbm",
+                     "achieved": round(t_bytes / (kt_us * 1e-6) / 1e9, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(t_bytes / (kt_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4), "traffic": t_traffic,
+                     "bytes_per_launch": t_bytes, "avg_launch_us": round(kt_us, 2),
+                     "source": "tsb_verify after each round, untimed pass"}
     wr = max(1, work["walk_requests"])
     walk = {"kernel": "verify_walk", "avg_launch_us": kern_us["verify_walk"],
             "nodes_per_request": round(work["walk_nodes"] / wr, 3),
@@ -603,11 +650,15 @@ def main():
         "nodes_verified_per_s": round(nodes_per_step * steps_per_s, 1),
         "accepted_tokens_per_s": round(tau * R * steps_per_s, 1),
         "tau": round(tau, 4),
-        "roofline": {"kernel": "target_partials", "bound": "hbm", "achieved": round(achieved, 1),
+        "roofline": {"kernel": "scan_target", "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": target_traffic(args.config), "bytes_per_launch": k4_bytes, "avg_launch_us": round(k4_ms * 1000, 2),
-                     "timed_launches": len(ev)},
+                     "traffic": traffic, "bytes_per_launch": k4_bytes, "target_bytes": t_bytes,
+                     "draft_bytes": d_bytes, "avg_launch_us": round(k4_ms * 1000, 2),
+                     "timed_launches": len(ev),
+                     "note": "one grid streams every target row of the tree (row normalisers for the walk) and "
+                             "scans the draft rows of the parents' depths (replay); bytes count each row once"},
         "kernels_us": kern_us,
+        "roofline_target_stream": target_stream,
         # the other logit-streaming kernel, from the untimed per-kernel pass
         "roofline_draft": {"kernel": "draft_partials", "bound": "hbm (VALU-bound: a table lookup and a binary64 add per logit)",
                            "achieved": round(k1_bytes / (kern_us["draft_partials"] * 1e-6) / 1e9, 1),

@@ -204,7 +204,9 @@ tsb_status tsb_verify(const tsb_config* cfg, const void* draft, const double* dr
                       uint32_t step, const tsb_verdict* out, void* workspace,
                       size_t workspace_bytes, hipStream_t stream);
 
-/* plan -> replay -> verify back to back on one stream (target supplied up front). */
+/* plan -> replay -> verify back to back on one stream (target supplied up
+ * front). The replay scan's grid also streams the target's row normalisers
+ * (one launch for both), so the walk follows the replay directly. */
 tsb_status tsb_step(const tsb_config* cfg, const void* draft, const void* target, uint32_t step,
                     double* draft_lse, int32_t* topk_tok, float* topk_lp, const tsb_tree* tree,
                     int32_t* node_tok, const tsb_verdict* out, void* workspace,
@@ -364,9 +366,9 @@ tsb_status tsb_pool_step(const tsb_config* cfg, int32_t P, const void* draft, co
 enum {
     TSB_KERNEL_DRAFT_PARTIALS = 0, /* draft row statistics + candidates (streams the draft) */
     TSB_KERNEL_PLAN_TREE = 1,      /* row merge + topology planning */
-    TSB_KERNEL_REPLAY_SCAN = 2,
+    TSB_KERNEL_REPLAY_SCAN = 2,    /* replay scan of tsb_replay (after its threshold kernel) */
     TSB_KERNEL_REPLAY_MERGE = 3,
-    TSB_KERNEL_TARGET_PARTIALS = 4, /* target row statistics (streams the target) */
+    TSB_KERNEL_TARGET_PARTIALS = 4, /* target row statistics (streams the target; verification entry points) */
     TSB_KERNEL_VERIFY_WALK = 5,
     TSB_KERNEL_VERIFY_NAIVE = 6,    /* target-sample matching walk */
     TSB_KERNEL_POOL_PARTIALS = 7,   /* pool selection (streams the draft) */
@@ -375,7 +377,8 @@ enum {
     TSB_KERNEL_POOL_REPLAY = 10,
     TSB_KERNEL_POOL_WALK = 11,      /* verification with pool-restricted q_u */
     TSB_KERNEL_TRAVERSAL_WALK = 12, /* traversal verification */
-    TSB_KERNEL_COUNT = 13
+    TSB_KERNEL_SCAN_TARGET = 13,    /* replay scan + target row statistics in one grid (whole rounds) */
+    TSB_KERNEL_COUNT = 14
 };
 tsb_status tsb_profile_kernel(int32_t kernel_id, hipEvent_t start, hipEvent_t stop);
 

@@ -33,7 +33,7 @@ FLAG_NO_PRUNE = 1
 MAX_D, MAX_K, MAX_B, TRACE_MAX = 64, 32, 1023, 256
 KERNELS = ("draft_partials", "plan_tree", "replay_scan", "replay_merge", "target_partials",
            "verify_walk", "verify_naive", "pool_partials", "pool_lists", "pool_plan", "pool_replay", "pool_walk",
-           "traversal_walk")
+           "traversal_walk", "scan_target")
 
 EXPORTS = ("tsb_workspace_bytes", "tsb_plan", "tsb_plan_ep", "tsb_replay", "tsb_verify", "tsb_step",
            "tsb_first_tokens", "tsb_verify_naive", "tsb_step_first",

@@ -17,6 +17,12 @@
 //                 wave and only they pay for Philox and two logarithms; the
 //                 wave keeps the parent's m best keys of the tile in a sorted
 //                 wave-wide list.
+//   replay_scan_target
+//                 the scan of a whole round (tsb_step and its variants): one
+//                 grid whose first workgroups stream the target's row
+//                 normalisers for verification (target_chunk) while the
+//                 others scan, so the HBM-bound stream and the VALU-bound
+//                 scan share the compute units.
 //   replay_merge  one wave per parent: merge the per-tile lists, keep the m
 //                 best (key desc, token asc) in slot order.
 //
@@ -29,6 +35,7 @@
 
 #include "tsb_device.hpp"
 #include "tsb_kernels.hpp"
+#include "tsb_target.hpp"
 
 namespace tsb {
 
@@ -36,6 +43,11 @@ constexpr int kTileGroups = kReplayTile / 4;  // groups of four tokens per tile
 constexpr int kPassGroups = kTileGroups / 4;  // groups per compaction pass
 constexpr int kScanWaves = kBlock / kWave;
 constexpr int kScanWorkgroups = 1536;  // resident at 6 waves per SIMD
+// Workgroups of replay_scan_target: the target's (4 waves per SIMD) and the
+// scan's beside them (they fill the other 4 as they fit, the rest start as
+// workgroups finish).
+constexpr int kFusedTargetWorkgroups = 1024;
+constexpr int kFusedScanWorkgroups = 1536;
 
 // A parent that replay fills: a well-formed node of the caller's topology
 // (entries in range, see tree_node) with 1 <= m <= K children. Malformed
@@ -222,134 +234,198 @@ __device__ __forceinline__ uint32_t gumbel_word_floor(float thr, float bmax, flo
     return (uint32_t)fmaxf(k, 0.0f) << 9;
 }
 
+struct ScanArgs {
+    const void* draft;
+    int V, D, B, T;
+    float invT;
+    const int* plist;
+    const float4* rec;
+    uint32_t k0, k1, step;
+    uint64_t* out_cand;
+    int* out_cnt;
+};
+// Work counters of one wave in LDS (items, tokens, live groups, keyed
+// groups), kept only while counting is on; lane 0 updates them.
+struct ScanCounters {
+    unsigned long long* c;  // null: not counting
+    __device__ void add(int k, unsigned long long v, int lane) const {
+        if (c && lane == 0) c[k] += v;
+    }
+    __device__ void flush(unsigned long long* stats, int lane) const {
+        if (c && lane == 0 && c[0]) {
+            atomicAdd(&stats[kStReplayItems], c[0]);
+            atomicAdd(&stats[kStReplayTokens], c[1]);
+            atomicAdd(&stats[kStReplayLive], c[2]);
+            atomicAdd(&stats[kStReplayKeyed], c[3]);
+        }
+    }
+};
+__device__ __forceinline__ ScanCounters scan_counters(unsigned long long (*s)[4], int wave, int lane,
+                                                      const unsigned long long* stats) {
+    ScanCounters C;
+    C.c = stats ? s[wave] : nullptr;
+    if (C.c && lane < 4) C.c[lane] = 0;
+    return C;
+}
+
+// One (parent, tile) item, by one wave; `queue` is the wave's LDS queue.
 template <int DT, bool VEC>
-__global__ __launch_bounds__(kBlock) void replay_scan(const void* __restrict__ draft, int V, int D, int B, int K,
-                                                      int T, float invT, const int32_t* __restrict__ topk_tok,
-                                                      tsb_tree tree, const int* __restrict__ plist,
-                                                      const int* __restrict__ ptotal, const float4* __restrict__ rec,
-                                                      uint32_t k0, uint32_t k1, uint32_t step,
-                                                      uint64_t* __restrict__ out_cand, int* __restrict__ out_cnt,
+__device__ __forceinline__ void scan_item(const ScanArgs& A, long long it, int lane, uint4* queue, const ScanCounters& C) {
+    const void* __restrict__ draft = A.draft;
+    const int V = A.V, D = A.D, B = A.B, T = A.T;
+    const float invT = A.invT;
+    const int pi = (int)(it / T);
+    const int t = (int)(it - (long long)pi * T);
+    const int node = A.plist[pi];
+    const float4 pr = A.rec[node];  // (c_d, thr, depth, m) of the parent
+    const int r = node / (B + 1);
+    const int u = node - r * (B + 1);
+    const int d = __float_as_int(pr.z);
+    const int m = __float_as_int(pr.w);
+    const size_t rowbase = ((size_t)r * D + d) * (size_t)V;
+    const float cd = pr.x;
+    const float thr = pr.y;
+    const float bound = thr - kGumbelMaxBound;
+    const int t0 = t * kReplayTile;
+    const int tn = min(kReplayTile, V - t0);
+    const size_t tbase = rowbase + t0;
+    const bool full = VEC && tn == kReplayTile;
+    const float slack = 0.25f + fabsf(thr) * 0x1p-20f;
+    RngKey key;
+    key.k0 = A.k0;
+    key.k1 = A.k1;
+    key.request = (uint32_t)r;
+    key.step = A.step;
+    const uint32_t blk0 = (uint32_t)(t0 >> 2);
+    WaveTopList top;
+    top.init(m);
+    constexpr int kPer = kPassGroups / kWave;  // groups per lane and pass
+#pragma unroll 1
+    for (int g0 = 0; g0 < kTileGroups; g0 += kPassGroups) {
+        // 1. largest b of each group of four (b = fl32(x invT - c_d) is
+        // non-decreasing in x, so it is that of the largest raw logit);
+        // groups whose largest b cannot reach thr are dropped, the rest
+        // are compacted within the wave
+        float x[kPer][4];
+        if (full) {
+#pragma unroll
+            for (int k = 0; k < kPer; ++k) load_x4<DT, VEC, true>(draft, tbase, (g0 + k * kWave + lane) * 4, tn, x[k]);
+        } else {
+#pragma unroll
+            for (int k = 0; k < kPer; ++k) load_x4<DT, VEC, false>(draft, tbase, (g0 + k * kWave + lane) * 4, tn, x[k]);
+        }
+        int qn = 0;
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const float gx = fmaxf(fmaxf(x[k][0], x[k][1]), fmaxf(x[k][2], x[k][3]));
+            const float bmax = gx * invT - cd;
+            const bool live = bmax >= bound && bmax > -INFINITY;
+            const uint64_t bal = __ballot(live);
+            if (live) {
+                // a bf16 logit is the top half of its binary32 value (-inf past tn included)
+                const uint32_t w0 = (__float_as_uint(x[k][0]) >> 16) | (__float_as_uint(x[k][1]) & 0xFFFF0000u);
+                const uint32_t w1 = (__float_as_uint(x[k][2]) >> 16) | (__float_as_uint(x[k][3]) & 0xFFFF0000u);
+                queue[qn + __popcll(bal & ((1ull << lane) - 1ull))] =
+                    make_uint4((uint32_t)(g0 + k * kWave + lane), w0, w1, __float_as_uint(bmax));
+            }
+            qn += __popcll(bal);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        C.add(2, (unsigned)qn, lane);
+
+        // 2. Philox for the survivors; a word below its group's floor is a
+        // certain miss; groups holding a word at or above it get their
+        // exact keys, and the m best keys >= thr are kept
+        for (int base = 0; base < qn; base += kWave) {
+            const int q = base + lane;
+            const bool valid = q < qn;
+            const uint4 ent = queue[valid ? q : 0];
+            const int gl = (int)ent.x;
+            const uint4 w = rng_block(key, (uint32_t)u, kStreamReplay, blk0 + (uint32_t)gl);
+            const uint32_t wf = gumbel_word_floor(thr, __uint_as_float(ent.w), slack);
+            const bool pass = valid && max(max(w.x, w.y), max(w.z, w.w)) >= wf;
+            const uint64_t pb = __ballot(pass);
+            C.add(3, (unsigned)__popcll(pb), lane);
+            if (pb == 0) continue;
+            float bv[4];
+            if constexpr (DT == TSB_BF16) {
+                // the group's logits come from the queue (no second read)
+                const float xq[4] = {__uint_as_float(ent.y << 16), __uint_as_float(ent.y & 0xFFFF0000u),
+                                     __uint_as_float(ent.z << 16), __uint_as_float(ent.z & 0xFFFF0000u)};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) bv[e] = (pass && gl * 4 + e < tn) ? xq[e] * invT - cd : -INFINITY;
+            } else {
+                load_b4<DT, VEC>(draft, tbase, gl * 4, pass ? tn : 0, invT, cd, bv);
+            }
+            const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+            float kv[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const bool in = bv[e] >= bound && bv[e] > -INFINITY;
+                kv[e] = in ? bv[e] + gumbel_f32(ws[e]) : -INFINITY;
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                top.offer(cand_key(kv[e], (uint32_t)(t0 + gl * 4 + e)), kv[e] >= thr && kv[e] > -INFINITY);
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");  // the queue is rewritten by the next pass
+    }
+    const size_t o = (size_t)node * (size_t)T + t;
+    const int cnt = __popcll(__ballot(lane < m && top.v != 0));
+    if (lane < cnt) A.out_cand[o * TSB_MAX_K + lane] = top.v;
+    if (lane == 0) A.out_cnt[o] = cnt;
+    C.add(0, 1, lane);
+    C.add(1, (unsigned)tn, lane);
+}
+
+template <int DT, bool VEC>
+__global__ __launch_bounds__(kBlock) void replay_scan(ScanArgs A, const int* __restrict__ ptotal,
                                                       unsigned long long* __restrict__ stats) {
     // surviving groups of the current pass, per wave: (group, its four bf16
     // logits as two words, largest b); binary32 rows keep (group, largest b)
     // and read the group again
     __shared__ uint4 s_queue[kScanWaves][kPassGroups];
     const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-    uint4* queue = s_queue[wave];
-    const long long items = (long long)ptotal[0] * T;
+    const long long items = (long long)ptotal[0] * A.T;
     const long long nw = (long long)gridDim.x * kScanWaves;
-    unsigned long long n_items = 0, n_tokens = 0, n_live = 0, n_keyed = 0;  // work counters (wave-uniform)
-    for (long long it = (long long)blockIdx.x * kScanWaves + wave; it < items; it += nw) {
-        const int pi = (int)(it / T);
-        const int t = (int)(it - (long long)pi * T);
-        const int node = plist[pi];
-        const float4 pr = rec[node];  // (c_d, thr, depth, m) of the parent
-        const int r = node / (B + 1);
-        const int u = node - r * (B + 1);
-        const int d = __float_as_int(pr.z);
-        const int m = __float_as_int(pr.w);
-        const size_t rowbase = ((size_t)r * D + d) * (size_t)V;
-        const float cd = pr.x;
-        const float thr = pr.y;
-        const float bound = thr - kGumbelMaxBound;
-        const int t0 = t * kReplayTile;
-        const int tn = min(kReplayTile, V - t0);
-        const size_t tbase = rowbase + t0;
-        const bool full = VEC && tn == kReplayTile;
-        const float slack = 0.25f + fabsf(thr) * 0x1p-20f;
-        RngKey key;
-        key.k0 = k0;
-        key.k1 = k1;
-        key.request = (uint32_t)r;
-        key.step = step;
-        const uint32_t blk0 = (uint32_t)(t0 >> 2);
-        WaveTopList top;
-        top.init(m);
-        constexpr int kPer = kPassGroups / kWave;  // groups per lane and pass
-#pragma unroll 1
-        for (int g0 = 0; g0 < kTileGroups; g0 += kPassGroups) {
-            // 1. largest b of each group of four (b = fl32(x invT - c_d) is
-            // non-decreasing in x, so it is that of the largest raw logit);
-            // groups whose largest b cannot reach thr are dropped, the rest
-            // are compacted within the wave
-            float x[kPer][4];
-            if (full) {
-#pragma unroll
-                for (int k = 0; k < kPer; ++k) load_x4<DT, VEC, true>(draft, tbase, (g0 + k * kWave + lane) * 4, tn, x[k]);
-            } else {
-#pragma unroll
-                for (int k = 0; k < kPer; ++k) load_x4<DT, VEC, false>(draft, tbase, (g0 + k * kWave + lane) * 4, tn, x[k]);
-            }
-            int qn = 0;
-#pragma unroll
-            for (int k = 0; k < kPer; ++k) {
-                const float gx = fmaxf(fmaxf(x[k][0], x[k][1]), fmaxf(x[k][2], x[k][3]));
-                const float bmax = gx * invT - cd;
-                const bool live = bmax >= bound && bmax > -INFINITY;
-                const uint64_t bal = __ballot(live);
-                if (live) {
-                    // a bf16 logit is the top half of its binary32 value (-inf past tn included)
-                    const uint32_t w0 = (__float_as_uint(x[k][0]) >> 16) | (__float_as_uint(x[k][1]) & 0xFFFF0000u);
-                    const uint32_t w1 = (__float_as_uint(x[k][2]) >> 16) | (__float_as_uint(x[k][3]) & 0xFFFF0000u);
-                    queue[qn + __popcll(bal & ((1ull << lane) - 1ull))] =
-                        make_uint4((uint32_t)(g0 + k * kWave + lane), w0, w1, __float_as_uint(bmax));
-                }
-                qn += __popcll(bal);
-            }
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-            n_live += (unsigned)qn;
+    __shared__ unsigned long long s_cnt[kScanWaves][4];
+    const ScanCounters C = scan_counters(s_cnt, wave, lane, stats);
+    for (long long it = (long long)blockIdx.x * kScanWaves + wave; it < items; it += nw)
+        scan_item<DT, VEC>(A, it, lane, s_queue[wave], C);
+    C.flush(stats, lane);
+}
 
-            // 2. Philox for the survivors; a word below its group's floor is a
-            // certain miss; groups holding a word at or above it get their
-            // exact keys, and the m best keys >= thr are kept
-            for (int base = 0; base < qn; base += kWave) {
-                const int q = base + lane;
-                const bool valid = q < qn;
-                const uint4 ent = queue[valid ? q : 0];
-                const int gl = (int)ent.x;
-                const uint4 w = rng_block(key, (uint32_t)u, kStreamReplay, blk0 + (uint32_t)gl);
-                const uint32_t wf = gumbel_word_floor(thr, __uint_as_float(ent.w), slack);
-                const bool pass = valid && max(max(w.x, w.y), max(w.z, w.w)) >= wf;
-                const uint64_t pb = __ballot(pass);
-                n_keyed += (unsigned)__popcll(pb);
-                if (pb == 0) continue;
-                float bv[4];
-                if constexpr (DT == TSB_BF16) {
-                    // the group's logits come from the queue (no second read)
-                    const float xq[4] = {__uint_as_float(ent.y << 16), __uint_as_float(ent.y & 0xFFFF0000u),
-                                         __uint_as_float(ent.z << 16), __uint_as_float(ent.z & 0xFFFF0000u)};
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) bv[e] = (pass && gl * 4 + e < tn) ? xq[e] * invT - cd : -INFINITY;
-                } else {
-                    load_b4<DT, VEC>(draft, tbase, gl * 4, pass ? tn : 0, invT, cd, bv);
-                }
-                const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
-                float kv[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const bool in = bv[e] >= bound && bv[e] > -INFINITY;
-                    kv[e] = in ? bv[e] + gumbel_f32(ws[e]) : -INFINITY;
-                }
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    top.offer(cand_key(kv[e], (uint32_t)(t0 + gl * 4 + e)), kv[e] >= thr && kv[e] > -INFINITY);
-            }
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");  // the queue is rewritten by the next pass
-        }
-        const size_t o = (size_t)node * (size_t)T + t;
-        const int cnt = __popcll(__ballot(lane < m && top.v != 0));
-        if (lane < cnt) out_cand[o * TSB_MAX_K + lane] = top.v;
-        if (lane == 0) out_cnt[o] = cnt;
-        n_items += 1;
-        n_tokens += (unsigned)tn;
+// The scan and the target stream of verification in one grid: the first nt
+// workgroups stream the target (the job's chunks dealt over them) and the
+// others scan (items dealt grid-stride over the scan's workgroups, as in
+// replay_scan). The target's workgroups come first, so they are dispatched
+// first and every compute unit mixes the target's HBM stream with the
+// scan's VALU work; the scan's workgroups beyond what fits start as others
+// finish.
+template <int DT, bool VEC, bool TVEC>
+__global__ __launch_bounds__(kBlock) void replay_scan_target(ScanArgs A, const int* __restrict__ ptotal,
+                                                             unsigned long long* __restrict__ stats, TargetJob job,
+                                                             int nt) {
+    if ((int)blockIdx.x < nt) {
+        // chunks blockIdx.x, blockIdx.x + nt, ... of the job
+        XRegion X;
+        X.slots = job.slots;
+        for (int g = blockIdx.x; g < job.ngroups; g += nt)
+            target_chunk<DT, TVEC>(g, job.ngroups, job.target, A.V, A.B, job.nrows, job.chunk, job.P, A.invT,
+                                   job.n_nodes, job.tm, job.ts, job.tf, X, job.R);
+        return;
     }
-    if (stats && lane == 0 && n_items) {
-        atomicAdd(&stats[kStReplayItems], n_items);
-        atomicAdd(&stats[kStReplayTokens], n_tokens);
-        atomicAdd(&stats[kStReplayLive], n_live);
-        atomicAdd(&stats[kStReplayKeyed], n_keyed);
-    }
+    __shared__ uint4 s_queue[kScanWaves][kPassGroups];
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    const long long items = (long long)ptotal[0] * A.T;
+    const int sb = (int)blockIdx.x - nt;
+    const long long nw = (long long)((int)gridDim.x - nt) * kScanWaves;
+    __shared__ unsigned long long s_cnt[kScanWaves][4];
+    const ScanCounters C = scan_counters(s_cnt, wave, lane, stats);
+    for (long long it = (long long)sb * kScanWaves + wave; it < items; it += nw)
+        scan_item<DT, VEC>(A, it, lane, s_queue[wave], C);
+    C.flush(stats, lane);
 }
 
 __global__ __launch_bounds__(kWave) void replay_merge(int B, int D, int K, int T, tsb_tree tree,
@@ -438,7 +514,8 @@ __global__ __launch_bounds__(kWave) void replay_merge(int B, int D, int K, int T
 }
 
 hipError_t launch_replay(const tsb_config& c, float invT, const void* draft, const int32_t* topk_tok,
-                         const tsb_tree& tree, uint32_t step, int32_t* node_tok, char* ws, hipStream_t st) {
+                         const tsb_tree& tree, uint32_t step, int32_t* node_tok, char* ws, hipStream_t st,
+                         const TargetJob* tj) {
     const Geometry g = geometry(c);
     const ReplayWs w = replay_ws(c);
     uint64_t* cand = (uint64_t*)(ws + w.cand);
@@ -448,8 +525,6 @@ hipError_t launch_replay(const tsb_config& c, float invT, const void* draft, con
     const uint32_t k0 = (uint32_t)c.seed, k1 = (uint32_t)(c.seed >> 32);
     const int prune = (c.flags & TSB_FLAG_NO_PRUNE) ? 0 : 1;
     const bool vec = c.V % 4 == 0 && ((uintptr_t)draft & 15) == 0;
-    hipError_t e = hook_before(TSB_KERNEL_REPLAY_SCAN, st);
-    if (e != hipSuccess) return e;
     float4* rec = (float4*)(ws + w.thr);
     // one workgroup per four nodes, and one more for the parent list
     const int nthr = (c.R * (c.B + 1) + kBlock / kWave - 1) / (kBlock / kWave) + 1;
@@ -459,29 +534,37 @@ hipError_t launch_replay(const tsb_config& c, float invT, const void* draft, con
     else
         replay_threshold<TSB_F32><<<nthr, kBlock, 0, st>>>(draft, c.R, c.V, c.D, c.B, c.K, invT, topk_tok, tree, k0,
                                                            k1, step, prune, rec, plist, ptotal);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int scan_id = tj ? TSB_KERNEL_SCAN_TARGET : TSB_KERNEL_REPLAY_SCAN;
+    if ((e = hook_before(scan_id, st)) != hipSuccess) return e;
     unsigned long long* const stats = stats_ptr();
-    // a persistent grid: the item count is only known on the device
-    const long long max_items = (long long)c.R * c.B * g.T;
-    const int grid = (int)std::max<long long>(1, std::min<long long>(kScanWorkgroups, (max_items + kScanWaves - 1) / kScanWaves));
-    if (c.dtype == TSB_BF16) {
-        if (vec)
-            replay_scan<TSB_BF16, true><<<grid, kBlock, 0, st>>>(draft, c.V, c.D, c.B, c.K, g.T, invT, topk_tok, tree,
-                                                                 plist, ptotal, rec, k0, k1, step, cand, cc, stats);
-        else
-            replay_scan<TSB_BF16, false><<<grid, kBlock, 0, st>>>(draft, c.V, c.D, c.B, c.K, g.T, invT, topk_tok,
-                                                                  tree, plist, ptotal, rec, k0, k1, step, cand, cc, stats);
+    ScanArgs A{draft, c.V, c.D, c.B, g.T, invT, plist, rec, k0, k1, step, cand, cc};
+    if (tj) {
+        const int nt = std::min(tj->ngroups, kFusedTargetWorkgroups);
+        const int grid = nt + kFusedScanWorkgroups;
+        const bool tv = tj->vec;
+        if (c.dtype == TSB_BF16) {
+            auto fn = vec ? (tv ? replay_scan_target<TSB_BF16, true, true> : replay_scan_target<TSB_BF16, true, false>)
+                          : (tv ? replay_scan_target<TSB_BF16, false, true> : replay_scan_target<TSB_BF16, false, false>);
+            fn<<<grid, kBlock, 0, st>>>(A, ptotal, stats, *tj, nt);
+        } else {
+            auto fn = vec ? (tv ? replay_scan_target<TSB_F32, true, true> : replay_scan_target<TSB_F32, true, false>)
+                          : (tv ? replay_scan_target<TSB_F32, false, true> : replay_scan_target<TSB_F32, false, false>);
+            fn<<<grid, kBlock, 0, st>>>(A, ptotal, stats, *tj, nt);
+        }
     } else {
-        if (vec)
-            replay_scan<TSB_F32, true><<<grid, kBlock, 0, st>>>(draft, c.V, c.D, c.B, c.K, g.T, invT, topk_tok, tree,
-                                                                plist, ptotal, rec, k0, k1, step, cand, cc, stats);
-        else
-            replay_scan<TSB_F32, false><<<grid, kBlock, 0, st>>>(draft, c.V, c.D, c.B, c.K, g.T, invT, topk_tok, tree,
-                                                                 plist, ptotal, rec, k0, k1, step, cand, cc, stats);
+        // a persistent grid: the item count is only known on the device
+        const long long max_items = (long long)c.R * c.B * g.T;
+        const int grid = (int)std::max<long long>(1, std::min<long long>(kScanWorkgroups,
+                                                                         (max_items + kScanWaves - 1) / kScanWaves));
+        auto fn = c.dtype == TSB_BF16 ? (vec ? replay_scan<TSB_BF16, true> : replay_scan<TSB_BF16, false>)
+                                      : (vec ? replay_scan<TSB_F32, true> : replay_scan<TSB_F32, false>);
+        fn<<<grid, kBlock, 0, st>>>(A, ptotal, stats);
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if ((e = hook_after(TSB_KERNEL_REPLAY_SCAN, st)) != hipSuccess) return e;
+    if ((e = hook_after(scan_id, st)) != hipSuccess) return e;
     if ((e = hook_before(TSB_KERNEL_REPLAY_MERGE, st)) != hipSuccess) return e;
     replay_merge<<<dim3(c.B + 1, c.R), kWave, 0, st>>>(c.B, c.D, c.K, g.T, tree, cand, cc, node_tok);
     e = hipGetLastError();

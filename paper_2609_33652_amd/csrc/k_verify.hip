@@ -27,150 +27,20 @@
 #include "tsb_device.hpp"
 #include "tsb_exchange.hpp"
 #include "tsb_kernels.hpp"
+#include "tsb_target.hpp"
 
 namespace tsb {
 
 // ------------------------------------------------------------------ K4
-// Streamed estimate of every target row's normaliser: per thread, four
-// 16-byte loads in flight, a running maximum of the raw logits and
-// sum 2^(x c - m c) with c = invT log2(e) (one FMA and one v_exp_f32 per
-// logit; partial sums of 8 terms in binary32, accumulated in binary64).
-// The estimate only has to be within ~1e-6 of ln sum exp(a): the walk uses it
-// to take acceptance tests that are clear of U by a wide band, and computes
-// the exact normaliser (binary64 terms) for every other node it tests.
-// A NaN or +inf logit surfaces as a non-finite maximum or sum.
-//
-// Loads are non-temporal: the rows stream through once, and keeping them out
-// of the caches' normal allocation was measured ~11% faster on this part.
-//
-// Layout: a persistent grid. The target is one flat array of R (B+1) V
-// logits cut into equal chunks, one per workgroup (all resident at once, so
-// no workgroup trails the others). A chunk covers pieces of one or two rows;
-// piece k of row t (its k-th workgroup) is partial slot k of the row, and
-// the row's first workgroup marks the slots no piece uses as empty. The grid
-// also zeroes the exchange slots of the walk launched after it.
-template <int DT, bool VEC>
-__device__ __forceinline__ void stream_piece(const void* __restrict__ target, size_t rowbase, int lo, int hi,
-                                             float c, float& m_out, double& sum_out) {
-    constexpr int kEl = 8;      // logits per 16-byte load (bf16); fp32 loads are 2 x 16 bytes
-    constexpr int kLoads = 4;   // loads in flight per thread
-    const int tid = threadIdx.x;
-    float m = -INFINITY;   // running max of the raw logits
-    double sum = 0.0;      // sum of 2^(x c - m c)
-    for (int base = lo; base < hi; base += kBlock * kEl * kLoads) {
-        float x[kLoads][kEl];
-#pragma unroll
-        for (int l = 0; l < kLoads; ++l) {
-            const int i0 = base + (l * kBlock + tid) * kEl;
-            if (VEC && i0 + kEl <= hi) {
-                if (DT == TSB_BF16) {
-                    const uint4 raw = load_stream16((const uint16_t*)target + rowbase + i0);
-                    const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        x[l][2 * j] = __uint_as_float(w[j] << 16);
-                        x[l][2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
-                    }
-                } else {
-                    const uint4 a = load_stream16((const float*)target + rowbase + i0);
-                    const uint4 b = load_stream16((const float*)target + rowbase + i0 + 4);
-                    x[l][0] = __uint_as_float(a.x); x[l][1] = __uint_as_float(a.y);
-                    x[l][2] = __uint_as_float(a.z); x[l][3] = __uint_as_float(a.w);
-                    x[l][4] = __uint_as_float(b.x); x[l][5] = __uint_as_float(b.y);
-                    x[l][6] = __uint_as_float(b.z); x[l][7] = __uint_as_float(b.w);
-                }
-            } else {
-#pragma unroll
-                for (int j = 0; j < kEl; ++j)
-                    x[l][j] = (i0 + j < hi) ? load_logit<DT>(target, rowbase + i0 + j) : -INFINITY;
-            }
-        }
-        float cm = m;
-#pragma unroll
-        for (int l = 0; l < kLoads; ++l)
-#pragma unroll
-            for (int j = 0; j < kEl; ++j) cm = fmaxf(cm, x[l][j]);
-        if (cm > m) {
-            if (m > -INFINITY) sum *= (double)exp2f((m - cm) * c);
-            m = cm;
-        }
-        if (m > -INFINITY) {
-            const float mc = m * c;
-#pragma unroll
-            for (int l = 0; l < kLoads; ++l) {
-                float cs = 0.f;
-#pragma unroll
-                for (int j = 0; j < kEl; ++j) cs += __builtin_amdgcn_exp2f(fmaf(x[l][j], c, -mc));
-                sum += (double)cs;
-            }
-        }
-    }
-    m_out = m;
-    sum_out = sum;
-}
-
+// The target stream on a grid of its own (tsb_verify and the other
+// verification entry points; a round runs it inside the replay scan's grid).
 template <int DT, bool VEC>
 __global__ __launch_bounds__(kBlock) void target_partials(const void* __restrict__ target, int V, int B, int nrows,
                                                           long long chunk, int P, float invT,
                                                           const int32_t* __restrict__ n_nodes,
                                                           float* __restrict__ tm, double* __restrict__ ts,
                                                           int* __restrict__ tf, XRegion X, int R) {
-    const int g = blockIdx.x;
-    const int tid = threadIdx.x;
-    // the walk that follows starts from cleared exchange slots
-    xclear(X, R, (size_t)g * kBlock + tid, (size_t)gridDim.x * kBlock);
-    const long long N = (long long)nrows * V;
-    const long long e0 = (long long)g * chunk;
-    if (e0 >= N) return;
-    const long long e1 = min(e0 + chunk, N);
-    const int t0 = (int)(e0 / V), t1 = (int)((e1 - 1) / V);
-    const float c = invT * 1.4426950408889634f;  // invT * log2(e)
-    __shared__ float s_m[kBlock / kWave];
-    __shared__ double s_s[kBlock / kWave];
-    const int wave = tid / kWave, lane = tid % kWave;
-    for (int t = t0; t <= t1; ++t) {
-        const int r = t / (B + 1);
-        const int node = t % (B + 1);
-        const long long rb = (long long)t * V;
-        const int gf = (int)(rb / chunk);            // the row's first workgroup
-        const int gl = (int)((rb + V - 1) / chunk);  // and its last
-        const size_t o = (size_t)t * P;
-        if (g == gf && tid == 0) {
-            for (int q = gl - gf + 1; q < P; ++q) {
-                tm[o + q] = -INFINITY;
-                ts[o + q] = 0.0;
-                tf[o + q] = 0;
-            }
-        }
-        if (node >= n_nodes[r]) continue;  // uniform over the workgroup
-        const int lo = (int)max(e0 - rb, 0LL);
-        const int hi = (int)min(e1 - rb, (long long)V);
-        float m;
-        double sum;
-        stream_piece<DT, VEC>(target, (size_t)rb, lo, hi, c, m, sum);
-        const float wm = wave_max(m);
-        const double contrib = (m == -INFINITY) ? 0.0 : sum * (double)exp2f((m - wm) * c);
-        const double wsum = wave_sum(contrib);
-        if (lane == 0) {
-            s_m[wave] = wm;
-            s_s[wave] = wsum;
-        }
-        __syncthreads();
-        if (tid == 0) {
-            float M = s_m[0];
-            for (int w = 1; w < kBlock / kWave; ++w) M = fmaxf(M, s_m[w]);
-            double tot = 0.0;
-            for (int w = 0; w < kBlock / kWave; ++w)
-                if (s_m[w] != -INFINITY) tot += s_s[w] * (double)exp2f((s_m[w] - M) * c);
-            const size_t q = o + (size_t)(g - gf);
-            // partial as (max of a, sum exp(a - max a)), a = x invT; non-finite input
-            // leaves a NaN or infinite max/sum
-            tm[q] = M * invT;
-            ts[q] = tot;
-            tf[q] = (isnan(M) || M == INFINITY || !isfinite(tot)) ? 1 : 0;
-        }
-        __syncthreads();
-    }
+    target_chunk<DT, VEC>(blockIdx.x, gridDim.x, target, V, B, nrows, chunk, P, invT, n_nodes, tm, ts, tf, X, R);
 }
 
 // ------------------------------------------------------------------ K5
@@ -1584,23 +1454,40 @@ static hipError_t walk_capacity(const void* fn, int kind, int dt, int vec, size_
     return hipSuccess;
 }
 
-static hipError_t launch_target_partials(const tsb_config& c, float invT, const void* target, const tsb_tree& tree,
-                                         char* ws, hipStream_t st) {
+TargetJob target_job(const tsb_config& c, const void* target, const tsb_tree& tree, char* ws) {
     const Geometry g = geometry(c);
     const VerifyWs w = verify_ws(c);
-    float* tm = (float*)(ws + w.tm);
-    double* ts = (double*)(ws + w.ts);
-    int* tf = (int*)(ws + w.tf);
+    TargetJob j;
+    j.target = target;
+    j.n_nodes = tree.n_nodes;
+    j.tm = (float*)(ws + w.tm);
+    j.ts = (double*)(ws + w.ts);
+    j.tf = (int*)(ws + w.tf);
+    j.slots = (uint64_t*)(ws + xchg_ws(c).slots);
+    j.chunk = g.chunk4;
+    j.nrows = c.R * (c.B + 1);
+    j.P = g.S4;
+    j.ngroups = g.G4;
+    j.R = c.R;
+    j.vec = (c.dtype == TSB_BF16) ? (c.V % 8 == 0 && ((uintptr_t)target & 15) == 0)
+                                  : (c.V % 4 == 0 && ((uintptr_t)target & 15) == 0);
+    return j;
+}
+
+static hipError_t launch_target_partials(const tsb_config& c, float invT, const void* target, const tsb_tree& tree,
+                                         const VerifyWs& w, char* ws, hipStream_t st) {
+    TargetJob j = target_job(c, target, tree, ws);
+    j.tm = (float*)(ws + w.tm);
+    j.ts = (double*)(ws + w.ts);
+    j.tf = (int*)(ws + w.tf);
     XRegion X;
-    X.slots = (uint64_t*)(ws + xchg_ws(c).slots);
-    const bool vec8 = (c.dtype == TSB_BF16) ? (c.V % 8 == 0 && ((uintptr_t)target & 15) == 0)
-                                            : (c.V % 4 == 0 && ((uintptr_t)target & 15) == 0);
-    const int nrows = c.R * (c.B + 1);
+    X.slots = j.slots;
     hipError_t e = hook_before(TSB_KERNEL_TARGET_PARTIALS, st);
     if (e != hipSuccess) return e;
-    auto fn = c.dtype == TSB_BF16 ? (vec8 ? target_partials<TSB_BF16, true> : target_partials<TSB_BF16, false>)
-                                  : (vec8 ? target_partials<TSB_F32, true> : target_partials<TSB_F32, false>);
-    fn<<<g.G4, kBlock, 0, st>>>(target, c.V, c.B, nrows, g.chunk4, g.S4, invT, tree.n_nodes, tm, ts, tf, X, c.R);
+    auto fn = c.dtype == TSB_BF16 ? (j.vec ? target_partials<TSB_BF16, true> : target_partials<TSB_BF16, false>)
+                                  : (j.vec ? target_partials<TSB_F32, true> : target_partials<TSB_F32, false>);
+    fn<<<j.ngroups, kBlock, 0, st>>>(target, c.V, c.B, j.nrows, j.chunk, j.P, invT, j.n_nodes, j.tm, j.ts, j.tf, X,
+                                     c.R);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     return hook_after(TSB_KERNEL_TARGET_PARTIALS, st);
@@ -1609,9 +1496,8 @@ static hipError_t launch_target_partials(const tsb_config& c, float invT, const 
 // Walk arguments shared by both walks.
 static WalkArgs walk_args(const tsb_config& c, float invT, const void* draft, const double* draft_lse,
                           const void* target, const tsb_tree& tree, const int32_t* node_tok, uint32_t step,
-                          const tsb_verdict& out, char* ws) {
+                          const tsb_verdict& out, const VerifyWs& w, char* ws) {
     const Geometry g = geometry(c);
-    const VerifyWs w = verify_ws(c);
     WalkArgs A;
     A.draft = draft;
     A.draft_lse = draft_lse;
@@ -1652,10 +1538,13 @@ static hipError_t launch_walk_grid(const void* fn, WalkArgs& A, int R, int G0, i
 
 hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, const double* draft_lse,
                          const void* target, const tsb_tree& tree, const int32_t* node_tok, uint32_t step,
-                         const tsb_verdict& out, char* ws, hipStream_t st) {
-    hipError_t e = launch_target_partials(c, invT, target, tree, ws, st);
-    if (e != hipSuccess) return e;
-    WalkArgs A = walk_args(c, invT, draft, draft_lse, target, tree, node_tok, step, out, ws);
+                         const tsb_verdict& out, char* ws, hipStream_t st, int stages) {
+    const VerifyWs w = verify_ws(c);
+    hipError_t e = hipSuccess;
+    if ((stages & kStageTarget) && (e = launch_target_partials(c, invT, target, tree, w, ws, st)) != hipSuccess)
+        return e;
+    if (!(stages & kStageWalk)) return hipSuccess;
+    WalkArgs A = walk_args(c, invT, draft, draft_lse, target, tree, node_tok, step, out, w, ws);
     const bool vec4 = c.V % 4 == 0 && ((uintptr_t)target & 15) == 0 && ((uintptr_t)draft & 15) == 0;
     const void* fn = nullptr;
     if (c.dtype == TSB_BF16)
@@ -1673,10 +1562,13 @@ hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, con
 
 hipError_t launch_verify_traversal(const tsb_config& c, float invT, const void* draft, const double* draft_lse,
                                    const void* target, const tsb_tree& tree, const int32_t* node_tok, uint32_t step,
-                                   const tsb_verdict& out, char* ws, hipStream_t st) {
-    hipError_t e = launch_target_partials(c, invT, target, tree, ws, st);
-    if (e != hipSuccess) return e;
-    WalkArgs A = walk_args(c, invT, draft, draft_lse, target, tree, node_tok, step, out, ws);
+                                   const tsb_verdict& out, char* ws, hipStream_t st, int stages) {
+    const VerifyWs w = verify_ws(c);
+    hipError_t e = hipSuccess;
+    if ((stages & kStageTarget) && (e = launch_target_partials(c, invT, target, tree, w, ws, st)) != hipSuccess)
+        return e;
+    if (!(stages & kStageWalk)) return hipSuccess;
+    WalkArgs A = walk_args(c, invT, draft, draft_lse, target, tree, node_tok, step, out, w, ws);
     const bool vec4 = c.V % 4 == 0 && ((uintptr_t)target & 15) == 0 && ((uintptr_t)draft & 15) == 0;
     const void* fn = nullptr;
     if (c.dtype == TSB_BF16)
@@ -1695,10 +1587,13 @@ hipError_t launch_verify_traversal(const tsb_config& c, float invT, const void* 
 hipError_t launch_pool_verify(const tsb_config& c, int P, float invT, const void* draft, const float* trans,
                               const int32_t* pool_tok, const void* target, const tsb_tree& tree,
                               const int32_t* node_tok, uint32_t step, const tsb_verdict& out, char* ws,
-                              hipStream_t st) {
-    hipError_t e = launch_target_partials(c, invT, target, tree, ws, st);
-    if (e != hipSuccess) return e;
-    WalkArgs A = walk_args(c, invT, draft, nullptr, target, tree, node_tok, step, out, ws);
+                              hipStream_t st, int stages) {
+    const VerifyWs w = pool_verify_ws(c);
+    hipError_t e = hipSuccess;
+    if ((stages & kStageTarget) && (e = launch_target_partials(c, invT, target, tree, w, ws, st)) != hipSuccess)
+        return e;
+    if (!(stages & kStageWalk)) return hipSuccess;
+    WalkArgs A = walk_args(c, invT, draft, nullptr, target, tree, node_tok, step, out, w, ws);
     A.pool_tok = pool_tok;
     A.trans = trans;
     A.P = P;

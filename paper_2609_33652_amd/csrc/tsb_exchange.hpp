@@ -12,10 +12,10 @@
 // slot can still hold (a workgroup publishes round e only after reading
 // round e - 1 from every workgroup, each of which had read round e - 2).
 //
-// Nothing persists between calls: the kernel enqueued right before a walk
-// clears the slots of every request of the call and the ticket counter
-// (xclear), and stream order
-// makes the zeros visible before the walk starts. Whatever the workspace
+// Nothing persists between calls: a kernel enqueued before each walk in the
+// same call (the target stream, or the naive walk's clearing kernel) clears
+// the slots of every request of the call and the ticket counter (xclear),
+// and stream order makes the zeros visible before the walk starts. Whatever the workspace
 // held before the call (another entry point's scratch, an abandoned wait of
 // an earlier call, uninitialised memory) can therefore never be taken for a
 // current word.

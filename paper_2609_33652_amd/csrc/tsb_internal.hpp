@@ -17,6 +17,7 @@ constexpr int kReplayTile = 4096;    // vocabulary tile of the replay scan
 constexpr int kWalkGroupsMax = 128;  // workgroups per request in verification
 constexpr int kWalkTokensPerGroup = 9728;  // tokens whose binary64 (p, q) one walk workgroup holds in LDS
 constexpr int kTargetWorkgroups = 2048;  // target stream: 8 resident workgroups on each of 256 CUs
+constexpr int kTargetMinChunk = 32768;   // shortest target chunk (logits), unless the whole target is shorter
 constexpr int kDraftWorkgroups = 512;    // row statistics: two 512-thread workgroups on each of 256 CUs
 constexpr int kDraftMinSeg = 16384;      // shortest draft segment (elements), unless the row is shorter
 
@@ -24,8 +25,8 @@ struct Geometry {
     int S1;          // workgroups per draft row (row statistics)
     int seg1;        // elements per draft segment (multiple of 8)
     int S4;          // partial slots per target row
-    int G4;          // workgroups of the target stream
-    long long chunk4;  // logits per target-stream workgroup (multiple of 8)
+    int G4;          // chunks of the target stream (one per workgroup of its own grid)
+    long long chunk4;  // logits per chunk (multiple of 8)
     int T;           // replay tiles per row
     int G;           // workgroups per request in verification (upper bound)
 };
@@ -43,7 +44,7 @@ inline Geometry geometry(const tsb_config& c) {
     // target stream: equal chunks of the flat [R (B+1) V] array, one per
     // resident workgroup; a row meets at most (V - 1) / chunk + 2 chunks
     const long long n4 = (long long)c.R * (c.B + 1) * c.V;
-    long long g4 = (n4 + 4095) / 4096;
+    long long g4 = (n4 + kTargetMinChunk - 1) / kTargetMinChunk;
     if (g4 > kTargetWorkgroups) g4 = kTargetWorkgroups;
     if (g4 < 1) g4 = 1;
     g.chunk4 = ((n4 + g4 - 1) / g4 + 7) / 8 * 8;
@@ -73,9 +74,9 @@ struct VerifyWs {  // target partials
 };
 
 // The exchange slots of the walks come first: [R][2][kWalkGroupsMax][8]
-// 64-bit words that the workgroups of a request poll (cleared by the kernel
-// enqueued right before each walk; nothing is kept between calls). Every
-// stage's scratch starts after them.
+// 64-bit words that the workgroups of a request poll (cleared by a kernel
+// enqueued before each walk in the same call; nothing is kept between
+// calls). Every stage's scratch starts after them.
 struct XchgWs {
     size_t slots, total;
 };
@@ -116,11 +117,11 @@ inline ReplayWs replay_ws(const tsb_config& c) {
     return w;
 }
 
-inline VerifyWs verify_ws(const tsb_config& c) {
+inline VerifyWs verify_ws_at(const tsb_config& c, size_t base) {
     const Geometry g = geometry(c);
     const size_t n = (size_t)c.R * (c.B + 1) * g.S4;
     VerifyWs w;
-    size_t o = xchg_ws(c).total;
+    size_t o = base;
     w.tm = o; o = align256(o + n * sizeof(float));
     w.ts = o; o = align256(o + n * sizeof(double));
     w.tf = o; o = align256(o + n * sizeof(int32_t));
@@ -128,14 +129,15 @@ inline VerifyWs verify_ws(const tsb_config& c) {
     return w;
 }
 
-inline size_t max3(size_t a, size_t b, size_t c) {
-    const size_t m = a > b ? a : b;
-    return m > c ? m : c;
-}
+// The target partials sit after the replay's region: a round streams the
+// target in the replay scan's grid (after the planner, whose region they may
+// reuse).
+inline VerifyWs verify_ws(const tsb_config& c) { return verify_ws_at(c, replay_ws(c).total); }
 
 // Whole workspace of the vocabulary-wide entry points.
 inline size_t ws_bytes(const tsb_config& c) {
-    return max3(plan_ws(c).total, replay_ws(c).total, verify_ws(c).total);
+    const size_t a = plan_ws(c).total, v = verify_ws(c).total;
+    return a > v ? a : v;
 }
 
 // Pools of P tokens per draft position: segment candidate lists of the pool
@@ -167,8 +169,12 @@ inline PoolWs pool_ws(const tsb_config& c, int P) {
     return w;
 }
 
+// The target partials of a pool round follow the pool replay (which keeps
+// nothing in the workspace) and may reuse the pool selection's region.
+inline VerifyWs pool_verify_ws(const tsb_config& c) { return verify_ws_at(c, xchg_ws(c).total); }
+
 inline size_t pool_ws_bytes(const tsb_config& c, int P) {
-    const size_t a = pool_ws(c, P).total, v = verify_ws(c).total;
+    const size_t a = pool_ws(c, P).total, v = pool_verify_ws(c).total;
     return a > v ? a : v;
 }
 

@@ -45,17 +45,43 @@ hipError_t launch_plan(const tsb_config& c, float invT, const void* draft, doubl
 int ep_generated_bound(const tsb_config& c, int frontier);
 constexpr int kEpFrontierLimit = 64;
 
+// The target stream of verification as a job: ngroups chunks of the flat
+// [R (B+1) V] target, each streamed by one workgroup (the target kernel's
+// own grid has one workgroup per chunk; the replay scan's grid deals them
+// over fewer). The partials do not depend on which workgroup takes a chunk.
+struct TargetJob {
+    const void* target;
+    const int32_t* n_nodes;  // rows at or beyond a request's node count are skipped
+    float* tm;               // per-row partials [R (B+1)][P]: max of a = x invT,
+    double* ts;              // sum exp(a - max),
+    int* tf;                 // non-finite flag
+    uint64_t* slots;         // exchange slots and ticket of the walk (cleared by the job)
+    long long chunk;
+    int nrows, P, ngroups, R;
+    bool vec;                // 16-byte loads (row length and base alignment allow them)
+};
+TargetJob target_job(const tsb_config& c, const void* target, const tsb_tree& tree, char* ws);
+
+// With a target job, the replay scan's grid carries it: ngroups more
+// workgroups stream the target while the others scan (one launch).
 hipError_t launch_replay(const tsb_config& c, float invT, const void* draft, const int32_t* topk_tok,
-                         const tsb_tree& tree, uint32_t step, int32_t* node_tok, char* ws, hipStream_t st);
+                         const tsb_tree& tree, uint32_t step, int32_t* node_tok, char* ws, hipStream_t st,
+                         const TargetJob* tj = nullptr);
+
+// Verification is two stages: the target stream (row normaliser partials of
+// the tree's rows) and the walk (which needs the replayed tokens and the
+// partials). A round runs the target stage in the replay scan's grid and
+// then the walk alone.
+enum : int { kStageTarget = 1, kStageWalk = 2, kStagesAll = 3 };
 
 hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, const double* draft_lse,
                          const void* target, const tsb_tree& tree, const int32_t* node_tok, uint32_t step,
-                         const tsb_verdict& out, char* ws, hipStream_t st);
+                         const tsb_verdict& out, char* ws, hipStream_t st, int stages = kStagesAll);
 
 // Traversal verification (sequence-level RRS over the tree) instead of WoR-RRS.
 hipError_t launch_verify_traversal(const tsb_config& c, float invT, const void* draft, const double* draft_lse,
                                    const void* target, const tsb_tree& tree, const int32_t* node_tok, uint32_t step,
-                                   const tsb_verdict& out, char* ws, hipStream_t st);
+                                   const tsb_verdict& out, char* ws, hipStream_t st, int stages = kStagesAll);
 
 // Sparse candidate pools of P tokens with context-dependent q_u.
 hipError_t launch_pool_partials(const tsb_config& c, int P, float invT, const void* draft, uint64_t* pk, int* pf,
@@ -69,7 +95,7 @@ hipError_t launch_pool_replay(const tsb_config& c, int P, float invT, const void
 hipError_t launch_pool_verify(const tsb_config& c, int P, float invT, const void* draft, const float* trans,
                               const int32_t* pool_tok, const void* target, const tsb_tree& tree,
                               const int32_t* node_tok, uint32_t step, const tsb_verdict& out, char* ws,
-                              hipStream_t st);
+                              hipStream_t st, int stages = kStagesAll);
 
 hipError_t launch_first_tokens(const tsb_config& c, const int32_t* topk_tok, const tsb_tree& tree, int32_t* node_tok,
                                hipStream_t st);

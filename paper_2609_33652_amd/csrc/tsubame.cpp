@@ -233,6 +233,31 @@ tsb_status tsb_verify(const tsb_config* cfg, const void* draft, const double* dr
     return e == hipSuccess ? TSB_OK : hip_fail(e, "tsb_verify");
 }
 
+namespace {
+
+// The stages of a vocabulary-wide round: planner, then the replay scan with
+// the target stream in its grid, then the walk.
+tsb_status step_round(const tsb_config* cfg, const void* draft, const void* target, uint32_t step,
+                      double* draft_lse, int32_t* topk_tok, float* topk_lp, const tsb_tree* tree,
+                      int32_t* node_tok, const tsb_verdict* out, char* ws, hipStream_t stream, bool traversal,
+                      const char* name) {
+    char where[64];
+    const float invT = inv_temperature(cfg->temperature);
+    hipError_t e = tsb::launch_plan(*cfg, invT, draft, draft_lse, topk_tok, topk_lp, *tree, out->req_status, ws, stream);
+    if (e != hipSuccess) return hip_fail(e, (snprintf(where, sizeof where, "%s/plan", name), where));
+    const tsb::TargetJob tj = tsb::target_job(*cfg, target, *tree, ws);
+    e = tsb::launch_replay(*cfg, invT, draft, topk_tok, *tree, step, node_tok, ws, stream, &tj);
+    if (e != hipSuccess) return hip_fail(e, (snprintf(where, sizeof where, "%s/replay+target", name), where));
+    e = traversal ? tsb::launch_verify_traversal(*cfg, invT, draft, draft_lse, target, *tree, node_tok, step, *out, ws,
+                                                 stream, tsb::kStageWalk)
+                  : tsb::launch_verify(*cfg, invT, draft, draft_lse, target, *tree, node_tok, step, *out, ws, stream,
+                                       tsb::kStageWalk);
+    if (e != hipSuccess) return hip_fail(e, (snprintf(where, sizeof where, "%s/walk", name), where));
+    return TSB_OK;
+}
+
+}  // namespace
+
 tsb_status tsb_step(const tsb_config* cfg, const void* draft, const void* target, uint32_t step, double* draft_lse,
                     int32_t* topk_tok, float* topk_lp, const tsb_tree* tree, int32_t* node_tok,
                     const tsb_verdict* out, void* workspace, size_t workspace_bytes, hipStream_t stream) {
@@ -243,15 +268,8 @@ tsb_status tsb_step(const tsb_config* cfg, const void* draft, const void* target
     TRY(check_tree(tree));
     TRY(check_verdict(out));
     TRY(check_ws(cfg, workspace, workspace_bytes));
-    const float invT = inv_temperature(cfg->temperature);
-    char* ws = (char*)workspace;
-    hipError_t e = tsb::launch_plan(*cfg, invT, draft, draft_lse, topk_tok, topk_lp, *tree, out->req_status, ws, stream);
-    if (e != hipSuccess) return hip_fail(e, "tsb_step/plan");
-    e = tsb::launch_replay(*cfg, invT, draft, topk_tok, *tree, step, node_tok, ws, stream);
-    if (e != hipSuccess) return hip_fail(e, "tsb_step/replay");
-    e = tsb::launch_verify(*cfg, invT, draft, draft_lse, target, *tree, node_tok, step, *out, ws, stream);
-    if (e != hipSuccess) return hip_fail(e, "tsb_step/verify");
-    return TSB_OK;
+    return step_round(cfg, draft, target, step, draft_lse, topk_tok, topk_lp, tree, node_tok, out, (char*)workspace,
+                      stream, false, "tsb_step");
 }
 
 tsb_status tsb_verify_traversal(const tsb_config* cfg, const void* draft, const double* draft_lse,
@@ -280,15 +298,8 @@ tsb_status tsb_step_traversal(const tsb_config* cfg, const void* draft, const vo
     TRY(check_tree(tree));
     TRY(check_verdict(out));
     TRY(check_ws(cfg, workspace, workspace_bytes));
-    const float invT = inv_temperature(cfg->temperature);
-    char* ws = (char*)workspace;
-    hipError_t e = tsb::launch_plan(*cfg, invT, draft, draft_lse, topk_tok, topk_lp, *tree, out->req_status, ws, stream);
-    if (e != hipSuccess) return hip_fail(e, "tsb_step_traversal/plan");
-    e = tsb::launch_replay(*cfg, invT, draft, topk_tok, *tree, step, node_tok, ws, stream);
-    if (e != hipSuccess) return hip_fail(e, "tsb_step_traversal/replay");
-    e = tsb::launch_verify_traversal(*cfg, invT, draft, draft_lse, target, *tree, node_tok, step, *out, ws, stream);
-    if (e != hipSuccess) return hip_fail(e, "tsb_step_traversal/verify");
-    return TSB_OK;
+    return step_round(cfg, draft, target, step, draft_lse, topk_tok, topk_lp, tree, node_tok, out, (char*)workspace,
+                      stream, true, "tsb_step_traversal");
 }
 
 tsb_status tsb_step_noalloc(const tsb_config* cfg, const void* draft, const void* target, uint32_t step,
@@ -307,8 +318,8 @@ tsb_status tsb_step_noalloc(const tsb_config* cfg, const void* draft, const void
     TRY(check_verdict(out));
     void* ws = nullptr;
     TRY(scratch_address(&ws));
-    return tsb_step(cfg, draft, target, step, draft_lse, topk_tok, topk_lp, tree, node_tok, out, ws,
-                    (size_t)TSB_NOALLOC_SCRATCH_BYTES, stream);
+    return step_round(cfg, draft, target, step, draft_lse, topk_tok, topk_lp, tree, node_tok, out, (char*)ws,
+                      stream, false, "tsb_step_noalloc");
 }
 
 tsb_status tsb_first_tokens(const tsb_config* cfg, const int32_t* topk_tok, const tsb_tree* tree, int32_t* node_tok,
