@@ -428,9 +428,39 @@ __global__ __launch_bounds__(kBlock) void replay_scan_target(ScanArgs A, const i
     C.flush(stats, lane);
 }
 
+// The walk's node record of u (a whole round: job.nrec set), from the same
+// loads and arithmetic as the walk would do; tok is child lane's token.
+template <int DT>
+__device__ void write_record(const TargetJob& job, const void* __restrict__ draft, int V, int D, float invT,
+                             const tsb_tree& tree, int r, int u, int n, size_t tb, int tok) {
+    const int lane = threadIdx.x;
+    const TreeNode t = tree_node(tree, tb, u, n, D);
+    uint32_t* rp = job.nrec + (tb + u) * kRecWords;
+    int bad;
+    const double L0 = target_row_lse(job.tm, job.ts, job.tf, job.P, tb + u, &bad);
+    const int m = t.ok ? t.m : 0;
+    if (lane == 0) {
+        const double Ld = m > 0 ? job.draft_lse[(size_t)r * D + t.d] : 0.0;
+        const uint64_t l0 = (uint64_t)__double_as_longlong(L0), ld = (uint64_t)__double_as_longlong(Ld);
+        *(uint4*)rp = make_uint4((uint32_t)m, (uint32_t)t.fc, (uint32_t)t.d,
+                                 (t.ok ? kRecOk : 0u) | (bad ? kRecTargetBad : 0u));
+        *(uint4*)(rp + 4) = make_uint4((uint32_t)l0, (uint32_t)(l0 >> 32), (uint32_t)ld, (uint32_t)(ld >> 32));
+    }
+    if (lane < m) {
+        const size_t trow = (tb + u) * (size_t)V;
+        const size_t drow = ((size_t)r * D + t.d) * (size_t)V;
+        const bool yok = tok >= 0 && tok < V;
+        const float xd = yok ? load_logit<DT>(draft, drow + tok) * invT : 0.f;
+        const float xt = yok ? load_logit<DT>(job.target, trow + tok) * invT : 0.f;
+        *(uint4*)(rp + 8 + 4 * lane) = make_uint4((uint32_t)tok, __float_as_uint(xd), __float_as_uint(xt), 0u);
+    }
+}
+
+template <int DT>
 __global__ __launch_bounds__(kWave) void replay_merge(int B, int D, int K, int T, tsb_tree tree,
                                                       const uint64_t* __restrict__ cand, const int* __restrict__ cc,
-                                                      int32_t* __restrict__ node_tok) {
+                                                      int32_t* __restrict__ node_tok, const void* __restrict__ draft,
+                                                      int V, float invT, TargetJob job) {
     const int r = blockIdx.y;
     const int u = blockIdx.x;
     const int lane = threadIdx.x;
@@ -441,9 +471,23 @@ __global__ __launch_bounds__(kWave) void replay_merge(int B, int D, int K, int T
         if (lane == 0) node_tok[tb + u] = -1;
     }
     TreeNode nd;
-    if (!replay_parent(tree, r, u, B, D, K, &nd)) return;
+    if (!replay_parent(tree, r, u, B, D, K, &nd)) {
+        if (job.nrec && u < n) {
+            // a leaf, or a node replay leaves alone: its children (if any) keep
+            // the tokens the caller's topology gave them
+            const TreeNode t = tree_node(tree, tb, u, n, D);
+            const int tok = (t.ok && lane < t.m) ? node_tok[tb + t.fc + lane] : -1;
+            write_record<DT>(job, draft, V, D, invT, tree, r, u, n, tb, tok);
+        }
+        return;
+    }
     const int m = nd.m;
     const int fc = nd.fc;
+    // the children's tokens (lane j < m: child j), then the node record
+    auto finish = [&](int tok) {
+        if (lane < m) node_tok[tb + fc + lane] = tok;
+        if (job.nrec) write_record<DT>(job, draft, V, D, invT, tree, r, u, n, tb, tok);
+    };
     const size_t o = (tb + u) * (size_t)T;
     if (T <= kWave) {
         // lane t holds tile t's count; the keys of all lists are gathered
@@ -468,7 +512,7 @@ __global__ __launch_bounds__(kWave) void replay_merge(int B, int D, int K, int T
             uint64_t v[1];
             v[0] = lane < nv ? cb[s_idx[lane]] : 0ull;
             wave_sort_desc<1>(v);
-            if (lane < m) node_tok[tb + fc + lane] = (int32_t)cand_id(v[0]);
+            finish((int32_t)cand_id(v[0]));
             return;
         }
         WaveTopList top;
@@ -496,7 +540,7 @@ __global__ __launch_bounds__(kWave) void replay_merge(int B, int D, int K, int T
                 }
             }
         }
-        if (lane < m) node_tok[tb + fc + lane] = (int32_t)cand_id(top.v);
+        finish((int32_t)cand_id(top.v));
         return;
     }
     WaveTopList top;
@@ -510,7 +554,7 @@ __global__ __launch_bounds__(kWave) void replay_merge(int B, int D, int K, int T
         if (i < ne && j < cc[o + tt]) k = cand[(o + tt) * TSB_MAX_K + j];
         top.offer(k, k != 0);
     }
-    if (lane < m) node_tok[tb + fc + lane] = (int32_t)cand_id(top.v);
+    finish((int32_t)cand_id(top.v));
 }
 
 hipError_t launch_replay(const tsb_config& c, float invT, const void* draft, const int32_t* topk_tok,
@@ -566,7 +610,14 @@ hipError_t launch_replay(const tsb_config& c, float invT, const void* draft, con
     if (e != hipSuccess) return e;
     if ((e = hook_after(scan_id, st)) != hipSuccess) return e;
     if ((e = hook_before(TSB_KERNEL_REPLAY_MERGE, st)) != hipSuccess) return e;
-    replay_merge<<<dim3(c.B + 1, c.R), kWave, 0, st>>>(c.B, c.D, c.K, g.T, tree, cand, cc, node_tok);
+    TargetJob none{};
+    const TargetJob& rj = tj ? *tj : none;  // node records only in a whole round
+    if (c.dtype == TSB_BF16)
+        replay_merge<TSB_BF16><<<dim3(c.B + 1, c.R), kWave, 0, st>>>(c.B, c.D, c.K, g.T, tree, cand, cc, node_tok,
+                                                                     draft, c.V, invT, rj);
+    else
+        replay_merge<TSB_F32><<<dim3(c.B + 1, c.R), kWave, 0, st>>>(c.B, c.D, c.K, g.T, tree, cand, cc, node_tok,
+                                                                    draft, c.V, invT, rj);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     return hook_after(TSB_KERNEL_REPLAY_MERGE, st);

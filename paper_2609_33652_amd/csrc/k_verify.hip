@@ -64,22 +64,27 @@ struct WalkArgs {
     const int32_t* pool_tok;
     const float* trans;
     int P;
+    // node records (kRecWords per node) when the round's merge wrote them, else null
+    const uint32_t* nrec;
 };
 
 // binary64 log-sum-exp of target row (r, node) from its segment partials
 __device__ double target_lse(const WalkArgs& A, int r, int node, int* bad) {
-    const size_t o = ((size_t)r * (A.B + 1) + node) * A.S4;
-    float M = -INFINITY;
-    int b = 0;
-    for (int s = 0; s < A.S4; ++s) {
-        M = fmaxf(M, A.tm[o + s]);
-        b |= A.tf[o + s];
-    }
-    double tot = 0.0;
-    for (int s = 0; s < A.S4; ++s)
-        if (A.tm[o + s] != -INFINITY) tot += A.ts[o + s] * exp((double)A.tm[o + s] - (double)M);
-    *bad = b || M == -INFINITY;
-    return (double)M + log(tot);
+    return target_row_lse(A.tm, A.ts, A.tf, A.S4, (size_t)r * (A.B + 1) + node, bad);
+}
+
+__device__ __forceinline__ double rec_f64(uint32_t lo, uint32_t hi) {
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// The same from the node record when the round's merge wrote them.
+__device__ double node_lse(const WalkArgs& A, int r, int node, int* bad) {
+    if (!A.nrec) return target_lse(A, r, node, bad);
+    const uint32_t* rp = A.nrec + ((size_t)r * (A.B + 1) + node) * kRecWords;
+    const uint4 h0 = *(const uint4*)rp;
+    const uint4 h1 = *(const uint4*)(rp + 4);
+    *bad = (h0.w & kRecTargetBad) != 0;
+    return rec_f64(h1.x, h1.y);
 }
 
 struct SplitF {  // binary64 value as binary32 hi + lo
@@ -522,7 +527,7 @@ __device__ void walk_tail(const WalkArgs& A, int r, int g, int G, int n, bool dr
     if (!draft_bad) {
         for (int i = g * kWalkThreads + tid; i < n; i += G * kWalkThreads) {
             int b;
-            const double l = target_lse(A, r, i, &b);
+            const double l = node_lse(A, r, i, &b);
             if (b) atomicOr(&s_bad, 1);
             if (A.out.target_lse) A.out.target_lse[tb + i] = b ? (double)NAN : l;
         }
@@ -537,7 +542,7 @@ __device__ void walk_tail(const WalkArgs& A, int r, int g, int G, int n, bool dr
         if (!draft_bad)
             for (int i = tid; i < n; i += kWalkThreads) {
                 int b;
-                target_lse(A, r, i, &b);
+                node_lse(A, r, i, &b);
                 if (b) atomicOr(&s_bad, 1);
             }
         __syncthreads();
@@ -622,7 +627,27 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
         while (true) {
             ++n_entered;
             // every workgroup reads the same entries, so all take the same exit
-            const TreeNode nd = tree_node(A.tree, tb, u, n, A.D);
+            TreeNode nd;
+            double L0, Ld = 0.0;
+            uint4 crec = make_uint4(0u, 0u, 0u, 0u);  // child tid's (token, x_d, x_t) from the record
+            if (A.nrec) {
+                // the node's record: its topology, normalisers and children in
+                // one round trip
+                const uint32_t* rp = A.nrec + (tb + u) * kRecWords;
+                const uint4 h0 = *(const uint4*)rp;
+                const uint4 h1 = *(const uint4*)(rp + 4);
+                if (tid < TSB_MAX_K) crec = *(const uint4*)(rp + 8 + 4 * tid);
+                nd.m = (int)h0.x;
+                nd.fc = (int)h0.y;
+                nd.d = (int)h0.z;
+                nd.ok = (h0.w & kRecOk) != 0;
+                L0 = rec_f64(h1.x, h1.y);
+                Ld = rec_f64(h1.z, h1.w);
+            } else {
+                nd = tree_node(A.tree, tb, u, n, A.D);
+                int tbad;
+                L0 = target_lse(A, r, u, &tbad);
+            }
             if (!nd.ok || (nd.m > 0 && nacc >= A.D)) {
                 add_status |= TSB_REQ_BAD_TREE;
                 invalid = true;
@@ -631,8 +656,6 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
             const int m = nd.m, d = nd.d;
             const size_t trow = ((size_t)r * B1 + u) * (size_t)A.V;
             const size_t drow = ((size_t)r * A.D + (m > 0 ? d : 0)) * (size_t)A.V;
-            int tbad;
-            const double L0 = target_lse(A, r, u, &tbad);
             if (m == 0) {  // accepted leaf: bonus from p_u
                 float bk;
                 int bi;
@@ -641,18 +664,26 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
                 bonus_out = X.best(bk, bi, 0.0, &unused);
                 break;
             }
-            const double Ld = A.draft_lse[(size_t)r * A.D + d];
+            if (!A.nrec) Ld = A.draft_lse[(size_t)r * A.D + d];
             // children of u: tokens, their logits and the uniforms, fetched
             // together; a token outside [0, V) is never used as an address
             const int fc = nd.fc;
             if (tid < m) {
-                const int y = A.node_tok[tb + fc + tid];
-                const bool yok = y >= 0 && y < A.V;
-                s_tok[tid] = y;
-                s_xd[tid] = yok ? load_logit<DT>(A.draft, drow + y) * A.invT : 0.f;
-                s_xt[tid] = yok ? load_logit<DT>(A.target, trow + y) * A.invT : 0.f;
+                if (A.nrec) {
+                    const int y = (int)crec.x;
+                    s_tok[tid] = y;
+                    s_xd[tid] = __uint_as_float(crec.y);
+                    s_xt[tid] = __uint_as_float(crec.z);
+                    if (!(y >= 0 && y < A.V)) s_badtok = 1;
+                } else {
+                    const int y = A.node_tok[tb + fc + tid];
+                    const bool yok = y >= 0 && y < A.V;
+                    s_tok[tid] = y;
+                    s_xd[tid] = yok ? load_logit<DT>(A.draft, drow + y) * A.invT : 0.f;
+                    s_xt[tid] = yok ? load_logit<DT>(A.target, trow + y) * A.invT : 0.f;
+                    if (!yok) s_badtok = 1;
+                }
                 s_u[tid] = u24d(rng_word(key, (uint32_t)(fc + tid), kStreamAccept, 0u));
-                if (!yok) s_badtok = 1;
             }
             __syncthreads();
             if (s_badtok) {
@@ -1454,7 +1485,8 @@ static hipError_t walk_capacity(const void* fn, int kind, int dt, int vec, size_
     return hipSuccess;
 }
 
-TargetJob target_job(const tsb_config& c, const void* target, const tsb_tree& tree, char* ws) {
+TargetJob target_job(const tsb_config& c, const void* target, const tsb_tree& tree, const double* draft_lse,
+                     char* ws) {
     const Geometry g = geometry(c);
     const VerifyWs w = verify_ws(c);
     TargetJob j;
@@ -1471,12 +1503,14 @@ TargetJob target_job(const tsb_config& c, const void* target, const tsb_tree& tr
     j.R = c.R;
     j.vec = (c.dtype == TSB_BF16) ? (c.V % 8 == 0 && ((uintptr_t)target & 15) == 0)
                                   : (c.V % 4 == 0 && ((uintptr_t)target & 15) == 0);
+    j.nrec = draft_lse ? (uint32_t*)(ws + w.nrec) : nullptr;
+    j.draft_lse = draft_lse;
     return j;
 }
 
 static hipError_t launch_target_partials(const tsb_config& c, float invT, const void* target, const tsb_tree& tree,
                                          const VerifyWs& w, char* ws, hipStream_t st) {
-    TargetJob j = target_job(c, target, tree, ws);
+    TargetJob j = target_job(c, target, tree, nullptr, ws);
     j.tm = (float*)(ws + w.tm);
     j.ts = (double*)(ws + w.ts);
     j.tf = (int*)(ws + w.tf);
@@ -1523,6 +1557,7 @@ static WalkArgs walk_args(const tsb_config& c, float invT, const void* draft, co
     A.pool_tok = nullptr;
     A.trans = nullptr;
     A.P = 0;
+    A.nrec = nullptr;
     return A;
 }
 
@@ -1545,6 +1580,7 @@ hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, con
         return e;
     if (!(stages & kStageWalk)) return hipSuccess;
     WalkArgs A = walk_args(c, invT, draft, draft_lse, target, tree, node_tok, step, out, w, ws);
+    if (stages & kWalkRecords) A.nrec = (const uint32_t*)(ws + w.nrec);
     const bool vec4 = c.V % 4 == 0 && ((uintptr_t)target & 15) == 0 && ((uintptr_t)draft & 15) == 0;
     const void* fn = nullptr;
     if (c.dtype == TSB_BF16)

@@ -69,8 +69,11 @@ struct PlanWs {  // row statistics partials
 struct ReplayWs {  // per (parent, tile) best keys, flat parent list, per-parent records
     size_t cand, cnt, plist, ptotal, thr, total;
 };
-struct VerifyWs {  // target partials
-    size_t tm, ts, tf, total;
+// 32-bit words of the walk's node record: eight of header, four per child.
+constexpr int kRecWords = 8 + 4 * TSB_MAX_K;
+
+struct VerifyWs {  // target partials, node records of the walk
+    size_t tm, ts, tf, nrec, total;
 };
 
 // The exchange slots of the walks come first: [R][2][kWalkGroupsMax][8]
@@ -125,6 +128,7 @@ inline VerifyWs verify_ws_at(const tsb_config& c, size_t base) {
     w.tm = o; o = align256(o + n * sizeof(float));
     w.ts = o; o = align256(o + n * sizeof(double));
     w.tf = o; o = align256(o + n * sizeof(int32_t));
+    w.nrec = o; o = align256(o + (size_t)c.R * (c.B + 1) * kRecWords * sizeof(uint32_t));
     w.total = o;
     return w;
 }

@@ -59,8 +59,13 @@ struct TargetJob {
     long long chunk;
     int nrows, P, ngroups, R;
     bool vec;                // 16-byte loads (row length and base alignment allow them)
+    // the walk's node records, written by the replay merge after the job
+    // (null: none), and the draft normalisers they copy
+    uint32_t* nrec;
+    const double* draft_lse;
 };
-TargetJob target_job(const tsb_config& c, const void* target, const tsb_tree& tree, char* ws);
+TargetJob target_job(const tsb_config& c, const void* target, const tsb_tree& tree, const double* draft_lse,
+                     char* ws);
 
 // With a target job, the replay scan's grid carries it: ngroups more
 // workgroups stream the target while the others scan (one launch).
@@ -70,9 +75,10 @@ hipError_t launch_replay(const tsb_config& c, float invT, const void* draft, con
 
 // Verification is two stages: the target stream (row normaliser partials of
 // the tree's rows) and the walk (which needs the replayed tokens and the
-// partials). A round runs the target stage in the replay scan's grid and
-// then the walk alone.
-enum : int { kStageTarget = 1, kStageWalk = 2, kStagesAll = 3 };
+// partials). A round runs the target stage in the replay scan's grid, its
+// merge writes the node records, and then the walk runs alone, reading them
+// (kWalkRecords).
+enum : int { kStageTarget = 1, kStageWalk = 2, kStagesAll = 3, kWalkRecords = 4 };
 
 hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, const double* draft_lse,
                          const void* target, const tsb_tree& tree, const int32_t* node_tok, uint32_t step,

@@ -37,8 +37,42 @@ __device__ __forceinline__ void stream_piece(const void* __restrict__ target, si
     const int tid = threadIdx.x;
     float m = -INFINITY;   // running max of the raw logits
     double sum = 0.0;      // sum of 2^(x c - m c)
-    for (int base = lo; base < hi; base += kBlock * kEl * kLoads) {
+    constexpr int kStep = kBlock * kEl * kLoads;
+    for (int base = lo; base < hi; base += kStep) {
         float x[kLoads][kEl];
+        if (VEC && base + kStep <= hi) {
+            // the whole step in range (uniform over the workgroup): every load
+            // is issued before the first is used
+            constexpr int kW = DT == TSB_BF16 ? 1 : 2;  // 16-byte loads per eight logits
+            uint4 raw[kLoads][kW];
+#pragma unroll
+            for (int l = 0; l < kLoads; ++l) {
+                const int i0 = base + (l * kBlock + tid) * kEl;
+                if (DT == TSB_BF16) {
+                    raw[l][0] = load_stream16((const uint16_t*)target + rowbase + i0);
+                } else {
+                    raw[l][0] = load_stream16((const float*)target + rowbase + i0);
+                    raw[l][kW - 1] = load_stream16((const float*)target + rowbase + i0 + 4);
+                }
+            }
+#pragma unroll
+            for (int l = 0; l < kLoads; ++l) {
+                if (DT == TSB_BF16) {
+                    const uint32_t w[4] = {raw[l][0].x, raw[l][0].y, raw[l][0].z, raw[l][0].w};
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        x[l][2 * j] = __uint_as_float(w[j] << 16);
+                        x[l][2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
+                    }
+                } else {
+                    const uint4 a = raw[l][0], b = raw[l][kW - 1];
+                    x[l][0] = __uint_as_float(a.x); x[l][1] = __uint_as_float(a.y);
+                    x[l][2] = __uint_as_float(a.z); x[l][3] = __uint_as_float(a.w);
+                    x[l][4] = __uint_as_float(b.x); x[l][5] = __uint_as_float(b.y);
+                    x[l][6] = __uint_as_float(b.z); x[l][7] = __uint_as_float(b.w);
+                }
+            }
+        } else {
 #pragma unroll
         for (int l = 0; l < kLoads; ++l) {
             const int i0 = base + (l * kBlock + tid) * kEl;
@@ -64,6 +98,7 @@ __device__ __forceinline__ void stream_piece(const void* __restrict__ target, si
                 for (int j = 0; j < kEl; ++j)
                     x[l][j] = (i0 + j < hi) ? load_logit<DT>(target, rowbase + i0 + j) : -INFINITY;
             }
+        }
         }
         float cm = m;
 #pragma unroll
@@ -152,5 +187,35 @@ __device__ __forceinline__ void target_chunk(int g, int ngroups, const void* __r
         __syncthreads();
     }
 }
+
+// binary64 log-sum-exp of one target row from its P partial slots (fixed
+// order), and whether the row held a non-finite logit (or none finite).
+__device__ __forceinline__ double target_row_lse(const float* __restrict__ tm, const double* __restrict__ ts,
+                                                 const int* __restrict__ tf, int P, size_t row, int* bad) {
+    const size_t o = row * (size_t)P;
+    float M = -INFINITY;
+    int b = 0;
+    for (int s = 0; s < P; ++s) {
+        M = fmaxf(M, tm[o + s]);
+        b |= tf[o + s];
+    }
+    double tot = 0.0;
+    for (int s = 0; s < P; ++s)
+        if (tm[o + s] != -INFINITY) tot += ts[o + s] * exp((double)tm[o + s] - (double)M);
+    *bad = b || M == -INFINITY;
+    return (double)M + log(tot);
+}
+
+// Node records for the walk, written by the replay merge of a whole round
+// once the target partials exist: everything the walk reads when it enters
+// node u, in one record of kRecWords 32-bit words, so that entering a node
+// costs one memory round trip. Words: 0 m (children; 0 for a leaf), 1 first
+// child, 2 depth, 3 flags (kRecOk: the node passed the topology checks;
+// kRecTargetBad: its target row is not finite), 4-5 the row's streamed
+// normaliser L0 (binary64), 6-7 the draft normaliser of the children's row,
+// then per child j (up to TSB_MAX_K) four words at 8 + 4 j: token, draft
+// logit x invT and target logit x invT (binary32 bits; 0 for a token
+// outside [0, V)), unused.
+constexpr uint32_t kRecOk = 1u, kRecTargetBad = 2u;
 
 }  // namespace tsb

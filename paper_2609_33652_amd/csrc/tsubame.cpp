@@ -245,13 +245,13 @@ tsb_status step_round(const tsb_config* cfg, const void* draft, const void* targ
     const float invT = inv_temperature(cfg->temperature);
     hipError_t e = tsb::launch_plan(*cfg, invT, draft, draft_lse, topk_tok, topk_lp, *tree, out->req_status, ws, stream);
     if (e != hipSuccess) return hip_fail(e, (snprintf(where, sizeof where, "%s/plan", name), where));
-    const tsb::TargetJob tj = tsb::target_job(*cfg, target, *tree, ws);
+    const tsb::TargetJob tj = tsb::target_job(*cfg, target, *tree, traversal ? nullptr : draft_lse, ws);
     e = tsb::launch_replay(*cfg, invT, draft, topk_tok, *tree, step, node_tok, ws, stream, &tj);
     if (e != hipSuccess) return hip_fail(e, (snprintf(where, sizeof where, "%s/replay+target", name), where));
     e = traversal ? tsb::launch_verify_traversal(*cfg, invT, draft, draft_lse, target, *tree, node_tok, step, *out, ws,
                                                  stream, tsb::kStageWalk)
                   : tsb::launch_verify(*cfg, invT, draft, draft_lse, target, *tree, node_tok, step, *out, ws, stream,
-                                       tsb::kStageWalk);
+                                       tsb::kStageWalk | tsb::kWalkRecords);
     if (e != hipSuccess) return hip_fail(e, (snprintf(where, sizeof where, "%s/walk", name), where));
     return TSB_OK;
 }
