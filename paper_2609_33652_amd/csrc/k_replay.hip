@@ -429,21 +429,34 @@ __global__ __launch_bounds__(kBlock) void replay_scan_target(ScanArgs A, const i
 }
 
 // The walk's node record of u (a whole round: job.nrec set), from the same
-// loads and arithmetic as the walk would do; tok is child lane's token.
-template <int DT>
-__device__ void write_record(const TargetJob& job, const void* __restrict__ draft, int V, int D, float invT,
-                             const tsb_tree& tree, int r, int u, int n, size_t tb, int tok) {
-    const int lane = threadIdx.x;
-    const TreeNode t = tree_node(tree, tb, u, n, D);
-    uint32_t* rp = job.nrec + (tb + u) * kRecWords;
+// loads and arithmetic as the walk would do. The parts that do not depend
+// on the children's tokens are read first (NodeHead), so their loads overlap
+// the merge; tok is child lane's token.
+struct NodeHead {
+    TreeNode t;
+    double L0, Ld;
     int bad;
-    const double L0 = target_row_lse(job.tm, job.ts, job.tf, job.P, tb + u, &bad);
+};
+__device__ __forceinline__ NodeHead node_head(const TargetJob& job, const tsb_tree& tree, int r, int u, int n,
+                                              size_t tb, int D) {
+    NodeHead h;
+    h.t = tree_node(tree, tb, u, n, D);
+    h.L0 = target_row_lse(job.tm, job.ts, job.tf, job.P, tb + u, &h.bad);
+    h.Ld = (h.t.ok && h.t.m > 0) ? job.draft_lse[(size_t)r * D + h.t.d] : 0.0;
+    return h;
+}
+
+template <int DT>
+__device__ void write_record(const TargetJob& job, const NodeHead& h, const void* __restrict__ draft, int V, int D,
+                             float invT, int r, int u, size_t tb, int tok) {
+    const int lane = threadIdx.x;
+    const TreeNode& t = h.t;
+    uint32_t* rp = job.nrec + (tb + u) * kRecWords;
     const int m = t.ok ? t.m : 0;
     if (lane == 0) {
-        const double Ld = m > 0 ? job.draft_lse[(size_t)r * D + t.d] : 0.0;
-        const uint64_t l0 = (uint64_t)__double_as_longlong(L0), ld = (uint64_t)__double_as_longlong(Ld);
+        const uint64_t l0 = (uint64_t)__double_as_longlong(h.L0), ld = (uint64_t)__double_as_longlong(h.Ld);
         *(uint4*)rp = make_uint4((uint32_t)m, (uint32_t)t.fc, (uint32_t)t.d,
-                                 (t.ok ? kRecOk : 0u) | (bad ? kRecTargetBad : 0u));
+                                 (t.ok ? kRecOk : 0u) | (h.bad ? kRecTargetBad : 0u));
         *(uint4*)(rp + 4) = make_uint4((uint32_t)l0, (uint32_t)(l0 >> 32), (uint32_t)ld, (uint32_t)(ld >> 32));
     }
     if (lane < m) {
@@ -470,14 +483,16 @@ __global__ __launch_bounds__(kWave) void replay_merge(int B, int D, int K, int T
     if (u == 0 || u >= n) {
         if (lane == 0) node_tok[tb + u] = -1;
     }
+    NodeHead head;
+    if (job.nrec && u < n) head = node_head(job, tree, r, u, n, tb, D);
     TreeNode nd;
     if (!replay_parent(tree, r, u, B, D, K, &nd)) {
         if (job.nrec && u < n) {
             // a leaf, or a node replay leaves alone: its children (if any) keep
             // the tokens the caller's topology gave them
-            const TreeNode t = tree_node(tree, tb, u, n, D);
+            const TreeNode& t = head.t;
             const int tok = (t.ok && lane < t.m) ? node_tok[tb + t.fc + lane] : -1;
-            write_record<DT>(job, draft, V, D, invT, tree, r, u, n, tb, tok);
+            write_record<DT>(job, head, draft, V, D, invT, r, u, tb, tok);
         }
         return;
     }
@@ -486,7 +501,7 @@ __global__ __launch_bounds__(kWave) void replay_merge(int B, int D, int K, int T
     // the children's tokens (lane j < m: child j), then the node record
     auto finish = [&](int tok) {
         if (lane < m) node_tok[tb + fc + lane] = tok;
-        if (job.nrec) write_record<DT>(job, draft, V, D, invT, tree, r, u, n, tb, tok);
+        if (job.nrec) write_record<DT>(job, head, draft, V, D, invT, r, u, tb, tok);
     };
     const size_t o = (tb + u) * (size_t)T;
     if (T <= kWave) {
