@@ -74,15 +74,29 @@ __device__ void prep_list(int R, int B, int D, int K, const tsb_tree& tree, int*
     const int total_nodes = R * (B + 1);
     int out = 0;
     for (int c0 = 0; c0 < total_nodes; c0 += kBlock * kPer) {
+        // every entry of the thread's nodes is loaded before any is tested
+        // (replay_parent's conditions, without its dependent loads)
+        int nn[kPer], nm[kPer], nfc[kPer], nd[kPer];
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) {
+            const int i = c0 + tid * kPer + k;
+            const bool in = i < total_nodes;
+            const int r = in ? i / (B + 1) : 0;
+            const size_t e = in ? (size_t)i : 0;
+            nn[k] = in ? tree.n_nodes[r] : 0;
+            nm[k] = tree.n_children[e];
+            nfc[k] = tree.first_child[e];
+            nd[k] = tree.depth[e];
+        }
         int flags = 0;  // bit k: node c0 + tid * kPer + k has children
 #pragma unroll
         for (int k = 0; k < kPer; ++k) {
             const int i = c0 + tid * kPer + k;
-            if (i < total_nodes) {
-                const int r = i / (B + 1), u = i - r * (B + 1);
-                TreeNode nd;
-                if (replay_parent(tree, r, u, B, D, K, &nd)) flags |= 1 << k;
-            }
+            const int u = i % (B + 1);
+            const int n = tree_count_ok(nn[k], B) ? nn[k] : 0;
+            const int m = nm[k], fc = nfc[k], d = nd[k];
+            const bool ok = m == 0 || (m > 0 && m <= TSB_MAX_K && fc > u && fc <= n - m && d >= 0 && d < D);
+            if (i < total_nodes && u < n && ok && m > 0 && m <= K) flags |= 1 << k;
         }
         int wt;
         const int off = wave_excl_scan<4>(__popc(flags), wt);
@@ -307,12 +321,32 @@ __device__ __forceinline__ void scan_item(const ScanArgs& A, long long it, int l
         // groups whose largest b cannot reach thr are dropped, the rest
         // are compacted within the wave
         float x[kPer][4];
+        uint32_t xw[kPer][2];  // bf16: the group's logits as two words
         if (full) {
 #pragma unroll
-            for (int k = 0; k < kPer; ++k) load_x4<DT, VEC, true>(draft, tbase, (g0 + k * kWave + lane) * 4, tn, x[k]);
+            for (int k = 0; k < kPer; ++k) {
+                const int e0 = (g0 + k * kWave + lane) * 4;
+                if (DT == TSB_BF16) {
+                    // the loaded words are kept for the queue
+                    const uint2 raw = *(const uint2*)((const uint16_t*)draft + tbase + e0);
+                    xw[k][0] = raw.x;
+                    xw[k][1] = raw.y;
+                    x[k][0] = __uint_as_float(raw.x << 16);
+                    x[k][1] = __uint_as_float(raw.x & 0xFFFF0000u);
+                    x[k][2] = __uint_as_float(raw.y << 16);
+                    x[k][3] = __uint_as_float(raw.y & 0xFFFF0000u);
+                } else {
+                    load_x4<DT, VEC, true>(draft, tbase, e0, tn, x[k]);
+                }
+            }
         } else {
 #pragma unroll
-            for (int k = 0; k < kPer; ++k) load_x4<DT, VEC, false>(draft, tbase, (g0 + k * kWave + lane) * 4, tn, x[k]);
+            for (int k = 0; k < kPer; ++k) {
+                load_x4<DT, VEC, false>(draft, tbase, (g0 + k * kWave + lane) * 4, tn, x[k]);
+                // a bf16 logit is the top half of its binary32 value (-inf past tn included)
+                xw[k][0] = (__float_as_uint(x[k][0]) >> 16) | (__float_as_uint(x[k][1]) & 0xFFFF0000u);
+                xw[k][1] = (__float_as_uint(x[k][2]) >> 16) | (__float_as_uint(x[k][3]) & 0xFFFF0000u);
+            }
         }
         int qn = 0;
 #pragma unroll
@@ -322,9 +356,7 @@ __device__ __forceinline__ void scan_item(const ScanArgs& A, long long it, int l
             const bool live = bmax >= bound && bmax > -INFINITY;
             const uint64_t bal = __ballot(live);
             if (live) {
-                // a bf16 logit is the top half of its binary32 value (-inf past tn included)
-                const uint32_t w0 = (__float_as_uint(x[k][0]) >> 16) | (__float_as_uint(x[k][1]) & 0xFFFF0000u);
-                const uint32_t w1 = (__float_as_uint(x[k][2]) >> 16) | (__float_as_uint(x[k][3]) & 0xFFFF0000u);
+                const uint32_t w0 = xw[k][0], w1 = xw[k][1];
                 queue[qn + __popcll(bal & ((1ull << lane) - 1ull))] =
                     make_uint4((uint32_t)(g0 + k * kWave + lane), w0, w1, __float_as_uint(bmax));
             }

@@ -113,9 +113,9 @@ __device__ __forceinline__ void stream_piece(const void* __restrict__ target, si
             const float mc = m * c;
 #pragma unroll
             for (int l = 0; l < kLoads; ++l) {
-                float cs = 0.f;
+                float cs = __builtin_amdgcn_exp2f(fmaf(x[l][0], c, -mc));
 #pragma unroll
-                for (int j = 0; j < kEl; ++j) cs += __builtin_amdgcn_exp2f(fmaf(x[l][j], c, -mc));
+                for (int j = 1; j < kEl; ++j) cs += __builtin_amdgcn_exp2f(fmaf(x[l][j], c, -mc));
                 sum += (double)cs;
             }
         }
