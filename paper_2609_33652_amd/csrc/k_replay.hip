@@ -50,6 +50,7 @@ constexpr int kScanWorkgroups = 1536;  // resident at 6 waves per SIMD
 // 1024 (two chunks each) by 7% and 512 (four each) by 2% at the batched
 // workload, where the scan ends last; the scan's count matters little.
 constexpr int kFusedTargetWorkgroups = 683;
+constexpr bool kFusedTargetPrefetch = false;  // see kTargetPrefetch
 constexpr int kFusedScanWorkgroups = 2048;
 
 // A parent that replay fills: a well-formed node of the caller's topology
@@ -447,7 +448,7 @@ __global__ __launch_bounds__(kBlock) void replay_scan_target(ScanArgs A, const i
         XRegion X;
         X.slots = job.slots;
         for (int g = blockIdx.x; g < job.ngroups; g += nt)
-            target_chunk<DT, TVEC>(g, job.ngroups, job.target, A.V, A.B, job.nrows, job.chunk, job.P, A.invT,
+            target_chunk<DT, TVEC, kFusedTargetPrefetch>(g, job.ngroups, job.target, A.V, A.B, job.nrows, job.chunk, job.P, A.invT,
                                    job.n_nodes, job.tm, job.ts, job.tf, X, job.R);
         return;
     }

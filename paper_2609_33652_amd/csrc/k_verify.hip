@@ -40,7 +40,7 @@ __global__ __launch_bounds__(kBlock) void target_partials(const void* __restrict
                                                           const int32_t* __restrict__ n_nodes,
                                                           float* __restrict__ tm, double* __restrict__ ts,
                                                           int* __restrict__ tf, XRegion X, int R) {
-    target_chunk<DT, VEC>(blockIdx.x, gridDim.x, target, V, B, nrows, chunk, P, invT, n_nodes, tm, ts, tf, X, R);
+    target_chunk<DT, VEC, kTargetPrefetch>(blockIdx.x, gridDim.x, target, V, B, nrows, chunk, P, invT, n_nodes, tm, ts, tf, X, R);
 }
 
 // ------------------------------------------------------------------ K5
@@ -272,21 +272,32 @@ __device__ void bonus_from_p(const WalkArgs& A, bool vec, const WalkSlice& S, si
     int bidx = 0x7FFFFFFF;
     const SplitF Ls = split(Lt);
     const int n = S.v1 - S.v0;
-    for (int i4 = threadIdx.x; i4 * 4 < n; i4 += kWalkThreads) {
-        const int i = i4 * 4;
-        const int valid = min(4, n - i);
-        float at[4];
-        load4_scaled<DT>(A.target, trow + S.v0 + i, valid, vec, A.invT, at);
-        const uint4 w = rng_block(key, node, kStreamBonus, (uint32_t)((S.v0 + i) >> 2));
-        const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+    // two groups of four per thread and iteration, both loads issued before
+    // either is used
+    for (int i4 = threadIdx.x; i4 * 4 < n; i4 += 2 * kWalkThreads) {
+        float at[2][4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            if (e >= valid || at[e] == -INFINITY) continue;
-            const float kv = ((at[e] - Ls.hi) - Ls.lo) + gumbel_f32(ws[e]);  // ln p_v + G_v
-            const int v = S.v0 + i + e;
-            if (kv > best || (kv == best && v < bidx)) {
-                best = kv;
-                bidx = v;
+        for (int h = 0; h < 2; ++h) {
+            const int i = (i4 + h * kWalkThreads) * 4;
+            const int valid = max(0, min(4, n - i));
+            load4_scaled<DT>(A.target, trow + S.v0 + (valid ? i : 0), valid, vec, A.invT, at[h]);
+        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int i = (i4 + h * kWalkThreads) * 4;
+            const int valid = max(0, min(4, n - i));
+            if (valid == 0) continue;
+            const uint4 w = rng_block(key, node, kStreamBonus, (uint32_t)((S.v0 + i) >> 2));
+            const uint32_t ws[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                if (e >= valid || at[h][e] == -INFINITY) continue;
+                const float kv = ((at[h][e] - Ls.hi) - Ls.lo) + gumbel_f32(ws[e]);  // ln p_v + G_v
+                const int v = S.v0 + i + e;
+                if (kv > best || (kv == best && v < bidx)) {
+                    best = kv;
+                    bidx = v;
+                }
             }
         }
     }
