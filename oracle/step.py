@@ -51,21 +51,40 @@ def plan_request(draft, T, K, B):
 VERIFIERS = ("rrs", "traversal")
 
 
+class _RowNotFinite(Exception):
+    """A target row the walk visits holds a NaN or +inf, or no finite entry."""
+
+
 def verify_request(draft, target, tree, node_tok, lse_draft64, T, seed, step, request, verifier="rrs"):
     """Target normalisers + the verification walk for one request: WoR-RRS (eq. (1); Appendix A) or
-    traversal verification (Appendix A; Table 2), both with the replayed candidates' probabilities."""
+    traversal verification (Appendix A; Table 2), both with the replayed candidates' probabilities.
+
+    Unusable target rows (a NaN, a +inf, or no finite entry; the paper has no such rows) end the round
+    with NONFINITE. WoR-RRS reads a row only when its walk enters the node, so only the rows of the
+    nodes it enters count, as in target-sample matching; traversal verification counts every row of the
+    tree. lse_t holds each row's normaliser (NaN for an unusable row) whatever the status.
+    """
     invT = inv_temperature(T)
     n = tree["n_nodes"]
     a_t = [scaled(target[u], invT) for u in range(n)]
-    if not all(row_ok(a) for a in a_t):
-        return dict(n_acc=-1, acc_node=[], acc_tok=[], bonus=-1, terminal=-1,
-                    status=STATUS_NONFINITE, tests=[], residual_Z=[], margins=[],
-                    lse_t=np.full(n, np.nan))
-    lse_t = np.array([lse64(a) for a in a_t])
+    ok = [row_ok(a) for a in a_t]
+    lse_t = np.array([lse64(a) if ok[u] else np.nan for u, a in enumerate(a_t)])
+    unusable = dict(n_acc=-1, acc_node=[], acc_tok=[], bonus=-1, terminal=-1,
+                    status=STATUS_NONFINITE, tests=[], residual_Z=[], margins=[], lse_t=lse_t)
+    if verifier != "rrs" and not all(ok):
+        return unusable
+
+    def p_rows(u):
+        if not ok[u]:
+            raise _RowNotFinite(u)
+        return probs(a_t[u], lse_t[u])
+
     a_d = scaled(draft, invT)
     walk = verify_mod.verify if verifier == "rrs" else traversal_mod.verify_traversal
-    res = walk(lambda u: probs(a_t[u], lse_t[u]), lambda d: probs(a_d[d], lse_draft64[d]),
-               tree, node_tok, seed, step, request)
+    try:
+        res = walk(p_rows, lambda d: probs(a_d[d], lse_draft64[d]), tree, node_tok, seed, step, request)
+    except _RowNotFinite:
+        return unusable
     res["lse_t"] = lse_t
     return res
 

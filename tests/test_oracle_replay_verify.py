@@ -177,3 +177,35 @@ def test_sampling_verifier_matches_exact_law():
     if exp2[-1] == 0:
         obs2, exp2 = obs2[:-1], exp2[:-1]
     assert stats.chisquare(obs2, exp2).pvalue > 1e-3
+
+
+def test_rrs_reads_only_the_target_rows_its_walk_enters():
+    """An unusable target row (here a NaN) ends a WoR-RRS round only when the walk enters its node: in a
+    row the walk never reads it changes no output but that row's normaliser; in the root row it ends the
+    round with NONFINITE. Traversal verification rejects it anywhere in the tree."""
+    from oracle import step
+    rng = np.random.default_rng(311)
+    V, D, B, K = 12, 3, 8, 3
+    draft = (rng.standard_normal((D, V)) * 1.5).astype(np.float32)
+    target = (rng.standard_normal((B + 1, V)) * 1.5).astype(np.float32)
+    for s in range(6):
+        ref = step.step_request(draft, target, 1.0, K, B, seed=0x7A, step=s, request=1)
+        entered = {0} | {int(c) for c in ref["acc_node"]}
+        spare = [u for u in range(ref["tree"]["n_nodes"]) if u not in entered]
+        assert spare and ref["n_acc"] >= 0
+        t = target.copy()
+        t[spare[-1], 3] = np.nan
+        out = step.step_request(draft, t, 1.0, K, B, seed=0x7A, step=s, request=1)
+        assert (out["n_acc"], out["acc_node"], out["acc_tok"], out["bonus"]) == \
+            (ref["n_acc"], ref["acc_node"], ref["acc_tok"], ref["bonus"])
+        assert not out["status"] & 1
+        lse_a, lse_b = ref["verify"]["lse_t"], out["verify"]["lse_t"]
+        assert np.isnan(lse_b[spare[-1]])
+        keep = np.arange(len(lse_a)) != spare[-1]
+        assert np.array_equal(lse_a[keep], lse_b[keep])
+        trav = step.step_request(draft, t, 1.0, K, B, seed=0x7A, step=s, request=1, verifier="traversal")
+        assert trav["status"] & 1 and trav["n_acc"] == -1
+        t = target.copy()
+        t[0, 5] = np.inf
+        out = step.step_request(draft, t, 1.0, K, B, seed=0x7A, step=s, request=1)
+        assert out["status"] & 1 and out["n_acc"] == -1 and out["bonus"] == -1
