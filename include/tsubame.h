@@ -87,7 +87,7 @@ extern "C" {
 typedef enum tsb_status {
     TSB_OK = 0,
     TSB_E_NULL = 1,        /* a required pointer is NULL */
-    TSB_E_SHAPE = 2,       /* R, D, V, B or K out of range */
+    TSB_E_SHAPE = 2,       /* R, D, V, B or K out of range, or flags that exclude each other */
     TSB_E_DTYPE = 3,       /* unknown logit dtype */
     TSB_E_TEMPERATURE = 4, /* temperature not finite or not > 0 */
     TSB_E_WORKSPACE = 5,   /* workspace too small or not 256-byte aligned */
@@ -111,7 +111,12 @@ enum {
 
 /* cfg.flags */
 enum {
-    TSB_FLAG_NO_PRUNE = 1 /* replay scores every token (no early rejection by the Gumbel bound) */
+    TSB_FLAG_NO_PRUNE = 1,   /* replay scores every token (no early rejection by the Gumbel bound) */
+    TSB_FLAG_READ_ROWS = 2,  /* the WoR-RRS walk reads each target row when it enters the row's node (the
+                                default when the target holds more than 128 MiB) */
+    TSB_FLAG_STREAM_ROWS = 4 /* the WoR-RRS walk takes the row normalisers from a stream of every target row
+                                before it (the default up to 128 MiB); not with TSB_FLAG_READ_ROWS. Results do
+                                not depend on the choice, except for rounding in trace values */
 };
 
 typedef struct tsb_config {
@@ -144,8 +149,9 @@ typedef struct tsb_tree {
 /* Outputs of verification. n_acc, bonus and req_status are [R]; acc_node and
  * acc_tok are [R, D] (entries >= n_acc[r] set to -1). req_status is OR-ed
  * into (tsb_plan clears it). target_lse ([R, B+1], binary64 log-sum-exp of
- * the scaled target rows, NaN beyond n_nodes) and trace are optional (NULL
- * to skip). trace is [R, TSB_TRACE_MAX, 4] doubles per acceptance test, in
+ * the scaled target rows, NaN for an unusable row and beyond n_nodes) and
+ * trace are optional (NULL to skip; asking for target_lse makes the WoR-RRS
+ * entry points stream every row of the tree). trace is [R, TSB_TRACE_MAX, 4] doubles per acceptance test, in
  * walk order: (child node, uniform U, ratio, residual mass after rejection or
  * -1), unused entries -1. */
 typedef struct tsb_verdict {
@@ -198,15 +204,24 @@ tsb_status tsb_replay(const tsb_config* cfg, const void* draft, const int32_t* t
 /* Verification (eq. (1); Appendix A). target: [R, B+1, V] logits, row i is
  * the target's next-token logits at tree node i (rows >= n_nodes unread).
  * draft_lse as written by tsb_plan. A visited node token outside [0, V)
- * stops the walk with TSB_REQ_BAD_TOKEN and n_acc = bonus = -1. */
+ * stops the walk with TSB_REQ_BAD_TOKEN and n_acc = bonus = -1. Only the
+ * target rows of the nodes the walk enters decide the request: one of them
+ * with a NaN or +inf logit, or with no finite logit, ends it with
+ * TSB_REQ_NONFINITE and n_acc = bonus = -1; other rows are not checked. The
+ * walk reads those rows as it enters their nodes (TSB_FLAG_READ_ROWS, the
+ * default above 128 MiB of target), or takes their normalisers from a stream
+ * of every row launched before it (TSB_FLAG_STREAM_ROWS, the default up to
+ * 128 MiB, and whenever out->target_lse is asked for). */
 tsb_status tsb_verify(const tsb_config* cfg, const void* draft, const double* draft_lse,
                       const void* target, const tsb_tree* tree, const int32_t* node_tok,
                       uint32_t step, const tsb_verdict* out, void* workspace,
                       size_t workspace_bytes, hipStream_t stream);
 
 /* plan -> replay -> verify back to back on one stream (target supplied up
- * front). The replay scan's grid also streams the target's row normalisers
- * (one launch for both), so the walk follows the replay directly. */
+ * front). When every target row is streamed (see tsb_verify), the replay
+ * scan's grid carries that stream (one launch for both); otherwise it clears
+ * the walk's exchange slots and the walk reads the rows of the nodes it
+ * enters. Results as tsb_plan, tsb_replay and tsb_verify in turn. */
 tsb_status tsb_step(const tsb_config* cfg, const void* draft, const void* target, uint32_t step,
                     double* draft_lse, int32_t* topk_tok, float* topk_lp, const tsb_tree* tree,
                     int32_t* node_tok, const tsb_verdict* out, void* workspace,
@@ -231,8 +246,9 @@ tsb_status tsb_step_noalloc(const tsb_config* cfg, const void* draft, const void
 
 /* Traversal verification (Appendix A; Table 2: the sequence-level verifier
  * paired with sampling without replacement; compared with layer-wise RRS on
- * replayed trees in Section 4.2). Same arguments and outputs as tsb_verify.
- * The replayed tree is traversed in post-order (the first remaining child
+ * replayed trees in Section 4.2). Same arguments and outputs as tsb_verify,
+ * except that every target row of the tree is streamed and must be usable
+ * (else TSB_REQ_NONFINITE). The replayed tree is traversed in post-order (the first remaining child
  * first, down to a node with no children left); the node reached is
  * accepted, with the path from the root, with probability alpha, where
  * alpha_root = 1 and a child c with token y of node u gets

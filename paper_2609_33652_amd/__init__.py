@@ -30,6 +30,8 @@ REQ_BAD_TOKEN = 16
 REQ_BAD_TREE = 32
 POOL_MAX = 64
 FLAG_NO_PRUNE = 1
+FLAG_READ_ROWS = 2
+FLAG_STREAM_ROWS = 4
 MAX_D, MAX_K, MAX_B, TRACE_MAX = 64, 32, 1023, 256
 KERNELS = ("draft_partials", "plan_tree", "replay_scan", "replay_merge", "target_partials",
            "verify_walk", "verify_naive", "pool_partials", "pool_lists", "pool_plan", "pool_replay", "pool_walk",
@@ -147,6 +149,16 @@ def load(path=LIB_PATH):
     lib.tsb_stats_read.argtypes = [ctypes.POINTER(TsbStats), ctypes.c_int32]
     _LIB = lib
     return lib
+
+
+def walk_reads_rows(cfg):
+    """Whether the WoR-RRS walk of cfg reads each target row as it enters the row's node (the library's
+    rule: the flags, else more than 128 MiB of target); the other way streams every row first."""
+    if cfg.flags & FLAG_READ_ROWS:
+        return True
+    if cfg.flags & FLAG_STREAM_ROWS:
+        return False
+    return cfg.R * (cfg.B + 1) * cfg.V * (2 if cfg.dtype == TSB_BF16 else 4) > (128 << 20)
 
 
 def make_config(R, D, V, B, K, temperature, dtype, seed, flags=0):

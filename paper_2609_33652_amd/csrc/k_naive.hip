@@ -358,6 +358,14 @@ __global__ __launch_bounds__(kBlock) void xchg_clear(XRegion X, int R) {
     xclear(X, R, (size_t)blockIdx.x * kBlock + threadIdx.x, (size_t)gridDim.x * kBlock);
 }
 
+hipError_t launch_xchg_clear(const tsb_config& c, uint64_t* slots, hipStream_t st) {
+    XRegion X;
+    X.slots = slots;
+    const int nclear = (int)std::min<size_t>(1024, (xwords(c.R) + kBlock - 1) / kBlock);
+    xchg_clear<<<nclear, kBlock, 0, st>>>(X, c.R);
+    return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ launch
 hipError_t launch_first_tokens(const tsb_config& c, const int32_t* topk_tok, const tsb_tree& tree, int32_t* node_tok,
                                hipStream_t st) {
@@ -429,9 +437,7 @@ hipError_t launch_verify_naive(const tsb_config& c, float invT, const void* targ
     A.R = c.R;
     A.G = G;
 
-    const int nclear = (int)std::min<size_t>(1024, (xwords(c.R) + kBlock - 1) / kBlock);
-    xchg_clear<<<nclear, kBlock, 0, st>>>(A.X, c.R);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if ((e = launch_xchg_clear(c, A.X.slots, st)) != hipSuccess) return e;
     if ((e = hook_before(TSB_KERNEL_VERIFY_NAIVE, st)) != hipSuccess) return e;
     void* args[] = {&A};
     e = hipLaunchKernel(fn, dim3((unsigned)(G * c.R)), dim3(kNaiveThreads), args, 0, st);

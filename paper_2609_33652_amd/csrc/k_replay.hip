@@ -477,7 +477,9 @@ __device__ __forceinline__ NodeHead node_head(const TargetJob& job, const tsb_tr
                                               size_t tb, int D) {
     NodeHead h;
     h.t = tree_node(tree, tb, u, n, D);
-    h.L0 = target_row_lse(job.tm, job.ts, job.tf, job.P, tb + u, &h.bad);
+    h.L0 = 0.0;
+    h.bad = 0;
+    if (job.nrows > 0) h.L0 = target_row_lse(job.tm, job.ts, job.tf, job.P, tb + u, &h.bad);
     h.Ld = (h.t.ok && h.t.m > 0) ? job.draft_lse[(size_t)r * D + h.t.d] : 0.0;
     return h;
 }

@@ -66,6 +66,10 @@ struct WalkArgs {
     int P;
     // node records (kRecWords per node) when the round's merge wrote them, else null
     const uint32_t* nrec;
+    // the RRS walk reads each target row as it enters the node (else the row
+    // normalisers come from a stream of every row, through the records or the
+    // partials)
+    int reads_rows;
 };
 
 // binary64 log-sum-exp of target row (r, node) from its segment partials
@@ -75,16 +79,6 @@ __device__ double target_lse(const WalkArgs& A, int r, int node, int* bad) {
 
 __device__ __forceinline__ double rec_f64(uint32_t lo, uint32_t hi) {
     return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
-}
-
-// The same from the node record when the round's merge wrote them.
-__device__ double node_lse(const WalkArgs& A, int r, int node, int* bad) {
-    if (!A.nrec) return target_lse(A, r, node, bad);
-    const uint32_t* rp = A.nrec + ((size_t)r * (A.B + 1) + node) * kRecWords;
-    const uint4 h0 = *(const uint4*)rp;
-    const uint4 h1 = *(const uint4*)(rp + 4);
-    *bad = (h0.w & kRecTargetBad) != 0;
-    return rec_f64(h1.x, h1.y);
 }
 
 struct SplitF {  // binary64 value as binary32 hi + lo
@@ -410,7 +404,134 @@ struct Exchange {
         *tot = t[0];
         return fk > -INFINITY ? fi : -1;
     }
+    // Log-sum-exp of the workgroups' (max a, sum exp(a - max a)) pairs: the
+    // largest max, then every sum rescaled to it and added in a fixed order
+    // (every workgroup gets the same value). *bad if a workgroup flagged its
+    // part, or if no part holds a finite logit.
+    __device__ double lse(double mx, double s, bool part_bad, bool* bad) {
+        constexpr int NH = kWalkGroupsMax / kWave;
+        const uint64_t w[3] = {xpack_f64(mx), xpack_f64(s), xpack_u32(part_bad ? 1u : 0u)};
+        xpublish<3>(A->X, r, g, nb, w);
+        __shared__ double s_l;
+        __shared__ int s_b, s_to;
+        if (threadIdx.x < kWave) {
+            const int lane = threadIdx.x;
+            double hm[NH], hs[NH];
+            int b = 0, to = 0;
+            double M = -INFINITY;
+#pragma unroll
+            for (int half = 0; half < NH; ++half) {
+                const int h = lane + half * kWave;
+                hm[half] = -INFINITY;
+                hs[half] = 0.0;
+                if (h < G) {
+                    uint64_t q[3];
+                    if (!xpoll<3>(A->X, r, h, nb, q)) to = 1;
+                    hm[half] = xunpack_f64(q[0]);
+                    hs[half] = xunpack_f64(q[1]);
+                    b |= xunpack_u32(q[2]) != 0u;
+                }
+                M = fmax(M, hm[half]);
+            }
+#pragma unroll
+            for (int off = 32; off > 0; off >>= 1) M = fmax(M, __shfl_xor(M, off, kWave));
+            double t = 0.0;
+            if (M > -INFINITY)
+#pragma unroll
+                for (int half = 0; half < NH; ++half)
+                    if (hm[half] > -INFINITY) t += hs[half] * exp(hm[half] - M);
+            t = wave_sum(t);
+            b = wave_or(b);
+            to = wave_or(to);
+            if (lane == 0) {
+                const bool none = !(M > -INFINITY) || !(t > 0.0);
+                s_l = none ? 0.0 : M + log(t);
+                s_b = b || none || !isfinite(M) || !isfinite(t);
+                s_to = to;
+            }
+        }
+        __syncthreads();
+        const double L = s_l;
+        *bad = s_b != 0;
+        if (s_to) timeout = 1;
+        ++nb;
+        __syncthreads();  // s_l is rewritten by the next exchange
+        return L;
+    }
 };
+
+// Streamed normaliser of the target row of the node the walk enters (the
+// walk reads a target row only when it enters its node): each workgroup
+// streams its slice (running maximum m of the raw logits, binary32 terms
+// 2^(x c - m c) with c = invT log2(e), added in binary64, as the target
+// stream does), then the request's workgroups combine their parts by one
+// exchange. Within ~1e-6 of ln sum_v exp(a_v); *bad if the row holds a NaN
+// or +inf logit, or no finite one.
+template <int DT>
+__device__ double entered_row_lse(const WalkArgs& A, bool vec, const WalkSlice& S, size_t trow, Exchange& X,
+                                  bool* bad) {
+    constexpr int kG = 4;  // groups of four logits loaded per thread before any is used
+    const float c = A.invT * 1.4426950408889634f;
+    const int n = S.v1 - S.v0;
+    float m = -INFINITY;
+    double sum = 0.0;
+    bool nf = false;
+    for (int base = 0; base < n; base += kG * 4 * kWalkThreads) {
+        float x[kG][4];
+#pragma unroll
+        for (int k = 0; k < kG; ++k) {
+            const int i = base + (k * kWalkThreads + (int)threadIdx.x) * 4;
+            const int valid = max(0, min(4, n - i));
+            load4<DT>(A.target, trow + S.v0 + (valid ? i : 0), valid, vec, x[k]);
+        }
+        float cm = m;
+#pragma unroll
+        for (int k = 0; k < kG; ++k)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                nf |= __builtin_amdgcn_classf(x[k][e], 0x203);  // signalling NaN, quiet NaN, +inf
+                cm = fmaxf(cm, x[k][e]);                        // NaN is ignored
+            }
+        if (cm > m) {
+            if (m > -INFINITY) sum *= (double)exp2f((m - cm) * c);
+            m = cm;
+        }
+        if (m > -INFINITY && m < INFINITY) {
+            const float mc = m * c;
+#pragma unroll
+            for (int k = 0; k < kG; ++k) {
+                float cs = 0.f;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) cs += __builtin_amdgcn_exp2f(fmaf(x[k][e], c, -mc));
+                sum += (double)cs;
+            }
+        }
+    }
+    // the workgroup's part: (max a, sum exp(a - max a)), fixed order
+    __shared__ float s_m[kWalkThreads / kWave];
+    __shared__ double s_s[kWalkThreads / kWave];
+    __shared__ int s_nf;
+    if (threadIdx.x == 0) s_nf = 0;
+    const float wm = wave_max(m);
+    const double ws = wave_sum((m == -INFINITY || m == wm) ? (m == -INFINITY ? 0.0 : sum)
+                                                           : sum * (double)exp2f((m - wm) * c));
+    const int wnf = wave_or(nf ? 1 : 0);
+    __syncthreads();
+    if ((threadIdx.x % kWave) == 0) {
+        s_m[threadIdx.x / kWave] = wm;
+        s_s[threadIdx.x / kWave] = ws;
+        if (wnf) s_nf = 1;
+    }
+    __syncthreads();
+    float M = s_m[0];
+    for (int w = 1; w < kWalkThreads / kWave; ++w) M = fmaxf(M, s_m[w]);
+    double tot = 0.0;
+    if (M > -INFINITY && M < INFINITY)
+        for (int w = 0; w < kWalkThreads / kWave; ++w)
+            if (s_m[w] > -INFINITY) tot += s_s[w] * (double)exp2f((s_m[w] - M) * c);
+    const bool part_bad = s_nf != 0 || M == INFINITY || !isfinite(tot);
+    return X.lse(M > -INFINITY && !part_bad ? (double)(M * A.invT) : -INFINITY, part_bad ? 0.0 : tot, part_bad, bad);
+}
 
 // Relative half-width of the band in which an acceptance test taken with the
 // streamed normaliser is recomputed with the exact one (the streamed
@@ -522,64 +643,61 @@ __device__ void fill_pass(const WalkArgs& A, bool vec, const WalkSlice& S, bool 
     walk_sum4(out);
 }
 
-// End of a walk, for every workgroup of the request: every target row of
-// the tree must be finite (workgroup 0 decides); outputs of the request.
+// End of a walk, for every workgroup of the request: the request's outputs,
+// and the optional normaliser output (from the target stream's partials,
+// which the caller streamed when it asked for it). rows_bad < 0: every target
+// row of the tree must be usable (each workgroup checks the partials, so all
+// agree); otherwise rows_bad is the walk's own verdict on the rows it entered.
 __device__ void walk_tail(const WalkArgs& A, int r, int g, int G, int n, bool draft_bad, bool invalid, int nacc,
-                          int bonus_out, int add_status, int tcount) {
+                          int bonus_out, int add_status, int tcount, int rows_bad = -1) {
     __shared__ int s_bad;
     const int tid = threadIdx.x;
     const int B1 = A.B + 1;
     const size_t tb = (size_t)r * B1;
     const bool lead = (g == 0 && tid == 0);
     int* status_p = A.out.req_status + r;
-    // every target row of the tree must be finite; optional normaliser output
     if (tid == 0) s_bad = 0;
     __syncthreads();
-    if (!draft_bad) {
-        for (int i = g * kWalkThreads + tid; i < n; i += G * kWalkThreads) {
+    if (!draft_bad && rows_bad < 0)
+        for (int i = tid; i < n; i += kWalkThreads) {
             int b;
-            const double l = node_lse(A, r, i, &b);
+            target_lse(A, r, i, &b);
             if (b) atomicOr(&s_bad, 1);
-            if (A.out.target_lse) A.out.target_lse[tb + i] = b ? (double)NAN : l;
+        }
+    __syncthreads();
+    const bool bad = draft_bad || (rows_bad < 0 ? s_bad != 0 : rows_bad != 0);
+    if (A.out.target_lse) {
+        // a request rejected by a verifier that reads every row reports no normaliser
+        const bool none = draft_bad || (bad && rows_bad < 0);
+        for (int i = g * kWalkThreads + tid; i < B1; i += G * kWalkThreads) {
+            double l = (double)NAN;
+            if (!none && i < n) {
+                int b;
+                l = target_lse(A, r, i, &b);
+                if (b) l = (double)NAN;
+            }
+            A.out.target_lse[tb + i] = l;
         }
     }
-    __syncthreads();
-    if (A.out.target_lse)
-        for (int i = n + g * kWalkThreads + tid; i < B1; i += G * kWalkThreads) A.out.target_lse[tb + i] = (double)NAN;
-    if (g == 0) {
-        // workgroup 0 decides the request's finiteness over all rows
-        if (tid == 0) s_bad = 0;
-        __syncthreads();
-        if (!draft_bad)
-            for (int i = tid; i < n; i += kWalkThreads) {
-                int b;
-                node_lse(A, r, i, &b);
-                if (b) atomicOr(&s_bad, 1);
-            }
-        __syncthreads();
-        const bool bad = draft_bad || s_bad;
-        if (bad && A.out.target_lse)
-            for (int i = tid; i < B1; i += kWalkThreads) A.out.target_lse[tb + i] = (double)NAN;
-        if (lead) {
-            if (bad) {
-                nacc = 0;
-                bonus_out = -1;
-                add_status = (add_status & ~(TSB_REQ_DEGENERATE_RESIDUAL | TSB_REQ_WALK_TIMEOUT)) | TSB_REQ_NONFINITE;
-            } else if (invalid) {  // a malformed tree or token: outputs defined, without meaning
-                nacc = 0;
-                bonus_out = -1;
-            }
-            for (int i = nacc; i < A.D; ++i) {
-                A.out.acc_node[(size_t)r * A.D + i] = -1;
-                A.out.acc_tok[(size_t)r * A.D + i] = -1;
-            }
-            A.out.n_acc[r] = (bad || invalid) ? -1 : nacc;
-            A.out.bonus[r] = bonus_out;
-            *status_p |= add_status;
-            if (A.out.trace)
-                for (int i = tcount; i < TSB_TRACE_MAX; ++i)
-                    for (int f = 0; f < 4; ++f) A.out.trace[((size_t)r * TSB_TRACE_MAX + i) * 4 + f] = -1.0;
+    if (lead) {
+        if (bad) {
+            nacc = 0;
+            bonus_out = -1;
+            add_status = (add_status & ~(TSB_REQ_DEGENERATE_RESIDUAL | TSB_REQ_WALK_TIMEOUT)) | TSB_REQ_NONFINITE;
+        } else if (invalid) {  // a malformed tree or token: outputs defined, without meaning
+            nacc = 0;
+            bonus_out = -1;
         }
+        for (int i = nacc; i < A.D; ++i) {
+            A.out.acc_node[(size_t)r * A.D + i] = -1;
+            A.out.acc_tok[(size_t)r * A.D + i] = -1;
+        }
+        A.out.n_acc[r] = (bad || invalid) ? -1 : nacc;
+        A.out.bonus[r] = bonus_out;
+        *status_p |= add_status;
+        if (A.out.trace)
+            for (int i = tcount; i < TSB_TRACE_MAX; ++i)
+                for (int f = 0; f < 4; ++f) A.out.trace[((size_t)r * TSB_TRACE_MAX + i) * 4 + f] = -1.0;
     }
 }
 
@@ -627,6 +745,7 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
 
     int bonus_out = -1, add_status = count_ok ? 0 : TSB_REQ_BAD_TREE, nacc = 0;
     bool invalid = !count_ok;
+    int rows_bad = 0;  // an entered node's target row is unusable
     if (!draft_bad && count_ok) {
         RngKey key;
         key.k0 = A.k0;
@@ -639,11 +758,12 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
             ++n_entered;
             // every workgroup reads the same entries, so all take the same exit
             TreeNode nd;
-            double L0, Ld = 0.0;
+            double L0 = 0.0, Ld = 0.0;
+            bool row_bad = false;  // u's target row is unusable
             uint4 crec = make_uint4(0u, 0u, 0u, 0u);  // child tid's (token, x_d, x_t) from the record
             if (A.nrec) {
-                // the node's record: its topology, normalisers and children in
-                // one round trip
+                // the node's record: its topology, draft normaliser and
+                // children in one round trip
                 const uint32_t* rp = A.nrec + (tb + u) * kRecWords;
                 const uint4 h0 = *(const uint4*)rp;
                 const uint4 h1 = *(const uint4*)(rp + 4);
@@ -653,11 +773,15 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
                 nd.d = (int)h0.z;
                 nd.ok = (h0.w & kRecOk) != 0;
                 L0 = rec_f64(h1.x, h1.y);
+                row_bad = (h0.w & kRecTargetBad) != 0;
                 Ld = rec_f64(h1.z, h1.w);
             } else {
                 nd = tree_node(A.tree, tb, u, n, A.D);
-                int tbad;
-                L0 = target_lse(A, r, u, &tbad);
+                if (!A.reads_rows) {
+                    int tbad;
+                    L0 = target_lse(A, r, u, &tbad);
+                    row_bad = tbad != 0;
+                }
             }
             if (!nd.ok || (nd.m > 0 && nacc >= A.D)) {
                 add_status |= TSB_REQ_BAD_TREE;
@@ -666,6 +790,13 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
             }
             const int m = nd.m, d = nd.d;
             const size_t trow = ((size_t)r * B1 + u) * (size_t)A.V;
+            // or the target row of u, read now that the walk has entered u: its
+            // streamed normaliser, and whether it is usable
+            if (A.reads_rows) L0 = entered_row_lse<DT>(A, vec, S, trow, X, &row_bad);
+            if (row_bad) {
+                rows_bad = 1;
+                break;
+            }
             const size_t drow = ((size_t)r * A.D + (m > 0 ? d : 0)) * (size_t)A.V;
             if (m == 0) {  // accepted leaf: bonus from p_u
                 float bk;
@@ -843,7 +974,7 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
         }
     }
 
-    walk_tail(A, r, g, G, n, draft_bad, invalid, nacc, bonus_out, add_status, tcount);
+    walk_tail(A, r, g, G, n, draft_bad, invalid, nacc, bonus_out, add_status, tcount, rows_bad);
 }
 
 
@@ -965,6 +1096,7 @@ __global__ __launch_bounds__(kWalkThreads) void verify_pool_walk(WalkArgs A) {
 
     int bonus_out = -1, add_status = count_ok ? 0 : TSB_REQ_BAD_TREE, nacc = 0;
     bool invalid = !count_ok;
+    int rows_bad = 0;  // an entered node's target row is unusable
     if (!draft_bad && count_ok) {
         RngKey key;
         key.k0 = A.k0;
@@ -1248,6 +1380,7 @@ __global__ __launch_bounds__(kWalkThreads) void verify_traversal(WalkArgs A) {
     double* const trace = (lead && A.out.trace) ? A.out.trace + (size_t)r * TSB_TRACE_MAX * 4 : nullptr;
     int bonus_out = -1, add_status = count_ok ? 0 : TSB_REQ_BAD_TREE, nacc = 0;
     bool invalid = !count_ok;
+    int rows_bad = 0;  // an entered node's target row is unusable
     if (!draft_bad && count_ok) {
         RngKey key;
         key.k0 = A.k0;
@@ -1497,7 +1630,7 @@ static hipError_t walk_capacity(const void* fn, int kind, int dt, int vec, size_
 }
 
 TargetJob target_job(const tsb_config& c, const void* target, const tsb_tree& tree, const double* draft_lse,
-                     char* ws) {
+                     char* ws, bool rows) {
     const Geometry g = geometry(c);
     const VerifyWs w = verify_ws(c);
     TargetJob j;
@@ -1516,6 +1649,11 @@ TargetJob target_job(const tsb_config& c, const void* target, const tsb_tree& tr
                                   : (c.V % 4 == 0 && ((uintptr_t)target & 15) == 0);
     j.nrec = draft_lse ? (uint32_t*)(ws + w.nrec) : nullptr;
     j.draft_lse = draft_lse;
+    if (!rows) {
+        // no row: the job's workgroups only clear the exchange slots
+        j.nrows = 0;
+        j.ngroups = kClearWorkgroups;
+    }
     return j;
 }
 
@@ -1569,6 +1707,7 @@ static WalkArgs walk_args(const tsb_config& c, float invT, const void* draft, co
     A.trans = nullptr;
     A.P = 0;
     A.nrec = nullptr;
+    A.reads_rows = 0;
     return A;
 }
 
@@ -1587,10 +1726,17 @@ hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, con
                          const tsb_verdict& out, char* ws, hipStream_t st, int stages) {
     const VerifyWs w = verify_ws(c);
     hipError_t e = hipSuccess;
-    if ((stages & kStageTarget) && (e = launch_target_partials(c, invT, target, tree, w, ws, st)) != hipSuccess)
-        return e;
+    // a walk that reads the rows of the nodes it enters needs every row
+    // streamed only for the optional normaliser output
+    const bool reads = walk_reads_rows(c);
+    if (stages & kStageTarget) {
+        e = (out.target_lse || !reads) ? launch_target_partials(c, invT, target, tree, w, ws, st)
+                                       : launch_xchg_clear(c, (uint64_t*)(ws + xchg_ws(c).slots), st);
+        if (e != hipSuccess) return e;
+    }
     if (!(stages & kStageWalk)) return hipSuccess;
     WalkArgs A = walk_args(c, invT, draft, draft_lse, target, tree, node_tok, step, out, w, ws);
+    A.reads_rows = reads ? 1 : 0;
     if (stages & kWalkRecords) A.nrec = (const uint32_t*)(ws + w.nrec);
     const bool vec4 = c.V % 4 == 0 && ((uintptr_t)target & 15) == 0 && ((uintptr_t)draft & 15) == 0;
     const void* fn = nullptr;

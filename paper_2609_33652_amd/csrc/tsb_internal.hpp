@@ -17,6 +17,12 @@ constexpr int kReplayTile = 4096;    // vocabulary tile of the replay scan
 constexpr int kWalkGroupsMax = 128;  // workgroups per request in verification
 constexpr int kWalkTokensPerGroup = 9728;  // tokens whose binary64 (p, q) one walk workgroup holds in LDS
 constexpr int kTargetWorkgroups = 2048;  // target stream: 8 resident workgroups on each of 256 CUs
+constexpr int kClearWorkgroups = 64;      // a target job without rows: workgroups that clear the exchange slots
+// Targets of up to this many bytes are streamed whole before the walk (one
+// pass beside the replay scan costs less than a row read and an exchange at
+// every node the walk enters); larger ones are read row by row as the walk
+// enters nodes.
+constexpr long long kStreamRowsBytes = 128ll << 20;
 constexpr int kTargetMinChunk = 32768;   // shortest target chunk (logits), unless the whole target is shorter
 constexpr int kDraftWorkgroups = 512;    // row statistics: two 512-thread workgroups on each of 256 CUs
 constexpr int kDraftMinSeg = 16384;      // shortest draft segment (elements), unless the row is shorter
@@ -32,6 +38,15 @@ struct Geometry {
 };
 
 inline int ceil_div(long long a, long long b) { return (int)((a + b - 1) / b); }
+
+// Whether the RRS walk reads each target row when it enters the node (true)
+// or takes the row normalisers from a stream of every row before it.
+inline bool walk_reads_rows(const tsb_config& c) {
+    if (c.flags & TSB_FLAG_READ_ROWS) return true;
+    if (c.flags & TSB_FLAG_STREAM_ROWS) return false;
+    const long long b = c.dtype == TSB_BF16 ? 2 : 4;
+    return (long long)c.R * (c.B + 1) * c.V * b > kStreamRowsBytes;
+}
 
 inline Geometry geometry(const tsb_config& c) {
     Geometry g;

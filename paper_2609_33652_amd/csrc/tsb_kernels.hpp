@@ -64,8 +64,15 @@ struct TargetJob {
     uint32_t* nrec;
     const double* draft_lse;
 };
+// rows = false: a job that streams nothing and only clears the exchange
+// slots of the walk launched after it (the walk then reads the target rows of
+// the nodes it enters).
 TargetJob target_job(const tsb_config& c, const void* target, const tsb_tree& tree, const double* draft_lse,
-                     char* ws);
+                     char* ws, bool rows = true);
+
+// Zeroes the exchange slots of the requests (before a walk that no target
+// stream precedes).
+hipError_t launch_xchg_clear(const tsb_config& c, uint64_t* slots, hipStream_t st);
 
 // With a target job, the replay scan's grid carries it: ngroups more
 // workgroups stream the target while the others scan (one launch).
@@ -74,10 +81,11 @@ hipError_t launch_replay(const tsb_config& c, float invT, const void* draft, con
                          const TargetJob* tj = nullptr);
 
 // Verification is two stages: the target stream (row normaliser partials of
-// the tree's rows) and the walk (which needs the replayed tokens and the
-// partials). A round runs the target stage in the replay scan's grid, its
-// merge writes the node records, and then the walk runs alone, reading them
-// (kWalkRecords).
+// every row of the tree, for the optional normaliser output, and for the
+// verifiers that need every row), or else the clearing of the exchange
+// slots, and the walk. A round runs the target stage in the replay scan's
+// grid, its merge writes the node records, and then the walk runs alone,
+// reading them (kWalkRecords).
 enum : int { kStageTarget = 1, kStageWalk = 2, kStagesAll = 3, kWalkRecords = 4 };
 
 hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, const double* draft_lse,

@@ -222,16 +222,17 @@ __device__ __forceinline__ double target_row_lse(const float* __restrict__ tm, c
     return (double)M + log(tot);
 }
 
-// Node records for the walk, written by the replay merge of a whole round
-// once the target partials exist: everything the walk reads when it enters
-// node u, in one record of kRecWords 32-bit words, so that entering a node
-// costs one memory round trip. Words: 0 m (children; 0 for a leaf), 1 first
-// child, 2 depth, 3 flags (kRecOk: the node passed the topology checks;
-// kRecTargetBad: its target row is not finite), 4-5 the row's streamed
-// normaliser L0 (binary64), 6-7 the draft normaliser of the children's row,
-// then per child j (up to TSB_MAX_K) four words at 8 + 4 j: token, draft
-// logit x invT and target logit x invT (binary32 bits; 0 for a token
-// outside [0, V)), unused.
+// Node records for the walk, written by the replay merge of a whole round:
+// everything the walk reads when it enters node u, in one record of
+// kRecWords 32-bit words, so that entering a node costs one memory round
+// trip (besides its target row, when the walk reads rows as it enters their
+// nodes). Words: 0 m (children; 0 for a leaf), 1 first child, 2 depth,
+// 3 flags (kRecOk: the node passed the topology checks; kRecTargetBad: its
+// target row is unusable), 4-5 the row's streamed normaliser L0 (binary64;
+// both only when every row was streamed before the merge, else 0), 6-7 the
+// draft normaliser of the children's row, then per child j (up to
+// TSB_MAX_K) four words at 8 + 4 j: token, draft logit x invT and target
+// logit x invT (binary32 bits; 0 for a token outside [0, V)), unused.
 constexpr uint32_t kRecOk = 1u, kRecTargetBad = 2u;
 
 }  // namespace tsb

@@ -42,6 +42,8 @@ tsb_status check_config(const tsb_config* c) {
     if (c->dtype != TSB_F32 && c->dtype != TSB_BF16) return fail(TSB_E_DTYPE, "dtype=%u unknown", c->dtype);
     if (!(isfinite(c->temperature) && c->temperature > 0.f))
         return fail(TSB_E_TEMPERATURE, "temperature=%g must be finite and > 0", (double)c->temperature);
+    if ((c->flags & TSB_FLAG_READ_ROWS) && (c->flags & TSB_FLAG_STREAM_ROWS))
+        return fail(TSB_E_SHAPE, "flags: TSB_FLAG_READ_ROWS and TSB_FLAG_STREAM_ROWS exclude each other");
     return TSB_OK;
 }
 
@@ -236,7 +238,10 @@ tsb_status tsb_verify(const tsb_config* cfg, const void* draft, const double* dr
 namespace {
 
 // The stages of a vocabulary-wide round: planner, then the replay scan with
-// the target stream in its grid, then the walk.
+// the target stream in its grid, then the walk. A large target is streamed in
+// full only for traversal verification (which needs every row) and for the
+// optional normaliser output; otherwise the scan's grid only clears the
+// exchange slots and the walk reads the rows of the nodes it enters.
 tsb_status step_round(const tsb_config* cfg, const void* draft, const void* target, uint32_t step,
                       double* draft_lse, int32_t* topk_tok, float* topk_lp, const tsb_tree* tree,
                       int32_t* node_tok, const tsb_verdict* out, char* ws, hipStream_t stream, bool traversal,
@@ -245,7 +250,9 @@ tsb_status step_round(const tsb_config* cfg, const void* draft, const void* targ
     const float invT = inv_temperature(cfg->temperature);
     hipError_t e = tsb::launch_plan(*cfg, invT, draft, draft_lse, topk_tok, topk_lp, *tree, out->req_status, ws, stream);
     if (e != hipSuccess) return hip_fail(e, (snprintf(where, sizeof where, "%s/plan", name), where));
-    const tsb::TargetJob tj = tsb::target_job(*cfg, target, *tree, traversal ? nullptr : draft_lse, ws);
+    const tsb::TargetJob tj = tsb::target_job(*cfg, target, *tree, traversal ? nullptr : draft_lse, ws,
+                                              traversal || out->target_lse != nullptr ||
+                                                  !tsb::walk_reads_rows(*cfg));
     e = tsb::launch_replay(*cfg, invT, draft, topk_tok, *tree, step, node_tok, ws, stream, &tj);
     if (e != hipSuccess) return hip_fail(e, (snprintf(where, sizeof where, "%s/replay+target", name), where));
     e = traversal ? tsb::launch_verify_traversal(*cfg, invT, draft, draft_lse, target, *tree, node_tok, step, *out, ws,

@@ -53,10 +53,10 @@ def to_np(t):
     return t.detach().cpu().numpy()
 
 
-def make_round(cfg_dict, seed, flags=0, trace=True):
+def make_round(cfg_dict, seed, flags=0, trace=True, target_lse=True):
     c = tsb.make_config(cfg_dict["R"], cfg_dict["D"], cfg_dict["V"], cfg_dict["B"], cfg_dict["K"],
                         cfg_dict["T"], cfg_dict["dtype"], seed, flags)
-    return tsb.Round(c, "cuda", target_lse=True, trace=trace)
+    return tsb.Round(c, "cuda", target_lse=target_lse, trace=trace)
 
 
 def tree_dict_np(h, r):

@@ -7,8 +7,11 @@ tests/parity_util.py. The workloads are checked on every request of every
 step run: all steps of the tiny and small workloads, 160 steps of the
 Qwen-vocabulary one, 16 steps of the batched one and 4 of the large-budget
 one (the oracle runs in a process pool over the host's cores). tsb_step must
-equal the staged calls bit for bit. Each case allows at most one flagged
-near-tie; the tallies are printed at the end of the run.
+equal the staged calls bit for bit, with the normaliser output requested
+and without it; the other way of reading the target rows (each row as the
+walk enters its node, or every row streamed first) must take the same
+decisions. Each case allows at most one flagged near-tie; the tallies are
+printed at the end of the run.
 """
 import sys
 
@@ -49,8 +52,12 @@ def _same(a, b):
 
 def run_case(pool, cfg, seed, steps, step0=0, sets=4, gen_device="cpu", check_step=True, name=""):
     """Stage-wise parity of every request of rounds step0 .. step0 + steps - 1 (plan, replay, verify), with
-    tsb_step on a second workspace compared with the staged calls bit for bit."""
+    tsb_step on two more workspaces (with and without the normaliser output) compared with the staged calls
+    bit for bit."""
     rnd2 = make_round(cfg, seed) if check_step else None
+    rnd3 = make_round(cfg, seed, target_lse=False) if check_step else None
+    other = tsb.FLAG_STREAM_ROWS if tsb.walk_reads_rows(rnd2.cfg) else tsb.FLAG_READ_ROWS
+    rnd4 = make_round(cfg, seed, flags=other) if check_step else None
 
     def gpu_round(rnd, draft_g, target_g, s):
         rnd.replay(draft_g, s)
@@ -61,6 +68,20 @@ def run_case(pool, cfg, seed, steps, step0=0, sets=4, gen_device="cpu", check_st
         h2 = rnd2.host()
         for k in STEP_KEYS:
             assert _same(h[k], h2[k]), (name, s, k)
+        rnd3.step(draft_g, target_g, s)
+        h3 = rnd3.host()
+        assert h3["target_lse"] is None
+        for k in STEP_KEYS:
+            if k != "target_lse":
+                assert _same(h[k], h3[k]), (name, s, k, "no normaliser output")
+        rnd4.step(draft_g, target_g, s)
+        h4 = rnd4.host()
+        for k in STEP_KEYS:
+            if k == "trace":
+                # a test taken clear of the band with the streamed normaliser records its ratio to ~1e-6
+                assert torch.allclose(h[k], h4[k], rtol=1e-5, atol=0.0, equal_nan=True), (name, s, k, other)
+            else:
+                assert _same(h[k], h4[k]), (name, s, k, other)
 
     return run_rounds(pool, cfg, seed, steps, "rrs", gpu_round, step0=step0, sets=sets, gen_device=gen_device,
                       name=name, check=check if check_step else None)
@@ -146,8 +167,8 @@ def _edge_cfg(**kw):
     return c
 
 
-def _run_edge(cfg, draft_np, target_np, seed=5, step=0, name="edge"):
-    rnd = make_round(cfg, seed)
+def _run_edge(cfg, draft_np, target_np, seed=5, step=0, name="edge", flags=0):
+    rnd = make_round(cfg, seed, flags=flags)
     draft = torch.from_numpy(draft_np).cuda()
     target = torch.from_numpy(target_np).cuda()
     rnd.step(draft, target, step)
@@ -187,18 +208,49 @@ def test_edge_budget_short_and_masked_tokens():
     assert tally.exact["plan"] >= 2 and tally.exact["verify"] >= 2
 
 
-def test_edge_nonfinite_rows_flag_only_their_request():
+@pytest.mark.parametrize("flags", [0, tsb.FLAG_READ_ROWS])
+def test_edge_nonfinite_rows_flag_only_their_request(flags):
     cfg = _edge_cfg(B=6)
     rng = np.random.default_rng(3)
     d = (rng.standard_normal((3, 3, 600)) * 2).astype(np.float32)
     t = (rng.standard_normal((3, 7, 600)) * 2).astype(np.float32)
     d[0, 2, 17] = np.nan
     t[2, 0, 5] = np.inf
-    h, tally = _run_edge(cfg, d, t)
+    h, tally = _run_edge(cfg, d, t, flags=flags)
     st = h["req_status"].numpy()
     assert st[0] & tsb.REQ_NONFINITE and int(h["n_nodes"][0]) == 1 and int(h["n_acc"][0]) == -1
     assert not st[1] & tsb.REQ_NONFINITE and int(h["n_acc"][1]) >= 0
     assert st[2] & tsb.REQ_NONFINITE and int(h["n_acc"][2]) == -1
+
+
+@pytest.mark.parametrize("flags", [0, tsb.FLAG_READ_ROWS])
+def test_edge_nonfinite_rows_off_the_walk(flags):
+    """A NaN or +inf in a target row counts only when the walk enters its node: the rows of the last tree
+    node (never entered at this acceptance level) get one, the requests keep their results, and the
+    normaliser output marks just that row; in the root row it ends the request."""
+    cfg = _edge_cfg(R=4, B=6)
+    rng = np.random.default_rng(31)
+    d = (rng.standard_normal((4, 3, 600)) * 2).astype(np.float32)
+    t = (rng.standard_normal((4, 7, 600)) * 2).astype(np.float32)
+    ref, _ = _run_edge(cfg, d, t, name="edge clean", flags=flags)
+    t2 = t.copy()
+    for r in range(3):
+        entered = {0} | {int(x) for x in ref["acc_node"][r, :max(0, int(ref["n_acc"][r]))]}
+        spare = [u for u in range(int(ref["n_nodes"][r])) if u not in entered]
+        t2[r, spare[-1], 11 + r] = np.nan if r % 2 else np.inf
+    t2[3, 0, 7] = np.nan
+    h, tally = _run_edge(cfg, d, t2, name="edge off-walk rows", flags=flags)
+    for r in range(3):
+        assert not int(h["req_status"][r]) & tsb.REQ_NONFINITE
+        for k in ("n_acc", "acc_node", "acc_tok", "bonus"):
+            assert torch.equal(h[k][r], ref[k][r]), (r, k)
+        assert int(torch.isnan(h["target_lse"][r, :int(h["n_nodes"][r])]).sum()) == 1
+    assert int(h["req_status"][3]) & tsb.REQ_NONFINITE and int(h["n_acc"][3]) == -1
+    rnd = make_round(cfg, 5, flags=flags, target_lse=False)
+    rnd.step(torch.from_numpy(d).cuda(), torch.from_numpy(t2).cuda(), 0)
+    h3 = rnd.host()
+    for k in ("n_acc", "acc_node", "acc_tok", "bonus", "req_status", "trace"):
+        assert _same(h[k], h3[k]), k
 
 
 def test_edge_chain_and_minimal_vocabulary():
