@@ -466,27 +466,55 @@ struct Exchange {
 // 2^(x c - m c) with c = invT log2(e), added in binary64, as the target
 // stream does), then the request's workgroups combine their parts by one
 // exchange. Within ~1e-6 of ln sum_v exp(a_v); *bad if the row holds a NaN
-// or +inf logit, or no finite one.
+// or +inf logit, or no finite one. The slice is read in batches of
+// kRowGroups groups of four logits per thread (one batch covers a slice of
+// up to 10240 logits).
+constexpr int kRowGroups = 5;
+template <int DT>
+struct RowBatch {
+    Raw4<DT> g[kRowGroups];
+};
+
+template <int DT>
+__device__ __forceinline__ void row_batch_load(const WalkArgs& A, bool vec, const WalkSlice& S, size_t trow, int base,
+                                               RowBatch<DT>& rb) {
+    const int n = S.v1 - S.v0;
+#pragma unroll
+    for (int k = 0; k < kRowGroups; ++k) {
+        const int i = base + (k * kWalkThreads + (int)threadIdx.x) * 4;
+        const int valid = max(0, min(4, n - i));
+        raw_load4<DT>(A.target, trow + S.v0 + (valid ? i : 0), valid, vec, rb.g[k]);
+    }
+}
+
 template <int DT>
 __device__ double entered_row_lse(const WalkArgs& A, bool vec, const WalkSlice& S, size_t trow, Exchange& X,
                                   bool* bad) {
-    constexpr int kG = 4;  // groups of four logits loaded per thread before any is used
     const float c = A.invT * 1.4426950408889634f;
     const int n = S.v1 - S.v0;
+    constexpr int kBatch = kRowGroups * 4 * kWalkThreads;
     float m = -INFINITY;
     double sum = 0.0;
     bool nf = false;
-    for (int base = 0; base < n; base += kG * 4 * kWalkThreads) {
-        float x[kG][4];
+    for (int base = 0; base < n; base += kBatch) {
+        RowBatch<DT> rb;
+        row_batch_load<DT>(A, vec, S, trow, base, rb);
+        float x[kRowGroups][4];
 #pragma unroll
-        for (int k = 0; k < kG; ++k) {
-            const int i = base + (k * kWalkThreads + (int)threadIdx.x) * 4;
-            const int valid = max(0, min(4, n - i));
-            load4<DT>(A.target, trow + S.v0 + (valid ? i : 0), valid, vec, x[k]);
+        for (int k = 0; k < kRowGroups; ++k) {
+            if (DT == TSB_BF16) {
+                x[k][0] = __uint_as_float(rb.g[k].w[0] << 16);
+                x[k][1] = __uint_as_float(rb.g[k].w[0] & 0xFFFF0000u);
+                x[k][2] = __uint_as_float(rb.g[k].w[1] << 16);
+                x[k][3] = __uint_as_float(rb.g[k].w[1] & 0xFFFF0000u);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) x[k][e] = __uint_as_float(rb.g[k].w[e]);
+            }
         }
         float cm = m;
 #pragma unroll
-        for (int k = 0; k < kG; ++k)
+        for (int k = 0; k < kRowGroups; ++k)
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 nf |= __builtin_amdgcn_classf(x[k][e], 0x203);  // signalling NaN, quiet NaN, +inf
@@ -499,7 +527,7 @@ __device__ double entered_row_lse(const WalkArgs& A, bool vec, const WalkSlice& 
         if (m > -INFINITY && m < INFINITY) {
             const float mc = m * c;
 #pragma unroll
-            for (int k = 0; k < kG; ++k) {
+            for (int k = 0; k < kRowGroups; ++k) {
                 float cs = 0.f;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) cs += __builtin_amdgcn_exp2f(fmaf(x[k][e], c, -mc));
@@ -756,6 +784,7 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
         int u = 0;
         while (true) {
             ++n_entered;
+            const size_t trow = ((size_t)r * B1 + u) * (size_t)A.V;
             // every workgroup reads the same entries, so all take the same exit
             TreeNode nd;
             double L0 = 0.0, Ld = 0.0;
@@ -789,7 +818,6 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
                 break;
             }
             const int m = nd.m, d = nd.d;
-            const size_t trow = ((size_t)r * B1 + u) * (size_t)A.V;
             // or the target row of u, read now that the walk has entered u: its
             // streamed normaliser, and whether it is usable
             if (A.reads_rows) L0 = entered_row_lse<DT>(A, vec, S, trow, X, &row_bad);
