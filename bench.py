@@ -9,9 +9,11 @@ are synthetic (workloads package), resident in HBM before timing starts; a
 pool of P distinct input sets is rotated so that no step reuses cached rows.
 
 Prints one JSON line: steps/s as `value`, verified tree nodes/s, the
-roofline of the dominant kernel (the replay scan, whose grid also streams
-the target's row normalisers) measured live with HIP events on the launch
-stream, the target stream alone, a per-kernel breakdown, and the CPU oracle
+roofline of the replay scan (the largest throughput-bound kernel: VALU-bound
+when the walk reads the target rows of the nodes it enters, as above 128 MiB
+of target; HBM-bound when its grid also streams every target row) measured
+live with HIP events on the launch stream, the target stream alone, a
+per-kernel breakdown with the walk's per-node latency, and the CPU oracle
 timed on a bounded sample of the same workload on the host cores.
 """
 import argparse
@@ -27,7 +29,8 @@ import workloads as W  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0
 # kernels launched by one replay + RRS round (the replay scan's grid also
-# streams the target), and by one round over sparse pools
+# streams the target when the rows are streamed), and by one round over
+# sparse pools
 STEP_KERNELS = ("draft_partials", "plan_tree", "scan_target", "replay_merge", "verify_walk")
 POOL_KERNELS = ("pool_partials", "pool_lists", "pool_plan", "pool_replay", "target_partials", "pool_walk")
 
@@ -501,8 +504,12 @@ def main():
         rnd.step(drafts[s % P], targets[s % P], s)
     torch.cuda.synchronize()
 
+    # above 128 MiB of target the walk reads the rows of the nodes it enters
+    # and the scan's grid streams no target row
+    streams = not tsb.walk_reads_rows(c)
     K4 = tsb.KERNELS.index("scan_target")
-    # the dominant kernel (replay scan + target stream) is bracketed by events
+    # the replay scan (with the target stream in its grid when the rows are
+    # streamed) is bracketed by events
     # on every `sample`-th timed step (each event pair costs a few
     # microseconds of idle GPU)
     sampled = list(range(0, args.steps, args.sample))
@@ -556,15 +563,18 @@ def main():
     tau = acc / (P * R)
     nodes_per_step = nodes / P
     # the target stream alone (the verification entry point launches it on
-    # its own grid), for its own roofline
+    # its own grid when the normaliser output is asked for), for its own
+    # roofline
     KT = tsb.KERNELS.index("target_partials")
+    trnd = tsb.Round(c, dev, target_lse=True)
     evt = events(args.breakdown_steps)
     for i in range(args.breakdown_steps):
-        rnd.step(drafts[i % P], targets[i % P], i)
+        trnd.step(drafts[i % P], targets[i % P], i)
         tsb.profile_kernel(KT, evt[i][0], evt[i][1])
-        rnd.verify(drafts[i % P], targets[i % P], i)
+        trnd.verify(drafts[i % P], targets[i % P], i)
         tsb.profile_kernel(KT, None)
     torch.cuda.synchronize()
+    del trnd
     kt_us = 1000.0 * sum(a.elapsed_time(b) for a, b in evt) / args.breakdown_steps
 
     first = first_naive(tsb, c, dev, drafts, targets, args, cfg)
@@ -586,11 +596,12 @@ def main():
         latency = {W.config(i)["name"]: latency_block(tsb, i, args) for i in (1, 2, 3)}
 
     b = 2 if cfg["dtype"] == "bf16" else 4
-    # algorithmic bytes of one scan_target launch: every target row of the
-    # tree and every draft row that holds parents, each read once
+    # algorithmic bytes of one scan_target launch: every draft row that holds
+    # parents and, when the rows are streamed, every target row of the tree,
+    # each read once
     t_bytes = trows * V * b // P
     d_bytes = drows * V * b // P
-    k4_bytes = t_bytes + d_bytes
+    k4_bytes = (t_bytes if streams else 0) + d_bytes
     nst = max(1, args.breakdown_steps)
     traffic, insts = counted("scan_target", args.config)
     replay = {
@@ -603,9 +614,10 @@ def main():
         "achieved": None if insts is None else round(insts / (kern_us["scan_target"] * 1e-6) / 1e9, 1),
         "peak": VALU_PEAK_WAVE_INSTS / 1e9, "unit": "G wave64 VALU instructions/s",
         "frac": None if insts is None else round(insts / (kern_us["scan_target"] * 1e-6) / VALU_PEAK_WAVE_INSTS, 4),
-        "note": "VALU issue of the whole launch (scan and target stream); fractions are of the scanned tiles' "
-                "tokens, in groups of four: live = the group's largest key bound reaches the parent's threshold "
-                "(its Philox words are drawn), keyed = a word passes the floor (its Gumbel keys are evaluated)"}
+        "note": "VALU issue of the whole launch (the scan, and the target stream when the rows are streamed); "
+                "fractions are of the scanned tiles' tokens, in groups of four: live = the group's largest key "
+                "bound reaches the parent's threshold (its Philox words are drawn), keyed = a word passes the "
+                "floor (its Gumbel keys are evaluated)"}
     t_traffic, t_insts = counted("target_partials", args.config)
     target_stream = {"kernel": "target_partials", "bound": "hbm",
                      "achieved": round(t_bytes / (kt_us * 1e-6) / 1e9, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -619,8 +631,10 @@ def main():
             "exchanges_per_request": round(work["walk_exchanges"] / wr, 3),
             "us_per_node": round(kern_us["verify_walk"] / max(1e-9, work["walk_nodes"] / wr), 2),
             "us_per_exchange": round(kern_us["verify_walk"] / max(1e-9, work["walk_exchanges"] / wr), 2),
+            "target_rows_read": "entered nodes only" if not streams else "none (streamed before the walk)",
             "note": "per-node and per-exchange times divide the launch time by the mean count of one request "
-                    "(the requests run side by side)"}
+                    "(the requests run side by side); the walk is bound by the latency of its exchanges and "
+                    "row reads, one node after another, not by bandwidth"}
     pr = max(1, work["plan_requests"])
     plan = {"kernel": "plan_tree", "avg_launch_us": kern_us["plan_tree"],
             "merge_us": round(work["plan_merge_ticks"] / pr * 0.01, 2),
@@ -630,6 +644,26 @@ def main():
             "note": "phase times of one request's workgroup from the 100 MHz real-time counter"}
     k1_bytes = R * D * V * b        # every draft row, read once
     achieved = k4_bytes / (k4_ms * 1e-3) / 1e9
+    if streams:
+        roofline = {"kernel": "scan_target", "bound": "hbm", "achieved": round(achieved, 1),
+                    "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                    "traffic": traffic, "bytes_per_launch": k4_bytes, "target_bytes": t_bytes,
+                    "draft_bytes": d_bytes, "avg_launch_us": round(k4_ms * 1000, 2), "timed_launches": len(ev),
+                    "note": "one grid streams every target row of the tree (row normalisers for the walk) and "
+                            "scans the draft rows of the parents' depths (replay); bytes count each row once"}
+    else:
+        va = None if insts is None else insts / (k4_ms * 1e-3)
+        roofline = {"kernel": "scan_target", "bound": "alu",
+                    "achieved": None if va is None else round(va / 1e9, 1),
+                    "peak": VALU_PEAK_WAVE_INSTS / 1e9, "unit": "G wave64 VALU instructions/s",
+                    "frac": None if va is None else round(va / VALU_PEAK_WAVE_INSTS, 4),
+                    "traffic": traffic, "valu_insts_per_launch": insts, "bytes_per_launch": k4_bytes,
+                    "hbm_gbs": round(achieved, 1), "avg_launch_us": round(k4_ms * 1000, 2),
+                    "timed_launches": len(ev),
+                    "note": "the replay scan of the draft rows of the parents' depths (Gumbel-top-k over every "
+                            "token, Philox words drawn where the key bound allows): VALU-bound; the target rows "
+                            "are read by the walk as it enters their nodes. verify_walk takes longer per round but "
+                            "is latency-bound (walk_breakdown)"}
     steps_per_s = 1000.0 / ms
     out = {
         "metric": "tree-replay steps/sec + verified nodes/sec at V=151936,B=128,bs=16; % HBM peak",
@@ -650,13 +684,7 @@ def main():
         "nodes_verified_per_s": round(nodes_per_step * steps_per_s, 1),
         "accepted_tokens_per_s": round(tau * R * steps_per_s, 1),
         "tau": round(tau, 4),
-        "roofline": {"kernel": "scan_target", "bound": "hbm", "achieved": round(achieved, 1),
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": traffic, "bytes_per_launch": k4_bytes, "target_bytes": t_bytes,
-                     "draft_bytes": d_bytes, "avg_launch_us": round(k4_ms * 1000, 2),
-                     "timed_launches": len(ev),
-                     "note": "one grid streams every target row of the tree (row normalisers for the walk) and "
-                             "scans the draft rows of the parents' depths (replay); bytes count each row once"},
+        "roofline": roofline,
         "kernels_us": kern_us,
         "roofline_target_stream": target_stream,
         # the other logit-streaming kernel, from the untimed per-kernel pass
