@@ -39,10 +39,12 @@ POOL_KERNELS = ("pool_partials", "pool_lists", "pool_plan", "pool_replay", "targ
 # scaled by a plain copy of known size: FETCH x2.0, WRITE x1.0) and VALU
 # wave-instructions from SQ_INSTS_VALU.
 COUNTERS = {
-    "scan_target": {"config": 4, "source_sha256_16": "cfae652b4b48e4a6", "fetch_kib": 352801.8, "write_kib": 1239.9,
-                    "insts_valu": 60382736.4},
-    "target_partials": {"config": 4, "source_sha256_16": "16942a55cf7295b1", "fetch_kib": 313239.9,
-                        "write_kib": 530.3, "insts_valu": 30312236.0},
+    # the round's launch at the batched workload, where the walk reads the
+    # target rows of the nodes it enters (the grid scans and clears only)
+    "scan_target": {"config": 4, "source_sha256_16": "6e6c7312a782299d", "fetch_kib": 42250.4, "write_kib": 892.9,
+                    "insts_valu": 30225698.1},
+    "target_partials": {"config": 4, "source_sha256_16": "8666cceb66bbb23f", "fetch_kib": 312167.3,
+                        "write_kib": 521.4, "insts_valu": 35377376.0},
 }
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 # peak VALU issue: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = 39.3e12 lane
