@@ -11,8 +11,11 @@
 //                   emitted in BFS order.
 #include <math.h>
 
+#include <algorithm>
+
 #include "tsb_device.hpp"
 #include "tsb_kernels.hpp"
+#include "tsb_target.hpp"
 
 namespace tsb {
 
@@ -848,6 +851,8 @@ __global__ __launch_bounds__(kDraftThreads) __attribute__((amdgpu_waves_per_eu(4
 //    children.
 constexpr int kPlanWaves = 16;
 constexpr int kPlanThreads = kPlanWaves * kWave;
+static_assert(kPlanThreads == kChainThreads, "the chain rows run on the planner's workgroups");
+constexpr int kChainGridMax = 1024;  // workgroups for the chain rows beside the planner
 constexpr int kPlanBuf = 12288;  // binary64 slots shared by the counting waves
 
 struct PlanShared {
@@ -1006,7 +1011,20 @@ __global__ __launch_bounds__(kPlanThreads) void plan_tree(int D, int S, int K, i
                                                           int32_t* __restrict__ topk_tok,
                                                           float* __restrict__ topk_lp, tsb_tree tree,
                                                           int32_t* __restrict__ req_status,
-                                                          unsigned long long* __restrict__ stats) {
+                                                          unsigned long long* __restrict__ stats, int R,
+                                                          ChainJob cj) {
+    if ((int)blockIdx.x >= R) {
+        // the chain rows, on the workgroups after the requests'
+        for (int g = (int)blockIdx.x - R; g < cj.items; g += (int)gridDim.x - R) {
+            if (cj.bf16)
+                cj.vec ? chain_piece<TSB_BF16, true>(g, cj.target, cj.V, cj.B, invT, cj.cm, cj.cs, cj.cf)
+                       : chain_piece<TSB_BF16, false>(g, cj.target, cj.V, cj.B, invT, cj.cm, cj.cs, cj.cf);
+            else
+                cj.vec ? chain_piece<TSB_F32, true>(g, cj.target, cj.V, cj.B, invT, cj.cm, cj.cs, cj.cf)
+                       : chain_piece<TSB_F32, false>(g, cj.target, cj.V, cj.B, invT, cj.cm, cj.cs, cj.cf);
+        }
+        return;
+    }
     __shared__ PlanShared sh;
     const int r = blockIdx.x;
     const int tid = threadIdx.x;
@@ -1581,9 +1599,25 @@ hipError_t launch_draft_partials(const tsb_config& c, int K, float invT, const v
     return hipGetLastError();
 }
 
+ChainJob chain_job(const tsb_config& c, const void* target, char* ws) {
+    const XchgWs x = xchg_ws(c);
+    ChainJob j;
+    j.target = target;
+    j.cm = (float*)(ws + x.cm);
+    j.cs = (double*)(ws + x.cs);
+    j.cf = (int*)(ws + x.cf);
+    j.items = walk_reads_rows(c) ? c.R * kChainRows * kChainPieces : 0;
+    j.V = c.V;
+    j.B = c.B;
+    j.bf16 = c.dtype == TSB_BF16;
+    j.vec = (c.dtype == TSB_BF16) ? (c.V % 8 == 0 && ((uintptr_t)target & 15) == 0)
+                                  : (c.V % 4 == 0 && ((uintptr_t)target & 15) == 0);
+    return j;
+}
+
 hipError_t launch_plan(const tsb_config& c, float invT, const void* draft, double* draft_lse, int32_t* topk_tok,
                        float* topk_lp, const tsb_tree& tree, int32_t* req_status, char* ws, hipStream_t st,
-                       int frontier) {
+                       int frontier, const ChainJob* cj) {
     const Geometry g = geometry(c);
     const PlanWs w = plan_ws(c);
     float* pm = (float*)(ws + w.pm);
@@ -1598,9 +1632,13 @@ hipError_t launch_plan(const tsb_config& c, float invT, const void* draft, doubl
     if (frontier > 0)
         plan_ep<<<c.R, kPlanThreads, 0, st>>>(c.D, g.S1, c.K, c.B, frontier, invT, pm, ps, pk, pf, draft_lse,
                                               topk_tok, topk_lp, tree, req_status);
-    else
-        plan_tree<<<c.R, kPlanThreads, 0, st>>>(c.D, g.S1, c.K, c.B, invT, pm, ps, pk, pf, draft_lse, topk_tok,
-                                                topk_lp, tree, req_status, stats_ptr());
+    else {
+        ChainJob none{};
+        const ChainJob& j = cj ? *cj : none;
+        plan_tree<<<c.R + std::min(j.items, kChainGridMax), kPlanThreads, 0, st>>>(
+            c.D, g.S1, c.K, c.B, invT, pm, ps, pk, pf, draft_lse, topk_tok, topk_lp, tree, req_status, stats_ptr(),
+            c.R, j);
+    }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     return hook_after(TSB_KERNEL_PLAN_TREE, st);

@@ -68,8 +68,12 @@ struct WalkArgs {
     const uint32_t* nrec;
     // the RRS walk reads each target row as it enters the node (else the row
     // normalisers come from a stream of every row, through the records or the
-    // partials)
+    // partials), except rows 0 and 1, streamed before it into their own
+    // partials [R][kChainRows][kChainPieces]
     int reads_rows;
+    const float* cm;
+    const double* cs;
+    const int* cf;
 };
 
 // binary64 log-sum-exp of target row (r, node) from its segment partials
@@ -676,7 +680,7 @@ __device__ void fill_pass(const WalkArgs& A, bool vec, const WalkSlice& S, bool 
 // which the caller streamed when it asked for it). rows_bad < 0: every target
 // row of the tree must be usable (each workgroup checks the partials, so all
 // agree); otherwise rows_bad is the walk's own verdict on the rows it entered.
-__device__ void walk_tail(const WalkArgs& A, int r, int g, int G, int n, bool draft_bad, bool invalid, int nacc,
+__device__ __forceinline__ void walk_tail(const WalkArgs& A, int r, int g, int G, int n, bool draft_bad, bool invalid, int nacc,
                           int bonus_out, int add_status, int tcount, int rows_bad = -1) {
     __shared__ int s_bad;
     const int tid = threadIdx.x;
@@ -820,7 +824,15 @@ __global__ __launch_bounds__(kWalkThreads) void verify_walk(WalkArgs A) {
             const int m = nd.m, d = nd.d;
             // or the target row of u, read now that the walk has entered u: its
             // streamed normaliser, and whether it is usable
-            if (A.reads_rows) L0 = entered_row_lse<DT>(A, vec, S, trow, X, &row_bad);
+            if (A.reads_rows) {
+                if (u < kChainRows) {  // the root or node 1: streamed before the walk
+                    int tbad;
+                    L0 = target_row_lse(A.cm, A.cs, A.cf, kChainPieces, (size_t)r * kChainRows + u, &tbad);
+                    row_bad = tbad != 0;
+                } else {
+                    L0 = entered_row_lse<DT>(A, vec, S, trow, X, &row_bad);
+                }
+            }
             if (row_bad) {
                 rows_bad = 1;
                 break;
@@ -1704,6 +1716,31 @@ static hipError_t launch_target_partials(const tsb_config& c, float invT, const 
     return hook_after(TSB_KERNEL_TARGET_PARTIALS, st);
 }
 
+// Rows 0 and 1 of every request for a walk that reads the other rows itself
+// (tsb_verify; a round streams them beside the planner), and the clearing of
+// the walk's exchange slots.
+template <int DT, bool VEC>
+__global__ __launch_bounds__(kChainThreads) void chain_rows(ChainJob cj, XRegion X, int R, float invT) {
+    xclear(X, R, (size_t)blockIdx.x * kChainThreads + threadIdx.x, (size_t)gridDim.x * kChainThreads);
+    for (int g = blockIdx.x; g < cj.items; g += gridDim.x)
+        chain_piece<DT, VEC>(g, cj.target, cj.V, cj.B, invT, cj.cm, cj.cs, cj.cf);
+}
+
+static hipError_t launch_chain_rows(const tsb_config& c, float invT, const void* target, char* ws, hipStream_t st) {
+    const ChainJob j = chain_job(c, target, ws);
+    XRegion X;
+    X.slots = (uint64_t*)(ws + xchg_ws(c).slots);
+    hipError_t e = hook_before(TSB_KERNEL_TARGET_PARTIALS, st);
+    if (e != hipSuccess) return e;
+    const int grid = std::max(kClearWorkgroups, std::min(j.items, 1024));
+    auto fn = c.dtype == TSB_BF16 ? (j.vec ? chain_rows<TSB_BF16, true> : chain_rows<TSB_BF16, false>)
+                                  : (j.vec ? chain_rows<TSB_F32, true> : chain_rows<TSB_F32, false>);
+    fn<<<grid, kChainThreads, 0, st>>>(j, X, c.R, invT);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return hook_after(TSB_KERNEL_TARGET_PARTIALS, st);
+}
+
 // Walk arguments shared by both walks.
 static WalkArgs walk_args(const tsb_config& c, float invT, const void* draft, const double* draft_lse,
                           const void* target, const tsb_tree& tree, const int32_t* node_tok, uint32_t step,
@@ -1736,6 +1773,10 @@ static WalkArgs walk_args(const tsb_config& c, float invT, const void* draft, co
     A.P = 0;
     A.nrec = nullptr;
     A.reads_rows = 0;
+    const XchgWs x = xchg_ws(c);
+    A.cm = (const float*)(ws + x.cm);
+    A.cs = (const double*)(ws + x.cs);
+    A.cf = (const int*)(ws + x.cf);
     return A;
 }
 
@@ -1758,9 +1799,9 @@ hipError_t launch_verify(const tsb_config& c, float invT, const void* draft, con
     // streamed only for the optional normaliser output
     const bool reads = walk_reads_rows(c);
     if (stages & kStageTarget) {
-        e = (out.target_lse || !reads) ? launch_target_partials(c, invT, target, tree, w, ws, st)
-                                       : launch_xchg_clear(c, (uint64_t*)(ws + xchg_ws(c).slots), st);
-        if (e != hipSuccess) return e;
+        if ((out.target_lse || !reads) && (e = launch_target_partials(c, invT, target, tree, w, ws, st)) != hipSuccess)
+            return e;
+        if (reads && (e = launch_chain_rows(c, invT, target, ws, st)) != hipSuccess) return e;
     }
     if (!(stages & kStageWalk)) return hipSuccess;
     WalkArgs A = walk_args(c, invT, draft, draft_lse, target, tree, node_tok, step, out, w, ws);

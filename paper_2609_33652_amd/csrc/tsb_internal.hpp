@@ -18,6 +18,12 @@ constexpr int kWalkGroupsMax = 128;  // workgroups per request in verification
 constexpr int kWalkTokensPerGroup = 9728;  // tokens whose binary64 (p, q) one walk workgroup holds in LDS
 constexpr int kTargetWorkgroups = 2048;  // target stream: 8 resident workgroups on each of 256 CUs
 constexpr int kClearWorkgroups = 64;      // a target job without rows: workgroups that clear the exchange slots
+// A walk that reads the target rows it enters takes the rows of nodes 0 and
+// 1 of every request (the root and, in BFS order, its first child: rows that
+// do not depend on the topology) from a stream beside the planner, in
+// kChainPieces equal pieces per row.
+constexpr int kChainRows = 2;
+constexpr int kChainPieces = 8;
 // Targets of up to this many bytes are streamed whole before the walk (one
 // pass beside the replay scan costs less than a row read and an exchange at
 // every node the walk enters); larger ones are read row by row as the walk
@@ -94,9 +100,10 @@ struct VerifyWs {  // target partials, node records of the walk
 // The exchange slots of the walks come first: [R][2][kWalkGroupsMax][8]
 // 64-bit words that the workgroups of a request poll (cleared by a kernel
 // enqueued before each walk in the same call; nothing is kept between
-// calls). Every stage's scratch starts after them.
+// calls), then the partials of every request's rows 0 and 1 for a walk that
+// reads the other rows itself. Every stage's scratch starts after them.
 struct XchgWs {
-    size_t slots, total;
+    size_t slots, cm, cs, cf, total;
 };
 
 inline XchgWs xchg_ws(const tsb_config& c) {
@@ -104,6 +111,12 @@ inline XchgWs xchg_ws(const tsb_config& c) {
     size_t o = 0;
     // slots [R][2][kWalkGroupsMax][8] words, then one line for the ticket counter
     w.slots = o; o = align256(o + ((size_t)c.R * 2 * kWalkGroupsMax * 8 + 8) * sizeof(uint64_t));
+    // partials of rows 0 and 1 of every request ([R][2][kChainPieces]), written
+    // beside the planner and read by the walk (no stage's scratch overlaps them)
+    const size_t nc = (size_t)c.R * kChainRows * kChainPieces;
+    w.cm = o; o = align256(o + nc * sizeof(float));
+    w.cs = o; o = align256(o + nc * sizeof(double));
+    w.cf = o; o = align256(o + nc * sizeof(int32_t));
     w.total = o;
     return w;
 }

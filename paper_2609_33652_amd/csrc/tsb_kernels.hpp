@@ -34,11 +34,24 @@ enum : int {
     kStCount = 16
 };
 
+// Rows 0 and 1 of every request, streamed beside the planner for a walk that
+// reads the other target rows itself (items = 0: none).
+struct ChainJob {
+    const void* target;
+    float* cm;   // partials [R][kChainRows][kChainPieces]: max of a = x invT,
+    double* cs;  // sum exp(a - max),
+    int* cf;     // non-finite flag
+    int items, V, B;
+    bool bf16, vec;
+};
+ChainJob chain_job(const tsb_config& c, const void* target, char* ws);
+
 // frontier > 0: the expand-then-prune first pass with that frontier width;
-// 0: the max-heap first pass.
+// 0: the max-heap first pass. With a chain job (max-heap pass only) the
+// planner's grid also streams its rows.
 hipError_t launch_plan(const tsb_config& c, float invT, const void* draft, double* draft_lse, int32_t* topk_tok,
                        float* topk_lp, const tsb_tree& tree, int32_t* req_status, char* ws, hipStream_t st,
-                       int frontier = 0);
+                       int frontier = 0, const ChainJob* cj = nullptr);
 
 // Nodes the expand-then-prune pass generates for this shape and frontier
 // width, or -1 if they exceed what a workgroup holds.

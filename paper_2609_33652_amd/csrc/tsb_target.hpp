@@ -34,7 +34,7 @@ constexpr bool kTargetPrefetch = true;
 // the chunk holding the row's first logit marks the slots no piece uses as
 // empty, so the partials depend on the chunking only, never on the grid.
 // The chunks also zero the exchange slots of the walk launched after them.
-template <int DT, bool VEC, bool PREF>
+template <int DT, bool VEC, bool PREF, int NT = kBlock>
 __device__ __forceinline__ void stream_piece(const void* __restrict__ target, size_t rowbase, int lo, int hi,
                                              float c, float& m_out, double& sum_out) {
     constexpr int kEl = 8;      // logits per 16-byte load (bf16); fp32 loads are 2 x 16 bytes
@@ -43,7 +43,7 @@ __device__ __forceinline__ void stream_piece(const void* __restrict__ target, si
     const int tid = threadIdx.x;
     float m = -INFINITY;   // running max of the raw logits
     double sum = 0.0;      // sum of 2^(x c - m c)
-    constexpr int kStep = kBlock * kEl * kLoads;
+    constexpr int kStep = NT * kEl * kLoads;
     // a whole step in range (uniform over the workgroup) has every load
     // issued before the first is used; with PREF the next whole step's loads
     // are issued before this step's arithmetic
@@ -51,7 +51,7 @@ __device__ __forceinline__ void stream_piece(const void* __restrict__ target, si
     auto issue = [&](int b) {
 #pragma unroll
         for (int l = 0; l < kLoads; ++l) {
-            const int i0 = b + (l * kBlock + tid) * kEl;
+            const int i0 = b + (l * NT + tid) * kEl;
             if (DT == TSB_BF16) {
                 nxt[l][0] = load_stream16((const uint16_t*)target + rowbase + i0);
             } else {
@@ -91,7 +91,7 @@ __device__ __forceinline__ void stream_piece(const void* __restrict__ target, si
         } else {
 #pragma unroll
         for (int l = 0; l < kLoads; ++l) {
-            const int i0 = base + (l * kBlock + tid) * kEl;
+            const int i0 = base + (l * NT + tid) * kEl;
             if (VEC && i0 + kEl <= hi) {
                 if (DT == TSB_BF16) {
                     const uint4 raw = load_stream16((const uint16_t*)target + rowbase + i0);
@@ -202,6 +202,51 @@ __device__ __forceinline__ void target_chunk(int g, int ngroups, const void* __r
         }
         __syncthreads();
     }
+}
+
+// Rows 0 and 1 of every request (the root, and its first child in BFS
+// order; neither depends on the topology), for a walk that reads the other
+// target rows itself: item g of R * kChainRows * kChainPieces is (request,
+// row, piece), one workgroup of kChainThreads threads streams that equal
+// piece of the row (multiples of 8 logits) with the target stream's
+// arithmetic and writes its partial slot. Row 1 exists only when B >= 1.
+constexpr int kChainThreads = 1024;
+template <int DT, bool VEC>
+__device__ __forceinline__ void chain_piece(int g, const void* __restrict__ target, int V, int B, float invT,
+                                            float* __restrict__ cm, double* __restrict__ cs,
+                                            int* __restrict__ cf) {
+    constexpr int P = kChainPieces;
+    const int r = g / (kChainRows * P), k = (g / P) % kChainRows, q = g % P;
+    if (k > B) return;
+    const int seg = ((V + P - 1) / P + 7) / 8 * 8;
+    const int lo = min(V, q * seg), hi = min(V, lo + seg);
+    const float c = invT * 1.4426950408889634f;
+    float m;
+    double sum;
+    stream_piece<DT, VEC, false, kChainThreads>(target, ((size_t)r * (B + 1) + k) * (size_t)V, lo, hi, c, m, sum);
+    __shared__ float s_m[kChainThreads / kWave];
+    __shared__ double s_s[kChainThreads / kWave];
+    const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+    const float wm = wave_max(m);
+    const double contrib = (m == -INFINITY) ? 0.0 : sum * (double)exp2f((m - wm) * c);
+    const double wsum = wave_sum(contrib);
+    if (lane == 0) {
+        s_m[wave] = wm;
+        s_s[wave] = wsum;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        float M = s_m[0];
+        for (int w = 1; w < kChainThreads / kWave; ++w) M = fmaxf(M, s_m[w]);
+        double tot = 0.0;
+        for (int w = 0; w < kChainThreads / kWave; ++w)
+            if (s_m[w] != -INFINITY) tot += s_s[w] * (double)exp2f((s_m[w] - M) * c);
+        const size_t o = ((size_t)r * kChainRows + k) * P + q;
+        cm[o] = M * invT;
+        cs[o] = tot;
+        cf[o] = (isnan(M) || M == INFINITY || !isfinite(tot)) ? 1 : 0;
+    }
+    __syncthreads();
 }
 
 // binary64 log-sum-exp of one target row from its P partial slots (fixed

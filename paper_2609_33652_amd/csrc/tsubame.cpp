@@ -248,7 +248,11 @@ tsb_status step_round(const tsb_config* cfg, const void* draft, const void* targ
                       const char* name) {
     char where[64];
     const float invT = inv_temperature(cfg->temperature);
-    hipError_t e = tsb::launch_plan(*cfg, invT, draft, draft_lse, topk_tok, topk_lp, *tree, out->req_status, ws, stream);
+    // a walk that reads the rows it enters gets rows 0 and 1 from the
+    // planner's grid
+    const tsb::ChainJob cj = tsb::chain_job(*cfg, target, ws);
+    hipError_t e = tsb::launch_plan(*cfg, invT, draft, draft_lse, topk_tok, topk_lp, *tree, out->req_status, ws, stream,
+                                    0, traversal ? nullptr : &cj);
     if (e != hipSuccess) return hip_fail(e, (snprintf(where, sizeof where, "%s/plan", name), where));
     const tsb::TargetJob tj = tsb::target_job(*cfg, target, *tree, traversal ? nullptr : draft_lse, ws,
                                               traversal || out->target_lse != nullptr ||
