@@ -41,10 +41,10 @@ POOL_KERNELS = ("pool_partials", "pool_lists", "pool_plan", "pool_replay", "targ
 COUNTERS = {
     # the round's launch at the batched workload, where the walk reads the
     # target rows of the nodes it enters (the grid scans and clears only)
-    "scan_target": {"config": 4, "source_sha256_16": "6e6c7312a782299d", "fetch_kib": 42250.4, "write_kib": 892.9,
+    "scan_target": {"config": 4, "source_sha256_16": "18036137b51afcf4", "fetch_kib": 42238.8, "write_kib": 893.2,
                     "insts_valu": 30225698.1},
-    "target_partials": {"config": 4, "source_sha256_16": "8666cceb66bbb23f", "fetch_kib": 312167.3,
-                        "write_kib": 521.4, "insts_valu": 35377376.0},
+    "target_partials": {"config": 4, "source_sha256_16": "fcb4baee469cbe10", "fetch_kib": 311708.5,
+                        "write_kib": 520.0, "insts_valu": 35377376.0},
 }
 FETCH_SCALE, WRITE_SCALE = 2.0, 1.0
 # peak VALU issue: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = 39.3e12 lane

@@ -1718,7 +1718,8 @@ static hipError_t launch_target_partials(const tsb_config& c, float invT, const 
 
 // Rows 0 and 1 of every request for a walk that reads the other rows itself
 // (tsb_verify; a round streams them beside the planner), and the clearing of
-// the walk's exchange slots.
+// the walk's exchange slots. No profiling id: tsb_profile_kernel's target
+// stream is target_partials alone.
 template <int DT, bool VEC>
 __global__ __launch_bounds__(kChainThreads) void chain_rows(ChainJob cj, XRegion X, int R, float invT) {
     xclear(X, R, (size_t)blockIdx.x * kChainThreads + threadIdx.x, (size_t)gridDim.x * kChainThreads);
@@ -1730,15 +1731,11 @@ static hipError_t launch_chain_rows(const tsb_config& c, float invT, const void*
     const ChainJob j = chain_job(c, target, ws);
     XRegion X;
     X.slots = (uint64_t*)(ws + xchg_ws(c).slots);
-    hipError_t e = hook_before(TSB_KERNEL_TARGET_PARTIALS, st);
-    if (e != hipSuccess) return e;
     const int grid = std::max(kClearWorkgroups, std::min(j.items, 1024));
     auto fn = c.dtype == TSB_BF16 ? (j.vec ? chain_rows<TSB_BF16, true> : chain_rows<TSB_BF16, false>)
                                   : (j.vec ? chain_rows<TSB_F32, true> : chain_rows<TSB_F32, false>);
     fn<<<grid, kChainThreads, 0, st>>>(j, X, c.R, invT);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    return hook_after(TSB_KERNEL_TARGET_PARTIALS, st);
+    return hipGetLastError();
 }
 
 // Walk arguments shared by both walks.
