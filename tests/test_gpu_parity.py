@@ -188,12 +188,13 @@ def _run_edge(cfg, draft_np, target_np, seed=5, step=0, name="edge", flags=0):
     return h, tally
 
 
-def test_edge_root_only_budget():
+@pytest.mark.parametrize("flags", [0, tsb.FLAG_READ_ROWS])
+def test_edge_root_only_budget(flags):
     cfg = _edge_cfg(B=0)
     rng = np.random.default_rng(1)
     d = (rng.standard_normal((3, 3, 600)) * 2).astype(np.float32)
     t = (rng.standard_normal((3, 1, 600)) * 2).astype(np.float32)
-    h, tally = _run_edge(cfg, d, t)
+    h, tally = _run_edge(cfg, d, t, flags=flags)
     assert (h["n_nodes"] == 1).all() and (h["n_acc"] == 0).all()
 
 
@@ -253,13 +254,14 @@ def test_edge_nonfinite_rows_off_the_walk(flags):
         assert _same(h[k], h3[k]), k
 
 
-def test_edge_chain_and_minimal_vocabulary():
+@pytest.mark.parametrize("flags", [0, tsb.FLAG_READ_ROWS])
+def test_edge_chain_and_minimal_vocabulary(flags):
     cfg = _edge_cfg(R=2, V=4, D=4, B=4, K=1)
     rng = np.random.default_rng(4)
     d = rng.standard_normal((2, 4, 4)).astype(np.float32)
     t = rng.standard_normal((2, 5, 4)).astype(np.float32)
     for s in range(20):
-        h, tally = _run_edge(cfg, d, t, step=s)
+        h, tally = _run_edge(cfg, d, t, step=s, flags=flags)
         assert tally.exact["verify"] == 2
 
 
