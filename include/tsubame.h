@@ -151,9 +151,9 @@ typedef struct tsb_tree {
  * into (tsb_plan clears it). target_lse ([R, B+1], binary64 log-sum-exp of
  * the scaled target rows, NaN for an unusable row and beyond n_nodes) and
  * trace are optional (NULL to skip; asking for target_lse makes the WoR-RRS
- * entry points stream every row of the tree). trace is [R, TSB_TRACE_MAX, 4] doubles per acceptance test, in
- * walk order: (child node, uniform U, ratio, residual mass after rejection or
- * -1), unused entries -1. */
+ * entry points stream every row of the tree). trace is [R, TSB_TRACE_MAX, 4]
+ * doubles per acceptance test, in walk order: (child node, uniform U, ratio,
+ * residual mass after rejection or -1), unused entries -1. */
 typedef struct tsb_verdict {
     int32_t* n_acc;
     int32_t* acc_node;
@@ -209,9 +209,11 @@ tsb_status tsb_replay(const tsb_config* cfg, const void* draft, const int32_t* t
  * with a NaN or +inf logit, or with no finite logit, ends it with
  * TSB_REQ_NONFINITE and n_acc = bonus = -1; other rows are not checked. The
  * walk reads those rows as it enters their nodes (TSB_FLAG_READ_ROWS, the
- * default above 128 MiB of target), or takes their normalisers from a stream
- * of every row launched before it (TSB_FLAG_STREAM_ROWS, the default up to
- * 128 MiB, and whenever out->target_lse is asked for). */
+ * default above 128 MiB of target; rows 0 and 1 of every request, the root
+ * and its first child, are streamed before the walk, in a round beside the
+ * planner), or takes their normalisers from a stream of every row launched
+ * before it (TSB_FLAG_STREAM_ROWS, the default up to 128 MiB, and whenever
+ * out->target_lse is asked for). */
 tsb_status tsb_verify(const tsb_config* cfg, const void* draft, const double* draft_lse,
                       const void* target, const tsb_tree* tree, const int32_t* node_tok,
                       uint32_t step, const tsb_verdict* out, void* workspace,
@@ -248,10 +250,10 @@ tsb_status tsb_step_noalloc(const tsb_config* cfg, const void* draft, const void
  * paired with sampling without replacement; compared with layer-wise RRS on
  * replayed trees in Section 4.2). Same arguments and outputs as tsb_verify,
  * except that every target row of the tree is streamed and must be usable
- * (else TSB_REQ_NONFINITE). The replayed tree is traversed in post-order (the first remaining child
- * first, down to a node with no children left); the node reached is
- * accepted, with the path from the root, with probability alpha, where
- * alpha_root = 1 and a child c with token y of node u gets
+ * (else TSB_REQ_NONFINITE). The replayed tree is traversed in post-order (the
+ * first remaining child first, down to a node with no children left); the
+ * node reached is accepted, with the path from the root, with probability
+ * alpha, where alpha_root = 1 and a child c with token y of node u gets
  * alpha_c = min(1, alpha_u Mb_u(y) / Ms_u(y)); Mb_u starts as p_u and Ms_u as
  * u's draft distribution. When c is rejected, u updates with the
  * distributions c was drawn from: T = sum_v max(alpha_u Mb_u - Ms_u, 0),
