@@ -48,10 +48,12 @@ constexpr int kScanWorkgroups = 1536;  // resident at 6 waves per SIMD
 // them (they fill the rest as they fit, and start as workgroups finish).
 // Measured with inputs rotated over four sets: 683 target workgroups beat
 // 1024 (two chunks each) by 7% and 512 (four each) by 2% at the batched
-// workload, where the scan ends last; the scan's count matters little.
+// workload, where the scan ends last. The scan's workgroups grow with the
+// tree's node count, from 2048 (batched: 1536 was 4% slower, 3072 even) to
+// 4096 (the 64-request large-budget workload: 3% faster than 2048).
 constexpr int kFusedTargetWorkgroups = 683;
 constexpr bool kFusedTargetPrefetch = false;  // see kTargetPrefetch
-constexpr int kFusedScanWorkgroups = 2048;
+constexpr int kFusedScanWorkgroupsMin = 2048, kFusedScanWorkgroupsMax = 4096;
 
 // A parent that replay fills: a well-formed node of the caller's topology
 // (entries in range, see tree_node) with 1 <= m <= K children. Malformed
@@ -639,7 +641,8 @@ hipError_t launch_replay(const tsb_config& c, float invT, const void* draft, con
     ScanArgs A{draft, c.V, c.D, c.B, g.T, invT, plist, rec, k0, k1, step, cand, cc};
     if (tj) {
         const int nt = std::min(tj->ngroups, kFusedTargetWorkgroups);
-        const int grid = nt + kFusedScanWorkgroups;
+        const int nscan = std::min(kFusedScanWorkgroupsMax, std::max(kFusedScanWorkgroupsMin, c.R * (c.B + 1) / 4));
+        const int grid = nt + nscan;
         const bool tv = tj->vec;
         if (c.dtype == TSB_BF16) {
             auto fn = vec ? (tv ? replay_scan_target<TSB_BF16, true, true> : replay_scan_target<TSB_BF16, true, false>)
